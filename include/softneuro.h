@@ -1,0 +1,227 @@
+/*
+ * softneuro.h -- C ABI of the MI355X routine-selection inference library.
+ *
+ * The calls follow the workflow of the SoftNeuro paper (Hilaga et al.,
+ * arXiv 2110.06037): build a net of layers (Sec. III-B), profile every
+ * routine of every layer on the device (Sec. III-C, unit profiling), select
+ * the optimal routine path with dynamic programming over the layer graph
+ * including adaptation costs (Sec. IV, Algorithm 1 "DPRS"), then run
+ * inference with the selected routines (Sec. III-A, step 3).
+ *
+ * Terms.  A *routine* is one implementation of a layer: an algorithm
+ * (direct, implicit GEMM, Winograd F(2x2,3x3)), a tensor layout and a
+ * routine parameter (a tile configuration).  The *schema* of a routine is its
+ * layout (NCHW, NHWC or NC8HW8 = channel blocks of 8, channels zero-padded to
+ * a multiple of 8).  Between two layers whose routines have different
+ * schemas an *adapt* routine (a layout converter) runs.
+ *
+ * Conventions.
+ *  - Every int-returning call returns SN_OK (0) or a negative sn_status.  No
+ *    C++ exception crosses this boundary.  sn_last_error() returns a
+ *    thread-local description of the last failure.
+ *  - A graph is not thread-safe; separate graphs are independent.
+ *  - State machine: create -> add_layer* -> (profile | set_costs) ->
+ *    (select_path | set_path) -> run*.  A call out of order returns
+ *    SN_E_STATE.  Adding a layer after selection is SN_E_STATE.
+ *  - Device pointers (d_in, d_out) are caller-owned HIP device memory; the
+ *    graph owns its weights, workspaces and intermediate tensors.
+ *  - Streams are hipStream_t passed as void*; NULL means the null stream.
+ *  - Element types: SN_F32 = IEEE binary32, SN_F16 = binary16, SN_BF16 =
+ *    bfloat16 (passed as 16-bit patterns).  Biases are always float32.
+ *    Accumulation is float32 in every routine; outputs are rounded to the run
+ *    dtype with round-to-nearest-even.
+ */
+#ifndef SOFTNEURO_H
+#define SOFTNEURO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sn_graph sn_graph;
+
+typedef enum {
+  SN_OK = 0,
+  SN_E_INVALID = -1,     /* bad argument, unknown id, malformed JSON          */
+  SN_E_SHAPE = -2,       /* inconsistent tensor shapes between layers          */
+  SN_E_STATE = -3,       /* call out of order                                  */
+  SN_E_UNSUPPORTED = -4, /* no routine for a layer / option not available      */
+  SN_E_DEVICE = -5,      /* HIP error or no device (host-only graph)           */
+  SN_E_NOMEM = -6,       /* caller buffer too small (required size reported)   */
+  SN_E_INTERNAL = -7     /* consistency check failed inside the library        */
+} sn_status;
+
+typedef enum { SN_F32 = 0, SN_F16 = 1, SN_BF16 = 2 } sn_dtype;
+
+/* Schemas (tensor layouts).  Values index cost matrices and bitmasks. */
+typedef enum { SN_NCHW = 0, SN_NHWC = 1, SN_NC8HW8 = 2 } sn_layout;
+#define SN_NUM_LAYOUTS 3
+
+/* Algorithms.  Non-convolution layers have one algorithm (SN_ALGO_DIRECT) per
+ * layout; FC layers also have SN_ALGO_IGEMM, the paper's dense childnet
+ * computed as a 1x1 convolution (Sec. III-D). */
+typedef enum { SN_ALGO_DIRECT = 0, SN_ALGO_IGEMM = 1, SN_ALGO_WINOGRAD = 2 } sn_algo;
+#define SN_NUM_ALGOS 3
+
+typedef enum {
+  SN_LAYER_INPUT = 0,  /* auxiliary input layer (id 0, created by sn_graph_create) */
+  SN_LAYER_CONV2D = 1, /* 2-D cross-correlation, groups 1 (dense) or C (depthwise) */
+  SN_LAYER_MAXPOOL = 2,
+  SN_LAYER_GAP = 3,    /* global average pooling to N x C x 1 x 1 */
+  SN_LAYER_ADD = 4,    /* residual merge of two inputs of equal shape */
+  SN_LAYER_FC = 5,     /* y = W x + b on the flattened N x C input */
+  SN_LAYER_OUTPUT = 6  /* auxiliary output layer (implicit, after the last layer) */
+} sn_layer_type;
+
+typedef enum { SN_ACT_NONE = 0, SN_ACT_RELU = 1, SN_ACT_RELU6 = 2 } sn_act;
+
+/* Layer description.  Fields not used by a type are ignored.
+ *   CONV2D : k = output channels, r x s kernel, stride, pad, groups, act
+ *   MAXPOOL: r (= s) window, stride, pad (padding never wins the max)
+ *   GAP    : -
+ *   ADD    : act
+ *   FC     : k = output features                                          */
+typedef struct {
+  int32_t type;
+  int32_t k;
+  int32_t r, s;
+  int32_t stride, pad;
+  int32_t groups;
+  int32_t act;
+} sn_layer_desc;
+
+typedef struct {
+  int32_t id;        /* routine id, unique within the layer; ids enumerate
+                        layout-major, then algorithm, then parameter index  */
+  int32_t layout;    /* sn_layout = schema                                   */
+  int32_t algo;      /* sn_algo                                              */
+  int32_t param;     /* routine-parameter index (tile configuration)         */
+  int64_t cost_ns;   /* profiled time T(r) in ns, -1 if not profiled         */
+  char name[64];     /* descriptor, e.g. "nhwc/igemm:128x128"                */
+} sn_routine_desc;
+
+typedef enum {
+  SN_SELECT_DPRS = 0,  /* optimal routine path by Algorithm 1 (layout, algo ignored) */
+  SN_SELECT_FIXED = 1  /* one layout for the whole net and one convolution
+                          algorithm wherever applicable (else implicit GEMM;
+                          depthwise layers use their direct routine; FC layers
+                          use igemm when algo is igemm, else direct); within
+                          that, the fastest routine parameter */
+} sn_select_mode;
+
+typedef enum {
+  SN_OPT_LAYOUTS = 0,   /* bitmask of allowed schemas (bit = sn_layout), default all */
+  SN_OPT_ALGOS = 1,     /* bitmask of allowed algorithms (bit = sn_algo), default all */
+  SN_OPT_PARAMS = 2,    /* 0: one routine parameter per algorithm; 1: all (default 1) */
+  SN_OPT_HIPGRAPH = 3,  /* 1: sn_run replays a captured HIP graph (default 0)        */
+  SN_OPT_SEED = 4       /* seed of the profiler's scratch-tensor fill (default 1)    */
+} sn_option;
+
+/* Creates a graph whose auxiliary input layer (id 0) carries the user tensor
+ * N x C x H x W in NCHW layout (Sec. IV-E: a zero-time single routine).
+ * device >= 0 selects a HIP device; device = -1 creates a host-only graph on
+ * which only the selection calls work (sn_set_costs, sn_select_path,
+ * sn_set_path, queries) -- the graph used by GPU-free tests.
+ * Errors: SN_E_INVALID (non-positive dims, unknown dtype), SN_E_DEVICE. */
+int sn_graph_create(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, int32_t device,
+                    sn_graph** out);
+
+/* Sets an sn_option.  Options that change the routine set (LAYOUTS, ALGOS,
+ * PARAMS) are accepted only before the first sn_add_layer.
+ * Errors: SN_E_INVALID (unknown option or value), SN_E_STATE. */
+int sn_set_option(sn_graph* g, int32_t option, int64_t value);
+
+/* Appends a layer (Sec. III-B: type, layer parameters, weights).  inputs
+ * lists existing layer ids (so insertion order is a topological order,
+ * Sec. IV-A); ADD takes two, the other types one.  weight: host memory in
+ * the run dtype, OIHW for CONV2D ([K][C/groups][R][S]) and [K][C] for FC;
+ * bias: host float32 [K] (may be NULL = zeros).  Both are copied.  The last
+ * added layer is the net output.  *out_id receives the new id.
+ * Errors: SN_E_INVALID (unknown input id, wrong arity, bad parameters),
+ * SN_E_SHAPE (channel or size mismatch), SN_E_UNSUPPORTED (groups other than
+ * 1 or C), SN_E_STATE (after selection), SN_E_DEVICE. */
+int sn_add_layer(sn_graph* g, const sn_layer_desc* d, const int32_t* inputs, int32_t n_inputs,
+                 const void* weight, const float* bias, int32_t* out_id);
+
+/* Unit profiling (Sec. III-C): times every routine of every layer on
+ * scratch tensors of the layer's real shape, and every layout converter on
+ * every edge (both directions of every schema pair), as the median of reps
+ * timed runs after warmup runs (HIP events on the given stream).  Identical
+ * layer signatures and converter shapes are timed once.  Synchronous.
+ * Errors: SN_E_STATE (no layers), SN_E_DEVICE (host-only graph, HIP error). */
+int sn_profile(sn_graph* g, int32_t warmup, int32_t reps, void* hip_stream);
+
+/* Selects the routine path (Sec. IV) and compiles the execution plan
+ * (buffers, converters, launch list).  See sn_select_mode.
+ * Errors: SN_E_STATE (no costs), SN_E_UNSUPPORTED (a layer has no routine of
+ * finite cost in any allowed schema), SN_E_INVALID (bad mode/layout/algo),
+ * SN_E_INTERNAL (the dynamic program found inconsistent subpaths). */
+int sn_select_path(sn_graph* g, int32_t mode, int32_t layout, int32_t algo);
+
+/* Sets the routine path explicitly: routine_ids[i] is the routine id of
+ * layer i for i = 0 .. n-1 (n = number of layers including the input).
+ * Errors: SN_E_INVALID (wrong n or unknown id), SN_E_STATE. */
+int sn_set_path(sn_graph* g, const int32_t* routine_ids, int32_t n);
+
+/* Enqueues inference on the stream; asynchronous.  d_in: device tensor
+ * N x C x H x W (NCHW, run dtype); d_out: device tensor of the output
+ * layer's shape in NCHW (N x K for a net ending in FC or GAP).
+ * Errors: SN_E_STATE (no plan), SN_E_DEVICE (host-only graph, HIP error). */
+int sn_run(sn_graph* g, const void* d_in, void* d_out, void* hip_stream);
+
+/* Like sn_run, then synchronises and writes the time of every layer's
+ * launches (its routine plus the converters feeding it) to layer_ms[0..n-1]
+ * (layer 0 and layers without launches get 0).  HIP events bracket each
+ * layer on the stream; used to attribute time per routine.
+ * Errors: as sn_run; SN_E_INVALID if n is not the number of layers. */
+int sn_run_timed(sn_graph* g, const void* d_in, void* d_out, void* hip_stream, float* layer_ms,
+                 int32_t n);
+
+/* Cost table as JSON (the profiling data of Sec. IV-A: T(r) per routine,
+ * adapt times per edge and schema pair), all times int64 ns, -1 = no
+ * routine / unavailable:
+ *   {"dtype":..., "layers":[{"id":i,"type":t,"routines":[{"rid":..,"layout":..,
+ *     "algo":..,"param":..,"ns":..}]}],
+ *    "edges":[{"from":j,"to":i,"ns":[[..3..],[..3..],[..3..]]}]}
+ * The implicit auxiliary output layer appears as the last layer with one
+ * NCHW routine of time 0, with an edge from the net output layer.
+ * sn_get_costs writes at most cap bytes including the terminating NUL; if
+ * cap is too small it returns SN_E_NOMEM with *len = required size.
+ * sn_set_costs replaces the table (host-only graphs included); it must list
+ * exactly the graph's layers, routines and edges.
+ * Errors: SN_E_INVALID (malformed or mismatched JSON), SN_E_NOMEM. */
+int sn_get_costs(const sn_graph* g, char* json, size_t cap, size_t* len);
+int sn_set_costs(sn_graph* g, const char* json);
+
+/* Selected routine id per layer (n = number of layers) and the model time
+ * T(S) = sum of routine and adapt times of the selected path (Definition 1).
+ * Errors: SN_E_STATE (no path), SN_E_INVALID (n mismatch). */
+int sn_get_path(const sn_graph* g, int32_t* routine_ids, int32_t n, int64_t* total_ns);
+
+/* Number of layers including the input layer (the implicit output layer is
+ * not counted). */
+int sn_num_layers(const sn_graph* g, int32_t* n);
+
+/* Number of routines of a layer, and their descriptions. */
+int sn_num_routines(const sn_graph* g, int32_t layer, int32_t* count);
+int sn_routine_info(const sn_graph* g, int32_t layer, int32_t idx, sn_routine_desc* out);
+
+/* Output shape N, C, H, W of a layer (logical NCHW). */
+int sn_layer_shape(const sn_graph* g, int32_t layer, int32_t* nchw);
+
+/* Statistics of the last DPRS run for one layer: number of (schema,
+ * constraint) states kept after the layer (Sec. IV-C, IV-D) and number of
+ * candidate unions evaluated at it (the "fastest" terms of Eq. 3). */
+int sn_dp_stats(const sn_graph* g, int32_t layer, int64_t* n_states, int64_t* n_candidates);
+
+void sn_graph_destroy(sn_graph* g);
+const char* sn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOFTNEURO_H */

@@ -1,0 +1,286 @@
+// C ABI: status codes in, no exception out (see include/softneuro.h).
+#include <algorithm>
+#include <cstdio>
+#include <string>
+
+#include "core.hpp"
+
+using namespace sn;
+
+struct sn_graph {
+  Graph g;
+};
+
+static thread_local std::string t_err;
+
+template <class F>
+static int guarded(F&& f) {
+  try {
+    f();
+    return SN_OK;
+  } catch (const Error& e) {
+    t_err = e.what();
+    return e.code;
+  } catch (const std::bad_alloc&) {
+    t_err = "out of host memory";
+    return SN_E_INTERNAL;
+  } catch (const std::exception& e) {
+    t_err = e.what();
+    return SN_E_INTERNAL;
+  } catch (...) {
+    t_err = "unknown error";
+    return SN_E_INTERNAL;
+  }
+}
+
+#define CHECK_G(gp)                                         \
+  do {                                                      \
+    if (!(gp)) fail(SN_E_INVALID, "null graph pointer");    \
+  } while (0)
+
+extern "C" {
+
+const char* sn_last_error(void) { return t_err.c_str(); }
+
+int sn_graph_create(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, int32_t device,
+                    sn_graph** out) {
+  return guarded([&] {
+    if (!out) fail(SN_E_INVALID, "null output pointer");
+    *out = nullptr;
+    if (dtype < SN_F32 || dtype > SN_BF16) fail(SN_E_INVALID, "unknown dtype");
+    if (n <= 0 || c <= 0 || h <= 0 || w <= 0) fail(SN_E_INVALID, "input dims must be positive");
+    if (device < -1) fail(SN_E_INVALID, "device must be >= -1");
+    auto* gp = new sn_graph;
+    try {
+      graph_init(gp->g, dtype, Shape{n, c, h, w}, device);
+      if (device >= 0) dev_create(gp->g);
+    } catch (...) {
+      delete gp;
+      throw;
+    }
+    *out = gp;
+  });
+}
+
+void sn_graph_destroy(sn_graph* gp) {
+  if (!gp) return;
+  try {
+    if (!gp->g.host_only()) {
+      plan_destroy(gp->g);
+      dev_destroy(gp->g);
+    }
+  } catch (...) {
+  }
+  delete gp;
+}
+
+int sn_set_option(sn_graph* gp, int32_t option, int64_t value) {
+  return guarded([&] {
+    CHECK_G(gp);
+    Graph& g = gp->g;
+    bool routine_set = option == SN_OPT_LAYOUTS || option == SN_OPT_ALGOS || option == SN_OPT_PARAMS;
+    if (routine_set && g.n_layers() > 1)
+      fail(SN_E_STATE, "routine-set options must be set before adding layers");
+    switch (option) {
+      case SN_OPT_LAYOUTS:
+        if (value <= 0 || value > 7) fail(SN_E_INVALID, "layout mask must be in 1..7");
+        g.opt_layouts = value;
+        break;
+      case SN_OPT_ALGOS:
+        if (value <= 0 || value > 7) fail(SN_E_INVALID, "algorithm mask must be in 1..7");
+        g.opt_algos = value;
+        break;
+      case SN_OPT_PARAMS:
+        if (value != 0 && value != 1) fail(SN_E_INVALID, "PARAMS is 0 or 1");
+        g.opt_params = value;
+        break;
+      case SN_OPT_HIPGRAPH:
+        if (value != 0 && value != 1) fail(SN_E_INVALID, "HIPGRAPH is 0 or 1");
+        g.opt_hipgraph = value;
+        break;
+      case SN_OPT_SEED:
+        g.opt_seed = value;
+        break;
+      default:
+        fail(SN_E_INVALID, "unknown option");
+    }
+  });
+}
+
+int sn_add_layer(sn_graph* gp, const sn_layer_desc* d, const int32_t* inputs, int32_t n_inputs,
+                 const void* weight, const float* bias, int32_t* out_id) {
+  return guarded([&] {
+    CHECK_G(gp);
+    if (!d) fail(SN_E_INVALID, "null layer description");
+    int id = graph_add_layer(gp->g, *d, inputs, n_inputs, weight, bias);
+    if (out_id) *out_id = id;
+  });
+}
+
+int sn_profile(sn_graph* gp, int32_t warmup, int32_t reps, void* stream) {
+  return guarded([&] {
+    CHECK_G(gp);
+    Graph& g = gp->g;
+    if (g.host_only()) fail(SN_E_DEVICE, "host-only graph cannot profile");
+    if (g.n_layers() < 2) fail(SN_E_STATE, "graph has no layers");
+    if (warmup < 0 || reps < 1) fail(SN_E_INVALID, "warmup >= 0 and reps >= 1 required");
+    dev_profile(g, warmup, reps, stream);
+    g.have_costs = true;
+  });
+}
+
+static void compile_if_device(Graph& g) {
+  if (!g.host_only()) plan_compile(g);
+}
+
+int sn_select_path(sn_graph* gp, int32_t mode, int32_t layout, int32_t algo) {
+  return guarded([&] {
+    CHECK_G(gp);
+    Graph& g = gp->g;
+    if (g.n_layers() < 2) fail(SN_E_STATE, "graph has no layers");
+    std::vector<int> old = g.path;
+    if (mode == SN_SELECT_DPRS) {
+      select_dprs(g);
+    } else if (mode == SN_SELECT_FIXED) {
+      select_fixed(g, layout, algo);
+    } else {
+      fail(SN_E_INVALID, "unknown selection mode");
+    }
+    try {
+      compile_if_device(g);
+    } catch (...) {
+      g.path = old;
+      throw;
+    }
+  });
+}
+
+int sn_set_path(sn_graph* gp, const int32_t* ids, int32_t n) {
+  return guarded([&] {
+    CHECK_G(gp);
+    if (!ids) fail(SN_E_INVALID, "null routine ids");
+    Graph& g = gp->g;
+    if (g.n_layers() < 2) fail(SN_E_STATE, "graph has no layers");
+    std::vector<int> old = g.path;
+    set_path(g, ids, n);
+    try {
+      compile_if_device(g);
+    } catch (...) {
+      g.path = old;
+      throw;
+    }
+  });
+}
+
+int sn_run(sn_graph* gp, const void* d_in, void* d_out, void* stream) {
+  return guarded([&] {
+    CHECK_G(gp);
+    Graph& g = gp->g;
+    if (g.host_only()) fail(SN_E_DEVICE, "host-only graph cannot run");
+    if (g.path.empty()) fail(SN_E_STATE, "no routine path selected");
+    if (!d_in || !d_out) fail(SN_E_INVALID, "null device pointer");
+    plan_run(g, d_in, d_out, stream, nullptr);
+  });
+}
+
+int sn_run_timed(sn_graph* gp, const void* d_in, void* d_out, void* stream, float* layer_ms,
+                 int32_t n) {
+  return guarded([&] {
+    CHECK_G(gp);
+    Graph& g = gp->g;
+    if (g.host_only()) fail(SN_E_DEVICE, "host-only graph cannot run");
+    if (g.path.empty()) fail(SN_E_STATE, "no routine path selected");
+    if (!d_in || !d_out || !layer_ms) fail(SN_E_INVALID, "null pointer");
+    if (n != g.n_layers()) fail(SN_E_INVALID, "layer_ms must have one entry per layer");
+    plan_run(g, d_in, d_out, stream, layer_ms);
+  });
+}
+
+int sn_get_costs(const sn_graph* gp, char* json, size_t cap, size_t* len) {
+  return guarded([&] {
+    CHECK_G(gp);
+    std::string s = costs_to_json(gp->g);
+    if (len) *len = s.size() + 1;
+    if (!json || cap < s.size() + 1) fail(SN_E_NOMEM, "buffer too small for the cost table");
+    std::memcpy(json, s.c_str(), s.size() + 1);
+  });
+}
+
+int sn_set_costs(sn_graph* gp, const char* json) {
+  return guarded([&] {
+    CHECK_G(gp);
+    costs_from_json(gp->g, json);
+  });
+}
+
+int sn_get_path(const sn_graph* gp, int32_t* ids, int32_t n, int64_t* total_ns) {
+  return guarded([&] {
+    CHECK_G(gp);
+    const Graph& g = gp->g;
+    if (g.path.empty()) fail(SN_E_STATE, "no routine path selected");
+    if (n != g.n_layers()) fail(SN_E_INVALID, "n must equal the number of layers");
+    if (ids)
+      for (int i = 0; i < n; ++i) ids[i] = g.path[i];
+    if (total_ns) *total_ns = g.path_cost;
+  });
+}
+
+int sn_num_layers(const sn_graph* gp, int32_t* n) {
+  return guarded([&] {
+    CHECK_G(gp);
+    if (!n) fail(SN_E_INVALID, "null pointer");
+    *n = gp->g.n_layers();
+  });
+}
+
+int sn_num_routines(const sn_graph* gp, int32_t layer, int32_t* count) {
+  return guarded([&] {
+    CHECK_G(gp);
+    if (!count) fail(SN_E_INVALID, "null pointer");
+    if (layer < 0 || layer >= gp->g.n_layers()) fail(SN_E_INVALID, "unknown layer");
+    *count = (int32_t)gp->g.layers[layer].routines.size();
+  });
+}
+
+int sn_routine_info(const sn_graph* gp, int32_t layer, int32_t idx, sn_routine_desc* out) {
+  return guarded([&] {
+    CHECK_G(gp);
+    if (!out) fail(SN_E_INVALID, "null pointer");
+    const Graph& g = gp->g;
+    if (layer < 0 || layer >= g.n_layers()) fail(SN_E_INVALID, "unknown layer");
+    const Layer& L = g.layers[layer];
+    if (idx < 0 || idx >= (int)L.routines.size()) fail(SN_E_INVALID, "unknown routine");
+    const Routine& r = L.routines[idx];
+    out->id = r.id;
+    out->layout = r.layout;
+    out->algo = r.algo;
+    out->param = r.param;
+    out->cost_ns = L.cost[idx];
+    std::snprintf(out->name, sizeof(out->name), "%s", r.name.c_str());
+  });
+}
+
+int sn_layer_shape(const sn_graph* gp, int32_t layer, int32_t* nchw) {
+  return guarded([&] {
+    CHECK_G(gp);
+    if (!nchw) fail(SN_E_INVALID, "null pointer");
+    if (layer < 0 || layer >= gp->g.n_layers()) fail(SN_E_INVALID, "unknown layer");
+    const Shape& s = gp->g.layers[layer].out;
+    nchw[0] = s.n;
+    nchw[1] = s.c;
+    nchw[2] = s.h;
+    nchw[3] = s.w;
+  });
+}
+
+int sn_dp_stats(const sn_graph* gp, int32_t layer, int64_t* n_states, int64_t* n_candidates) {
+  return guarded([&] {
+    CHECK_G(gp);
+    const Graph& g = gp->g;
+    if (layer < 0 || layer >= (int)g.dp_stats.size()) fail(SN_E_INVALID, "no DPRS statistics");
+    if (n_states) *n_states = g.dp_stats[layer].states;
+    if (n_candidates) *n_candidates = g.dp_stats[layer].candidates;
+  });
+}
+
+}  // extern "C"

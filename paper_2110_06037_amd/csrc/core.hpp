@@ -1,0 +1,139 @@
+// Internal types of the routine-selection library (host side).
+#pragma once
+
+#include <cstdint>
+#include <cstring>
+#include <memory>
+#include <stdexcept>
+#include <string>
+#include <vector>
+
+#include "../../include/softneuro.h"
+
+namespace sn {
+
+constexpr int64_t kInf = INT64_MAX / 4;
+
+// Error carried to the C boundary as a status code plus message.
+struct Error : std::runtime_error {
+  int code;
+  Error(int c, const std::string& m) : std::runtime_error(m), code(c) {}
+};
+[[noreturn]] inline void fail(int code, const std::string& msg) { throw Error(code, msg); }
+
+struct Shape {
+  int n = 0, c = 0, h = 0, w = 0;
+  int64_t numel() const { return (int64_t)n * c * h * w; }
+  bool operator==(const Shape& o) const { return n == o.n && c == o.c && h == o.h && w == o.w; }
+};
+
+inline int round8(int c) { return (c + 7) / 8 * 8; }
+inline int dtype_size(int dt) { return dt == SN_F32 ? 4 : 2; }
+
+// Channels as stored by a layout (NC8HW8 pads to a multiple of 8).
+inline int stored_c(const Shape& s, int layout) { return layout == SN_NC8HW8 ? round8(s.c) : s.c; }
+inline int64_t stored_numel(const Shape& s, int layout) {
+  return (int64_t)s.n * stored_c(s, layout) * s.h * s.w;
+}
+
+// Two layouts hold identical bytes for this shape (the adapt is void).
+inline bool layouts_equivalent(const Shape& s, int a, int b) {
+  if (a == b) return true;
+  auto canon = [&](int l) { return l == SN_NC8HW8 && s.c % 8 != 0 ? -1 : l; };
+  if (canon(a) < 0 || canon(b) < 0) return false;  // padded NC8HW8 differs from the others
+  bool spatial1 = (int64_t)s.h * s.w == 1;
+  if (spatial1) return true;                        // N x C x 1 x 1 in all three
+  // NCHW == NHWC when C == 1; NC8HW8 == NHWC when C == 8
+  auto pair = [&](int x, int y) { return (a == x && b == y) || (a == y && b == x); };
+  if (pair(SN_NCHW, SN_NHWC)) return s.c == 1;
+  if (pair(SN_NHWC, SN_NC8HW8)) return s.c == 8;
+  return false;
+}
+
+struct Routine {
+  int id = 0;
+  int layout = 0;
+  int algo = 0;
+  int param = 0;
+  std::string name;
+};
+
+struct Layer {
+  int id = 0;
+  int type = SN_LAYER_INPUT;
+  sn_layer_desc d{};
+  std::vector<int> inputs;
+  Shape out;
+  // host copies of the user's weights (run dtype bytes, OIHW / [K][C]) and bias
+  std::vector<uint8_t> weight;
+  std::vector<float> bias;
+  std::vector<Routine> routines;
+  std::vector<int64_t> cost;  // per routine, ns; -1 = not profiled
+  std::string signature;      // identical signatures share profiling results
+};
+
+struct Edge {
+  int from = 0, to = 0;
+  int64_t adapt[SN_NUM_LAYOUTS][SN_NUM_LAYOUTS];  // ns, -1 = unavailable
+};
+
+struct Plan;      // execution plan (plan.cpp)
+struct DevState;  // device-side weights and profiling caches (device.cpp)
+
+struct DPLayerStats {
+  int64_t states = 0;      // (schema, constraint) states evaluated at the layer
+  int64_t candidates = 0;  // candidate unions per state (|Lambda|^|H|)
+};
+
+struct Graph {
+  int dtype = SN_F32;
+  int device = -1;
+  Shape in;
+  int64_t opt_layouts = 7, opt_algos = 7, opt_params = 1, opt_hipgraph = 0, opt_seed = 1;
+  std::vector<Layer> layers;  // layers[0] = auxiliary input
+  std::vector<Edge> edges;    // every (input -> layer) edge, in insertion order
+  Edge out_edge{};            // (last layer -> auxiliary output); from/to set on use
+  bool have_costs = false;
+  std::vector<int> path;      // routine index per layer; empty = none
+  int64_t path_cost = -1;
+  std::vector<DPLayerStats> dp_stats;
+  std::unique_ptr<Plan> plan;
+  std::unique_ptr<DevState> dev;
+  bool host_only() const { return device < 0; }
+  int n_layers() const { return (int)layers.size(); }
+  Graph();
+  ~Graph();
+};
+
+// graph.cpp
+void graph_init(Graph& g, int dtype, Shape in, int device);
+int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int n_inputs,
+                    const void* weight, const float* bias);
+// all edges including the one into the auxiliary output layer (id = n_layers())
+std::vector<Edge> all_edges(const Graph& g);
+int igemm_num_params(int dtype);
+void igemm_tile(int dtype, int param, int* bm, int* bn);
+std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L);
+bool winograd_applicable(const Layer& L, const Shape& in);
+std::string routine_name(const Layer& L, const Routine& r);
+
+// select.cpp
+void select_dprs(Graph& g);
+void select_fixed(Graph& g, int layout, int algo);
+void set_path(Graph& g, const int32_t* ids, int n);
+int64_t path_total(const Graph& g, const std::vector<int>& path);
+
+// json.cpp
+std::string costs_to_json(const Graph& g);
+void costs_from_json(Graph& g, const char* json);
+
+// device.cpp (HIP)
+void dev_create(Graph& g);
+void dev_destroy(Graph& g);
+void dev_upload_layer(Graph& g, int layer);
+void dev_profile(Graph& g, int warmup, int reps, void* stream);
+void plan_compile(Graph& g);
+void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms);
+void plan_destroy(Graph& g);
+
+}  // namespace sn

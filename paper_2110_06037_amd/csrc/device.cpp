@@ -1,0 +1,624 @@
+// Device side of the library: weight preparation per routine format, unit
+// profiling (Sec. III-C), plan compilation with adapt (layout converter)
+// insertion on edges whose routines use different schemas (Sec. III-C,
+// Definition 1), liveness-based activation memory, and execution (optionally
+// replayed from a captured HIP graph).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <map>
+
+#include "core.hpp"
+#include "kernels/launch.hpp"
+
+namespace sn {
+
+#define HIPCHK(expr)                                                                        \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess) fail(SN_E_DEVICE, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+struct DevLayer {
+  void* w = nullptr;    // dense [Kp][R][S][C8] | depthwise [R][S][C8] | fc [Kp][C8]
+  void* wu = nullptr;   // Winograd U [16][Kp][C8]
+  float* bias = nullptr;  // [Kp]
+};
+
+struct DevState {
+  int device = 0;
+  std::vector<DevLayer> L;
+  std::map<std::string, int64_t> cost_cache;  // "signature|routine" or "cvt|shape|a|b" -> ns
+};
+
+struct BufRef {
+  int kind = 0;  // 0 arena, 1 user input, 2 user output
+  size_t off = 0;
+};
+
+struct Step {
+  int type = 0;   // 0 convert, 1 layer
+  int layer = 0;  // layer the step is accounted to
+  BufRef src, dst;
+  k::TDesc sd{}, dd{};
+  int n_in = 0;
+  BufRef in[2];
+  k::TDesc ind[2]{};
+  BufRef out;
+  k::TDesc outd{};
+  BufRef ws;
+  size_t ws_bytes = 0;
+};
+
+struct Plan {
+  std::vector<Step> steps;
+  void* arena = nullptr;
+  size_t arena_bytes = 0;
+  std::vector<int> first_step, last_step;  // per layer, -1 if none
+  std::vector<hipEvent_t> ev;              // 2 per layer (timed runs)
+  hipStream_t gstream = nullptr;           // stream the captured graph replays on
+  hipGraphExec_t gexec = nullptr;
+  hipGraph_t graph = nullptr;
+  const void* g_in = nullptr;
+  void* g_out = nullptr;
+  hipEvent_t gev[2] = {nullptr, nullptr};
+};
+
+Graph::Graph() = default;
+Graph::~Graph() = default;
+
+// ------------------------------------------------------------------ helpers
+static k::TDesc tdesc(const Shape& s, int layout) {
+  return k::TDesc{s.n, s.c, s.h, s.w, stored_c(s, layout), layout};
+}
+
+static double decode(const uint8_t* p, int dtype) {
+  if (dtype == SN_F32) {
+    float f;
+    std::memcpy(&f, p, 4);
+    return f;
+  }
+  uint16_t b;
+  std::memcpy(&b, p, 2);
+  if (dtype == SN_F16) {
+    _Float16 h;
+    std::memcpy(&h, &b, 2);
+    return (double)h;
+  }
+  uint32_t u = (uint32_t)b << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+
+static void encode(double v, int dtype, uint8_t* p) {
+  if (dtype == SN_F32) {
+    float f = (float)v;
+    std::memcpy(p, &f, 4);
+  } else if (dtype == SN_F16) {
+    _Float16 h = (_Float16)v;  // one rounding, nearest-even
+    std::memcpy(p, &h, 2);
+  } else {
+    __bf16 b = (__bf16)v;      // one rounding, nearest-even
+    std::memcpy(p, &b, 2);
+  }
+}
+
+static void* dev_upload(const void* host, size_t bytes) {
+  void* d = nullptr;
+  HIPCHK(hipMalloc(&d, std::max<size_t>(bytes, 256)));
+  HIPCHK(hipMemcpy(d, host, bytes, hipMemcpyHostToDevice));
+  return d;
+}
+
+static bool is_depthwise(const Graph& g, const Layer& L) {
+  return L.type == SN_LAYER_CONV2D && L.d.groups > 1;
+}
+
+// ------------------------------------------------------------------ lifetime
+void dev_create(Graph& g) {
+  int n = 0;
+  HIPCHK(hipGetDeviceCount(&n));
+  if (g.device >= n) fail(SN_E_DEVICE, "no such HIP device");
+  HIPCHK(hipSetDevice(g.device));
+  g.dev.reset(new DevState);
+  g.dev->device = g.device;
+  g.dev->L.resize(1);
+}
+
+void plan_destroy(Graph& g) {
+  if (!g.plan) return;
+  Plan& p = *g.plan;
+  if (p.gexec) (void)hipGraphExecDestroy(p.gexec);
+  if (p.graph) (void)hipGraphDestroy(p.graph);
+  for (auto e : p.ev) (void)hipEventDestroy(e);
+  for (auto e : p.gev)
+    if (e) (void)hipEventDestroy(e);
+  if (p.gstream) (void)hipStreamDestroy(p.gstream);
+  if (p.arena) (void)hipFree(p.arena);
+  g.plan.reset();
+}
+
+void dev_destroy(Graph& g) {
+  if (!g.dev) return;
+  (void)hipSetDevice(g.dev->device);
+  for (auto& d : g.dev->L) {
+    if (d.w) (void)hipFree(d.w);
+    if (d.wu) (void)hipFree(d.wu);
+    if (d.bias) (void)hipFree(d.bias);
+  }
+  g.dev.reset();
+}
+
+// Prepared weight formats (see kernels/launch.hpp).
+void dev_upload_layer(Graph& g, int id) {
+  HIPCHK(hipSetDevice(g.device));
+  DevState& D = *g.dev;
+  D.L.resize(g.n_layers());
+  Layer& L = g.layers[id];
+  DevLayer& dl = D.L[id];
+  if (L.weight.empty()) return;
+  const int es = dtype_size(g.dtype);
+  const Shape& in = g.layers[L.inputs[0]].out;
+  const int K = L.out.c, Kp = round8(K), C = in.c, C8 = round8(C);
+  std::vector<float> bias(Kp, 0.f);
+  std::copy(L.bias.begin(), L.bias.end(), bias.begin());
+  dl.bias = static_cast<float*>(dev_upload(bias.data(), bias.size() * 4));
+  const uint8_t* src = L.weight.data();
+  if (L.type == SN_LAYER_FC) {
+    std::vector<uint8_t> w((size_t)Kp * C8 * es, 0);
+    for (int kk = 0; kk < K; ++kk)
+      std::memcpy(&w[((size_t)kk * C8) * es], src + (size_t)kk * C * es, (size_t)C * es);
+    dl.w = dev_upload(w.data(), w.size());
+    return;
+  }
+  const int R = L.d.r, S = L.d.s;
+  if (is_depthwise(g, L)) {  // OIHW [C][1][R][S] -> [R][S][C8]
+    std::vector<uint8_t> w((size_t)R * S * C8 * es, 0);
+    for (int c = 0; c < C; ++c)
+      for (int r = 0; r < R; ++r)
+        for (int s = 0; s < S; ++s)
+          std::memcpy(&w[(((size_t)r * S + s) * C8 + c) * es], src + (((size_t)c * R + r) * S + s) * es, es);
+    dl.w = dev_upload(w.data(), w.size());
+    return;
+  }
+  // dense OIHW [K][C][R][S] -> [Kp][R][S][C8]
+  std::vector<uint8_t> w((size_t)Kp * R * S * C8 * es, 0);
+  for (int kk = 0; kk < K; ++kk)
+    for (int c = 0; c < C; ++c)
+      for (int r = 0; r < R; ++r)
+        for (int s = 0; s < S; ++s)
+          std::memcpy(&w[((((size_t)kk * R + r) * S + s) * C8 + c) * es],
+                      src + ((((size_t)kk * C + c) * R + r) * S + s) * es, es);
+  dl.w = dev_upload(w.data(), w.size());
+  if (winograd_applicable(L, in)) {
+    // U = G g G^T per (k, c), in float64, rounded once to the run dtype
+    static const double G[4][3] = {{1, 0, 0}, {0.5, 0.5, 0.5}, {0.5, -0.5, 0.5}, {0, 0, 1}};
+    std::vector<uint8_t> u((size_t)16 * Kp * C8 * es, 0);
+    for (int kk = 0; kk < K; ++kk)
+      for (int c = 0; c < C; ++c) {
+        double gg[3][3], t[4][3];
+        for (int r = 0; r < 3; ++r)
+          for (int s = 0; s < 3; ++s) gg[r][s] = decode(src + ((((size_t)kk * C + c) * 3 + r) * 3 + s) * es, g.dtype);
+        for (int i = 0; i < 4; ++i)
+          for (int s = 0; s < 3; ++s) t[i][s] = G[i][0] * gg[0][s] + G[i][1] * gg[1][s] + G[i][2] * gg[2][s];
+        for (int i = 0; i < 4; ++i)
+          for (int j = 0; j < 4; ++j) {
+            double v = t[i][0] * G[j][0] + t[i][1] * G[j][1] + t[i][2] * G[j][2];
+            encode(v, g.dtype, &u[(((size_t)(i * 4 + j) * Kp + kk) * C8 + c) * es]);
+          }
+      }
+    dl.wu = dev_upload(u.data(), u.size());
+  }
+}
+
+// ------------------------------------------------------------------ launching
+static size_t layer_ws_bytes(const Graph& g, const Layer& L, const Routine& r) {
+  if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_WINOGRAD) {
+    const Shape& in = g.layers[L.inputs[0]].out;
+    return k::winograd_ws_bytes(g.dtype, tdesc(in, r.layout), L.out.c);
+  }
+  return 0;
+}
+
+static void launch_layer(const Graph& g, int id, const Routine& r, const void* const* in,
+                         const k::TDesc* ind, void* out, const k::TDesc& outd, void* ws,
+                         size_t ws_bytes, hipStream_t st) {
+  const Layer& L = g.layers[id];
+  const DevLayer& dl = g.dev->L[id];
+  const int dt = g.dtype;
+  switch (L.type) {
+    case SN_LAYER_CONV2D: {
+      k::ConvArgs a{};
+      a.x = in[0];
+      a.xd = ind[0];
+      a.w = r.algo == SN_ALGO_WINOGRAD ? dl.wu : dl.w;
+      a.bias = dl.bias;
+      a.y = out;
+      a.yd = outd;
+      a.r = L.d.r;
+      a.s = L.d.s;
+      a.stride = L.d.stride;
+      a.pad = L.d.pad;
+      a.act = L.d.act;
+      a.ws = ws;
+      a.ws_bytes = ws_bytes;
+      if (L.d.groups > 1) {
+        k::dwconv(dt, a, st);
+      } else if (r.algo == SN_ALGO_DIRECT) {
+        k::conv_direct(dt, a, st);
+      } else if (r.algo == SN_ALGO_IGEMM) {
+        int bm, bn;
+        igemm_tile(dt, r.param, &bm, &bn);
+        k::conv_igemm(dt, bm, bn, a, st);
+      } else {
+        k::conv_winograd(dt, a, st);
+      }
+      break;
+    }
+    case SN_LAYER_MAXPOOL:
+      k::maxpool(dt, in[0], ind[0], out, outd, L.d.r, L.d.stride, L.d.pad, st);
+      break;
+    case SN_LAYER_GAP:
+      k::gap(dt, in[0], ind[0], out, outd, st);
+      break;
+    case SN_LAYER_ADD: {
+      const Shape& s = L.out;
+      k::add_act(dt, in[0], in[1], out, stored_numel(s, r.layout), L.d.act, st);
+      break;
+    }
+    case SN_LAYER_FC: {
+      const Shape& xs = g.layers[L.inputs[0]].out;
+      if (r.algo == SN_ALGO_IGEMM) {  // dense childnet: 1x1 convolution
+        k::ConvArgs a{};
+        a.x = in[0];
+        a.xd = ind[0];
+        a.w = dl.w;
+        a.bias = dl.bias;
+        a.y = out;
+        a.yd = outd;
+        a.r = a.s = 1;
+        a.stride = 1;
+        a.pad = 0;
+        a.act = SN_ACT_NONE;
+        int bm, bn;
+        igemm_tile(dt, 0, &bm, &bn);
+        if (dt != SN_F32) bm = bn = 64;
+        k::conv_igemm(dt, bm, bn, a, st);
+      } else {
+        k::fc_direct(dt, in[0], xs.n, xs.c, stored_c(xs, r.layout), dl.w, round8(xs.c), dl.bias, out,
+                     L.out.c, stored_c(L.out, r.layout), st);
+      }
+      break;
+    }
+    default:
+      fail(SN_E_INTERNAL, "no launcher for layer type");
+  }
+}
+
+// ------------------------------------------------------------------ profiling
+static int64_t median_ns(std::vector<float>& ms) {
+  std::sort(ms.begin(), ms.end());
+  return (int64_t)std::llround((double)ms[ms.size() / 2] * 1e6);
+}
+
+void dev_profile(Graph& g, int warmup, int reps, void* stream) {
+  HIPCHK(hipSetDevice(g.device));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  DevState& D = *g.dev;
+  const int es = dtype_size(g.dtype);
+  // scratch sized for the largest tensor of any layout and the largest workspace
+  size_t tmax = 0, wsmax = 0;
+  for (const Layer& L : g.layers) {
+    for (int l = 0; l < SN_NUM_LAYOUTS; ++l) tmax = std::max(tmax, (size_t)stored_numel(L.out, l) * es);
+    for (const Routine& r : L.routines) wsmax = std::max(wsmax, layer_ws_bytes(g, L, r));
+  }
+  tmax = align256(tmax);
+  void *in0 = nullptr, *in1 = nullptr, *outb = nullptr, *ws = nullptr;
+  std::vector<hipEvent_t> ev(2 * reps, nullptr);
+  auto cleanup = [&]() {
+    for (auto e : ev)
+      if (e) (void)hipEventDestroy(e);
+    for (void* p : {in0, in1, outb, ws})
+      if (p) (void)hipFree(p);
+  };
+  try {
+    HIPCHK(hipMalloc(&in0, tmax));
+    HIPCHK(hipMalloc(&in1, tmax));
+    HIPCHK(hipMalloc(&outb, tmax));
+    if (wsmax) HIPCHK(hipMalloc(&ws, wsmax));
+    for (auto& e : ev) HIPCHK(hipEventCreate(&e));
+    k::fill_random(g.dtype, in0, tmax / es, (uint64_t)g.opt_seed, st);
+    k::fill_random(g.dtype, in1, tmax / es, (uint64_t)g.opt_seed + 7, st);
+    HIPCHK(hipGetLastError());
+    auto time_it = [&](auto&& launch) -> int64_t {
+      for (int i = 0; i < warmup; ++i) launch();
+      for (int i = 0; i < reps; ++i) {
+        HIPCHK(hipEventRecord(ev[2 * i], st));
+        launch();
+        HIPCHK(hipEventRecord(ev[2 * i + 1], st));
+      }
+      HIPCHK(hipGetLastError());
+      HIPCHK(hipEventSynchronize(ev[2 * reps - 1]));
+      std::vector<float> ms(reps);
+      for (int i = 0; i < reps; ++i) HIPCHK(hipEventElapsedTime(&ms[i], ev[2 * i], ev[2 * i + 1]));
+      return median_ns(ms);
+    };
+    for (int i = 1; i < g.n_layers(); ++i) {
+      Layer& L = g.layers[i];
+      for (size_t ri = 0; ri < L.routines.size(); ++ri) {
+        const Routine& r = L.routines[ri];
+        std::string key = L.signature + "|" + r.name;
+        auto it = D.cost_cache.find(key);
+        if (it != D.cost_cache.end()) {
+          L.cost[ri] = it->second;
+          continue;
+        }
+        const void* ins[2] = {in0, in1};
+        k::TDesc ind[2];
+        for (size_t q = 0; q < L.inputs.size(); ++q) ind[q] = tdesc(g.layers[L.inputs[q]].out, r.layout);
+        k::TDesc od = tdesc(L.out, r.layout);
+        size_t wsb = layer_ws_bytes(g, L, r);
+        int64_t ns = time_it([&] { launch_layer(g, i, r, ins, ind, outb, od, ws, wsb, st); });
+        D.cost_cache[key] = ns;
+        L.cost[ri] = ns;
+      }
+    }
+    int64_t allowed = g.opt_layouts | (1 << SN_NCHW);
+    auto edge_costs = [&](Edge& e, const Shape& s) {
+      for (int a = 0; a < SN_NUM_LAYOUTS; ++a)
+        for (int b = 0; b < SN_NUM_LAYOUTS; ++b) {
+          if (a == b) {
+            e.adapt[a][b] = 0;
+            continue;
+          }
+          if (!(allowed >> a & 1) || !(allowed >> b & 1)) {
+            e.adapt[a][b] = -1;
+            continue;
+          }
+          if (layouts_equivalent(s, a, b)) {
+            e.adapt[a][b] = 0;  // identical bytes: void adapt
+            continue;
+          }
+          std::string key = "cvt|" + std::to_string(s.n) + "," + std::to_string(s.c) + "," +
+                            std::to_string(s.h) + "," + std::to_string(s.w) + "|" +
+                            std::to_string(a) + ">" + std::to_string(b);
+          auto it = D.cost_cache.find(key);
+          if (it == D.cost_cache.end()) {
+            k::TDesc sd = tdesc(s, a), dd = tdesc(s, b);
+            int64_t ns = time_it([&] { k::convert(g.dtype, in0, sd, outb, dd, st); });
+            it = D.cost_cache.emplace(key, ns).first;
+          }
+          e.adapt[a][b] = it->second;
+        }
+    };
+    for (Edge& e : g.edges) edge_costs(e, g.layers[e.from].out);
+    edge_costs(g.out_edge, g.layers.back().out);
+    HIPCHK(hipStreamSynchronize(st));
+  } catch (...) {
+    cleanup();
+    throw;
+  }
+  cleanup();
+}
+
+// ------------------------------------------------------------------ plan
+void plan_compile(Graph& g) {
+  HIPCHK(hipSetDevice(g.device));
+  plan_destroy(g);
+  std::unique_ptr<Plan> P(new Plan);
+  const int n = g.n_layers();
+  const int es = dtype_size(g.dtype);
+  struct Buf {
+    size_t bytes;
+    int def, last;
+    size_t off;
+  };
+  std::vector<Buf> bufs;
+  auto new_buf = [&](size_t bytes, int def) {
+    bufs.push_back(Buf{align256(bytes), def, def, 0});
+    return (int)bufs.size() - 1;
+  };
+  // output tensor of each layer: kind/buffer index
+  std::vector<int> out_buf(n, -1);  // -1 = user input (layer 0) / user output
+  std::vector<BufRef> out_ref(n);
+  std::vector<std::vector<int>> step_bufs;
+  out_ref[0].kind = 1;
+  P->first_step.assign(n, -1);
+  P->last_step.assign(n, -1);
+  auto push = [&](Step s, std::vector<int> uses) {
+    int idx = (int)P->steps.size();
+    for (int b : uses) bufs[b].last = std::max(bufs[b].last, idx);
+    if (P->first_step[s.layer] < 0) P->first_step[s.layer] = idx;
+    P->last_step[s.layer] = idx;
+    P->steps.push_back(s);
+    step_bufs.push_back(uses);
+  };
+  for (int i = 1; i < n; ++i) {
+    const Layer& L = g.layers[i];
+    const Routine& r = L.routines[g.path[i]];
+    Step s;
+    s.type = 1;
+    s.layer = i;
+    s.n_in = (int)L.inputs.size();
+    std::vector<int> uses;
+    for (int q = 0; q < s.n_in; ++q) {
+      const int j = L.inputs[q];
+      const Shape& js = g.layers[j].out;
+      const int lj = g.layers[j].routines[g.path[j]].layout;
+      s.ind[q] = tdesc(js, r.layout);
+      if (layouts_equivalent(js, lj, r.layout)) {
+        s.in[q] = out_ref[j];
+        if (out_buf[j] >= 0) uses.push_back(out_buf[j]);
+      } else {
+        Step c;
+        c.type = 0;
+        c.layer = i;
+        c.src = out_ref[j];
+        c.sd = tdesc(js, lj);
+        c.dd = tdesc(js, r.layout);
+        const int step_idx = (int)P->steps.size();
+        int b = new_buf((size_t)stored_numel(js, r.layout) * es, step_idx);
+        c.dst.kind = 0;
+        c.dst.off = (size_t)b;  // buffer id; resolved to an offset below
+        std::vector<int> cu{b};
+        if (out_buf[j] >= 0) cu.push_back(out_buf[j]);
+        push(c, cu);
+        s.in[q] = c.dst;
+        uses.push_back(b);
+      }
+    }
+    s.outd = tdesc(L.out, r.layout);
+    const bool last = i == n - 1;
+    const int step_idx = (int)P->steps.size();
+    if (last && layouts_equivalent(L.out, r.layout, SN_NCHW)) {
+      s.out.kind = 2;
+    } else {
+      int b = new_buf((size_t)stored_numel(L.out, r.layout) * es, step_idx);
+      out_buf[i] = b;
+      s.out.kind = 0;
+      s.out.off = (size_t)b;
+      uses.push_back(b);
+    }
+    s.ws_bytes = layer_ws_bytes(g, L, r);
+    if (s.ws_bytes) {
+      int b = new_buf(s.ws_bytes, step_idx);
+      s.ws.kind = 0;
+      s.ws.off = (size_t)b;
+      uses.push_back(b);
+    }
+    out_ref[i] = s.out;
+    push(s, uses);
+    if (last && s.out.kind != 2) {  // adapt into the user's NCHW output
+      Step c;
+      c.type = 0;
+      c.layer = i;
+      c.src = s.out;
+      c.sd = s.outd;
+      c.dd = tdesc(L.out, SN_NCHW);
+      c.dst.kind = 2;
+      push(c, {out_buf[i]});
+    }
+  }
+  // first-fit offsets, largest buffers first; buffers whose step ranges
+  // overlap never share bytes
+  std::vector<int> order(bufs.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = (int)i;
+  std::sort(order.begin(), order.end(), [&](int a, int b) {
+    return bufs[a].bytes != bufs[b].bytes ? bufs[a].bytes > bufs[b].bytes : a < b;
+  });
+  std::vector<int> placed;
+  size_t total = 0;
+  for (int b : order) {
+    std::vector<std::pair<size_t, size_t>> busy;
+    for (int o : placed)
+      if (!(bufs[o].last < bufs[b].def || bufs[b].last < bufs[o].def))
+        busy.push_back({bufs[o].off, bufs[o].off + bufs[o].bytes});
+    std::sort(busy.begin(), busy.end());
+    size_t off = 0;
+    for (auto& iv : busy) {
+      if (off + bufs[b].bytes <= iv.first) break;
+      off = std::max(off, iv.second);
+    }
+    bufs[b].off = off;
+    total = std::max(total, off + bufs[b].bytes);
+    placed.push_back(b);
+  }
+  auto resolve = [&](BufRef& r) {
+    if (r.kind == 0) r.off = bufs[r.off].off;
+  };
+  for (Step& s : P->steps) {
+    if (s.type == 0) {
+      resolve(s.src);
+      resolve(s.dst);
+    } else {
+      for (int q = 0; q < s.n_in; ++q) resolve(s.in[q]);
+      resolve(s.out);
+      if (s.ws_bytes) resolve(s.ws);
+    }
+  }
+  P->arena_bytes = std::max<size_t>(total, 256);
+  HIPCHK(hipMalloc(&P->arena, P->arena_bytes));
+  P->ev.resize(2 * n, nullptr);
+  for (auto& e : P->ev) HIPCHK(hipEventCreate(&e));
+  g.plan = std::move(P);
+}
+
+static void enqueue_steps(const Graph& g, const Plan& P, const void* d_in, void* d_out,
+                          hipStream_t st, bool timed) {
+  char* base = static_cast<char*>(P.arena);
+  auto ptr = [&](const BufRef& r) -> void* {
+    if (r.kind == 1) return const_cast<void*>(d_in);
+    if (r.kind == 2) return d_out;
+    return base + r.off;
+  };
+  for (size_t si = 0; si < P.steps.size(); ++si) {
+    const Step& s = P.steps[si];
+    if (timed && P.first_step[s.layer] == (int)si) HIPCHK(hipEventRecord(P.ev[2 * s.layer], st));
+    if (s.type == 0) {
+      k::convert(g.dtype, ptr(s.src), s.sd, ptr(s.dst), s.dd, st);
+    } else {
+      const Routine& r = g.layers[s.layer].routines[g.path[s.layer]];
+      const void* ins[2] = {ptr(s.in[0]), s.n_in > 1 ? ptr(s.in[1]) : nullptr};
+      launch_layer(g, s.layer, r, ins, s.ind, ptr(s.out), s.outd, s.ws_bytes ? ptr(s.ws) : nullptr,
+                   s.ws_bytes, st);
+    }
+    if (timed && P.last_step[s.layer] == (int)si) HIPCHK(hipEventRecord(P.ev[2 * s.layer + 1], st));
+  }
+  HIPCHK(hipGetLastError());
+}
+
+void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms) {
+  if (!g.plan) fail(SN_E_STATE, "no execution plan");
+  HIPCHK(hipSetDevice(g.device));
+  Plan& P = *g.plan;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (layer_ms) {
+    enqueue_steps(g, P, d_in, d_out, st, true);
+    HIPCHK(hipStreamSynchronize(st));
+    for (int i = 0; i < g.n_layers(); ++i) {
+      layer_ms[i] = 0.f;
+      if (P.first_step[i] >= 0) HIPCHK(hipEventElapsedTime(&layer_ms[i], P.ev[2 * i], P.ev[2 * i + 1]));
+    }
+    return;
+  }
+  if (!g.opt_hipgraph) {
+    enqueue_steps(g, P, d_in, d_out, st, false);
+    return;
+  }
+  // replay a captured graph on the plan's stream, ordered after/before the caller's stream
+  if (!P.gstream) {
+    HIPCHK(hipStreamCreateWithFlags(&P.gstream, hipStreamNonBlocking));
+    HIPCHK(hipEventCreateWithFlags(&P.gev[0], hipEventDisableTiming));
+    HIPCHK(hipEventCreateWithFlags(&P.gev[1], hipEventDisableTiming));
+  }
+  if (!P.gexec || P.g_in != d_in || P.g_out != d_out) {
+    if (P.gexec) HIPCHK(hipGraphExecDestroy(P.gexec));
+    if (P.graph) HIPCHK(hipGraphDestroy(P.graph));
+    P.gexec = nullptr;
+    P.graph = nullptr;
+    HIPCHK(hipStreamBeginCapture(P.gstream, hipStreamCaptureModeThreadLocal));
+    try {
+      enqueue_steps(g, P, d_in, d_out, P.gstream, false);
+    } catch (...) {
+      hipGraph_t tmp = nullptr;
+      (void)hipStreamEndCapture(P.gstream, &tmp);
+      if (tmp) (void)hipGraphDestroy(tmp);
+      throw;
+    }
+    HIPCHK(hipStreamEndCapture(P.gstream, &P.graph));
+    HIPCHK(hipGraphInstantiate(&P.gexec, P.graph, nullptr, nullptr, 0));
+    P.g_in = d_in;
+    P.g_out = d_out;
+  }
+  HIPCHK(hipEventRecord(P.gev[0], st));
+  HIPCHK(hipStreamWaitEvent(P.gstream, P.gev[0], 0));
+  HIPCHK(hipGraphLaunch(P.gexec, P.gstream));
+  HIPCHK(hipEventRecord(P.gev[1], P.gstream));
+  HIPCHK(hipStreamWaitEvent(st, P.gev[1], 0));
+}
+
+}  // namespace sn

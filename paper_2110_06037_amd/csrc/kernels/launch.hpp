@@ -1,0 +1,47 @@
+// Host-callable launchers of the routine kernels.  Every launcher checks
+// that its operands fit the kernel's assumptions and enqueues on the given
+// stream; none allocates or synchronises.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sn {
+namespace k {
+
+// Logical tensor N x C x H x W stored in `layout` with `cs` stored channels.
+struct TDesc {
+  int n, c, h, w, cs, layout;
+};
+
+struct ConvArgs {
+  const void* x;
+  TDesc xd;
+  const void* w;      // dense: [Kp][R][S][C8]; winograd: U [16][Kp][C8]; depthwise: [R][S][C8]
+  const float* bias;  // [Kp], zero-padded
+  void* y;
+  TDesc yd;
+  int r, s, stride, pad, act;
+  void* ws;           // workspace (winograd); ws_bytes its size
+  size_t ws_bytes;
+};
+
+void conv_direct(int dtype, const ConvArgs& a, hipStream_t st);
+void conv_igemm(int dtype, int bm, int bn, const ConvArgs& a, hipStream_t st);
+size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k);
+void conv_winograd(int dtype, const ConvArgs& a, hipStream_t st);
+void dwconv(int dtype, const ConvArgs& a, hipStream_t st);
+
+void maxpool(int dtype, const void* x, const TDesc& xd, void* y, const TDesc& yd, int k,
+             int stride, int pad, hipStream_t st);
+void gap(int dtype, const void* x, const TDesc& xd, void* y, const TDesc& yd, hipStream_t st);
+void add_act(int dtype, const void* a, const void* b, void* y, int64_t n, int act, hipStream_t st);
+// FC as a VALU dot-product kernel: x [N][cin_s] (stored), w [Kp][C8], y [N][kout_s]
+void fc_direct(int dtype, const void* x, int n, int cin, int cin_s, const void* w, int c8,
+               const float* bias, void* y, int kout, int kout_s, hipStream_t st);
+void convert(int dtype, const void* x, const TDesc& xd, void* y, const TDesc& yd, hipStream_t st);
+void fill_random(int dtype, void* p, int64_t n, uint64_t seed, hipStream_t st);
+
+}  // namespace k
+}  // namespace sn

@@ -1,0 +1,242 @@
+"""Python face of the C ABI: a net of layers, profiling, routine-path
+selection and inference.  PyTorch is used only to hold device tensors and to
+name the stream; all computation happens in libsoftneuro.so.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import json
+
+import numpy as np
+
+from . import native as N
+
+_STORAGE = {N.F32: np.float32, N.F16: np.float16, N.BF16: np.uint16}
+
+
+def _stream_ptr(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+class Graph:
+    """A net (Sec. III-B of the paper) with its routine set and selected path.
+
+    ``device=-1`` makes a host-only graph: only cost-table import, selection
+    and queries work (no weights are uploaded)."""
+
+    def __init__(self, dtype, n, c, h, w, device=0, layouts=None, algos=None, params=True):
+        self.lib = N.lib()
+        self.dtype = N.DTYPE[dtype] if isinstance(dtype, str) else dtype
+        self.dtype_name = {v: k for k, v in N.DTYPE.items()}[self.dtype]
+        self.device = device
+        p = ctypes.c_void_p()
+        N.check(self.lib.sn_graph_create(self.dtype, n, c, h, w, device, ctypes.byref(p)))
+        self._g = p
+        if layouts is not None:
+            mask = sum(1 << N.LAYOUT[l] if isinstance(l, str) else 1 << l for l in layouts)
+            self.set_option(N.OPT_LAYOUTS, mask)
+        if algos is not None:
+            mask = sum(1 << N.ALGO[a] if isinstance(a, str) else 1 << a for a in algos)
+            self.set_option(N.OPT_ALGOS, mask)
+        if not params:
+            self.set_option(N.OPT_PARAMS, 0)
+        self.in_shape = (n, c, h, w)
+
+    # ---------------------------------------------------------------- lifetime
+    def close(self):
+        if getattr(self, "_g", None):
+            self.lib.sn_graph_destroy(self._g)
+            self._g = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def set_option(self, opt, value):
+        N.check(self.lib.sn_set_option(self._g, opt, int(value)))
+
+    # ---------------------------------------------------------------- layers
+    def _add(self, desc, inputs, weight=None, bias=None):
+        ins = (ctypes.c_int32 * len(inputs))(*inputs)
+        wptr = None
+        if weight is not None:
+            w = np.ascontiguousarray(weight, dtype=_STORAGE[self.dtype])
+            self._keep = w
+            wptr = ctypes.c_void_p(w.ctypes.data)
+        bptr = None
+        if bias is not None:
+            b = np.ascontiguousarray(bias, dtype=np.float32)
+            self._keepb = b
+            bptr = b.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+        out = ctypes.c_int32()
+        N.check(self.lib.sn_add_layer(self._g, ctypes.byref(desc), ins, len(inputs), wptr, bptr,
+                                      ctypes.byref(out)))
+        return out.value
+
+    def add_conv(self, inp, weight, bias, stride=1, pad=0, groups=1, act="none"):
+        k, _, r, s = weight.shape
+        d = N.LayerDesc(N.L_CONV2D, k, r, s, stride, pad, groups, N.ACT[act])
+        return self._add(d, [inp], weight, bias)
+
+    def add_maxpool(self, inp, k=3, stride=2, pad=1):
+        return self._add(N.LayerDesc(N.L_MAXPOOL, 0, k, k, stride, pad, 1, 0), [inp])
+
+    def add_gap(self, inp):
+        return self._add(N.LayerDesc(N.L_GAP, 0, 0, 0, 1, 0, 1, 0), [inp])
+
+    def add_add(self, a, b, act="none"):
+        return self._add(N.LayerDesc(N.L_ADD, 0, 0, 0, 1, 0, 1, N.ACT[act]), [a, b])
+
+    def add_fc(self, inp, weight, bias):
+        k = weight.shape[0]
+        return self._add(N.LayerDesc(N.L_FC, k, 1, 1, 1, 0, 1, 0), [inp], weight, bias)
+
+    def add_spec(self, layer, weight=None, bias=None):
+        """Add one layer given as a ``workloads`` spec dict."""
+        t = layer["type"]
+        if t == "conv":
+            return self.add_conv(layer["in"][0], weight, bias, layer["stride"], layer["pad"],
+                                 layer["groups"], layer["act"])
+        if t == "maxpool":
+            return self.add_maxpool(layer["in"][0], layer["k"], layer["stride"], layer["pad"])
+        if t == "gap":
+            return self.add_gap(layer["in"][0])
+        if t == "add":
+            return self.add_add(layer["in"][0], layer["in"][1], layer.get("act", "none"))
+        if t == "fc":
+            return self.add_fc(layer["in"][0], weight, bias)
+        raise ValueError(t)
+
+    # ---------------------------------------------------------------- tuning
+    def profile(self, warmup=5, reps=20, stream=None):
+        N.check(self.lib.sn_profile(self._g, warmup, reps, _stream_ptr(stream)))
+
+    def costs(self):
+        n = ctypes.c_size_t()
+        rc = self.lib.sn_get_costs(self._g, None, 0, ctypes.byref(n))
+        if rc not in (0, -6):
+            N.check(rc)
+        buf = ctypes.create_string_buffer(n.value)
+        N.check(self.lib.sn_get_costs(self._g, buf, n.value, ctypes.byref(n)))
+        return json.loads(buf.value.decode())
+
+    def set_costs(self, costs):
+        s = costs if isinstance(costs, str) else json.dumps(costs)
+        N.check(self.lib.sn_set_costs(self._g, s.encode()))
+
+    def select(self, mode="dprs", layout="NCHW", algo="igemm"):
+        if mode == "dprs":
+            N.check(self.lib.sn_select_path(self._g, N.SELECT_DPRS, 0, 0))
+        else:
+            lay = N.LAYOUT[layout] if isinstance(layout, str) else layout
+            alg = N.ALGO[algo] if isinstance(algo, str) else algo
+            N.check(self.lib.sn_select_path(self._g, N.SELECT_FIXED, lay, alg))
+
+    def set_path(self, ids):
+        arr = (ctypes.c_int32 * len(ids))(*ids)
+        N.check(self.lib.sn_set_path(self._g, arr, len(ids)))
+
+    def path(self):
+        n = self.num_layers()
+        arr = (ctypes.c_int32 * n)()
+        t = ctypes.c_int64()
+        N.check(self.lib.sn_get_path(self._g, arr, n, ctypes.byref(t)))
+        return list(arr), t.value
+
+    # ---------------------------------------------------------------- queries
+    def num_layers(self):
+        n = ctypes.c_int32()
+        N.check(self.lib.sn_num_layers(self._g, ctypes.byref(n)))
+        return n.value
+
+    def routines(self, layer):
+        c = ctypes.c_int32()
+        N.check(self.lib.sn_num_routines(self._g, layer, ctypes.byref(c)))
+        out = []
+        for i in range(c.value):
+            d = N.RoutineDesc()
+            N.check(self.lib.sn_routine_info(self._g, layer, i, ctypes.byref(d)))
+            out.append({"id": d.id, "layout": d.layout, "algo": d.algo, "param": d.param,
+                        "cost_ns": d.cost_ns, "name": d.name.decode()})
+        return out
+
+    def layer_shape(self, layer):
+        arr = (ctypes.c_int32 * 4)()
+        N.check(self.lib.sn_layer_shape(self._g, layer, arr))
+        return tuple(arr)
+
+    def output_shape(self):
+        return self.layer_shape(self.num_layers() - 1)
+
+    def dp_stats(self, layer):
+        s, c = ctypes.c_int64(), ctypes.c_int64()
+        N.check(self.lib.sn_dp_stats(self._g, layer, ctypes.byref(s), ctypes.byref(c)))
+        return s.value, c.value
+
+    # ---------------------------------------------------------------- inference
+    def _torch_dtype(self):
+        import torch
+        return {N.F32: torch.float32, N.F16: torch.float16, N.BF16: torch.bfloat16}[self.dtype]
+
+    def empty_output(self):
+        import torch
+        n, c, h, w = self.output_shape()
+        shape = (n, c) if h == 1 and w == 1 else (n, c, h, w)
+        return torch.empty(shape, dtype=self._torch_dtype(), device=f"cuda:{self.device}")
+
+    def run(self, x, out=None, stream=None):
+        """Enqueue inference of NCHW device tensor x; returns the output tensor."""
+        if out is None:
+            out = self.empty_output()
+        assert x.is_contiguous() and out.is_contiguous()
+        assert x.dtype == self._torch_dtype() and tuple(x.shape) == tuple(self.in_shape)
+        N.check(self.lib.sn_run(self._g, ctypes.c_void_p(x.data_ptr()),
+                                ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)))
+        return out
+
+    def run_timed(self, x, out=None, stream=None):
+        """Synchronous run; returns (out, per-layer milliseconds)."""
+        if out is None:
+            out = self.empty_output()
+        n = self.num_layers()
+        ms = (ctypes.c_float * n)()
+        N.check(self.lib.sn_run_timed(self._g, ctypes.c_void_p(x.data_ptr()),
+                                      ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream), ms, n))
+        return out, list(ms)
+
+
+def build_from_spec(spec, tensors=None, device=0, layouts=None, algos=None, params=True):
+    """Create a graph from a ``workloads`` net spec.  ``tensors`` holds the
+    generated weights (``workloads.generate``); host-only graphs (device -1)
+    may pass None and get zero weights of the right shapes."""
+    from workloads import weight_shapes
+    n = spec["batch"]
+    c, h, w = spec["in_chw"]
+    g = Graph(spec["dtype"], n, c, h, w, device=device,
+              layouts=spec.get("layouts") if layouts is None else layouts,
+              algos=spec.get("algos") if algos is None else algos, params=params)
+    shapes = weight_shapes(spec)
+    for i, layer in enumerate(spec["layers"]):
+        wt = bt = None
+        if shapes[i] is not None:
+            if tensors is not None:
+                wt, bt = tensors["w"][i], tensors["b"][i]
+            else:
+                wt = np.zeros(shapes[i][0], dtype=_STORAGE[g.dtype])
+                bt = np.zeros(shapes[i][1], dtype=np.float32)
+        g.add_spec(layer, wt, bt)
+    return g

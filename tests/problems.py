@@ -9,34 +9,35 @@ SCHEMAS3 = [0, 1, 2]
 
 
 def random_dag(n_mid, seed, max_preds=2):
-    """A 1-in-1-out DAG with layers 0..n_mid+1 (0 = input, last = output)."""
-    g = np.random.default_rng(seed)
+    """A 1-in-1-out DAG with layers 0..n_mid+1 (0 = input, last = output):
+    every middle layer has 1..max_preds inputs and at least one consumer,
+    and the output takes the last middle layer.  Rejection-sampled."""
     L = n_mid + 2
-    edges = set()
-    for i in range(1, L - 1):
-        k = int(g.integers(1, max_preds + 1))
-        preds = g.choice(i, size=min(k, i), replace=False)
-        for j in preds:
-            edges.add((int(j), i))
-    # every middle layer must reach the output
-    has_succ = {j for j, _ in edges}
-    for j in range(1, L - 1):
-        if j not in has_succ:
-            # connect to a random later middle layer or the output
-            i = int(g.integers(j + 1, L))
-            edges.add((j, i))
-    if not any(i == L - 1 for _, i in edges):
+    for attempt in range(1000):
+        g = np.random.default_rng(seed * 1000 + attempt)
+        edges = set()
+        indeg = [0] * L
+        for i in range(1, L - 1):
+            k = int(g.integers(1, max_preds + 1))
+            for j in g.choice(i, size=min(k, i), replace=False):
+                edges.add((int(j), i))
+                indeg[i] += 1
         edges.add((L - 2, L - 1))
-    # the output takes exactly one input: funnel everything into the last middle layer
-    outs = [j for j, i in edges if i == L - 1]
-    if len(outs) > 1:
-        edges = {(j, i) for (j, i) in edges if i != L - 1}
-        last = L - 2
-        for j in outs:
-            if j != last:
-                edges.add((j, last))
-        edges.add((last, L - 1))
-    return L, sorted(edges)
+        indeg[L - 1] = 1
+        ok = True
+        for j in range(0, L - 2):
+            if any(a == j for a, _ in edges):
+                continue
+            later = [i for i in range(j + 1, L - 1) if indeg[i] < max_preds]
+            if not later:
+                ok = False
+                break
+            i = int(g.choice(later))
+            edges.add((j, i))
+            indeg[i] += 1
+        if ok:
+            return L, sorted(edges)
+    raise RuntimeError("no DAG found")
 
 
 def residual_chain(n_blocks, seed):
