@@ -1,0 +1,246 @@
+"""Benchmark: ResNet-50-shaped CNN inference (bf16, batch 32) on one MI355X
+through the routine-selection library, plus batch 1, the fixed-routine paths,
+per-layer roofline fractions and the CPU oracle baseline.
+
+A step is one inference of the whole net over one batch of synthetic input
+with the DPRS-selected routine path (the tuning -- profiling and selection --
+runs once before the timed region and is reported as tuning_s).  Prints one
+JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "img/s ResNet-50-shape bs1/32 bf16; conv MFMA util %; DP-path vs best fixed"
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}
+PEAK_HBM_GBS = 8000.0
+LAYOUTS = ("NCHW", "NHWC", "NC8HW8")
+ALGOS = ("direct", "igemm", "winograd")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def layer_work(spec, g, i, routine):
+    """(category, flops, algorithmic bytes) of layer i (1-based) for a routine."""
+    layer = spec["layers"][i - 1]
+    es = 4 if spec["dtype"] == "f32" else 2
+    n, k, p, q = g.layer_shape(i)
+    ins = [g.layer_shape(j) for j in layer["in"]]
+    _, c, h, w = ins[0]
+    t = layer["type"]
+    if t == "conv":
+        r, s, grp = layer["r"], layer["s"], layer["groups"]
+        wbytes = k * (c // grp) * r * s * es
+        byt = es * (n * c * h * w + n * k * p * q) + wbytes + 4 * k
+        if grp > 1:
+            return "dwconv", 2 * n * k * r * s * p * q, byt
+        flops = 2 * n * k * c * r * s * p * q
+        if routine["algo"] == 2:  # Winograd: the MFMA work is the 16 tile GEMMs
+            tiles = n * ((h + 1) // 2) * ((w + 1) // 2)
+            flops = 2 * 16 * k * c * tiles
+        cat = "conv%dx%d" % (r, s) if r in (1, 3) else "conv_stem"
+        return cat, flops, byt
+    if t == "add":
+        return "add", n * k * p * q, 3 * es * n * k * p * q
+    if t == "maxpool":
+        return "maxpool", 0, es * (n * c * h * w + n * k * p * q)
+    if t == "gap":
+        return "gap", n * c * h * w, es * (n * c * h * w + n * k)
+    if t == "fc":
+        return "fc", 2 * n * c * k, es * (n * c + c * k + n * k)
+    return t, 0, 0
+
+
+def time_steps(g, x, out, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        g.run(x, out)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.run(x, out)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps
+
+
+def cpu_baseline(spec, t, budget_s):
+    """The oracle (naive float64, OpenMP) on the first images of the batch."""
+    import numpy as np
+    from oracle import numeric as O
+    from workloads import to_f64, with_batch
+    d = {"x": to_f64(t["x"], spec["dtype"]),
+         "w": [None if w is None else to_f64(w, spec["dtype"]) for w in t["w"]],
+         "b": [None if b is None else b.astype(np.float64) for b in t["b"]]}
+    done = 0
+    t0 = time.perf_counter()
+    while done < spec["batch"]:
+        one = dict(d)
+        one["x"] = d["x"][done:done + 1]
+        O.forward(with_batch(spec, 1), one, storage="dtype")
+        done += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": round(done / el, 4), "unit": "img/s", "cores": O.num_threads(),
+            "kind": "oracle",
+            "sample": f"{done} image(s) of the batch-{spec['batch']} ResNet-50 input, naive float64 "
+                      f"direct convolution with bf16 storage rounding, {el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--batch", type=int, default=32)
+    ap.add_argument("--dtype", default="bf16")
+    ap.add_argument("--profile-reps", type=int, default=20)
+    ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-path sweep")
+    ap.add_argument("--no-bs1", action="store_true", help="skip the batch-1 measurement")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--costs-out", default=None, help="write the measured cost table here")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the path shards over the "
+              "batch with no exchange, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2110_06037_amd import build_from_spec, native as N, to_device as to_dev
+    from workloads import generate, resnet50
+
+    dev = torch.device("cuda:0")
+    spec = resnet50(args.batch, args.dtype)
+    t = generate(spec)
+    log(f"[bench] {spec['name']}: building graph")
+    g = build_from_spec(spec, t, device=0)
+    t0 = time.perf_counter()
+    g.profile(warmup=5, reps=args.profile_reps)
+    t_prof = time.perf_counter() - t0
+    t1 = time.perf_counter()
+    g.select("dprs")
+    t_sel = time.perf_counter() - t1
+    log(f"[bench] profiled in {t_prof:.1f} s, selected in {t_sel * 1e3:.2f} ms")
+    if args.costs_out:
+        with open(args.costs_out, "w") as f:
+            json.dump(g.costs(), f)
+    ids, model_ns = g.path()
+    x = to_dev(t["x"], args.dtype)
+    out = g.empty_output()
+
+    sec = time_steps(g, x, out, args.steps, args.warmup)
+    value = args.batch / sec
+    log(f"[bench] DP path: {sec * 1e3:.3f} ms/step, {value:.1f} img/s")
+
+    # per-layer times over K instrumented steps (HIP events around each layer)
+    nl = g.num_layers()
+    acc = np.zeros(nl)
+    for _ in range(args.steps):
+        _, ms = g.run_timed(x, out)
+        acc += np.array(ms)
+    layer_ms = acc / args.steps
+    groups = {}
+    per_layer = []
+    for i in range(1, nl):
+        rt = g.routines(i)[ids[i]]
+        cat, flops, byt = layer_work(spec, g, i, rt)
+        key = (cat, rt["name"])
+        gr = groups.setdefault(key, {"ms": 0.0, "flops": 0, "bytes": 0, "launches": 0})
+        gr["ms"] += layer_ms[i]
+        gr["flops"] += flops
+        gr["bytes"] += byt
+        gr["launches"] += 1
+        per_layer.append({"layer": i, "type": cat, "routine": rt["name"],
+                          "us": round(layer_ms[i] * 1e3, 2),
+                          "tflops": round(flops / (layer_ms[i] * 1e-3) / 1e12, 2) if flops and layer_ms[i] else 0,
+                          "gbs": round(byt / (layer_ms[i] * 1e-3) / 1e9, 1) if layer_ms[i] else 0})
+    dom_key = max(groups, key=lambda k: groups[k]["ms"])
+    dom = groups[dom_key]
+    cat = dom_key[0]
+    if cat.startswith("conv"):
+        ach = dom["flops"] / dom["launches"] / (dom["ms"] / dom["launches"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_MFMA_TFLOPS[args.dtype],
+                "unit": "TFLOP/s"}
+    else:
+        ach = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = None
+    roof["kernel"] = f"{dom_key[1]} on {cat} layers ({dom['launches']} launches/step)"
+    roof["avg_launch_us"] = round(dom["ms"] / dom["launches"] * 1e3, 2)
+    # headline: MFMA utilisation over the 3x3 convolutions
+    c3 = [(k, v) for k, v in groups.items() if k[0] == "conv3x3"]
+    c3_ms = sum(v["ms"] for _, v in c3)
+    c3_fl = sum(v["flops"] for _, v in c3)
+    conv3_util = c3_fl / (c3_ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS[args.dtype] if c3_ms else None
+
+    fixed = {}
+    best_fixed = None
+    if not args.no_fixed:
+        for lay in LAYOUTS:
+            for algo in ALGOS:
+                g.select("fixed", lay, algo)
+                s = time_steps(g, x, out, max(3, args.steps // 2), 2)
+                fixed[f"{lay}/{algo}"] = round(args.batch / s, 2)
+                log(f"[bench] fixed {lay}/{algo}: {args.batch / s:.1f} img/s")
+        best_fixed = max(fixed, key=fixed.get)
+        g.set_path(ids)
+    dp_vs_fixed = round(value / fixed[best_fixed], 4) if best_fixed else None
+
+    bs1 = None
+    if not args.no_bs1:
+        spec1 = resnet50(1, args.dtype)
+        t1_ = generate(spec1)
+        g1 = build_from_spec(spec1, t1_, device=0)
+        g1.profile(warmup=5, reps=args.profile_reps)
+        g1.select("dprs")
+        g1.set_option(N.OPT_HIPGRAPH, 1)
+        x1 = to_dev(t1_["x"], args.dtype)
+        o1 = g1.empty_output()
+        s1 = time_steps(g1, x1, o1, max(args.steps, 50), args.warmup)
+        bs1 = round(1.0 / s1, 1)
+        log(f"[bench] bs1 DP path (HIP graph): {s1 * 1e3:.3f} ms, {bs1} img/s")
+        g1.close()
+
+    cpu = cpu_baseline(spec, t, args.cpu_budget)
+    log(f"[bench] cpu oracle: {cpu}")
+
+    line = {
+        "metric": METRIC, "value": round(value, 2), "unit": "img/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sec * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": args.dtype,
+        "data": "synthetic (seeded random input and He-normal weights)",
+        "config": {"workload": f"resnet50-shaped CNN, batch {args.batch}, {args.dtype}, 224x224",
+                   "batch": args.batch, "path": "DPRS-selected routines"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "img_s_bs1": bs1,
+        "conv3x3_mfma_util": round(conv3_util, 4) if conv3_util else None,
+        "dp_vs_best_fixed": dp_vs_fixed, "best_fixed": best_fixed, "fixed_img_s": fixed,
+        "model_time_ms": round(model_ns / 1e6, 4), "tuning_s": round(t_prof + t_sel, 2),
+    }
+    sel = {}
+    for i in range(1, nl):
+        nm = g.routines(i)[ids[i]]["name"]
+        sel[nm] = sel.get(nm, 0) + 1
+    line["selected"] = sel
+    if os.environ.get("SN_BENCH_LAYERS"):
+        with open(os.environ["SN_BENCH_LAYERS"], "w") as f:
+            json.dump(per_layer, f, indent=1)
+    print(json.dumps(line), flush=True)
+    g.close()
+
+
+if __name__ == "__main__":
+    main()

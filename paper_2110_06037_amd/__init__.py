@@ -8,7 +8,7 @@ The work is done by libsoftneuro.so (C ABI in include/softneuro.h, HIP
 kernels for gfx950); this package is its Python binding.
 """
 
-from .graph import Graph, build_from_spec
+from .graph import Graph, build_from_spec, to_device
 from . import native
 
-__all__ = ["Graph", "build_from_spec", "native"]
+__all__ = ["Graph", "build_from_spec", "to_device", "native"]

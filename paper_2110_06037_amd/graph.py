@@ -219,6 +219,16 @@ class Graph:
         return out, list(ms)
 
 
+def to_device(arr, dtype, device=0):
+    """Copy a host array of stored ``dtype`` values (bf16 as uint16 bits) to a
+    torch device tensor of the matching dtype."""
+    import torch
+    a = np.ascontiguousarray(arr)
+    if dtype == "bf16":
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(f"cuda:{device}")
+    return torch.from_numpy(a).to(f"cuda:{device}")
+
+
 def build_from_spec(spec, tensors=None, device=0, layouts=None, algos=None, params=True):
     """Create a graph from a ``workloads`` net spec.  ``tensors`` holds the
     generated weights (``workloads.generate``); host-only graphs (device -1)

@@ -1,0 +1,154 @@
+"""Per-routine parity on the GPU: every routine (algorithm x layout x routine
+parameter) of every layer type, in every dtype, against the float64 oracle
+on the same seeded inputs, through the C ABI.  Shapes span several tiles
+and ragged tails (channels not multiples of 8, odd spatial sizes)."""
+
+import numpy as np
+import pytest
+
+from oracle import numeric as O
+from tests.gpu_util import TOL, err, from_dev, oracle_layer, run_routine, single_layer_graph, to_dev
+from workloads import random_tensor, to_f64
+
+pytestmark = pytest.mark.gpu
+
+DTYPES = ["f32", "f16", "bf16"]
+
+CONV_CASES = [
+    # (N, C, H, W, K, R, stride, pad, act)
+    (2, 24, 13, 11, 40, 3, 1, 1, "relu"),     # ragged M and N tiles, Winograd odd sizes
+    (1, 64, 16, 16, 72, 3, 2, 1, "relu6"),    # stride 2
+    (2, 40, 9, 9, 136, 1, 1, 0, "none"),      # pointwise, N > 128
+    (1, 3, 37, 37, 16, 7, 2, 3, "relu"),      # stem-like: C = 3
+    (3, 16, 8, 8, 10, 3, 1, 1, "none"),       # K = 10 (not a multiple of 8)
+    (1, 130, 7, 7, 24, 3, 1, 1, "relu"),      # C = 130: partial last channel chunk
+]
+
+
+def conv_layer(case):
+    n, c, h, w, k, r, st, pad, act = case
+    return {"type": "conv", "in": [0], "k": k, "r": r, "s": r, "stride": st, "pad": pad,
+            "groups": 1, "act": act}
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("ci", range(len(CONV_CASES)))
+def test_conv_every_routine(dtype, ci):
+    case = CONV_CASES[ci]
+    n, c, h, w, k, r = case[:6]
+    layer = conv_layer(case)
+    x = random_tensor((n, c, h, w), dtype, seed=10 + ci)
+    wt = random_tensor((k, c, r, r), dtype, seed=20 + ci, dist="normal", scale=np.sqrt(2 / (c * r * r)))
+    b = random_tensor((k,), "f32", seed=30 + ci, scale=0.1)
+    ref = oracle_layer(layer, x, wt, b, dtype)
+    g = single_layer_graph(dtype, (n, c, h, w), layer, wt, b)
+    xd = to_dev(x, dtype)
+    for rt in g.routines(1):
+        out = from_dev(run_routine(g, rt["id"], xd), dtype)
+        e = err(out, ref, dtype)
+        print(f"{dtype} case{ci} {rt['name']}: err {e:.2e}", flush=True)
+        assert e <= TOL[dtype], (rt["name"], e)
+    g.close()
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_conv_bit_exact_small_integers(dtype):
+    # values in {-1, 0, 1} with C*R*S = 72: every product and partial sum is an
+    # integer <= 72, exact in every dtype, so every routine must match exactly
+    n, c, h, w, k = 2, 8, 10, 9, 16
+    layer = {"type": "conv", "in": [0], "k": k, "r": 3, "s": 3, "stride": 1, "pad": 1,
+             "groups": 1, "act": "none"}
+    x = random_tensor((n, c, h, w), dtype, seed=1, dist="int")
+    wt = random_tensor((k, c, 3, 3), dtype, seed=2, dist="int")
+    b = np.zeros(k, np.float32)
+    ref = oracle_layer(layer, x, wt, b, dtype)
+    g = single_layer_graph(dtype, (n, c, h, w), layer, wt, b)
+    xd = to_dev(x, dtype)
+    for rt in g.routines(1):
+        out = from_dev(run_routine(g, rt["id"], xd), dtype)
+        assert np.array_equal(out, ref), rt["name"]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("case", [(2, 32, 15, 15, 1), (1, 96, 14, 14, 2), (2, 20, 9, 9, 2)])
+def test_depthwise(dtype, case):
+    n, c, h, w, st = case
+    layer = {"type": "conv", "in": [0], "k": c, "r": 3, "s": 3, "stride": st, "pad": 1,
+             "groups": c, "act": "relu6"}
+    x = random_tensor((n, c, h, w), dtype, seed=3, scale=3.0)
+    wt = random_tensor((c, 1, 3, 3), dtype, seed=4, dist="normal", scale=0.5)
+    b = random_tensor((c,), "f32", seed=5, scale=0.1)
+    ref = oracle_layer(layer, x, wt, b, dtype)
+    g = single_layer_graph(dtype, (n, c, h, w), layer, wt, b)
+    xd = to_dev(x, dtype)
+    for rt in g.routines(1):
+        out = from_dev(run_routine(g, rt["id"], xd), dtype)
+        assert err(out, ref, dtype) <= TOL[dtype], rt["name"]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("shape", [(2, 16, 17, 17), (1, 3, 12, 10), (2, 64, 56, 56)])
+def test_maxpool_exact(dtype, shape):
+    layer = {"type": "maxpool", "in": [0], "k": 3, "stride": 2, "pad": 1}
+    x = random_tensor(shape, dtype, seed=6)
+    ref = oracle_layer(layer, x, None, None, dtype)
+    g = single_layer_graph(dtype, shape, layer)
+    xd = to_dev(x, dtype)
+    for rt in g.routines(1):
+        out = from_dev(run_routine(g, rt["id"], xd), dtype)
+        assert np.array_equal(out, ref), rt["name"]          # max is exact
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("shape", [(2, 24, 7, 7), (1, 13, 5, 5), (4, 2048, 7, 7)])
+def test_gap(dtype, shape):
+    layer = {"type": "gap", "in": [0]}
+    x = random_tensor(shape, dtype, seed=7)
+    ref = oracle_layer(layer, x, None, None, dtype)
+    g = single_layer_graph(dtype, shape, layer)
+    xd = to_dev(x, dtype)
+    for rt in g.routines(1):
+        out = from_dev(run_routine(g, rt["id"], xd), dtype).reshape(ref.shape)
+        assert err(out, ref, dtype) <= TOL[dtype] * 0.1, rt["name"]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("case", [(1, 32, 10), (3, 2048, 1000), (32, 1280, 1000), (2, 12, 5)])
+def test_fc(dtype, case):
+    n, cin, k = case
+    from paper_2110_06037_amd import Graph
+    x = random_tensor((n, cin, 1, 1), dtype, seed=8)
+    wt = random_tensor((k, cin), dtype, seed=9, dist="normal", scale=np.sqrt(2 / cin))
+    b = random_tensor((k,), "f32", seed=10, scale=0.1)
+    ref = O.round_to(O.fc(to_f64(x, dtype), to_f64(wt, dtype), b.astype(np.float64)), dtype)
+    g = Graph(dtype, n, cin, 1, 1, device=0)
+    g.add_fc(0, wt, b)
+    xd = to_dev(x, dtype)
+    for rt in g.routines(1):
+        out = from_dev(run_routine(g, rt["id"], xd), dtype).reshape(ref.shape)
+        assert err(out, ref, dtype) <= TOL[dtype], rt["name"]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_add_and_converters_bit_exact(dtype):
+    # two maxpools feeding an add: every (layout_a, layout_b, layout_add)
+    # combination exercises the converters between all layout pairs; max and
+    # an exactly representable sum keep the result bit-exact
+    from paper_2110_06037_amd import Graph
+    n, c, h, w = 2, 12, 9, 9
+    x = random_tensor((n, c, h, w), dtype, seed=11, dist="int")
+    xs = to_f64(x, dtype)
+    p = O.maxpool(xs, 3, 1, 1)
+    ref = O.add(O.maxpool(p, 3, 1, 1), p, "relu")
+    g = Graph(dtype, n, c, h, w, device=0)
+    a = g.add_maxpool(0, 3, 1, 1)
+    b2 = g.add_maxpool(a, 3, 1, 1)
+    g.add_add(b2, a, "relu")
+    xd = to_dev(x, dtype)
+    for la in range(3):
+        for lb in range(3):
+            for lc in range(3):
+                ids = [0, la, lb, lc]
+                g.set_path(ids)
+                out = from_dev(g.run(xd), dtype)
+                assert np.array_equal(out, ref), ids
