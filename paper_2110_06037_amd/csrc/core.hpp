@@ -111,8 +111,6 @@ int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int
                     const void* weight, const float* bias);
 // all edges including the one into the auxiliary output layer (id = n_layers())
 std::vector<Edge> all_edges(const Graph& g);
-int igemm_num_params(int dtype);
-void igemm_tile(int dtype, int param, int* bm, int* bn);
 std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L);
 bool winograd_applicable(const Layer& L, const Shape& in);
 std::string routine_name(const Layer& L, const Routine& r);

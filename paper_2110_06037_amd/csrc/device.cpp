@@ -217,10 +217,11 @@ void dev_upload_layer(Graph& g, int id) {
 
 // ------------------------------------------------------------------ launching
 static size_t layer_ws_bytes(const Graph& g, const Layer& L, const Routine& r) {
-  if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_WINOGRAD) {
-    const Shape& in = g.layers[L.inputs[0]].out;
-    return k::winograd_ws_bytes(g.dtype, tdesc(in, r.layout), L.out.c);
-  }
+  if (L.type != SN_LAYER_CONV2D || L.d.groups > 1) return 0;
+  const Shape& in = g.layers[L.inputs[0]].out;
+  if (r.algo == SN_ALGO_WINOGRAD) return k::winograd_ws_bytes(g.dtype, tdesc(in, r.layout), L.out.c);
+  if (r.algo == SN_ALGO_IGEMM)
+    return k::igemm_ws_bytes(g.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), L.d.r, L.d.s);
   return 0;
 }
 
@@ -251,9 +252,7 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
       } else if (r.algo == SN_ALGO_DIRECT) {
         k::conv_direct(dt, a, st);
       } else if (r.algo == SN_ALGO_IGEMM) {
-        int bm, bn;
-        igemm_tile(dt, r.param, &bm, &bn);
-        k::conv_igemm(dt, bm, bn, a, st);
+        k::conv_igemm(dt, r.param, a, st);
       } else {
         k::conv_winograd(dt, a, st);
       }
@@ -284,10 +283,7 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
         a.stride = 1;
         a.pad = 0;
         a.act = SN_ACT_NONE;
-        int bm, bn;
-        igemm_tile(dt, 0, &bm, &bn);
-        if (dt != SN_F32) bm = bn = 64;
-        k::conv_igemm(dt, bm, bn, a, st);
+        k::conv_igemm(dt, 0, a, st);  // 64 x 64 tiles, no reduction split
       } else {
         k::fc_direct(dt, in[0], xs.n, xs.c, stored_c(xs, r.layout), dl.w, round8(xs.c), dl.bias, out,
                      L.out.c, stored_c(L.out, r.layout), st);

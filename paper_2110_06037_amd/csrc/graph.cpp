@@ -7,26 +7,12 @@
 #include <sstream>
 
 #include "core.hpp"
+#include "kernels/launch.hpp"
 
 namespace sn {
 
 static const char* kLayoutName[SN_NUM_LAYOUTS] = {"nchw", "nhwc", "nc8hw8"};
 static const char* kAlgoName[SN_NUM_ALGOS] = {"direct", "igemm", "winograd"};
-
-// Routine parameters of the implicit-GEMM routine: (output pixels x output
-// channels) tile of one workgroup.
-static const int kIgemmTiles16[][2] = {{128, 128}, {64, 64}, {128, 64}};
-static const int kIgemmTiles32[][2] = {{64, 64}};
-
-int igemm_num_params(int dtype) {
-  return dtype == SN_F32 ? (int)(sizeof(kIgemmTiles32) / sizeof(kIgemmTiles32[0]))
-                         : (int)(sizeof(kIgemmTiles16) / sizeof(kIgemmTiles16[0]));
-}
-void igemm_tile(int dtype, int param, int* bm, int* bn) {
-  const int(*t)[2] = dtype == SN_F32 ? kIgemmTiles32 : kIgemmTiles16;
-  *bm = t[param][0];
-  *bn = t[param][1];
-}
 
 std::vector<Edge> all_edges(const Graph& g) {
   std::vector<Edge> e = g.edges;
@@ -99,8 +85,9 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
         }
         if (g.opt_algos >> SN_ALGO_DIRECT & 1) add(lay, SN_ALGO_DIRECT, 0);
         if (g.opt_algos >> SN_ALGO_IGEMM & 1) {
-          int np = g.opt_params ? igemm_num_params(g.dtype) : 1;
-          for (int p = 0; p < np; ++p) add(lay, SN_ALGO_IGEMM, p);
+          int np = g.opt_params ? k::igemm_num_params(g.dtype) : 1;
+          for (int p = 0; p < np; ++p)
+            if (k::igemm_param_valid(g.dtype, p, lay, in.c)) add(lay, SN_ALGO_IGEMM, p);
         }
         if ((g.opt_algos >> SN_ALGO_WINOGRAD & 1) && winograd_applicable(L, in))
           add(lay, SN_ALGO_WINOGRAD, 0);

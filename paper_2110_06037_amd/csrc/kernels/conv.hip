@@ -55,22 +55,48 @@ struct Mfma<float> {
 // GEMM view: rows m = (n, p, q) output pixels, columns = output channels,
 // reduction = (r, s, c).  One workgroup (4 waves, 2 x 2) computes a BM x BN
 // tile; each wave a (BM/2) x (BN/2) sub-tile of 16 x 16 MFMA blocks.  The
-// reduction advances 32 elements (4 chunks of 8 channels) per step through
-// double-buffered LDS tiles: A is gathered from the input (im2col on the
-// fly), B streams from the prepared weights.
+// reduction advances BK elements (BK/8 chunks of 8 channels) per step
+// through double-buffered LDS tiles: A is gathered from the input (im2col on
+// the fly), B streams from the prepared weights; the next step's global
+// loads are issued before the current step's MFMAs.  Workgroups are ordered
+// so that each XCD (L2 domain) works on a contiguous group of tiles that
+// share input rows, and small problems split the reduction over several
+// workgroups (fp32 partial tiles, summed by a second kernel).
 struct IgArgs {
   const void* x;
   const void* w;
   const float* bias;
   void* y;
+  float* part;         // split-K partial tiles [splits][M][Ng]
   int C, H, W, Cs;     // input channels, spatial size, stored channels
   int K, P, Q, Ks;     // output channels (real), spatial size, stored channels
   int R, S, stride, pad, act;
   int M, Ng, CB, KC, Kred;  // rows, GEMM columns, chunks/tap, chunks total, weight row length
   int PQ;
+  int tiles_m, tiles_n, splits, kt_per;  // grid decomposition
   long long x_bs, w_bs, y_bs;  // per-blockIdx.z offsets (batched GEMM), elements
-  int vec;                     // A chunks are aligned 8-element vectors (NHWC, C % 8 == 0)
+  int vec;                     // NHWC input with C % 8 == 0 (aligned 8-channel vectors)
+  long long x_elems, w_elems;  // elements addressable per blockIdx.z (buffer ranges)
 };
+
+// Raw buffer access: an SGPR resource (base, byte range) plus a 32-bit
+// offset; loads at offsets beyond the range return zero, which implements
+// the zero padding and the ragged tile edges without branches.
+constexpr unsigned kOOB = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, long long bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
+}
+template <typename T>
+__device__ __forceinline__ V8<T> bload8(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
+  V8<T> out;
+  auto v0 = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, soff, 0);
+  __builtin_memcpy(&out, &v0, 16);
+  if constexpr (sizeof(T) == 4) {
+    auto v1 = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(voff + 16), soff, 0);
+    __builtin_memcpy(reinterpret_cast<char*>(&out) + 16, &v1, 16);
+  }
+  return out;
+}
 
 struct ChunkPos {
   int r, s, cb;
@@ -81,8 +107,8 @@ __device__ __forceinline__ void chunk_set(ChunkPos& p, int g, int CB, int S) {
   p.r = rs / S;
   p.s = rs - p.r * S;
 }
-__device__ __forceinline__ void chunk_adv4(ChunkPos& p, int CB, int S) {
-  p.cb += 4;
+__device__ __forceinline__ void chunk_adv(ChunkPos& p, int step, int CB, int S) {
+  p.cb += step;
   while (p.cb >= CB) {
     p.cb -= CB;
     if (++p.s == S) {
@@ -92,109 +118,229 @@ __device__ __forceinline__ void chunk_adv4(ChunkPos& p, int CB, int S) {
   }
 }
 
-template <typename T, int L, int BM, int BN, bool RAW>
+// epilogue modes
+constexpr int EPI_LAYOUT = 0;  // bias + activation, store in the tensor layout
+constexpr int EPI_RAW = 1;     // raw float32 [M][Ng] (Winograd tile GEMMs)
+constexpr int EPI_SPLIT = 2;   // raw float32 partial tile of one reduction split
+
+// Map the linear workgroup id to (m-tile, n-tile): consecutive ids are
+// dispatched round-robin over the 8 XCDs, so first regroup them into one
+// contiguous range per XCD, then walk groups of 8 m-tiles across all
+// n-tiles (tiles of a group share A rows in that XCD's L2).
+__device__ __forceinline__ void tile_of(int pid, int tiles_m, int tiles_n, int& mt, int& nt) {
+  const int nb = tiles_m * tiles_n;
+  const int q = nb >> 3, r = nb & 7;
+  const int xcd = pid & 7, slot = pid >> 3;
+  const int v = xcd * q + min(xcd, r) + slot;
+  constexpr int GM = 8;
+  const int group = v / (GM * tiles_n);
+  const int first = group * GM;
+  const int gsize = min(tiles_m - first, GM);
+  const int in = v - group * GM * tiles_n;
+  mt = first + in % gsize;
+  nt = in / gsize;
+}
+
+// Read-only zero page: masked-off lanes load from here, so every global load
+// is unconditional (no divergent branches around loads, which would force
+// the compiler to drain all outstanding loads).
+__device__ __attribute__((aligned(256))) unsigned char g_zero_page[256];
+
+// Workgroup barrier for the LDS pipeline: waits only for this wave's LDS
+// operations (the tile stores), not for its in-flight global loads, which
+// target registers and belong to the next step.  (__syncthreads() also
+// drains all global loads, which would serialise the prefetch.)  The memory
+// clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <typename T, int L, bool VEC, bool ALIGNED, int BM, int BN, int BK, int EPI, int PF>
 __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
-  constexpr int BK = 32;
   constexpr bool F32 = std::is_same<T, float>::value;
-  constexpr int LDK = BK + (F32 ? 4 : 8);
+  constexpr int CPR = BK / 8;                   // chunks per tile row
+  // 16-bit tiles: unpadded rows of BK elements with the 16-byte chunk slot
+  // XOR-swizzled by the row, so both the 16-byte stores (consecutive chunks
+  // of a few rows) and the MFMA fragment reads (one chunk of 16 rows) hit
+  // distinct LDS banks.  fp32 tiles use padded rows instead.
+  constexpr int LDK = BK + (F32 ? 4 : 0);
+  constexpr int RPR = F32 ? 1 : 128 / BK;  // rows sharing one bank range
   constexpr int WTM = BM / 2, WTN = BN / 2;
   constexpr int FM = WTM / 16, FN = WTN / 16;
-  constexpr int NSA = BM / 64, NSB = BN / 64;  // 8-element chunks per thread
+  constexpr int NA = BM * CPR / 256;            // A chunks per thread
+  constexpr int NB = BN * CPR / 256;            // B chunks per thread
+  constexpr int RS = VEC ? NA : 1;              // distinct A rows per thread
+  constexpr int CS = VEC ? 1 : NA;              // distinct A chunks per thread
+  static_assert(NA >= 1 && NB >= 1 && (VEC || 256 % BM == 0), "tile too small for 256 threads");
+  static_assert(PF >= 2 && PF % 2 == 0, "prefetch depth must be even (LDS double buffer parity)");
   constexpr int CPAD = F32 ? 4 : 8;
+  // SWAP: weights are the MFMA's first operand, so each lane's 4 accumulator
+  // values are 4 consecutive output channels of one pixel (channel-vector
+  // layouts); otherwise 4 consecutive pixels of one channel (NCHW).
+  constexpr bool SWAP = L != NCHW;
   constexpr int SM_AB = 2 * (BM + BN) * LDK * (int)sizeof(T);
-  constexpr int SM_C = BM * (BN + CPAD) * (int)sizeof(T);
+  constexpr int SM_C = EPI == EPI_LAYOUT ? BM * (BN + CPAD) * (int)sizeof(T) : 0;
   constexpr int SM = SM_AB > SM_C ? SM_AB : SM_C;
   __shared__ __attribute__((aligned(16))) char smem[SM];
   T(*As)[BM][LDK] = reinterpret_cast<T(*)[BM][LDK]>(smem);
   T(*Bs)[BN][LDK] = reinterpret_cast<T(*)[BN][LDK]>(smem + 2 * BM * LDK * sizeof(T));
+  auto slot = [](int row, int chunk) { return F32 ? chunk : chunk ^ ((row / RPR) % CPR); };
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  int mt, nt;
+  tile_of(blockIdx.x, a.tiles_m, a.tiles_n, mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int split = blockIdx.y;
+  const int KT_all = (a.KC + CPR - 1) / CPR;
+  const int kt0 = split * a.kt_per;
+  const int KT = min(KT_all - kt0, a.kt_per);
   const T* __restrict__ x = reinterpret_cast<const T*>(a.x) + blockIdx.z * a.x_bs;
   const T* __restrict__ w = reinterpret_cast<const T*>(a.w) + blockIdx.z * a.w_bs;
 
-  constexpr bool VEC_L = (L == NC8);
-  const bool vec = VEC_L || (L == NHWC && a.vec);
-
-  // per-slot A state: row decode and reduction position
-  int arow[NSA], aj[NSA], aimg[NSA], ah0[NSA], aw0[NSA];
-  bool arv[NSA];
-  ChunkPos apos[NSA];
+  // A: thread -> (rows, chunk columns) of the tile
+  int arow[RS], aimg[RS], ah0[RS], aw0[RS];
+  bool arv[RS];
+  int aj[CS];
+  ChunkPos apos[CS];
 #pragma unroll
-  for (int i = 0; i < NSA; ++i) {
-    if (vec) {
-      arow[i] = (tid >> 2) + 64 * i;
-      aj[i] = tid & 3;
-    } else {
-      arow[i] = tid % BM;
-      aj[i] = (tid / BM) * NSA + i;
-    }
-    int m = m0 + arow[i];
+  for (int i = 0; i < RS; ++i) {
+    arow[i] = VEC ? (tid / CPR + (256 / CPR) * i) : (tid % BM);
+    const int m = m0 + arow[i];
     arv[i] = m < a.M;
-    int mm = arv[i] ? m : 0;
-    int img = mm / a.PQ, pq = mm - img * a.PQ;
-    int p = pq / a.Q, q = pq - p * a.Q;
+    const int mm = arv[i] ? m : 0;
+    const int img = mm / a.PQ, pq = mm - img * a.PQ;
+    const int p = pq / a.Q, q = pq - p * a.Q;
     aimg[i] = img;
     ah0[i] = p * a.stride - a.pad;
     aw0[i] = q * a.stride - a.pad;
-    chunk_set(apos[i], aj[i], a.CB, a.S);
+  }
+#pragma unroll
+  for (int c = 0; c < CS; ++c) {
+    aj[c] = VEC ? tid % CPR : (tid / BM) * CS + c;
+    if constexpr (!ALIGNED) chunk_set(apos[c], kt0 * CPR + aj[c], a.CB, a.S);
+  }
+  // ALIGNED (C % BK == 0, R*S <= 32): every reduction step lies inside one
+  // filter tap, so the tap (r, s) and first channel block cb0 are uniform per
+  // step; each A row keeps its byte offset and a bitmask of the taps that
+  // fall inside the (unpadded) input.
+  const T* zp = reinterpret_cast<const T*>(g_zero_page);
+  constexpr int ES = (int)sizeof(T);
+  unsigned rbyte[RS], tvm[RS];
+  ChunkPos upos{0, 0, 0};
+  __amdgpu_buffer_rsrc_t rx = make_rsrc(x, a.x_elems * ES);
+  __amdgpu_buffer_rsrc_t rw = make_rsrc(w, a.w_elems * ES);
+  if constexpr (ALIGNED) {
+#pragma unroll
+    for (int i = 0; i < RS; ++i) {
+      int e;
+      if constexpr (L == NC8)
+        e = (aimg[i] * a.CB * a.H * a.W + ah0[i] * a.W + aw0[i]) * 8 + aj[0] * a.H * a.W * 8;
+      else
+        e = ((aimg[i] * a.H + ah0[i]) * a.W + aw0[i]) * a.Cs + aj[0] * 8;
+      rbyte[i] = (unsigned)(e * ES);
+      unsigned m = 0;
+      for (int r = 0; r < a.R; ++r)
+        for (int q = 0; q < a.S; ++q)
+          if (arv[i] && (unsigned)(ah0[i] + r) < (unsigned)a.H && (unsigned)(aw0[i] + q) < (unsigned)a.W)
+            m |= 1u << (r * a.S + q);
+      tvm[i] = m;
+    }
+    chunk_set(upos, kt0 * CPR, a.CB, a.S);
+  }
+  unsigned bbyte[NB];
+  int brow[NB];
+  bool bv[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int row = tid / CPR + (256 / CPR) * i;
+    bv[i] = n0 + row < a.Ng;
+    brow[i] = (n0 + row) * a.Kred + (tid % CPR) * 8;
+    bbyte[i] = bv[i] ? (unsigned)(brow[i] * ES) : kOOB;
   }
 
-  V8<T> ra[NSA], rb[NSB];
-  auto load_a = [&](int kt) {
+  // PF register staging sets: the loads of step t+1 are issued PF-1 steps
+  // before they are stored to LDS (prefetch distance PF, LDS double buffer)
+  V8<T> ra[PF][NA], rb[PF][NB];
+  auto load_a = [&](V8<T>(&rs)[NA], int kt) {
+    if constexpr (ALIGNED) {
+      int tap;
+      if constexpr (L == NC8)
+        tap = upos.cb * a.H * a.W * 8 + (upos.r * a.W + upos.s) * 8;
+      else
+        tap = (upos.r * a.W + upos.s) * a.Cs + upos.cb * 8;
+      const unsigned tb = (unsigned)(tap * ES);
+      const int t = upos.r * a.S + upos.s;
 #pragma unroll
-    for (int i = 0; i < NSA; ++i) {
-      const int g = kt * 4 + aj[i];
-      const int h = ah0[i] + apos[i].r, ww = aw0[i] + apos[i].s;
-      const bool ok = arv[i] && g < a.KC && (unsigned)h < (unsigned)a.H && (unsigned)ww < (unsigned)a.W;
-      if (vec) {
-        if (ok) {
+      for (int i = 0; i < RS; ++i) {
+        const unsigned off = ((tvm[i] >> t) & 1u) ? rbyte[i] + tb : kOOB;
+        rs[i] = bload8<T>(rx, off, 0);
+      }
+      // next step: channel blocks advance by CPR; CB is a multiple of CPR
+      upos.cb += CPR;
+      if (upos.cb == a.CB) {
+        upos.cb = 0;
+        if (++upos.s == a.S) {
+          upos.s = 0;
+          ++upos.r;
+        }
+      }
+      return;
+    }
+#pragma unroll
+    for (int i = 0; i < RS; ++i)
+#pragma unroll
+      for (int c = 0; c < CS; ++c) {
+        const int slot = i * CS + c;
+        const int g = kt * CPR + aj[c];
+        const int h = ah0[i] + apos[c].r, ww = aw0[i] + apos[c].s;
+        const bool ok = arv[i] && g < a.KC && (unsigned)h < (unsigned)a.H && (unsigned)ww < (unsigned)a.W;
+        if constexpr (VEC) {
           const T* p;
           if constexpr (L == NC8)
-            p = x + ((((long long)aimg[i] * a.CB + apos[i].cb) * a.H + h) * a.W + ww) * 8;
+            p = x + ((((long long)aimg[i] * a.CB + apos[c].cb) * a.H + h) * a.W + ww) * 8;
           else
-            p = x + (((long long)aimg[i] * a.H + h) * a.W + ww) * a.Cs + apos[i].cb * 8;
-          ra[i] = ld8(p);
+            p = x + (((long long)aimg[i] * a.H + h) * a.W + ww) * a.Cs + apos[c].cb * 8;
+          rs[slot] = ld8(ok ? p : zp);
         } else {
-          ra[i] = zero8<T>();
-        }
-      } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int c = apos[i].cb * 8 + e;
-          T v = (T)0.f;
-          if (ok && c < a.C) {
-            if constexpr (L == NCHW)
-              v = x[(((long long)aimg[i] * a.Cs + c) * a.H + h) * a.W + ww];
-            else
-              v = x[(((long long)aimg[i] * a.H + h) * a.W + ww) * a.Cs + c];
+          for (int e = 0; e < 8; ++e) {
+            const int ch = apos[c].cb * 8 + e;
+            T v = (T)0.f;
+            if (ok && ch < a.C) {
+              if constexpr (L == NCHW)
+                v = x[(((long long)aimg[i] * a.Cs + ch) * a.H + h) * a.W + ww];
+              else if constexpr (L == NHWC)
+                v = x[(((long long)aimg[i] * a.H + h) * a.W + ww) * a.Cs + ch];
+              else
+                v = x[((((long long)aimg[i] * a.CB + (ch >> 3)) * a.H + h) * a.W + ww) * 8 + (ch & 7)];
+            }
+            rs[slot].v[e] = v;
           }
-          ra[i].v[e] = v;
         }
+      }
+#pragma unroll
+    for (int c = 0; c < CS; ++c) chunk_adv(apos[c], CPR, a.CB, a.S);
+  };
+  auto load_b = [&](V8<T>(&rs)[NB], int kt) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      if constexpr (ALIGNED) {
+        rs[i] = bload8<T>(rw, bbyte[i], kt * BK * ES);
+      } else {
+        const bool ok = bv[i] && kt * CPR + (tid % CPR) < a.KC;
+        rs[i] = ld8(ok ? w + (brow[i] + kt * BK) : zp);
       }
     }
   };
-  auto load_b = [&](int kt) {
+  auto store_ab = [&](const V8<T>(&sa)[NA], const V8<T>(&sb)[NB], int buf) {
 #pragma unroll
-    for (int i = 0; i < NSB; ++i) {
-      const int row = (tid >> 2) + 64 * i, j = tid & 3;
-      const int g = kt * 4 + j, n = n0 + row;
-      if (n < a.Ng && g < a.KC)
-        rb[i] = ld8(w + (long long)n * a.Kred + g * 8);
-      else
-        rb[i] = zero8<T>();
-    }
-  };
-  auto store_ab = [&](int buf) {
+    for (int i = 0; i < RS; ++i)
 #pragma unroll
-    for (int i = 0; i < NSA; ++i) st8(&As[buf][arow[i]][aj[i] * 8], ra[i]);
+      for (int c = 0; c < CS; ++c) st8(&As[buf][arow[i]][slot(arow[i], aj[c]) * 8], sa[i * CS + c]);
 #pragma unroll
-    for (int i = 0; i < NSB; ++i) st8(&Bs[buf][(tid >> 2) + 64 * i][(tid & 3) * 8], rb[i]);
-  };
-  auto advance = [&]() {
-#pragma unroll
-    for (int i = 0; i < NSA; ++i) chunk_adv4(apos[i], a.CB, a.S);
+    for (int i = 0; i < NB; ++i)
+      st8(&Bs[buf][tid / CPR + (256 / CPR) * i][slot(tid / CPR + (256 / CPR) * i, tid % CPR) * 8], sb[i]);
   };
 
   f32x4 acc[FM][FN];
@@ -203,18 +349,7 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int KT = (a.KC + 3) / 4;
-  load_a(0);
-  load_b(0);
-  store_ab(0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) {
-      advance();
-      load_a(kt + 1);
-      load_b(kt + 1);
-    }
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int ks = 0; ks < BK / Mfma<T>::KSTEP; ++ks) {
       typename Mfma<T>::frag fa[FM], fb[FN];
@@ -224,7 +359,7 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
         if constexpr (F32)
           fa[i] = As[buf][r][ks * 4 + (lane >> 4)];
         else
-          fa[i] = *reinterpret_cast<const typename Mfma<T>::frag*>(&As[buf][r][ks * 32 + (lane >> 4) * 8]);
+          fa[i] = *reinterpret_cast<const typename Mfma<T>::frag*>(&As[buf][r][slot(r, ks * 4 + (lane >> 4)) * 8]);
       }
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
@@ -232,55 +367,117 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
         if constexpr (F32)
           fb[j] = Bs[buf][r][ks * 4 + (lane >> 4)];
         else
-          fb[j] = *reinterpret_cast<const typename Mfma<T>::frag*>(&Bs[buf][r][ks * 32 + (lane >> 4) * 8]);
+          fb[j] = *reinterpret_cast<const typename Mfma<T>::frag*>(&Bs[buf][r][slot(r, ks * 4 + (lane >> 4)) * 8]);
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fa[i], fb[j], acc[i][j]);
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = SWAP ? Mfma<T>::run(fb[j], fa[i], acc[i][j]) : Mfma<T>::run(fa[i], fb[j], acc[i][j]);
     }
-    if (kt + 1 < KT) store_ab(buf ^ 1);
-    __syncthreads();
+  };
+
+  // step t: store tile t+1 (register set (t+1) % PF, loaded PF-1 steps
+  // earlier) into LDS[(t+1)&1], issue the loads of tile t+PF into set t % PF
+  // (tile t went to LDS at step t-1), compute LDS[t&1]; one barrier per step
+#pragma unroll
+  for (int u = 0; u < PF; ++u)
+    if (u < KT) {
+      load_a(ra[u], kt0 + u);
+      load_b(rb[u], kt0 + u);
+    }
+  if (KT > 0) store_ab(ra[0], rb[0], 0);
+  lds_barrier();
+  for (int it0 = 0; it0 < KT; it0 += PF) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int t = it0 + u;
+      if (t < KT) {
+        if (t + 1 < KT) store_ab(ra[(u + 1) % PF], rb[(u + 1) % PF], (u + 1) & 1);
+        if (t + PF < KT) {
+          load_a(ra[u], kt0 + t + PF);
+          load_b(rb[u], kt0 + t + PF);
+        }
+        compute(u & 1);
+        lds_barrier();
+      }
+    }
   }
 
-  // accumulator element (i, j, v) is C[wm*WTM + i*16 + (lane>>4)*4 + v][wn*WTN + j*16 + (lane&15)]
-  if constexpr (RAW) {
-    float* __restrict__ y = reinterpret_cast<float*>(a.y) + blockIdx.z * a.y_bs;
+  // accumulator element (i, j, v):
+  //   !SWAP: C[wm*WTM + i*16 + (lane>>4)*4 + v][wn*WTN + j*16 + (lane&15)]
+  //    SWAP: C[wm*WTM + i*16 + (lane&15)][wn*WTN + j*16 + (lane>>4)*4 + v]
+  if constexpr (EPI != EPI_LAYOUT) {
+    float* __restrict__ y = EPI == EPI_RAW ? reinterpret_cast<float*>(a.y) + blockIdx.z * a.y_bs
+                                           : a.part + (long long)split * a.M * a.Ng;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
-        const int n = n0 + wn * WTN + j * 16 + (lane & 15);
+        if constexpr (SWAP) {
+          const int m = m0 + wm * WTM + i * 16 + (lane & 15);
+          const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
+          if (m < a.M) {
+            if (n + 4 <= a.Ng && (a.Ng & 3) == 0) {
+              *reinterpret_cast<f32x4*>(y + (long long)m * a.Ng + n) = acc[i][j];
+            } else {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int m = m0 + wm * WTM + i * 16 + (lane >> 4) * 4 + v;
-          if (m < a.M && n < a.Ng) y[(long long)m * a.Ng + n] = acc[i][j][v];
+              for (int v = 0; v < 4; ++v)
+                if (n + v < a.Ng) y[(long long)m * a.Ng + n + v] = acc[i][j][v];
+            }
+          }
+        } else {
+          const int n = n0 + wn * WTN + j * 16 + (lane & 15);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int m = m0 + wm * WTM + i * 16 + (lane >> 4) * 4 + v;
+            if (m < a.M && n < a.Ng) y[(long long)m * a.Ng + n] = acc[i][j][v];
+          }
         }
       }
     return;
   } else {
     T(*Cs)[BN + CPAD] = reinterpret_cast<T(*)[BN + CPAD]>(smem);
+    if constexpr (SWAP) {
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int nl = wn * WTN + j * 16 + (lane & 15);
-      const int n = n0 + nl;
-      const float bv = n < a.Ng ? a.bias[n] : 0.f;
+      for (int j = 0; j < FN; ++j) {
+        const int nl = wn * WTN + j * 16 + (lane >> 4) * 4;
+        float bv[4];
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+        for (int v = 0; v < 4; ++v) bv[v] = n0 + nl + v < a.Ng ? a.bias[n0 + nl + v] : 0.f;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int ml = wm * WTM + i * 16 + (lane >> 4) * 4 + v;
-          Cs[ml][nl] = from_f<T>(act_f(acc[i][j][v] + bv, a.act));
+        for (int i = 0; i < FM; ++i) {
+          const int ml = wm * WTM + i * 16 + (lane & 15);
+          T o[4];
+#pragma unroll
+          for (int v = 0; v < 4; ++v) o[v] = from_f<T>(act_f(acc[i][j][v] + bv[v], a.act));
+          __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
         }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int nl = wn * WTN + j * 16 + (lane & 15);
+        const int n = n0 + nl;
+        const float bv = n < a.Ng ? a.bias[n] : 0.f;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int ml = wm * WTM + i * 16 + (lane >> 4) * 4 + v;
+            Cs[ml][nl] = from_f<T>(act_f(acc[i][j][v] + bv, a.act));
+          }
+      }
     }
     __syncthreads();
     T* __restrict__ y = reinterpret_cast<T*>(a.y) + blockIdx.z * a.y_bs;
     if constexpr (L == NCHW) {
-      const int row = tid % BM, m = m0 + row;
-      if (m < a.M) {
+      for (int row = tid % BM; row < BM; row += 256) {
+        const int m = m0 + row;
+        if (m >= a.M) continue;
         const int img = m / a.PQ, pq = m - img * a.PQ;
         T* yb = y + (long long)img * a.Ks * a.PQ + pq;
-        for (int col = tid / BM; col < BN; col += 256 / BM) {
+        for (int col = tid / BM; col < BN; col += (BM >= 256 ? 1 : 256 / BM)) {
           const int n = n0 + col;
           if (n < a.Ng) yb[(long long)n * a.PQ] = Cs[row][col];
         }
@@ -308,26 +505,154 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
   }
 }
 
-template <typename T, int L, int BM, int BN, bool RAW>
-static void igemm_go(const IgArgs& a, int batch, hipStream_t st) {
-  dim3 grid((a.M + BM - 1) / BM, (a.Ng + BN - 1) / BN, batch);
-  hipLaunchKernelGGL((igemm_kernel<T, L, BM, BN, RAW>), grid, dim3(256), 0, st, a);
+// Sum the split-K partial tiles, add the bias, apply the activation and
+// store in the tensor layout.  One thread per (pixel, 8 output channels);
+// NCHW: one thread per (channel, pixel), pixels fastest.
+template <typename T, int L>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(IgArgs a) {
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  const long long plane = (long long)a.M * a.Ng;
+  T* __restrict__ y = reinterpret_cast<T*>(a.y);
+  if constexpr (L == NCHW) {
+    if (idx >= plane) return;
+    const int m = (int)(idx % a.M), n = (int)(idx / a.M);
+    float s = a.bias[n];
+    for (int k = 0; k < a.splits; ++k) s += a.part[k * plane + (long long)m * a.Ng + n];
+    const int img = m / a.PQ, pq = m - img * a.PQ;
+    y[((long long)img * a.Ks + n) * a.PQ + pq] = from_f<T>(act_f(s, a.act));
+  } else {
+    const int NB8 = (a.Ng + 7) / 8;
+    if (idx >= (long long)a.M * NB8) return;
+    const int nb = (int)(idx % NB8), m = (int)(idx / NB8);
+    const int n0 = nb * 8;
+    float s[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] = n0 + e < a.Ng ? a.bias[n0 + e] : 0.f;
+    for (int k = 0; k < a.splits; ++k) {
+      const float* p = a.part + k * plane + (long long)m * a.Ng + n0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (n0 + e < a.Ng) s[e] += p[e];
+    }
+    V8<T> o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o.v[e] = from_f<T>(act_f(s[e], a.act));
+    if constexpr (L == NC8) {
+      const int img = m / a.PQ, pq = m - img * a.PQ;
+      st8(y + (((long long)img * (a.Ks >> 3) + nb) * a.PQ + pq) * 8, o);
+    } else if (a.Ks % 8 == 0) {
+      st8(y + (long long)m * a.Ks + n0, o);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (n0 + e < a.Ng) y[(long long)m * a.Ks + n0 + e] = o.v[e];
+    }
+  }
 }
 
-template <typename T, int L, bool RAW>
-static void igemm_tiles(int bm, int bn, const IgArgs& a, int batch, hipStream_t st) {
+// Routine parameters of the implicit-GEMM routine (index = routine param).
+struct IgCfg {
+  int bm, bn, bk, split, pf;  // split: 0 = none, 1 = split the reduction when tiles are few;
+                              // pf: prefetch depth (register staging sets)
+};
+static const IgCfg kIg16[] = {{64, 64, 32, 0, 2},   {128, 128, 64, 0, 2}, {256, 128, 32, 0, 2},
+                              {128, 64, 64, 0, 2},  {64, 128, 64, 0, 4},  {128, 128, 64, 1, 2},
+                              {64, 64, 64, 1, 4},   {128, 64, 32, 0, 4},  {64, 128, 64, 0, 2},
+                              {96, 128, 64, 0, 2},  {64, 64, 64, 0, 4},   {128, 128, 32, 0, 4},
+                              {64, 128, 32, 0, 4},  {128, 64, 64, 0, 4},  {64, 128, 128, 0, 2},
+                              {128, 64, 128, 0, 2}, {128, 128, 128, 0, 2}};
+static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
+
+int igemm_num_params(int dtype) {
+  return dtype == 0 ? (int)(sizeof(kIg32) / sizeof(kIg32[0])) : (int)(sizeof(kIg16) / sizeof(kIg16[0]));
+}
+
+// A configuration whose tile rows do not divide the 256 threads needs the
+// 8-channel vector loader (NHWC with C % 8 == 0, or NC8HW8).
+bool igemm_param_valid(int dtype, int param, int layout, int c) {
+  if (param < 0 || param >= igemm_num_params(dtype)) return false;
+  const IgCfg& g = dtype == 0 ? kIg32[param] : kIg16[param];
+  const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
+  return vec || 256 % g.bm == 0;
+}
+
+static IgCfg ig_cfg(int dtype, int param) {
+  check(param >= 0 && param < igemm_num_params(dtype), "unknown implicit-GEMM parameter");
+  return dtype == 0 ? kIg32[param] : kIg16[param];
+}
+
+// Fills the grid decomposition of `a` for configuration `c`.
+static void ig_decompose(IgArgs& a, const IgCfg& c) {
+  a.tiles_m = (a.M + c.bm - 1) / c.bm;
+  a.tiles_n = (a.Ng + c.bn - 1) / c.bn;
+  const int cpr = c.bk / 8;
+  const int KT = (a.KC + cpr - 1) / cpr;
+  int splits = 1;
+  if (c.split) {
+    const int tiles = a.tiles_m * a.tiles_n;
+    if (tiles < 384) splits = std::min(std::min((768 + tiles - 1) / tiles, 8), std::max(1, KT / 2));
+  }
+  a.kt_per = (KT + splits - 1) / splits;
+  a.splits = (KT + a.kt_per - 1) / a.kt_per;
+}
+
+template <typename T, int L, bool VEC, int BM, int BN, int BK, int EPI, int PF>
+static void igemm_go(const IgArgs& a, int batch, hipStream_t st) {
+  check(a.x_elems * (long long)sizeof(T) < (long long)kOOB && a.w_elems * (long long)sizeof(T) < (long long)kOOB,
+        "tensor too large for 32-bit buffer offsets");
+  dim3 grid(a.tiles_m * a.tiles_n, a.splits, batch);
+  if (VEC && a.CB % (BK / 8) == 0 && a.R * a.S <= 32)
+    hipLaunchKernelGGL((igemm_kernel<T, L, VEC, VEC, BM, BN, BK, EPI, PF>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((igemm_kernel<T, L, VEC, false, BM, BN, BK, EPI, PF>), grid, dim3(256), 0, st, a);
+}
+
+template <typename T, int L, bool VEC, int EPI>
+static void igemm_cfg(const IgCfg& c, const IgArgs& a, int batch, hipStream_t st) {
   if constexpr (std::is_same<T, float>::value) {
-    check(bm == 64 && bn == 64, "fp32 implicit GEMM has one 64x64 tile");
-    igemm_go<T, L, 64, 64, RAW>(a, batch, st);
+    igemm_go<T, L, VEC, 64, 64, 32, EPI, 2>(a, batch, st);
   } else {
-    if (bm == 128 && bn == 128)
-      igemm_go<T, L, 128, 128, RAW>(a, batch, st);
-    else if (bm == 64 && bn == 64)
-      igemm_go<T, L, 64, 64, RAW>(a, batch, st);
-    else if (bm == 128 && bn == 64)
-      igemm_go<T, L, 128, 64, RAW>(a, batch, st);
-    else
-      check(false, "unknown implicit-GEMM tile");
+    const int key = ((c.bm * 1000 + c.bn) * 100 + c.bk) * 10 + c.pf;
+#define IGC(BM_, BN_, BK_, PF_) \
+  case ((BM_ * 1000 + BN_) * 100 + BK_) * 10 + PF_: igemm_go<T, L, VEC, BM_, BN_, BK_, EPI, PF_>(a, batch, st); break;
+    if constexpr (EPI == EPI_RAW) {  // Winograd tile GEMMs
+      switch (key) {
+        IGC(64, 64, 64, 4)
+        IGC(128, 64, 64, 4)
+        default: check(false, "tile not instantiated for the raw epilogue");
+      }
+      return;
+    }
+    if constexpr (EPI == EPI_SPLIT) {  // split-reduction configurations
+      switch (key) {
+        IGC(128, 128, 64, 2)
+        IGC(64, 64, 64, 4)
+        default: check(false, "tile not instantiated for split reduction");
+      }
+      return;
+    }
+    switch (key) {
+      IGC(64, 64, 32, 2)
+      IGC(128, 128, 64, 2)
+      IGC(256, 128, 32, 2)
+      IGC(128, 64, 64, 2)
+      IGC(64, 128, 64, 4)
+      IGC(64, 64, 64, 4)
+      IGC(128, 64, 32, 4)
+      IGC(64, 128, 64, 2)
+      IGC(128, 128, 32, 4)
+      IGC(64, 128, 32, 4)
+      IGC(128, 64, 64, 4)
+      IGC(64, 128, 128, 2)
+      IGC(128, 64, 128, 2)
+      IGC(128, 128, 128, 2)
+      case ((96 * 1000 + 128) * 100 + 64) * 10 + 2:
+        if constexpr (VEC) igemm_go<T, L, VEC, 96, 128, 64, EPI, 2>(a, batch, st);
+        else check(false, "96-row tiles need the vector loader");
+        break;
+      default: check(false, "implicit-GEMM tile not instantiated");
+    }
+#undef IGC
   }
 }
 
@@ -357,27 +682,65 @@ static IgArgs make_ig(const ConvArgs& c) {
   a.KC = a.R * a.S * a.CB;
   a.Kred = a.KC * 8;
   a.vec = (c.xd.layout == NHWC && a.C % 8 == 0) ? 1 : 0;
+  a.x_elems = (long long)c.xd.n * c.xd.cs * c.xd.h * c.xd.w;
+  a.w_elems = (long long)((a.K + 7) / 8 * 8) * a.Kred;
   return a;
 }
 
+size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s) {
+  const IgCfg c = ig_cfg(dtype, param);
+  if (!c.split) return 0;
+  ConvArgs cv{};
+  cv.xd = xd;
+  cv.yd = yd;
+  cv.r = r;
+  cv.s = s;
+  cv.stride = 1;
+  IgArgs a = make_ig(cv);
+  a.M = xd.n * yd.h * yd.w;
+  ig_decompose(a, c);
+  if (a.splits <= 1) return 0;
+  return (size_t)a.splits * a.M * a.Ng * sizeof(float);
+}
+
+template <typename T, int L, bool VEC>
+static void igemm_run(const IgCfg& cfg, IgArgs& a, const ConvArgs& c, hipStream_t st) {
+  if (a.splits > 1) {
+    check(c.ws && c.ws_bytes >= (size_t)a.splits * a.M * a.Ng * sizeof(float), "split-K workspace too small");
+    a.part = reinterpret_cast<float*>(c.ws);
+    igemm_cfg<T, L, VEC, EPI_SPLIT>(cfg, a, 1, st);
+    const long long n = L == NCHW ? (long long)a.M * a.Ng : (long long)a.M * ((a.Ng + 7) / 8);
+    hipLaunchKernelGGL((splitk_reduce_kernel<T, L>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a);
+  } else {
+    igemm_cfg<T, L, VEC, EPI_LAYOUT>(cfg, a, 1, st);
+  }
+}
+
 template <typename T>
-static void igemm_dispatch(int bm, int bn, const ConvArgs& c, hipStream_t st) {
+static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t st) {
+  const IgCfg cfg = ig_cfg(dtype, param);
   IgArgs a = make_ig(c);
   check(c.xd.layout == c.yd.layout, "implicit GEMM reads and writes one layout");
   check((long long)a.M * a.Ks < (1ll << 31) && (long long)c.xd.n * a.Cs * a.H * a.W < (1ll << 31),
         "tensor too large");
+  ig_decompose(a, cfg);
   switch (c.xd.layout) {
-    case NCHW: igemm_tiles<T, NCHW, false>(bm, bn, a, 1, st); break;
-    case NHWC: igemm_tiles<T, NHWC, false>(bm, bn, a, 1, st); break;
-    case NC8: igemm_tiles<T, NC8, false>(bm, bn, a, 1, st); break;
+    case NCHW: igemm_run<T, NCHW, false>(cfg, a, c, st); break;
+    case NHWC:
+      if (a.C % 8 == 0)
+        igemm_run<T, NHWC, true>(cfg, a, c, st);
+      else
+        igemm_run<T, NHWC, false>(cfg, a, c, st);
+      break;
+    case NC8: igemm_run<T, NC8, true>(cfg, a, c, st); break;
     default: check(false, "layout");
   }
 }
 
-void conv_igemm(int dtype, int bm, int bn, const ConvArgs& c, hipStream_t st) {
-  if (dtype == 0) igemm_dispatch<float>(bm, bn, c, st);
-  else if (dtype == 1) igemm_dispatch<f16>(bm, bn, c, st);
-  else igemm_dispatch<bf16>(bm, bn, c, st);
+void conv_igemm(int dtype, int param, const ConvArgs& c, hipStream_t st) {
+  if (dtype == 0) igemm_dispatch<float>(dtype, param, c, st);
+  else if (dtype == 1) igemm_dispatch<f16>(dtype, param, c, st);
+  else igemm_dispatch<bf16>(dtype, param, c, st);
 }
 
 // ------------------------------------------------------------------ direct (VALU)
@@ -727,15 +1090,17 @@ static void wino_dispatch(int dtype, const ConvArgs& c, hipStream_t st) {
   g.w_bs = (long long)Kp * a.C8;
   g.y_bs = (long long)a.T * a.Ng;
   g.vec = 1;
+  g.x_elems = (long long)a.T * a.C8;
+  g.w_elems = (long long)Kp * a.C8;
+  const IgCfg gc = std::is_same<T, float>::value ? IgCfg{64, 64, 32, 0, 2}
+                   : (a.T >= 4096 && a.Ng >= 128 ? IgCfg{128, 64, 64, 0, 4} : IgCfg{64, 64, 64, 0, 4});
+  ig_decompose(g, gc);
   switch (c.xd.layout) {
     case NCHW: hipLaunchKernelGGL((wino_in_kernel<T, NCHW>), gin, dim3(256), 0, st, a); break;
     case NHWC: hipLaunchKernelGGL((wino_in_kernel<T, NHWC>), gin, dim3(256), 0, st, a); break;
     case NC8: hipLaunchKernelGGL((wino_in_kernel<T, NC8>), gin, dim3(256), 0, st, a); break;
   }
-  if constexpr (std::is_same<T, float>::value)
-    igemm_tiles<T, NHWC, true>(64, 64, g, 16, st);
-  else
-    igemm_tiles<T, NHWC, true>(a.T >= 4096 ? 128 : 64, a.Ng >= 128 && a.T >= 4096 ? 128 : 64, g, 16, st);
+  igemm_cfg<T, NHWC, true, EPI_RAW>(gc, g, 16, st);
   switch (c.xd.layout) {
     case NCHW: hipLaunchKernelGGL((wino_out_kernel<T, NCHW>), gout, dim3(256), 0, st, a); break;
     case NHWC: hipLaunchKernelGGL((wino_out_kernel<T, NHWC>), gout, dim3(256), 0, st, a); break;

@@ -28,7 +28,12 @@ struct ConvArgs {
 };
 
 void conv_direct(int dtype, const ConvArgs& a, hipStream_t st);
-void conv_igemm(int dtype, int bm, int bn, const ConvArgs& a, hipStream_t st);
+// Implicit GEMM; `param` selects the tile configuration (routine parameter).
+// Parameters that split the reduction need a workspace of igemm_ws_bytes.
+void conv_igemm(int dtype, int param, const ConvArgs& a, hipStream_t st);
+int igemm_num_params(int dtype);
+bool igemm_param_valid(int dtype, int param, int layout, int c);
+size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s);
 size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k);
 void conv_winograd(int dtype, const ConvArgs& a, hipStream_t st);
 void dwconv(int dtype, const ConvArgs& a, hipStream_t st);
