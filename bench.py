@@ -61,6 +61,67 @@ def layer_work(spec, g, i, routine):
     return t, 0, 0
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_resnet50_bs32_bf16.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2110_06037_amd", "csrc", "kernels", f)
+                  for f in ("conv.hip", "kcommon.hpp")]
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(routine):
+    """HBM bytes per launch of `routine` from the committed PMC summary, or None
+    when there is none for it or the kernel sources changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("routine") != routine or t.get("source_hash") != kernel_source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def _pmc_rows(d):
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        rows += list(csv.DictReader(open(f)))
+    return rows
+
+
+def summarize_pmc(fetch_dir, write_dir, routine, ksub, out, calib_mib):
+    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the DP-path igemm launches,
+    scaled by what the counters read for a plain device copy of known size."""
+    res = {}
+    for name, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = [r for r in _pmc_rows(d) if r["Counter_Name"] == name]
+        # the calibration copy is by far the largest copy dispatch of the run
+        copy = [float(r["Counter_Value"]) for r in rows if "copy" in r["Kernel_Name"].lower()]
+        conv = [float(r["Counter_Value"]) for r in rows if ksub in r["Kernel_Name"]]
+        known_kib = calib_mib * 1024.0
+        scale = known_kib / max(copy) if copy and calib_mib else None
+        res[name] = {"dispatches": len(conv), "mean_kib": sum(conv) / max(1, len(conv)),
+                     "copy_kib": max(copy) if copy else None, "scale": scale}
+    f, w = res["FETCH_SIZE"], res["WRITE_SIZE"]
+    per = None
+    if f["scale"] and w["scale"]:
+        per = int((f["mean_kib"] * f["scale"] + w["mean_kib"] * w["scale"]) * 1024)
+    t = {"routine": routine, "kernel_symbol_part": ksub, "source_hash": kernel_source_hash(),
+         "bytes_per_launch": per,
+         "counters": res, "calibration": f"device copy of {calib_mib} MiB (read and write)"}
+    with open(out, "w") as fh:
+        json.dump(t, fh, indent=1)
+    print(json.dumps(t))
+
+
 def time_steps(g, x, out, steps, warmup):
     import torch
     for _ in range(warmup):
@@ -105,11 +166,28 @@ def main():
     ap.add_argument("--batch", type=int, default=32)
     ap.add_argument("--dtype", default="bf16")
     ap.add_argument("--profile-reps", type=int, default=20)
+    ap.add_argument("--timing-reps", type=int, default=50,
+                    help="back-to-back repetitions per layer in the per-layer timing pass")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-path sweep")
     ap.add_argument("--no-bs1", action="store_true", help="skip the batch-1 measurement")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--costs-out", default=None, help="write the measured cost table here")
+    ap.add_argument("--costs-in", default=None,
+                    help="select from this cost table instead of profiling (same workload)")
+    ap.add_argument("--tune-only", action="store_true",
+                    help="profile and select, write --costs-out, and exit")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the timed region, run one device copy of this size "
+                         "(a known-size kernel for scaling PMC byte counters)")
+    ap.add_argument("--summarize-pmc", nargs=5,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "ROUTINE", "KERNEL_SUBSTR", "OUT"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this script "
+                         "into the traffic summary OUT for the dispatches whose kernel name "
+                         "contains KERNEL_SUBSTR (the routine's kernel symbol), and exit")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, calib_mib=args.calib_copy_mib)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the path shards over the "
               "batch with no exchange, see DESIGN.md", file=sys.stderr)
@@ -126,15 +204,23 @@ def main():
     log(f"[bench] {spec['name']}: building graph")
     g = build_from_spec(spec, t, device=0)
     t0 = time.perf_counter()
-    g.profile(warmup=5, reps=args.profile_reps)
+    if args.costs_in:
+        with open(args.costs_in) as f:
+            g.set_costs(f.read())
+    else:
+        g.profile(warmup=5, reps=args.profile_reps)
     t_prof = time.perf_counter() - t0
     t1 = time.perf_counter()
     g.select("dprs")
     t_sel = time.perf_counter() - t1
-    log(f"[bench] profiled in {t_prof:.1f} s, selected in {t_sel * 1e3:.2f} ms")
+    log(f"[bench] {'loaded costs' if args.costs_in else 'profiled'} in {t_prof:.1f} s, "
+        f"selected in {t_sel * 1e3:.2f} ms")
     if args.costs_out:
         with open(args.costs_out, "w") as f:
             json.dump(g.costs(), f)
+    if args.tune_only:
+        g.close()
+        return
     ids, model_ns = g.path()
     x = to_dev(t["x"], args.dtype)
     out = g.empty_output()
@@ -143,47 +229,57 @@ def main():
     value = args.batch / sec
     log(f"[bench] DP path: {sec * 1e3:.3f} ms/step, {value:.1f} img/s")
 
-    # per-layer times over K instrumented steps (HIP events around each layer)
+    # per-layer times over K instrumented steps: each layer's launches are
+    # repeated back to back with HIP events tied to the first and last dispatch
     nl = g.num_layers()
     acc = np.zeros(nl)
     for _ in range(args.steps):
-        _, ms = g.run_timed(x, out)
+        _, ms = g.run_timed(x, out, reps=args.timing_reps)
         acc += np.array(ms)
     layer_ms = acc / args.steps
-    groups = {}
+    groups = {}      # routine -> its launches in one step (one kernel symbol per routine)
+    cats = {}        # layer category -> totals (for the 3x3 MFMA utilisation)
     per_layer = []
     for i in range(1, nl):
         rt = g.routines(i)[ids[i]]
         cat, flops, byt = layer_work(spec, g, i, rt)
-        key = (cat, rt["name"])
-        gr = groups.setdefault(key, {"ms": 0.0, "flops": 0, "bytes": 0, "launches": 0})
-        gr["ms"] += layer_ms[i]
-        gr["flops"] += flops
-        gr["bytes"] += byt
-        gr["launches"] += 1
+        for key, d in ((rt["name"], groups), (cat, cats)):
+            gr = d.setdefault(key, {"ms": 0.0, "flops": 0, "bytes": 0, "launches": 0, "cats": set()})
+            gr["ms"] += layer_ms[i]
+            gr["flops"] += flops
+            gr["bytes"] += byt
+            gr["launches"] += 1
+            gr["cats"].add(cat)
         per_layer.append({"layer": i, "type": cat, "routine": rt["name"],
                           "us": round(layer_ms[i] * 1e3, 2),
                           "tflops": round(flops / (layer_ms[i] * 1e-3) / 1e12, 2) if flops and layer_ms[i] else 0,
                           "gbs": round(byt / (layer_ms[i] * 1e-3) / 1e9, 1) if layer_ms[i] else 0})
     dom_key = max(groups, key=lambda k: groups[k]["ms"])
     dom = groups[dom_key]
-    cat = dom_key[0]
-    if cat.startswith("conv"):
-        ach = dom["flops"] / dom["launches"] / (dom["ms"] / dom["launches"] * 1e-3) / 1e12
+    avg_s = dom["ms"] / dom["launches"] * 1e-3
+    if any(c.startswith("conv") for c in dom["cats"]) and "direct" not in dom_key:
+        ach = dom["flops"] / dom["launches"] / avg_s / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_MFMA_TFLOPS[args.dtype],
                 "unit": "TFLOP/s"}
     else:
-        ach = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
+        ach = dom["bytes"] / dom["launches"] / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = None
-    roof["kernel"] = f"{dom_key[1]} on {cat} layers ({dom['launches']} launches/step)"
-    roof["avg_launch_us"] = round(dom["ms"] / dom["launches"] * 1e3, 2)
+    roof["traffic"] = traffic_for(dom_key)
+    roof["kernel"] = (f"routine {dom_key} ({dom['launches']} launches/step on "
+                      f"{'/'.join(sorted(dom['cats']))} layers)")
+    roof["avg_launch_us"] = round(avg_s * 1e6, 2)
+    roof["algorithmic"] = {"flops_per_launch": dom["flops"] // dom["launches"],
+                           "bytes_per_launch": dom["bytes"] // dom["launches"]}
     # headline: MFMA utilisation over the 3x3 convolutions
-    c3 = [(k, v) for k, v in groups.items() if k[0] == "conv3x3"]
-    c3_ms = sum(v["ms"] for _, v in c3)
-    c3_fl = sum(v["flops"] for _, v in c3)
-    conv3_util = c3_fl / (c3_ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS[args.dtype] if c3_ms else None
+    c3 = cats.get("conv3x3")
+    conv3_util = (c3["flops"] / (c3["ms"] * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS[args.dtype]) if c3 else None
+
+    if args.calib_copy_mib:
+        src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.zeros_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
 
     fixed = {}
     best_fixed = None

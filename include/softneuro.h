@@ -148,10 +148,14 @@ int sn_add_layer(sn_graph* g, const sn_layer_desc* d, const int32_t* inputs, int
 
 /* Unit profiling (Sec. III-C): times every routine of every layer on
  * scratch tensors of the layer's real shape, and every layout converter on
- * every edge (both directions of every schema pair), as the median of reps
- * timed runs after warmup runs (HIP events on the given stream).  Identical
- * layer signatures and converter shapes are timed once.  Synchronous.
- * Errors: SN_E_STATE (no layers), SN_E_DEVICE (host-only graph, HIP error). */
+ * every edge (both directions of every schema pair), after warmup runs, as
+ * the mean time of reps back-to-back runs.  HIP events are tied to the
+ * start of the first run's first kernel dispatch and the end of the last
+ * run's last one (hipExtLaunchKernelGGL), so host launch latency and the
+ * events' own dispatch gaps are amortised over the block.  Identical layer
+ * signatures and converter shapes are timed once.  Synchronous.
+ * Errors: SN_E_STATE (no layers), SN_E_INVALID (reps < 1 or warmup < 0),
+ * SN_E_DEVICE (host-only graph, HIP error). */
 int sn_profile(sn_graph* g, int32_t warmup, int32_t reps, void* hip_stream);
 
 /* Selects the routine path (Sec. IV) and compiles the execution plan
@@ -172,13 +176,18 @@ int sn_set_path(sn_graph* g, const int32_t* routine_ids, int32_t n);
  * Errors: SN_E_STATE (no plan), SN_E_DEVICE (host-only graph, HIP error). */
 int sn_run(sn_graph* g, const void* d_in, void* d_out, void* hip_stream);
 
-/* Like sn_run, then synchronises and writes the time of every layer's
- * launches (its routine plus the converters feeding it) to layer_ms[0..n-1]
- * (layer 0 and layers without launches get 0).  HIP events bracket each
- * layer on the stream; used to attribute time per routine.
- * Errors: as sn_run; SN_E_INVALID if n is not the number of layers. */
-int sn_run_timed(sn_graph* g, const void* d_in, void* d_out, void* hip_stream, float* layer_ms,
-                 int32_t n);
+/* Like sn_run, but enqueues every layer's launches (its routine plus the
+ * converters feeding it) reps times back to back, then synchronises and
+ * writes each layer's mean time per repetition to layer_ms[0..n-1] (layer 0
+ * gets 0).  HIP events are tied to the start of a layer's first kernel
+ * dispatch and the end of its last (hipExtLaunchKernelGGL), so host launch
+ * latency and the events' own dispatch gaps are amortised over reps.  Every
+ * launch writes buffers distinct from the ones it reads, so d_out holds the
+ * same result as after sn_run.  Used to attribute time per routine.
+ * Errors: as sn_run; SN_E_INVALID if n is not the number of layers or reps
+ * is outside 1..10000. */
+int sn_run_timed(sn_graph* g, const void* d_in, void* d_out, void* hip_stream, int32_t reps,
+                 float* layer_ms, int32_t n);
 
 /* Cost table as JSON (the profiling data of Sec. IV-A: T(r) per routine,
  * adapt times per edge and schema pair), all times int64 ns, -1 = no

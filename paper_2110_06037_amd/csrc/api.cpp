@@ -183,8 +183,8 @@ int sn_run(sn_graph* gp, const void* d_in, void* d_out, void* stream) {
   });
 }
 
-int sn_run_timed(sn_graph* gp, const void* d_in, void* d_out, void* stream, float* layer_ms,
-                 int32_t n) {
+int sn_run_timed(sn_graph* gp, const void* d_in, void* d_out, void* stream, int32_t reps,
+                 float* layer_ms, int32_t n) {
   return guarded([&] {
     CHECK_G(gp);
     Graph& g = gp->g;
@@ -192,7 +192,8 @@ int sn_run_timed(sn_graph* gp, const void* d_in, void* d_out, void* stream, floa
     if (g.path.empty()) fail(SN_E_STATE, "no routine path selected");
     if (!d_in || !d_out || !layer_ms) fail(SN_E_INVALID, "null pointer");
     if (n != g.n_layers()) fail(SN_E_INVALID, "layer_ms must have one entry per layer");
-    plan_run(g, d_in, d_out, stream, layer_ms);
+    if (reps < 1 || reps > 10000) fail(SN_E_INVALID, "reps must be in 1..10000");
+    plan_run(g, d_in, d_out, stream, layer_ms, reps);
   });
 }
 

@@ -131,7 +131,8 @@ void dev_destroy(Graph& g);
 void dev_upload_layer(Graph& g, int layer);
 void dev_profile(Graph& g, int warmup, int reps, void* stream);
 void plan_compile(Graph& g);
-void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms);
+void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms = nullptr,
+              int reps = 1);
 void plan_destroy(Graph& g);
 
 }  // namespace sn

@@ -57,8 +57,8 @@ struct Plan {
   std::vector<Step> steps;
   void* arena = nullptr;
   size_t arena_bytes = 0;
-  std::vector<int> first_step, last_step;  // per layer, -1 if none
-  std::vector<hipEvent_t> ev;              // 2 per layer (timed runs)
+  std::vector<int> first_step, last_step;  // per layer (steps of a layer are contiguous)
+  std::vector<hipEvent_t> ev;              // timed runs: 2 per layer
   hipStream_t gstream = nullptr;           // stream the captured graph replays on
   hipGraphExec_t gexec = nullptr;
   hipGraph_t graph = nullptr;
@@ -296,11 +296,6 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
 }
 
 // ------------------------------------------------------------------ profiling
-static int64_t median_ns(std::vector<float>& ms) {
-  std::sort(ms.begin(), ms.end());
-  return (int64_t)std::llround((double)ms[ms.size() / 2] * 1e6);
-}
-
 void dev_profile(Graph& g, int warmup, int reps, void* stream) {
   HIPCHK(hipSetDevice(g.device));
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -314,7 +309,7 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
   }
   tmax = align256(tmax);
   void *in0 = nullptr, *in1 = nullptr, *outb = nullptr, *ws = nullptr;
-  std::vector<hipEvent_t> ev(2 * reps, nullptr);
+  std::vector<hipEvent_t> ev(2, nullptr);
   auto cleanup = [&]() {
     for (auto e : ev)
       if (e) (void)hipEventDestroy(e);
@@ -326,22 +321,29 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
     HIPCHK(hipMalloc(&in1, tmax));
     HIPCHK(hipMalloc(&outb, tmax));
     if (wsmax) HIPCHK(hipMalloc(&ws, wsmax));
-    for (auto& e : ev) HIPCHK(hipEventCreate(&e));
+    for (auto& e : ev) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
     k::fill_random(g.dtype, in0, tmax / es, (uint64_t)g.opt_seed, st);
     k::fill_random(g.dtype, in1, tmax / es, (uint64_t)g.opt_seed + 7, st);
     HIPCHK(hipGetLastError());
+    struct Clear {
+      ~Clear() { k::g_timing = k::LaunchTiming{}; }
+    } clear_on_exit;
+    // a routine's cost is the mean time of reps back-to-back runs: events
+    // are tied to the start of the first run's first kernel and to the end
+    // of the last run's last kernel, so host launch latency and the events'
+    // own dispatch gaps are amortised over the block
     auto time_it = [&](auto&& launch) -> int64_t {
       for (int i = 0; i < warmup; ++i) launch();
       for (int i = 0; i < reps; ++i) {
-        HIPCHK(hipEventRecord(ev[2 * i], st));
+        k::g_timing = k::LaunchTiming{i == 0 ? ev[0] : nullptr, i == reps - 1 ? ev[1] : nullptr};
         launch();
-        HIPCHK(hipEventRecord(ev[2 * i + 1], st));
+        k::g_timing = k::LaunchTiming{};
       }
       HIPCHK(hipGetLastError());
-      HIPCHK(hipEventSynchronize(ev[2 * reps - 1]));
-      std::vector<float> ms(reps);
-      for (int i = 0; i < reps; ++i) HIPCHK(hipEventElapsedTime(&ms[i], ev[2 * i], ev[2 * i + 1]));
-      return median_ns(ms);
+      HIPCHK(hipEventSynchronize(ev[1]));
+      float ms = 0.f;
+      HIPCHK(hipEventElapsedTime(&ms, ev[0], ev[1]));
+      return (int64_t)std::llround((double)ms * 1e6 / reps);
     };
     for (int i = 1; i < g.n_layers(); ++i) {
       Layer& L = g.layers[i];
@@ -427,9 +429,9 @@ void plan_compile(Graph& g) {
   P->last_step.assign(n, -1);
   auto push = [&](Step s, std::vector<int> uses) {
     int idx = (int)P->steps.size();
-    for (int b : uses) bufs[b].last = std::max(bufs[b].last, idx);
     if (P->first_step[s.layer] < 0) P->first_step[s.layer] = idx;
     P->last_step[s.layer] = idx;
+    for (int b : uses) bufs[b].last = std::max(bufs[b].last, idx);
     P->steps.push_back(s);
     step_bufs.push_back(uses);
   };
@@ -539,50 +541,74 @@ void plan_compile(Graph& g) {
   P->arena_bytes = std::max<size_t>(total, 256);
   HIPCHK(hipMalloc(&P->arena, P->arena_bytes));
   P->ev.resize(2 * n, nullptr);
-  for (auto& e : P->ev) HIPCHK(hipEventCreate(&e));
+  for (auto& e : P->ev) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
   g.plan = std::move(P);
 }
 
-static void enqueue_steps(const Graph& g, const Plan& P, const void* d_in, void* d_out,
-                          hipStream_t st, bool timed) {
+static void enqueue_step(const Graph& g, const Plan& P, const Step& s, const void* d_in,
+                         void* d_out, hipStream_t st) {
   char* base = static_cast<char*>(P.arena);
   auto ptr = [&](const BufRef& r) -> void* {
     if (r.kind == 1) return const_cast<void*>(d_in);
     if (r.kind == 2) return d_out;
     return base + r.off;
   };
-  for (size_t si = 0; si < P.steps.size(); ++si) {
-    const Step& s = P.steps[si];
-    if (timed && P.first_step[s.layer] == (int)si) HIPCHK(hipEventRecord(P.ev[2 * s.layer], st));
-    if (s.type == 0) {
-      k::convert(g.dtype, ptr(s.src), s.sd, ptr(s.dst), s.dd, st);
-    } else {
-      const Routine& r = g.layers[s.layer].routines[g.path[s.layer]];
-      const void* ins[2] = {ptr(s.in[0]), s.n_in > 1 ? ptr(s.in[1]) : nullptr};
-      launch_layer(g, s.layer, r, ins, s.ind, ptr(s.out), s.outd, s.ws_bytes ? ptr(s.ws) : nullptr,
-                   s.ws_bytes, st);
-    }
-    if (timed && P.last_step[s.layer] == (int)si) HIPCHK(hipEventRecord(P.ev[2 * s.layer + 1], st));
+  if (s.type == 0) {
+    k::convert(g.dtype, ptr(s.src), s.sd, ptr(s.dst), s.dd, st);
+  } else {
+    const Routine& r = g.layers[s.layer].routines[g.path[s.layer]];
+    const void* ins[2] = {ptr(s.in[0]), s.n_in > 1 ? ptr(s.in[1]) : nullptr};
+    launch_layer(g, s.layer, r, ins, s.ind, ptr(s.out), s.outd, s.ws_bytes ? ptr(s.ws) : nullptr,
+                 s.ws_bytes, st);
   }
+}
+
+static void enqueue_steps(const Graph& g, const Plan& P, const void* d_in, void* d_out,
+                          hipStream_t st) {
+  for (const Step& s : P.steps) enqueue_step(g, P, s, d_in, d_out, st);
   HIPCHK(hipGetLastError());
 }
 
-void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms) {
+// Timed run: each layer's steps (converters feeding it, then its routine) are
+// enqueued reps times back to back, with events tied to the start of the
+// first repetition's first kernel and the end of the last repetition's last
+// kernel.  Every step writes buffers distinct from the ones it reads, so a
+// repetition recomputes the same values and the run's result is unchanged.
+static void enqueue_timed(const Graph& g, const Plan& P, const void* d_in, void* d_out,
+                          hipStream_t st, int reps) {
+  struct Clear {
+    ~Clear() { k::g_timing = k::LaunchTiming{}; }
+  } clear_on_exit;
+  for (int i = 1; i < g.n_layers(); ++i) {
+    const int a = P.first_step[i], b = P.last_step[i];
+    for (int rep = 0; rep < reps; ++rep)
+      for (int si = a; si <= b; ++si) {
+        k::g_timing = k::LaunchTiming{rep == 0 && si == a ? P.ev[2 * i] : nullptr,
+                                      rep == reps - 1 && si == b ? P.ev[2 * i + 1] : nullptr};
+        enqueue_step(g, P, P.steps[si], d_in, d_out, st);
+      }
+  }
+  k::g_timing = k::LaunchTiming{};
+  HIPCHK(hipGetLastError());
+}
+
+void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms, int reps) {
   if (!g.plan) fail(SN_E_STATE, "no execution plan");
   HIPCHK(hipSetDevice(g.device));
   Plan& P = *g.plan;
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (layer_ms) {
-    enqueue_steps(g, P, d_in, d_out, st, true);
+    enqueue_timed(g, P, d_in, d_out, st, reps);
     HIPCHK(hipStreamSynchronize(st));
-    for (int i = 0; i < g.n_layers(); ++i) {
-      layer_ms[i] = 0.f;
-      if (P.first_step[i] >= 0) HIPCHK(hipEventElapsedTime(&layer_ms[i], P.ev[2 * i], P.ev[2 * i + 1]));
+    layer_ms[0] = 0.f;
+    for (int i = 1; i < g.n_layers(); ++i) {
+      HIPCHK(hipEventElapsedTime(&layer_ms[i], P.ev[2 * i], P.ev[2 * i + 1]));
+      layer_ms[i] /= (float)reps;
     }
     return;
   }
   if (!g.opt_hipgraph) {
-    enqueue_steps(g, P, d_in, d_out, st, false);
+    enqueue_steps(g, P, d_in, d_out, st);
     return;
   }
   // replay a captured graph on the plan's stream, ordered after/before the caller's stream
@@ -598,7 +624,7 @@ void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* laye
     P.graph = nullptr;
     HIPCHK(hipStreamBeginCapture(P.gstream, hipStreamCaptureModeThreadLocal));
     try {
-      enqueue_steps(g, P, d_in, d_out, P.gstream, false);
+      enqueue_steps(g, P, d_in, d_out, P.gstream);
     } catch (...) {
       hipGraph_t tmp = nullptr;
       (void)hipStreamEndCapture(P.gstream, &tmp);

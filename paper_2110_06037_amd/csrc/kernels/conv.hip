@@ -602,9 +602,9 @@ static void igemm_go(const IgArgs& a, int batch, hipStream_t st) {
         "tensor too large for 32-bit buffer offsets");
   dim3 grid(a.tiles_m * a.tiles_n, a.splits, batch);
   if (VEC && a.CB % (BK / 8) == 0 && a.R * a.S <= 32)
-    hipLaunchKernelGGL((igemm_kernel<T, L, VEC, VEC, BM, BN, BK, EPI, PF>), grid, dim3(256), 0, st, a);
+    SN_LAUNCH((igemm_kernel<T, L, VEC, VEC, BM, BN, BK, EPI, PF>), grid, dim3(256), 0, st, a);
   else
-    hipLaunchKernelGGL((igemm_kernel<T, L, VEC, false, BM, BN, BK, EPI, PF>), grid, dim3(256), 0, st, a);
+    SN_LAUNCH((igemm_kernel<T, L, VEC, false, BM, BN, BK, EPI, PF>), grid, dim3(256), 0, st, a);
 }
 
 template <typename T, int L, bool VEC, int EPI>
@@ -710,7 +710,7 @@ static void igemm_run(const IgCfg& cfg, IgArgs& a, const ConvArgs& c, hipStream_
     a.part = reinterpret_cast<float*>(c.ws);
     igemm_cfg<T, L, VEC, EPI_SPLIT>(cfg, a, 1, st);
     const long long n = L == NCHW ? (long long)a.M * a.Ng : (long long)a.M * ((a.Ng + 7) / 8);
-    hipLaunchKernelGGL((splitk_reduce_kernel<T, L>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a);
+    SN_LAUNCH((splitk_reduce_kernel<T, L>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a);
   } else {
     igemm_cfg<T, L, VEC, EPI_LAYOUT>(cfg, a, 1, st);
   }
@@ -839,9 +839,9 @@ static void direct_dispatch(const ConvArgs& c, hipStream_t st) {
   check(c.xd.layout == c.yd.layout, "direct convolution reads and writes one layout");
   dim3 grid((a.M + 255) / 256, (a.Ng + 7) / 8);
   switch (c.xd.layout) {
-    case NCHW: hipLaunchKernelGGL((direct_kernel<T, NCHW>), grid, dim3(256), 0, st, a); break;
-    case NHWC: hipLaunchKernelGGL((direct_kernel<T, NHWC>), grid, dim3(256), 0, st, a); break;
-    case NC8: hipLaunchKernelGGL((direct_kernel<T, NC8>), grid, dim3(256), 0, st, a); break;
+    case NCHW: SN_LAUNCH((direct_kernel<T, NCHW>), grid, dim3(256), 0, st, a); break;
+    case NHWC: SN_LAUNCH((direct_kernel<T, NHWC>), grid, dim3(256), 0, st, a); break;
+    case NC8: SN_LAUNCH((direct_kernel<T, NC8>), grid, dim3(256), 0, st, a); break;
   }
 }
 
@@ -1096,15 +1096,15 @@ static void wino_dispatch(int dtype, const ConvArgs& c, hipStream_t st) {
                    : (a.T >= 4096 && a.Ng >= 128 ? IgCfg{128, 64, 64, 0, 4} : IgCfg{64, 64, 64, 0, 4});
   ig_decompose(g, gc);
   switch (c.xd.layout) {
-    case NCHW: hipLaunchKernelGGL((wino_in_kernel<T, NCHW>), gin, dim3(256), 0, st, a); break;
-    case NHWC: hipLaunchKernelGGL((wino_in_kernel<T, NHWC>), gin, dim3(256), 0, st, a); break;
-    case NC8: hipLaunchKernelGGL((wino_in_kernel<T, NC8>), gin, dim3(256), 0, st, a); break;
+    case NCHW: SN_LAUNCH((wino_in_kernel<T, NCHW>), gin, dim3(256), 0, st, a); break;
+    case NHWC: SN_LAUNCH((wino_in_kernel<T, NHWC>), gin, dim3(256), 0, st, a); break;
+    case NC8: SN_LAUNCH((wino_in_kernel<T, NC8>), gin, dim3(256), 0, st, a); break;
   }
   igemm_cfg<T, NHWC, true, EPI_RAW>(gc, g, 16, st);
   switch (c.xd.layout) {
-    case NCHW: hipLaunchKernelGGL((wino_out_kernel<T, NCHW>), gout, dim3(256), 0, st, a); break;
-    case NHWC: hipLaunchKernelGGL((wino_out_kernel<T, NHWC>), gout, dim3(256), 0, st, a); break;
-    case NC8: hipLaunchKernelGGL((wino_out_kernel<T, NC8>), gout, dim3(256), 0, st, a); break;
+    case NCHW: SN_LAUNCH((wino_out_kernel<T, NCHW>), gout, dim3(256), 0, st, a); break;
+    case NHWC: SN_LAUNCH((wino_out_kernel<T, NHWC>), gout, dim3(256), 0, st, a); break;
+    case NC8: SN_LAUNCH((wino_out_kernel<T, NC8>), gout, dim3(256), 0, st, a); break;
   }
 }
 
@@ -1236,9 +1236,9 @@ static void dw_dispatch(const ConvArgs& c, hipStream_t st) {
                                         : (long long)a.N * a.P * a.Q * (a.C8 / 8);
   dim3 grid((unsigned)((total + 255) / 256));
   switch (c.xd.layout) {
-    case NCHW: hipLaunchKernelGGL((dw_kernel<T, NCHW>), grid, dim3(256), 0, st, a); break;
-    case NHWC: hipLaunchKernelGGL((dw_kernel<T, NHWC>), grid, dim3(256), 0, st, a); break;
-    case NC8: hipLaunchKernelGGL((dw_kernel<T, NC8>), grid, dim3(256), 0, st, a); break;
+    case NCHW: SN_LAUNCH((dw_kernel<T, NCHW>), grid, dim3(256), 0, st, a); break;
+    case NHWC: SN_LAUNCH((dw_kernel<T, NHWC>), grid, dim3(256), 0, st, a); break;
+    case NC8: SN_LAUNCH((dw_kernel<T, NC8>), grid, dim3(256), 0, st, a); break;
   }
 }
 

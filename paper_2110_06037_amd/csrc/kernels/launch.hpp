@@ -4,11 +4,34 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stddef.h>
 #include <stdint.h>
 
 namespace sn {
 namespace k {
+
+// Kernel-execution timing.  While `start` or `stop` is set, launches go
+// through hipExtLaunchKernelGGL with these events, which the runtime ties to
+// the kernel dispatches themselves: `start` to the start of the next launch
+// (then cleared), `stop` to the end of every launch while it stays set.
+// Each such event adds a dispatch gap of a few microseconds, so timers set
+// them only at the first and last launch of a long back-to-back sequence.
+struct LaunchTiming {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local LaunchTiming g_timing;
+
+#define SN_LAUNCH(K, G, B, S, ST, ...)                                                  \
+  do {                                                                                  \
+    if (::sn::k::g_timing.start || ::sn::k::g_timing.stop) {                            \
+      hipExtLaunchKernelGGL(K, G, B, S, ST, ::sn::k::g_timing.start, ::sn::k::g_timing.stop, 0, \
+                            __VA_ARGS__);                                               \
+      ::sn::k::g_timing.start = nullptr;                                                \
+    } else {                                                                            \
+      hipLaunchKernelGGL(K, G, B, S, ST, __VA_ARGS__);                                  \
+    }                                                                                   \
+  } while (0)
 
 // Logical tensor N x C x H x W stored in `layout` with `cs` stored channels.
 struct TDesc {

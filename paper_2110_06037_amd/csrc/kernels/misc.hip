@@ -11,6 +11,8 @@
 namespace sn {
 namespace k {
 
+thread_local LaunchTiming g_timing;
+
 static void check(bool ok, const char* what) {
   if (!ok) throw std::invalid_argument(std::string("kernel launch: ") + what);
 }
@@ -104,7 +106,7 @@ static void maxpool_t(const void* x, const TDesc& xd, void* y, const TDesc& yd, 
   const T* xp = reinterpret_cast<const T*>(x);
   T* yp = reinterpret_cast<T*>(y);
 #define MP(LL)                                                                                   \
-  hipLaunchKernelGGL((maxpool_kernel<T, LL>), dim3(blocks(total)), dim3(256), 0, s, xp, yp, xd.n, \
+  SN_LAUNCH((maxpool_kernel<T, LL>), dim3(blocks(total)), dim3(256), 0, s, xp, yp, xd.n, \
                      xd.c, xd.h, xd.w, xd.cs, yd.h, yd.w, k, st, pad)
   switch (xd.layout) {
     case NCHW: MP(NCHW); break;
@@ -162,15 +164,15 @@ static void gap_t(const void* x, const TDesc& xd, void* y, const TDesc& yd, hipS
   T* yp = reinterpret_cast<T*>(y);
   switch (xd.layout) {
     case NCHW:
-      hipLaunchKernelGGL((gap_kernel<T, NCHW>), dim3(blocks((long long)xd.n * xd.c, 4)), dim3(256), 0, s,
+      SN_LAUNCH((gap_kernel<T, NCHW>), dim3(blocks((long long)xd.n * xd.c, 4)), dim3(256), 0, s,
                          xp, yp, xd.n, xd.c, HW, xd.cs);
       break;
     case NHWC:
-      hipLaunchKernelGGL((gap_kernel<T, NHWC>), dim3(blocks((long long)xd.n * xd.cs)), dim3(256), 0, s,
+      SN_LAUNCH((gap_kernel<T, NHWC>), dim3(blocks((long long)xd.n * xd.cs)), dim3(256), 0, s,
                          xp, yp, xd.n, xd.c, HW, xd.cs);
       break;
     case NC8:
-      hipLaunchKernelGGL((gap_kernel<T, NC8>), dim3(blocks((long long)xd.n * xd.cs)), dim3(256), 0, s,
+      SN_LAUNCH((gap_kernel<T, NC8>), dim3(blocks((long long)xd.n * xd.cs)), dim3(256), 0, s,
                          xp, yp, xd.n, xd.c, HW, xd.cs);
       break;
   }
@@ -202,11 +204,11 @@ __global__ __launch_bounds__(256) void add_kernel(const T* __restrict__ a, const
 void add_act(int dtype, const void* a, const void* b, void* y, int64_t n, int act, hipStream_t s) {
   dim3 g(blocks((n + 7) / 8));
   if (dtype == 0)
-    hipLaunchKernelGGL(add_kernel<float>, g, dim3(256), 0, s, (const float*)a, (const float*)b, (float*)y, (long long)n, act);
+    SN_LAUNCH(add_kernel<float>, g, dim3(256), 0, s, (const float*)a, (const float*)b, (float*)y, (long long)n, act);
   else if (dtype == 1)
-    hipLaunchKernelGGL(add_kernel<f16>, g, dim3(256), 0, s, (const f16*)a, (const f16*)b, (f16*)y, (long long)n, act);
+    SN_LAUNCH(add_kernel<f16>, g, dim3(256), 0, s, (const f16*)a, (const f16*)b, (f16*)y, (long long)n, act);
   else
-    hipLaunchKernelGGL(add_kernel<bf16>, g, dim3(256), 0, s, (const bf16*)a, (const bf16*)b, (bf16*)y, (long long)n, act);
+    SN_LAUNCH(add_kernel<bf16>, g, dim3(256), 0, s, (const bf16*)a, (const bf16*)b, (bf16*)y, (long long)n, act);
 }
 
 // ------------------------------------------------------------------ FC (dot products)
@@ -257,11 +259,11 @@ void fc_direct(int dtype, const void* x, int n, int cin, int cin_s, const void* 
   check(kout_s >= kout && c8 >= cin, "fc shapes");
   dim3 g(blocks(kout_s, 4));
   if (dtype == 0)
-    hipLaunchKernelGGL(fc_kernel<float>, g, dim3(256), 0, s, (const float*)x, n, cin, cin_s, (const float*)w, c8, bias, (float*)y, kout_s);
+    SN_LAUNCH(fc_kernel<float>, g, dim3(256), 0, s, (const float*)x, n, cin, cin_s, (const float*)w, c8, bias, (float*)y, kout_s);
   else if (dtype == 1)
-    hipLaunchKernelGGL(fc_kernel<f16>, g, dim3(256), 0, s, (const f16*)x, n, cin, cin_s, (const f16*)w, c8, bias, (f16*)y, kout_s);
+    SN_LAUNCH(fc_kernel<f16>, g, dim3(256), 0, s, (const f16*)x, n, cin, cin_s, (const f16*)w, c8, bias, (f16*)y, kout_s);
   else
-    hipLaunchKernelGGL(fc_kernel<bf16>, g, dim3(256), 0, s, (const bf16*)x, n, cin, cin_s, (const bf16*)w, c8, bias, (bf16*)y, kout_s);
+    SN_LAUNCH(fc_kernel<bf16>, g, dim3(256), 0, s, (const bf16*)x, n, cin, cin_s, (const bf16*)w, c8, bias, (bf16*)y, kout_s);
 }
 
 // ------------------------------------------------------------------ layout converters
@@ -341,15 +343,15 @@ static void convert_e(const void* xv, const TDesc& xd, void* yv, const TDesc& yd
     dim3 g((HW + 63) / 64, (xd.c + 63) / 64, xd.n);
     check(xd.n <= 65535, "batch too large for the transpose grid");
     if (yd.layout == NHWC)
-      hipLaunchKernelGGL((transpose_kernel<E, true>), g, dim3(256), 0, s, x, y, xd.c, HW);
+      SN_LAUNCH((transpose_kernel<E, true>), g, dim3(256), 0, s, x, y, xd.c, HW);
     else
-      hipLaunchKernelGGL((transpose_kernel<E, false>), g, dim3(256), 0, s, x, y, xd.c, HW);
+      SN_LAUNCH((transpose_kernel<E, false>), g, dim3(256), 0, s, x, y, xd.c, HW);
     return;
   }
   const long long total = (long long)yd.n * yd.cs * yd.h * yd.w;
   dim3 g(blocks(total));
 #define CV(A, B)                                                                              \
-  hipLaunchKernelGGL((convert_kernel<E, A, B>), g, dim3(256), 0, s, x, y, xd.n, xd.c, xd.h, xd.w, \
+  SN_LAUNCH((convert_kernel<E, A, B>), g, dim3(256), 0, s, x, y, xd.n, xd.c, xd.h, xd.w, \
                      xd.cs, yd.cs)
   const int key = xd.layout * 3 + yd.layout;
   switch (key) {
@@ -387,9 +389,9 @@ __global__ __launch_bounds__(256) void fill_kernel(T* __restrict__ p, long long 
 
 void fill_random(int dtype, void* p, int64_t n, uint64_t seed, hipStream_t s) {
   dim3 g(blocks(n));
-  if (dtype == 0) hipLaunchKernelGGL(fill_kernel<float>, g, dim3(256), 0, s, (float*)p, (long long)n, (unsigned long long)seed);
-  else if (dtype == 1) hipLaunchKernelGGL(fill_kernel<f16>, g, dim3(256), 0, s, (f16*)p, (long long)n, (unsigned long long)seed);
-  else hipLaunchKernelGGL(fill_kernel<bf16>, g, dim3(256), 0, s, (bf16*)p, (long long)n, (unsigned long long)seed);
+  if (dtype == 0) SN_LAUNCH(fill_kernel<float>, g, dim3(256), 0, s, (float*)p, (long long)n, (unsigned long long)seed);
+  else if (dtype == 1) SN_LAUNCH(fill_kernel<f16>, g, dim3(256), 0, s, (f16*)p, (long long)n, (unsigned long long)seed);
+  else SN_LAUNCH(fill_kernel<bf16>, g, dim3(256), 0, s, (bf16*)p, (long long)n, (unsigned long long)seed);
 }
 
 }  // namespace k

@@ -208,14 +208,16 @@ class Graph:
                                 ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)))
         return out
 
-    def run_timed(self, x, out=None, stream=None):
-        """Synchronous run; returns (out, per-layer milliseconds)."""
+    def run_timed(self, x, out=None, stream=None, reps=1):
+        """Synchronous run with every layer's launches repeated ``reps`` times
+        back to back; returns (out, per-layer milliseconds per repetition)."""
         if out is None:
             out = self.empty_output()
         n = self.num_layers()
         ms = (ctypes.c_float * n)()
         N.check(self.lib.sn_run_timed(self._g, ctypes.c_void_p(x.data_ptr()),
-                                      ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream), ms, n))
+                                      ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream),
+                                      int(reps), ms, n))
         return out, list(ms)
 
 

@@ -54,8 +54,12 @@ def test_tiny_chain_measured_table_dp_equals_exhaustive_and_parity():
     tt, tup, count = exhaustive(problem_from_costs(costs))
     assert tuple(ids) + (0,) == tup and total == tt
     ref = oracle_out(spec, t)
-    out, _ = run_out(g, spec, t)
+    out, xd = run_out(g, spec, t)
     assert err(out, ref, "f32") <= TOL["f32"]
+    # the timed run repeats every layer's launches; its result is the same bits
+    y, ms = g.run_timed(xd, reps=3)
+    assert np.array_equal(from_dev(y, "f32").reshape(spec["batch"], -1), out)
+    assert ms[0] == 0 and all(m > 0 for m in ms[1:]), ms
     for lay in ("NCHW", "NHWC"):
         for algo in ("direct", "igemm"):
             g.select("fixed", lay, algo)
