@@ -122,6 +122,57 @@ def summarize_pmc(fetch_dir, write_dir, routine, ksub, out, calib_mib):
     print(json.dumps(t))
 
 
+def _nets():
+    from workloads import mobilenet_v2, resnet18, resnet50
+    return {"resnet50": resnet50, "resnet18": resnet18, "mobilenetv2": mobilenet_v2}
+
+
+NETS = {"resnet50": None, "resnet18": None, "mobilenetv2": None}
+
+
+def sweep(args):
+    """Cost table of the 3x3 stride-1 sweep (C = K in 64..512 at 56..7 pixels, batch 32):
+    every routine of the conv layer and every converter of its input, as profiled."""
+    from paper_2110_06037_amd import build_from_spec
+    from workloads import CONV_SWEEP_SHAPES, conv_sweep, generate
+    dt = args.dtype
+    out = []
+    for c, hw in CONV_SWEEP_SHAPES:
+        spec = conv_sweep(c, hw, args.batch, dt)
+        g = build_from_spec(spec, generate(spec), device=0)
+        g.profile(warmup=5, reps=args.profile_reps)
+        costs = g.costs()
+        flops = 2 * args.batch * c * c * 9 * hw * hw
+        tiles = args.batch * ((hw + 1) // 2) ** 2
+        es = 4 if dt == "f32" else 2
+        mbytes = es * 2 * args.batch * c * hw * hw + es * c * c * 9 + 4 * c
+        rows = []
+        for r in costs["layers"][1]["routines"]:
+            if r["ns"] is None or r["ns"] < 0:
+                continue
+            f = 2 * 16 * c * c * tiles if "winograd" in r["name"] else flops
+            tfl = f / (r["ns"] * 1e-9) / 1e12
+            rows.append({"routine": r["name"], "us": round(r["ns"] / 1e3, 2),
+                         "tflops": round(tfl, 1),
+                         "mfma_frac": round(tfl / PEAK_MFMA_TFLOPS[dt], 4) if "direct" not in r["name"] else None,
+                         "gbs": round(mbytes / (r["ns"] * 1e-9) / 1e9, 1)})
+        cvt = {}
+        e = next(e for e in costs["edges"] if e["from"] == 0)   # the conv's input tensor
+        for a, row in enumerate(e["ns"]):
+            for b, v in enumerate(row):
+                if a != b and v > 0:
+                    cvt[f"{LAYOUTS[a]}>{LAYOUTS[b]}"] = {
+                        "us": round(v / 1e3, 2),
+                        "gbs": round(2 * es * args.batch * c * hw * hw / (v * 1e-9) / 1e9, 1)}
+        best = min(rows, key=lambda r: r["us"])
+        out.append({"shape": f"C=K={c} HxW={hw}x{hw} bs{args.batch} {dt}", "gflop": round(flops / 1e9, 2),
+                    "best": best["routine"], "routines": rows, "converters": cvt})
+        log(f"[sweep] {out[-1]['shape']}: best {best['routine']} {best['us']} us "
+            f"({best['tflops']} TFLOP/s)")
+        g.close()
+    print(json.dumps({"sweep": out}), flush=True)
+
+
 def time_steps(g, x, out, steps, warmup):
     import torch
     for _ in range(warmup):
@@ -168,6 +219,10 @@ def main():
     ap.add_argument("--profile-reps", type=int, default=20)
     ap.add_argument("--timing-reps", type=int, default=50,
                     help="back-to-back repetitions per layer in the per-layer timing pass")
+    ap.add_argument("--net", default="resnet50", choices=sorted(NETS),
+                    help="workload (the headline line is resnet50 at batch 32)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="print the measured cost table of the four 3x3 sweep shapes and exit")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-path sweep")
     ap.add_argument("--no-bs1", action="store_true", help="skip the batch-1 measurement")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -193,13 +248,16 @@ def main():
               "batch with no exchange, see DESIGN.md", file=sys.stderr)
         sys.exit(2)
 
+    if args.sweep:
+        sweep(args)
+        return
+
     import numpy as np
     import torch
     from paper_2110_06037_amd import build_from_spec, native as N, to_device as to_dev
     from workloads import generate, resnet50
 
-    dev = torch.device("cuda:0")
-    spec = resnet50(args.batch, args.dtype)
+    spec = _nets()[args.net](args.batch, args.dtype)
     t = generate(spec)
     log(f"[bench] {spec['name']}: building graph")
     g = build_from_spec(spec, t, device=0)
@@ -265,7 +323,8 @@ def main():
         ach = dom["bytes"] / dom["launches"] / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = traffic_for(dom_key)
+    roof["traffic"] = (traffic_for(dom_key)
+                       if (args.net, args.batch, args.dtype) == ("resnet50", 32, "bf16") else None)
     roof["kernel"] = (f"routine {dom_key} ({dom['launches']} launches/step on "
                       f"{'/'.join(sorted(dom['cats']))} layers)")
     roof["avg_launch_us"] = round(avg_s * 1e6, 2)
@@ -295,7 +354,7 @@ def main():
     dp_vs_fixed = round(value / fixed[best_fixed], 4) if best_fixed else None
 
     bs1 = None
-    if not args.no_bs1:
+    if not args.no_bs1 and args.net == "resnet50":
         spec1 = resnet50(1, args.dtype)
         t1_ = generate(spec1)
         g1 = build_from_spec(spec1, t1_, device=0)
@@ -317,7 +376,7 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sec * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": args.dtype,
         "data": "synthetic (seeded random input and He-normal weights)",
-        "config": {"workload": f"resnet50-shaped CNN, batch {args.batch}, {args.dtype}, 224x224",
+        "config": {"workload": f"{args.net}-shaped CNN, batch {args.batch}, {args.dtype}, 224x224",
                    "batch": args.batch, "path": "DPRS-selected routines"},
         "roofline": roof,
         "cpu_baseline": cpu,

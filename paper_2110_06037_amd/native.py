@@ -86,6 +86,10 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: run paper_2110_06037_amd/build.py "
                               "(or __graft_entry__.build()) first")
+        # torch (device memory and streams) must load its HIP runtime first:
+        # loaded after the library it would bind to the runtime the library
+        # pulled in and find no GPU; loaded before, both share one device view
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in SIGNATURES.items():
             f = getattr(L, name)
