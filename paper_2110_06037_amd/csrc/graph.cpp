@@ -87,7 +87,9 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
         if (g.opt_algos >> SN_ALGO_IGEMM & 1) {
           int np = g.opt_params ? k::igemm_num_params(g.dtype) : 1;
           for (int p = 0; p < np; ++p)
-            if (k::igemm_param_valid(g.dtype, p, lay, in.c)) add(lay, SN_ALGO_IGEMM, p);
+            if (k::igemm_param_valid(g.dtype, p, lay, in.n, in.c, in.h, in.w, L.d.r, L.d.s, L.d.stride,
+                                     L.d.pad))
+              add(lay, SN_ALGO_IGEMM, p);
         }
         if ((g.opt_algos >> SN_ALGO_WINOGRAD & 1) && winograd_applicable(L, in))
           add(lay, SN_ALGO_WINOGRAD, 0);

@@ -13,43 +13,12 @@
 #include <stdexcept>
 #include <string>
 
+#include "gemm_common.hpp"
 #include "kcommon.hpp"
 #include "launch.hpp"
 
 namespace sn {
 namespace k {
-
-static void check(bool ok, const char* what) {
-  if (!ok) throw std::invalid_argument(std::string("kernel launch: ") + what);
-}
-
-// ------------------------------------------------------------------ MFMA
-template <typename T>
-struct Mfma;
-template <>
-struct Mfma<bf16> {
-  static constexpr int KSTEP = 32;  // reduction elements per instruction
-  typedef bf16x8 frag;
-  static __device__ __forceinline__ f32x4 run(frag a, frag b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-  }
-};
-template <>
-struct Mfma<f16> {
-  static constexpr int KSTEP = 32;
-  typedef f16x8 frag;
-  static __device__ __forceinline__ f32x4 run(frag a, frag b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-  }
-};
-template <>
-struct Mfma<float> {
-  static constexpr int KSTEP = 4;
-  typedef float frag;
-  static __device__ __forceinline__ f32x4 run(frag a, frag b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-  }
-};
 
 // ------------------------------------------------------------------ implicit GEMM
 // GEMM view: rows m = (n, p, q) output pixels, columns = output channels,
@@ -79,13 +48,6 @@ struct IgArgs {
   long long x_elems, w_elems;  // elements addressable per blockIdx.z (buffer ranges)
 };
 
-// Raw buffer access: an SGPR resource (base, byte range) plus a 32-bit
-// offset; loads at offsets beyond the range return zero, which implements
-// the zero padding and the ragged tile edges without branches.
-constexpr unsigned kOOB = 0x80000000u;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, long long bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
-}
 template <typename T>
 __device__ __forceinline__ V8<T> bload8(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
   V8<T> out;
@@ -118,42 +80,11 @@ __device__ __forceinline__ void chunk_adv(ChunkPos& p, int step, int CB, int S) 
   }
 }
 
-// epilogue modes
-constexpr int EPI_LAYOUT = 0;  // bias + activation, store in the tensor layout
-constexpr int EPI_RAW = 1;     // raw float32 [M][Ng] (Winograd tile GEMMs)
-constexpr int EPI_SPLIT = 2;   // raw float32 partial tile of one reduction split
-
-// Map the linear workgroup id to (m-tile, n-tile): consecutive ids are
-// dispatched round-robin over the 8 XCDs, so first regroup them into one
-// contiguous range per XCD, then walk groups of 8 m-tiles across all
-// n-tiles (tiles of a group share A rows in that XCD's L2).
-__device__ __forceinline__ void tile_of(int pid, int tiles_m, int tiles_n, int& mt, int& nt) {
-  const int nb = tiles_m * tiles_n;
-  const int q = nb >> 3, r = nb & 7;
-  const int xcd = pid & 7, slot = pid >> 3;
-  const int v = xcd * q + min(xcd, r) + slot;
-  constexpr int GM = 8;
-  const int group = v / (GM * tiles_n);
-  const int first = group * GM;
-  const int gsize = min(tiles_m - first, GM);
-  const int in = v - group * GM * tiles_n;
-  mt = first + in % gsize;
-  nt = in / gsize;
-}
-
 // Read-only zero page: masked-off lanes load from here, so every global load
 // is unconditional (no divergent branches around loads, which would force
 // the compiler to drain all outstanding loads).
 __device__ __attribute__((aligned(256))) unsigned char g_zero_page[256];
 
-// Workgroup barrier for the LDS pipeline: waits only for this wave's LDS
-// operations (the tile stores), not for its in-flight global loads, which
-// target registers and belong to the next step.  (__syncthreads() also
-// drains all global loads, which would serialise the prefetch.)  The memory
-// clobber keeps the compiler from moving LDS accesses across it.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
 
 template <typename T, int L, bool VEC, bool ALIGNED, int BM, int BN, int BK, int EPI, int PF>
 __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
@@ -186,7 +117,8 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
   T(*Bs)[BN][LDK] = reinterpret_cast<T(*)[BN][LDK]>(smem + 2 * BM * LDK * sizeof(T));
   auto slot = [](int row, int chunk) { return F32 ? chunk : chunk ^ ((row / RPR) % CPR); };
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int wm = wave >> 1, wn = wave & 1;
   int mt, nt;
   tile_of(blockIdx.x, a.tiles_m, a.tiles_n, mt, nt);
@@ -505,6 +437,227 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
   }
 }
 
+// ------------------------------------------------------------------ implicit GEMM, LDS DMA
+// The same GEMM and routine semantics as igemm_kernel, for 16-bit types in
+// the channel-vector layouts (NHWC with C % 8 == 0, NC8HW8) when the channel
+// count is a multiple of BK, so every reduction step lies inside one filter
+// tap.  The tiles travel from global memory straight into LDS: buffer loads
+// with the LDS as destination (16 bytes per lane; offsets beyond the buffer
+// range write zeros, which gives the padding halo and the ragged edges), ST
+// stages deep.  No registers stage the tiles and no LDS store instructions
+// are issued, so the vector-memory and LDS pipes carry only the tile bytes
+// and the MFMA operand reads.  One such load fills 1 KB of LDS, the 64 lanes'
+// 16 bytes in lane order; the XOR swizzle of the tile rows is therefore
+// applied on the global side: the lane that fills LDS slot (row, c) fetches
+// logical chunk c ^ swizzle(row).  Each of the 4 waves computes a
+// (BM/WM) x (BN/(4/WM)) sub-tile with the weights as the MFMA's first
+// operand (4 consecutive output channels of one pixel per lane).
+
+template <typename T, int L, int BM, int BN, int BK, int WM, int ST, int EPI>
+__global__ __launch_bounds__(256) void igemm_dma_kernel(IgArgs a) {
+  static_assert(sizeof(T) == 2 && L != NCHW, "16-bit channel-vector layouts only");
+  constexpr int WN = 4 / WM;
+  constexpr int CPR = BK / 8;       // 16-byte chunks per tile row
+  constexpr int RPB = 64 / CPR;     // tile rows filled by one load instruction (1 KB)
+  constexpr int RPR = 128 / BK;     // rows per swizzle period (one 128-byte bank range)
+  constexpr int NA = BM / RPB / 4;  // A load instructions per wave and stage
+  constexpr int NB = BN / RPB / 4;  // B load instructions per wave and stage
+  static_assert(NA * RPB * 4 == BM && NB * RPB * 4 == BN && WM * WN == 4, "tile shape");
+  static_assert(ST >= 2 && (ST - 2) * (NA + NB) <= 63, "pipeline depth");
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  constexpr int A_BYTES = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
+  constexpr int CPAD = 8;
+  constexpr int SM_C = EPI == EPI_LAYOUT ? BM * (BN + CPAD) * 2 : 0;
+  constexpr int SM = ST * STAGE > SM_C ? ST * STAGE : SM_C;
+  __shared__ __attribute__((aligned(1024))) char smem[SM];
+  auto swz = [](int row) { return (row / RPR) % CPR; };
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+  const int wm = wave / WN, wn = wave % WN;
+  int mt, nt;
+  tile_of(blockIdx.x, a.tiles_m, a.tiles_n, mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int split = blockIdx.y;
+  const int kt0 = split * a.kt_per;
+  const int KT = min(a.KC / CPR - kt0, a.kt_per);
+  const T* __restrict__ x = reinterpret_cast<const T*>(a.x);
+  const T* __restrict__ w = reinterpret_cast<const T*>(a.w);
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, a.x_elems * 2);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(w, a.w_elems * 2);
+
+  // this lane's load slots: block b = wave + 4 i fills tile rows
+  // [b * RPB, (b + 1) * RPB); the lane fills row b * RPB + lane / CPR,
+  // physical chunk lane % CPR, i.e. logical chunk (lane % CPR) ^ swz(row)
+  const int prow = lane / CPR, pch = lane % CPR;
+  unsigned rbyte[NA], tvm[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    const int row = (wave + 4 * i) * RPB + prow;
+    const int lc = pch ^ swz(row);
+    const int m = m0 + row;
+    const bool ok = m < a.M;
+    const int mm = ok ? m : 0;
+    const int img = mm / a.PQ, pq = mm - img * a.PQ;
+    const int p = pq / a.Q, q = pq - p * a.Q;
+    const int h0 = p * a.stride - a.pad, w0 = q * a.stride - a.pad;
+    int e;
+    if constexpr (L == NC8)
+      e = img * a.CB * a.H * a.W * 8 + (h0 * a.W + w0) * 8 + lc * a.H * a.W * 8;
+    else
+      e = ((img * a.H + h0) * a.W + w0) * a.Cs + lc * 8;
+    rbyte[i] = (unsigned)e * 2u;  // may wrap for the halo; valid taps add back
+    unsigned msk = 0;
+    for (int r = 0; r < a.R; ++r)
+      for (int c = 0; c < a.S; ++c)
+        if (ok && (unsigned)(h0 + r) < (unsigned)a.H && (unsigned)(w0 + c) < (unsigned)a.W)
+          msk |= 1u << (r * a.S + c);
+    tvm[i] = msk;
+  }
+  unsigned bbyte[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int row = (wave + 4 * i) * RPB + prow;
+    const int lc = pch ^ swz(row);
+    const int k = n0 + row;
+    bbyte[i] = k < a.Ng ? (unsigned)((k * a.Kred + lc * 8) * 2) : kOOB;
+  }
+
+  // reduction position of the next step to load: tap (r, s), channel block cb
+  ChunkPos upos;
+  chunk_set(upos, kt0 * CPR, a.CB, a.S);
+  auto issue = [&](int buf, int kt) {
+    char* base = smem + buf * STAGE;
+    const int t = upos.r * a.S + upos.s;
+    int tap;
+    if constexpr (L == NC8)
+      tap = upos.cb * a.H * a.W * 8 + (upos.r * a.W + upos.s) * 8;
+    else
+      tap = (upos.r * a.W + upos.s) * a.Cs + upos.cb * 8;
+    const unsigned tb = (unsigned)tap * 2u;
+#pragma unroll
+    for (int i = 0; i < NA; ++i)
+      dma16(rx, base + (wave + 4 * i) * 1024, ((tvm[i] >> t) & 1u) ? rbyte[i] + tb : kOOB, 0);
+#pragma unroll
+    for (int i = 0; i < NB; ++i) dma16(rw, base + A_BYTES + (wave + 4 * i) * 1024, bbyte[i], kt * BK * 2);
+    upos.cb += CPR;  // CB is a multiple of CPR
+    if (upos.cb == a.CB) {
+      upos.cb = 0;
+      if (++upos.s == a.S) {
+        upos.s = 0;
+        ++upos.r;
+      }
+    }
+  };
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  typedef typename Mfma<T>::frag frag;
+  auto compute = [&](int buf) {
+    const char* As = smem + buf * STAGE;
+    const char* Bs = As + A_BYTES;
+#pragma unroll
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      const int c = ks * 4 + (lane >> 4);
+      frag fa[FM], fb[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int r = wm * WTM + i * 16 + (lane & 15);
+        fa[i] = *reinterpret_cast<const frag*>(As + r * (BK * 2) + ((c ^ swz(r)) << 4));
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int r = wn * WTN + j * 16 + (lane & 15);
+        fb[j] = *reinterpret_cast<const frag*>(Bs + r * (BK * 2) + ((c ^ swz(r)) << 4));
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fb[j], fa[i], acc[i][j]);
+    }
+  };
+
+  // step t: wait for tile t (the ST-2 tiles after it may stay in flight),
+  // barrier, issue tile t+ST-1 into the buffer read at step t-1, compute t
+#pragma unroll
+  for (int u = 0; u < ST - 1; ++u)
+    if (u < KT) issue(u, kt0 + u);
+  for (int t = 0; t < KT; ++t) {
+    if (t + ST - 2 < KT)
+      wait_vmcnt<(ST - 2) * (NA + NB)>();
+    else
+      wait_vmcnt<0>();
+    dma_barrier();
+    if (t + ST - 1 < KT) issue((t + ST - 1) % ST, kt0 + t + ST - 1);
+    compute(t % ST);
+  }
+
+  // accumulator element (i, j, v) is C[wm*WTM + i*16 + (lane&15)][wn*WTN + j*16 + (lane>>4)*4 + v]
+  if constexpr (EPI == EPI_SPLIT) {
+    float* __restrict__ y = a.part + (long long)split * a.M * a.Ng;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int m = m0 + wm * WTM + i * 16 + (lane & 15);
+        const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
+        if (m < a.M) {
+          if (n + 4 <= a.Ng && (a.Ng & 3) == 0) {
+            *reinterpret_cast<f32x4*>(y + (long long)m * a.Ng + n) = acc[i][j];
+          } else {
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+              if (n + v < a.Ng) y[(long long)m * a.Ng + n + v] = acc[i][j][v];
+          }
+        }
+      }
+  } else {
+    __syncthreads();  // every wave is done with the last tile
+    T(*Cs)[BN + CPAD] = reinterpret_cast<T(*)[BN + CPAD]>(smem);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int nl = wn * WTN + j * 16 + (lane >> 4) * 4;
+      float bv[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) bv[v] = n0 + nl + v < a.Ng ? a.bias[n0 + nl + v] : 0.f;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int ml = wm * WTM + i * 16 + (lane & 15);
+        T o[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) o[v] = from_f<T>(act_f(acc[i][j][v] + bv[v], a.act));
+        __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
+      }
+    }
+    __syncthreads();
+    T* __restrict__ y = reinterpret_cast<T*>(a.y);
+    if (L == NC8 || a.Ks % 8 == 0) {
+      for (int idx = tid; idx < BM * BN / 8; idx += 256) {
+        const int row = idx / (BN / 8), cj = idx % (BN / 8);
+        const int m = m0 + row, n = n0 + cj * 8;
+        if (m >= a.M || n >= a.Ng) continue;
+        V8<T> v = ld8(&Cs[row][cj * 8]);
+        if constexpr (L == NC8) {
+          const int img = m / a.PQ, pq = m - img * a.PQ;
+          st8(y + (((long long)img * (a.Ks >> 3) + (n >> 3)) * a.PQ + pq) * 8, v);
+        } else {
+          st8(y + (long long)m * a.Ks + n, v);
+        }
+      }
+    } else {
+      for (int idx = tid; idx < BM * BN; idx += 256) {
+        const int row = idx / BN, col = idx % BN;
+        const int m = m0 + row, n = n0 + col;
+        if (m < a.M && n < a.Ng) y[(long long)m * a.Ks + n] = Cs[row][col];
+      }
+    }
+  }
+}
+
 // Sum the split-K partial tiles, add the bias, apply the activation and
 // store in the tensor layout.  One thread per (pixel, 8 output channels);
 // NCHW: one thread per (channel, pixel), pixels fastest.
@@ -554,13 +707,24 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(IgArgs a) {
 struct IgCfg {
   int bm, bn, bk, split, pf;  // split: 0 = none, 1 = split the reduction when tiles are few;
                               // pf: prefetch depth (register staging sets)
+  int dma = 0, wm = 2, st = 2;  // 1: LDS-DMA kernel, 2: 3x3 patch kernel (bm = 16 * row blocks);
+                                // wave rows WM (of 4 waves), LDS stages ST
+  int ppx = 0;                  // patch kernel: patch capacity in pixels
 };
-static const IgCfg kIg16[] = {{64, 64, 32, 0, 2},   {128, 128, 64, 0, 2}, {256, 128, 32, 0, 2},
-                              {128, 64, 64, 0, 2},  {64, 128, 64, 0, 4},  {128, 128, 64, 1, 2},
-                              {64, 64, 64, 1, 4},   {128, 64, 32, 0, 4},  {64, 128, 64, 0, 2},
-                              {96, 128, 64, 0, 2},  {64, 64, 64, 0, 4},   {128, 128, 32, 0, 4},
-                              {64, 128, 32, 0, 4},  {128, 64, 64, 0, 4},  {64, 128, 128, 0, 2},
-                              {128, 64, 128, 0, 2}, {128, 128, 128, 0, 2}};
+static const IgCfg kIg16[] = {
+    {64, 64, 32, 0, 2},   {128, 128, 64, 0, 2}, {256, 128, 32, 0, 2}, {128, 64, 64, 0, 2},
+    {64, 128, 64, 0, 4},  {128, 128, 64, 1, 2}, {64, 64, 64, 1, 4},   {128, 64, 32, 0, 4},
+    {64, 128, 64, 0, 2},  {96, 128, 64, 0, 2},  {64, 64, 64, 0, 4},   {128, 128, 32, 0, 4},
+    {64, 128, 32, 0, 4},  {128, 64, 64, 0, 4},  {64, 128, 128, 0, 2}, {128, 64, 128, 0, 2},
+    {128, 128, 128, 0, 2},
+    // LDS-DMA kernel (channel counts that are multiples of BK)
+    {128, 128, 64, 0, 0, 1, 2, 2}, {128, 128, 64, 0, 0, 1, 2, 3}, {256, 64, 64, 0, 0, 1, 4, 2},
+    {256, 64, 64, 0, 0, 1, 4, 3},  {128, 64, 64, 0, 0, 1, 2, 3},  {64, 128, 64, 0, 0, 1, 1, 3},
+    {256, 128, 64, 0, 0, 1, 2, 2}, {128, 128, 32, 0, 0, 1, 2, 3}, {64, 64, 64, 0, 0, 1, 2, 3},
+    {128, 128, 64, 1, 0, 1, 2, 3}, {128, 64, 64, 1, 0, 1, 2, 3},
+    // 3x3 stride-1 patch kernel
+    {224, 64, 32, 0, 0, 2, 2, 2, 352}, {224, 64, 32, 0, 0, 2, 2, 1, 352}, {224, 32, 32, 0, 0, 2, 4, 1, 352},
+    {112, 64, 32, 0, 0, 2, 1, 2, 256}, {112, 64, 32, 0, 0, 2, 2, 1, 256}, {112, 32, 32, 0, 0, 2, 4, 2, 256}};
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 
 int igemm_num_params(int dtype) {
@@ -569,10 +733,13 @@ int igemm_num_params(int dtype) {
 
 // A configuration whose tile rows do not divide the 256 threads needs the
 // 8-channel vector loader (NHWC with C % 8 == 0, or NC8HW8).
-bool igemm_param_valid(int dtype, int param, int layout, int c) {
+bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, int w, int r, int s,
+                       int stride, int pad) {
   if (param < 0 || param >= igemm_num_params(dtype)) return false;
   const IgCfg& g = dtype == 0 ? kIg32[param] : kIg16[param];
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
+  if (g.dma == 2) return patch_applicable(layout, c, h, w, r, s, stride, pad, n, g.bm / 16, g.bn, g.bk, g.ppx);
+  if (g.dma) return vec && ((c + 7) / 8) % (g.bk / 8) == 0 && r * s <= 32;
   return vec || 256 % g.bm == 0;
 }
 
@@ -607,8 +774,56 @@ static void igemm_go(const IgArgs& a, int batch, hipStream_t st) {
     SN_LAUNCH((igemm_kernel<T, L, VEC, false, BM, BN, BK, EPI, PF>), grid, dim3(256), 0, st, a);
 }
 
+template <typename T, int L, int BM, int BN, int BK, int WM, int ST, int EPI>
+static void igemm_dma_go(const IgArgs& a, hipStream_t st) {
+  check(a.x_elems * 2 < (long long)kOOB && a.w_elems * 2 < (long long)kOOB,
+        "tensor too large for 32-bit buffer offsets");
+  check(a.CB % (BK / 8) == 0 && a.R * a.S <= 32, "LDS-DMA tile needs C % BK == 0 and R*S <= 32");
+  dim3 grid(a.tiles_m * a.tiles_n, a.splits, 1);
+  SN_LAUNCH((igemm_dma_kernel<T, L, BM, BN, BK, WM, ST, EPI>), grid, dim3(256), 0, st, a);
+}
+
+template <typename T, int L, int EPI>
+static void igemm_dma_cfg(const IgCfg& c, const IgArgs& a, hipStream_t st) {
+  const long long key = (((c.bm * 1000LL + c.bn) * 1000 + c.bk) * 10 + c.wm) * 10 + c.st;
+#define IGD(BM_, BN_, BK_, WM_, ST_)                                  \
+  case (((BM_ * 1000LL + BN_) * 1000 + BK_) * 10 + WM_) * 10 + ST_: \
+    igemm_dma_go<T, L, BM_, BN_, BK_, WM_, ST_, EPI>(a, st);          \
+    break;
+  if constexpr (EPI == EPI_SPLIT) {
+    switch (key) {
+      IGD(128, 128, 64, 2, 3)
+      IGD(128, 64, 64, 2, 3)
+      default: check(false, "LDS-DMA tile not instantiated for split reduction");
+    }
+    return;
+  }
+  switch (key) {
+    IGD(128, 128, 64, 2, 2)
+    IGD(128, 128, 64, 2, 3)
+    IGD(256, 64, 64, 4, 2)
+    IGD(256, 64, 64, 4, 3)
+    IGD(128, 64, 64, 2, 3)
+    IGD(64, 128, 64, 1, 3)
+    IGD(256, 128, 64, 2, 2)
+    IGD(128, 128, 32, 2, 3)
+    IGD(64, 64, 64, 2, 3)
+    default: check(false, "LDS-DMA tile not instantiated");
+  }
+#undef IGD
+}
+
 template <typename T, int L, bool VEC, int EPI>
 static void igemm_cfg(const IgCfg& c, const IgArgs& a, int batch, hipStream_t st) {
+  if (c.dma) {
+    if constexpr (sizeof(T) == 2 && VEC && L != NCHW && EPI != EPI_RAW) {
+      check(batch == 1, "LDS-DMA tiles run unbatched GEMMs");
+      igemm_dma_cfg<T, L, EPI>(c, a, st);
+    } else {
+      check(false, "LDS-DMA tiles need 16-bit channel-vector tensors");
+    }
+    return;
+  }
   if constexpr (std::is_same<T, float>::value) {
     igemm_go<T, L, VEC, 64, 64, 32, EPI, 2>(a, batch, st);
   } else {
@@ -719,6 +934,10 @@ static void igemm_run(const IgCfg& cfg, IgArgs& a, const ConvArgs& c, hipStream_
 template <typename T>
 static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t st) {
   const IgCfg cfg = ig_cfg(dtype, param);
+  if (cfg.dma == 2) {
+    conv_patch(dtype, cfg.bm / 16, cfg.bn, cfg.bk, cfg.wm, cfg.st, cfg.ppx, c, st);
+    return;
+  }
   IgArgs a = make_ig(c);
   check(c.xd.layout == c.yd.layout, "implicit GEMM reads and writes one layout");
   check((long long)a.M * a.Ks < (1ll << 31) && (long long)c.xd.n * a.Cs * a.H * a.W < (1ll << 31),

@@ -55,8 +55,15 @@ void conv_direct(int dtype, const ConvArgs& a, hipStream_t st);
 // Parameters that split the reduction need a workspace of igemm_ws_bytes.
 void conv_igemm(int dtype, int param, const ConvArgs& a, hipStream_t st);
 int igemm_num_params(int dtype);
-bool igemm_param_valid(int dtype, int param, int layout, int c);
+bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, int w, int r, int s,
+                       int stride, int pad);
 size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s);
+// 3x3 stride-1 convolution with the input patch in LDS (an implicit-GEMM
+// parameter family; see conv_patch.hip)
+bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
+                      int fmt, int bn, int bk, int ppx);
+void conv_patch(int dtype, int fmt, int bn, int bk, int wm, int stg, int ppx, const ConvArgs& a,
+                hipStream_t st);
 size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k);
 void conv_winograd(int dtype, const ConvArgs& a, hipStream_t st);
 void dwconv(int dtype, const ConvArgs& a, hipStream_t st);

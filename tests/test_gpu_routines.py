@@ -22,6 +22,12 @@ CONV_CASES = [
     (1, 3, 37, 37, 16, 7, 2, 3, "relu"),      # stem-like: C = 3
     (3, 16, 8, 8, 10, 3, 1, 1, "none"),       # K = 10 (not a multiple of 8)
     (1, 130, 7, 7, 24, 3, 1, 1, "relu"),      # C = 130: partial last channel chunk
+    # channel counts that are multiples of the LDS-DMA reduction tile
+    (2, 64, 15, 13, 200, 3, 1, 1, "relu"),    # 3x3/1, ragged M (390) and N (200)
+    (1, 128, 9, 9, 64, 1, 1, 0, "none"),      # pointwise, one N tile
+    (2, 32, 11, 11, 48, 3, 1, 1, "relu"),     # C = 32: only the BK = 32 tiles apply
+    (3, 64, 5, 5, 40, 3, 1, 1, "relu6"),      # several whole images per patch tile
+    (5, 32, 7, 7, 24, 3, 1, 1, "none"),       # image groups with a ragged last group
 ]
 
 
@@ -52,10 +58,12 @@ def test_conv_every_routine(dtype, ci):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-def test_conv_bit_exact_small_integers(dtype):
-    # values in {-1, 0, 1} with C*R*S = 72: every product and partial sum is an
-    # integer <= 72, exact in every dtype, so every routine must match exactly
-    n, c, h, w, k = 2, 8, 10, 9, 16
+@pytest.mark.parametrize("c,k", [(8, 16), (64, 72)])
+def test_conv_bit_exact_small_integers(dtype, c, k):
+    # values in {-1, 0, 1}: every product and partial sum is an integer of at
+    # most C*R*S <= 576, exact in the fp32 accumulators, and the one rounding
+    # to the storage dtype is the oracle's, so every routine must match exactly
+    n, h, w = 2, 10, 9
     layer = {"type": "conv", "in": [0], "k": k, "r": 3, "s": 3, "stride": 1, "pad": 1,
              "groups": 1, "act": "none"}
     x = random_tensor((n, c, h, w), dtype, seed=1, dist="int")
