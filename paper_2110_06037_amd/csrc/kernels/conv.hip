@@ -723,8 +723,8 @@ static const IgCfg kIg16[] = {
     {256, 128, 64, 0, 0, 1, 2, 2}, {128, 128, 32, 0, 0, 1, 2, 3}, {64, 64, 64, 0, 0, 1, 2, 3},
     {128, 128, 64, 1, 0, 1, 2, 3}, {128, 64, 64, 1, 0, 1, 2, 3},
     // 3x3 stride-1 patch kernel
-    {224, 64, 32, 0, 0, 2, 2, 2, 352}, {224, 64, 32, 0, 0, 2, 2, 1, 352}, {224, 32, 32, 0, 0, 2, 4, 1, 352},
-    {112, 64, 32, 0, 0, 2, 1, 2, 256}, {112, 64, 32, 0, 0, 2, 2, 1, 256}, {112, 32, 32, 0, 0, 2, 4, 2, 256}};
+    {224, 64, 32, 0, 0, 2, 2, 2, 384}, {224, 64, 32, 0, 0, 2, 2, 1, 384}, {224, 32, 32, 0, 0, 2, 4, 1, 384},
+    {112, 64, 32, 0, 0, 2, 1, 2, 320}, {112, 64, 32, 0, 0, 2, 2, 1, 320}, {112, 32, 32, 0, 0, 2, 4, 2, 320}};
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 
 int igemm_num_params(int dtype) {

@@ -45,6 +45,9 @@ struct PatchArgs {
   FastDiv fd_ti_tiles;                    // division by tiles_img
   float inv_pw, inv_ph, inv_trq, inv_q;   // 1/PW, 1/PH, 1/(TR*Q), 1/Q for sdiv
   int HW8, W8;                            // NC8HW8 strides: H*W*8, W*8
+  int lpw;                                // log2 of the patch row pitch PW
+  float inv_pq;                           // 1/(P*Q) for sdiv
+  long long y_elems;
   long long x_elems, w_elems;
 };
 
@@ -55,13 +58,14 @@ template <typename T, int L, int FMT, int BN, int BK, int WM, int ST, int PPX, i
 __global__ __launch_bounds__(256, OCC) void conv3x3_patch_kernel(PatchArgs a) {
   static_assert(sizeof(T) == 2 && L != NCHW, "16-bit channel-vector layouts only");
   static_assert(BK == 32, "one 16x16x32 MFMA k-slice per step");
+  static_assert(BN == 32 || BN == 64, "filter rows per load round must be whole taps");
   constexpr int WN = 4 / WM;
   constexpr int CPR = BK / 8;     // 16-byte chunks per 64-byte LDS row
   constexpr int RB = BK * 2;      // bytes per LDS row
   constexpr int PROWS = (PPX + 63) / 64 * 64;           // patch rows (whole load rounds)
   constexpr int WROWS = (9 * BN + 63) / 64 * 64;        // filter rows
   constexpr int NP = PROWS / 64, NW = WROWS / 64;       // load instructions per wave and step
-  static_assert(ST <= 2 || (ST - 2) * (NP + NW) <= 63, "pipeline depth");
+  static_assert(ST == 1 || ST == 2, "one or two LDS stages");
   constexpr int FMW = (FMT + WM - 1) / WM;  // row blocks per wave
   constexpr int WTN = BN / WN, FNW = WTN / 16;
   static_assert(FNW * 16 * WN == BN, "BN must split over the wave columns");
@@ -70,6 +74,7 @@ __global__ __launch_bounds__(256, OCC) void conv3x3_patch_kernel(PatchArgs a) {
   constexpr int SM_C = FMT * 16 * (BN + CPAD) * 2;
   constexpr int SM = ST * STAGE > SM_C ? ST * STAGE : SM_C;
   __shared__ __attribute__((aligned(1024))) char smem[SM];
+  lds_char* const sl = (lds_char*)smem;
   // 16-byte chunk c of LDS row r sits at chunk c ^ swz(r): any 16 consecutive
   // rows of one chunk then cover all 16 chunk positions of a 256-byte bank line
   auto swz = [](int row) { return (row >> 2) & 3; };
@@ -86,81 +91,89 @@ __global__ __launch_bounds__(256, OCC) void conv3x3_patch_kernel(PatchArgs a) {
   const int rows = min(a.TR, a.P - row0);
   const int n0 = nt * BN;
   const int KT = a.CB / CPR;
-  const int PHW = a.PH * a.PW;
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_elems * 2);
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, a.w_elems * 2);
 
-  // load slots: instruction q = wave + 4 i fills LDS rows [16 q, 16 q + 16);
-  // this lane fills row 16 q + lane / 4, physical chunk lane % 4, i.e.
-  // logical chunk (lane % 4) ^ swz(row).  (Index arithmetic uses 24-bit
-  // multiplies and fp32 division: all values are far below 2^24.)
+  // Patch rows are (image, ph, pw) with a row pitch PW (a multiple of 16
+  // that divides 64, at least Q + 2; columns past Q + 2 load zeros).  Load
+  // instruction q = wave + 4 i fills LDS rows [16 q, 16 q + 16): this lane
+  // fills row 16 q + lane / 4, physical chunk lane % 4 (logical chunk
+  // (lane % 4) ^ swz(row)).  Consecutive i add 64 rows, i.e. 64 / PW patch
+  // rows at the same column.  (Index arithmetic: 24-bit multiplies and fp32
+  // division; every value is far below 2^24.)
+  const int r0 = wave * 16 + (lane >> 2);
+  const int pw = r0 & (a.PW - 1), ww = pw - 1;
+  const int prow0 = r0 >> a.lpw;
+  const int lcp = (lane & 3) ^ swz(r0);  // row + 64 i keeps swz
   unsigned poff[NP];
 #pragma unroll
   for (int i = 0; i < NP; ++i) {
-    const int pp = (wave + 4 * i) * 16 + (lane >> 2);
-    const int lc = (lane & 3) ^ swz(pp);
-    const int prow = sdiv(pp, a.inv_pw), pw = pp - __umul24(prow, a.PW);  // patch row over images
+    const int prow = prow0 + (i << (6 - a.lpw));
     const int ii = sdiv(prow, a.inv_ph), ph = prow - __umul24(ii, a.PH);
-    const int img = img0 + ii, h = row0 - 1 + ph, ww = pw - 1;
+    const int img = img0 + ii, h = row0 - 1 + ph;
     const bool ok = ii < a.TI && img < a.N && (unsigned)h < (unsigned)a.H && (unsigned)ww < (unsigned)a.W;
     unsigned e;
     if constexpr (L == NC8)
-      e = __umul24(__umul24(img, a.CB) + lc, a.HW8) + __umul24(h, a.W8) + ww * 8;
+      e = __umul24(__umul24(img, a.CB) + lcp, a.HW8) + __umul24(h, a.W8) + ww * 8;
     else
-      e = __umul24(__umul24(__umul24(img, a.H) + h, a.W) + ww, a.Cs) + lc * 8;
+      e = __umul24(__umul24(__umul24(img, a.H) + h, a.W) + ww, a.Cs) + lcp * 8;
     poff[i] = ok ? e * 2u : kOOB;
   }
+  // filter rows (tap, channel): + 64 rows = + 64 / BN taps, same channel
+  const int tap0 = r0 / BN, kch = n0 + r0 % BN;
+  const unsigned wof0 = (__umul24(kch, a.Kred) + __umul24(tap0, a.C8) + lcp * 8) * 2u;
   unsigned woff[NW];
 #pragma unroll
   for (int i = 0; i < NW; ++i) {
-    const int row = (wave + 4 * i) * 16 + (lane >> 2);
-    const int lc = (lane & 3) ^ swz(row);
-    const int tap = row / BN, k = n0 + (row - tap * BN);
-    woff[i] = row < 9 * BN && k < a.Ng ? (__umul24(k, a.Kred) + __umul24(tap, a.C8) + lc * 8) * 2u : kOOB;
+    const int tap = tap0 + i * (64 / BN);
+    woff[i] = tap < 9 && kch < a.Ng ? wof0 + (unsigned)(i * (64 / BN)) * (unsigned)a.C8 * 2u : kOOB;
   }
-  // bias of this lane's output channels, fetched early (used by the epilogue)
-  float bias[FNW][4];
-#pragma unroll
-  for (int j = 0; j < FNW; ++j)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4 + v;
-      bias[j][v] = n < a.Ng ? a.bias[n] : 0.f;
-    }
   // per-step uniform offsets of channel block kt * CPR
   const int xstep = L == NC8 ? CPR * a.HW8 * 2 : BK * 2;
   auto issue = [&](int buf, int kt) {
-    char* base = smem + buf * STAGE;
+    lds_char* base = sl + buf * STAGE + wave * 1024;
 #pragma unroll
-    for (int i = 0; i < NP; ++i) dma16(rx, base + (wave + 4 * i) * 1024, poff[i], kt * xstep);
+    for (int i = 0; i < NP; ++i) dma16(rx, base + i * 4096, poff[i], kt * xstep);
 #pragma unroll
-    for (int i = 0; i < NW; ++i) dma16(rw, base + P_BYTES + (wave + 4 * i) * 1024, woff[i], kt * BK * 2);
+    for (int i = 0; i < NW; ++i) dma16(rw, base + P_BYTES + i * 4096, woff[i], kt * BK * 2);
   };
+  issue(0, 0);  // the first step's tiles travel while the offsets below are computed
 
-  // LDS byte offsets (within a stage) of this lane's operand chunks: every
-  // tap of every pixel row block, and the filter rows of each tap (those are
-  // 16-row aligned, so their swizzle is the lane's own)
+  // accumulators start at the bias of the lane's output channels
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.bias, (long long)a.Ng * 4);
+  typedef typename Mfma<T>::frag frag;
+  f32x4 acc[FMW][FNW];
+#pragma unroll
+  for (int j = 0; j < FNW; ++j) {
+    const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
+    f32x4 b;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) b[v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n + v) * 4, 0, 0));
+#pragma unroll
+    for (int i = 0; i < FMW; ++i) acc[i][j] = b;
+  }
+
+  // LDS byte offsets (within a stage) of this lane's operand chunks for every
+  // tap: the three column taps of a pixel row block computed, the tap rows
+  // one pitch apart (a multiple of 16 rows, so the swizzle is unchanged)
   int aoff[FMW][9];
+  const int rowpitch = a.PW * RB;
 #pragma unroll
   for (int i = 0; i < FMW; ++i) {
     const int m = (wm * FMW + i) * 16 + (lane & 15);
     const int ii = sdiv(m, a.inv_trq), rem = m - __umul24(ii, a.TR * a.Q);
     const int pr = sdiv(rem, a.inv_q), pc = rem - __umul24(pr, a.Q);
-    const int pb = ii < a.TI ? __umul24(ii, PHW) + __umul24(pr, a.PW) + pc : 0;
+    const int pb = ii < a.TI ? __umul24(ii, a.PH * a.PW) + __umul24(pr, a.PW) + pc : 0;
 #pragma unroll
-    for (int tap = 0; tap < 9; ++tap) {
-      const int r = pb + (tap / 3) * a.PW + tap % 3;
-      aoff[i][tap] = r * RB + ((((lane >> 4)) ^ swz(r)) << 4);
+    for (int c = 0; c < 3; ++c) {
+      const int r = pb + c;
+      aoff[i][c] = (r << 6) | (((lane >> 4) ^ swz(r)) << 4);
+      aoff[i][3 + c] = aoff[i][c] + rowpitch;
+      aoff[i][6 + c] = aoff[i][c] + 2 * rowpitch;
     }
   }
   const int boff = P_BYTES + (wn * WTN + (lane & 15)) * RB + (((lane >> 4) ^ ((lane >> 2) & 3)) << 4);
 
-  typedef typename Mfma<T>::frag frag;
-  f32x4 acc[FMW][FNW];
-#pragma unroll
-  for (int i = 0; i < FMW; ++i)
-#pragma unroll
-    for (int j = 0; j < FNW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   // the fragments of tap t+1 are read from LDS while tap t's MFMAs run
   auto load_frags = [&](const char* S, int tap, frag(&fa)[FMW], frag(&fb)[FNW]) {
 #pragma unroll
@@ -188,24 +201,18 @@ __global__ __launch_bounds__(256, OCC) void conv3x3_patch_kernel(PatchArgs a) {
     // one LDS stage: load, compute, and only then load the next step (the
     // other workgroups on the CU keep its MFMAs busy meanwhile)
     for (int t = 0; t < KT; ++t) {
-      issue(0, t);
+      if (t > 0) issue(0, t);
       wait_vmcnt<0>();
       dma_barrier();
       compute(0);
       dma_barrier();
     }
   } else {
-#pragma unroll
-    for (int u = 0; u < ST - 1; ++u)
-      if (u < KT) issue(u, u);
     for (int t = 0; t < KT; ++t) {
-      if (t + ST - 2 < KT)
-        wait_vmcnt<(ST - 2) * (NP + NW)>();
-      else
-        wait_vmcnt<0>();
+      wait_vmcnt<0>();
       dma_barrier();
-      if (t + ST - 1 < KT) issue((t + ST - 1) % ST, t + ST - 1);
-      compute(t % ST);
+      if (t + 1 < KT) issue((t + 1) & 1, t + 1);
+      compute(t & 1);
     }
   }
 
@@ -223,7 +230,7 @@ __global__ __launch_bounds__(256, OCC) void conv3x3_patch_kernel(PatchArgs a) {
       const int ml = (wm * FMW + i) * 16 + (lane & 15);
       T o[4];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) o[v] = from_f<T>(act_apply(acc[i][j][v] + bias[j][v], ac));
+      for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v], ac.lo, ac.hi));
       __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
     }
   }
@@ -231,28 +238,31 @@ __global__ __launch_bounds__(256, OCC) void conv3x3_patch_kernel(PatchArgs a) {
   // the tile's valid pixels are consecutive rows of the GEMM: whole rows of
   // one image, or whole images
   const int valid = imgs * rows * a.Q;
-  const long long mbase = (long long)img0 * a.P * a.Q + (long long)row0 * a.Q;
+  const int mbase = img0 * a.P * a.Q + row0 * a.Q;
   T* __restrict__ y = reinterpret_cast<T*>(a.y);
   const int PQ = a.P * a.Q;
   if (L == NC8 || a.Ks % 8 == 0) {
+    // 16-byte rows through a buffer resource (32-bit offsets)
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, a.y_elems * 2);
     for (int idx = tid; idx < FMT * 16 * BN / 8; idx += 256) {
       const int row = idx / (BN / 8), cj = idx % (BN / 8);
       const int n = n0 + cj * 8;
       if (row >= valid || n >= a.Ng) continue;
-      const long long m = mbase + row;
-      V8<T> v = ld8(&Cs[row][cj * 8]);
+      const int m = mbase + row;
+      unsigned off;
       if constexpr (L == NC8) {
-        const long long img = m / PQ, pq = m - img * PQ;
-        st8(y + ((img * (a.Ks >> 3) + (n >> 3)) * PQ + pq) * 8, v);
+        const int img = sdiv(m, a.inv_pq), pq = m - img * PQ;
+        off = (unsigned)(((img * (a.Ks >> 3) + (n >> 3)) * PQ + pq) * 8) * 2u;
       } else {
-        st8(y + m * a.Ks + n, v);
+        off = (unsigned)(m * a.Ks + n) * 2u;
       }
+      __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4*>(&Cs[row][cj * 8]), ry, (int)off, 0, 0);
     }
   } else {
     for (int idx = tid; idx < FMT * 16 * BN; idx += 256) {
       const int row = idx / BN, col = idx % BN;
       const int n = n0 + col;
-      if (row < valid && n < a.Ng) y[(mbase + row) * a.Ks + n] = Cs[row][col];
+      if (row < valid && n < a.Ng) y[(long long)(mbase + row) * a.Ks + n] = Cs[row][col];
     }
   }
 }
@@ -276,11 +286,16 @@ static bool patch_tiling(PatchArgs& a, int fmt, int ppx) {
     a.tiles_m = a.N * a.tiles_img;
   }
   a.PH = a.TR + 2;
-  a.PW = a.Q + 2;
+  // row pitch: a multiple of 16 dividing 64, at least Q + 2
+  a.PW = 16;
+  while (a.PW < a.Q + 2) a.PW *= 2;
+  if (a.PW > 64) return false;
+  a.lpw = a.PW == 16 ? 4 : a.PW == 32 ? 5 : 6;
   a.fd_ti_tiles = make_fastdiv(a.tiles_img);
   a.inv_pw = 1.f / (float)a.PW;
   a.inv_ph = 1.f / (float)a.PH;
   a.HW8 = a.H * a.W * 8;
+  a.inv_pq = 1.f / (float)(a.P * a.Q);
   a.W8 = a.W * 8;
   a.inv_trq = 1.f / (float)(a.TR * a.Q);
   a.inv_q = 1.f / (float)a.Q;
@@ -309,6 +324,7 @@ static PatchArgs make_patch(const ConvArgs& c) {
   a.Kred = 9 * a.C8;
   a.x_elems = (long long)c.xd.n * c.xd.cs * c.xd.h * c.xd.w;
   a.w_elems = (long long)((a.K + 7) / 8 * 8) * a.Kred;
+  a.y_elems = (long long)c.yd.n * c.yd.cs * c.yd.h * c.yd.w;
   return a;
 }
 
@@ -345,12 +361,12 @@ static void patch_layout(int fmt, int bn, int bk, int wm, int stg, int ppx, cons
     patch_go<T, L, FMT_, BN_, BK_, WM_, ST_, PPX_, OCC_>(a, st);                        \
     break;
   switch (key) {
-    PGO(14, 64, 32, 2, 2, 352, 1)
-    PGO(14, 64, 32, 2, 1, 352, 2)
-    PGO(14, 32, 32, 4, 1, 352, 3)
-    PGO(7, 64, 32, 1, 2, 256, 1)
-    PGO(7, 64, 32, 2, 1, 256, 2)
-    PGO(7, 32, 32, 4, 2, 256, 2)
+    PGO(14, 64, 32, 2, 2, 384, 1)
+    PGO(14, 64, 32, 2, 1, 384, 2)
+    PGO(14, 32, 32, 4, 1, 384, 3)
+    PGO(7, 64, 32, 1, 2, 320, 1)
+    PGO(7, 64, 32, 2, 1, 320, 2)
+    PGO(7, 32, 32, 4, 2, 320, 2)
     default: check(false, "patch tile not instantiated");
   }
 #undef PGO
@@ -362,7 +378,7 @@ void conv_patch(int dtype, int fmt, int bn, int bk, int wm, int stg, int ppx, co
   check(c.xd.layout == c.yd.layout && c.r == 3 && c.s == 3 && c.stride == 1 && c.pad == 1,
         "patch kernel: 3x3 stride 1 pad 1, one layout");
   check(c.xd.layout == NC8 || (c.xd.layout == NHWC && c.xd.c % 8 == 0), "patch kernel: channel-vector layout");
-  check((long long)c.yd.n * c.yd.cs * c.yd.h * c.yd.w < (1ll << 31), "tensor too large");
+  check((long long)c.yd.n * c.yd.cs * c.yd.h * c.yd.w * 2 < (long long)kOOB, "tensor too large");
   const PatchArgs a = make_patch(c);
   if (dtype == 1) {
     if (c.xd.layout == NC8) patch_layout<f16, NC8>(fmt, bn, bk, wm, stg, ppx, a, st);

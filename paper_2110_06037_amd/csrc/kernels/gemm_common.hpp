@@ -133,8 +133,13 @@ __device__ __forceinline__ void wait_vmcnt() {
 __device__ __forceinline__ void dma_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 typedef __attribute__((address_space(3))) void* lds_void_ptr;
+typedef __attribute__((address_space(3))) char lds_char;
 
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, char* lds_block, unsigned voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_ptr)lds_block, 16, (int)voff, soff, 0, 0);
+}
+// The same with a 32-bit LDS address (uniform offsets stay scalar).
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, lds_char* lds_block, unsigned voff, int soff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_ptr)lds_block, 16, (int)voff, soff, 0, 0);
 }
 

@@ -14,6 +14,7 @@ typedef _Float16 f16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 // layouts (same values as sn_layout)
 constexpr int NCHW = 0, NHWC = 1, NC8 = 2;
