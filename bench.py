@@ -30,6 +30,16 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def layer_kind(spec, i):
+    """Layer type of layer i (1-based), convolutions by filter size and grouping."""
+    layer = spec["layers"][i - 1]
+    if layer["type"] == "conv":
+        if layer["groups"] > 1:
+            return "dwconv"
+        return "conv%dx%d" % (layer["r"], layer["s"])
+    return layer["type"]
+
+
 def layer_work(spec, g, i, routine):
     """(category, flops, algorithmic bytes) of layer i (1-based) for a routine."""
     layer = spec["layers"][i - 1]
@@ -63,7 +73,7 @@ def layer_work(spec, g, i, routine):
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_resnet50_bs32_bf16.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2110_06037_amd", "csrc", "kernels", f)
-                  for f in ("conv.hip", "kcommon.hpp")]
+                  for f in ("conv.hip", "conv_patch.hip", "misc.hip", "gemm_common.hpp", "kcommon.hpp")]
 
 
 def kernel_source_hash():
@@ -295,13 +305,14 @@ def main():
         _, ms = g.run_timed(x, out, reps=args.timing_reps)
         acc += np.array(ms)
     layer_ms = acc / args.steps
-    groups = {}      # routine -> its launches in one step (one kernel symbol per routine)
+    groups = {}      # (routine, layer type) -> its launches in one step: one kernel symbol each
+                     # (the direct routine of an add and of a pool are different kernels)
     cats = {}        # layer category -> totals (for the 3x3 MFMA utilisation)
     per_layer = []
     for i in range(1, nl):
         rt = g.routines(i)[ids[i]]
         cat, flops, byt = layer_work(spec, g, i, rt)
-        for key, d in ((rt["name"], groups), (cat, cats)):
+        for key, d in ((f"{rt['name']} on {layer_kind(spec, i)}", groups), (cat, cats)):
             gr = d.setdefault(key, {"ms": 0.0, "flops": 0, "bytes": 0, "launches": 0, "cats": set()})
             gr["ms"] += layer_ms[i]
             gr["flops"] += flops

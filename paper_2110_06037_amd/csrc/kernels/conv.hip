@@ -46,6 +46,8 @@ struct IgArgs {
   long long x_bs, w_bs, y_bs;  // per-blockIdx.z offsets (batched GEMM), elements
   int vec;                     // NHWC input with C % 8 == 0 (aligned 8-channel vectors)
   long long x_elems, w_elems;  // elements addressable per blockIdx.z (buffer ranges)
+  long long y_elems;
+  float inv_pq, inv_q;         // 1/(P*Q), 1/Q for sdiv
 };
 
 template <typename T>
@@ -453,8 +455,21 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
 // (BM/WM) x (BN/(4/WM)) sub-tile with the weights as the MFMA's first
 // operand (4 consecutive output channels of one pixel per lane).
 
+// LDS bytes of an LDS-DMA tile configuration, and the workgroups per CU it
+// allows (the occupancy the register allocation is sized for).
+template <int BM, int BN, int BK, int ST, int EPI>
+constexpr int dma_lds_bytes() {
+  return ST * (BM + BN) * BK * 2 > (EPI == EPI_LAYOUT ? BM * (BN + 8) * 2 : 0)
+             ? ST * (BM + BN) * BK * 2
+             : (EPI == EPI_LAYOUT ? BM * (BN + 8) * 2 : 0);
+}
+template <int BM, int BN, int BK, int ST, int EPI>
+constexpr int dma_occ() {
+  return 160 * 1024 / dma_lds_bytes<BM, BN, BK, ST, EPI>() > 4 ? 4 : 160 * 1024 / dma_lds_bytes<BM, BN, BK, ST, EPI>();
+}
+
 template <typename T, int L, int BM, int BN, int BK, int WM, int ST, int EPI>
-__global__ __launch_bounds__(256) void igemm_dma_kernel(IgArgs a) {
+__global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_dma_kernel(IgArgs a) {
   static_assert(sizeof(T) == 2 && L != NCHW, "16-bit channel-vector layouts only");
   constexpr int WN = 4 / WM;
   constexpr int CPR = BK / 8;       // 16-byte chunks per tile row
@@ -499,14 +514,15 @@ __global__ __launch_bounds__(256) void igemm_dma_kernel(IgArgs a) {
     const int m = m0 + row;
     const bool ok = m < a.M;
     const int mm = ok ? m : 0;
-    const int img = mm / a.PQ, pq = mm - img * a.PQ;
-    const int p = pq / a.Q, q = pq - p * a.Q;
-    const int h0 = p * a.stride - a.pad, w0 = q * a.stride - a.pad;
+    // fp32 division and 24-bit multiplies: indices stay far below 2^21
+    const int img = sdiv(mm, a.inv_pq), pq = mm - __mul24(img, a.PQ);
+    const int p = sdiv(pq, a.inv_q), q = pq - __mul24(p, a.Q);
+    const int h0 = __mul24(p, a.stride) - a.pad, w0 = __mul24(q, a.stride) - a.pad;
     int e;
     if constexpr (L == NC8)
-      e = img * a.CB * a.H * a.W * 8 + (h0 * a.W + w0) * 8 + lc * a.H * a.W * 8;
+      e = __mul24(img, a.CB * a.H * a.W * 8) + __mul24(__mul24(h0, a.W) + w0, 8) + __mul24(lc, a.H * a.W * 8);
     else
-      e = ((img * a.H + h0) * a.W + w0) * a.Cs + lc * 8;
+      e = __mul24(__mul24(__mul24(img, a.H) + h0, a.W) + w0, a.Cs) + lc * 8;
     rbyte[i] = (unsigned)e * 2u;  // may wrap for the halo; valid taps add back
     unsigned msk = 0;
     for (int r = 0; r < a.R; ++r)
@@ -521,7 +537,7 @@ __global__ __launch_bounds__(256) void igemm_dma_kernel(IgArgs a) {
     const int row = (wave + 4 * i) * RPB + prow;
     const int lc = pch ^ swz(row);
     const int k = n0 + row;
-    bbyte[i] = k < a.Ng ? (unsigned)((k * a.Kred + lc * 8) * 2) : kOOB;
+    bbyte[i] = k < a.Ng ? (unsigned)((__mul24(k, a.Kred) + lc * 8) * 2) : kOOB;
   }
 
   // reduction position of the next step to load: tap (r, s), channel block cb
@@ -551,11 +567,22 @@ __global__ __launch_bounds__(256) void igemm_dma_kernel(IgArgs a) {
     }
   };
 
+  // accumulators start at the bias of the lane's output channels (at zero
+  // for a partial sum of a split reduction)
   f32x4 acc[FM][FN];
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+  for (int j = 0; j < FN; ++j) {
+    f32x4 b = f32x4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (EPI == EPI_LAYOUT) {
+      const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.bias, (long long)a.Ng * 4);
+      const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
 #pragma unroll
-    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int v = 0; v < 4; ++v)
+        b[v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n + v) * 4, 0, 0));
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i) acc[i][j] = b;
+  }
   typedef typename Mfma<T>::frag frag;
   auto compute = [&](int buf) {
     const char* As = smem + buf * STAGE;
@@ -618,35 +645,37 @@ __global__ __launch_bounds__(256) void igemm_dma_kernel(IgArgs a) {
   } else {
     __syncthreads();  // every wave is done with the last tile
     T(*Cs)[BN + CPAD] = reinterpret_cast<T(*)[BN + CPAD]>(smem);
+    const ActClamp ac = act_clamp(a.act);
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int nl = wn * WTN + j * 16 + (lane >> 4) * 4;
-      float bv[4];
-#pragma unroll
-      for (int v = 0; v < 4; ++v) bv[v] = n0 + nl + v < a.Ng ? a.bias[n0 + nl + v] : 0.f;
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const int ml = wm * WTM + i * 16 + (lane & 15);
         T o[4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) o[v] = from_f<T>(act_f(acc[i][j][v] + bv[v], a.act));
+        for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v], ac.lo, ac.hi));
         __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
       }
     }
     __syncthreads();
     T* __restrict__ y = reinterpret_cast<T*>(a.y);
     if (L == NC8 || a.Ks % 8 == 0) {
+      // 16-byte rows through a buffer resource (32-bit offsets)
+      const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, a.y_elems * 2);
       for (int idx = tid; idx < BM * BN / 8; idx += 256) {
         const int row = idx / (BN / 8), cj = idx % (BN / 8);
         const int m = m0 + row, n = n0 + cj * 8;
         if (m >= a.M || n >= a.Ng) continue;
-        V8<T> v = ld8(&Cs[row][cj * 8]);
+        const u32x4 v = *reinterpret_cast<const u32x4*>(&Cs[row][cj * 8]);
+        unsigned off;
         if constexpr (L == NC8) {
-          const int img = m / a.PQ, pq = m - img * a.PQ;
-          st8(y + (((long long)img * (a.Ks >> 3) + (n >> 3)) * a.PQ + pq) * 8, v);
+          const int img = sdiv(m, a.inv_pq), pq = m - __mul24(img, a.PQ);
+          off = (unsigned)(((img * (a.Ks >> 3) + (n >> 3)) * a.PQ + pq) * 8) * 2u;
         } else {
-          st8(y + (long long)m * a.Ks + n, v);
+          off = (unsigned)(m * a.Ks + n) * 2u;
         }
+        __builtin_amdgcn_raw_buffer_store_b128(v, ry, (int)off, 0, 0);
       }
     } else {
       for (int idx = tid; idx < BM * BN; idx += 256) {
@@ -739,7 +768,12 @@ bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, in
   const IgCfg& g = dtype == 0 ? kIg32[param] : kIg16[param];
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
   if (g.dma == 2) return patch_applicable(layout, c, h, w, r, s, stride, pad, n, g.bm / 16, g.bn, g.bk, g.ppx);
-  if (g.dma) return vec && ((c + 7) / 8) % (g.bk / 8) == 0 && r * s <= 32;
+  if (g.dma) {
+    // fp32 index division and 32-bit byte offsets bound the output size
+    const long long p = (h + 2 * pad - r) / stride + 1, q = (w + 2 * pad - s) / stride + 1;
+    const long long m = (long long)n * p * q;
+    return vec && ((c + 7) / 8) % (g.bk / 8) == 0 && r * s <= 32 && m + p * q < (1 << 21);
+  }
   return vec || 256 % g.bm == 0;
 }
 
@@ -779,6 +813,8 @@ static void igemm_dma_go(const IgArgs& a, hipStream_t st) {
   check(a.x_elems * 2 < (long long)kOOB && a.w_elems * 2 < (long long)kOOB,
         "tensor too large for 32-bit buffer offsets");
   check(a.CB % (BK / 8) == 0 && a.R * a.S <= 32, "LDS-DMA tile needs C % BK == 0 and R*S <= 32");
+  check(a.y_elems * 2 < (long long)kOOB && (long long)a.M + a.PQ < (1 << 21),
+        "tensor too large for 32-bit offsets / fp32 index division");
   dim3 grid(a.tiles_m * a.tiles_n, a.splits, 1);
   SN_LAUNCH((igemm_dma_kernel<T, L, BM, BN, BK, WM, ST, EPI>), grid, dim3(256), 0, st, a);
 }
@@ -899,6 +935,9 @@ static IgArgs make_ig(const ConvArgs& c) {
   a.vec = (c.xd.layout == NHWC && a.C % 8 == 0) ? 1 : 0;
   a.x_elems = (long long)c.xd.n * c.xd.cs * c.xd.h * c.xd.w;
   a.w_elems = (long long)((a.K + 7) / 8 * 8) * a.Kred;
+  a.y_elems = (long long)c.yd.n * c.yd.cs * c.yd.h * c.yd.w;
+  a.inv_pq = 1.f / (float)std::max(a.PQ, 1);
+  a.inv_q = 1.f / (float)std::max(a.Q, 1);
   return a;
 }
 

@@ -334,6 +334,7 @@ bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride,
   if (r != 3 || s != 3 || stride != 1 || pad != 1) return false;
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
   if (!vec || ((c + 7) / 8) % (bk / 8) != 0) return false;
+  if ((long long)n * h * w + h * w >= (1 << 21)) return false;  // fp32 index division
   PatchArgs a{};
   a.N = n;
   a.P = h;
