@@ -736,7 +736,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(IgArgs a) {
 struct IgCfg {
   int bm, bn, bk, split, pf;  // split: 0 = none, 1 = split the reduction when tiles are few;
                               // pf: prefetch depth (register staging sets)
-  int dma = 0, wm = 2, st = 2;  // 1: LDS-DMA kernel, 2: 3x3 patch kernel (bm = 16 * row blocks);
+  int dma = 0, wm = 2, st = 2;  // 1: LDS-DMA kernel, 2: 3x3 patch kernel (bm = 16 * row blocks),
+                                // 3: small-channel kernel;
                                 // wave rows WM (of 4 waves), LDS stages ST
   int ppx = 0;                  // patch kernel: patch capacity in pixels
 };
@@ -753,7 +754,9 @@ static const IgCfg kIg16[] = {
     {128, 128, 64, 1, 0, 1, 2, 3}, {128, 64, 64, 1, 0, 1, 2, 3},
     // 3x3 stride-1 patch kernel
     {224, 64, 32, 0, 0, 2, 2, 2, 384}, {224, 64, 32, 0, 0, 2, 2, 1, 384}, {224, 32, 32, 0, 0, 2, 4, 1, 384},
-    {112, 64, 32, 0, 0, 2, 1, 2, 320}, {112, 64, 32, 0, 0, 2, 2, 1, 320}, {112, 32, 32, 0, 0, 2, 4, 2, 320}};
+    {112, 64, 32, 0, 0, 2, 1, 2, 320}, {112, 64, 32, 0, 0, 2, 2, 1, 320}, {112, 32, 32, 0, 0, 2, 4, 2, 320},
+    // small-channel (stem) kernel: NHWC, C <= 4, stride 2
+    {112, 64, 32, 0, 0, 3, 2, 1, 1664}, {224, 64, 32, 0, 0, 3, 2, 1, 2112}};
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 
 int igemm_num_params(int dtype) {
@@ -768,6 +771,7 @@ bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, in
   const IgCfg& g = dtype == 0 ? kIg32[param] : kIg16[param];
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
   if (g.dma == 2) return patch_applicable(layout, c, h, w, r, s, stride, pad, n, g.bm / 16, g.bn, g.bk, g.ppx);
+  if (g.dma == 3) return smallc_applicable(layout, c, h, w, r, s, stride, pad, n, g.bm / 16, g.ppx, 28);
   if (g.dma) {
     // fp32 index division and 32-bit byte offsets bound the output size
     const long long p = (h + 2 * pad - r) / stride + 1, q = (w + 2 * pad - s) / stride + 1;
@@ -975,6 +979,10 @@ static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t 
   const IgCfg cfg = ig_cfg(dtype, param);
   if (cfg.dma == 2) {
     conv_patch(dtype, cfg.bm / 16, cfg.bn, cfg.bk, cfg.wm, cfg.st, cfg.ppx, c, st);
+    return;
+  }
+  if (cfg.dma == 3) {
+    conv_smallc(dtype, cfg.bm / 16, c, st);
     return;
   }
   IgArgs a = make_ig(c);

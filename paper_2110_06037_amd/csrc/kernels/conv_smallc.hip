@@ -1,0 +1,294 @@
+// Convolution of an input with few channels (C <= 4; the RGB stem of a CNN)
+// in NHWC, stride 2, any R x S filter, as an implicit GEMM on MFMA.
+//
+// Padding three channels to the 8 of a 16-byte vector would waste 5/8 of
+// the MFMA work, so the reduction is packed differently: the input patch of
+// a tile sits in LDS with 4 channels per pixel (8 bytes, the fourth zero),
+// and one 8-element MFMA operand chunk is a pixel pair -- filter columns
+// (s, s + 1) of filter row r, 4 channels each.  With stride 2 an output
+// pixel's pairs start at even patch columns, so every chunk is an aligned
+// 16-byte LDS read.  The reduction has R * ceil(S / 2) such chunks (28 for a
+// 7 x 7 filter: 224 MFMA elements for 147 real ones).  The filter is
+// repacked into the same chunks in LDS once per workgroup; workgroups are
+// persistent over output-row tiles and prefetch the next tile's input
+// pixels into registers while the current tile's MFMAs run.
+#include "gemm_common.hpp"
+#include "kcommon.hpp"
+#include "launch.hpp"
+
+namespace sn {
+namespace k {
+
+struct SmallCArgs {
+  const void* x;
+  const void* w;  // prepared [Kp][R][S][C8]
+  const float* bias;
+  void* y;
+  int N, C, H, W;
+  int K, P, Q, Ks, Ng;
+  int R, S, pad, act;
+  int C8, Kred;          // prepared filter: channels per tap, row length R * S * C8
+  int G, SP;             // operand chunks R * SP, column pairs per filter row SP = ceil(S / 2)
+  int TR, PH, PWP;       // output rows per tile, patch rows, patch pitch in pixels (even)
+  int tiles_img, tiles;  // row tiles per image, tiles in all
+  float inv_sp, inv_pwp2, inv_q;  // 1/SP, 1/(PWP/2), 1/Q for sdiv
+  FastDiv fd_tiles_img;
+  long long x_elems, w_elems, y_elems;
+};
+
+// FMT: MFMA row blocks (16 output pixels) per tile; 64 output channels per
+// workgroup; WM wave rows (of 4 waves); PPX patch capacity in pixels; GMAX
+// operand chunks of the filter (multiple of 4: one k-slice of 32 is 4).
+template <typename T, int FMT, int WM, int PPX, int GMAX, int OCC>
+__global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
+  static_assert(sizeof(T) == 2, "16-bit types");
+  static_assert(GMAX % 4 == 0 && PPX % 2 == 0, "shape");
+  constexpr int BN = 64;
+  constexpr int WN = 4 / WM;
+  constexpr int FMW = (FMT + WM - 1) / WM;
+  constexpr int WTN = BN / WN, FNW = WTN / 16;
+  constexpr int WPITCH = GMAX * 16 + 16;  // filter row bytes (odd number of 16-byte units)
+  constexpr int P_BYTES = PPX * 8;
+  constexpr int PAIRS = PPX / 2;                 // patch pixel pairs (16 bytes each)
+  constexpr int NPF = (PAIRS + 255) / 256;       // pairs per thread
+  constexpr int SM = P_BYTES + BN * WPITCH;
+  __shared__ __attribute__((aligned(1024))) char smem[SM];
+  char* const Ws = smem + P_BYTES;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  const int n0 = blockIdx.y * BN;
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_elems * 2);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, a.w_elems * 2);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.bias, (long long)a.Ng * 4);
+  const __amdgpu_buffer_rsrc_t ry = make_rsrc(a.y, a.y_elems * 2);
+
+  // filter chunks: row n, chunk g = (r, sp) holds taps (r, 2 sp) and
+  // (r, 2 sp + 1), channels 0..3 each (zero past C, S, G)
+  for (int idx = tid; idx < BN * GMAX; idx += 256) {
+    const int n = idx / GMAX, g = idx - n * GMAX;
+    const int r = sdiv(g, a.inv_sp), sp = g - __umul24(r, a.SP);
+    const int s0 = 2 * sp, k = n0 + n;
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (g < a.G && k < a.Ng) {
+      const unsigned base = (unsigned)(__umul24(k, a.Kred) + __umul24(__umul24(r, a.S) + s0, a.C8)) * 2u;
+      const unsigned lo = s0 < a.S ? base : kOOB, hi = s0 + 1 < a.S ? base + (unsigned)a.C8 * 2u : kOOB;
+      const auto d0 = __builtin_amdgcn_raw_buffer_load_b64(rw, (int)lo, 0, 0);
+      const auto d1 = __builtin_amdgcn_raw_buffer_load_b64(rw, (int)hi, 0, 0);
+      v = u32x4{d0[0], d0[1], d1[0], d1[1]};  // channels past C are zero in the prepared filter
+    }
+    *reinterpret_cast<u32x4*>(Ws + n * WPITCH + g * 16) = v;
+  }
+
+  // patch pixels of a tile: pair j = (row, column pair), 16 bytes in LDS;
+  // an input pixel is C <= 4 bf16 values at any 2-byte alignment: three
+  // aligned dwords cover it, realigned by the byte offset
+  const int Cm = a.C;
+  auto fetch = [&](int tile, u32x4 (&raw)[NPF][2], unsigned (&shf)[NPF][2], bool (&ok)[NPF][2]) {
+    const int img = fdiv(tile, a.fd_tiles_img), rt = tile - img * a.tiles_img;
+    const int h0 = rt * a.TR * 2 - a.pad;
+#pragma unroll
+    for (int u = 0; u < NPF; ++u) {
+      const int j = tid + u * 256;
+      const int prw = sdiv(j, a.inv_pwp2), pc2 = j - __umul24(prw, a.PWP >> 1);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int h = h0 + prw, w = 2 * pc2 + e - a.pad;
+        ok[u][e] = j < PAIRS && prw < a.PH && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+        const unsigned byte = (unsigned)(__umul24(__umul24(img, a.H) + h, a.W) + w) * (unsigned)Cm * 2u;
+        shf[u][e] = (byte & 3u) * 8u;
+        const auto d = __builtin_amdgcn_raw_buffer_load_b96(rx, ok[u][e] ? (int)(byte & ~3u) : (int)kOOB, 0, 0);
+        raw[u][e] = u32x4{d[0], d[1], d[2], 0u};
+      }
+    }
+  };
+  auto store_patch = [&](const u32x4 (&raw)[NPF][2], const unsigned (&shf)[NPF][2], const bool (&ok)[NPF][2]) {
+#pragma unroll
+    for (int u = 0; u < NPF; ++u) {
+      const int j = tid + u * 256;
+      if (j >= PAIRS) continue;
+      unsigned px[2][2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        // 8 bytes from the byte shift: channels 0..3 of the pixel
+        const unsigned long long lo = ((unsigned long long)raw[u][e][1] << 32) | raw[u][e][0];
+        const unsigned long long hi = ((unsigned long long)raw[u][e][2] << 32) | raw[u][e][1];
+        unsigned d0 = (unsigned)(lo >> shf[u][e]), d1 = (unsigned)(hi >> shf[u][e]);
+        // keep channels < C: d0 = (c0, c1), d1 = (c2, c3)
+        if (Cm < 2) d0 &= 0xFFFFu;
+        if (Cm < 3) d1 = 0u;
+        else if (Cm < 4) d1 &= 0xFFFFu;
+        px[e][0] = ok[u][e] ? d0 : 0u;
+        px[e][1] = ok[u][e] ? d1 : 0u;
+      }
+      *reinterpret_cast<u32x4*>(smem + j * 16) = u32x4{px[0][0], px[0][1], px[1][0], px[1][1]};
+    }
+  };
+
+  // operand offsets: output pixel m of the tile -> patch pixel (2 pr, 2 pc);
+  // chunk g = (r, sp) adds r rows and 2 sp columns
+  int abase[FMW];
+#pragma unroll
+  for (int i = 0; i < FMW; ++i) {
+    const int m = (wm * FMW + i) * 16 + (lane & 15);
+    const int pr = sdiv(m, a.inv_q), pc = m - __umul24(pr, a.Q);
+    abase[i] = ((2 * pr) * a.PWP + 2 * pc) * 8;
+  }
+  const int bbase = (wn * WTN + (lane & 15)) * WPITCH + (lane >> 4) * 16;
+  const ActClamp ac = act_clamp(a.act);
+  typedef typename Mfma<T>::frag frag;
+
+  // accumulator start: the bias of the lane's output channels
+  f32x4 bias[FNW];
+#pragma unroll
+  for (int j = 0; j < FNW; ++j) {
+    const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      bias[j][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n + v) * 4, 0, 0));
+  }
+
+  u32x4 raw[NPF][2];
+  unsigned shf[NPF][2];
+  bool ok[NPF][2];
+  int tile = blockIdx.x;
+  if (tile < a.tiles) fetch(tile, raw, shf, ok);
+  for (; tile < a.tiles; tile += gridDim.x) {
+    __syncthreads();  // every wave is done reading the previous tile's patch
+    store_patch(raw, shf, ok);
+    __syncthreads();
+    if (tile + (int)gridDim.x < a.tiles) fetch(tile + gridDim.x, raw, shf, ok);  // in flight during the MFMAs
+
+    f32x4 acc[FMW][FNW];
+#pragma unroll
+    for (int i = 0; i < FMW; ++i)
+#pragma unroll
+      for (int j = 0; j < FNW; ++j) acc[i][j] = bias[j];
+#pragma unroll
+    for (int st = 0; st < GMAX / 4; ++st) {
+      const int g = st * 4 + (lane >> 4);
+      const int r = sdiv(g, a.inv_sp), sp = g - __umul24(r, a.SP);
+      const int toff = g < a.G ? (r * a.PWP + 2 * sp) * 8 : 0;
+      frag fa[FMW], fb[FNW];
+#pragma unroll
+      for (int i = 0; i < FMW; ++i)
+        if (wm * FMW + i < FMT) fa[i] = *reinterpret_cast<const frag*>(smem + abase[i] + toff);
+#pragma unroll
+      for (int j = 0; j < FNW; ++j) fb[j] = *reinterpret_cast<const frag*>(Ws + bbase + j * 16 * WPITCH + st * 64);
+#pragma unroll
+      for (int i = 0; i < FMW; ++i)
+        if (wm * FMW + i < FMT)
+#pragma unroll
+          for (int j = 0; j < FNW; ++j) acc[i][j] = Mfma<T>::run(fb[j], fa[i], acc[i][j]);
+    }
+
+    // epilogue: each lane stores its 4 consecutive channels of a pixel (8 bytes)
+    const int img = fdiv(tile, a.fd_tiles_img), rt = tile - img * a.tiles_img;
+    const int row0 = rt * a.TR;
+    const int valid = min(a.TR, a.P - row0) * a.Q;
+    const int mbase = (img * a.P + row0) * a.Q;
+#pragma unroll
+    for (int i = 0; i < FMW; ++i) {
+      const int ml = (wm * FMW + i) * 16 + (lane & 15);
+      if (wm * FMW + i >= FMT || ml >= valid) continue;
+#pragma unroll
+      for (int j = 0; j < FNW; ++j) {
+        const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
+        if (n >= a.Ng) continue;
+        T o[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v], ac.lo, ac.hi));
+        u32x2 pk;
+        __builtin_memcpy(&pk, o, 8);
+        __builtin_amdgcn_raw_buffer_store_b64(pk, ry, (int)((unsigned)((mbase + ml) * a.Ks + n) * 2u), 0, 0);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ host
+static bool smallc_tiling(SmallCArgs& a, int fmt, int ppx, int gmax) {
+  const int maxpx = fmt * 16;
+  if (a.Q > maxpx) return false;
+  const int fit = maxpx / a.Q;
+  a.tiles_img = (a.P + fit - 1) / fit;
+  a.TR = (a.P + a.tiles_img - 1) / a.tiles_img;
+  a.tiles = a.N * a.tiles_img;
+  a.PH = (a.TR - 1) * 2 + a.R;
+  const int pw = (a.Q - 1) * 2 + a.S;
+  a.PWP = (pw + 1) / 2 * 2;
+  a.SP = (a.S + 1) / 2;
+  a.G = a.R * a.SP;
+  a.inv_sp = 1.f / (float)a.SP;
+  a.inv_pwp2 = 1.f / (float)(a.PWP / 2);
+  a.inv_q = 1.f / (float)a.Q;
+  a.fd_tiles_img = make_fastdiv(a.tiles_img);
+  return a.PH * a.PWP <= ppx && a.G <= gmax;
+}
+
+bool smallc_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
+                       int fmt, int ppx, int gmax) {
+  if (layout != NHWC || c > 4 || stride != 2) return false;
+  SmallCArgs a{};
+  a.N = n;
+  a.P = (h + 2 * pad - r) / 2 + 1;
+  a.Q = (w + 2 * pad - s) / 2 + 1;
+  a.R = r;
+  a.S = s;
+  if ((long long)n * h * w * c * 2 >= (long long)kOOB || (long long)n * a.P * a.Q * 2048 >= (long long)kOOB)
+    return false;
+  return smallc_tiling(a, fmt, ppx, gmax);
+}
+
+template <typename T, int FMT, int WM, int PPX, int GMAX, int OCC>
+static void smallc_go(SmallCArgs a, hipStream_t st) {
+  check(smallc_tiling(a, FMT, PPX, GMAX), "small-channel tile does not fit");
+  const int tn = (a.Ng + 63) / 64;
+  // persistent: OCC workgroups per CU over 256 CUs, split over the channel tiles
+  const int per_n = std::max(1, std::min(a.tiles, 256 * OCC / tn));
+  dim3 grid(per_n, tn);
+  SN_LAUNCH((conv_smallc_kernel<T, FMT, WM, PPX, GMAX, OCC>), grid, dim3(256), 0, st, a);
+}
+
+void conv_smallc(int dtype, int fmt, const ConvArgs& c, hipStream_t st) {
+  check(dtype != 0, "small-channel kernel runs 16-bit types");
+  check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.xd.c <= 4 && c.stride == 2,
+        "small-channel kernel: NHWC, C <= 4, stride 2");
+  SmallCArgs a{};
+  a.x = c.x;
+  a.w = c.w;
+  a.bias = c.bias;
+  a.y = c.y;
+  a.N = c.xd.n;
+  a.C = c.xd.c;
+  a.H = c.xd.h;
+  a.W = c.xd.w;
+  a.K = c.yd.c;
+  a.P = c.yd.h;
+  a.Q = c.yd.w;
+  a.Ks = c.yd.cs;
+  a.Ng = c.yd.c;
+  a.R = c.r;
+  a.S = c.s;
+  a.pad = c.pad;
+  a.act = c.act;
+  a.C8 = (a.C + 7) / 8 * 8;
+  a.Kred = a.R * a.S * a.C8;
+  a.x_elems = (long long)c.xd.n * c.xd.cs * c.xd.h * c.xd.w;
+  a.w_elems = (long long)((a.K + 7) / 8 * 8) * a.Kred;
+  a.y_elems = (long long)c.yd.n * c.yd.cs * c.yd.h * c.yd.w;
+  check(a.x_elems * 2 < (long long)kOOB && a.y_elems * 2 < (long long)kOOB && a.w_elems * 2 < (long long)kOOB,
+        "tensor too large for 32-bit offsets");
+  check(c.yd.cs % 4 == 0 && c.yd.c % 4 == 0, "small-channel kernel stores 4-channel groups");
+  if (fmt == 7) {
+    if (dtype == 1) smallc_go<f16, 7, 2, 1664, 28, 3>(a, st);
+    else smallc_go<bf16, 7, 2, 1664, 28, 3>(a, st);
+  } else {
+    if (dtype == 1) smallc_go<f16, 14, 2, 2112, 28, 3>(a, st);
+    else smallc_go<bf16, 14, 2, 2112, 28, 3>(a, st);
+  }
+}
+
+}  // namespace k
+}  // namespace sn

@@ -64,6 +64,10 @@ bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride,
                       int fmt, int bn, int bk, int ppx);
 void conv_patch(int dtype, int fmt, int bn, int bk, int wm, int stg, int ppx, const ConvArgs& a,
                 hipStream_t st);
+// Stride-2 convolution of an NHWC input with C <= 4 (a CNN stem; see conv_smallc.hip)
+bool smallc_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
+                       int fmt, int ppx, int gmax);
+void conv_smallc(int dtype, int fmt, const ConvArgs& a, hipStream_t st);
 size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k);
 void conv_winograd(int dtype, const ConvArgs& a, hipStream_t st);
 void dwconv(int dtype, const ConvArgs& a, hipStream_t st);

@@ -304,6 +304,25 @@ __global__ __launch_bounds__(256) void transpose_kernel(const E* __restrict__ x,
   }
 }
 
+// NCHW <-> NHWC for few channels (C <= 8): one pixel per thread, its C
+// values read from (or written to) C planes; both sides stay coalesced
+// across the threads, where the 64 x 64 tile of the general transpose
+// would be almost empty.
+template <typename E, bool TO_NHWC>
+__global__ __launch_bounds__(256) void transpose_smallc_kernel(const E* __restrict__ x, E* __restrict__ y,
+                                                               int C, long long HW, long long pixels) {
+  const long long p = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (p >= pixels) return;
+  const long long n = p / HW, hw = p - n * HW;
+  const long long plane = n * C * HW + hw;
+  for (int c = 0; c < C; ++c) {
+    if (TO_NHWC)
+      y[p * C + c] = x[plane + c * HW];
+    else
+      y[plane + c * HW] = x[p * C + c];
+  }
+}
+
 // Any layout -> any layout, one destination element per thread (padded
 // channels get zero).  Used for the pairs without a specialised kernel.
 template <typename E, int LI, int LO>
@@ -340,6 +359,16 @@ static void convert_e(const void* xv, const TDesc& xd, void* yv, const TDesc& yd
   E* y = reinterpret_cast<E*>(yv);
   const int HW = xd.h * xd.w;
   if ((xd.layout == NCHW && yd.layout == NHWC) || (xd.layout == NHWC && yd.layout == NCHW)) {
+    if (xd.c <= 8) {
+      const long long pixels = (long long)xd.n * HW;
+      if (yd.layout == NHWC)
+        SN_LAUNCH((transpose_smallc_kernel<E, true>), dim3(blocks(pixels)), dim3(256), 0, s, x, y, xd.c,
+                  (long long)HW, pixels);
+      else
+        SN_LAUNCH((transpose_smallc_kernel<E, false>), dim3(blocks(pixels)), dim3(256), 0, s, x, y, xd.c,
+                  (long long)HW, pixels);
+      return;
+    }
     dim3 g((HW + 63) / 64, (xd.c + 63) / 64, xd.n);
     check(xd.n <= 65535, "batch too large for the transpose grid");
     if (yd.layout == NHWC)

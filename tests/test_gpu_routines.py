@@ -28,6 +28,8 @@ CONV_CASES = [
     (2, 32, 11, 11, 48, 3, 1, 1, "relu"),     # C = 32: only the BK = 32 tiles apply
     (3, 64, 5, 5, 40, 3, 1, 1, "relu6"),      # several whole images per patch tile
     (5, 32, 7, 7, 24, 3, 1, 1, "none"),       # image groups with a ragged last group
+    (2, 3, 45, 38, 64, 7, 2, 3, "relu"),      # stem: C = 3, 7x7/2, odd output sizes
+    (1, 2, 21, 24, 72, 5, 2, 2, "relu6"),     # C = 2, 5x5/2, K = 72 (two channel tiles)
 ]
 
 
@@ -138,12 +140,14 @@ def test_fc(dtype, case):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-def test_add_and_converters_bit_exact(dtype):
+@pytest.mark.parametrize("c", [12, 3])
+def test_add_and_converters_bit_exact(dtype, c):
     # two maxpools feeding an add: every (layout_a, layout_b, layout_add)
-    # combination exercises the converters between all layout pairs; max and
-    # an exactly representable sum keep the result bit-exact
+    # combination exercises the converters between all layout pairs (few
+    # channels take their own transpose kernel); max and an exactly
+    # representable sum keep the result bit-exact
     from paper_2110_06037_amd import Graph
-    n, c, h, w = 2, 12, 9, 9
+    n, h, w = 2, 9, 9
     x = random_tensor((n, c, h, w), dtype, seed=11, dist="int")
     xs = to_f64(x, dtype)
     p = O.maxpool(xs, 3, 1, 1)
