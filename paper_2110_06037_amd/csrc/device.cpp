@@ -217,8 +217,11 @@ void dev_upload_layer(Graph& g, int id) {
 
 // ------------------------------------------------------------------ launching
 static size_t layer_ws_bytes(const Graph& g, const Layer& L, const Routine& r) {
-  if (L.type != SN_LAYER_CONV2D || L.d.groups > 1) return 0;
+  if (L.inputs.empty()) return 0;  // the input layer
   const Shape& in = g.layers[L.inputs[0]].out;
+  if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM)
+    return k::igemm_ws_bytes(g.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), 1, 1);
+  if (L.type != SN_LAYER_CONV2D || L.d.groups > 1) return 0;
   if (r.algo == SN_ALGO_WINOGRAD) return k::winograd_ws_bytes(g.dtype, tdesc(in, r.layout), L.out.c);
   if (r.algo == SN_ALGO_IGEMM)
     return k::igemm_ws_bytes(g.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), L.d.r, L.d.s);
@@ -283,7 +286,9 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
         a.stride = 1;
         a.pad = 0;
         a.act = SN_ACT_NONE;
-        k::conv_igemm(dt, 0, a, st);  // 64 x 64 tiles, no reduction split
+        a.ws = ws;
+        a.ws_bytes = ws_bytes;
+        k::conv_igemm(dt, r.param, a, st);
       } else {
         k::fc_direct(dt, in[0], xs.n, xs.c, stored_c(xs, r.layout), dl.w, round8(xs.c), dl.bias, out,
                      L.out.c, stored_c(L.out, r.layout), st);

@@ -58,7 +58,7 @@ std::string routine_name(const Layer& L, const Routine& r) {
   std::ostringstream o;
   o << kLayoutName[r.layout] << "/" << kAlgoName[r.algo];
   if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_IGEMM) o << ":p" << r.param;
-  if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM) o << ":1x1conv";
+  if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM) o << ":1x1conv:p" << r.param;
   return o.str();
 }
 
@@ -96,7 +96,12 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
         break;
       case SN_LAYER_FC:
         add(lay, SN_ALGO_DIRECT, 0);
-        if (g.opt_algos >> SN_ALGO_IGEMM & 1) add(lay, SN_ALGO_IGEMM, 0);
+        if (g.opt_algos >> SN_ALGO_IGEMM & 1) {  // the dense childnet: a 1x1 convolution
+          int np = g.opt_params ? k::igemm_num_params(g.dtype) : 1;
+          for (int p = 0; p < np; ++p)
+            if (k::igemm_param_valid(g.dtype, p, lay, in.n, in.c, 1, 1, 1, 1, 1, 0))
+              add(lay, SN_ALGO_IGEMM, p);
+        }
         break;
       default:
         add(lay, SN_ALGO_DIRECT, 0);
