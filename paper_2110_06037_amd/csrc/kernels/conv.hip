@@ -584,27 +584,35 @@ __global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_d
     for (int i = 0; i < FM; ++i) acc[i][j] = b;
   }
   typedef typename Mfma<T>::frag frag;
+  // operand chunk offsets in a stage: a 16-row block starts at a multiple of
+  // 16 rows, so the row swizzle is the lane's own; the chunk of k-slice ks is
+  // fixed per lane and the block offset is an instruction immediate
+  constexpr int KS = BK / 32;
+  int aofs[KS], bofs[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const int l = lane & 15, xo = (((ks * 4 + (lane >> 4)) ^ swz(l)) << 4);
+    aofs[ks] = (wm * WTM + l) * (BK * 2) + xo;
+    bofs[ks] = A_BYTES + (wn * WTN + l) * (BK * 2) + xo;
+  }
+  auto load_frags = [&](const char* S, int ks, frag(&fa)[FM], frag(&fb)[FN]) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[i] = *reinterpret_cast<const frag*>(S + aofs[ks] + i * 16 * (BK * 2));
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fb[j] = *reinterpret_cast<const frag*>(S + bofs[ks] + j * 16 * (BK * 2));
+  };
+  // the fragments of k-slice ks+1 are read while the MFMAs of ks run
   auto compute = [&](int buf) {
-    const char* As = smem + buf * STAGE;
-    const char* Bs = As + A_BYTES;
+    const char* S = smem + buf * STAGE;
+    frag fa[2][FM], fb[2][FN];
+    load_frags(S, 0, fa[0], fb[0]);
 #pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
-      const int c = ks * 4 + (lane >> 4);
-      frag fa[FM], fb[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int r = wm * WTM + i * 16 + (lane & 15);
-        fa[i] = *reinterpret_cast<const frag*>(As + r * (BK * 2) + ((c ^ swz(r)) << 4));
-      }
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int r = wn * WTN + j * 16 + (lane & 15);
-        fb[j] = *reinterpret_cast<const frag*>(Bs + r * (BK * 2) + ((c ^ swz(r)) << 4));
-      }
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) load_frags(S, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fb[j], fa[i], acc[i][j]);
+        for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fb[ks & 1][j], fa[ks & 1][i], acc[i][j]);
     }
   };
 
@@ -752,6 +760,9 @@ static const IgCfg kIg16[] = {
     {256, 64, 64, 0, 0, 1, 4, 3},  {128, 64, 64, 0, 0, 1, 2, 3},  {64, 128, 64, 0, 0, 1, 1, 3},
     {256, 128, 64, 0, 0, 1, 2, 2}, {128, 128, 32, 0, 0, 1, 2, 3}, {64, 64, 64, 0, 0, 1, 2, 3},
     {128, 128, 64, 1, 0, 1, 2, 3}, {128, 64, 64, 1, 0, 1, 2, 3},
+    // deeper pipelines (short reduction steps, more in flight)
+    {128, 128, 32, 0, 0, 1, 2, 4}, {128, 64, 32, 0, 0, 1, 2, 4}, {64, 128, 32, 0, 0, 1, 1, 4},
+    {64, 64, 64, 0, 0, 1, 2, 4},   {64, 64, 32, 0, 0, 1, 2, 6},  {256, 64, 32, 0, 0, 1, 4, 4},
     // 3x3 stride-1 patch kernel
     {224, 64, 32, 0, 0, 2, 2, 2, 384}, {224, 64, 32, 0, 0, 2, 2, 1, 384}, {224, 32, 32, 0, 0, 2, 4, 1, 384},
     {112, 64, 32, 0, 0, 2, 1, 2, 320}, {112, 64, 32, 0, 0, 2, 2, 1, 320}, {112, 32, 32, 0, 0, 2, 4, 2, 320},
@@ -848,6 +859,12 @@ static void igemm_dma_cfg(const IgCfg& c, const IgArgs& a, hipStream_t st) {
     IGD(256, 128, 64, 2, 2)
     IGD(128, 128, 32, 2, 3)
     IGD(64, 64, 64, 2, 3)
+    IGD(128, 128, 32, 2, 4)
+    IGD(128, 64, 32, 2, 4)
+    IGD(64, 128, 32, 1, 4)
+    IGD(64, 64, 64, 2, 4)
+    IGD(64, 64, 32, 2, 6)
+    IGD(256, 64, 32, 4, 4)
     default: check(false, "LDS-DMA tile not instantiated");
   }
 #undef IGD
