@@ -132,6 +132,10 @@ def summarize_pmc(fetch_dir, write_dir, routine, ksub, out, calib_mib):
     print(json.dumps(t))
 
 
+def _mask_name(m):
+    return "+".join(n for i, n in enumerate(("NCHW", "NHWC", "NC8HW8")) if m >> i & 1)
+
+
 def _nets():
     from workloads import mobilenet_v2, resnet18, resnet50
     return {"resnet50": resnet50, "resnet18": resnet18, "mobilenetv2": mobilenet_v2}
@@ -222,8 +226,8 @@ def cpu_baseline(spec, t, budget_s):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--batch", type=int, default=32)
     ap.add_argument("--dtype", default="bf16")
     ap.add_argument("--profile-reps", type=int, default=20)
@@ -235,6 +239,8 @@ def main():
                     help="print the measured cost table of the four 3x3 sweep shapes and exit")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-path sweep")
     ap.add_argument("--no-bs1", action="store_true", help="skip the batch-1 measurement")
+    ap.add_argument("--integrated-reps", type=int, default=10,
+                    help="runs per candidate in integrated profiling (0 = keep the DPRS path)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--costs-out", default=None, help="write the measured cost table here")
     ap.add_argument("--costs-in", default=None,
@@ -289,22 +295,45 @@ def main():
     if args.tune_only:
         g.close()
         return
-    ids, model_ns = g.path()
+    dp_ids, dp_model_ns = g.path()
     x = to_dev(t["x"], args.dtype)
     out = g.empty_output()
 
-    sec = time_steps(g, x, out, args.steps, args.warmup)
+    sec_dp = time_steps(g, x, out, args.steps, args.warmup)
+    log(f"[bench] DPRS path: {sec_dp * 1e3:.3f} ms/step, {args.batch / sec_dp:.1f} img/s")
+    # integrated profiling (Sec. III-C): the DPRS candidates and the fixed
+    # paths timed end to end; the library keeps the fastest
+    integ = None
+    t_int = 0.0
+    sec = sec_dp
+    if args.integrated_reps > 0:
+        t2 = time.perf_counter()
+        cands = g.profile_integrated(warmup=2, reps=args.integrated_reps)
+        t_int = time.perf_counter() - t2
+        ids, _ = g.path()
+        pick = next(c for c in cands if c["path"] == ids)
+        label = (f"dprs/{_mask_name(pick['a'])}" if pick["kind"] == "dprs"
+                 else f"fixed/{N.LAYOUT_NAME[pick['a']]}/{N.ALGO_NAME[pick['b']]}")
+        if ids != dp_ids:
+            sec = time_steps(g, x, out, args.steps, args.warmup)
+        integ = {"candidates": len(cands), "selected": label, "seconds": round(t_int, 2),
+                 "measured_ms": {(f"dprs/{_mask_name(c['a'])}" if c["kind"] == "dprs" else
+                                  f"fixed/{N.LAYOUT_NAME[c['a']]}/{N.ALGO_NAME[c['b']]}"):
+                                 round(c["measured_ns"] / 1e6, 4) for c in cands}}
+        log(f"[bench] integrated profiling: {len(cands)} candidates in {t_int:.1f} s, "
+            f"selected {label}: {sec * 1e3:.3f} ms/step")
+    ids, model_ns = g.path()
     value = args.batch / sec
-    log(f"[bench] DP path: {sec * 1e3:.3f} ms/step, {value:.1f} img/s")
 
     # per-layer times over K instrumented steps: each layer's launches are
     # repeated back to back with HIP events tied to the first and last dispatch
     nl = g.num_layers()
     acc = np.zeros(nl)
-    for _ in range(args.steps):
+    passes = min(args.steps, 20)
+    for _ in range(passes):
         _, ms = g.run_timed(x, out, reps=args.timing_reps)
         acc += np.array(ms)
-    layer_ms = acc / args.steps
+    layer_ms = acc / passes
     groups = {}      # (routine, layer type) -> its launches in one step: one kernel symbol each
                      # (the direct routine of an add and of a pool are different kernels)
     cats = {}        # layer category -> totals (for the 3x3 MFMA utilisation)
@@ -357,12 +386,13 @@ def main():
         for lay in LAYOUTS:
             for algo in ALGOS:
                 g.select("fixed", lay, algo)
-                s = time_steps(g, x, out, max(3, args.steps // 2), 2)
+                s = time_steps(g, x, out, args.steps, args.warmup)
                 fixed[f"{lay}/{algo}"] = round(args.batch / s, 2)
                 log(f"[bench] fixed {lay}/{algo}: {args.batch / s:.1f} img/s")
         best_fixed = max(fixed, key=fixed.get)
         g.set_path(ids)
-    dp_vs_fixed = round(value / fixed[best_fixed], 4) if best_fixed else None
+    dp_vs_fixed = round(args.batch / sec_dp / fixed[best_fixed], 4) if best_fixed else None
+    sel_vs_fixed = round(value / fixed[best_fixed], 4) if best_fixed else None
 
     bs1 = None
     if not args.no_bs1 and args.net == "resnet50":
@@ -372,6 +402,8 @@ def main():
         g1.profile(warmup=5, reps=args.profile_reps)
         g1.select("dprs")
         g1.set_option(N.OPT_HIPGRAPH, 1)
+        if args.integrated_reps > 0:
+            g1.profile_integrated(warmup=2, reps=max(args.integrated_reps, 20))
         x1 = to_dev(t1_["x"], args.dtype)
         o1 = g1.empty_output()
         s1 = time_steps(g1, x1, o1, max(args.steps, 50), args.warmup)
@@ -388,13 +420,18 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": args.dtype,
         "data": "synthetic (seeded random input and He-normal weights)",
         "config": {"workload": f"{args.net}-shaped CNN, batch {args.batch}, {args.dtype}, 224x224",
-                   "batch": args.batch, "path": "DPRS-selected routines"},
+                   "batch": args.batch,
+                   "path": ("DPRS candidates + fixed paths, integrated profiling keeps the fastest"
+                            if integ else "DPRS-selected routines")},
         "roofline": roof,
         "cpu_baseline": cpu,
         "img_s_bs1": bs1,
         "conv3x3_mfma_util": round(conv3_util, 4) if conv3_util else None,
-        "dp_vs_best_fixed": dp_vs_fixed, "best_fixed": best_fixed, "fixed_img_s": fixed,
-        "model_time_ms": round(model_ns / 1e6, 4), "tuning_s": round(t_prof + t_sel, 2),
+        "dprs_img_s": round(args.batch / sec_dp, 2),
+        "dp_vs_best_fixed": dp_vs_fixed, "selected_vs_best_fixed": sel_vs_fixed,
+        "best_fixed": best_fixed, "fixed_img_s": fixed, "integrated": integ,
+        "model_time_ms": round(model_ns / 1e6, 4), "dprs_model_time_ms": round(dp_model_ns / 1e6, 4),
+        "tuning_s": round(t_prof + t_sel + t_int, 2),
     }
     sel = {}
     for i in range(1, nl):

@@ -189,6 +189,40 @@ int sn_run(sn_graph* g, const void* d_in, void* d_out, void* hip_stream);
 int sn_run_timed(sn_graph* g, const void* d_in, void* d_out, void* hip_stream, int32_t reps,
                  float* layer_ms, int32_t n);
 
+/* Integrated profiling (Sec. III-C): the unit-profiled table filters the
+ * routine patterns down to a short list of whole paths, and those are timed
+ * end to end, which sees what a sum of isolated layer times misses (cache
+ * reuse between layers, launch gaps).  Candidates, in this order, identical
+ * paths kept once:
+ *   1. the DPRS path over the allowed schemas (SN_OPT_LAYOUTS);
+ *   2. the DPRS path with layers 1..n-1 restricted to each non-empty proper
+ *      subset of those schemas, subsets in increasing bitmask order;
+ *   3. every fixed path (SN_SELECT_FIXED) of an allowed schema and algorithm.
+ * A candidate that does not exist (some layer has no routine in the subset)
+ * is skipped.  Each candidate's plan is compiled and run on a zero-filled
+ * scratch input: warmup runs, then two rounds (candidate order, then
+ * reverse) of reps back-to-back runs between HIP events on the stream; its
+ * measured time is the smaller block mean.  The fastest candidate (the
+ * earlier one on ties) is selected and its plan compiled, as after
+ * sn_select_path.  Synchronous.  reps = 0 only enumerates the candidates
+ * (measured time -1) and leaves the selection unchanged; this works on
+ * host-only graphs.  *n_candidates (may be NULL) receives the count.
+ * Errors: SN_E_STATE (no costs, no layers), SN_E_INVALID (warmup < 0, reps
+ * outside 0..10000), SN_E_DEVICE (reps > 0 on a host-only graph, HIP
+ * error); on an error during timing no path is selected. */
+int sn_profile_integrated(sn_graph* g, int32_t warmup, int32_t reps, void* hip_stream,
+                          int32_t* n_candidates);
+
+/* Candidate idx of the last sn_profile_integrated: routine id per layer
+ * (routine_ids may be NULL; else n = number of layers), model time T(S) under
+ * the unit-profiled table, measured end-to-end ns per run (-1 if not
+ * measured), and kind_ab[3] = {kind, a, b}: kind 0 = DPRS over the schema
+ * bitmask a, kind 1 = fixed path of layout a and algorithm b.  Any output
+ * pointer may be NULL.
+ * Errors: SN_E_INVALID (idx out of range, n mismatch). */
+int sn_integrated_candidate(const sn_graph* g, int32_t idx, int32_t* routine_ids, int32_t n,
+                            int64_t* model_ns, int64_t* measured_ns, int32_t* kind_ab);
+
 /* Cost table as JSON (the profiling data of Sec. IV-A: T(r) per routine,
  * adapt times per edge and schema pair), all times int64 ns, -1 = no
  * routine / unavailable:

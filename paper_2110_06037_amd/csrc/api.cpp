@@ -197,6 +197,43 @@ int sn_run_timed(sn_graph* gp, const void* d_in, void* d_out, void* stream, int3
   });
 }
 
+int sn_profile_integrated(sn_graph* gp, int32_t warmup, int32_t reps, void* stream,
+                          int32_t* n_candidates) {
+  return guarded([&] {
+    CHECK_G(gp);
+    Graph& g = gp->g;
+    if (g.n_layers() < 2) fail(SN_E_STATE, "graph has no layers");
+    if (warmup < 0 || reps < 0 || reps > 10000)
+      fail(SN_E_INVALID, "warmup >= 0 and reps in 0..10000 required");
+    if (reps > 0 && g.host_only()) fail(SN_E_DEVICE, "host-only graph cannot run candidates");
+    std::vector<Candidate> c = integrated_candidates(g);
+    if (reps > 0) integrated_measure(g, c, warmup, reps, stream);
+    g.candidates = std::move(c);
+    if (n_candidates) *n_candidates = (int32_t)g.candidates.size();
+  });
+}
+
+int sn_integrated_candidate(const sn_graph* gp, int32_t idx, int32_t* routine_ids, int32_t n,
+                            int64_t* model_ns, int64_t* measured_ns, int32_t* kind_ab) {
+  return guarded([&] {
+    CHECK_G(gp);
+    const Graph& g = gp->g;
+    if (idx < 0 || idx >= (int32_t)g.candidates.size()) fail(SN_E_INVALID, "candidate index out of range");
+    const Candidate& c = g.candidates[idx];
+    if (routine_ids) {
+      if (n != g.n_layers()) fail(SN_E_INVALID, "routine_ids must have one entry per layer");
+      for (int i = 0; i < n; ++i) routine_ids[i] = c.path[i];
+    }
+    if (model_ns) *model_ns = c.model_ns;
+    if (measured_ns) *measured_ns = c.measured_ns;
+    if (kind_ab) {
+      kind_ab[0] = c.kind;
+      kind_ab[1] = c.a;
+      kind_ab[2] = c.b;
+    }
+  });
+}
+
 int sn_get_costs(const sn_graph* gp, char* json, size_t cap, size_t* len) {
   return guarded([&] {
     CHECK_G(gp);

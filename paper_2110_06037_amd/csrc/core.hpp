@@ -85,6 +85,15 @@ struct DPLayerStats {
   int64_t candidates = 0;  // candidate unions per state (|Lambda|^|H|)
 };
 
+// One routine path timed end to end by integrated profiling.
+struct Candidate {
+  std::vector<int> path;
+  int64_t model_ns = -1;     // T(S) under the unit-profiled table
+  int64_t measured_ns = -1;  // end-to-end time per run, -1 = not measured
+  int kind = 0;              // 0: DPRS over the layouts in mask a; 1: fixed (layout a, algo b)
+  int a = 0, b = 0;
+};
+
 struct Graph {
   int dtype = SN_F32;
   int device = -1;
@@ -97,6 +106,7 @@ struct Graph {
   std::vector<int> path;      // routine index per layer; empty = none
   int64_t path_cost = -1;
   std::vector<DPLayerStats> dp_stats;
+  std::vector<Candidate> candidates;  // last integrated profiling
   std::unique_ptr<Plan> plan;
   std::unique_ptr<DevState> dev;
   bool host_only() const { return device < 0; }
@@ -116,7 +126,11 @@ bool winograd_applicable(const Layer& L, const Shape& in);
 std::string routine_name(const Layer& L, const Routine& r);
 
 // select.cpp
-void select_dprs(Graph& g);
+void select_dprs(Graph& g, int layout_mask = -1);
+// integrated profiling's candidate paths (Sec. III-C): DPRS over every
+// non-empty subset of the allowed layouts, then every fixed path; identical
+// paths kept once; g.path is left unchanged
+std::vector<Candidate> integrated_candidates(Graph& g);
 void select_fixed(Graph& g, int layout, int algo);
 void set_path(Graph& g, const int32_t* ids, int n);
 int64_t path_total(const Graph& g, const std::vector<int>& path);
@@ -134,5 +148,8 @@ void plan_compile(Graph& g);
 void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms = nullptr,
               int reps = 1);
 void plan_destroy(Graph& g);
+// times every candidate end to end and selects the fastest (compiles its plan)
+void integrated_measure(Graph& g, std::vector<Candidate>& cands, int warmup, int reps,
+                        void* stream);
 
 }  // namespace sn

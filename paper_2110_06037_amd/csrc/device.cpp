@@ -648,4 +648,69 @@ void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* laye
   HIPCHK(hipStreamWaitEvent(st, P.gev[1], 0));
 }
 
+// ------------------------------------------------------------------ integrated profiling
+// Every candidate path is compiled and run end to end on scratch tensors
+// (zero-filled input): warmup runs, then two rounds (candidate order, then
+// reverse order, so slow drift does not favour one end of the list) of reps
+// back-to-back runs between HIP events; a candidate's time is the smaller of
+// its two block means.  The fastest candidate (earliest on ties) is selected.
+void integrated_measure(Graph& g, std::vector<Candidate>& cands, int warmup, int reps,
+                        void* stream) {
+  if (cands.empty()) fail(SN_E_INTERNAL, "no candidate paths");
+  HIPCHK(hipSetDevice(g.device));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int es = dtype_size(g.dtype);
+  const size_t in_bytes = (size_t)g.in.numel() * es;
+  const size_t out_bytes = (size_t)g.layers.back().out.numel() * es;
+  void* din = nullptr;
+  void* dout = nullptr;
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  const std::vector<int> saved = g.path;
+  const int64_t saved_cost = g.path_cost;
+  auto cleanup = [&] {
+    for (auto& e : ev)
+      if (e) (void)hipEventDestroy(e);
+    if (din) (void)hipFree(din);
+    if (dout) (void)hipFree(dout);
+  };
+  try {
+    HIPCHK(hipMalloc(&din, std::max<size_t>(in_bytes, 256)));
+    HIPCHK(hipMalloc(&dout, std::max<size_t>(out_bytes, 256)));
+    HIPCHK(hipMemsetAsync(din, 0, in_bytes, st));
+    for (auto& e : ev) HIPCHK(hipEventCreate(&e));
+    for (Candidate& c : cands) c.measured_ns = -1;
+    const int nc = (int)cands.size();
+    for (int round = 0; round < 2; ++round) {
+      for (int q = 0; q < nc; ++q) {
+        Candidate& c = cands[round == 0 ? q : nc - 1 - q];
+        g.path = c.path;
+        g.path_cost = c.model_ns;
+        plan_compile(g);
+        for (int w = 0; w < warmup; ++w) plan_run(g, din, dout, st);
+        HIPCHK(hipEventRecord(ev[0], st));
+        for (int r = 0; r < reps; ++r) plan_run(g, din, dout, st);
+        HIPCHK(hipEventRecord(ev[1], st));
+        HIPCHK(hipEventSynchronize(ev[1]));
+        float ms = 0.f;
+        HIPCHK(hipEventElapsedTime(&ms, ev[0], ev[1]));
+        const int64_t ns = std::max<int64_t>(1, (int64_t)((double)ms * 1e6 / reps + 0.5));
+        if (c.measured_ns < 0 || ns < c.measured_ns) c.measured_ns = ns;
+      }
+    }
+    int best = 0;
+    for (int q = 1; q < nc; ++q)
+      if (cands[q].measured_ns < cands[best].measured_ns) best = q;
+    g.path = cands[best].path;
+    g.path_cost = cands[best].model_ns;
+    plan_compile(g);
+  } catch (...) {
+    cleanup();
+    g.path = saved;
+    g.path_cost = saved_cost;
+    plan_destroy(g);
+    throw;
+  }
+  cleanup();
+}
+
 }  // namespace sn

@@ -48,7 +48,9 @@ struct Problem {
   std::vector<E> edges;
 };
 
-Problem make_problem(const Graph& g) {
+// layout_mask restricts the routines of layers 1..n-1 to those layouts
+// (the auxiliary layers keep their NCHW routine)
+Problem make_problem(const Graph& g, int layout_mask = -1) {
   Problem P;
   int n = g.n_layers();
   P.L = n + 1;
@@ -62,6 +64,7 @@ Problem make_problem(const Graph& g) {
     const Layer& L = g.layers[i];
     for (size_t r = 0; r < L.routines.size(); ++r) {
       int64_t c = L.cost[r];
+      if (i > 0 && !(layout_mask >> L.routines[r].layout & 1)) c = -1;
       P.cost[i].push_back(c < 0 ? kInf : c);
       P.schema[i].push_back(P.schema_of_layout[L.routines[r].layout]);
     }
@@ -141,9 +144,9 @@ int64_t ipow(int64_t b, int e) {
 
 }  // namespace
 
-void select_dprs(Graph& g) {
+void select_dprs(Graph& g, int layout_mask) {
   if (!g.have_costs) fail(SN_E_STATE, "no cost table: call sn_profile or sn_set_costs first");
-  Problem P = make_problem(g);
+  Problem P = make_problem(g, layout_mask);
   const int L = P.L, S = P.S;
 
   // post-dominator sets on the 1-in-1-out DAG (the output post-dominates all)
@@ -339,6 +342,60 @@ void select_fixed(Graph& g, int layout, int algo) {
   }
   g.path = path;
   g.path_cost = g.have_costs ? path_total(g, path) : -1;
+}
+
+std::vector<Candidate> integrated_candidates(Graph& g) {
+  if (!g.have_costs) fail(SN_E_STATE, "no cost table: call sn_profile or sn_set_costs first");
+  const std::vector<int> saved = g.path;
+  const int64_t saved_cost = g.path_cost;
+  std::vector<Candidate> out;
+  auto add = [&](int kind, int a, int b) {
+    for (const Candidate& c : out)
+      if (c.path == g.path) return;
+    Candidate c;
+    c.path = g.path;
+    c.model_ns = g.path_cost;
+    c.kind = kind;
+    c.a = a;
+    c.b = b;
+    out.push_back(std::move(c));
+  };
+  // the schemas the DP may use; subsets in increasing mask order, the full set first
+  const int full = (int)(g.opt_layouts & ((1 << SN_NUM_LAYOUTS) - 1));
+  std::vector<int> masks{full};
+  for (int m = 1; m < full; ++m)
+    if ((m & full) == m) masks.push_back(m);
+  try {
+    for (int m : masks) {
+      try {
+        select_dprs(g, m);
+      } catch (const Error& e) {
+        if (e.code != SN_E_UNSUPPORTED) throw;
+        continue;  // some layer has no routine in these layouts
+      }
+      add(0, m, 0);
+    }
+    for (int l = 0; l < SN_NUM_LAYOUTS; ++l) {
+      if (!(full >> l & 1)) continue;
+      for (int a = 0; a < SN_NUM_ALGOS; ++a) {
+        if (!(g.opt_algos >> a & 1)) continue;
+        try {
+          select_fixed(g, l, a);
+        } catch (const Error& e) {
+          if (e.code != SN_E_UNSUPPORTED) throw;
+          continue;
+        }
+        add(1, l, a);
+      }
+    }
+  } catch (...) {
+    g.path = saved;
+    g.path_cost = saved_cost;
+    throw;
+  }
+  g.path = saved;
+  g.path_cost = saved_cost;
+  return out;
 }
 
 void set_path(Graph& g, const int32_t* ids, int n) {

@@ -146,6 +146,25 @@ class Graph:
             alg = N.ALGO[algo] if isinstance(algo, str) else algo
             N.check(self.lib.sn_select_path(self._g, N.SELECT_FIXED, lay, alg))
 
+    def profile_integrated(self, warmup=3, reps=10, stream=None):
+        """Integrated profiling (Sec. III-C): time the candidate paths end to
+        end and select the fastest; reps=0 only lists the candidates.
+        Returns the candidates as dicts (path, model_ns, measured_ns, kind, a, b)."""
+        n = ctypes.c_int32()
+        sp = _stream_ptr(stream) if reps > 0 and self.device >= 0 else ctypes.c_void_p(0)
+        N.check(self.lib.sn_profile_integrated(self._g, warmup, reps, sp, ctypes.byref(n)))
+        nl = self.num_layers()
+        out = []
+        for i in range(n.value):
+            ids = (ctypes.c_int32 * nl)()
+            mo, me = ctypes.c_int64(), ctypes.c_int64()
+            kab = (ctypes.c_int32 * 3)()
+            N.check(self.lib.sn_integrated_candidate(self._g, i, ids, nl, ctypes.byref(mo),
+                                                     ctypes.byref(me), kab))
+            out.append({"path": list(ids), "model_ns": mo.value, "measured_ns": me.value,
+                        "kind": "dprs" if kab[0] == 0 else "fixed", "a": kab[1], "b": kab[2]})
+        return out
+
     def set_path(self, ids):
         arr = (ctypes.c_int32 * len(ids))(*ids)
         N.check(self.lib.sn_set_path(self._g, arr, len(ids)))

@@ -306,3 +306,67 @@ def test_dangling_layer_is_rejected():
     costs = randomise(g.costs(), 1)
     g.set_costs(costs)
     assert status_of(g.select) == -1
+
+
+# ------------------------------------------------------------------ integrated profiling candidates
+
+def _restricted(problem, mask):
+    """The problem with the routines of layers 1..L-2 limited to the layouts in mask."""
+    rts = [list(r) for r in problem["routines"]]
+    for i in range(1, len(rts) - 1):
+        rts[i] = [(rid, lay, ns if (mask >> lay) & 1 else None) for rid, lay, ns in rts[i]]
+    return dict(problem, routines=rts)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_integrated_candidates_are_restricted_optima_and_fixed_paths(seed):
+    # Sec. III-C: unit profiling filters the routine patterns that integrated
+    # profiling times; every candidate is an exact optimum of the unit-profiled
+    # model within its restriction, checked by exhaustive enumeration
+    L, E = random_dag(5, seed)
+    g = graph_from_edges(L, E, layouts=("NCHW", "NHWC", "NC8HW8"))
+    costs = randomise(g.costs(), 900 + seed, max_cost=6, p_missing=0.15)
+    g.set_costs(costs)
+    g.select("dprs")
+    before = g.path()
+    cands = g.profile_integrated(reps=0)
+    assert g.path() == before, "enumeration must not change the selection"
+    paths = [tuple(c["path"]) for c in cands]
+    assert len(set(paths)) == len(paths), "identical paths are kept once"
+    assert cands[0]["kind"] == "dprs" and cands[0]["a"] == 7
+    assert tuple(cands[0]["path"]) == tuple(before[0]) and cands[0]["model_ns"] == before[1]
+    problem = problem_from_costs(costs)
+    seen_masks = []
+    for c in cands:
+        assert c["measured_ns"] == -1
+        if c["kind"] == "dprs":
+            seen_masks.append(c["a"])
+            t, tup, _ = exhaustive(_restricted(problem, c["a"]))
+            assert (tuple(c["path"]) + (0,), c["model_ns"]) == (tup, t)
+        else:
+            g.select("fixed", c["a"], c["b"])
+            assert tuple(c["path"]) == tuple(g.path()[0])
+    assert seen_masks[0] == 7 and seen_masks[1:] == sorted(seen_masks[1:])
+    # every subset whose restricted optimum exists and differs from the earlier candidates appears
+    for m in range(1, 7):
+        t, tup, _ = exhaustive(_restricted(problem, m))
+        if t is not None:
+            assert tup[:-1] in paths
+    for lay in range(3):
+        for algo in range(2):
+            try:
+                g.select("fixed", lay, algo)
+            except N.SNError:
+                continue
+            assert tuple(g.path()[0]) in paths
+
+
+def test_integrated_profiling_needs_costs_and_a_device():
+    g = graph_from_edges(3, [(0, 1), (1, 2)])
+    with pytest.raises(N.SNError, match="SN_E_STATE"):
+        g.profile_integrated(reps=0)
+    g.set_costs(randomise(g.costs(), 1))
+    with pytest.raises(N.SNError, match="SN_E_DEVICE"):
+        g.profile_integrated(reps=5)
+    with pytest.raises(N.SNError, match="SN_E_INVALID"):
+        g.profile_integrated(warmup=-1, reps=0)

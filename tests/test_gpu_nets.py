@@ -67,6 +67,27 @@ def test_tiny_chain_measured_table_dp_equals_exhaustive_and_parity():
             assert err(out, ref, "f32") <= TOL["f32"], (lay, algo)
 
 
+@pytest.mark.parametrize("name", ["tiny", "mobilenetv2"])
+def test_integrated_profiling_selects_the_measured_fastest_candidate(name):
+    spec = tiny_chain() if name == "tiny" else mobilenet_v2(1)
+    t = generate(spec)
+    g = build_from_spec(spec, t)
+    g.profile(warmup=2, reps=5)
+    g.select("dprs")
+    dp_ids, dp_t = g.path()
+    cands = g.profile_integrated(warmup=2, reps=5)
+    print(name, [(c["kind"], c["a"], c["b"], c["model_ns"], c["measured_ns"]) for c in cands],
+          flush=True)
+    assert cands[0]["kind"] == "dprs" and cands[0]["path"] == dp_ids and cands[0]["model_ns"] == dp_t
+    assert all(c["measured_ns"] > 0 for c in cands)
+    best = min(range(len(cands)), key=lambda i: (cands[i]["measured_ns"], i))
+    ids, total = g.path()
+    assert ids == cands[best]["path"] and total == cands[best]["model_ns"]
+    out, _ = run_out(g, spec, t)
+    assert err(out, oracle_out(spec, t), spec["dtype"]) <= TOL[spec["dtype"]]
+    g.close()
+
+
 @pytest.mark.parametrize("name", ["resnet18", "mobilenetv2", "resnet50_bf16", "resnet50_f16"])
 def test_net_dp_and_fixed_paths_match_oracle(name):
     spec = {"resnet18": lambda: resnet18(1), "mobilenetv2": lambda: mobilenet_v2(1),
