@@ -239,7 +239,7 @@ def main():
                     help="print the measured cost table of the four 3x3 sweep shapes and exit")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-path sweep")
     ap.add_argument("--no-bs1", action="store_true", help="skip the batch-1 measurement")
-    ap.add_argument("--integrated-reps", type=int, default=10,
+    ap.add_argument("--integrated-reps", type=int, default=20,
                     help="runs per candidate in integrated profiling (0 = keep the DPRS path)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--costs-out", default=None, help="write the measured cost table here")

@@ -747,7 +747,8 @@ struct IgCfg {
   int dma = 0, wm = 2, st = 2;  // 1: LDS-DMA kernel, 2: 3x3 patch kernel (bm = 16 * row blocks),
                                 // 3: small-channel kernel;
                                 // wave rows WM (of 4 waves), LDS stages ST
-  int ppx = 0;                  // patch kernel: patch capacity in pixels
+  int ppx = 0;                  // small-channel kernel: patch capacity in pixels
+  PatchCfg pc{};                // patch kernel tile
 };
 static const IgCfg kIg16[] = {
     {64, 64, 32, 0, 2},   {128, 128, 64, 0, 2}, {256, 128, 32, 0, 2}, {128, 64, 64, 0, 2},
@@ -764,8 +765,10 @@ static const IgCfg kIg16[] = {
     {128, 128, 32, 0, 0, 1, 2, 4}, {128, 64, 32, 0, 0, 1, 2, 4}, {64, 128, 32, 0, 0, 1, 1, 4},
     {64, 64, 64, 0, 0, 1, 2, 4},   {64, 64, 32, 0, 0, 1, 2, 6},  {256, 64, 32, 0, 0, 1, 4, 4},
     // 3x3 stride-1 patch kernel
-    {224, 64, 32, 0, 0, 2, 2, 2, 384}, {224, 64, 32, 0, 0, 2, 2, 1, 384}, {224, 32, 32, 0, 0, 2, 4, 1, 384},
-    {112, 64, 32, 0, 0, 2, 1, 2, 320}, {112, 64, 32, 0, 0, 2, 2, 1, 320}, {112, 32, 32, 0, 0, 2, 4, 2, 320},
+#define SN_PATCH_IG(FMT, BN, PWT, WM, WN, TG, ST, PROWS) \
+  {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS}},
+    PATCH_CONFIGS(SN_PATCH_IG)
+#undef SN_PATCH_IG
     // small-channel (stem) kernel: NHWC, C <= 4, stride 2
     {112, 64, 32, 0, 0, 3, 2, 1, 1664}, {224, 64, 32, 0, 0, 3, 2, 1, 2112}};
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
@@ -781,7 +784,7 @@ bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, in
   if (param < 0 || param >= igemm_num_params(dtype)) return false;
   const IgCfg& g = dtype == 0 ? kIg32[param] : kIg16[param];
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
-  if (g.dma == 2) return patch_applicable(layout, c, h, w, r, s, stride, pad, n, g.bm / 16, g.bn, g.bk, g.ppx);
+  if (g.dma == 2) return patch_applicable(layout, c, h, w, r, s, stride, pad, n, g.pc.fmt, g.pc.pwt, g.pc.prows);
   if (g.dma == 3) return smallc_applicable(layout, c, h, w, r, s, stride, pad, n, g.bm / 16, g.ppx, 28);
   if (g.dma) {
     // fp32 index division and 32-bit byte offsets bound the output size
@@ -995,7 +998,7 @@ template <typename T>
 static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t st) {
   const IgCfg cfg = ig_cfg(dtype, param);
   if (cfg.dma == 2) {
-    conv_patch(dtype, cfg.bm / 16, cfg.bn, cfg.bk, cfg.wm, cfg.st, cfg.ppx, c, st);
+    conv_patch(dtype, cfg.pc, c, st);
     return;
   }
   if (cfg.dma == 3) {

@@ -3,29 +3,35 @@
 //
 // A workgroup computes the outputs of TI whole images, or of TR consecutive
 // output rows of one image (all Q columns), for BN output channels.  For
-// every step of BK input channels it loads the tile's input patch -- the
+// every step of 32 input channels it loads the tile's input patch -- the
 // (TR + 2) x (Q + 2) input pixels (one halo pixel on each side; the zero
 // padding comes from out-of-range buffer offsets) -- and the filter taps of
 // those channels for all 9 taps, then runs the 9 taps' MFMAs out of LDS: tap
 // (r, s) of output pixel (p, q) is patch pixel (p + r, q + s), so the per-tap
 // operand rows are the same patch rows shifted by the uniform offset
-// r * (Q + 2) + s.  Each input element therefore crosses the memory system
-// about (TR + 2) / TR times per workgroup instead of 9 times, which is what
-// bounds the per-tap (im2col) implicit GEMM on this chip.
+// r * PW + s (PW = the patch row pitch).  Each input element therefore
+// crosses the memory system about (TR + 2) / TR times per workgroup instead
+// of 9 times, which is what bounds the per-tap (im2col) implicit GEMM.
 //
 // Tiles move from global memory into LDS with direct loads (16 bytes per
-// lane, 1 KB per wave instruction in lane order).  LDS rows are padded by one
-// 16-byte chunk (the lanes that land on a pad chunk load zeros), so 16
-// consecutive rows of one chunk hit distinct banks and every operand address
-// is a per-lane base plus compile-time offsets: tap (r, s) adds r row-strides
-// of the patch (one add per row block and r) and s padded rows (an
-// instruction immediate).  The MFMA takes the filter as its first operand, so
-// each lane's 4 accumulators are 4 consecutive output channels of one
-// pixel; the epilogue adds the bias, applies the activation and stores
-// through LDS as 16-byte rows.
+// lane, 1 KB per wave instruction in lane order) through ST stages, so up to
+// ST - 1 channel steps are in flight while one is computed.  An LDS row holds
+// the 32 channels of one pixel (64 bytes); 16-byte chunk c of row r sits at
+// chunk c ^ ((r >> 2) & 3), so 16 rows that are distinct modulo 16 hit 16
+// distinct bank groups.  An MFMA operand reads 16 consecutive pixels of the
+// tile; with the row pitch PW = Q (mod 16) and the image pitch IP = P * Q
+// (mod 16) the patch row of pixel m is m plus a constant modulo 16, so every
+// operand read of every tap is free of bank conflicts ("conflict-free
+// pitch").  The dense pitch (PW = Q + 2, IP = PH * PW) loads fewer rows and
+// accepts some conflicts; both are routine parameters.  The MFMA takes the
+// filter as its first operand, so each lane's 4 accumulators are 4
+// consecutive output channels of one pixel; the epilogue adds the bias,
+// applies the activation and stores through LDS as 16-byte rows.
 #include "gemm_common.hpp"
 #include "kcommon.hpp"
 #include "launch.hpp"
+
+#include <type_traits>
 
 namespace sn {
 namespace k {
@@ -39,49 +45,56 @@ struct PatchArgs {
   int K, P, Q, Ks, Ng;
   int act;
   int CB, C8, Kred;      // channel blocks of 8, padded channels, weight row length 9 * C8
-  int TI, TR, PH, PW;    // images / output rows per tile, patch rows / columns per image
+  int TI, TR, PH, PW;    // images / output rows per tile, patch rows, patch row pitch
+  int IP;                // patch image pitch (rows of LDS per image)
   int tiles_img;         // row tiles per image
   int tiles_m, tiles_n;
-  FastDiv fd_ti_tiles;                    // division by tiles_img
-  float inv_pw, inv_ph, inv_trq, inv_q;   // 1/PW, 1/PH, 1/(TR*Q), 1/Q for sdiv
+  FastDiv fd_ti_tiles;   // division by tiles_img
+  float inv_pw, inv_ip, inv_trq, inv_q;   // 1/PW, 1/IP, 1/(TR*Q), 1/Q for sdiv
   int HW8, W8;                            // NC8HW8 strides: H*W*8, W*8
-  int lpw;                                // log2 of the patch row pitch PW
   float inv_pq;                           // 1/(P*Q) for sdiv
   long long y_elems;
   long long x_elems, w_elems;
 };
 
-// FMT: MFMA row blocks (16 pixels) per tile; BN output channels; BK input
-// channels per step; WM wave rows (of 4 waves); ST LDS stages; PPX patch
-// capacity in pixels.
-template <typename T, int L, int FMT, int BN, int BK, int WM, int ST, int PPX, int OCC>
-__global__ __launch_bounds__(256, OCC) void conv3x3_patch_kernel(PatchArgs a) {
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+// FMT: MFMA row blocks (16 pixels) per tile; BN output channels; PWT patch
+// row pitch (a power of two >= Q + 2); the 8 waves form TG tap groups of
+// WM x WN waves (group g runs taps [9g/TG, 9(g+1)/TG) of every step on the
+// whole tile; the groups' sums meet in LDS at the end); ST LDS stages;
+// PROWS patch rows per stage.
+template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS>
+__global__ __launch_bounds__(512, 1) void conv3x3_patch_kernel(PatchArgs a) {
   static_assert(sizeof(T) == 2 && L != NCHW, "16-bit channel-vector layouts only");
-  static_assert(BK == 32, "one 16x16x32 MFMA k-slice per step");
-  static_assert(BN == 32 || BN == 64, "filter rows per load round must be whole taps");
-  constexpr int WN = 4 / WM;
-  constexpr int CPR = BK / 8;     // 16-byte chunks per 64-byte LDS row
-  constexpr int RB = BK * 2;      // bytes per LDS row
-  constexpr int PROWS = (PPX + 63) / 64 * 64;           // patch rows (whole load rounds)
-  constexpr int WROWS = (9 * BN + 63) / 64 * 64;        // filter rows
-  constexpr int NP = PROWS / 64, NW = WROWS / 64;       // load instructions per wave and step
-  static_assert(ST == 1 || ST == 2, "one or two LDS stages");
-  constexpr int FMW = (FMT + WM - 1) / WM;  // row blocks per wave
+  constexpr int NWV = 8;
+  static_assert(WM * WN * TG == NWV, "8 waves");
+  static_assert(PWT == 16 || PWT == 32 || PWT == 64, "patch pitch: a multiple of 16 rows");
+  constexpr int LPW = PWT == 16 ? 4 : PWT == 32 ? 5 : 6;
+  constexpr int BK = 32, RB = 64;                    // channels per step, bytes per LDS row
+  constexpr int FMW = (FMT + WM - 1) / WM;           // row blocks per wave
   constexpr int WTN = BN / WN, FNW = WTN / 16;
-  static_assert(FNW * 16 * WN == BN, "BN must split over the wave columns");
-  constexpr int P_BYTES = PROWS * RB, STAGE = (PROWS + WROWS) * RB;
-  constexpr int CPAD = 8;
-  constexpr int SM_C = FMT * 16 * (BN + CPAD) * 2;
-  constexpr int SM = ST * STAGE > SM_C ? ST * STAGE : SM_C;
+  static_assert(FNW >= 1 && FNW * 16 * WN == BN, "BN must split over the wave columns");
+  static_assert(PROWS % 16 == 0, "patch rows in whole 16-row loads");
+  constexpr int WR = 9 * BN;                         // filter rows
+  constexpr int NINS = (PROWS + WR + 15) / 16;       // 16-row load instructions per stage
+  constexpr int NL = (NINS + NWV - 1) / NWV;         // per wave
+  constexpr int STAGE = NL * NWV * 16 * RB;
+  static_assert(ST >= 2 && ST <= 4, "two to four LDS stages");
+  constexpr int RPITCH = BN * 4 + 16;                // partial-sum row pitch (bytes)
+  constexpr int RED = TG > 1 ? FMT * 16 * RPITCH : 0;
+  constexpr int SM = ST * STAGE > RED ? ST * STAGE : RED;
+  static_assert(SM <= 160 * 1024, "LDS capacity");
   __shared__ __attribute__((aligned(1024))) char smem[SM];
   lds_char* const sl = (lds_char*)smem;
-  // 16-byte chunk c of LDS row r sits at chunk c ^ swz(r): any 16 consecutive
-  // rows of one chunk then cover all 16 chunk positions of a 256-byte bank line
   auto swz = [](int row) { return (row >> 2) & 3; };
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
-  const int wm = wave / WN, wn = wave % WN;
+  const int grp = wave / (WM * WN), wig = wave % (WM * WN);
+  const int wm = wig / WN, wn = wig % WN;
+  const int blk0 = wm * FMW;
   int mt, nt;
   tile_of(blockIdx.x, a.tiles_m, a.tiles_n, mt, nt);
   const int ig = fdiv(mt, a.fd_ti_tiles), rt = mt - ig * a.tiles_img;
@@ -90,179 +103,213 @@ __global__ __launch_bounds__(256, OCC) void conv3x3_patch_kernel(PatchArgs a) {
   const int imgs = min(a.TI, a.N - img0);
   const int rows = min(a.TR, a.P - row0);
   const int n0 = nt * BN;
-  const int KT = a.CB / CPR;
+  const int KT = a.CB / 4;
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_elems * 2);
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, a.w_elems * 2);
-
-  // Patch rows are (image, ph, pw) with a row pitch PW (a multiple of 16
-  // that divides 64, at least Q + 2; columns past Q + 2 load zeros).  Load
-  // instruction q = wave + 4 i fills LDS rows [16 q, 16 q + 16): this lane
-  // fills row 16 q + lane / 4, physical chunk lane % 4 (logical chunk
-  // (lane % 4) ^ swz(row)).  Consecutive i add 64 rows, i.e. 64 / PW patch
-  // rows at the same column.  (Index arithmetic: 24-bit multiplies and fp32
-  // division; every value is far below 2^24.)
-  const int r0 = wave * 16 + (lane >> 2);
-  const int pw = r0 & (a.PW - 1), ww = pw - 1;
-  const int prow0 = r0 >> a.lpw;
-  const int lcp = (lane & 3) ^ swz(r0);  // row + 64 i keeps swz
-  unsigned poff[NP];
-#pragma unroll
-  for (int i = 0; i < NP; ++i) {
-    const int prow = prow0 + (i << (6 - a.lpw));
-    const int ii = sdiv(prow, a.inv_ph), ph = prow - __umul24(ii, a.PH);
-    const int img = img0 + ii, h = row0 - 1 + ph;
-    const bool ok = ii < a.TI && img < a.N && (unsigned)h < (unsigned)a.H && (unsigned)ww < (unsigned)a.W;
-    unsigned e;
-    if constexpr (L == NC8)
-      e = __umul24(__umul24(img, a.CB) + lcp, a.HW8) + __umul24(h, a.W8) + ww * 8;
-    else
-      e = __umul24(__umul24(__umul24(img, a.H) + h, a.W) + ww, a.Cs) + lcp * 8;
-    poff[i] = ok ? e * 2u : kOOB;
-  }
-  // filter rows (tap, channel): + 64 rows = + 64 / BN taps, same channel
-  const int tap0 = r0 / BN, kch = n0 + r0 % BN;
-  const unsigned wof0 = (__umul24(kch, a.Kred) + __umul24(tap0, a.C8) + lcp * 8) * 2u;
-  unsigned woff[NW];
-#pragma unroll
-  for (int i = 0; i < NW; ++i) {
-    const int tap = tap0 + i * (64 / BN);
-    woff[i] = tap < 9 && kch < a.Ng ? wof0 + (unsigned)(i * (64 / BN)) * (unsigned)a.C8 * 2u : kOOB;
-  }
-  // per-step uniform offsets of channel block kt * CPR
-  const int xstep = L == NC8 ? CPR * a.HW8 * 2 : BK * 2;
-  auto issue = [&](int buf, int kt) {
-    lds_char* base = sl + buf * STAGE + wave * 1024;
-#pragma unroll
-    for (int i = 0; i < NP; ++i) dma16(rx, base + i * 4096, poff[i], kt * xstep);
-#pragma unroll
-    for (int i = 0; i < NW; ++i) dma16(rw, base + P_BYTES + i * 4096, woff[i], kt * BK * 2);
-  };
-  issue(0, 0);  // the first step's tiles travel while the offsets below are computed
-
-  // accumulators start at the bias of the lane's output channels
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.bias, (long long)a.Ng * 4);
-  typedef typename Mfma<T>::frag frag;
-  f32x4 acc[FMW][FNW];
+
+  // bias of the lane's output channels (tap group 0 starts its sums there)
+  float bias[FNW][4];
 #pragma unroll
   for (int j = 0; j < FNW; ++j) {
     const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
-    f32x4 b;
 #pragma unroll
-    for (int v = 0; v < 4; ++v) b[v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n + v) * 4, 0, 0));
-#pragma unroll
-    for (int i = 0; i < FMW; ++i) acc[i][j] = b;
+    for (int v = 0; v < 4; ++v)
+      bias[j][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n + v) * 4, 0, 0));
   }
 
-  // LDS byte offsets (within a stage) of this lane's operand chunks for every
-  // tap: the three column taps of a pixel row block computed, the tap rows
-  // one pitch apart (a multiple of 16 rows, so the swizzle is unchanged)
-  int aoff[FMW][9];
-  const int rowpitch = a.PW * RB;
+  // A stage holds PROWS patch rows (image ii at ii * IP, patch row ph at
+  // + ph * PWT, column pw; pitch padding loads zeros), then the 9 * BN
+  // filter rows (tap, output channel), then rows no load fills.  Load
+  // instruction q = wave + 8 i fills stage rows [16 q, 16 q + 16): this lane
+  // fills row 16 q + lane / 4, physical chunk lane % 4 (logical chunk
+  // (lane % 4) ^ swz(row)).  (Index arithmetic: 24-bit multiplies and fp32
+  // division; every value is far below 2^21.)
+  unsigned loff[NL];
+  const int lrow = lane >> 2;
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int q = wave + NWV * i;
+    const int row = 16 * q + lrow;
+    const int lcp = (lane & 3) ^ swz(row);
+    unsigned off = kOOB;
+    if (16 * q < PROWS) {
+      const int ii = sdiv(row, a.inv_ip), rem = row - __umul24(ii, a.IP);
+      const int ph = rem >> LPW, pw = rem & (PWT - 1);
+      const int img = img0 + ii, h = row0 - 1 + ph, ww = pw - 1;
+      const bool ok = ii < a.TI && img < a.N && ph < a.PH && (unsigned)h < (unsigned)a.H &&
+                      (unsigned)ww < (unsigned)a.W;
+      unsigned e;
+      if constexpr (L == NC8)
+        e = __umul24(__umul24(img, a.CB) + lcp, a.HW8) + __umul24(h, a.W8) + ww * 8;
+      else
+        e = __umul24(__umul24(__umul24(img, a.H) + h, a.W) + ww, a.Cs) + lcp * 8;
+      if (ok) off = e * 2u;
+    } else if (16 * q < PROWS + WR) {
+      const int fr = row - PROWS, tap = fr / BN, kch = n0 + fr % BN;
+      if (kch < a.Ng) off = (__umul24(kch, a.Kred) + __umul24(tap, a.C8) + lcp * 8) * 2u;
+    }
+    loff[i] = off;
+  }
+  const int xstep = L == NC8 ? 4 * a.HW8 * 2 : BK * 2;
+  auto issue = [&](auto SC, int kt) {
+    constexpr int SI = decltype(SC)::value;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int q = wave + NWV * i;
+      const bool patch = 16 * q < PROWS;
+      dma16(patch ? rx : rw, sl + SI * STAGE + q * 1024, loff[i], kt * (patch ? xstep : BK * 2));
+    }
+  };
+  issue(IC<0>{}, 0);
+  if constexpr (ST > 2) {
+    if (1 < KT) issue(IC<1>{}, 1);
+  }
+  if constexpr (ST > 3) {
+    if (2 < KT) issue(IC<2>{}, 2);
+  }
+
+  // LDS byte offsets of this lane's operand chunk for the three column taps
+  // of each row block; tap (r, s) adds r * PWT rows (a multiple of 16, so the
+  // swizzle is unchanged) as an instruction immediate
+  int aoff[FMW][3];
 #pragma unroll
   for (int i = 0; i < FMW; ++i) {
-    const int m = (wm * FMW + i) * 16 + (lane & 15);
+    const int m = (blk0 + i) * 16 + (lane & 15);
     const int ii = sdiv(m, a.inv_trq), rem = m - __umul24(ii, a.TR * a.Q);
     const int pr = sdiv(rem, a.inv_q), pc = rem - __umul24(pr, a.Q);
-    const int pb = ii < a.TI ? __umul24(ii, a.PH * a.PW) + __umul24(pr, a.PW) + pc : 0;
+    const int pb = blk0 + i < FMT && ii < a.TI ? __umul24(ii, a.IP) + (pr << LPW) + pc : 0;
 #pragma unroll
     for (int c = 0; c < 3; ++c) {
       const int r = pb + c;
       aoff[i][c] = (r << 6) | (((lane >> 4) ^ swz(r)) << 4);
-      aoff[i][3 + c] = aoff[i][c] + rowpitch;
-      aoff[i][6 + c] = aoff[i][c] + 2 * rowpitch;
     }
   }
-  const int boff = P_BYTES + (wn * WTN + (lane & 15)) * RB + (((lane >> 4) ^ ((lane >> 2) & 3)) << 4);
+  const int boff = PROWS * RB + (wn * WTN + (lane & 15)) * RB + (((lane >> 4) ^ ((lane >> 2) & 3)) << 4);
 
-  // the fragments of tap t+1 are read from LDS while tap t's MFMAs run
-  auto load_frags = [&](const char* S, int tap, frag(&fa)[FMW], frag(&fb)[FNW]) {
+  typedef typename Mfma<T>::frag frag;
+  f32x4 acc[FMW][FNW];
+#pragma unroll
+  for (int j = 0; j < FNW; ++j)
 #pragma unroll
     for (int i = 0; i < FMW; ++i)
-      if (wm * FMW + i < FMT) fa[i] = *reinterpret_cast<const frag*>(S + aoff[i][tap]);
-#pragma unroll
-    for (int j = 0; j < FNW; ++j) fb[j] = *reinterpret_cast<const frag*>(S + boff + (tap * BN + j * 16) * RB);
-  };
-  auto compute = [&](int buf) {
-    const char* S = smem + buf * STAGE;
+      acc[i][j] = grp == 0 ? f32x4{bias[j][0], bias[j][1], bias[j][2], bias[j][3]} : f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // taps [T0, T1) of the stage SI; the fragments of tap t+1 are read from LDS
+  // while tap t's MFMAs run
+  auto compute = [&](auto SC, auto T0C, auto T1C) {
+    constexpr int SI = decltype(SC)::value, T0 = decltype(T0C)::value, T1 = decltype(T1C)::value;
+    const char* S = smem + SI * STAGE;
     frag fa[2][FMW], fb[2][FNW];
-    load_frags(S, 0, fa[0], fb[0]);
-#pragma unroll
-    for (int u = 0; u < 9; ++u) {
-      if (u + 1 < 9) load_frags(S, u + 1, fa[(u + 1) & 1], fb[(u + 1) & 1]);
+    auto load = [&](int tap, int b) {
 #pragma unroll
       for (int i = 0; i < FMW; ++i)
-        if (wm * FMW + i < FMT)
+        fa[b][i] = *reinterpret_cast<const frag*>(S + aoff[i][tap % 3] + (tap / 3) * PWT * RB);
 #pragma unroll
-          for (int j = 0; j < FNW; ++j) acc[i][j] = Mfma<T>::run(fb[u & 1][j], fa[u & 1][i], acc[i][j]);
+      for (int j = 0; j < FNW; ++j) fb[b][j] = *reinterpret_cast<const frag*>(S + boff + (tap * BN + j * 16) * RB);
+    };
+    load(T0, 0);
+#pragma unroll
+    for (int u = T0; u < T1; ++u) {
+      const int b = (u - T0) & 1;
+      if (u + 1 < T1) load(u + 1, b ^ 1);
+      // keep the next tap's reads ahead of this tap's MFMAs
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < FMW; ++i)
+#pragma unroll
+        for (int j = 0; j < FNW; ++j) acc[i][j] = Mfma<T>::run(fb[b][j], fa[b][i], acc[i][j]);
     }
   };
-
-  if constexpr (ST == 1) {
-    // one LDS stage: load, compute, and only then load the next step (the
-    // other workgroups on the CU keep its MFMAs busy meanwhile)
-    for (int t = 0; t < KT; ++t) {
-      if (t > 0) issue(0, t);
-      wait_vmcnt<0>();
-      dma_barrier();
-      compute(0);
-      dma_barrier();
+  // step t on stage t % ST: wait for its own tiles (the ST - 2 later steps may
+  // still be in flight), barrier (which also ends every wave's reads of the
+  // stage the next issue overwrites), issue step t + ST - 1, compute
+  auto step = [&](auto UC, int t) {
+    constexpr int U = decltype(UC)::value;
+    if (t >= KT) return;
+    if (t + ST - 2 < KT) wait_vmcnt<(ST - 2) * NL>();
+    else wait_vmcnt<0>();
+    dma_barrier();
+    if (t + ST - 1 < KT) issue(IC<(U + ST - 1) % ST>{}, t + ST - 1);
+    if constexpr (TG == 1) {
+      compute(UC, IC<0>{}, IC<9>{});
+    } else {
+      if (grp == 0) compute(UC, IC<0>{}, IC<5>{});
+      else compute(UC, IC<5>{}, IC<9>{});
     }
-  } else {
-    for (int t = 0; t < KT; ++t) {
-      wait_vmcnt<0>();
-      dma_barrier();
-      if (t + 1 < KT) issue((t + 1) & 1, t + 1);
-      compute(t & 1);
-    }
+  };
+  for (int t0 = 0; t0 < KT; t0 += ST) {
+    step(IC<0>{}, t0);
+    step(IC<1>{}, t0 + 1);
+    if constexpr (ST > 2) step(IC<2>{}, t0 + 2);
+    if constexpr (ST > 3) step(IC<3>{}, t0 + 3);
   }
 
-  // epilogue: accumulator (i, j, v) is output pixel (wm*FMW + i)*16 + (lane&15)
-  // of the tile, channel wn*WTN + j*16 + (lane>>4)*4 + v
-  __syncthreads();
-  T(*Cs)[BN + CPAD] = reinterpret_cast<T(*)[BN + CPAD]>(smem);
+  // tap group 1 hands its sums to group 0 through LDS
+  if constexpr (TG > 1) {
+    __syncthreads();
+    if (grp == 1) {
+#pragma unroll
+      for (int i = 0; i < FMW; ++i)
+#pragma unroll
+        for (int j = 0; j < FNW; ++j) {
+          const int ml = (blk0 + i) * 16 + (lane & 15);
+          if (blk0 + i < FMT)
+            *reinterpret_cast<f32x4*>(smem + ml * RPITCH + (wn * WTN + j * 16 + (lane >> 4) * 4) * 4) = acc[i][j];
+        }
+    }
+    __syncthreads();
+    if (grp == 1) return;
+#pragma unroll
+    for (int i = 0; i < FMW; ++i)
+#pragma unroll
+      for (int j = 0; j < FNW; ++j) {
+        const int ml = (blk0 + i) * 16 + (lane & 15);
+        if (blk0 + i < FMT)
+          acc[i][j] += *reinterpret_cast<const f32x4*>(smem + ml * RPITCH + (wn * WTN + j * 16 + (lane >> 4) * 4) * 4);
+      }
+  }
+
+  // epilogue: accumulator (i, j, v) is output pixel (blk0 + i)*16 + (lane&15)
+  // of the tile, channel wn*WTN + j*16 + (lane>>4)*4 + v; the tile's valid
+  // pixels are consecutive rows of the GEMM (whole rows of one image, or
+  // whole images); each lane stores its 4 channels as one 8-byte store
   const ActClamp ac = act_clamp(a.act);
+  const int valid = imgs * rows * a.Q;
+  const int mbase = img0 * a.P * a.Q + row0 * a.Q;
+  const int PQ = a.P * a.Q;
+  T* __restrict__ y = reinterpret_cast<T*>(a.y);
+  const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, a.y_elems * 2);
+  const bool vec4 = L == NC8 || (a.Ks % 4 == 0 && a.Ng % 4 == 0);
 #pragma unroll
-  for (int j = 0; j < FNW; ++j) {
-    const int nl = wn * WTN + j * 16 + (lane >> 4) * 4;
+  for (int i = 0; i < FMW; ++i) {
+    const int ml = (blk0 + i) * 16 + (lane & 15);
+    const bool okm = blk0 + i < FMT && ml < valid;
+    const int m = mbase + ml;
+    unsigned mo;
+    if constexpr (L == NC8) {
+      const int img = sdiv(m, a.inv_pq), pq = m - img * PQ;
+      mo = (unsigned)((img * (a.Ks >> 3) * PQ + pq) * 8);
+    } else {
+      mo = (unsigned)(m * a.Ks);
+    }
 #pragma unroll
-    for (int i = 0; i < FMW; ++i) {
-      if (wm * FMW + i >= FMT) continue;
-      const int ml = (wm * FMW + i) * 16 + (lane & 15);
+    for (int j = 0; j < FNW; ++j) {
+      const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
       T o[4];
 #pragma unroll
       for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v], ac.lo, ac.hi));
-      __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
-    }
-  }
-  __syncthreads();
-  // the tile's valid pixels are consecutive rows of the GEMM: whole rows of
-  // one image, or whole images
-  const int valid = imgs * rows * a.Q;
-  const int mbase = img0 * a.P * a.Q + row0 * a.Q;
-  T* __restrict__ y = reinterpret_cast<T*>(a.y);
-  const int PQ = a.P * a.Q;
-  if (L == NC8 || a.Ks % 8 == 0) {
-    // 16-byte rows through a buffer resource (32-bit offsets)
-    const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, a.y_elems * 2);
-    for (int idx = tid; idx < FMT * 16 * BN / 8; idx += 256) {
-      const int row = idx / (BN / 8), cj = idx % (BN / 8);
-      const int n = n0 + cj * 8;
-      if (row >= valid || n >= a.Ng) continue;
-      const int m = mbase + row;
-      unsigned off;
-      if constexpr (L == NC8) {
-        const int img = sdiv(m, a.inv_pq), pq = m - img * PQ;
-        off = (unsigned)(((img * (a.Ks >> 3) + (n >> 3)) * PQ + pq) * 8) * 2u;
-      } else {
-        off = (unsigned)(m * a.Ks + n) * 2u;
+      if (vec4) {
+        unsigned e;
+        if constexpr (L == NC8) e = mo + (unsigned)((n >> 3) * PQ * 8 + (n & 7));
+        else e = mo + (unsigned)n;
+        const unsigned off = okm && n < a.Ng ? e * 2u : kOOB;
+        __builtin_amdgcn_raw_buffer_store_b64(*reinterpret_cast<const u32x2*>(o), ry, (int)off, 0, 0);
+      } else if (okm) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (n + v < a.Ng) y[(long long)m * a.Ks + n + v] = o[v];
       }
-      __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4*>(&Cs[row][cj * 8]), ry, (int)off, 0, 0);
-    }
-  } else {
-    for (int idx = tid; idx < FMT * 16 * BN; idx += 256) {
-      const int row = idx / BN, col = idx % BN;
-      const int n = n0 + col;
-      if (row < valid && n < a.Ng) y[(long long)(mbase + row) * a.Ks + n] = Cs[row][col];
     }
   }
 }
@@ -270,9 +317,11 @@ __global__ __launch_bounds__(256, OCC) void conv3x3_patch_kernel(PatchArgs a) {
 // ------------------------------------------------------------------ host
 // Tiling of a P x Q output for a tile of FMT * 16 pixels: whole images when
 // one fits, else as many whole output rows as fit, balanced over the rows.
-static bool patch_tiling(PatchArgs& a, int fmt, int ppx) {
+// The patch row pitch is pwt and the image pitch PH * pwt.  Returns whether
+// the patch fits `prows`.
+static bool patch_tiling(PatchArgs& a, int fmt, int pwt, int prows) {
   const int maxpx = fmt * 16;
-  if (a.Q > maxpx) return false;
+  if (a.Q > maxpx || a.Q + 2 > pwt) return false;
   if (a.P * a.Q <= maxpx) {
     a.TI = std::min(a.N, maxpx / (a.P * a.Q));
     a.TR = a.P;
@@ -286,20 +335,17 @@ static bool patch_tiling(PatchArgs& a, int fmt, int ppx) {
     a.tiles_m = a.N * a.tiles_img;
   }
   a.PH = a.TR + 2;
-  // row pitch: a multiple of 16 dividing 64, at least Q + 2
-  a.PW = 16;
-  while (a.PW < a.Q + 2) a.PW *= 2;
-  if (a.PW > 64) return false;
-  a.lpw = a.PW == 16 ? 4 : a.PW == 32 ? 5 : 6;
+  a.PW = pwt;
+  a.IP = a.PH * pwt;
   a.fd_ti_tiles = make_fastdiv(a.tiles_img);
   a.inv_pw = 1.f / (float)a.PW;
-  a.inv_ph = 1.f / (float)a.PH;
+  a.inv_ip = 1.f / (float)a.IP;
   a.HW8 = a.H * a.W * 8;
   a.inv_pq = 1.f / (float)(a.P * a.Q);
   a.W8 = a.W * 8;
   a.inv_trq = 1.f / (float)(a.TR * a.Q);
   a.inv_q = 1.f / (float)a.Q;
-  return a.TI * a.PH * a.PW <= ppx;
+  return (long long)a.TI * a.IP <= prows;
 }
 
 static PatchArgs make_patch(const ConvArgs& c) {
@@ -329,52 +375,47 @@ static PatchArgs make_patch(const ConvArgs& c) {
 }
 
 bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
-                      int fmt, int bn, int bk, int ppx) {
-  (void)bn;
+                      int fmt, int pwt, int prows) {
   if (r != 3 || s != 3 || stride != 1 || pad != 1) return false;
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
-  if (!vec || ((c + 7) / 8) % (bk / 8) != 0) return false;
+  if (!vec || ((c + 7) / 8) % 4 != 0) return false;
   if ((long long)n * h * w + h * w >= (1 << 21)) return false;  // fp32 index division
   PatchArgs a{};
   a.N = n;
   a.P = h;
   a.Q = w;
-  return patch_tiling(a, fmt, ppx);
+  return patch_tiling(a, fmt, pwt, prows);
 }
 
-template <typename T, int L, int FMT, int BN, int BK, int WM, int ST, int PPX, int OCC>
+template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS>
 static void patch_go(PatchArgs a, hipStream_t st) {
-  check(patch_tiling(a, FMT, PPX), "output too wide for the patch tile");
-  check(a.CB % (BK / 8) == 0, "patch kernel needs C % BK == 0");
+  check(patch_tiling(a, FMT, PWT, PROWS), "output too wide for the patch tile");
+  check(a.CB % 4 == 0, "patch kernel needs C % 32 == 0");
   check(a.x_elems * 2 < (long long)kOOB && a.w_elems * 2 < (long long)kOOB,
         "tensor too large for 32-bit buffer offsets");
   a.tiles_n = (a.Ng + BN - 1) / BN;
   dim3 grid(a.tiles_m * a.tiles_n);
-  SN_LAUNCH((conv3x3_patch_kernel<T, L, FMT, BN, BK, WM, ST, PPX, OCC>), grid, dim3(256), 0, st, a);
+  SN_LAUNCH((conv3x3_patch_kernel<T, L, FMT, BN, PWT, WM, WN, TG, ST, PROWS>), grid, dim3(512), 0, st, a);
+}
+
+static long long patch_key(int fmt, int bn, int pwt, int wm, int wn, int tg, int stg, int prows) {
+  return ((((((fmt * 1000LL + bn) * 100 + pwt) * 10 + wm) * 10 + wn) * 10 + tg) * 10 + stg) * 10000 + prows;
 }
 
 template <typename T, int L>
-static void patch_layout(int fmt, int bn, int bk, int wm, int stg, int ppx, const PatchArgs& a,
-                         hipStream_t st) {
-  const long long key = ((((fmt * 1000LL + bn) * 1000 + bk) * 10 + wm) * 10 + stg) * 10000 + ppx;
-#define PGO(FMT_, BN_, BK_, WM_, ST_, PPX_, OCC_)                                      \
-  case ((((FMT_ * 1000LL + BN_) * 1000 + BK_) * 10 + WM_) * 10 + ST_) * 10000 + PPX_: \
-    patch_go<T, L, FMT_, BN_, BK_, WM_, ST_, PPX_, OCC_>(a, st);                        \
-    break;
-  switch (key) {
-    PGO(14, 64, 32, 2, 2, 384, 1)
-    PGO(14, 64, 32, 2, 1, 384, 2)
-    PGO(14, 32, 32, 4, 1, 384, 3)
-    PGO(7, 64, 32, 1, 2, 320, 1)
-    PGO(7, 64, 32, 2, 1, 320, 2)
-    PGO(7, 32, 32, 4, 2, 320, 2)
-    default: check(false, "patch tile not instantiated");
+static void patch_layout(const PatchCfg& c, const PatchArgs& a, hipStream_t st) {
+  const long long key = patch_key(c.fmt, c.bn, c.pwt, c.wm, c.wn, c.tg, c.st, c.prows);
+#define PGO(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                               \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)) {                  \
+    patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_>(a, st);                 \
+    return;                                                                            \
   }
+  PATCH_CONFIGS(PGO)
 #undef PGO
+  check(false, "patch tile not instantiated");
 }
 
-void conv_patch(int dtype, int fmt, int bn, int bk, int wm, int stg, int ppx, const ConvArgs& c,
-                hipStream_t st) {
+void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& c, hipStream_t st) {
   check(dtype != 0, "patch kernel runs 16-bit types");
   check(c.xd.layout == c.yd.layout && c.r == 3 && c.s == 3 && c.stride == 1 && c.pad == 1,
         "patch kernel: 3x3 stride 1 pad 1, one layout");
@@ -382,11 +423,11 @@ void conv_patch(int dtype, int fmt, int bn, int bk, int wm, int stg, int ppx, co
   check((long long)c.yd.n * c.yd.cs * c.yd.h * c.yd.w * 2 < (long long)kOOB, "tensor too large");
   const PatchArgs a = make_patch(c);
   if (dtype == 1) {
-    if (c.xd.layout == NC8) patch_layout<f16, NC8>(fmt, bn, bk, wm, stg, ppx, a, st);
-    else patch_layout<f16, NHWC>(fmt, bn, bk, wm, stg, ppx, a, st);
+    if (c.xd.layout == NC8) patch_layout<f16, NC8>(cfg, a, st);
+    else patch_layout<f16, NHWC>(cfg, a, st);
   } else {
-    if (c.xd.layout == NC8) patch_layout<bf16, NC8>(fmt, bn, bk, wm, stg, ppx, a, st);
-    else patch_layout<bf16, NHWC>(fmt, bn, bk, wm, stg, ppx, a, st);
+    if (c.xd.layout == NC8) patch_layout<bf16, NC8>(cfg, a, st);
+    else patch_layout<bf16, NHWC>(cfg, a, st);
   }
 }
 

@@ -60,10 +60,24 @@ bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, in
 size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s);
 // 3x3 stride-1 convolution with the input patch in LDS (an implicit-GEMM
 // parameter family; see conv_patch.hip)
+struct PatchCfg {
+  int fmt, bn, pwt, wm, wn, tg, st, prows;  // one PATCH_CONFIGS tuple
+};
+// Instantiated patch tiles (FMT, BN, PWT, WM, WN, TG, ST, PROWS): FMT row
+// blocks of 16 output pixels, BN output channels, patch row pitch PWT, 8
+// waves as TG tap groups of WM x WN, ST LDS stages, PROWS patch rows per
+// stage.  Each is one implicit-GEMM routine parameter.
+#define PATCH_CONFIGS(X)         \
+  X(25, 64, 64, 4, 2, 1, 2, 576) \
+  X(13, 64, 32, 4, 2, 1, 2, 288) \
+  X(13, 64, 32, 2, 2, 2, 2, 288) \
+  X(13, 32, 16, 4, 1, 2, 3, 256) \
+  X(13, 32, 16, 4, 2, 1, 3, 256) \
+  X(7, 32, 16, 4, 1, 2, 3, 288)  \
+  X(7, 32, 64, 4, 1, 2, 2, 256)
 bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
-                      int fmt, int bn, int bk, int ppx);
-void conv_patch(int dtype, int fmt, int bn, int bk, int wm, int stg, int ppx, const ConvArgs& a,
-                hipStream_t st);
+                      int fmt, int pwt, int prows);
+void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& a, hipStream_t st);
 // Stride-2 convolution of an NHWC input with C <= 4 (a CNN stem; see conv_smallc.hip)
 bool smallc_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
                        int fmt, int ppx, int gmax);
