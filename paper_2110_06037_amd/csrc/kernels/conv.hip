@@ -12,6 +12,7 @@
 #include <algorithm>
 #include <stdexcept>
 #include <string>
+#include <type_traits>
 
 #include "gemm_common.hpp"
 #include "kcommon.hpp"
@@ -97,7 +98,7 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
   // of a few rows) and the MFMA fragment reads (one chunk of 16 rows) hit
   // distinct LDS banks.  fp32 tiles use padded rows instead.
   constexpr int LDK = BK + (F32 ? 4 : 0);
-  constexpr int RPR = F32 ? 1 : 128 / BK;  // rows sharing one bank range
+  constexpr int RPR = F32 || BK > 64 ? 1 : 2;  // rows sharing one chunk XOR key
   constexpr int WTM = BM / 2, WTN = BN / 2;
   constexpr int FM = WTM / 16, FN = WTN / 16;
   constexpr int NA = BM * CPR / 256;            // A chunks per thread
@@ -463,22 +464,33 @@ constexpr int dma_lds_bytes() {
              ? ST * (BM + BN) * BK * 2
              : (EPI == EPI_LAYOUT ? BM * (BN + 8) * 2 : 0);
 }
-template <int BM, int BN, int BK, int ST, int EPI>
+template <int BM, int BN, int BK, int ST, int EPI, int NWV = 4>
 constexpr int dma_occ() {
-  return 160 * 1024 / dma_lds_bytes<BM, BN, BK, ST, EPI>() > 4 ? 4 : 160 * 1024 / dma_lds_bytes<BM, BN, BK, ST, EPI>();
+  return 160 * 1024 / dma_lds_bytes<BM, BN, BK, ST, EPI>() > 16 / NWV ? 16 / NWV
+                                                                        : 160 * 1024 / dma_lds_bytes<BM, BN, BK, ST, EPI>();
 }
 
-template <typename T, int L, int BM, int BN, int BK, int WM, int ST, int EPI>
-__global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_dma_kernel(IgArgs a) {
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+// NWV waves (4 or 8) as WM x (NWV / WM); with 8 waves two share each SIMD,
+// so one wave's loads and epilogue overlap the other's MFMAs.
+template <typename T, int L, int BM, int BN, int BK, int WM, int ST, int EPI, int NWV = 4>
+__global__ __launch_bounds__(64 * NWV, (dma_occ<BM, BN, BK, ST, EPI, NWV>()))
+void igemm_dma_kernel(IgArgs a) {
   static_assert(sizeof(T) == 2 && L != NCHW, "16-bit channel-vector layouts only");
-  constexpr int WN = 4 / WM;
+  static_assert(NWV == 4 || NWV == 8, "4 or 8 waves");
+  constexpr int NT = 64 * NWV;
+  constexpr int WN = NWV / WM;
   constexpr int CPR = BK / 8;       // 16-byte chunks per tile row
   constexpr int RPB = 64 / CPR;     // tile rows filled by one load instruction (1 KB)
-  constexpr int RPR = 128 / BK;     // rows per swizzle period (one 128-byte bank range)
-  constexpr int NA = BM / RPB / 4;  // A load instructions per wave and stage
-  constexpr int NB = BN / RPB / 4;  // B load instructions per wave and stage
-  static_assert(NA * RPB * 4 == BM && NB * RPB * 4 == BN && WM * WN == 4, "tile shape");
-  static_assert(ST >= 2 && (ST - 2) * (NA + NB) <= 63, "pipeline depth");
+  // the chunk XOR key changes every 2 rows: one chunk of 16 consecutive rows
+  // is then read in a single LDS pass on gfx950 for 64- and 128-byte rows
+  constexpr int RPR = 2;
+  constexpr int NA = BM / RPB / NWV;  // A load instructions per wave and stage
+  constexpr int NB = BN / RPB / NWV;  // B load instructions per wave and stage
+  static_assert(NA * RPB * NWV == BM && NB * RPB * NWV == BN && WM * WN == NWV, "tile shape");
+  static_assert(ST >= 2 && ST <= 6 && (ST - 2) * (NA + NB) <= 63, "pipeline depth");
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int FM = WTM / 16, FN = WTN / 16;
   constexpr int A_BYTES = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
@@ -502,14 +514,33 @@ __global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_d
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, a.x_elems * 2);
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(w, a.w_elems * 2);
 
-  // this lane's load slots: block b = wave + 4 i fills tile rows
+  // accumulators start at the bias of the lane's output channels (at zero
+  // for a partial sum of a split reduction); the bias is loaded before the
+  // tiles so that waiting for it does not wait for them
+  float bias[FN][4];
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) bias[j][v] = 0.f;
+  if constexpr (EPI == EPI_LAYOUT) {
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.bias, (long long)a.Ng * 4);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        bias[j][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n + v) * 4, 0, 0));
+    }
+  }
+
+  // this lane's load slots: block b = wave + NWV i fills tile rows
   // [b * RPB, (b + 1) * RPB); the lane fills row b * RPB + lane / CPR,
   // physical chunk lane % CPR, i.e. logical chunk (lane % CPR) ^ swz(row)
   const int prow = lane / CPR, pch = lane % CPR;
   unsigned rbyte[NA], tvm[NA];
 #pragma unroll
   for (int i = 0; i < NA; ++i) {
-    const int row = (wave + 4 * i) * RPB + prow;
+    const int row = (wave + NWV * i) * RPB + prow;
     const int lc = pch ^ swz(row);
     const int m = m0 + row;
     const bool ok = m < a.M;
@@ -534,7 +565,7 @@ __global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_d
   unsigned bbyte[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
-    const int row = (wave + 4 * i) * RPB + prow;
+    const int row = (wave + NWV * i) * RPB + prow;
     const int lc = pch ^ swz(row);
     const int k = n0 + row;
     bbyte[i] = k < a.Ng ? (unsigned)((__mul24(k, a.Kred) + lc * 8) * 2) : kOOB;
@@ -543,8 +574,8 @@ __global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_d
   // reduction position of the next step to load: tap (r, s), channel block cb
   ChunkPos upos;
   chunk_set(upos, kt0 * CPR, a.CB, a.S);
-  auto issue = [&](int buf, int kt) {
-    char* base = smem + buf * STAGE;
+  auto issue = [&](auto SC, int kt) {
+    char* base = smem + decltype(SC)::value * STAGE;
     const int t = upos.r * a.S + upos.s;
     int tap;
     if constexpr (L == NC8)
@@ -554,9 +585,9 @@ __global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_d
     const unsigned tb = (unsigned)tap * 2u;
 #pragma unroll
     for (int i = 0; i < NA; ++i)
-      dma16(rx, base + (wave + 4 * i) * 1024, ((tvm[i] >> t) & 1u) ? rbyte[i] + tb : kOOB, 0);
+      dma16(rx, base + (wave + NWV * i) * 1024, ((tvm[i] >> t) & 1u) ? rbyte[i] + tb : kOOB, 0);
 #pragma unroll
-    for (int i = 0; i < NB; ++i) dma16(rw, base + A_BYTES + (wave + 4 * i) * 1024, bbyte[i], kt * BK * 2);
+    for (int i = 0; i < NB; ++i) dma16(rw, base + A_BYTES + (wave + NWV * i) * 1024, bbyte[i], kt * BK * 2);
     upos.cb += CPR;  // CB is a multiple of CPR
     if (upos.cb == a.CB) {
       upos.cb = 0;
@@ -567,23 +598,8 @@ __global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_d
     }
   };
 
-  // accumulators start at the bias of the lane's output channels (at zero
-  // for a partial sum of a split reduction)
-  f32x4 acc[FM][FN];
-#pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    f32x4 b = f32x4{0.f, 0.f, 0.f, 0.f};
-    if constexpr (EPI == EPI_LAYOUT) {
-      const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.bias, (long long)a.Ng * 4);
-      const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        b[v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n + v) * 4, 0, 0));
-    }
-#pragma unroll
-    for (int i = 0; i < FM; ++i) acc[i][j] = b;
-  }
   typedef typename Mfma<T>::frag frag;
+  f32x4 acc[FM][FN];
   // operand chunk offsets in a stage: a 16-row block starts at a multiple of
   // 16 rows, so the row swizzle is the lane's own; the chunk of k-slice ks is
   // fixed per lane and the block offset is an instruction immediate
@@ -601,14 +617,16 @@ __global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_d
 #pragma unroll
     for (int j = 0; j < FN; ++j) fb[j] = *reinterpret_cast<const frag*>(S + bofs[ks] + j * 16 * (BK * 2));
   };
-  // the fragments of k-slice ks+1 are read while the MFMAs of ks run
-  auto compute = [&](int buf) {
-    const char* S = smem + buf * STAGE;
+  // the fragments of k-slice ks+1 are read while the MFMAs of ks run (the
+  // stage index is a template constant, so every LDS offset is an immediate)
+  auto compute = [&](auto SC) {
+    const char* S = smem + decltype(SC)::value * STAGE;
     frag fa[2][FM], fb[2][FN];
     load_frags(S, 0, fa[0], fb[0]);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       if (ks + 1 < KS) load_frags(S, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -617,18 +635,35 @@ __global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_d
   };
 
   // step t: wait for tile t (the ST-2 tiles after it may stay in flight),
-  // barrier, issue tile t+ST-1 into the buffer read at step t-1, compute t
+  // barrier, issue tile t+ST-1 into the buffer read at step t-1, compute t;
+  // the loop is unrolled by ST so that stage indices are constants
+  issue(IC<0>{}, kt0);
+  if constexpr (ST > 2) { if (1 < KT) issue(IC<1>{}, kt0 + 1); }
+  if constexpr (ST > 3) { if (2 < KT) issue(IC<2>{}, kt0 + 2); }
+  if constexpr (ST > 4) { if (3 < KT) issue(IC<3>{}, kt0 + 3); }
+  if constexpr (ST > 5) { if (4 < KT) issue(IC<4>{}, kt0 + 4); }
 #pragma unroll
-  for (int u = 0; u < ST - 1; ++u)
-    if (u < KT) issue(u, kt0 + u);
-  for (int t = 0; t < KT; ++t) {
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int i = 0; i < FM; ++i) acc[i][j] = f32x4{bias[j][0], bias[j][1], bias[j][2], bias[j][3]};
+  auto step = [&](auto UC, int t) {
+    constexpr int U = decltype(UC)::value;
+    if (t >= KT) return;
     if (t + ST - 2 < KT)
       wait_vmcnt<(ST - 2) * (NA + NB)>();
     else
       wait_vmcnt<0>();
     dma_barrier();
-    if (t + ST - 1 < KT) issue((t + ST - 1) % ST, kt0 + t + ST - 1);
-    compute(t % ST);
+    if (t + ST - 1 < KT) issue(IC<(U + ST - 1) % ST>{}, kt0 + t + ST - 1);
+    compute(UC);
+  };
+  for (int t0 = 0; t0 < KT; t0 += ST) {
+    step(IC<0>{}, t0);
+    step(IC<1>{}, t0 + 1);
+    if constexpr (ST > 2) step(IC<2>{}, t0 + 2);
+    if constexpr (ST > 3) step(IC<3>{}, t0 + 3);
+    if constexpr (ST > 4) step(IC<4>{}, t0 + 4);
+    if constexpr (ST > 5) step(IC<5>{}, t0 + 5);
   }
 
   // accumulator element (i, j, v) is C[wm*WTM + i*16 + (lane&15)][wn*WTN + j*16 + (lane>>4)*4 + v]
@@ -671,7 +706,7 @@ __global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_d
     if (L == NC8 || a.Ks % 8 == 0) {
       // 16-byte rows through a buffer resource (32-bit offsets)
       const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, a.y_elems * 2);
-      for (int idx = tid; idx < BM * BN / 8; idx += 256) {
+      for (int idx = tid; idx < BM * BN / 8; idx += NT) {
         const int row = idx / (BN / 8), cj = idx % (BN / 8);
         const int m = m0 + row, n = n0 + cj * 8;
         if (m >= a.M || n >= a.Ng) continue;
@@ -686,7 +721,7 @@ __global__ __launch_bounds__(256, (dma_occ<BM, BN, BK, ST, EPI>())) void igemm_d
         __builtin_amdgcn_raw_buffer_store_b128(v, ry, (int)off, 0, 0);
       }
     } else {
-      for (int idx = tid; idx < BM * BN; idx += 256) {
+      for (int idx = tid; idx < BM * BN; idx += NT) {
         const int row = idx / BN, col = idx % BN;
         const int m = m0 + row, n = n0 + col;
         if (m < a.M && n < a.Ng) y[(long long)m * a.Ks + n] = Cs[row][col];
@@ -749,6 +784,7 @@ struct IgCfg {
                                 // wave rows WM (of 4 waves), LDS stages ST
   int ppx = 0;                  // small-channel kernel: patch capacity in pixels
   PatchCfg pc{};                // patch kernel tile
+  int nw = 4;                   // LDS-DMA kernel: waves per workgroup (4 or 8)
 };
 static const IgCfg kIg16[] = {
     {64, 64, 32, 0, 2},   {128, 128, 64, 0, 2}, {256, 128, 32, 0, 2}, {128, 64, 64, 0, 2},
@@ -764,6 +800,12 @@ static const IgCfg kIg16[] = {
     // deeper pipelines (short reduction steps, more in flight)
     {128, 128, 32, 0, 0, 1, 2, 4}, {128, 64, 32, 0, 0, 1, 2, 4}, {64, 128, 32, 0, 0, 1, 1, 4},
     {64, 64, 64, 0, 0, 1, 2, 4},   {64, 64, 32, 0, 0, 1, 2, 6},  {256, 64, 32, 0, 0, 1, 4, 4},
+    // LDS-DMA kernel with 8 waves (two per SIMD)
+    {128, 128, 64, 0, 0, 1, 4, 2, 0, {}, 8}, {128, 128, 64, 0, 0, 1, 4, 3, 0, {}, 8},
+    {128, 128, 64, 0, 0, 1, 4, 4, 0, {}, 8}, {256, 128, 64, 0, 0, 1, 4, 3, 0, {}, 8},
+    {128, 64, 64, 0, 0, 1, 4, 4, 0, {}, 8},  {256, 64, 64, 0, 0, 1, 8, 3, 0, {}, 8},
+    {64, 128, 64, 0, 0, 1, 2, 4, 0, {}, 8},  {128, 256, 64, 0, 0, 1, 2, 3, 0, {}, 8},
+    {128, 128, 32, 0, 0, 1, 4, 4, 0, {}, 8}, {256, 128, 32, 0, 0, 1, 4, 4, 0, {}, 8},
     // 3x3 stride-1 patch kernel
 #define SN_PATCH_IG(FMT, BN, PWT, WM, WN, TG, ST, PROWS) \
   {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS}},
@@ -826,7 +868,7 @@ static void igemm_go(const IgArgs& a, int batch, hipStream_t st) {
     SN_LAUNCH((igemm_kernel<T, L, VEC, false, BM, BN, BK, EPI, PF>), grid, dim3(256), 0, st, a);
 }
 
-template <typename T, int L, int BM, int BN, int BK, int WM, int ST, int EPI>
+template <typename T, int L, int BM, int BN, int BK, int WM, int ST, int EPI, int NWV = 4>
 static void igemm_dma_go(const IgArgs& a, hipStream_t st) {
   check(a.x_elems * 2 < (long long)kOOB && a.w_elems * 2 < (long long)kOOB,
         "tensor too large for 32-bit buffer offsets");
@@ -834,15 +876,16 @@ static void igemm_dma_go(const IgArgs& a, hipStream_t st) {
   check(a.y_elems * 2 < (long long)kOOB && (long long)a.M + a.PQ < (1 << 21),
         "tensor too large for 32-bit offsets / fp32 index division");
   dim3 grid(a.tiles_m * a.tiles_n, a.splits, 1);
-  SN_LAUNCH((igemm_dma_kernel<T, L, BM, BN, BK, WM, ST, EPI>), grid, dim3(256), 0, st, a);
+  SN_LAUNCH((igemm_dma_kernel<T, L, BM, BN, BK, WM, ST, EPI, NWV>), grid, dim3(64 * NWV), 0, st, a);
 }
 
 template <typename T, int L, int EPI>
 static void igemm_dma_cfg(const IgCfg& c, const IgArgs& a, hipStream_t st) {
-  const long long key = (((c.bm * 1000LL + c.bn) * 1000 + c.bk) * 10 + c.wm) * 10 + c.st;
-#define IGD(BM_, BN_, BK_, WM_, ST_)                                  \
-  case (((BM_ * 1000LL + BN_) * 1000 + BK_) * 10 + WM_) * 10 + ST_: \
-    igemm_dma_go<T, L, BM_, BN_, BK_, WM_, ST_, EPI>(a, st);          \
+  const long long key = ((((c.bm * 1000LL + c.bn) * 1000 + c.bk) * 10 + c.wm) * 10 + c.st) * 10 + c.nw;
+#define IGD(BM_, BN_, BK_, WM_, ST_) IGDN(BM_, BN_, BK_, WM_, ST_, 4)
+#define IGDN(BM_, BN_, BK_, WM_, ST_, NW_)                                       \
+  case ((((BM_ * 1000LL + BN_) * 1000 + BK_) * 10 + WM_) * 10 + ST_) * 10 + NW_: \
+    igemm_dma_go<T, L, BM_, BN_, BK_, WM_, ST_, EPI, NW_>(a, st);                \
     break;
   if constexpr (EPI == EPI_SPLIT) {
     switch (key) {
@@ -868,9 +911,20 @@ static void igemm_dma_cfg(const IgCfg& c, const IgArgs& a, hipStream_t st) {
     IGD(64, 64, 64, 2, 4)
     IGD(64, 64, 32, 2, 6)
     IGD(256, 64, 32, 4, 4)
+    IGDN(128, 128, 64, 4, 2, 8)
+    IGDN(128, 128, 64, 4, 3, 8)
+    IGDN(128, 128, 64, 4, 4, 8)
+    IGDN(256, 128, 64, 4, 3, 8)
+    IGDN(128, 64, 64, 4, 4, 8)
+    IGDN(256, 64, 64, 8, 3, 8)
+    IGDN(64, 128, 64, 2, 4, 8)
+    IGDN(128, 256, 64, 2, 3, 8)
+    IGDN(128, 128, 32, 4, 4, 8)
+    IGDN(256, 128, 32, 4, 4, 8)
     default: check(false, "LDS-DMA tile not instantiated");
   }
 #undef IGD
+#undef IGDN
 }
 
 template <typename T, int L, bool VEC, int EPI>

@@ -9,24 +9,32 @@
 // those channels for all 9 taps, then runs the 9 taps' MFMAs out of LDS: tap
 // (r, s) of output pixel (p, q) is patch pixel (p + r, q + s), so the per-tap
 // operand rows are the same patch rows shifted by the uniform offset
-// r * PW + s (PW = the patch row pitch).  Each input element therefore
-// crosses the memory system about (TR + 2) / TR times per workgroup instead
-// of 9 times, which is what bounds the per-tap (im2col) implicit GEMM.
+// r * PWT + s (PWT = the patch row pitch, a power of two).  Each input
+// element therefore crosses the memory system about (TR + 2) / TR times per
+// workgroup instead of 9 times, which is what bounds the per-tap (im2col)
+// implicit GEMM.
 //
 // Tiles move from global memory into LDS with direct loads (16 bytes per
 // lane, 1 KB per wave instruction in lane order) through ST stages, so up to
 // ST - 1 channel steps are in flight while one is computed.  An LDS row holds
 // the 32 channels of one pixel (64 bytes); 16-byte chunk c of row r sits at
-// chunk c ^ ((r >> 2) & 3), so 16 rows that are distinct modulo 16 hit 16
-// distinct bank groups.  An MFMA operand reads 16 consecutive pixels of the
-// tile; with the row pitch PW = Q (mod 16) and the image pitch IP = P * Q
-// (mod 16) the patch row of pixel m is m plus a constant modulo 16, so every
-// operand read of every tap is free of bank conflicts ("conflict-free
-// pitch").  The dense pitch (PW = Q + 2, IP = PH * PW) loads fewer rows and
-// accepts some conflicts; both are routine parameters.  The MFMA takes the
-// filter as its first operand, so each lane's 4 accumulators are 4
-// consecutive output channels of one pixel; the epilogue adds the bias,
-// applies the activation and stores through LDS as 16-byte rows.
+// chunk c ^ ((r >> 1) & 3).  An MFMA operand read takes one chunk of 16
+// consecutive rows, which this placement serves in a single LDS pass on
+// gfx950 for any starting row (an XOR of (r >> 2) & 3 measures two passes).
+// Operand rows that wrap to the next image row are not consecutive and may
+// take two passes.  Tap row offsets r * PWT are multiples of 16 rows, so they
+// keep the placement and become instruction immediates, as do the stage
+// offsets (the step loop is unrolled by the stage count): an operand read
+// costs no address arithmetic.
+//
+// Eight waves (two per SIMD, so one wave's loads and epilogue overlap the
+// other's MFMAs) form TG tap groups: group g runs taps [9g/TG, 9(g+1)/TG) of
+// every step on the whole tile, which keeps each wave's operand tile large
+// when the workgroup tile is small; the groups' sums meet in LDS at the end.
+// The MFMA takes the filter as its first operand, so each lane's 4
+// accumulators are 4 consecutive output channels of one pixel; sums start at
+// the bias, and the epilogue applies the activation and stores each lane's 4
+// channels as one 8-byte store.
 #include "gemm_common.hpp"
 #include "kcommon.hpp"
 #include "launch.hpp"
@@ -88,7 +96,7 @@ __global__ __launch_bounds__(512, 1) void conv3x3_patch_kernel(PatchArgs a) {
   static_assert(SM <= 160 * 1024, "LDS capacity");
   __shared__ __attribute__((aligned(1024))) char smem[SM];
   lds_char* const sl = (lds_char*)smem;
-  auto swz = [](int row) { return (row >> 2) & 3; };
+  auto swz = [](int row) { return (row >> 1) & 3; };
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
@@ -185,7 +193,7 @@ __global__ __launch_bounds__(512, 1) void conv3x3_patch_kernel(PatchArgs a) {
       aoff[i][c] = (r << 6) | (((lane >> 4) ^ swz(r)) << 4);
     }
   }
-  const int boff = PROWS * RB + (wn * WTN + (lane & 15)) * RB + (((lane >> 4) ^ ((lane >> 2) & 3)) << 4);
+  const int boff = PROWS * RB + (wn * WTN + (lane & 15)) * RB + (((lane >> 4) ^ ((lane >> 1) & 3)) << 4);
 
   typedef typename Mfma<T>::frag frag;
   f32x4 acc[FMW][FNW];
