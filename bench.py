@@ -72,15 +72,24 @@ def layer_work(spec, g, i, routine):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_resnet50_bs32_bf16.json")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2110_06037_amd", "csrc", "kernels", f)
-                  for f in ("conv.hip", "conv_patch.hip", "misc.hip", "gemm_common.hpp", "kcommon.hpp")]
+KDIR = os.path.join(ROOT, "paper_2110_06037_amd", "csrc", "kernels")
+# sources each dominant kernel is built from (its traffic summary goes stale
+# when any of them changes)
+KERNEL_SOURCES = {
+    "add_kernel": ("misc.hip", "kcommon.hpp"),
+    "igemm_dma_kernel": ("conv.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
+    "igemm_kernel": ("conv.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
+    "conv3x3_patch_kernel": ("conv_patch.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
+}
+ALL_KERNEL_SOURCES = ("conv.hip", "conv_patch.hip", "conv_smallc.hip", "misc.hip", "gemm_common.hpp",
+                      "kcommon.hpp", "launch.hpp")
 
 
-def kernel_source_hash():
+def kernel_source_hash(ksub=None):
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
-        with open(f, "rb") as fh:
+    for f in KERNEL_SOURCES.get(ksub, ALL_KERNEL_SOURCES):
+        with open(os.path.join(KDIR, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
@@ -93,7 +102,7 @@ def traffic_for(routine):
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("routine") != routine or t.get("source_hash") != kernel_source_hash():
+    if t.get("routine") != routine or t.get("source_hash") != kernel_source_hash(t.get("kernel_symbol_part")):
         return None
     return t.get("bytes_per_launch")
 
@@ -124,7 +133,7 @@ def summarize_pmc(fetch_dir, write_dir, routine, ksub, out, calib_mib):
     per = None
     if f["scale"] and w["scale"]:
         per = int((f["mean_kib"] * f["scale"] + w["mean_kib"] * w["scale"]) * 1024)
-    t = {"routine": routine, "kernel_symbol_part": ksub, "source_hash": kernel_source_hash(),
+    t = {"routine": routine, "kernel_symbol_part": ksub, "source_hash": kernel_source_hash(ksub),
          "bytes_per_launch": per,
          "counters": res, "calibration": f"device copy of {calib_mib} MiB (read and write)"}
     with open(out, "w") as fh:
