@@ -52,6 +52,8 @@ def layer_work(spec, g, i, routine):
         r, s, grp = layer["r"], layer["s"], layer["groups"]
         wbytes = k * (c // grp) * r * s * es
         byt = es * (n * c * h * w + n * k * p * q) + wbytes + 4 * k
+        if len(layer["in"]) > 1:  # residual read in the epilogue
+            byt += es * n * k * p * q
         if grp > 1:
             return "dwconv", 2 * n * k * r * s * p * q, byt
         flops = 2 * n * k * c * r * s * p * q
@@ -248,6 +250,9 @@ def main():
                     help="print the measured cost table of the four 3x3 sweep shapes and exit")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-path sweep")
     ap.add_argument("--no-bs1", action="store_true", help="skip the batch-1 measurement")
+    ap.add_argument("--no-fuse", action="store_true",
+                    help="keep residual adds as their own layers (default: fold each into the 1x1 "
+                         "convolution that produces its operand)")
     ap.add_argument("--integrated-reps", type=int, default=20,
                     help="runs per candidate in integrated profiling (0 = keep the DPRS path)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -280,9 +285,11 @@ def main():
     import numpy as np
     import torch
     from paper_2110_06037_amd import build_from_spec, native as N, to_device as to_dev
-    from workloads import generate, resnet50
+    from workloads import fuse_residual, generate, resnet50
 
     spec = _nets()[args.net](args.batch, args.dtype)
+    if not args.no_fuse:
+        spec = fuse_residual(spec)
     t = generate(spec)
     log(f"[bench] {spec['name']}: building graph")
     g = build_from_spec(spec, t, device=0)
@@ -364,7 +371,11 @@ def main():
     dom_key = max(groups, key=lambda k: groups[k]["ms"])
     dom = groups[dom_key]
     avg_s = dom["ms"] / dom["launches"] * 1e-3
-    if any(c.startswith("conv") for c in dom["cats"]) and "direct" not in dom_key:
+    # the roof that binds: MFMA when the routine's arithmetic intensity is above
+    # the ridge point (peak flops / peak bandwidth), HBM otherwise
+    ridge = PEAK_MFMA_TFLOPS[args.dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if (any(c.startswith("conv") for c in dom["cats"]) and "direct" not in dom_key
+            and dom["flops"] > ridge * dom["bytes"]):
         ach = dom["flops"] / dom["launches"] / avg_s / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_MFMA_TFLOPS[args.dtype],
                 "unit": "TFLOP/s"}
@@ -406,6 +417,8 @@ def main():
     bs1 = None
     if not args.no_bs1 and args.net == "resnet50":
         spec1 = resnet50(1, args.dtype)
+        if not args.no_fuse:
+            spec1 = fuse_residual(spec1)
         t1_ = generate(spec1)
         g1 = build_from_spec(spec1, t1_, device=0)
         g1.profile(warmup=5, reps=args.profile_reps)
@@ -428,7 +441,9 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sec * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": args.dtype,
         "data": "synthetic (seeded random input and He-normal weights)",
-        "config": {"workload": f"{args.net}-shaped CNN, batch {args.batch}, {args.dtype}, 224x224",
+        "config": {"workload": f"{args.net}-shaped CNN, batch {args.batch}, {args.dtype}, 224x224"
+                               + ("" if args.no_fuse else
+                                  ", residual adds folded into the 1x1 convolutions that produce them"),
                    "batch": args.batch,
                    "path": ("DPRS candidates + fixed paths, integrated profiling keeps the fastest"
                             if integ else "DPRS-selected routines")},

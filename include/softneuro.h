@@ -79,7 +79,11 @@ typedef enum {
 typedef enum { SN_ACT_NONE = 0, SN_ACT_RELU = 1, SN_ACT_RELU6 = 2 } sn_act;
 
 /* Layer description.  Fields not used by a type are ignored.
- *   CONV2D : k = output channels, r x s kernel, stride, pad, groups, act
+ *   CONV2D : k = output channels, r x s kernel, stride, pad, groups, act;
+ *            an optional second input is a residual of the output's shape
+ *            (dense convolutions only): y = act(conv(x) + bias + residual),
+ *            a residual add fused into the convolution that produces its
+ *            other operand
  *   MAXPOOL: r (= s) window, stride, pad (padding never wins the max)
  *   GAP    : -
  *   ADD    : act
@@ -136,7 +140,10 @@ int sn_set_option(sn_graph* g, int32_t option, int64_t value);
 
 /* Appends a layer (Sec. III-B: type, layer parameters, weights).  inputs
  * lists existing layer ids (so insertion order is a topological order,
- * Sec. IV-A); ADD takes two, the other types one.  weight: host memory in
+ * Sec. IV-A); ADD takes two, CONV2D one or two (data, residual), the other
+ * types one.  A CONV2D with a residual has the direct and implicit-GEMM
+ * routines whose epilogue adds it (no Winograd, patch or small-channel
+ * tiles).  weight: host memory in
  * the run dtype, OIHW for CONV2D ([K][C/groups][R][S]) and [K][C] for FC;
  * bias: host float32 [K] (may be NULL = zeros).  Both are copied.  The last
  * added layer is the net output.  *out_id receives the new id.

@@ -134,6 +134,9 @@ def round_to(a, dtype):
 def layer_forward(layer, inputs, w=None, b=None):
     t = layer["type"]
     if t == "conv":
+        if len(inputs) > 1:  # residual added before the activation
+            y = conv2d(inputs[0], w, b, layer["stride"], layer["pad"], layer["groups"], "none")
+            return add(y, inputs[1], layer["act"])
         return conv2d(inputs[0], w, b, layer["stride"], layer["pad"], layer["groups"],
                       layer["act"])
     if t == "maxpool":

@@ -250,6 +250,7 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
       a.act = L.d.act;
       a.ws = ws;
       a.ws_bytes = ws_bytes;
+      a.res = L.inputs.size() > 1 ? in[1] : nullptr;
       if (L.d.groups > 1) {
         k::dwconv(dt, a, st);
       } else if (r.algo == SN_ALGO_DIRECT) {

@@ -66,6 +66,7 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
   std::vector<Routine> out;
   if (L.type == SN_LAYER_INPUT) return out;
   const Shape& in = g.layers[L.inputs[0]].out;
+  const int residual = L.type == SN_LAYER_CONV2D && L.inputs.size() == 2;
   auto add = [&](int layout, int algo, int param) {
     Routine r;
     r.id = (int)out.size();
@@ -88,10 +89,11 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
           int np = g.opt_params ? k::igemm_num_params(g.dtype) : 1;
           for (int p = 0; p < np; ++p)
             if (k::igemm_param_valid(g.dtype, p, lay, in.n, in.c, in.h, in.w, L.d.r, L.d.s, L.d.stride,
-                                     L.d.pad))
+                                     L.d.pad) &&
+                (residual == 0 || k::igemm_param_takes_residual(g.dtype, p)))
               add(lay, SN_ALGO_IGEMM, p);
         }
-        if ((g.opt_algos >> SN_ALGO_WINOGRAD & 1) && winograd_applicable(L, in))
+        if ((g.opt_algos >> SN_ALGO_WINOGRAD & 1) && !residual && winograd_applicable(L, in))
           add(lay, SN_ALGO_WINOGRAD, 0);
         break;
       case SN_LAYER_FC:
@@ -129,6 +131,7 @@ int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int
   L.type = d.type;
   L.d = d;
   int want = d.type == SN_LAYER_ADD ? 2 : 1;
+  if (d.type == SN_LAYER_CONV2D && n_inputs == 2) want = 2;  // convolution with a residual
   if (d.type < SN_LAYER_CONV2D || d.type > SN_LAYER_FC)
     fail(SN_E_INVALID, "unknown layer type " + std::to_string(d.type));
   if (n_inputs != want || !inputs)
@@ -155,6 +158,10 @@ int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int
         fail(SN_E_SHAPE, "kernel larger than the padded input");
       out = {in.n, d.k, outdim(in.h, d.r, d.stride, d.pad), outdim(in.w, d.s, d.stride, d.pad)};
       wbytes = (int64_t)d.k * (in.c / d.groups) * d.r * d.s * ds;
+      if (L.inputs.size() == 2) {
+        if (d.groups != 1) fail(SN_E_UNSUPPORTED, "a residual input needs a dense convolution");
+        if (!(g.layers[L.inputs[1]].out == out)) fail(SN_E_SHAPE, "residual differs from the output shape");
+      }
       if (!weight) fail(SN_E_INVALID, "convolution needs weights");
       break;
     }

@@ -49,7 +49,47 @@ struct IgArgs {
   long long x_elems, w_elems;  // elements addressable per blockIdx.z (buffer ranges)
   long long y_elems;
   float inv_pq, inv_q;         // 1/(P*Q), 1/Q for sdiv
+  const void* res;             // residual [M][Ng] in the output layout, or null
 };
+
+// Element offset of GEMM position (m, n) in the output tensor's layout (the
+// residual has the output's shape and layout).
+template <int L>
+__device__ __forceinline__ long long out_index(const IgArgs& a, int m, int n) {
+  if constexpr (L == NHWC) {
+    return (long long)m * a.Ks + n;
+  } else {
+    const int img = m / a.PQ, pq = m - img * a.PQ;
+    if constexpr (L == NCHW) return ((long long)img * a.Ks + n) * a.PQ + pq;
+    else return (((long long)img * (a.Ks >> 3) + (n >> 3)) * a.PQ + pq) * 8 + (n & 7);
+  }
+}
+
+// Residual values of channels n..n+3 of row m (zero outside the tensor).
+template <typename T, int L>
+__device__ __forceinline__ void residual4(const IgArgs& a, int m, int n, float (&r)[4]) {
+  const T* rp = reinterpret_cast<const T*>(a.res);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) r[v] = 0.f;
+  if (m >= a.M) return;
+  if (L != NCHW && n + 4 <= a.Ng && (L == NC8 || (a.Ks & 3) == 0)) {
+    // 4 consecutive channels: 8 bytes (16-bit types) or 16 bytes (fp32)
+    T t[4];
+    if constexpr (sizeof(T) == 2) {
+      const u32x2 w = *reinterpret_cast<const u32x2*>(rp + out_index<L>(a, m, n));
+      __builtin_memcpy(t, &w, 8);
+    } else {
+      const u32x4 w = *reinterpret_cast<const u32x4*>(rp + out_index<L>(a, m, n));
+      __builtin_memcpy(t, &w, 16);
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) r[v] = to_f(t[v]);
+  } else {
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      if (n + v < a.Ng) r[v] = to_f(rp[out_index<L>(a, m, n + v)]);
+  }
+}
 
 template <typename T>
 __device__ __forceinline__ V8<T> bload8(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
@@ -383,9 +423,11 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
           const int ml = wm * WTM + i * 16 + (lane & 15);
+          float rv[4] = {0.f, 0.f, 0.f, 0.f};
+          if (a.res) residual4<T, L>(a, m0 + ml, n0 + nl, rv);
           T o[4];
 #pragma unroll
-          for (int v = 0; v < 4; ++v) o[v] = from_f<T>(act_f(acc[i][j][v] + bv[v], a.act));
+          for (int v = 0; v < 4; ++v) o[v] = from_f<T>(act_f(acc[i][j][v] + bv[v] + rv[v], a.act));
           __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
         }
       }
@@ -400,7 +442,10 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const int ml = wm * WTM + i * 16 + (lane >> 4) * 4 + v;
-            Cs[ml][nl] = from_f<T>(act_f(acc[i][j][v] + bv, a.act));
+            float rv = 0.f;
+            if (a.res && m0 + ml < a.M && n < a.Ng)
+              rv = to_f(reinterpret_cast<const T*>(a.res)[out_index<L>(a, m0 + ml, n)]);
+            Cs[ml][nl] = from_f<T>(act_f(acc[i][j][v] + bv + rv, a.act));
           }
       }
     }
@@ -530,6 +575,32 @@ void igemm_dma_kernel(IgArgs a) {
 #pragma unroll
       for (int v = 0; v < 4; ++v)
         bias[j][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n + v) * 4, 0, 0));
+    }
+  }
+
+  // residual of the lane's 4 channels of each output pixel, loaded now so
+  // that it arrives during the main loop (8 bytes per accumulator)
+  u32x2 resv[EPI == EPI_LAYOUT ? FM : 1][FN];
+  if constexpr (EPI == EPI_LAYOUT) {
+    if (a.res) {
+      const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.res, a.y_elems * 2);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int m = m0 + wm * WTM + i * 16 + (lane & 15);
+          const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
+          unsigned off = kOOB;
+          if (m < a.M && n < a.Ng) {
+            if constexpr (L == NC8) {
+              const int img = sdiv(m, a.inv_pq), pq = m - __mul24(img, a.PQ);
+              off = (unsigned)(((img * (a.Ks >> 3) + (n >> 3)) * a.PQ + pq) * 8 + (n & 7)) * 2u;
+            } else {
+              off = (unsigned)(m * a.Ks + n) * 2u;
+            }
+          }
+          resv[i][j] = __builtin_amdgcn_raw_buffer_load_b64(rr, (int)off, 0, 0);
+        }
     }
   }
 
@@ -695,9 +766,16 @@ void igemm_dma_kernel(IgArgs a) {
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const int ml = wm * WTM + i * 16 + (lane & 15);
+        float rv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (a.res) {
+          T t[4];
+          __builtin_memcpy(t, &resv[i][j], 8);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) rv[v] = to_f(t[v]);
+        }
         T o[4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v], ac.lo, ac.hi));
+        for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v] + rv[v], ac.lo, ac.hi));
         __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
       }
     }
@@ -744,7 +822,9 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(IgArgs a) {
     float s = a.bias[n];
     for (int k = 0; k < a.splits; ++k) s += a.part[k * plane + (long long)m * a.Ng + n];
     const int img = m / a.PQ, pq = m - img * a.PQ;
-    y[((long long)img * a.Ks + n) * a.PQ + pq] = from_f<T>(act_f(s, a.act));
+    const long long o = ((long long)img * a.Ks + n) * a.PQ + pq;
+    if (a.res) s += to_f(reinterpret_cast<const T*>(a.res)[o]);
+    y[o] = from_f<T>(act_f(s, a.act));
   } else {
     const int NB8 = (a.Ng + 7) / 8;
     if (idx >= (long long)a.M * NB8) return;
@@ -758,6 +838,12 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(IgArgs a) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         if (n0 + e < a.Ng) s[e] += p[e];
+    }
+    if (a.res) {
+      const T* rp = reinterpret_cast<const T*>(a.res);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (n0 + e < a.Ng) s[e] += to_f(rp[out_index<L>(a, m, n0 + e)]);
     }
     V8<T> o;
 #pragma unroll
@@ -835,6 +921,12 @@ bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, in
     return vec && ((c + 7) / 8) % (g.bk / 8) == 0 && r * s <= 32 && m + p * q < (1 << 21);
   }
   return vec || 256 % g.bm == 0;
+}
+
+bool igemm_param_takes_residual(int dtype, int param) {
+  if (param < 0 || param >= igemm_num_params(dtype)) return false;
+  const IgCfg& g = dtype == 0 ? kIg32[param] : kIg16[param];
+  return g.dma == 0 || g.dma == 1;
 }
 
 static IgCfg ig_cfg(int dtype, int param) {
@@ -1016,6 +1108,7 @@ static IgArgs make_ig(const ConvArgs& c) {
   a.y_elems = (long long)c.yd.n * c.yd.cs * c.yd.h * c.yd.w;
   a.inv_pq = 1.f / (float)std::max(a.PQ, 1);
   a.inv_q = 1.f / (float)std::max(a.Q, 1);
+  a.res = c.res;
   return a;
 }
 
@@ -1051,6 +1144,7 @@ static void igemm_run(const IgCfg& cfg, IgArgs& a, const ConvArgs& c, hipStream_
 template <typename T>
 static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t st) {
   const IgCfg cfg = ig_cfg(dtype, param);
+  check(!c.res || cfg.dma == 0 || cfg.dma == 1, "this tile configuration takes no residual");
   if (cfg.dma == 2) {
     conv_patch(dtype, cfg.pc, c, st);
     return;
@@ -1148,7 +1242,9 @@ __global__ __launch_bounds__(256) void direct_kernel(IgArgs a) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int n = n0 + j;
-    out[j] = from_f<T>(act_f(acc[j] + (n < a.Ng ? a.bias[n] : 0.f), a.act));
+    float rv = 0.f;
+    if (a.res && n < a.Ng) rv = to_f(reinterpret_cast<const T*>(a.res)[out_index<L>(a, m, n)]);
+    out[j] = from_f<T>(act_f(acc[j] + (n < a.Ng ? a.bias[n] : 0.f) + rv, a.act));
   }
   if constexpr (L == NCHW) {
 #pragma unroll
@@ -1449,6 +1545,7 @@ static void wino_dispatch(int dtype, const ConvArgs& c, hipStream_t st) {
 }
 
 void conv_winograd(int dtype, const ConvArgs& c, hipStream_t st) {
+  check(!c.res, "Winograd routine takes no residual");
   if (dtype == 0) wino_dispatch<float>(dtype, c, st);
   else if (dtype == 1) wino_dispatch<f16>(dtype, c, st);
   else wino_dispatch<bf16>(dtype, c, st);
@@ -1583,6 +1680,7 @@ static void dw_dispatch(const ConvArgs& c, hipStream_t st) {
 }
 
 void dwconv(int dtype, const ConvArgs& c, hipStream_t st) {
+  check(!c.res, "depthwise routine takes no residual");
   if (dtype == 0) dw_dispatch<float>(c, st);
   else if (dtype == 1) dw_dispatch<f16>(c, st);
   else dw_dispatch<bf16>(c, st);

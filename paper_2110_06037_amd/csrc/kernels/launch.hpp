@@ -48,6 +48,8 @@ struct ConvArgs {
   int r, s, stride, pad, act;
   void* ws;           // workspace (winograd); ws_bytes its size
   size_t ws_bytes;
+  const void* res = nullptr;  // residual of the output's shape and layout, added before the
+                              // activation (direct and implicit-GEMM routines), or null
 };
 
 void conv_direct(int dtype, const ConvArgs& a, hipStream_t st);
@@ -55,6 +57,8 @@ void conv_direct(int dtype, const ConvArgs& a, hipStream_t st);
 // Parameters that split the reduction need a workspace of igemm_ws_bytes.
 void conv_igemm(int dtype, int param, const ConvArgs& a, hipStream_t st);
 int igemm_num_params(int dtype);
+// whether the tile configuration adds a residual in its epilogue
+bool igemm_param_takes_residual(int dtype, int param);
 bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, int w, int r, int s,
                        int stride, int pad);
 size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s);

@@ -87,10 +87,12 @@ class Graph:
                                       ctypes.byref(out)))
         return out.value
 
-    def add_conv(self, inp, weight, bias, stride=1, pad=0, groups=1, act="none"):
+    def add_conv(self, inp, weight, bias, stride=1, pad=0, groups=1, act="none", residual=None):
+        """Convolution; ``residual`` (a layer id) is added before the activation."""
         k, _, r, s = weight.shape
         d = N.LayerDesc(N.L_CONV2D, k, r, s, stride, pad, groups, N.ACT[act])
-        return self._add(d, [inp], weight, bias)
+        ins = [inp] if residual is None else [inp, residual]
+        return self._add(d, ins, weight, bias)
 
     def add_maxpool(self, inp, k=3, stride=2, pad=1):
         return self._add(N.LayerDesc(N.L_MAXPOOL, 0, k, k, stride, pad, 1, 0), [inp])
@@ -109,8 +111,9 @@ class Graph:
         """Add one layer given as a ``workloads`` spec dict."""
         t = layer["type"]
         if t == "conv":
+            res = layer["in"][1] if len(layer["in"]) > 1 else None
             return self.add_conv(layer["in"][0], weight, bias, layer["stride"], layer["pad"],
-                                 layer["groups"], layer["act"])
+                                 layer["groups"], layer["act"], res)
         if t == "maxpool":
             return self.add_maxpool(layer["in"][0], layer["k"], layer["stride"], layer["pad"])
         if t == "gap":

@@ -11,7 +11,7 @@ from oracle import numeric as O
 from oracle.select import blockwise, exhaustive, problem_from_costs
 from paper_2110_06037_amd import build_from_spec, native as N
 from tests.gpu_util import TOL, err, from_dev, to_dev
-from workloads import (CONV_SWEEP_SHAPES, conv_sweep, generate, mobilenet_v2, resnet18, resnet50,
+from workloads import (CONV_SWEEP_SHAPES, conv_sweep, fuse_residual, generate, mobilenet_v2, resnet18, resnet50,
                        tiny_chain, to_f64, with_batch)
 
 pytestmark = pytest.mark.gpu
@@ -88,11 +88,14 @@ def test_integrated_profiling_selects_the_measured_fastest_candidate(name):
     g.close()
 
 
-@pytest.mark.parametrize("name", ["resnet18", "mobilenetv2", "resnet50_bf16", "resnet50_f16"])
+@pytest.mark.parametrize("name", ["resnet18", "mobilenetv2", "resnet50_bf16", "resnet50_f16",
+                                  "resnet50_fused", "mobilenetv2_fused"])
 def test_net_dp_and_fixed_paths_match_oracle(name):
     spec = {"resnet18": lambda: resnet18(1), "mobilenetv2": lambda: mobilenet_v2(1),
             "resnet50_bf16": lambda: resnet50(1, "bf16"),
-            "resnet50_f16": lambda: resnet50(1, "f16")}[name]()
+            "resnet50_f16": lambda: resnet50(1, "f16"),
+            "resnet50_fused": lambda: fuse_residual(resnet50(1, "bf16")),
+            "mobilenetv2_fused": lambda: fuse_residual(mobilenet_v2(1))}[name]()
     t = generate(spec)
     g = build_from_spec(spec, t)
     g.profile(warmup=2, reps=5)

@@ -164,3 +164,41 @@ def test_add_and_converters_bit_exact(dtype, c):
                 g.set_path(ids)
                 out = from_dev(g.run(xd), dtype)
                 assert np.array_equal(out, ref), ids
+
+
+RESIDUAL_CASES = [
+    # (N, C, H, W, R, act): K = C, stride 1, so the residual is an ADD of the input with itself
+    (2, 64, 9, 11, 1, "relu"),      # pointwise, LDS-DMA tiles apply (C % 64 == 0)
+    (1, 128, 7, 7, 1, "none"),      # linear, as in an inverted-residual projection
+    (2, 24, 13, 11, 3, "relu6"),    # 3x3, C % 8 == 0 but not a multiple of 32
+    (3, 40, 5, 5, 1, "relu"),       # K = 40: channel tiles with a ragged end
+    (1, 256, 14, 14, 1, "relu"),    # split-reduction parameters apply
+]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("ci", range(len(RESIDUAL_CASES)))
+def test_conv_with_residual_every_routine(dtype, ci):
+    # y = act(conv(x) + b + r): every routine that takes a residual, against
+    # the oracle's conv (no activation) + add (with the activation) in fp64
+    n, c, h, w, r, act = RESIDUAL_CASES[ci]
+    spec_layers = [{"type": "add", "in": [0, 0], "act": "none"},
+                   {"type": "conv", "in": [0, 1], "k": c, "r": r, "s": r, "stride": 1,
+                    "pad": r // 2, "groups": 1, "act": act}]
+    x = random_tensor((n, c, h, w), dtype, seed=40 + ci)
+    wt = random_tensor((c, c, r, r), dtype, seed=50 + ci, dist="normal", scale=np.sqrt(2 / (c * r * r)))
+    b = random_tensor((c,), "f32", seed=60 + ci, scale=0.1)
+    xs = to_f64(x, dtype)
+    res = O.round_to(O.layer_forward(spec_layers[0], [xs, xs]), dtype)
+    ref = O.round_to(O.layer_forward(spec_layers[1], [xs, res], to_f64(wt, dtype), b.astype(np.float64)), dtype)
+    g = single_layer_graph(dtype, (n, c, h, w), spec_layers[0])
+    g.add_spec(spec_layers[1], wt, b)
+    algos = {rt["algo"] for rt in g.routines(2)}
+    assert 2 not in algos, "no Winograd routine takes a residual"
+    xd = to_dev(x, dtype)
+    for rt in g.routines(2):
+        out = from_dev(run_routine(g, rt["id"], xd, n_layers=3), dtype)
+        e = err(out, ref, dtype)
+        print(f"{dtype} residual case{ci} {rt['name']}: err {e:.2e}", flush=True)
+        assert e <= TOL[dtype], (rt["name"], e)
+    g.close()

@@ -8,7 +8,8 @@ paper's auxiliary input layer, Sec. IV-E); layers 1..n are listed in
 * ``{"type": "conv", "in": [j], "k": K, "r": R, "s": S, "stride": st,
   "pad": p, "groups": g, "act": "none"|"relu"|"relu6"}`` -- 2-D convolution
   (cross-correlation) with a fused activation; ``groups`` is 1 (dense) or the
-  channel count (depthwise).  Batch-norm layers of the original models are
+  channel count (depthwise).  ``"in": [j, r]`` adds layer r's output (a
+  residual of the output's shape) before the activation.  Batch-norm layers of the original models are
   taken as folded into the convolution bias, as the paper's importer does
   when it fuses BN and ReLU into the preceding layer (Sec. III-A).
 * ``{"type": "maxpool", "in": [j], "k": 3, "stride": 2, "pad": 1}``
@@ -199,3 +200,59 @@ def channels(spec):
         else:
             ch.append(ch[layer["in"][0]])
     return ch
+
+
+def fuse_residual(spec, tensors=None, only_1x1=True):
+    """Structure-only transform: every residual add whose operand is a dense
+    convolution without activation, consumed by that add alone (a 1x1 one if
+    ``only_1x1``), becomes that convolution with the add's other operand as
+    residual input and the add's activation, placed where the add was (all
+    its inputs come earlier).  Returns the new spec and, if given, the
+    generated tensors re-listed for the new layer order (no value changes)."""
+    layers = spec["layers"]
+    n = len(layers)
+    consumers = {i: [] for i in range(n + 1)}
+    for i, layer in enumerate(layers, start=1):
+        for j in layer["in"]:
+            consumers[j].append(i)
+    fused_into = {}   # add id -> conv id
+    for i, layer in enumerate(layers, start=1):
+        if layer["type"] != "add":
+            continue
+        for a, b in ((layer["in"][0], layer["in"][1]), (layer["in"][1], layer["in"][0])):
+            if a == 0:
+                continue
+            c = layers[a - 1]
+            if (c["type"] == "conv" and len(c["in"]) == 1 and c["groups"] == 1 and c["act"] == "none"
+                    and consumers[a] == [i] and a not in fused_into.values()
+                    and (not only_1x1 or (c["r"] == 1 and c["s"] == 1))):
+                fused_into[i] = a
+                break
+    gone = set(fused_into.values())
+    order = []        # old ids in the new order; an add's slot takes its conv
+    for i in range(1, n + 1):
+        if i in gone:
+            continue
+        order.append(fused_into.get(i, i))
+    new_id = {0: 0}
+    for k, old in enumerate(order, start=1):
+        new_id[old] = k
+    for add_id, conv_id in fused_into.items():
+        new_id[add_id] = new_id[conv_id]
+    out_layers = []
+    for old in order:
+        lay = copy.deepcopy(layers[old - 1])
+        add_id = next((a for a, c in fused_into.items() if c == old), None)
+        if add_id is not None:
+            add = layers[add_id - 1]
+            other = add["in"][1] if add["in"][0] == old else add["in"][0]
+            lay["in"] = [lay["in"][0], other]
+            lay["act"] = add.get("act", "none")
+        lay["in"] = [new_id[j] for j in lay["in"]]
+        out_layers.append(lay)
+    out = dict(spec, layers=out_layers, name=spec["name"] + "_fused")
+    if tensors is None:
+        return out
+    t2 = dict(tensors, w=[tensors["w"][old - 1] for old in order], b=[tensors["b"][old - 1] for old in order])
+    return out, t2
+
