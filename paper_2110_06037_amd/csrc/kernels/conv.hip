@@ -503,11 +503,13 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
 
 // LDS bytes of an LDS-DMA tile configuration, and the workgroups per CU it
 // allows (the occupancy the register allocation is sized for).
+// (the epilogue tile: fp32 rows of BN + 4 values, which also hold the
+// 16-bit rows of BN + 8 values)
 template <int BM, int BN, int BK, int ST, int EPI>
 constexpr int dma_lds_bytes() {
-  return ST * (BM + BN) * BK * 2 > (EPI == EPI_LAYOUT ? BM * (BN + 8) * 2 : 0)
+  return ST * (BM + BN) * BK * 2 > (EPI == EPI_LAYOUT ? BM * (BN + 4) * 4 : 0)
              ? ST * (BM + BN) * BK * 2
-             : (EPI == EPI_LAYOUT ? BM * (BN + 8) * 2 : 0);
+             : (EPI == EPI_LAYOUT ? BM * (BN + 4) * 4 : 0);
 }
 template <int BM, int BN, int BK, int ST, int EPI, int NWV = 4>
 constexpr int dma_occ() {
@@ -540,7 +542,7 @@ void igemm_dma_kernel(IgArgs a) {
   constexpr int FM = WTM / 16, FN = WTN / 16;
   constexpr int A_BYTES = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
   constexpr int CPAD = 8;
-  constexpr int SM_C = EPI == EPI_LAYOUT ? BM * (BN + CPAD) * 2 : 0;
+  constexpr int SM_C = EPI == EPI_LAYOUT ? BM * (BN + 4) * 4 : 0;  // fp32 epilogue rows
   constexpr int SM = ST * STAGE > SM_C ? ST * STAGE : SM_C;
   __shared__ __attribute__((aligned(1024))) char smem[SM];
   auto swz = [](int row) { return (row / RPR) % CPR; };
@@ -575,32 +577,6 @@ void igemm_dma_kernel(IgArgs a) {
 #pragma unroll
       for (int v = 0; v < 4; ++v)
         bias[j][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n + v) * 4, 0, 0));
-    }
-  }
-
-  // residual of the lane's 4 channels of each output pixel, loaded now so
-  // that it arrives during the main loop (8 bytes per accumulator)
-  u32x2 resv[EPI == EPI_LAYOUT ? FM : 1][FN];
-  if constexpr (EPI == EPI_LAYOUT) {
-    if (a.res) {
-      const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.res, a.y_elems * 2);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int m = m0 + wm * WTM + i * 16 + (lane & 15);
-          const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
-          unsigned off = kOOB;
-          if (m < a.M && n < a.Ng) {
-            if constexpr (L == NC8) {
-              const int img = sdiv(m, a.inv_pq), pq = m - __mul24(img, a.PQ);
-              off = (unsigned)(((img * (a.Ks >> 3) + (n >> 3)) * a.PQ + pq) * 8 + (n & 7)) * 2u;
-            } else {
-              off = (unsigned)(m * a.Ks + n) * 2u;
-            }
-          }
-          resv[i][j] = __builtin_amdgcn_raw_buffer_load_b64(rr, (int)off, 0, 0);
-        }
     }
   }
 
@@ -756,6 +732,50 @@ void igemm_dma_kernel(IgArgs a) {
           }
         }
       }
+  } else if (a.res && (L == NC8 || a.Ks % 8 == 0)) {
+    // residual: the fp32 sums go through LDS, and each thread adds the
+    // residual to 8 channels of one output row as it stores them, reading
+    // and writing whole 16-byte chunks of consecutive channels
+    __syncthreads();  // every wave is done with the last tile
+    float(*Cf)[BN + 4] = reinterpret_cast<float(*)[BN + 4]>(smem);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int nl = wn * WTN + j * 16 + (lane >> 4) * 4;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) *reinterpret_cast<f32x4*>(&Cf[wm * WTM + i * 16 + (lane & 15)][nl]) = acc[i][j];
+    }
+    __syncthreads();
+    const ActClamp ac = act_clamp(a.act);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(a.y, a.y_elems * 2);
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.res, a.y_elems * 2);
+    constexpr int IT = (BM * BN / 8 + NT - 1) / NT;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + it * NT;
+      const int row = idx / (BN / 8), cj = idx % (BN / 8);
+      const int m = m0 + row, n = n0 + cj * 8;
+      unsigned off = kOOB;
+      if (idx < BM * BN / 8 && m < a.M && n < a.Ng) {
+        if constexpr (L == NC8) {
+          const int img = sdiv(m, a.inv_pq), pq = m - __mul24(img, a.PQ);
+          off = (unsigned)(((img * (a.Ks >> 3) + (n >> 3)) * a.PQ + pq) * 8) * 2u;
+        } else {
+          off = (unsigned)(m * a.Ks + n) * 2u;
+        }
+      }
+      const u32x4 rraw = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
+      T rt[8], o[8];
+      __builtin_memcpy(rt, &rraw, 16);
+      const int rrow = idx < BM * BN / 8 ? row : 0;
+      const f32x4 c0 = *reinterpret_cast<const f32x4*>(&Cf[rrow][cj * 8]);
+      const f32x4 c1 = *reinterpret_cast<const f32x4*>(&Cf[rrow][cj * 8 + 4]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o[e] = from_f<T>(__builtin_amdgcn_fmed3f(c0[e] + to_f(rt[e]), ac.lo, ac.hi));
+        o[4 + e] = from_f<T>(__builtin_amdgcn_fmed3f(c1[e] + to_f(rt[4 + e]), ac.lo, ac.hi));
+      }
+      __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4*>(o), ry, (int)off, 0, 0);
+    }
   } else {
     __syncthreads();  // every wave is done with the last tile
     T(*Cs)[BN + CPAD] = reinterpret_cast<T(*)[BN + CPAD]>(smem);
@@ -767,12 +787,7 @@ void igemm_dma_kernel(IgArgs a) {
       for (int i = 0; i < FM; ++i) {
         const int ml = wm * WTM + i * 16 + (lane & 15);
         float rv[4] = {0.f, 0.f, 0.f, 0.f};
-        if (a.res) {
-          T t[4];
-          __builtin_memcpy(t, &resv[i][j], 8);
-#pragma unroll
-          for (int v = 0; v < 4; ++v) rv[v] = to_f(t[v]);
-        }
+        if (a.res) residual4<T, L>(a, m0 + ml, n0 + nl, rv);  // rows without 16-byte chunks
         T o[4];
 #pragma unroll
         for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v] + rv[v], ac.lo, ac.hi));
