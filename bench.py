@@ -90,7 +90,8 @@ ALL_KERNEL_SOURCES = ("conv.hip", "conv_patch.hip", "conv_smallc.hip", "misc.hip
 def kernel_source_hash(ksub=None):
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES.get(ksub, ALL_KERNEL_SOURCES):
+    files = next((v for k, v in KERNEL_SOURCES.items() if ksub and k in ksub), ALL_KERNEL_SOURCES)
+    for f in files:
         with open(os.path.join(KDIR, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
