@@ -90,7 +90,7 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
           for (int p = 0; p < np; ++p)
             if (k::igemm_param_valid(g.dtype, p, lay, in.n, in.c, in.h, in.w, L.d.r, L.d.s, L.d.stride,
                                      L.d.pad) &&
-                (residual == 0 || k::igemm_param_takes_residual(g.dtype, p)))
+                (residual == 0 || k::igemm_param_takes_residual(g.dtype, p, lay, L.d.k)))
               add(lay, SN_ALGO_IGEMM, p);
         }
         if ((g.opt_algos >> SN_ALGO_WINOGRAD & 1) && !residual && winograd_applicable(L, in))

@@ -420,15 +420,26 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
         float bv[4];
 #pragma unroll
         for (int v = 0; v < 4; ++v) bv[v] = n0 + nl + v < a.Ng ? a.bias[n0 + nl + v] : 0.f;
+        if (a.res) {
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-          const int ml = wm * WTM + i * 16 + (lane & 15);
-          float rv[4] = {0.f, 0.f, 0.f, 0.f};
-          if (a.res) residual4<T, L>(a, m0 + ml, n0 + nl, rv);
-          T o[4];
+          for (int i = 0; i < FM; ++i) {
+            const int ml = wm * WTM + i * 16 + (lane & 15);
+            float rv[4];
+            residual4<T, L>(a, m0 + ml, n0 + nl, rv);
+            T o[4];
 #pragma unroll
-          for (int v = 0; v < 4; ++v) o[v] = from_f<T>(act_f(acc[i][j][v] + bv[v] + rv[v], a.act));
-          __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
+            for (int v = 0; v < 4; ++v) o[v] = from_f<T>(act_f(acc[i][j][v] + bv[v] + rv[v], a.act));
+            __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < FM; ++i) {
+            const int ml = wm * WTM + i * 16 + (lane & 15);
+            T o[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) o[v] = from_f<T>(act_f(acc[i][j][v] + bv[v], a.act));
+            __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
+          }
         }
       }
     } else {
@@ -437,16 +448,26 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
         const int nl = wn * WTN + j * 16 + (lane & 15);
         const int n = n0 + nl;
         const float bv = n < a.Ng ? a.bias[n] : 0.f;
+        if (a.res) {
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+          for (int i = 0; i < FM; ++i)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int ml = wm * WTM + i * 16 + (lane >> 4) * 4 + v;
-            float rv = 0.f;
-            if (a.res && m0 + ml < a.M && n < a.Ng)
-              rv = to_f(reinterpret_cast<const T*>(a.res)[out_index<L>(a, m0 + ml, n)]);
-            Cs[ml][nl] = from_f<T>(act_f(acc[i][j][v] + bv + rv, a.act));
-          }
+            for (int v = 0; v < 4; ++v) {
+              const int ml = wm * WTM + i * 16 + (lane >> 4) * 4 + v;
+              float rv = 0.f;
+              if (m0 + ml < a.M && n < a.Ng)
+                rv = to_f(reinterpret_cast<const T*>(a.res)[out_index<L>(a, m0 + ml, n)]);
+              Cs[ml][nl] = from_f<T>(act_f(acc[i][j][v] + bv + rv, a.act));
+            }
+        } else {
+#pragma unroll
+          for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int ml = wm * WTM + i * 16 + (lane >> 4) * 4 + v;
+              Cs[ml][nl] = from_f<T>(act_f(acc[i][j][v] + bv, a.act));
+            }
+        }
       }
     }
     __syncthreads();
@@ -732,8 +753,10 @@ void igemm_dma_kernel(IgArgs a) {
           }
         }
       }
-  } else if (a.res && (L == NC8 || a.Ks % 8 == 0)) {
-    // residual: the fp32 sums go through LDS, and each thread adds the
+  } else if (a.res) {
+    // residual (output rows of whole 16-byte chunks: NC8HW8, or NHWC with
+    // K % 8 == 0, which the routine's validity requires): the fp32 sums go
+    // through LDS, and each thread adds the
     // residual to 8 channels of one output row as it stores them, reading
     // and writing whole 16-byte chunks of consecutive channels
     __syncthreads();  // every wave is done with the last tile
@@ -786,11 +809,9 @@ void igemm_dma_kernel(IgArgs a) {
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const int ml = wm * WTM + i * 16 + (lane & 15);
-        float rv[4] = {0.f, 0.f, 0.f, 0.f};
-        if (a.res) residual4<T, L>(a, m0 + ml, n0 + nl, rv);  // rows without 16-byte chunks
         T o[4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v] + rv[v], ac.lo, ac.hi));
+        for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v], ac.lo, ac.hi));
         __builtin_memcpy(&Cs[ml][nl], o, sizeof(o));
       }
     }
@@ -907,6 +928,9 @@ static const IgCfg kIg16[] = {
     {128, 64, 64, 0, 0, 1, 4, 4, 0, {}, 8},  {256, 64, 64, 0, 0, 1, 8, 3, 0, {}, 8},
     {64, 128, 64, 0, 0, 1, 2, 4, 0, {}, 8},  {128, 256, 64, 0, 0, 1, 2, 3, 0, {}, 8},
     {128, 128, 32, 0, 0, 1, 4, 4, 0, {}, 8}, {256, 128, 32, 0, 0, 1, 4, 4, 0, {}, 8},
+    // deep pipelines for the small-M layers (more bytes in flight per CU)
+    {64, 128, 64, 0, 0, 1, 2, 6, 0, {}, 8},  {128, 64, 64, 0, 0, 1, 4, 6, 0, {}, 8},
+    {128, 128, 32, 0, 0, 1, 4, 6, 0, {}, 8}, {64, 64, 64, 0, 0, 1, 2, 6, 0, {}, 8},
     // 3x3 stride-1 patch kernel
 #define SN_PATCH_IG(FMT, BN, PWT, WM, WN, TG, ST, PROWS) \
   {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS}},
@@ -938,10 +962,10 @@ bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, in
   return vec || 256 % g.bm == 0;
 }
 
-bool igemm_param_takes_residual(int dtype, int param) {
+bool igemm_param_takes_residual(int dtype, int param, int layout, int k) {
   if (param < 0 || param >= igemm_num_params(dtype)) return false;
   const IgCfg& g = dtype == 0 ? kIg32[param] : kIg16[param];
-  return g.dma == 0 || g.dma == 1;
+  return g.dma == 0 || (g.dma == 1 && (layout == NC8 || k % 8 == 0));
 }
 
 static IgCfg ig_cfg(int dtype, int param) {
@@ -1028,6 +1052,10 @@ static void igemm_dma_cfg(const IgCfg& c, const IgArgs& a, hipStream_t st) {
     IGDN(128, 256, 64, 2, 3, 8)
     IGDN(128, 128, 32, 4, 4, 8)
     IGDN(256, 128, 32, 4, 4, 8)
+    IGDN(64, 128, 64, 2, 6, 8)
+    IGDN(128, 64, 64, 4, 6, 8)
+    IGDN(128, 128, 32, 4, 6, 8)
+    IGDN(64, 64, 64, 2, 6, 8)
     default: check(false, "LDS-DMA tile not instantiated");
   }
 #undef IGD
@@ -1159,7 +1187,8 @@ static void igemm_run(const IgCfg& cfg, IgArgs& a, const ConvArgs& c, hipStream_
 template <typename T>
 static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t st) {
   const IgCfg cfg = ig_cfg(dtype, param);
-  check(!c.res || cfg.dma == 0 || cfg.dma == 1, "this tile configuration takes no residual");
+  check(!c.res || cfg.dma == 0 || (cfg.dma == 1 && (c.yd.layout == NC8 || c.yd.cs % 8 == 0)),
+        "this tile configuration takes no residual");
   if (cfg.dma == 2) {
     conv_patch(dtype, cfg.pc, c, st);
     return;

@@ -57,8 +57,9 @@ void conv_direct(int dtype, const ConvArgs& a, hipStream_t st);
 // Parameters that split the reduction need a workspace of igemm_ws_bytes.
 void conv_igemm(int dtype, int param, const ConvArgs& a, hipStream_t st);
 int igemm_num_params(int dtype);
-// whether the tile configuration adds a residual in its epilogue
-bool igemm_param_takes_residual(int dtype, int param);
+// whether the tile configuration adds a residual in its epilogue (for an
+// output of k channels in the layout)
+bool igemm_param_takes_residual(int dtype, int param, int layout, int k);
 bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, int w, int r, int s,
                        int stride, int pad);
 size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s);
