@@ -44,20 +44,25 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const T* __restrict__ x, T
     }
     y[idx] = from_f<T>(m);
   } else {
+    // 32-bit index arithmetic (the host checks N * P * Q * CB < 2^31): the
+    // 64-bit divisions it replaces cost more than the nine 16-byte loads
     const int CB = (Cs + 7) / 8;
     const bool vec = L == NC8 || C % 8 == 0;
-    if (idx >= (long long)N * PQ * CB) return;
+    const unsigned total = (unsigned)N * (unsigned)PQ * (unsigned)CB;
+    const unsigned id = (unsigned)idx;
+    if (idx >= (long long)total) return;
     int cb;
-    long long mm;
+    unsigned mm;
     if constexpr (L == NC8) {
-      mm = idx % ((long long)N * PQ);
-      cb = (int)(idx / ((long long)N * PQ));
+      const unsigned npq = (unsigned)N * (unsigned)PQ;
+      cb = (int)(id / npq);
+      mm = id - (unsigned)cb * npq;
     } else {
-      cb = (int)(idx % CB);
-      mm = idx / CB;
+      mm = id / (unsigned)CB;
+      cb = (int)(id - mm * (unsigned)CB);
     }
-    const int n = (int)(mm / PQ), pq = (int)(mm % PQ);
-    const int p = pq / Q, q = pq - p * Q;
+    const int n = (int)(mm / (unsigned)PQ), pq = (int)(mm - (unsigned)n * (unsigned)PQ);
+    const int p = (int)((unsigned)pq / (unsigned)Q), q = pq - p * Q;
     float m[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) m[e] = -INFINITY;
@@ -103,6 +108,7 @@ static void maxpool_t(const void* x, const TDesc& xd, void* y, const TDesc& yd, 
   check(xd.layout == yd.layout && xd.cs == yd.cs, "pooling keeps the layout");
   long long total = xd.layout == NCHW ? (long long)xd.n * xd.c * yd.h * yd.w
                                       : (long long)xd.n * yd.h * yd.w * ((xd.cs + 7) / 8);
+  check(total < (1ll << 31), "pooling output too large for 32-bit indices");
   const T* xp = reinterpret_cast<const T*>(x);
   T* yp = reinterpret_cast<T*>(y);
 #define MP(LL)                                                                                   \
@@ -323,6 +329,37 @@ __global__ __launch_bounds__(256) void transpose_smallc_kernel(const E* __restri
   }
 }
 
+// NCHW -> NHWC for C <= 8 with 16-bit elements and H * W % 8 == 0: a
+// thread moves 8 consecutive pixels of one image, reading C 16-byte runs
+// (one per channel plane) and writing the 8 * C interleaved values as C
+// 16-byte stores (C is a template constant so the shuffle stays in
+// registers).
+template <typename E, int C>
+__global__ __launch_bounds__(256) void transpose_smallc8_kernel(const E* __restrict__ x, E* __restrict__ y,
+                                                                int HW, int groups) {
+  static_assert(sizeof(E) == 2 && C >= 1 && C <= 8, "16-bit elements, C <= 8");
+  const int g = blockIdx.x * 256 + threadIdx.x;  // group of 8 pixels
+  if (g >= groups) return;
+  const int gpi = HW >> 3;                       // groups per image
+  const int n = g / gpi, hw = (g - n * gpi) * 8;
+  const E* xp = x + ((long long)n * C) * HW + hw;
+  E o[8 * C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const V8<E> t = ld8(xp + (long long)c * HW);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e * C + c] = t.v[e];
+  }
+  E* yp = y + (long long)g * 8 * C;
+#pragma unroll
+  for (int k = 0; k < C; ++k) {
+    V8<E> w;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) w.v[e] = o[k * 8 + e];
+    st8(yp + k * 8, w);
+  }
+}
+
 // Any layout -> any layout, one destination element per thread (padded
 // channels get zero).  Used for the pairs without a specialised kernel.
 template <typename E, int LI, int LO>
@@ -359,6 +396,17 @@ static void convert_e(const void* xv, const TDesc& xd, void* yv, const TDesc& yd
   E* y = reinterpret_cast<E*>(yv);
   const int HW = xd.h * xd.w;
   if ((xd.layout == NCHW && yd.layout == NHWC) || (xd.layout == NHWC && yd.layout == NCHW)) {
+    if constexpr (sizeof(E) == 2) {
+      if (xd.c <= 8 && yd.layout == NHWC && HW % 8 == 0 && (long long)xd.n * HW < (1ll << 31)) {
+        const int groups = xd.n * HW / 8;
+#define T8(CC)                                                                                       \
+  case CC:                                                                                           \
+    SN_LAUNCH((transpose_smallc8_kernel<E, CC>), dim3(blocks(groups)), dim3(256), 0, s, x, y, HW, groups); \
+    return;
+        switch (xd.c) { T8(1) T8(2) T8(3) T8(4) T8(5) T8(6) T8(7) T8(8) }
+#undef T8
+      }
+    }
     if (xd.c <= 8) {
       const long long pixels = (long long)xd.n * HW;
       if (yd.layout == NHWC)

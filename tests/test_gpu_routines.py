@@ -141,13 +141,14 @@ def test_fc(dtype, case):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("c", [12, 3])
-def test_add_and_converters_bit_exact(dtype, c):
+@pytest.mark.parametrize("hw", [(9, 9), (12, 10)])  # H * W % 8 == 0 takes the 8-pixel transpose
+def test_add_and_converters_bit_exact(dtype, c, hw):
     # two maxpools feeding an add: every (layout_a, layout_b, layout_add)
     # combination exercises the converters between all layout pairs (few
     # channels take their own transpose kernel); max and an exactly
     # representable sum keep the result bit-exact
     from paper_2110_06037_amd import Graph
-    n, h, w = 2, 9, 9
+    n, (h, w) = 2, hw
     x = random_tensor((n, c, h, w), dtype, seed=11, dist="int")
     xs = to_f64(x, dtype)
     p = O.maxpool(xs, 3, 1, 1)
