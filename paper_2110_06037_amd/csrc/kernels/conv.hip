@@ -918,7 +918,7 @@ static const IgCfg kIg16[] = {
     {128, 128, 64, 0, 0, 1, 2, 2}, {128, 128, 64, 0, 0, 1, 2, 3}, {256, 64, 64, 0, 0, 1, 4, 2},
     {256, 64, 64, 0, 0, 1, 4, 3},  {128, 64, 64, 0, 0, 1, 2, 3},  {64, 128, 64, 0, 0, 1, 1, 3},
     {256, 128, 64, 0, 0, 1, 2, 2}, {128, 128, 32, 0, 0, 1, 2, 3}, {64, 64, 64, 0, 0, 1, 2, 3},
-    {128, 128, 64, 1, 0, 1, 2, 3}, {128, 64, 64, 1, 0, 1, 2, 3},
+    {128, 128, 64, 1, 0, 1, 2, 3}, {128, 64, 64, 1, 0, 1, 2, 3}, {64, 64, 64, 1, 0, 1, 2, 3},
     // deeper pipelines (short reduction steps, more in flight)
     {128, 128, 32, 0, 0, 1, 2, 4}, {128, 64, 32, 0, 0, 1, 2, 4}, {64, 128, 32, 0, 0, 1, 1, 4},
     {64, 64, 64, 0, 0, 1, 2, 4},   {64, 64, 32, 0, 0, 1, 2, 6},  {256, 64, 32, 0, 0, 1, 4, 4},
@@ -1022,6 +1022,7 @@ static void igemm_dma_cfg(const IgCfg& c, const IgArgs& a, hipStream_t st) {
     switch (key) {
       IGD(128, 128, 64, 2, 3)
       IGD(128, 64, 64, 2, 3)
+      IGD(64, 64, 64, 2, 3)
       default: check(false, "LDS-DMA tile not instantiated for split reduction");
     }
     return;

@@ -153,9 +153,11 @@ __global__ __launch_bounds__(256) void gap_kernel(const T* __restrict__ x, T* __
     float s = 0.f;
     if constexpr (L == NC8) {
       const T* xp = x + ((long long)n * (Cs >> 3) + (c >> 3)) * HW * 8 + (c & 7);
+#pragma unroll 8
       for (int i = 0; i < HW; ++i) s += to_f(xp[(long long)i * 8]);
     } else {
       const T* xp = x + (long long)n * HW * Cs + c;
+#pragma unroll 8
       for (int i = 0; i < HW; ++i) s += to_f(xp[(long long)i * Cs]);
     }
     y[idx] = from_f<T>(s * inv);  // [N][Cs]: N x C x 1 x 1 in every layout
