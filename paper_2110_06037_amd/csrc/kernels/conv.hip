@@ -485,7 +485,8 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
       }
     } else if (L == NC8 || a.Ks % 8 == 0) {
       for (int idx = tid; idx < BM * BN / 8; idx += 256) {
-        const int row = idx / (BN / 8), cj = idx % (BN / 8);
+        // NC8HW8: consecutive threads take consecutive pixels of one channel block
+        const int row = L == NC8 ? idx % BM : idx / (BN / 8), cj = L == NC8 ? idx / BM : idx % (BN / 8);
         const int m = m0 + row, n = n0 + cj * 8;
         if (m >= a.M || n >= a.Ng) continue;
         V8<T> v = ld8(&Cs[row][cj * 8]);
@@ -775,7 +776,8 @@ void igemm_dma_kernel(IgArgs a) {
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int idx = tid + it * NT;
-      const int row = idx / (BN / 8), cj = idx % (BN / 8);
+      // NC8HW8: consecutive threads take consecutive pixels of one channel block
+      const int row = L == NC8 ? idx % BM : idx / (BN / 8), cj = L == NC8 ? idx / BM : idx % (BN / 8);
       const int m = m0 + row, n = n0 + cj * 8;
       unsigned off = kOOB;
       if (idx < BM * BN / 8 && m < a.M && n < a.Ng) {
@@ -789,9 +791,9 @@ void igemm_dma_kernel(IgArgs a) {
       const u32x4 rraw = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
       T rt[8], o[8];
       __builtin_memcpy(rt, &rraw, 16);
-      const int rrow = idx < BM * BN / 8 ? row : 0;
-      const f32x4 c0 = *reinterpret_cast<const f32x4*>(&Cf[rrow][cj * 8]);
-      const f32x4 c1 = *reinterpret_cast<const f32x4*>(&Cf[rrow][cj * 8 + 4]);
+      const int rrow = idx < BM * BN / 8 ? row : 0, rcj = idx < BM * BN / 8 ? cj : 0;
+      const f32x4 c0 = *reinterpret_cast<const f32x4*>(&Cf[rrow][rcj * 8]);
+      const f32x4 c1 = *reinterpret_cast<const f32x4*>(&Cf[rrow][rcj * 8 + 4]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         o[e] = from_f<T>(__builtin_amdgcn_fmed3f(c0[e] + to_f(rt[e]), ac.lo, ac.hi));
@@ -821,7 +823,8 @@ void igemm_dma_kernel(IgArgs a) {
       // 16-byte rows through a buffer resource (32-bit offsets)
       const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, a.y_elems * 2);
       for (int idx = tid; idx < BM * BN / 8; idx += NT) {
-        const int row = idx / (BN / 8), cj = idx % (BN / 8);
+        // NC8HW8: consecutive threads take consecutive pixels of one channel block
+        const int row = L == NC8 ? idx % BM : idx / (BN / 8), cj = L == NC8 ? idx / BM : idx % (BN / 8);
         const int m = m0 + row, n = n0 + cj * 8;
         if (m >= a.M || n >= a.Ng) continue;
         const u32x4 v = *reinterpret_cast<const u32x4*>(&Cs[row][cj * 8]);
