@@ -83,7 +83,7 @@ KERNEL_SOURCES = {
     "igemm_kernel": ("conv.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
     "conv3x3_patch_kernel": ("conv_patch.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
 }
-ALL_KERNEL_SOURCES = ("conv.hip", "conv_patch.hip", "conv_smallc.hip", "misc.hip", "gemm_common.hpp",
+ALL_KERNEL_SOURCES = ("conv.hip", "conv_patch.hip", "conv_smallc.hip", "fc.hip", "misc.hip", "gemm_common.hpp",
                       "kcommon.hpp", "launch.hpp")
 
 

@@ -51,7 +51,7 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
   constexpr int P_BYTES = PPX * 8;
   constexpr int PAIRS = PPX / 2;                 // patch pixel pairs (16 bytes each)
   constexpr int NPF = (PAIRS + 255) / 256;       // pairs per thread
-  constexpr int SM = P_BYTES + BN * WPITCH;
+  constexpr int SM = P_BYTES + BN * WPITCH + BN * 4;
   __shared__ __attribute__((aligned(1024))) char smem[SM];
   char* const Ws = smem + P_BYTES;
 
@@ -82,28 +82,46 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
   }
 
   // patch pixels of a tile: pair j = (row, column pair), 16 bytes in LDS;
-  // an input pixel is C <= 4 bf16 values at any 2-byte alignment: three
-  // aligned dwords cover it, realigned by the byte offset
+  // an input pixel is C <= 4 16-bit values at any 2-byte alignment: three
+  // aligned dwords cover it, realigned by the byte offset (a funnel shift).
+  // A thread's pairs j = tid + 256 u sit at the same patch row and columns
+  // in every tile, so their row index and column byte offsets are set once.
   const int Cm = a.C;
-  auto fetch = [&](int tile, u32x4 (&raw)[NPF][2], unsigned (&shf)[NPF][2], bool (&ok)[NPF][2]) {
+  const unsigned cmask0 = Cm < 2 ? 0xFFFFu : 0xFFFFFFFFu;                      // channels 0, 1
+  const unsigned cmask1 = Cm < 3 ? 0u : Cm < 4 ? 0xFFFFu : 0xFFFFFFFFu;        // channels 2, 3
+  int fprw[NPF], fcb[NPF][2];
+  bool fcok[NPF][2];
+#pragma unroll
+  for (int u = 0; u < NPF; ++u) {
+    const int j = tid + u * 256;
+    const int prw = sdiv(j, a.inv_pwp2), pc2 = j - __umul24(prw, a.PWP >> 1);
+    fprw[u] = j < PAIRS && prw < a.PH ? prw : -(1 << 24);  // a row no tile has
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int w = 2 * pc2 + e - a.pad;
+      fcok[u][e] = (unsigned)w < (unsigned)a.W;
+      fcb[u][e] = (prw * a.W + w) * Cm * 2;
+    }
+  }
+  auto fetch = [&](int tile, u32x4 (&raw)[NPF][2], unsigned (&shf)[NPF][2], unsigned (&okm)[NPF][2]) {
     const int img = fdiv(tile, a.fd_tiles_img), rt = tile - img * a.tiles_img;
     const int h0 = rt * a.TR * 2 - a.pad;
+    const int tb = (img * a.H + h0) * a.W * Cm * 2;  // byte offset of input row h0 (may be < 0)
 #pragma unroll
     for (int u = 0; u < NPF; ++u) {
-      const int j = tid + u * 256;
-      const int prw = sdiv(j, a.inv_pwp2), pc2 = j - __umul24(prw, a.PWP >> 1);
+      const bool rok = (unsigned)(h0 + fprw[u]) < (unsigned)a.H;
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const int h = h0 + prw, w = 2 * pc2 + e - a.pad;
-        ok[u][e] = j < PAIRS && prw < a.PH && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
-        const unsigned byte = (unsigned)(__umul24(__umul24(img, a.H) + h, a.W) + w) * (unsigned)Cm * 2u;
-        shf[u][e] = (byte & 3u) * 8u;
-        const auto d = __builtin_amdgcn_raw_buffer_load_b96(rx, ok[u][e] ? (int)(byte & ~3u) : (int)kOOB, 0, 0);
+        const bool ok = rok && fcok[u][e];
+        const int byte = tb + fcb[u][e];
+        okm[u][e] = ok ? 0xFFFFFFFFu : 0u;
+        shf[u][e] = (unsigned)(byte & 3) * 8u;
+        const auto d = __builtin_amdgcn_raw_buffer_load_b96(rx, ok ? (byte & ~3) : (int)kOOB, 0, 0);
         raw[u][e] = u32x4{d[0], d[1], d[2], 0u};
       }
     }
   };
-  auto store_patch = [&](const u32x4 (&raw)[NPF][2], const unsigned (&shf)[NPF][2], const bool (&ok)[NPF][2]) {
+  auto store_patch = [&](const u32x4 (&raw)[NPF][2], const unsigned (&shf)[NPF][2], const unsigned (&okm)[NPF][2]) {
 #pragma unroll
     for (int u = 0; u < NPF; ++u) {
       const int j = tid + u * 256;
@@ -111,16 +129,10 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
       unsigned px[2][2];
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        // 8 bytes from the byte shift: channels 0..3 of the pixel
-        const unsigned long long lo = ((unsigned long long)raw[u][e][1] << 32) | raw[u][e][0];
-        const unsigned long long hi = ((unsigned long long)raw[u][e][2] << 32) | raw[u][e][1];
-        unsigned d0 = (unsigned)(lo >> shf[u][e]), d1 = (unsigned)(hi >> shf[u][e]);
-        // keep channels < C: d0 = (c0, c1), d1 = (c2, c3)
-        if (Cm < 2) d0 &= 0xFFFFu;
-        if (Cm < 3) d1 = 0u;
-        else if (Cm < 4) d1 &= 0xFFFFu;
-        px[e][0] = ok[u][e] ? d0 : 0u;
-        px[e][1] = ok[u][e] ? d1 : 0u;
+        // channels (0, 1) and (2, 3) of the pixel; channels >= C and
+        // pixels outside the image are zero
+        px[e][0] = __builtin_amdgcn_alignbit(raw[u][e][1], raw[u][e][0], shf[u][e]) & (cmask0 & okm[u][e]);
+        px[e][1] = __builtin_amdgcn_alignbit(raw[u][e][2], raw[u][e][1], shf[u][e]) & (cmask1 & okm[u][e]);
       }
       *reinterpret_cast<u32x4*>(smem + j * 16) = u32x4{px[0][0], px[0][1], px[1][0], px[1][1]};
     }
@@ -128,37 +140,48 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
 
   // operand offsets: output pixel m of the tile -> patch pixel (2 pr, 2 pc);
   // chunk g = (r, sp) adds r rows and 2 sp columns
+  // (a wave row's blocks past FMT read patch offset 0 and compute values
+  // that are never stored, which keeps the step loop free of branches)
   int abase[FMW];
 #pragma unroll
   for (int i = 0; i < FMW; ++i) {
     const int m = (wm * FMW + i) * 16 + (lane & 15);
     const int pr = sdiv(m, a.inv_q), pc = m - __umul24(pr, a.Q);
-    abase[i] = ((2 * pr) * a.PWP + 2 * pc) * 8;
+    abase[i] = wm * FMW + i < FMT ? ((2 * pr) * a.PWP + 2 * pc) * 8 : 0;
   }
   const int bbase = (wn * WTN + (lane & 15)) * WPITCH + (lane >> 4) * 16;
   const ActClamp ac = act_clamp(a.act);
   typedef typename Mfma<T>::frag frag;
 
-  // accumulator start: the bias of the lane's output channels
-  f32x4 bias[FNW];
-#pragma unroll
-  for (int j = 0; j < FNW; ++j) {
-    const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
-#pragma unroll
-    for (int v = 0; v < 4; ++v)
-      bias[j][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n + v) * 4, 0, 0));
-  }
+  // the bias of the lane's output channels, staged through LDS so that no
+  // global load of it is outstanding inside the tile loop (the compiler
+  // would otherwise wait for every load there, the prefetch included)
+  float* const Bs = reinterpret_cast<float*>(smem + P_BYTES + BN * WPITCH);
+  if (tid < BN)
+    Bs[tid] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, (n0 + tid) * 4, 0, 0));
 
   u32x4 raw[NPF][2];
   unsigned shf[NPF][2];
-  bool ok[NPF][2];
+  unsigned ok[NPF][2];
   int tile = blockIdx.x;
-  if (tile < a.tiles) fetch(tile, raw, shf, ok);
-  for (; tile < a.tiles; tile += gridDim.x) {
-    __syncthreads();  // every wave is done reading the previous tile's patch
-    store_patch(raw, shf, ok);
-    __syncthreads();
-    if (tile + (int)gridDim.x < a.tiles) fetch(tile + gridDim.x, raw, shf, ok);  // in flight during the MFMAs
+  if (tile >= a.tiles) return;
+  fetch(tile, raw, shf, ok);
+  store_patch(raw, shf, ok);
+  __syncthreads();  // filter, bias and the first patch are in LDS
+  f32x4 bias[FNW];
+#pragma unroll
+  for (int j = 0; j < FNW; ++j)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) bias[j][v] = Bs[wn * WTN + j * 16 + (lane >> 4) * 4 + v];
+
+  // The patch of tile t + G (G = grid size) is loaded into registers while
+  // tile t's MFMAs and stores run, then written to LDS.  The barriers wait
+  // for LDS operations only, and every store is issued unconditionally
+  // (masked by an out-of-range offset), so the wait for the prefetched
+  // registers leaves the preceding output stores in flight.
+  for (;; tile += gridDim.x) {
+    const bool more = tile + (int)gridDim.x < a.tiles;
+    if (more) fetch(tile + gridDim.x, raw, shf, ok);
 
     f32x4 acc[FMW][FNW];
 #pragma unroll
@@ -172,15 +195,13 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
       const int toff = g < a.G ? (r * a.PWP + 2 * sp) * 8 : 0;
       frag fa[FMW], fb[FNW];
 #pragma unroll
-      for (int i = 0; i < FMW; ++i)
-        if (wm * FMW + i < FMT) fa[i] = *reinterpret_cast<const frag*>(smem + abase[i] + toff);
+      for (int i = 0; i < FMW; ++i) fa[i] = *reinterpret_cast<const frag*>(smem + abase[i] + toff);
 #pragma unroll
       for (int j = 0; j < FNW; ++j) fb[j] = *reinterpret_cast<const frag*>(Ws + bbase + j * 16 * WPITCH + st * 64);
 #pragma unroll
       for (int i = 0; i < FMW; ++i)
-        if (wm * FMW + i < FMT)
 #pragma unroll
-          for (int j = 0; j < FNW; ++j) acc[i][j] = Mfma<T>::run(fb[j], fa[i], acc[i][j]);
+        for (int j = 0; j < FNW; ++j) acc[i][j] = Mfma<T>::run(fb[j], fa[i], acc[i][j]);
     }
 
     // epilogue: each lane stores its 4 consecutive channels of a pixel (8 bytes)
@@ -191,19 +212,23 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
 #pragma unroll
     for (int i = 0; i < FMW; ++i) {
       const int ml = (wm * FMW + i) * 16 + (lane & 15);
-      if (wm * FMW + i >= FMT || ml >= valid) continue;
+      const bool mok = wm * FMW + i < FMT && ml < valid;
 #pragma unroll
       for (int j = 0; j < FNW; ++j) {
         const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
-        if (n >= a.Ng) continue;
         T o[4];
 #pragma unroll
         for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v], ac.lo, ac.hi));
         u32x2 pk;
         __builtin_memcpy(&pk, o, 8);
-        __builtin_amdgcn_raw_buffer_store_b64(pk, ry, (int)((unsigned)((mbase + ml) * a.Ks + n) * 2u), 0, 0);
+        const unsigned off = mok && n < a.Ng ? (unsigned)((mbase + ml) * a.Ks + n) * 2u : kOOB;
+        __builtin_amdgcn_raw_buffer_store_b64(pk, ry, (int)off, 0, 0);
       }
     }
+    if (!more) break;
+    lds_barrier();  // every wave is done reading this tile's patch
+    store_patch(raw, shf, ok);
+    lds_barrier();  // the next patch is in LDS
   }
 }
 

@@ -1,5 +1,6 @@
 // Bandwidth-bound routines for gfx950: max pooling, global average pooling,
-// residual add (+ activation), FC as a dot-product kernel, layout converters
+// residual add (+ activation), FC as a dot-product kernel (large batches and
+// float32; small 16-bit batches go to the MFMA kernel), layout converters
 // (the adapt routines of the paper, Sec. III-C, job 3: changing data layout)
 // and the profiler's scratch fill.
 #include <stdexcept>
@@ -46,11 +47,18 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const T* __restrict__ x, T
   } else {
     // 32-bit index arithmetic (the host checks N * P * Q * CB < 2^31): the
     // 64-bit divisions it replaces cost more than the nine 16-byte loads
+    // Consecutive workgroups are dispatched round-robin over the 8 XCDs;
+    // renumber them so each XCD takes one contiguous range of output rows,
+    // and the input row shared by vertically adjacent windows is read into
+    // that XCD's L2 once.
+    const unsigned nb = gridDim.x, b = blockIdx.x;
+    const unsigned xq = nb >> 3, xr = nb & 7, xcd = b & 7;
+    const unsigned vb = xcd * xq + min(xcd, xr) + (b >> 3);
     const int CB = (Cs + 7) / 8;
     const bool vec = L == NC8 || C % 8 == 0;
     const unsigned total = (unsigned)N * (unsigned)PQ * (unsigned)CB;
-    const unsigned id = (unsigned)idx;
-    if (idx >= (long long)total) return;
+    const unsigned id = vb * 256u + threadIdx.x;
+    if (id >= total) return;
     int cb;
     unsigned mm;
     if constexpr (L == NC8) {
@@ -262,9 +270,18 @@ __global__ __launch_bounds__(256) void fc_kernel(const T* __restrict__ x, int N,
   }
 }
 
+// the MFMA kernel for small 16-bit batches (fc.hip)
+bool fc_mfma_applicable(int dtype, int n, int cin, int cin_s);
+void fc_mfma(int dtype, const void* x, int n, int cin, int cin_s, const void* w, int c8,
+             const float* bias, void* y, int kout, int kout_s, hipStream_t st);
+
 void fc_direct(int dtype, const void* x, int n, int cin, int cin_s, const void* w, int c8,
                const float* bias, void* y, int kout, int kout_s, hipStream_t s) {
   check(kout_s >= kout && c8 >= cin, "fc shapes");
+  if (fc_mfma_applicable(dtype, n, cin, cin_s)) {
+    fc_mfma(dtype, x, n, cin, cin_s, w, c8, bias, y, kout, kout_s, s);
+    return;
+  }
   dim3 g(blocks(kout_s, 4));
   if (dtype == 0)
     SN_LAUNCH(fc_kernel<float>, g, dim3(256), 0, s, (const float*)x, n, cin, cin_s, (const float*)w, c8, bias, (float*)y, kout_s);
@@ -332,33 +349,44 @@ __global__ __launch_bounds__(256) void transpose_smallc_kernel(const E* __restri
 }
 
 // NCHW -> NHWC for C <= 8 with 16-bit elements and H * W % 8 == 0: a
-// thread moves 8 consecutive pixels of one image, reading C 16-byte runs
-// (one per channel plane) and writing the 8 * C interleaved values as C
-// 16-byte stores (C is a template constant so the shuffle stays in
-// registers).
+// thread reads 8 consecutive pixels of one image from each of the C planes
+// (16-byte loads) and interleaves them into the workgroup's LDS copy of its
+// output run (256 * 8 pixels, contiguous in NHWC); the run then goes out in
+// 16-byte stores with consecutive lanes on consecutive addresses.  C is a
+// template constant so the shuffle stays in registers.
 template <typename E, int C>
 __global__ __launch_bounds__(256) void transpose_smallc8_kernel(const E* __restrict__ x, E* __restrict__ y,
                                                                 int HW, int groups) {
   static_assert(sizeof(E) == 2 && C >= 1 && C <= 8, "16-bit elements, C <= 8");
-  const int g = blockIdx.x * 256 + threadIdx.x;  // group of 8 pixels
-  if (g >= groups) return;
-  const int gpi = HW >> 3;                       // groups per image
-  const int n = g / gpi, hw = (g - n * gpi) * 8;
-  const E* xp = x + ((long long)n * C) * HW + hw;
-  E o[8 * C];
+  __shared__ __attribute__((aligned(16))) E run[256 * 8 * C];
+  const int g0 = blockIdx.x * 256;
+  const int g = g0 + threadIdx.x;  // group of 8 pixels
+  if (g < groups) {
+    const int gpi = HW >> 3;       // groups per image
+    const int n = g / gpi, hw = (g - n * gpi) * 8;
+    const E* xp = x + ((long long)n * C) * HW + hw;
+    E o[8 * C];
 #pragma unroll
-  for (int c = 0; c < C; ++c) {
-    const V8<E> t = ld8(xp + (long long)c * HW);
+    for (int c = 0; c < C; ++c) {
+      const V8<E> t = ld8(xp + (long long)c * HW);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[e * C + c] = t.v[e];
+      for (int e = 0; e < 8; ++e) o[e * C + c] = t.v[e];
+    }
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      V8<E> w;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w.v[e] = o[k * 8 + e];
+      *reinterpret_cast<V8<E>*>(run + (threadIdx.x * C + k) * 8) = w;
+    }
   }
-  E* yp = y + (long long)g * 8 * C;
+  __syncthreads();
+  const int chunks = min(256, groups - g0) * C;  // 16-byte chunks of this run
+  E* yp = y + (long long)g0 * 8 * C;
 #pragma unroll
   for (int k = 0; k < C; ++k) {
-    V8<E> w;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) w.v[e] = o[k * 8 + e];
-    st8(yp + k * 8, w);
+    const int i = k * 256 + threadIdx.x;
+    if (i < chunks) st8(yp + i * 8, *reinterpret_cast<const V8<E>*>(run + i * 8));
   }
 }
 

@@ -123,8 +123,11 @@ def test_gap(dtype, shape):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("case", [(1, 32, 10), (3, 2048, 1000), (32, 1280, 1000), (2, 12, 5)])
+@pytest.mark.parametrize("case", [(1, 32, 10), (3, 2048, 1000), (32, 1280, 1000), (2, 12, 5),
+                                  (40, 24, 37), (64, 2048, 1000)])
 def test_fc(dtype, case):
+    # 16-bit batches up to 64 with C % 8 == 0 take the MFMA kernel (1, 2 or 4
+    # blocks of 16 batch rows; K = 37 leaves a ragged feature tile)
     n, cin, k = case
     from paper_2110_06037_amd import Graph
     x = random_tensor((n, cin, 1, 1), dtype, seed=8)
@@ -141,7 +144,9 @@ def test_fc(dtype, case):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("c", [12, 3])
-@pytest.mark.parametrize("hw", [(9, 9), (12, 10)])  # H * W % 8 == 0 takes the 8-pixel transpose
+# H * W % 8 == 0 takes the 8-pixel transpose; 40 x 40 spans several of its
+# workgroups with a ragged last one
+@pytest.mark.parametrize("hw", [(9, 9), (12, 10), (40, 40)])
 def test_add_and_converters_bit_exact(dtype, c, hw):
     # two maxpools feeding an add: every (layout_a, layout_b, layout_add)
     # combination exercises the converters between all layout pairs (few
