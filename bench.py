@@ -60,7 +60,7 @@ def layer_work(spec, g, i, routine):
         if routine["algo"] == 2:  # Winograd: the MFMA work is the 16 tile GEMMs
             tiles = n * ((h + 1) // 2) * ((w + 1) // 2)
             flops = 2 * 16 * k * c * tiles
-        cat = "conv%dx%d" % (r, s) if r in (1, 3) else "conv_stem"
+        cat = "conv_stem" if c <= 4 else "conv%dx%d" % (r, s)
         return cat, flops, byt
     if t == "add":
         return "add", n * k * p * q, 3 * es * n * k * p * q
@@ -149,11 +149,11 @@ def _mask_name(m):
 
 
 def _nets():
-    from workloads import mobilenet_v2, resnet18, resnet50
-    return {"resnet50": resnet50, "resnet18": resnet18, "mobilenetv2": mobilenet_v2}
+    from workloads import mobilenet_v2, resnet18, resnet50, vgg16
+    return {"resnet50": resnet50, "resnet18": resnet18, "mobilenetv2": mobilenet_v2, "vgg16": vgg16}
 
 
-NETS = {"resnet50": None, "resnet18": None, "mobilenetv2": None}
+NETS = {"resnet50": None, "resnet18": None, "mobilenetv2": None, "vgg16": None}
 
 
 def sweep(args):
@@ -231,8 +231,8 @@ def cpu_baseline(spec, t, budget_s):
     el = time.perf_counter() - t0
     return {"value": round(done / el, 4), "unit": "img/s", "cores": O.num_threads(),
             "kind": "oracle",
-            "sample": f"{done} image(s) of the batch-{spec['batch']} ResNet-50 input, naive float64 "
-                      f"direct convolution with bf16 storage rounding, {el:.1f} s"}
+            "sample": f"{done} image(s) of the batch-{spec['batch']} {spec['name'].split('_')[0]} input, "
+                      f"naive float64 direct convolution with {spec['dtype']} storage rounding, {el:.1f} s"}
 
 
 def main():
@@ -275,8 +275,9 @@ def main():
         summarize_pmc(*args.summarize_pmc, calib_mib=args.calib_copy_mib)
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the path shards over the "
-              "batch with no exchange, see DESIGN.md", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the path would shard over "
+              "the batch (one graph per GPU, tuned at its share of the batch, no exchange)",
+              file=sys.stderr)
         sys.exit(2)
 
     if args.sweep:
@@ -443,8 +444,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": args.dtype,
         "data": "synthetic (seeded random input and He-normal weights)",
         "config": {"workload": f"{args.net}-shaped CNN, batch {args.batch}, {args.dtype}, 224x224"
-                               + ("" if args.no_fuse else
-                                  ", residual adds folded into the 1x1 convolutions that produce them"),
+                               + ("" if not any(l["type"] == "conv" and len(l["in"]) > 1 for l in spec["layers"])
+                                  else ", residual adds folded into the 1x1 convolutions that produce them"),
                    "batch": args.batch,
                    "path": ("DPRS candidates + fixed paths, integrated profiling keeps the fastest"
                             if integ else "DPRS-selected routines")},

@@ -72,7 +72,7 @@ typedef enum {
   SN_LAYER_MAXPOOL = 2,
   SN_LAYER_GAP = 3,    /* global average pooling to N x C x 1 x 1 */
   SN_LAYER_ADD = 4,    /* residual merge of two inputs of equal shape */
-  SN_LAYER_FC = 5,     /* y = W x + b on the flattened N x C input */
+  SN_LAYER_FC = 5,     /* y = act(W x + b) on an N x C x 1 x 1 input */
   SN_LAYER_OUTPUT = 6  /* auxiliary output layer (implicit, after the last layer) */
 } sn_layer_type;
 
@@ -87,7 +87,7 @@ typedef enum { SN_ACT_NONE = 0, SN_ACT_RELU = 1, SN_ACT_RELU6 = 2 } sn_act;
  *   MAXPOOL: r (= s) window, stride, pad (padding never wins the max)
  *   GAP    : -
  *   ADD    : act
- *   FC     : k = output features                                          */
+ *   FC     : k = output features, act                                    */
 typedef struct {
   int32_t type;
   int32_t k;

@@ -111,6 +111,17 @@ def add(a, b, act="none"):
     return y
 
 
+def activate(y, act):
+    """The fused activations: identity, ReLU = max(y, 0), ReLU6 = min(max(y, 0), 6)."""
+    y = _f64(y)
+    if act == "relu":
+        return np.maximum(y, 0.0)
+    if act == "relu6":
+        return np.minimum(np.maximum(y, 0.0), 6.0)
+    assert act == "none", act
+    return y.copy()
+
+
 def fc(x, w, b):
     x, w = _f64(x), _f64(w)
     n = x.shape[0]
@@ -146,7 +157,7 @@ def layer_forward(layer, inputs, w=None, b=None):
     if t == "add":
         return add(inputs[0], inputs[1], layer.get("act", "none"))
     if t == "fc":
-        return fc(inputs[0], w, b)
+        return activate(fc(inputs[0], w, b), layer.get("act", "none"))
     raise ValueError(t)
 
 

@@ -286,13 +286,13 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
         a.r = a.s = 1;
         a.stride = 1;
         a.pad = 0;
-        a.act = SN_ACT_NONE;
+        a.act = L.d.act;
         a.ws = ws;
         a.ws_bytes = ws_bytes;
         k::conv_igemm(dt, r.param, a, st);
       } else {
         k::fc_direct(dt, in[0], xs.n, xs.c, stored_c(xs, r.layout), dl.w, round8(xs.c), dl.bias, out,
-                     L.out.c, stored_c(L.out, r.layout), st);
+                     L.out.c, stored_c(L.out, r.layout), L.d.act, st);
       }
       break;
     }

@@ -1,4 +1,4 @@
-// Fully connected layer for a small batch (y = W x + b with W [K][C], the
+// Fully connected layer for a small batch (y = act(W x + b) with W [K][C], the
 // FC layer type of Sec. III-B) on MFMA, 16-bit types.
 //
 // With a batch of at most 64 the layer is a skinny GEMM whose cost is
@@ -23,7 +23,7 @@ __global__ __launch_bounds__(64 * kFcWaves) void fc_mfma_kernel(const T* __restr
                                                                 int cin_s, const T* __restrict__ w,
                                                                 int c8, int kp,
                                                                 const float* __restrict__ bias,
-                                                                T* __restrict__ y, int kout_s) {
+                                                                T* __restrict__ y, int kout_s, int act) {
   typedef typename Mfma<T>::frag frag;
   __shared__ f32x4 red[kFcWaves][NB][64];
   const int lane = threadIdx.x & 63;
@@ -80,7 +80,7 @@ __global__ __launch_bounds__(64 * kFcWaves) void fc_mfma_kernel(const T* __restr
   if (n >= N) return;
   T o[4];
 #pragma unroll
-  for (int v = 0; v < 4; ++v) o[v] = from_f<T>(s[v] + (kb + v < kout_s ? bias[kb + v] : 0.f));
+  for (int v = 0; v < 4; ++v) o[v] = from_f<T>(act_f(s[v] + (kb + v < kout_s ? bias[kb + v] : 0.f), act));
   T* yp = y + (long long)n * kout_s + kb;
   if (kout_s % 4 == 0 && kb + 4 <= kout_s) {
     u32x2 pk;
@@ -100,7 +100,7 @@ bool fc_mfma_applicable(int dtype, int n, int cin, int cin_s) {
 
 template <typename T>
 static void fc_mfma_t(const void* x, int n, int cin, int cin_s, const void* w, int c8, const float* bias,
-                      void* y, int kout, int kout_s, hipStream_t st) {
+                      void* y, int kout, int kout_s, int act, hipStream_t st) {
   const int kp = (kout + 7) / 8 * 8;
   check((long long)kp * c8 * 2 < (long long)kOOB, "FC weights too large for 32-bit offsets");
   check(kout_s <= kp && c8 >= cin, "FC shapes");
@@ -109,18 +109,18 @@ static void fc_mfma_t(const void* x, int n, int cin, int cin_s, const void* w, i
   const T* wp = static_cast<const T*>(w);
   T* yp = static_cast<T*>(y);
   if (n <= 16)
-    SN_LAUNCH((fc_mfma_kernel<T, 1, 4>), grid, block, 0, st, xp, n, cin, cin_s, wp, c8, kp, bias, yp, kout_s);
+    SN_LAUNCH((fc_mfma_kernel<T, 1, 4>), grid, block, 0, st, xp, n, cin, cin_s, wp, c8, kp, bias, yp, kout_s, act);
   else if (n <= 32)
-    SN_LAUNCH((fc_mfma_kernel<T, 2, 4>), grid, block, 0, st, xp, n, cin, cin_s, wp, c8, kp, bias, yp, kout_s);
+    SN_LAUNCH((fc_mfma_kernel<T, 2, 4>), grid, block, 0, st, xp, n, cin, cin_s, wp, c8, kp, bias, yp, kout_s, act);
   else
-    SN_LAUNCH((fc_mfma_kernel<T, 4, 2>), grid, block, 0, st, xp, n, cin, cin_s, wp, c8, kp, bias, yp, kout_s);
+    SN_LAUNCH((fc_mfma_kernel<T, 4, 2>), grid, block, 0, st, xp, n, cin, cin_s, wp, c8, kp, bias, yp, kout_s, act);
 }
 
 void fc_mfma(int dtype, const void* x, int n, int cin, int cin_s, const void* w, int c8, const float* bias,
-             void* y, int kout, int kout_s, hipStream_t st) {
+             void* y, int kout, int kout_s, int act, hipStream_t st) {
   check(fc_mfma_applicable(dtype, n, cin, cin_s), "FC on MFMA: 16-bit types, batch <= 64, C % 8 == 0");
-  if (dtype == 1) fc_mfma_t<f16>(x, n, cin, cin_s, w, c8, bias, y, kout, kout_s, st);
-  else fc_mfma_t<bf16>(x, n, cin, cin_s, w, c8, bias, y, kout, kout_s, st);
+  if (dtype == 1) fc_mfma_t<f16>(x, n, cin, cin_s, w, c8, bias, y, kout, kout_s, act, st);
+  else fc_mfma_t<bf16>(x, n, cin, cin_s, w, c8, bias, y, kout, kout_s, act, st);
 }
 
 }  // namespace k

@@ -95,9 +95,10 @@ void maxpool(int dtype, const void* x, const TDesc& xd, void* y, const TDesc& yd
              int stride, int pad, hipStream_t st);
 void gap(int dtype, const void* x, const TDesc& xd, void* y, const TDesc& yd, hipStream_t st);
 void add_act(int dtype, const void* a, const void* b, void* y, int64_t n, int act, hipStream_t st);
-// FC as a VALU dot-product kernel: x [N][cin_s] (stored), w [Kp][C8], y [N][kout_s]
+// FC: x [N][cin_s] (stored), w [Kp][C8], y [N][kout_s] = act(W x + b); small
+// 16-bit batches run on MFMA, the rest as VALU dot products
 void fc_direct(int dtype, const void* x, int n, int cin, int cin_s, const void* w, int c8,
-               const float* bias, void* y, int kout, int kout_s, hipStream_t st);
+               const float* bias, void* y, int kout, int kout_s, int act, hipStream_t st);
 void convert(int dtype, const void* x, const TDesc& xd, void* y, const TDesc& yd, hipStream_t st);
 void fill_random(int dtype, void* p, int64_t n, uint64_t seed, hipStream_t st);
 

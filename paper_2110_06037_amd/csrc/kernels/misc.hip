@@ -235,7 +235,7 @@ template <typename T>
 __global__ __launch_bounds__(256) void fc_kernel(const T* __restrict__ x, int N, int cin, int cin_s,
                                                  const T* __restrict__ w, int c8,
                                                  const float* __restrict__ bias, T* __restrict__ y,
-                                                 int kout_s) {
+                                                 int kout_s, int act) {
   const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (k >= kout_s) return;
@@ -265,7 +265,7 @@ __global__ __launch_bounds__(256) void fc_kernel(const T* __restrict__ x, int N,
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float s = wave_sum(acc[j]);
-      if (lane == 0 && n0 + j < N) y[(long long)(n0 + j) * kout_s + k] = from_f<T>(s + bias[k]);
+      if (lane == 0 && n0 + j < N) y[(long long)(n0 + j) * kout_s + k] = from_f<T>(act_f(s + bias[k], act));
     }
   }
 }
@@ -273,22 +273,22 @@ __global__ __launch_bounds__(256) void fc_kernel(const T* __restrict__ x, int N,
 // the MFMA kernel for small 16-bit batches (fc.hip)
 bool fc_mfma_applicable(int dtype, int n, int cin, int cin_s);
 void fc_mfma(int dtype, const void* x, int n, int cin, int cin_s, const void* w, int c8,
-             const float* bias, void* y, int kout, int kout_s, hipStream_t st);
+             const float* bias, void* y, int kout, int kout_s, int act, hipStream_t st);
 
 void fc_direct(int dtype, const void* x, int n, int cin, int cin_s, const void* w, int c8,
-               const float* bias, void* y, int kout, int kout_s, hipStream_t s) {
+               const float* bias, void* y, int kout, int kout_s, int act, hipStream_t s) {
   check(kout_s >= kout && c8 >= cin, "fc shapes");
   if (fc_mfma_applicable(dtype, n, cin, cin_s)) {
-    fc_mfma(dtype, x, n, cin, cin_s, w, c8, bias, y, kout, kout_s, s);
+    fc_mfma(dtype, x, n, cin, cin_s, w, c8, bias, y, kout, kout_s, act, s);
     return;
   }
   dim3 g(blocks(kout_s, 4));
   if (dtype == 0)
-    SN_LAUNCH(fc_kernel<float>, g, dim3(256), 0, s, (const float*)x, n, cin, cin_s, (const float*)w, c8, bias, (float*)y, kout_s);
+    SN_LAUNCH(fc_kernel<float>, g, dim3(256), 0, s, (const float*)x, n, cin, cin_s, (const float*)w, c8, bias, (float*)y, kout_s, act);
   else if (dtype == 1)
-    SN_LAUNCH(fc_kernel<f16>, g, dim3(256), 0, s, (const f16*)x, n, cin, cin_s, (const f16*)w, c8, bias, (f16*)y, kout_s);
+    SN_LAUNCH(fc_kernel<f16>, g, dim3(256), 0, s, (const f16*)x, n, cin, cin_s, (const f16*)w, c8, bias, (f16*)y, kout_s, act);
   else
-    SN_LAUNCH(fc_kernel<bf16>, g, dim3(256), 0, s, (const bf16*)x, n, cin, cin_s, (const bf16*)w, c8, bias, (bf16*)y, kout_s);
+    SN_LAUNCH(fc_kernel<bf16>, g, dim3(256), 0, s, (const bf16*)x, n, cin, cin_s, (const bf16*)w, c8, bias, (bf16*)y, kout_s, act);
 }
 
 // ------------------------------------------------------------------ layout converters

@@ -103,9 +103,9 @@ class Graph:
     def add_add(self, a, b, act="none"):
         return self._add(N.LayerDesc(N.L_ADD, 0, 0, 0, 1, 0, 1, N.ACT[act]), [a, b])
 
-    def add_fc(self, inp, weight, bias):
+    def add_fc(self, inp, weight, bias, act="none"):
         k = weight.shape[0]
-        return self._add(N.LayerDesc(N.L_FC, k, 1, 1, 1, 0, 1, 0), [inp], weight, bias)
+        return self._add(N.LayerDesc(N.L_FC, k, 1, 1, 1, 0, 1, N.ACT[act]), [inp], weight, bias)
 
     def add_spec(self, layer, weight=None, bias=None):
         """Add one layer given as a ``workloads`` spec dict."""
@@ -121,7 +121,7 @@ class Graph:
         if t == "add":
             return self.add_add(layer["in"][0], layer["in"][1], layer.get("act", "none"))
         if t == "fc":
-            return self.add_fc(layer["in"][0], weight, bias)
+            return self.add_fc(layer["in"][0], weight, bias, layer.get("act", "none"))
         raise ValueError(t)
 
     # ---------------------------------------------------------------- tuning

@@ -15,7 +15,7 @@ import pytest
 from oracle.select import blockwise, exhaustive, path_time, problem_from_costs
 from paper_2110_06037_amd import Graph, build_from_spec, native as N
 from tests.problems import random_dag, residual_chain
-from workloads import mobilenet_v2, resnet18, resnet50, tiny_chain
+from workloads import mobilenet_v2, resnet18, resnet50, tiny_chain, vgg16
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 GOLD = json.load(open(os.path.join(ROOT, "tests", "golden", "dprs_paper_counts.json")))
@@ -139,7 +139,7 @@ def test_dprs_tiny_chain_256_paths():
 
 
 @pytest.mark.parametrize("maker", [lambda: resnet18(1), lambda: resnet50(32),
-                                   lambda: mobilenet_v2(8)])
+                                   lambda: mobilenet_v2(8), lambda: vgg16(32)])
 def test_dprs_equals_blockwise_exact_on_full_nets(maker):
     spec = maker()
     g = build_from_spec(spec, device=-1)

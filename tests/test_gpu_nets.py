@@ -12,7 +12,7 @@ from oracle.select import blockwise, exhaustive, problem_from_costs
 from paper_2110_06037_amd import build_from_spec, native as N
 from tests.gpu_util import TOL, err, from_dev, to_dev
 from workloads import (CONV_SWEEP_SHAPES, conv_sweep, fuse_residual, generate, mobilenet_v2, resnet18, resnet50,
-                       tiny_chain, to_f64, with_batch)
+                       tiny_chain, to_f64, vgg16, with_batch)
 
 pytestmark = pytest.mark.gpu
 
@@ -89,9 +89,10 @@ def test_integrated_profiling_selects_the_measured_fastest_candidate(name):
 
 
 @pytest.mark.parametrize("name", ["resnet18", "mobilenetv2", "resnet50_bf16", "resnet50_f16",
-                                  "resnet50_fused", "mobilenetv2_fused"])
+                                  "resnet50_fused", "mobilenetv2_fused", "vgg16_64px"])
 def test_net_dp_and_fixed_paths_match_oracle(name):
     spec = {"resnet18": lambda: resnet18(1), "mobilenetv2": lambda: mobilenet_v2(1),
+            "vgg16_64px": lambda: vgg16(2, "bf16", 64),
             "resnet50_bf16": lambda: resnet50(1, "bf16"),
             "resnet50_f16": lambda: resnet50(1, "f16"),
             "resnet50_fused": lambda: fuse_residual(resnet50(1, "bf16")),

@@ -143,6 +143,25 @@ def test_fc(dtype, case):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("case", [(32, 1024, 100, "relu"), (3, 64, 24, "relu6"), (2, 12, 5, "relu")])
+def test_fc_activation(dtype, case):
+    # y = act(W x + b) in every FC routine (dot products, MFMA, 1x1 childnet)
+    n, cin, k, act = case
+    from paper_2110_06037_amd import Graph
+    x = random_tensor((n, cin, 1, 1), dtype, seed=12)
+    wt = random_tensor((k, cin), dtype, seed=13, dist="normal", scale=np.sqrt(2 / cin))
+    b = random_tensor((k,), "f32", seed=14, scale=0.5)
+    ref = O.round_to(O.activate(O.fc(to_f64(x, dtype), to_f64(wt, dtype), b.astype(np.float64)), act), dtype)
+    g = Graph(dtype, n, cin, 1, 1, device=0)
+    g.add_fc(0, wt, b, act)
+    xd = to_dev(x, dtype)
+    for rt in g.routines(1):
+        out = from_dev(run_routine(g, rt["id"], xd), dtype).reshape(ref.shape)
+        assert err(out, ref, dtype) <= TOL[dtype], rt["name"]
+        assert np.all(out >= 0) and (act != "relu6" or np.all(out <= 6)), rt["name"]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("c", [12, 3])
 # H * W % 8 == 0 takes the 8-pixel transpose; 40 x 40 spans several of its
 # workgroups with a ragged last one

@@ -239,6 +239,40 @@ def test_fc_matches_torch_and_pointwise_conv():
     assert np.max(np.abs(yc - y)) <= 1e-13
 
 
+def test_activate_hand_values():
+    y = np.array([-1.5, 0.0, 2.0, 7.25, 6.0])
+    assert np.array_equal(O.activate(y, "none"), y)
+    assert np.array_equal(O.activate(y, "relu"), [0.0, 0.0, 2.0, 7.25, 6.0])
+    assert np.array_equal(O.activate(y, "relu6"), [0.0, 0.0, 2.0, 6.0, 6.0])
+
+
+def test_fc_layer_activation_matches_the_conv_oracles():
+    # an FC layer with an activation == the same dense childnet as a 1x1
+    # convolution whose activation the C oracle applies
+    g = rng(31)
+    x = g.standard_normal((2, 24, 1, 1))
+    w = g.standard_normal((9, 24))
+    b = g.standard_normal(9)
+    for act in ("none", "relu", "relu6"):
+        y = O.layer_forward({"type": "fc", "in": [0], "k": 9, "act": act}, [x], w, b)
+        yc = O.conv2d(x, w.reshape(9, 24, 1, 1), b, act=act)
+        assert np.max(np.abs(y - yc)) <= 1e-13, act
+
+
+def test_full_window_conv_is_flatten_then_fc():
+    # a convolution whose kernel covers the whole C x H x W input (no padding)
+    # is the dense layer on the NCHW-flattened input: how a classifier that
+    # flattens a feature map is expressed with an H x W convolution
+    g = rng(32)
+    x = g.standard_normal((3, 5, 4, 4))
+    w = g.standard_normal((7, 5, 4, 4))
+    b = g.standard_normal(7)
+    yc = O.conv2d(x, w, b, 1, 0)
+    yf = O.fc(x.reshape(3, 80, 1, 1), w.reshape(7, 80), b)
+    assert yc.shape == (3, 7, 1, 1)
+    assert np.max(np.abs(yc - yf)) <= 1e-13
+
+
 # ---------------------------------------------------------------- storage rounding
 
 def test_round_f32_f16_match_numpy_casts():

@@ -5,9 +5,9 @@ it contains no arithmetic of the method (no convolution, no path selection).
 """
 
 from .nets import (all_configs, channels, conv_sweep, edges, fuse_residual, mobilenet_v2, resnet18,
-                   resnet50, tiny_chain, with_batch, CONV_SWEEP_SHAPES)
+                   resnet50, tiny_chain, vgg16, with_batch, CONV_SWEEP_SHAPES)
 from .gen import generate, materialise, random_tensor, to_f64, weight_shapes
 
 __all__ = ["all_configs", "channels", "conv_sweep", "edges", "mobilenet_v2", "resnet18",
-           "resnet50", "tiny_chain", "with_batch", "CONV_SWEEP_SHAPES", "generate",
+           "resnet50", "tiny_chain", "vgg16", "with_batch", "CONV_SWEEP_SHAPES", "generate",
            "materialise", "random_tensor", "to_f64", "weight_shapes"]

@@ -15,11 +15,12 @@ paper's auxiliary input layer, Sec. IV-E); layers 1..n are listed in
 * ``{"type": "maxpool", "in": [j], "k": 3, "stride": 2, "pad": 1}``
 * ``{"type": "gap", "in": [j]}`` -- global average pooling to N x C x 1 x 1.
 * ``{"type": "add", "in": [a, b], "act": ...}`` -- residual merge.
-* ``{"type": "fc", "in": [j], "k": out}`` -- dense layer, y = W x + b.
+* ``{"type": "fc", "in": [j], "k": out, "act": ...}`` -- dense layer,
+  y = act(W x + b) on an N x C x 1 x 1 input ("act" optional, default none).
 
 The shapes follow the model families the paper evaluates (Sec. V: ResNet50,
-MobileNetV2; ResNet-18 and a tiny chain are smaller members of the same
-families).  Weights are random (He-normal) since no trained model is used.
+MobileNetV2, VGG16; ResNet-18 and a tiny chain are smaller members of the
+same families).  Weights are random (He-normal) since no trained model is used.
 """
 
 from __future__ import annotations
@@ -157,6 +158,33 @@ def mobilenet_v2(batch=1, dtype="bf16", first_t=1):
     b.add({"type": "fc", "in": [x], "k": 1000})
     return {"name": f"mobilenetv2_bs{batch}", "dtype": dtype, "batch": batch,
             "in_chw": [3, 224, 224], "input_dist": "uniform", "seed": 0, "layers": b.layers,
+            "layouts": ["NCHW", "NHWC", "NC8HW8"], "algos": ["direct", "igemm", "winograd"]}
+
+
+VGG16_CONVS = [64, 64, "M", 128, 128, "M", 256, 256, 256, "M", 512, 512, 512, "M", 512, 512, 512, "M"]
+
+
+def vgg16(batch=1, dtype="bf16", hw=224):
+    """VGG16 shape: thirteen 3x3 convolutions with ReLU in five groups, each
+    closed by 2x2/2 max pooling, then the classifier 4096 -> 4096 -> 1000.
+    A straight chain (no branch or merge).  The first classifier layer reads
+    the flattened 512 x (hw/32) x (hw/32) map; it is written as a convolution
+    whose kernel covers that whole map (no padding), which is the same
+    affine map on the NCHW-flattened input, so the net holds no reshape."""
+    assert hw % 32 == 0, hw
+    b = _Builder()
+    x = 0
+    for v in VGG16_CONVS:
+        if v == "M":
+            x = b.add({"type": "maxpool", "in": [x], "k": 2, "stride": 2, "pad": 0})
+        else:
+            x = b.add(_conv(x, v, 3, 1, 1, act="relu"))
+    f = hw // 32
+    x = b.add(_conv(x, 4096, f, 1, 0, act="relu"))
+    x = b.add({"type": "fc", "in": [x], "k": 4096, "act": "relu"})
+    b.add({"type": "fc", "in": [x], "k": 1000})
+    return {"name": f"vgg16_bs{batch}_{dtype}" + ("" if hw == 224 else f"_{hw}px"), "dtype": dtype,
+            "batch": batch, "in_chw": [3, hw, hw], "input_dist": "uniform", "seed": 0, "layers": b.layers,
             "layouts": ["NCHW", "NHWC", "NC8HW8"], "algos": ["direct", "igemm", "winograd"]}
 
 
