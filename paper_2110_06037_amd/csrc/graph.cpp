@@ -89,7 +89,7 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
           int np = g.opt_params ? k::igemm_num_params(g.dtype) : 1;
           for (int p = 0; p < np; ++p)
             if (k::igemm_param_valid(g.dtype, p, lay, in.n, in.c, in.h, in.w, L.d.r, L.d.s, L.d.stride,
-                                     L.d.pad) &&
+                                     L.d.pad, L.d.k) &&
                 (residual == 0 || k::igemm_param_takes_residual(g.dtype, p, lay, L.d.k)))
               add(lay, SN_ALGO_IGEMM, p);
         }
@@ -101,7 +101,7 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
         if (g.opt_algos >> SN_ALGO_IGEMM & 1) {  // the dense childnet: a 1x1 convolution
           int np = g.opt_params ? k::igemm_num_params(g.dtype) : 1;
           for (int p = 0; p < np; ++p)
-            if (k::igemm_param_valid(g.dtype, p, lay, in.n, in.c, 1, 1, 1, 1, 1, 0))
+            if (k::igemm_param_valid(g.dtype, p, lay, in.n, in.c, 1, 1, 1, 1, 1, 0, L.d.k))
               add(lay, SN_ALGO_IGEMM, p);
         }
         break;

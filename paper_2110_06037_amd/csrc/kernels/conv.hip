@@ -910,6 +910,7 @@ struct IgCfg {
   int ppx = 0;                  // small-channel kernel: patch capacity in pixels
   PatchCfg pc{};                // patch kernel tile
   int nw = 4;                   // LDS-DMA kernel: waves per workgroup (4 or 8)
+  int gmax = 0;                 // small-channel kernel: filter chunks held (R * ceil(S / 2) <= gmax)
 };
 static const IgCfg kIg16[] = {
     {64, 64, 32, 0, 2},   {128, 128, 64, 0, 2}, {256, 128, 32, 0, 2}, {128, 64, 64, 0, 2},
@@ -939,8 +940,9 @@ static const IgCfg kIg16[] = {
   {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS}},
     PATCH_CONFIGS(SN_PATCH_IG)
 #undef SN_PATCH_IG
-    // small-channel (stem) kernel: NHWC, C <= 4, stride 2
-    {112, 64, 32, 0, 0, 3, 2, 1, 1664}, {224, 64, 32, 0, 0, 3, 2, 1, 2112}};
+    // small-channel (stem) kernel: NHWC, C <= 4, stride 1 or 2; 7 x 7 and 3 x 3 filters
+    {112, 64, 32, 0, 0, 3, 2, 1, 1664, {}, 4, 28}, {224, 64, 32, 0, 0, 3, 2, 1, 2112, {}, 4, 28},
+    {112, 64, 32, 0, 0, 3, 2, 1, 704, {}, 4, 8},   {224, 64, 32, 0, 0, 3, 2, 1, 1152, {}, 4, 8}};
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 
 int igemm_num_params(int dtype) {
@@ -950,12 +952,12 @@ int igemm_num_params(int dtype) {
 // A configuration whose tile rows do not divide the 256 threads needs the
 // 8-channel vector loader (NHWC with C % 8 == 0, or NC8HW8).
 bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, int w, int r, int s,
-                       int stride, int pad) {
+                       int stride, int pad, int k) {
   if (param < 0 || param >= igemm_num_params(dtype)) return false;
   const IgCfg& g = dtype == 0 ? kIg32[param] : kIg16[param];
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
   if (g.dma == 2) return patch_applicable(layout, c, h, w, r, s, stride, pad, n, g.pc.fmt, g.pc.pwt, g.pc.prows);
-  if (g.dma == 3) return smallc_applicable(layout, c, h, w, r, s, stride, pad, n, g.bm / 16, g.ppx, 28);
+  if (g.dma == 3) return smallc_applicable(layout, c, h, w, r, s, stride, pad, n, k, g.bm / 16, g.ppx, g.gmax);
   if (g.dma) {
     // fp32 index division and 32-bit byte offsets bound the output size
     const long long p = (h + 2 * pad - r) / stride + 1, q = (w + 2 * pad - s) / stride + 1;
@@ -1198,7 +1200,7 @@ static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t 
     return;
   }
   if (cfg.dma == 3) {
-    conv_smallc(dtype, cfg.bm / 16, c, st);
+    conv_smallc(dtype, cfg.bm / 16, cfg.gmax, c, st);
     return;
   }
   IgArgs a = make_ig(c);

@@ -1,14 +1,14 @@
 // Convolution of an input with few channels (C <= 4; the RGB stem of a CNN)
-// in NHWC, stride 2, any R x S filter, as an implicit GEMM on MFMA.
+// in NHWC, stride 1 or 2, any R x S filter, as an implicit GEMM on MFMA.
 //
 // Padding three channels to the 8 of a 16-byte vector would waste 5/8 of
 // the MFMA work, so the reduction is packed differently: the input patch of
 // a tile sits in LDS with 4 channels per pixel (8 bytes, the fourth zero),
 // and one 8-element MFMA operand chunk is a pixel pair -- filter columns
-// (s, s + 1) of filter row r, 4 channels each.  With stride 2 an output
-// pixel's pairs start at even patch columns, so every chunk is an aligned
-// 16-byte LDS read.  The reduction has R * ceil(S / 2) such chunks (28 for a
-// 7 x 7 filter: 224 MFMA elements for 147 real ones).  The filter is
+// (s, s + 1) of filter row r, 4 channels each, 16 consecutive LDS bytes
+// (16-byte aligned with stride 2, 8-byte aligned with stride 1).  The
+// reduction has R * ceil(S / 2) such chunks (28 for a 7 x 7 filter: 224 MFMA
+// elements for 147 real ones; 6 for a 3 x 3 filter).  The filter is
 // repacked into the same chunks in LDS once per workgroup; workgroups are
 // persistent over output-row tiles and prefetch the next tile's input
 // pixels into registers while the current tile's MFMAs run.
@@ -26,7 +26,7 @@ struct SmallCArgs {
   void* y;
   int N, C, H, W;
   int K, P, Q, Ks, Ng;
-  int R, S, pad, act;
+  int R, S, pad, act, stride;
   int C8, Kred;          // prepared filter: channels per tap, row length R * S * C8
   int G, SP;             // operand chunks R * SP, column pairs per filter row SP = ceil(S / 2)
   int TR, PH, PWP;       // output rows per tile, patch rows, patch pitch in pixels (even)
@@ -105,7 +105,7 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
   }
   auto fetch = [&](int tile, u32x4 (&raw)[NPF][2], unsigned (&shf)[NPF][2], unsigned (&okm)[NPF][2]) {
     const int img = fdiv(tile, a.fd_tiles_img), rt = tile - img * a.tiles_img;
-    const int h0 = rt * a.TR * 2 - a.pad;
+    const int h0 = rt * a.TR * a.stride - a.pad;
     const int tb = (img * a.H + h0) * a.W * Cm * 2;  // byte offset of input row h0 (may be < 0)
 #pragma unroll
     for (int u = 0; u < NPF; ++u) {
@@ -138,16 +138,17 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
     }
   };
 
-  // operand offsets: output pixel m of the tile -> patch pixel (2 pr, 2 pc);
+  // operand offsets: output pixel m of the tile -> patch pixel (stride pr, stride pc);
   // chunk g = (r, sp) adds r rows and 2 sp columns
-  // (a wave row's blocks past FMT read patch offset 0 and compute values
-  // that are never stored, which keeps the step loop free of branches)
+  // (pixels past the tile's rows, and a wave row's blocks past FMT, read
+  // patch offset 0 and compute values that are never stored, which keeps
+  // the step loop free of branches and every read inside the patch)
   int abase[FMW];
 #pragma unroll
   for (int i = 0; i < FMW; ++i) {
     const int m = (wm * FMW + i) * 16 + (lane & 15);
     const int pr = sdiv(m, a.inv_q), pc = m - __umul24(pr, a.Q);
-    abase[i] = wm * FMW + i < FMT ? ((2 * pr) * a.PWP + 2 * pc) * 8 : 0;
+    abase[i] = wm * FMW + i < FMT && m < a.TR * a.Q ? (a.stride * (pr * a.PWP + pc)) * 8 : 0;
   }
   const int bbase = (wn * WTN + (lane & 15)) * WPITCH + (lane >> 4) * 16;
   const ActClamp ac = act_clamp(a.act);
@@ -240,8 +241,8 @@ static bool smallc_tiling(SmallCArgs& a, int fmt, int ppx, int gmax) {
   a.tiles_img = (a.P + fit - 1) / fit;
   a.TR = (a.P + a.tiles_img - 1) / a.tiles_img;
   a.tiles = a.N * a.tiles_img;
-  a.PH = (a.TR - 1) * 2 + a.R;
-  const int pw = (a.Q - 1) * 2 + a.S;
+  a.PH = (a.TR - 1) * a.stride + a.R;
+  const int pw = (a.Q - 1) * a.stride + a.S;
   a.PWP = (pw + 1) / 2 * 2;
   a.SP = (a.S + 1) / 2;
   a.G = a.R * a.SP;
@@ -253,15 +254,18 @@ static bool smallc_tiling(SmallCArgs& a, int fmt, int ppx, int gmax) {
 }
 
 bool smallc_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
-                       int fmt, int ppx, int gmax) {
-  if (layout != NHWC || c > 4 || stride != 2) return false;
+                       int k, int fmt, int ppx, int gmax) {
+  if (layout != NHWC || c > 4 || k % 4 != 0 || (stride != 1 && stride != 2)) return false;
   SmallCArgs a{};
   a.N = n;
-  a.P = (h + 2 * pad - r) / 2 + 1;
-  a.Q = (w + 2 * pad - s) / 2 + 1;
+  a.stride = stride;
+  a.P = (h + 2 * pad - r) / stride + 1;
+  a.Q = (w + 2 * pad - s) / stride + 1;
   a.R = r;
   a.S = s;
-  if ((long long)n * h * w * c * 2 >= (long long)kOOB || (long long)n * a.P * a.Q * 2048 >= (long long)kOOB)
+  // 32-bit byte offsets of the input and of the output (channels padded to 8)
+  if ((long long)n * h * w * c * 2 >= (long long)kOOB ||
+      (long long)n * a.P * a.Q * ((k + 7) / 8 * 8) * 2 >= (long long)kOOB)
     return false;
   return smallc_tiling(a, fmt, ppx, gmax);
 }
@@ -276,10 +280,10 @@ static void smallc_go(SmallCArgs a, hipStream_t st) {
   SN_LAUNCH((conv_smallc_kernel<T, FMT, WM, PPX, GMAX, OCC>), grid, dim3(256), 0, st, a);
 }
 
-void conv_smallc(int dtype, int fmt, const ConvArgs& c, hipStream_t st) {
+void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& c, hipStream_t st) {
   check(dtype != 0, "small-channel kernel runs 16-bit types");
-  check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.xd.c <= 4 && c.stride == 2,
-        "small-channel kernel: NHWC, C <= 4, stride 2");
+  check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.xd.c <= 4 && (c.stride == 1 || c.stride == 2),
+        "small-channel kernel: NHWC, C <= 4, stride 1 or 2");
   SmallCArgs a{};
   a.x = c.x;
   a.w = c.w;
@@ -298,6 +302,7 @@ void conv_smallc(int dtype, int fmt, const ConvArgs& c, hipStream_t st) {
   a.S = c.s;
   a.pad = c.pad;
   a.act = c.act;
+  a.stride = c.stride;
   a.C8 = (a.C + 7) / 8 * 8;
   a.Kred = a.R * a.S * a.C8;
   a.x_elems = (long long)c.xd.n * c.xd.cs * c.xd.h * c.xd.w;
@@ -306,13 +311,18 @@ void conv_smallc(int dtype, int fmt, const ConvArgs& c, hipStream_t st) {
   check(a.x_elems * 2 < (long long)kOOB && a.y_elems * 2 < (long long)kOOB && a.w_elems * 2 < (long long)kOOB,
         "tensor too large for 32-bit offsets");
   check(c.yd.cs % 4 == 0 && c.yd.c % 4 == 0, "small-channel kernel stores 4-channel groups");
-  if (fmt == 7) {
-    if (dtype == 1) smallc_go<f16, 7, 2, 1664, 28, 3>(a, st);
-    else smallc_go<bf16, 7, 2, 1664, 28, 3>(a, st);
-  } else {
-    if (dtype == 1) smallc_go<f16, 14, 2, 2112, 28, 3>(a, st);
-    else smallc_go<bf16, 14, 2, 2112, 28, 3>(a, st);
+#define SC(FMT, PPX, GMAX)                                                  \
+  if (fmt == FMT && gmax == GMAX) {                                         \
+    if (dtype == 1) smallc_go<f16, FMT, 2, PPX, GMAX, 3>(a, st);            \
+    else smallc_go<bf16, FMT, 2, PPX, GMAX, 3>(a, st);                      \
+    return;                                                                 \
   }
+  SC(7, 1664, 28)
+  SC(14, 2112, 28)
+  SC(7, 704, 8)
+  SC(14, 1152, 8)
+#undef SC
+  check(false, "small-channel tile not instantiated");
 }
 
 }  // namespace k

@@ -61,7 +61,7 @@ int igemm_num_params(int dtype);
 // output of k channels in the layout)
 bool igemm_param_takes_residual(int dtype, int param, int layout, int k);
 bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, int w, int r, int s,
-                       int stride, int pad);
+                       int stride, int pad, int k);
 size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s);
 // 3x3 stride-1 convolution with the input patch in LDS (an implicit-GEMM
 // parameter family; see conv_patch.hip)
@@ -83,10 +83,11 @@ struct PatchCfg {
 bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
                       int fmt, int pwt, int prows);
 void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& a, hipStream_t st);
-// Stride-2 convolution of an NHWC input with C <= 4 (a CNN stem; see conv_smallc.hip)
+// Stride-1 or -2 convolution of an NHWC input with C <= 4 (a CNN stem; see
+// conv_smallc.hip); gmax: filter chunks the kernel holds (28 for 7 x 7, 8 for 3 x 3)
 bool smallc_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
-                       int fmt, int ppx, int gmax);
-void conv_smallc(int dtype, int fmt, const ConvArgs& a, hipStream_t st);
+                       int k, int fmt, int ppx, int gmax);
+void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st);
 size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k);
 void conv_winograd(int dtype, const ConvArgs& a, hipStream_t st);
 void dwconv(int dtype, const ConvArgs& a, hipStream_t st);

@@ -30,6 +30,8 @@ CONV_CASES = [
     (5, 32, 7, 7, 24, 3, 1, 1, "none"),       # image groups with a ragged last group
     (2, 3, 45, 38, 64, 7, 2, 3, "relu"),      # stem: C = 3, 7x7/2, odd output sizes
     (1, 2, 21, 24, 72, 5, 2, 2, "relu6"),     # C = 2, 5x5/2, K = 72 (two channel tiles)
+    (2, 3, 40, 36, 64, 3, 1, 1, "relu"),      # C = 3, 3x3/1: a VGG-style first layer, several rows per tile
+    (1, 4, 19, 23, 24, 3, 2, 1, "relu6"),     # C = 4, 3x3/2: a MobileNet-style stem, K = 24
 ]
 
 
