@@ -1,0 +1,257 @@
+// 1x1 stride-1 convolution of a 64-channel NHWC input (16-bit types), an
+// implicit-GEMM routine for the layers of a bottleneck that read 64 channels.
+//
+// Such a layer reads each pixel's 128 bytes once and writes K channels (plus
+// a residual of K channels when an add is folded in), so memory traffic, not
+// MFMA work, bounds it, and its reduction is a single 64-wide step: a
+// workgroup of the tiled implicit GEMM loads its tiles, waits, computes and
+// stores with nothing to overlap.  Here workgroups are persistent: each keeps
+// its BN filter rows in LDS and streams tiles of BM pixels, loading the next
+// tile's pixels (LDS direct loads) and the current tile's residual (into
+// registers) while the current tile's MFMAs and stores run.  The tile's fp32
+// sums go through LDS so that the residual add and the stores move whole
+// 16-byte chunks of consecutive channels with consecutive lanes on
+// consecutive addresses.  LDS rows are 64 channels (128 bytes, 8 chunks);
+// chunk c of row r sits at c ^ ((r >> 1) & 7), which serves an MFMA operand
+// read of 16 consecutive rows in one pass.
+#include "gemm_common.hpp"
+#include "kcommon.hpp"
+#include "launch.hpp"
+
+namespace sn {
+namespace k {
+
+struct StreamArgs {
+  const void* x;     // [M][64]
+  const void* w;     // [Kp][64]
+  const float* bias; // [Kp]
+  const void* res;   // [M][Ks] or null
+  void* y;           // [M][Ks]
+  int M, K, Ks, act;
+  int tiles_m;
+  long long x_elems, w_elems, y_elems;
+};
+
+template <typename T, int BM, int BN, int WM, bool RES>
+__global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
+  static_assert(sizeof(T) == 2, "16-bit types");
+  constexpr int NWV = 8, NT = 512, WN = NWV / WM;
+  constexpr int RB = 128;                      // LDS row: 64 channels
+  constexpr int WTM = BM / WM, WTN = BN / WN, FM = WTM / 16, FN = WTN / 16;
+  constexpr int NA = BM * RB / 1024 / NWV;     // pixel-tile load instructions per wave
+  constexpr int NBL = BN * RB / 1024 / NWV;    // filter load instructions per wave
+  constexpr int NE = BM * BN / 8 / NT;         // 16-byte output chunks per thread and tile
+  static_assert(NA >= 1 && NBL >= 1 && NE >= 1 && NA * 1024 * NWV == BM * RB &&
+                    NBL * 1024 * NWV == BN * RB && NE * 8 * NT == BM * BN && FM >= 1 && FN >= 1,
+                "tile shape");
+  constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB;
+  constexpr int CP = BN + 4;                   // fp32 staging row pitch (floats)
+  constexpr int SM = B_BYTES + 2 * A_BYTES + BM * CP * 4 + BN * 4;
+  static_assert(SM <= 160 * 1024, "LDS capacity");
+  __shared__ __attribute__((aligned(1024))) char smem[SM];
+  char* const Bs = smem;
+  char* const As = smem + B_BYTES;
+  float* const Cs = reinterpret_cast<float*>(As + 2 * A_BYTES);
+  float* const Bias = Cs + BM * CP;
+  auto swz = [](int row) { return (row >> 1) & 7; };
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  const int n0 = blockIdx.y * BN;
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_elems * 2);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, a.w_elems * 2);
+  const __amdgpu_buffer_rsrc_t ry = make_rsrc(a.y, a.y_elems * 2);
+  const __amdgpu_buffer_rsrc_t rr = make_rsrc(RES ? a.res : a.y, a.y_elems * 2);
+
+  // bias of the workgroup's channels through LDS (no global load of it
+  // stays outstanding in the tile loop)
+  if (tid < BN) Bias[tid] = n0 + tid < a.K ? a.bias[n0 + tid] : 0.f;
+
+  // load slots: instruction b = wave + 8 i fills rows [8 b, 8 b + 8); this
+  // lane fills row 8 b + lane / 8, physical chunk lane % 8 = logical chunk
+  // (lane % 8) ^ swz(row)
+  const int prow = lane >> 3, pch = lane & 7;
+#pragma unroll
+  for (int i = 0; i < NBL; ++i) {
+    const int row = (wave + NWV * i) * 8 + prow;
+    const int k = n0 + row;
+    const unsigned off = k < a.K ? (unsigned)(k * 64 + ((pch ^ swz(row)) << 3)) * 2u : kOOB;
+    dma16(rw, Bs + (wave + NWV * i) * 1024, off, 0);
+  }
+  unsigned aoff[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    const int row = (wave + NWV * i) * 8 + prow;
+    aoff[i] = (unsigned)(row * 64 + ((pch ^ swz(row)) << 3)) * 2u;
+  }
+  auto issue_a = [&](int mt, int buf) {
+    const int m0 = mt * BM;
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int m = m0 + (wave + NWV * i) * 8 + prow;
+      dma16(rx, As + buf * A_BYTES + (wave + NWV * i) * 1024, m < a.M ? (unsigned)m0 * 128u + aoff[i] : kOOB, 0);
+    }
+  };
+
+  // operand chunk offsets (16-row blocks keep the lane's swizzle)
+  int aofs[2], bofs[2];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const int l = lane & 15, xo = ((ks * 4 + (lane >> 4)) ^ swz(l)) << 4;
+    aofs[ks] = (wm * WTM + l) * RB + xo;
+    bofs[ks] = (wn * WTN + l) * RB + xo;
+  }
+  typedef typename Mfma<T>::frag frag;
+  const ActClamp ac = act_clamp(a.act);
+
+  int mt = blockIdx.x;
+  issue_a(mt, 0);
+  __syncthreads();  // the bias in LDS
+  float bias[FN][4];
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) bias[j][v] = Bias[wn * WTN + j * 16 + (lane >> 4) * 4 + v];
+
+  for (int t = 0; mt < a.tiles_m; ++t, mt += gridDim.x) {
+    const int buf = t & 1;
+    const int m0 = mt * BM;
+    // this tile's residual, in flight during the MFMAs
+    u32x4 rres[NE];
+    if constexpr (RES) {
+#pragma unroll
+      for (int e = 0; e < NE; ++e) {
+        const int q = tid + e * NT, row = q / (BN / 8), cj = q % (BN / 8);
+        const int m = m0 + row, n = n0 + cj * 8;
+        const unsigned off = m < a.M && n < a.K ? (unsigned)(m * a.Ks + n) * 2u : kOOB;
+        rres[e] = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    const bool next = mt + (int)gridDim.x < a.tiles_m;
+    if (next) issue_a(mt + gridDim.x, buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+    // wait for this tile's pixels: younger are the previous tile's stores
+    // (NE), this tile's residual loads and the next tile's pixel loads
+    constexpr int YR = RES ? NE : 0;
+    if (t == 0) {
+      if (next) wait_vmcnt<YR + NA>();
+      else wait_vmcnt<YR>();
+    } else {
+      if (next) wait_vmcnt<NE + YR + NA>();
+      else wait_vmcnt<NE + YR>();
+    }
+    dma_barrier();  // every wave's share landed; every wave is done with the last tile's Cs
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{bias[j][0], bias[j][1], bias[j][2], bias[j][3]};
+    const char* A = As + buf * A_BYTES;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      frag fa[FM], fb[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) fa[i] = *reinterpret_cast<const frag*>(A + aofs[ks] + i * 16 * RB);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) fb[j] = *reinterpret_cast<const frag*>(Bs + bofs[ks] + j * 16 * RB);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fb[j], fa[i], acc[i][j]);
+    }
+    // sums (bias included) to LDS: element (i, j, v) is pixel
+    // wm*WTM + i*16 + (lane&15), channel wn*WTN + j*16 + (lane>>4)*4 + v
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        *reinterpret_cast<f32x4*>(Cs + (wm * WTM + i * 16 + (lane & 15)) * CP + wn * WTN + j * 16 + (lane >> 4) * 4) =
+            acc[i][j];
+    lds_barrier();
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      const int q = tid + e * NT, row = q / (BN / 8), cj = q % (BN / 8);
+      const int m = m0 + row, n = n0 + cj * 8;
+      const unsigned off = m < a.M && n < a.K ? (unsigned)(m * a.Ks + n) * 2u : kOOB;
+      const f32x4 c0 = *reinterpret_cast<const f32x4*>(Cs + row * CP + cj * 8);
+      const f32x4 c1 = *reinterpret_cast<const f32x4*>(Cs + row * CP + cj * 8 + 4);
+      float s[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+      if constexpr (RES) {
+        T rt[8];
+        __builtin_memcpy(rt, &rres[e], 16);
+#pragma unroll
+        for (int v = 0; v < 8; ++v) s[v] += to_f(rt[v]);
+      }
+      T o[8];
+#pragma unroll
+      for (int v = 0; v < 8; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(s[v], ac.lo, ac.hi));
+      u32x4 pk;
+      __builtin_memcpy(&pk, o, 16);
+      __builtin_amdgcn_raw_buffer_store_b128(pk, ry, (int)off, 0, 0);
+    }
+  }
+}
+
+bool stream1x1_applicable(int layout, int c, int cs, int r, int s, int stride, int pad, int k, long long m,
+                          int bn) {
+  return layout == NHWC && c == 64 && cs == 64 && r == 1 && s == 1 && stride == 1 && pad == 0 &&
+         k % 8 == 0 && (k + bn - 1) / bn * bn >= k && m * 64 * 2 < (long long)kOOB &&
+         m * ((k + 7) / 8 * 8) * 2 < (long long)kOOB;
+}
+
+template <typename T, int BM, int BN, int WM>
+static void stream_go(const StreamArgs& a, int tiles_n, hipStream_t st) {
+  // persistent: about one workgroup per CU over all channel tiles
+  const int gx = std::max(1, std::min(a.tiles_m, 256 / tiles_n));
+  const dim3 grid(gx, tiles_n);
+  if (a.res)
+    SN_LAUNCH((conv1x1_stream_kernel<T, BM, BN, WM, true>), grid, dim3(512), 0, st, a);
+  else
+    SN_LAUNCH((conv1x1_stream_kernel<T, BM, BN, WM, false>), grid, dim3(512), 0, st, a);
+}
+
+void conv1x1_stream(int dtype, int bm, int bn, const ConvArgs& c, hipStream_t st) {
+  check(dtype != 0, "streaming 1x1 kernel runs 16-bit types");
+  const long long m = (long long)c.xd.n * c.xd.h * c.xd.w;
+  check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.yd.h == c.xd.h && c.yd.w == c.xd.w &&
+            stream1x1_applicable(c.xd.layout, c.xd.c, c.xd.cs, c.r, c.s, c.stride, c.pad, c.yd.c, m, bn),
+        "streaming 1x1 kernel: NHWC, C = 64, 1x1 stride 1, K % 8 == 0");
+  StreamArgs a{};
+  a.x = c.x;
+  a.w = c.w;
+  a.bias = c.bias;
+  a.res = c.res;
+  a.y = c.y;
+  a.M = (int)m;
+  a.K = c.yd.c;
+  a.Ks = c.yd.cs;
+  a.act = c.act;
+  a.tiles_m = (int)((m + bm - 1) / bm);
+  a.x_elems = m * 64;
+  a.w_elems = (long long)((a.K + 7) / 8 * 8) * 64;
+  a.y_elems = m * a.Ks;
+  const int tiles_n = (a.K + bn - 1) / bn;
+  const int key = bm * 1000 + bn;
+  switch (key) {
+    case 64 * 1000 + 256:
+      if (dtype == 1) stream_go<f16, 64, 256, 2>(a, tiles_n, st);
+      else stream_go<bf16, 64, 256, 2>(a, tiles_n, st);
+      break;
+    case 128 * 1000 + 128:
+      if (dtype == 1) stream_go<f16, 128, 128, 4>(a, tiles_n, st);
+      else stream_go<bf16, 128, 128, 4>(a, tiles_n, st);
+      break;
+    case 128 * 1000 + 64:
+      if (dtype == 1) stream_go<f16, 128, 64, 4>(a, tiles_n, st);
+      else stream_go<bf16, 128, 64, 4>(a, tiles_n, st);
+      break;
+    default:
+      check(false, "streaming 1x1 tile not instantiated");
+  }
+}
+
+}  // namespace k
+}  // namespace sn

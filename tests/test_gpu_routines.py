@@ -32,6 +32,10 @@ CONV_CASES = [
     (1, 2, 21, 24, 72, 5, 2, 2, "relu6"),     # C = 2, 5x5/2, K = 72 (two channel tiles)
     (2, 3, 40, 36, 64, 3, 1, 1, "relu"),      # C = 3, 3x3/1: a VGG-style first layer, several rows per tile
     (1, 4, 19, 23, 24, 3, 2, 1, "relu6"),     # C = 4, 3x3/2: a MobileNet-style stem, K = 24
+    # C = 64 pointwise (the streaming kernel): ragged pixel and channel tiles,
+    # and enough pixels that persistent workgroups take several tiles
+    (3, 64, 17, 19, 200, 1, 1, 0, "relu6"),
+    (8, 64, 48, 50, 72, 1, 1, 0, "relu"),
 ]
 
 
@@ -200,6 +204,7 @@ RESIDUAL_CASES = [
     (2, 24, 13, 11, 3, "relu6"),    # 3x3, C % 8 == 0 but not a multiple of 32
     (3, 40, 5, 5, 1, "relu"),       # K = 40: channel tiles with a ragged end
     (1, 256, 14, 14, 1, "relu"),    # split-reduction parameters apply
+    (4, 64, 72, 64, 1, "relu"),     # C = 64: streaming kernel, several tiles per workgroup
 ]
 
 
