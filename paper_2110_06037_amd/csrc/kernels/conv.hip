@@ -905,7 +905,7 @@ struct IgCfg {
   int bm, bn, bk, split, pf;  // split: 0 = none, 1 = split the reduction when tiles are few;
                               // pf: prefetch depth (register staging sets)
   int dma = 0, wm = 2, st = 2;  // 1: LDS-DMA kernel, 2: 3x3 patch kernel (bm = 16 * row blocks),
-                                // 3: small-channel kernel, 4: streaming 1x1 kernel (C = 64);
+                                // 3: small-channel kernel, 4: streaming 1x1 kernel (C = bk);
                                 // wave rows WM (of 4 waves), LDS stages ST
   int ppx = 0;                  // small-channel kernel: patch capacity in pixels
   PatchCfg pc{};                // patch kernel tile
@@ -943,8 +943,10 @@ static const IgCfg kIg16[] = {
     // small-channel (stem) kernel: NHWC, C <= 4, stride 1 or 2; 7 x 7 and 3 x 3 filters
     {112, 64, 32, 0, 0, 3, 2, 1, 1664, {}, 4, 28}, {224, 64, 32, 0, 0, 3, 2, 1, 2112, {}, 4, 28},
     {112, 64, 32, 0, 0, 3, 2, 1, 704, {}, 4, 8},   {224, 64, 32, 0, 0, 3, 2, 1, 1152, {}, 4, 8},
-    // streaming 1x1 kernel: NHWC, C = 64 (BM pixels x BN channels per tile, WM wave rows)
-    {64, 256, 64, 0, 0, 4, 2}, {128, 128, 64, 0, 0, 4, 4}, {128, 64, 64, 0, 0, 4, 4}};
+    // streaming 1x1 kernel: NHWC, C = bk (BM pixels x BN channels per tile, WM wave rows)
+    {64, 256, 64, 0, 0, 4, 2}, {128, 128, 64, 0, 0, 4, 4}, {128, 64, 64, 0, 0, 4, 4},
+    {64, 128, 128, 0, 0, 4, 2}, {32, 256, 128, 0, 0, 4, 1}, {64, 64, 256, 0, 0, 4, 4},
+    {32, 128, 256, 0, 0, 4, 2}};
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 
 int igemm_num_params(int dtype) {
@@ -960,7 +962,7 @@ bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, in
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
   if (g.dma == 2) return patch_applicable(layout, c, h, w, r, s, stride, pad, n, g.pc.fmt, g.pc.pwt, g.pc.prows);
   if (g.dma == 3) return smallc_applicable(layout, c, h, w, r, s, stride, pad, n, k, g.bm / 16, g.ppx, g.gmax);
-  if (g.dma == 4) return stream1x1_applicable(layout, c, c, r, s, stride, pad, k, (long long)n * h * w, g.bn);
+  if (g.dma == 4) return stream1x1_applicable(layout, c, c, r, s, stride, pad, k, (long long)n * h * w, g.bk);
   if (g.dma) {
     // fp32 index division and 32-bit byte offsets bound the output size
     const long long p = (h + 2 * pad - r) / stride + 1, q = (w + 2 * pad - s) / stride + 1;
@@ -1207,7 +1209,7 @@ static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t 
     return;
   }
   if (cfg.dma == 4) {
-    conv1x1_stream(dtype, cfg.bm, cfg.bn, c, st);
+    conv1x1_stream(dtype, cfg.bk, cfg.bm, cfg.bn, c, st);
     return;
   }
   IgArgs a = make_ig(c);

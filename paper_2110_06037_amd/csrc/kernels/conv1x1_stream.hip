@@ -1,19 +1,20 @@
-// 1x1 stride-1 convolution of a 64-channel NHWC input (16-bit types), an
-// implicit-GEMM routine for the layers of a bottleneck that read 64 channels.
+// 1x1 stride-1 convolution of an NHWC input with CC = 64, 128 or 256
+// channels (16-bit types), an implicit-GEMM routine for the pointwise layers
+// of a bottleneck whose reduction is short.
 //
-// Such a layer reads each pixel's 128 bytes once and writes K channels (plus
-// a residual of K channels when an add is folded in), so memory traffic, not
-// MFMA work, bounds it, and its reduction is a single 64-wide step: a
-// workgroup of the tiled implicit GEMM loads its tiles, waits, computes and
-// stores with nothing to overlap.  Here workgroups are persistent: each keeps
-// its BN filter rows in LDS and streams tiles of BM pixels, loading the next
-// tile's pixels (LDS direct loads) and the current tile's residual (into
-// registers) while the current tile's MFMAs and stores run.  The tile's fp32
-// sums go through LDS so that the residual add and the stores move whole
-// 16-byte chunks of consecutive channels with consecutive lanes on
-// consecutive addresses.  LDS rows are 64 channels (128 bytes, 8 chunks);
-// chunk c of row r sits at c ^ ((r >> 1) & 7), which serves an MFMA operand
-// read of 16 consecutive rows in one pass.
+// Such a layer reads each pixel once and writes K channels (plus a residual
+// of K channels when an add is folded in), so memory traffic, not MFMA work,
+// bounds it, and its reduction takes one to four 64-wide steps: a workgroup
+// of the tiled implicit GEMM loads its tiles, waits, computes and stores with
+// little to overlap.  Here workgroups are persistent: each keeps its BN
+// filter rows in LDS and streams tiles of BM pixels, loading the next tile's
+// pixels (LDS direct loads) and the current tile's residual (into registers)
+// while the current tile's MFMAs and stores run.  The tile's fp32 sums go
+// through LDS so that the residual add and the stores move whole 16-byte
+// chunks of consecutive channels with consecutive lanes on consecutive
+// addresses.  In LDS a tile is CC / 64 slabs of 64 channels, each with
+// 128-byte rows (8 chunks); chunk c of row r sits at c ^ ((r >> 1) & 7),
+// which serves an MFMA operand read of 16 consecutive rows in one pass.
 #include "gemm_common.hpp"
 #include "kcommon.hpp"
 #include "launch.hpp"
@@ -22,8 +23,8 @@ namespace sn {
 namespace k {
 
 struct StreamArgs {
-  const void* x;     // [M][64]
-  const void* w;     // [Kp][64]
+  const void* x;     // [M][CC]
+  const void* w;     // [Kp][CC]
   const float* bias; // [Kp]
   const void* res;   // [M][Ks] or null
   void* y;           // [M][Ks]
@@ -32,19 +33,20 @@ struct StreamArgs {
   long long x_elems, w_elems, y_elems;
 };
 
-template <typename T, int BM, int BN, int WM, bool RES>
+template <typename T, int CC, int BM, int BN, int WM, bool RES>
 __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
-  static_assert(sizeof(T) == 2, "16-bit types");
+  static_assert(sizeof(T) == 2 && CC % 64 == 0, "16-bit types, 64-channel slabs");
   constexpr int NWV = 8, NT = 512, WN = NWV / WM;
-  constexpr int RB = 128;                      // LDS row: 64 channels
+  constexpr int RB = 128;                      // LDS row of a slab: 64 channels
+  constexpr int NSL = CC / 64;                 // slabs
   constexpr int WTM = BM / WM, WTN = BN / WN, FM = WTM / 16, FN = WTN / 16;
-  constexpr int NA = BM * RB / 1024 / NWV;     // pixel-tile load instructions per wave
-  constexpr int NBL = BN * RB / 1024 / NWV;    // filter load instructions per wave
-  constexpr int NE = BM * BN / 8 / NT;         // 16-byte output chunks per thread and tile
-  static_assert(NA >= 1 && NBL >= 1 && NE >= 1 && NA * 1024 * NWV == BM * RB &&
-                    NBL * 1024 * NWV == BN * RB && NE * 8 * NT == BM * BN && FM >= 1 && FN >= 1,
+  constexpr int NA = NSL * BM * RB / 1024 / NWV;   // pixel-tile load instructions per wave
+  constexpr int NBL = NSL * BN * RB / 1024 / NWV;  // filter load instructions per wave
+  constexpr int NE = BM * BN / 8 / NT;             // 16-byte output chunks per thread and tile
+  static_assert(NA >= 1 && NBL >= 1 && NE >= 1 && NA * 1024 * NWV == NSL * BM * RB &&
+                    NBL * 1024 * NWV == NSL * BN * RB && NE * 8 * NT == BM * BN && FM >= 1 && FN >= 1,
                 "tile shape");
-  constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB;
+  constexpr int A_BYTES = NSL * BM * RB, B_BYTES = NSL * BN * RB;
   constexpr int CP = BN + 4;                   // fp32 staging row pitch (floats)
   constexpr int SM = B_BYTES + 2 * A_BYTES + BM * CP * 4 + BN * 4;
   static_assert(SM <= 160 * 1024, "LDS capacity");
@@ -68,39 +70,44 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   // stays outstanding in the tile loop)
   if (tid < BN) Bias[tid] = n0 + tid < a.K ? a.bias[n0 + tid] : 0.f;
 
-  // load slots: instruction b = wave + 8 i fills rows [8 b, 8 b + 8); this
-  // lane fills row 8 b + lane / 8, physical chunk lane % 8 = logical chunk
-  // (lane % 8) ^ swz(row)
+  // load slots: instruction b = wave + 8 i fills rows [8 r, 8 r + 8) of
+  // slab s (b = s * rows / 8 + r); this lane fills row 8 r + lane / 8,
+  // physical chunk lane % 8 = logical chunk (lane % 8) ^ swz(row) of the slab
   const int prow = lane >> 3, pch = lane & 7;
 #pragma unroll
   for (int i = 0; i < NBL; ++i) {
-    const int row = (wave + NWV * i) * 8 + prow;
+    const int b = wave + NWV * i, sl = b / (BN / 8), row = (b % (BN / 8)) * 8 + prow;
     const int k = n0 + row;
-    const unsigned off = k < a.K ? (unsigned)(k * 64 + ((pch ^ swz(row)) << 3)) * 2u : kOOB;
-    dma16(rw, Bs + (wave + NWV * i) * 1024, off, 0);
+    const unsigned off = k < a.K ? (unsigned)(k * CC + sl * 64 + ((pch ^ swz(row)) << 3)) * 2u : kOOB;
+    dma16(rw, Bs + b * 1024, off, 0);
   }
   unsigned aoff[NA];
+  int arow[NA];
 #pragma unroll
   for (int i = 0; i < NA; ++i) {
-    const int row = (wave + NWV * i) * 8 + prow;
-    aoff[i] = (unsigned)(row * 64 + ((pch ^ swz(row)) << 3)) * 2u;
+    const int b = wave + NWV * i, sl = b / (BM / 8), row = (b % (BM / 8)) * 8 + prow;
+    arow[i] = row;
+    aoff[i] = (unsigned)(row * CC + sl * 64 + ((pch ^ swz(row)) << 3)) * 2u;
   }
   auto issue_a = [&](int mt, int buf) {
     const int m0 = mt * BM;
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
-      const int m = m0 + (wave + NWV * i) * 8 + prow;
-      dma16(rx, As + buf * A_BYTES + (wave + NWV * i) * 1024, m < a.M ? (unsigned)m0 * 128u + aoff[i] : kOOB, 0);
+      const int m = m0 + arow[i];
+      dma16(rx, As + buf * A_BYTES + (wave + NWV * i) * 1024,
+            m < a.M ? (unsigned)m0 * (unsigned)(CC * 2) + aoff[i] : kOOB, 0);
     }
   };
 
-  // operand chunk offsets (16-row blocks keep the lane's swizzle)
-  int aofs[2], bofs[2];
+  // operand chunk offsets of the 32-wide reduction steps ks (slab ks / 2;
+  // 16-row blocks keep the lane's swizzle)
+  constexpr int KS = CC / 32;
+  int aofs[KS], bofs[KS];
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
-    const int l = lane & 15, xo = ((ks * 4 + (lane >> 4)) ^ swz(l)) << 4;
-    aofs[ks] = (wm * WTM + l) * RB + xo;
-    bofs[ks] = (wn * WTN + l) * RB + xo;
+  for (int ks = 0; ks < KS; ++ks) {
+    const int l = lane & 15, xo = (((ks % 2) * 4 + (lane >> 4)) ^ swz(l)) << 4;
+    aofs[ks] = (ks / 2) * BM * RB + (wm * WTM + l) * RB + xo;
+    bofs[ks] = (ks / 2) * BN * RB + (wn * WTN + l) * RB + xo;
   }
   typedef typename Mfma<T>::frag frag;
   const ActClamp ac = act_clamp(a.act);
@@ -151,7 +158,7 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
       for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{bias[j][0], bias[j][1], bias[j][2], bias[j][3]};
     const char* A = As + buf * A_BYTES;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < KS; ++ks) {
       frag fa[FM], fb[FN];
 #pragma unroll
       for (int i = 0; i < FM; ++i) fa[i] = *reinterpret_cast<const frag*>(A + aofs[ks] + i * 16 * RB);
@@ -196,29 +203,28 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
 }
 
 bool stream1x1_applicable(int layout, int c, int cs, int r, int s, int stride, int pad, int k, long long m,
-                          int bn) {
-  return layout == NHWC && c == 64 && cs == 64 && r == 1 && s == 1 && stride == 1 && pad == 0 &&
-         k % 8 == 0 && (k + bn - 1) / bn * bn >= k && m * 64 * 2 < (long long)kOOB &&
-         m * ((k + 7) / 8 * 8) * 2 < (long long)kOOB;
+                          int cc) {
+  return layout == NHWC && c == cc && cs == cc && r == 1 && s == 1 && stride == 1 && pad == 0 &&
+         k % 8 == 0 && m * cc * 2 < (long long)kOOB && m * ((k + 7) / 8 * 8) * 2 < (long long)kOOB;
 }
 
-template <typename T, int BM, int BN, int WM>
+template <typename T, int CC, int BM, int BN, int WM>
 static void stream_go(const StreamArgs& a, int tiles_n, hipStream_t st) {
   // persistent: about one workgroup per CU over all channel tiles
   const int gx = std::max(1, std::min(a.tiles_m, 256 / tiles_n));
   const dim3 grid(gx, tiles_n);
   if (a.res)
-    SN_LAUNCH((conv1x1_stream_kernel<T, BM, BN, WM, true>), grid, dim3(512), 0, st, a);
+    SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, true>), grid, dim3(512), 0, st, a);
   else
-    SN_LAUNCH((conv1x1_stream_kernel<T, BM, BN, WM, false>), grid, dim3(512), 0, st, a);
+    SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, false>), grid, dim3(512), 0, st, a);
 }
 
-void conv1x1_stream(int dtype, int bm, int bn, const ConvArgs& c, hipStream_t st) {
+void conv1x1_stream(int dtype, int cc, int bm, int bn, const ConvArgs& c, hipStream_t st) {
   check(dtype != 0, "streaming 1x1 kernel runs 16-bit types");
   const long long m = (long long)c.xd.n * c.xd.h * c.xd.w;
   check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.yd.h == c.xd.h && c.yd.w == c.xd.w &&
-            stream1x1_applicable(c.xd.layout, c.xd.c, c.xd.cs, c.r, c.s, c.stride, c.pad, c.yd.c, m, bn),
-        "streaming 1x1 kernel: NHWC, C = 64, 1x1 stride 1, K % 8 == 0");
+            stream1x1_applicable(c.xd.layout, c.xd.c, c.xd.cs, c.r, c.s, c.stride, c.pad, c.yd.c, m, cc),
+        "streaming 1x1 kernel: NHWC, C = CC, 1x1 stride 1, K % 8 == 0");
   StreamArgs a{};
   a.x = c.x;
   a.w = c.w;
@@ -230,27 +236,25 @@ void conv1x1_stream(int dtype, int bm, int bn, const ConvArgs& c, hipStream_t st
   a.Ks = c.yd.cs;
   a.act = c.act;
   a.tiles_m = (int)((m + bm - 1) / bm);
-  a.x_elems = m * 64;
-  a.w_elems = (long long)((a.K + 7) / 8 * 8) * 64;
+  a.x_elems = m * cc;
+  a.w_elems = (long long)((a.K + 7) / 8 * 8) * cc;
   a.y_elems = m * a.Ks;
   const int tiles_n = (a.K + bn - 1) / bn;
-  const int key = bm * 1000 + bn;
-  switch (key) {
-    case 64 * 1000 + 256:
-      if (dtype == 1) stream_go<f16, 64, 256, 2>(a, tiles_n, st);
-      else stream_go<bf16, 64, 256, 2>(a, tiles_n, st);
-      break;
-    case 128 * 1000 + 128:
-      if (dtype == 1) stream_go<f16, 128, 128, 4>(a, tiles_n, st);
-      else stream_go<bf16, 128, 128, 4>(a, tiles_n, st);
-      break;
-    case 128 * 1000 + 64:
-      if (dtype == 1) stream_go<f16, 128, 64, 4>(a, tiles_n, st);
-      else stream_go<bf16, 128, 64, 4>(a, tiles_n, st);
-      break;
-    default:
-      check(false, "streaming 1x1 tile not instantiated");
+#define SG(CC_, BM_, BN_, WM_)                                                \
+  if (cc == CC_ && bm == BM_ && bn == BN_) {                                  \
+    if (dtype == 1) stream_go<f16, CC_, BM_, BN_, WM_>(a, tiles_n, st);       \
+    else stream_go<bf16, CC_, BM_, BN_, WM_>(a, tiles_n, st);                 \
+    return;                                                                   \
   }
+  SG(64, 64, 256, 2)
+  SG(64, 128, 128, 4)
+  SG(64, 128, 64, 4)
+  SG(128, 64, 128, 2)
+  SG(128, 32, 256, 1)
+  SG(256, 64, 64, 4)
+  SG(256, 32, 128, 2)
+#undef SG
+  check(false, "streaming 1x1 tile not instantiated");
 }
 
 }  // namespace k

@@ -36,6 +36,8 @@ CONV_CASES = [
     # and enough pixels that persistent workgroups take several tiles
     (3, 64, 17, 19, 200, 1, 1, 0, "relu6"),
     (8, 64, 48, 50, 72, 1, 1, 0, "relu"),
+    (6, 128, 56, 56, 136, 1, 1, 0, "relu"),   # C = 128 and 256 pointwise, several tiles per workgroup
+    (12, 256, 40, 40, 72, 1, 1, 0, "none"),
 ]
 
 
@@ -205,6 +207,7 @@ RESIDUAL_CASES = [
     (3, 40, 5, 5, 1, "relu"),       # K = 40: channel tiles with a ragged end
     (1, 256, 14, 14, 1, "relu"),    # split-reduction parameters apply
     (4, 64, 72, 64, 1, "relu"),     # C = 64: streaming kernel, several tiles per workgroup
+    (8, 128, 50, 50, 1, "relu"),    # C = 128: streaming kernel with two 64-channel slabs
 ]
 
 
