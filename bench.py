@@ -82,8 +82,10 @@ KERNEL_SOURCES = {
     "igemm_dma_kernel": ("conv.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
     "igemm_kernel": ("conv.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
     "conv3x3_patch_kernel": ("conv_patch.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
+    "conv1x1_stream_kernel": ("conv1x1_stream.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
 }
-ALL_KERNEL_SOURCES = ("conv.hip", "conv_patch.hip", "conv_smallc.hip", "fc.hip", "misc.hip", "gemm_common.hpp",
+ALL_KERNEL_SOURCES = ("conv.hip", "conv1x1_stream.hip", "conv_patch.hip", "conv_smallc.hip", "fc.hip", "misc.hip",
+                      "gemm_common.hpp",
                       "kcommon.hpp", "launch.hpp")
 
 
@@ -97,17 +99,21 @@ def kernel_source_hash(ksub=None):
     return h.hexdigest()[:16]
 
 
-def traffic_for(routine):
-    """HBM bytes per launch of `routine` from the committed PMC summary, or None
-    when there is none for it or the kernel sources changed since it was taken."""
+def _traffic_entries():
     try:
         with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
-        return None
-    if t.get("routine") != routine or t.get("source_hash") != kernel_source_hash(t.get("kernel_symbol_part")):
-        return None
-    return t.get("bytes_per_launch")
+            return json.load(f).get("entries", [])
+    except (OSError, ValueError, AttributeError):
+        return []
+
+
+def traffic_for(routine):
+    """HBM bytes per launch of `routine` from the committed PMC summaries, or None
+    when there is none for it or its kernel sources changed since it was taken."""
+    for t in _traffic_entries():
+        if t.get("routine") == routine and t.get("source_hash") == kernel_source_hash(t.get("kernel_symbol_part")):
+            return t.get("bytes_per_launch")
+    return None
 
 
 def _pmc_rows(d):
@@ -139,8 +145,16 @@ def summarize_pmc(fetch_dir, write_dir, routine, ksub, out, calib_mib):
     t = {"routine": routine, "kernel_symbol_part": ksub, "source_hash": kernel_source_hash(ksub),
          "bytes_per_launch": per,
          "counters": res, "calibration": f"device copy of {calib_mib} MiB (read and write)"}
+    # one entry per routine: replace this routine's entry, keep the others
+    entries = []
+    try:
+        with open(out) as fh:
+            entries = json.load(fh).get("entries", [])
+    except (OSError, ValueError, AttributeError):
+        pass
+    entries = [e for e in entries if e.get("routine") != routine] + [t]
     with open(out, "w") as fh:
-        json.dump(t, fh, indent=1)
+        json.dump({"entries": entries}, fh, indent=1)
     print(json.dumps(t))
 
 
