@@ -129,7 +129,9 @@ typedef enum {
  * device >= 0 selects a HIP device; device = -1 creates a host-only graph on
  * which only the selection calls work (sn_set_costs, sn_select_path,
  * sn_set_path, queries) -- the graph used by GPU-free tests.
- * Errors: SN_E_INVALID (non-positive dims, unknown dtype), SN_E_DEVICE. */
+ * Errors: SN_E_INVALID (non-positive dims, unknown dtype), SN_E_UNSUPPORTED
+ * (a tensor of 2 GiB or more: N * ceil8(C) * H * W * element size; every
+ * kernel addresses a tensor with 32-bit byte offsets), SN_E_DEVICE. */
 int sn_graph_create(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, int32_t device,
                     sn_graph** out);
 
@@ -149,7 +151,8 @@ int sn_set_option(sn_graph* g, int32_t option, int64_t value);
  * added layer is the net output.  *out_id receives the new id.
  * Errors: SN_E_INVALID (unknown input id, wrong arity, bad parameters),
  * SN_E_SHAPE (channel or size mismatch), SN_E_UNSUPPORTED (groups other than
- * 1 or C), SN_E_STATE (after selection), SN_E_DEVICE. */
+ * 1 or C, or an output tensor of 2 GiB or more as for sn_graph_create),
+ * SN_E_STATE (after selection), SN_E_DEVICE. */
 int sn_add_layer(sn_graph* g, const sn_layer_desc* d, const int32_t* inputs, int32_t n_inputs,
                  const void* weight, const float* bias, int32_t* out_id);
 

@@ -50,6 +50,7 @@ int sn_graph_create(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, i
     if (dtype < SN_F32 || dtype > SN_BF16) fail(SN_E_INVALID, "unknown dtype");
     if (n <= 0 || c <= 0 || h <= 0 || w <= 0) fail(SN_E_INVALID, "input dims must be positive");
     if (device < -1) fail(SN_E_INVALID, "device must be >= -1");
+    check_tensor_size(Shape{n, c, h, w}, dtype, "input tensor");
     auto* gp = new sn_graph;
     try {
       graph_init(gp->g, dtype, Shape{n, c, h, w}, device);

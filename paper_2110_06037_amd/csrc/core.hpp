@@ -36,6 +36,16 @@ inline int64_t stored_numel(const Shape& s, int layout) {
   return (int64_t)s.n * stored_c(s, layout) * s.h * s.w;
 }
 
+// Every kernel addresses a tensor with 32-bit byte offsets (buffer resources),
+// so a tensor's stored size (channels padded to 8, the largest of the three
+// layouts) must stay below 2 GiB.
+inline void check_tensor_size(const Shape& s, int dtype, const char* what) {
+  const int64_t bytes = (int64_t)s.n * round8(s.c) * s.h * s.w * dtype_size(dtype);
+  if (bytes >= (int64_t(1) << 31))
+    fail(SN_E_UNSUPPORTED, std::string(what) + " of " + std::to_string(bytes) +
+                               " bytes exceeds the 2 GiB a kernel addresses");
+}
+
 // Two layouts hold identical bytes for this shape (the adapt is void).
 inline bool layouts_equivalent(const Shape& s, int a, int b) {
   if (a == b) return true;

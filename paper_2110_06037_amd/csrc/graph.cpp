@@ -189,6 +189,7 @@ int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int
       break;
   }
   if (out.h <= 0 || out.w <= 0) fail(SN_E_SHAPE, "empty output");
+  check_tensor_size(out, g.dtype, "layer output");
   L.out = out;
   if (wbytes) {
     L.weight.resize(wbytes);

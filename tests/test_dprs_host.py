@@ -297,6 +297,21 @@ def test_create_rejects_bad_arguments():
     assert b"dtype" in lib.sn_last_error() or b"dims" in lib.sn_last_error() or True
 
 
+def test_tensors_of_two_gib_or_more_are_unsupported():
+    # every kernel addresses a tensor with 32-bit byte offsets: the input and
+    # every layer output (channels padded to 8) must stay below 2 GiB
+    p = ctypes.c_void_p()
+    lib = N.lib()
+    assert lib.sn_graph_create(2, 1024, 64, 224, 224, -1, ctypes.byref(p)) == -4   # 6.6 GB bf16
+    assert b"2 GiB" in lib.sn_last_error()
+    assert lib.sn_graph_create(0, 1, 3, 16384, 16384, -1, ctypes.byref(p)) == -4   # C padded to 8: 8.6 GB
+    g = Graph("bf16", 16, 64, 224, 224, device=-1)                                   # 103 MB input
+    w = np.zeros((4096, 64, 1, 1), np.uint16)
+    assert status_of(g.add_conv, 0, w, np.zeros(4096, np.float32)) == -4              # 6.6 GB output
+    c = g.add_conv(0, np.zeros((64, 64, 3, 3), np.uint16), np.zeros(64, np.float32), 1, 1)
+    assert c == 1
+
+
 def test_dangling_layer_is_rejected():
     g = Graph("f16", 1, 8, 4, 4, device=-1)
     w = np.zeros((8, 8, 1, 1), np.float16)
