@@ -8,8 +8,9 @@
 // of the tiled implicit GEMM loads its tiles, waits, computes and stores with
 // little to overlap.  Here workgroups are persistent: each keeps its BN
 // filter rows in LDS and streams tiles of BM pixels, loading the next tile's
-// pixels (LDS direct loads) and the current tile's residual (into registers)
-// while the current tile's MFMAs and stores run.  The tile's fp32 sums go
+// pixels (LDS direct loads) and its residual (into registers) while the
+// current tile's MFMAs and stores run; each wave holds its filter
+// fragments in registers, so LDS serves only pixel fragments.  The tile's fp32 sums go
 // through LDS so that the residual add and the stores move whole 16-byte
 // chunks of consecutive channels with consecutive lanes on consecutive
 // addresses.  In LDS a tile is CC / 64 slabs of 64 channels, each with
@@ -114,40 +115,58 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
 
   int mt = blockIdx.x;
   issue_a(mt, 0);
-  __syncthreads();  // the bias in LDS
+  // the wave's filter fragments stay in registers for the whole kernel, so
+  // the tile loop reads only pixel fragments from LDS
+  wait_vmcnt<0>();  // this wave's filter and first-tile loads
+  __syncthreads();  // every wave's filter share, first pixel tile and the bias are in LDS
+  frag fbr[KS][FN];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fbr[ks][j] = *reinterpret_cast<const frag*>(Bs + bofs[ks] + j * 16 * RB);
   float bias[FN][4];
 #pragma unroll
   for (int j = 0; j < FN; ++j)
 #pragma unroll
     for (int v = 0; v < 4; ++v) bias[j][v] = Bias[wn * WTN + j * 16 + (lane >> 4) * 4 + v];
 
-  for (int t = 0; mt < a.tiles_m; ++t, mt += gridDim.x) {
+  // the residual of a tile is loaded one tile ahead, like its pixels
+  auto load_res = [&](int mtile, u32x4 (&r)[NE]) {
+    const int m0r = mtile * BM;
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      const int q = tid + e * NT, row = q / (BN / 8), cj = q % (BN / 8);
+      const int m = m0r + row, n = n0 + cj * 8;
+      const unsigned off = m < a.M && n < a.K ? (unsigned)(m * a.Ks + n) * 2u : kOOB;
+      r[e] = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
+    }
+  };
+  // two residual register sets alternate between tiles (a copy from the
+  // set still being loaded would wait for every outstanding load)
+  u32x4 ra[NE], rb[NE];
+  if constexpr (RES) load_res(mt, ra);
+
+  // one tile: its pixels are in LDS buffer t % 2 (the first tile's landed
+  // before the barrier above) and its residual in cur; the next tile's
+  // residual goes to nxt and its pixels to the other buffer; returns whether
+  // another tile follows
+  auto tile = [&](int t, u32x4 (&cur)[NE], u32x4 (&nxt)[NE]) {
     const int buf = t & 1;
     const int m0 = mt * BM;
-    // this tile's residual, in flight during the MFMAs
-    u32x4 rres[NE];
+    const bool next = mt + (int)gridDim.x < a.tiles_m;
     if constexpr (RES) {
-#pragma unroll
-      for (int e = 0; e < NE; ++e) {
-        const int q = tid + e * NT, row = q / (BN / 8), cj = q % (BN / 8);
-        const int m = m0 + row, n = n0 + cj * 8;
-        const unsigned off = m < a.M && n < a.K ? (unsigned)(m * a.Ks + n) * 2u : kOOB;
-        rres[e] = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
-      }
+      if (next) load_res(mt + gridDim.x, nxt);
     }
     __builtin_amdgcn_sched_barrier(0);
-    const bool next = mt + (int)gridDim.x < a.tiles_m;
     if (next) issue_a(mt + gridDim.x, buf ^ 1);
     __builtin_amdgcn_sched_barrier(0);
     // wait for this tile's pixels: younger are the previous tile's stores
-    // (NE), this tile's residual loads and the next tile's pixel loads
+    // (NE), the next tile's residual and the next tile's pixel loads; this
+    // tile's residual is older, so it has arrived too
     constexpr int YR = RES ? NE : 0;
-    if (t == 0) {
-      if (next) wait_vmcnt<YR + NA>();
-      else wait_vmcnt<YR>();
-    } else {
+    if (t > 0) {
       if (next) wait_vmcnt<NE + YR + NA>();
-      else wait_vmcnt<NE + YR>();
+      else wait_vmcnt<NE>();
     }
     dma_barrier();  // every wave's share landed; every wave is done with the last tile's Cs
 
@@ -159,15 +178,13 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
     const char* A = As + buf * A_BYTES;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      frag fa[FM], fb[FN];
+      frag fa[FM];
 #pragma unroll
       for (int i = 0; i < FM; ++i) fa[i] = *reinterpret_cast<const frag*>(A + aofs[ks] + i * 16 * RB);
 #pragma unroll
-      for (int j = 0; j < FN; ++j) fb[j] = *reinterpret_cast<const frag*>(Bs + bofs[ks] + j * 16 * RB);
-#pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fb[j], fa[i], acc[i][j]);
+        for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fbr[ks][j], fa[i], acc[i][j]);
     }
     // sums (bias included) to LDS: element (i, j, v) is pixel
     // wm*WTM + i*16 + (lane&15), channel wn*WTN + j*16 + (lane>>4)*4 + v
@@ -188,7 +205,7 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
       float s[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
       if constexpr (RES) {
         T rt[8];
-        __builtin_memcpy(rt, &rres[e], 16);
+        __builtin_memcpy(rt, &cur[e], 16);
 #pragma unroll
         for (int v = 0; v < 8; ++v) s[v] += to_f(rt[v]);
       }
@@ -199,6 +216,15 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
       __builtin_memcpy(&pk, o, 16);
       __builtin_amdgcn_raw_buffer_store_b128(pk, ry, (int)off, 0, 0);
     }
+    return next;
+  };
+  // tiles mt, mt + G, ... (G = grid size); the loop is unrolled by two so
+  // that the residual sets swap roles without copies
+  for (int t = 0;; t += 2) {
+    if (!tile(t, ra, rb)) break;
+    mt += gridDim.x;
+    if (!tile(t + 1, rb, ra)) break;
+    mt += gridDim.x;
   }
 }
 
