@@ -962,7 +962,7 @@ bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, in
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
   if (g.dma == 2) return patch_applicable(layout, c, h, w, r, s, stride, pad, n, g.pc.fmt, g.pc.pwt, g.pc.prows);
   if (g.dma == 3) return smallc_applicable(layout, c, h, w, r, s, stride, pad, n, k, g.bm / 16, g.ppx, g.gmax);
-  if (g.dma == 4) return stream1x1_applicable(layout, c, c, r, s, stride, pad, k, (long long)n * h * w, g.bk);
+  if (g.dma == 4) return stream1x1_applicable(layout, c, c, n, h, w, r, s, stride, pad, k, g.bk);
   if (g.dma) {
     // fp32 index division and 32-bit byte offsets bound the output size
     const long long p = (h + 2 * pad - r) / stride + 1, q = (w + 2 * pad - s) / stride + 1;

@@ -1,5 +1,5 @@
-// 1x1 stride-1 convolution of an NHWC input with CC = 64, 128 or 256
-// channels (16-bit types), an implicit-GEMM routine for the pointwise layers
+// 1x1 convolution (stride 1 or 2, no padding) of an NHWC input with CC =
+// 64, 128 or 256 channels (16-bit types), an implicit-GEMM routine for the pointwise layers
 // of a bottleneck whose reduction is short.
 //
 // Such a layer reads each pixel once and writes K channels (plus a residual
@@ -24,12 +24,14 @@ namespace sn {
 namespace k {
 
 struct StreamArgs {
-  const void* x;     // [M][CC]
+  const void* x;     // [N][H][W][CC]
   const void* w;     // [Kp][CC]
   const float* bias; // [Kp]
   const void* res;   // [M][Ks] or null
-  void* y;           // [M][Ks]
+  void* y;           // [M][Ks], M = N * P * Q output pixels
   int M, K, Ks, act;
+  int H, W, P, Q, stride;
+  FastDiv fd_pq, fd_q;
   int tiles_m;
   long long x_elems, w_elems, y_elems;
 };
@@ -82,21 +84,28 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
     const unsigned off = k < a.K ? (unsigned)(k * CC + sl * 64 + ((pch ^ swz(row)) << 3)) * 2u : kOOB;
     dma16(rw, Bs + b * 1024, off, 0);
   }
-  unsigned aoff[NA];
+  unsigned achk[NA];  // the lane's chunk within a pixel's channels (bytes)
   int arow[NA];
 #pragma unroll
   for (int i = 0; i < NA; ++i) {
     const int b = wave + NWV * i, sl = b / (BM / 8), row = (b % (BM / 8)) * 8 + prow;
     arow[i] = row;
-    aoff[i] = (unsigned)(row * CC + sl * 64 + ((pch ^ swz(row)) << 3)) * 2u;
+    achk[i] = (unsigned)(sl * 64 + ((pch ^ swz(row)) << 3)) * 2u;
   }
+  // output pixel m reads input pixel m (stride 1) or (img, 2p, 2q) (stride 2)
   auto issue_a = [&](int mt, int buf) {
     const int m0 = mt * BM;
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       const int m = m0 + arow[i];
+      int pix = m;
+      if (a.stride != 1) {
+        const int img = fdiv(m, a.fd_pq), pq = m - img * (a.P * a.Q);
+        const int p = fdiv(pq, a.fd_q), q = pq - p * a.Q;
+        pix = (img * a.H + p * a.stride) * a.W + q * a.stride;
+      }
       dma16(rx, As + buf * A_BYTES + (wave + NWV * i) * 1024,
-            m < a.M ? (unsigned)m0 * (unsigned)(CC * 2) + aoff[i] : kOOB, 0);
+            m < a.M ? (unsigned)pix * (unsigned)(CC * 2) + achk[i] : kOOB, 0);
     }
   };
 
@@ -228,10 +237,12 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   }
 }
 
-bool stream1x1_applicable(int layout, int c, int cs, int r, int s, int stride, int pad, int k, long long m,
-                          int cc) {
-  return layout == NHWC && c == cc && cs == cc && r == 1 && s == 1 && stride == 1 && pad == 0 &&
-         k % 8 == 0 && m * cc * 2 < (long long)kOOB && m * ((k + 7) / 8 * 8) * 2 < (long long)kOOB;
+bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
+                          int k, int cc) {
+  const long long p = (h - 1) / stride + 1, q = (w - 1) / stride + 1;
+  return layout == NHWC && c == cc && cs == cc && r == 1 && s == 1 && (stride == 1 || stride == 2) &&
+         pad == 0 && k % 8 == 0 && (long long)n * h * w * cc * 2 < (long long)kOOB &&
+         (long long)n * p * q * ((k + 7) / 8 * 8) * 2 < (long long)kOOB;
 }
 
 template <typename T, int CC, int BM, int BN, int WM>
@@ -247,10 +258,12 @@ static void stream_go(const StreamArgs& a, int tiles_n, hipStream_t st) {
 
 void conv1x1_stream(int dtype, int cc, int bm, int bn, const ConvArgs& c, hipStream_t st) {
   check(dtype != 0, "streaming 1x1 kernel runs 16-bit types");
-  const long long m = (long long)c.xd.n * c.xd.h * c.xd.w;
-  check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.yd.h == c.xd.h && c.yd.w == c.xd.w &&
-            stream1x1_applicable(c.xd.layout, c.xd.c, c.xd.cs, c.r, c.s, c.stride, c.pad, c.yd.c, m, cc),
-        "streaming 1x1 kernel: NHWC, C = CC, 1x1 stride 1, K % 8 == 0");
+  const long long m = (long long)c.yd.n * c.yd.h * c.yd.w;
+  check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.stride >= 1 &&
+            c.yd.h == (c.xd.h - 1) / c.stride + 1 && c.yd.w == (c.xd.w - 1) / c.stride + 1 &&
+            stream1x1_applicable(c.xd.layout, c.xd.c, c.xd.cs, c.xd.n, c.xd.h, c.xd.w, c.r, c.s, c.stride,
+                                 c.pad, c.yd.c, cc),
+        "streaming 1x1 kernel: NHWC, C = CC, 1x1 stride 1 or 2 without padding, K % 8 == 0");
   StreamArgs a{};
   a.x = c.x;
   a.w = c.w;
@@ -262,7 +275,14 @@ void conv1x1_stream(int dtype, int cc, int bm, int bn, const ConvArgs& c, hipStr
   a.Ks = c.yd.cs;
   a.act = c.act;
   a.tiles_m = (int)((m + bm - 1) / bm);
-  a.x_elems = m * cc;
+  a.H = c.xd.h;
+  a.W = c.xd.w;
+  a.P = c.yd.h;
+  a.Q = c.yd.w;
+  a.stride = c.stride;
+  a.fd_pq = make_fastdiv(a.P * a.Q);
+  a.fd_q = make_fastdiv(a.Q);
+  a.x_elems = (long long)c.xd.n * c.xd.h * c.xd.w * cc;
   a.w_elems = (long long)((a.K + 7) / 8 * 8) * cc;
   a.y_elems = m * a.Ks;
   const int tiles_n = (a.K + bn - 1) / bn;

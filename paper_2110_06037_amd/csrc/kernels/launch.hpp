@@ -88,11 +88,11 @@ void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& a, hipStream_t s
 bool smallc_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
                        int k, int fmt, int ppx, int gmax);
 void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st);
-// 1x1 stride-1 convolution of an NHWC input with cc = 64, 128 or 256
-// channels by persistent workgroups streaming pixel tiles (see
-// conv1x1_stream.hip); m = pixels
-bool stream1x1_applicable(int layout, int c, int cs, int r, int s, int stride, int pad, int k, long long m,
-                          int cc);
+// 1x1 convolution (stride 1 or 2, no padding) of an NHWC input with cc =
+// 64, 128 or 256 channels by persistent workgroups streaming pixel tiles
+// (see conv1x1_stream.hip)
+bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
+                          int k, int cc);
 void conv1x1_stream(int dtype, int cc, int bm, int bn, const ConvArgs& a, hipStream_t st);
 size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k);
 void conv_winograd(int dtype, const ConvArgs& a, hipStream_t st);

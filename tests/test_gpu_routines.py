@@ -38,6 +38,8 @@ CONV_CASES = [
     (8, 64, 48, 50, 72, 1, 1, 0, "relu"),
     (6, 128, 56, 56, 136, 1, 1, 0, "relu"),   # C = 128 and 256 pointwise, several tiles per workgroup
     (12, 256, 40, 40, 72, 1, 1, 0, "none"),
+    (16, 128, 57, 50, 264, 1, 2, 0, "relu6"),  # stride-2 pointwise projections (odd input sizes)
+    (8, 64, 40, 41, 72, 1, 2, 0, "none"),
 ]
 
 
