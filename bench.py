@@ -225,6 +225,23 @@ def time_steps(g, x, out, steps, warmup):
     return (time.perf_counter() - t0) / steps
 
 
+def step_stats(g, x, out, n):
+    """Per-step latency distribution of the selected path: n steps, each between
+    its own pair of HIP events on the stream the path runs on (the pair adds a
+    few microseconds of dispatch gap that the block-timed value does not have)."""
+    import statistics
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for a, b in ev:
+        a.record()
+        g.run(x, out)
+        b.record()
+    torch.cuda.synchronize()
+    ms = [a.elapsed_time(b) for a, b in ev]
+    return {"median": round(statistics.median(ms), 4), "mean": round(statistics.fmean(ms), 4),
+            "std": round(statistics.pstdev(ms), 4), "min": round(min(ms), 4), "runs": n}
+
+
 def cpu_baseline(spec, t, budget_s):
     """The oracle (naive float64, OpenMP) on the first images of the batch."""
     import numpy as np
@@ -356,6 +373,8 @@ def main():
             f"selected {label}: {sec * 1e3:.3f} ms/step")
     ids, model_ns = g.path()
     value = args.batch / sec
+    steps_dist = step_stats(g, x, out, min(max(args.steps, 10), 100))
+    log(f"[bench] per-step latency (ms): {steps_dist}")
 
     # per-layer times over K instrumented steps: each layer's launches are
     # repeated back to back with HIP events tied to the first and last dispatch
@@ -366,6 +385,12 @@ def main():
         _, ms = g.run_timed(x, out, reps=args.timing_reps)
         acc += np.array(ms)
     layer_ms = acc / passes
+    # cache-cold per-layer times: the library writes a 512 MiB buffer (more
+    # than L2 and the Infinity Cache hold) before each layer; one repetition
+    # per layer, median over 5 passes
+    g.set_option(N.OPT_FLUSH, 512 << 20)
+    cold = np.median(np.array([g.run_timed(x, out, reps=1)[1] for _ in range(5)]), axis=0)
+    g.set_option(N.OPT_FLUSH, 0)
     groups = {}      # (routine, layer type) -> its launches in one step: one kernel symbol each
                      # (the direct routine of an add and of a pool are different kernels)
     cats = {}        # layer category -> totals (for the 3x3 MFMA utilisation)
@@ -381,7 +406,7 @@ def main():
             gr["launches"] += 1
             gr["cats"].add(cat)
         per_layer.append({"layer": i, "type": cat, "routine": rt["name"],
-                          "us": round(layer_ms[i] * 1e3, 2),
+                          "us": round(layer_ms[i] * 1e3, 2), "us_cold": round(float(cold[i]) * 1e3, 2),
                           "tflops": round(flops / (layer_ms[i] * 1e-3) / 1e12, 2) if flops and layer_ms[i] else 0,
                           "gbs": round(byt / (layer_ms[i] * 1e-3) / 1e9, 1) if layer_ms[i] else 0})
     dom_key = max(groups, key=lambda k: groups[k]["ms"])
@@ -465,6 +490,8 @@ def main():
                             if integ else "DPRS-selected routines")},
         "roofline": roof,
         "cpu_baseline": cpu,
+        "step_ms": steps_dist,
+        "layer_sum_ms": {"warm": round(float(layer_ms[1:].sum()), 4), "cold": round(float(cold[1:].sum()), 4)},
         "img_s_bs1": bs1,
         "conv3x3_mfma_util": round(conv3_util, 4) if conv3_util else None,
         "dprs_img_s": round(args.batch / sec_dp, 2),

@@ -121,7 +121,9 @@ typedef enum {
   SN_OPT_ALGOS = 1,     /* bitmask of allowed algorithms (bit = sn_algo), default all */
   SN_OPT_PARAMS = 2,    /* 0: one routine parameter per algorithm; 1: all (default 1) */
   SN_OPT_HIPGRAPH = 3,  /* 1: sn_run replays a captured HIP graph (default 0)        */
-  SN_OPT_SEED = 4       /* seed of the profiler's scratch-tensor fill (default 1)    */
+  SN_OPT_SEED = 4,      /* seed of the profiler's scratch-tensor fill (default 1)    */
+  SN_OPT_FLUSH = 5      /* bytes sn_run_timed writes to a scratch buffer before each
+                           layer, evicting the caches (0 = off, the default)        */
 } sn_option;
 
 /* Creates a graph whose auxiliary input layer (id 0) carries the user tensor
@@ -193,7 +195,10 @@ int sn_run(sn_graph* g, const void* d_in, void* d_out, void* hip_stream);
  * dispatch and the end of its last (hipExtLaunchKernelGGL), so host launch
  * latency and the events' own dispatch gaps are amortised over reps.  Every
  * launch writes buffers distinct from the ones it reads, so d_out holds the
- * same result as after sn_run.  Used to attribute time per routine.
+ * same result as after sn_run.  Used to attribute time per routine.  With
+ * SN_OPT_FLUSH > 0 a device buffer of that many bytes is written before each
+ * layer's repetitions (outside the timed launches), so with reps = 1 the
+ * times are cache-cold ones; the buffer is allocated and freed by the call.
  * Errors: as sn_run; SN_E_INVALID if n is not the number of layers or reps
  * is outside 1..10000. */
 int sn_run_timed(sn_graph* g, const void* d_in, void* d_out, void* hip_stream, int32_t reps,

@@ -102,6 +102,10 @@ int sn_set_option(sn_graph* gp, int32_t option, int64_t value) {
       case SN_OPT_SEED:
         g.opt_seed = value;
         break;
+      case SN_OPT_FLUSH:
+        if (value < 0 || value > (int64_t(1) << 34)) fail(SN_E_INVALID, "FLUSH is 0..16 GiB");
+        g.opt_flush = value;
+        break;
       default:
         fail(SN_E_INVALID, "unknown option");
     }

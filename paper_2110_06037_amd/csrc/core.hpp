@@ -109,6 +109,7 @@ struct Graph {
   int device = -1;
   Shape in;
   int64_t opt_layouts = 7, opt_algos = 7, opt_params = 1, opt_hipgraph = 0, opt_seed = 1;
+  int64_t opt_flush = 0;  // bytes written before each layer of a timed run (0 = none)
   std::vector<Layer> layers;  // layers[0] = auxiliary input
   std::vector<Edge> edges;    // every (input -> layer) edge, in insertion order
   Edge out_edge{};            // (last layer -> auxiliary output); from/to set on use

@@ -25,7 +25,7 @@ ALGO_NAME = {v: k for k, v in ALGO.items()}
 L_INPUT, L_CONV2D, L_MAXPOOL, L_GAP, L_ADD, L_FC, L_OUTPUT = range(7)
 ACT = {"none": 0, "relu": 1, "relu6": 2}
 SELECT_DPRS, SELECT_FIXED = 0, 1
-OPT_LAYOUTS, OPT_ALGOS, OPT_PARAMS, OPT_HIPGRAPH, OPT_SEED = range(5)
+OPT_LAYOUTS, OPT_ALGOS, OPT_PARAMS, OPT_HIPGRAPH, OPT_SEED, OPT_FLUSH = range(6)
 
 STATUS = {0: "SN_OK", -1: "SN_E_INVALID", -2: "SN_E_SHAPE", -3: "SN_E_STATE",
           -4: "SN_E_UNSUPPORTED", -5: "SN_E_DEVICE", -6: "SN_E_NOMEM", -7: "SN_E_INTERNAL"}

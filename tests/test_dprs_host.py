@@ -288,6 +288,14 @@ def test_abi_state_machine_and_errors():
     assert g.path()[0] == [0, 0, 0, 0]
 
 
+def test_flush_option_bounds():
+    g = Graph("bf16", 1, 8, 8, 8, device=-1)
+    g.set_option(N.OPT_FLUSH, 512 << 20)   # accepted at any time (a timing setting)
+    g.set_option(N.OPT_FLUSH, 0)
+    assert status_of(g.set_option, N.OPT_FLUSH, -1) == -1
+    assert status_of(g.set_option, N.OPT_FLUSH, 1 << 40) == -1
+
+
 def test_create_rejects_bad_arguments():
     p = ctypes.c_void_p()
     lib = N.lib()

@@ -60,6 +60,13 @@ def test_tiny_chain_measured_table_dp_equals_exhaustive_and_parity():
     y, ms = g.run_timed(xd, reps=3)
     assert np.array_equal(from_dev(y, "f32").reshape(spec["batch"], -1), out)
     assert ms[0] == 0 and all(m > 0 for m in ms[1:]), ms
+    # cache-cold timing: a scratch buffer is written before each layer; the
+    # result is unchanged
+    g.set_option(N.OPT_FLUSH, 64 << 20)
+    y, ms = g.run_timed(xd, reps=1)
+    g.set_option(N.OPT_FLUSH, 0)
+    assert np.array_equal(from_dev(y, "f32").reshape(spec["batch"], -1), out)
+    assert ms[0] == 0 and all(m > 0 for m in ms[1:]), ms
     for lay in ("NCHW", "NHWC"):
         for algo in ("direct", "igemm"):
             g.select("fixed", lay, algo)
