@@ -288,6 +288,16 @@ def test_abi_state_machine_and_errors():
     assert g.path()[0] == [0, 0, 0, 0]
 
 
+def test_missing_library_fails_loudly(monkeypatch):
+    # the binding has no CPU fallback: without the built library every call raises
+    monkeypatch.setattr(N, "_lib", None)
+    monkeypatch.setattr(N, "LIB_PATH", "/nonexistent/libsoftneuro.so")
+    with pytest.raises(ImportError):
+        N.lib()
+    with pytest.raises(ImportError):
+        Graph("bf16", 1, 8, 8, 8, device=-1)
+
+
 def test_flush_option_bounds():
     g = Graph("bf16", 1, 8, 8, 8, device=-1)
     g.set_option(N.OPT_FLUSH, 512 << 20)   # accepted at any time (a timing setting)
