@@ -40,6 +40,9 @@ CONV_CASES = [
     (12, 256, 40, 40, 72, 1, 1, 0, "none"),
     (16, 128, 57, 50, 264, 1, 2, 0, "relu6"),  # stride-2 pointwise projections (odd input sizes)
     (8, 64, 40, 41, 72, 1, 2, 0, "none"),
+    (2, 1, 17, 15, 8, 3, 1, 1, "relu"),      # degenerate channel counts: one input channel,
+    (1, 5, 9, 9, 1, 3, 1, 1, "none"),        # one output channel,
+    (3, 8, 1, 1, 16, 1, 1, 0, "relu6"),      # a 1 x 1 image
 ]
 
 
