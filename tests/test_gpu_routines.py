@@ -175,7 +175,9 @@ def test_fc_activation(dtype, case):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("c", [12, 3])
+# C = 1 (NCHW and NHWC hold the same bytes) and C = 8 (NHWC and NC8HW8 do)
+# take the void adapt between those layouts
+@pytest.mark.parametrize("c", [12, 3, 1, 8])
 # H * W % 8 == 0 takes the 8-pixel transpose; 40 x 40 spans several of its
 # workgroups with a ragged last one
 @pytest.mark.parametrize("hw", [(9, 9), (12, 10), (40, 40)])
