@@ -3,7 +3,7 @@
 //
 // With a batch of at most 64 the layer is a skinny GEMM whose cost is
 // reading W once (2048 x 1000 bf16 = 4 MB for a ResNet classifier).  A
-// workgroup owns 16 output features and all of the batch; its 8 waves split
+// workgroup owns 16 output features and 16 rows of the batch; its 8 waves split
 // the input features (wave w takes the 32-wide reduction steps w, w + 8, ...)
 // so every workgroup keeps many 16-byte loads in flight, and the 8 partial
 // sums meet in LDS.  Operands come straight from global memory: W rows are
@@ -38,7 +38,7 @@ __global__ __launch_bounds__(64 * kFcWaves) void fc_mfma_kernel(const T* __restr
   unsigned xrow[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
-    const int n = j * 16 + (lane & 15);
+    const int n = (blockIdx.y * NB + j) * 16 + (lane & 15);
     xrow[j] = n < N ? (unsigned)n * (unsigned)cin_s : kOOB;
   }
   f32x4 acc[NB];
@@ -75,7 +75,7 @@ __global__ __launch_bounds__(64 * kFcWaves) void fc_mfma_kernel(const T* __restr
   f32x4 s = red[0][j][l];
 #pragma unroll
   for (int v = 1; v < kFcWaves; ++v) s += red[v][j][l];
-  const int n = j * 16 + (l & 15);
+  const int n = (blockIdx.y * NB + j) * 16 + (l & 15);
   const int kb = k0 + (l >> 4) * 4;
   if (n >= N) return;
   T o[4];
@@ -104,16 +104,13 @@ static void fc_mfma_t(const void* x, int n, int cin, int cin_s, const void* w, i
   const int kp = (kout + 7) / 8 * 8;
   check((long long)kp * c8 * 2 < (long long)kOOB, "FC weights too large for 32-bit offsets");
   check(kout_s <= kp && c8 >= cin, "FC shapes");
-  const dim3 grid((kout_s + 15) / 16), block(64 * kFcWaves);
+  // one 16-row batch block per workgroup (grid.y): more workgroups to read
+  // W, whose rows the batch blocks then share through L2
+  const dim3 grid((kout_s + 15) / 16, (n + 15) / 16), block(64 * kFcWaves);
   const T* xp = static_cast<const T*>(x);
   const T* wp = static_cast<const T*>(w);
   T* yp = static_cast<T*>(y);
-  if (n <= 16)
-    SN_LAUNCH((fc_mfma_kernel<T, 1, 4>), grid, block, 0, st, xp, n, cin, cin_s, wp, c8, kp, bias, yp, kout_s, act);
-  else if (n <= 32)
-    SN_LAUNCH((fc_mfma_kernel<T, 2, 4>), grid, block, 0, st, xp, n, cin, cin_s, wp, c8, kp, bias, yp, kout_s, act);
-  else
-    SN_LAUNCH((fc_mfma_kernel<T, 4, 2>), grid, block, 0, st, xp, n, cin, cin_s, wp, c8, kp, bias, yp, kout_s, act);
+  SN_LAUNCH((fc_mfma_kernel<T, 1, 4>), grid, block, 0, st, xp, n, cin, cin_s, wp, c8, kp, bias, yp, kout_s, act);
 }
 
 void fc_mfma(int dtype, const void* x, int n, int cin, int cin_s, const void* w, int c8, const float* bias,
