@@ -442,11 +442,13 @@ def main():
         torch.cuda.synchronize()
 
     fixed = {}
+    fixed_model = {}   # the additive model's T(S) of each fixed path, from the same cost table
     best_fixed = None
     if not args.no_fixed:
         for lay in LAYOUTS:
             for algo in ALGOS:
                 g.select("fixed", lay, algo)
+                fixed_model[f"{lay}/{algo}"] = round(g.path()[1] / 1e6, 4)
                 s = time_steps(g, x, out, args.steps, args.warmup)
                 fixed[f"{lay}/{algo}"] = round(args.batch / s, 2)
                 log(f"[bench] fixed {lay}/{algo}: {args.batch / s:.1f} img/s")
@@ -496,7 +498,7 @@ def main():
         "conv3x3_mfma_util": round(conv3_util, 4) if conv3_util else None,
         "dprs_img_s": round(args.batch / sec_dp, 2),
         "dp_vs_best_fixed": dp_vs_fixed, "selected_vs_best_fixed": sel_vs_fixed,
-        "best_fixed": best_fixed, "fixed_img_s": fixed, "integrated": integ,
+        "best_fixed": best_fixed, "fixed_img_s": fixed, "fixed_model_time_ms": fixed_model, "integrated": integ,
         "model_time_ms": round(model_ns / 1e6, 4), "dprs_model_time_ms": round(dp_model_ns / 1e6, 4),
         "tuning_s": round(t_prof + t_sel + t_int, 2),
     }
