@@ -122,8 +122,11 @@ typedef enum {
   SN_OPT_PARAMS = 2,    /* 0: one routine parameter per algorithm; 1: all (default 1) */
   SN_OPT_HIPGRAPH = 3,  /* 1: sn_run replays a captured HIP graph (default 0)        */
   SN_OPT_SEED = 4,      /* seed of the profiler's scratch-tensor fill (default 1)    */
-  SN_OPT_FLUSH = 5      /* bytes sn_run_timed writes to a scratch buffer before each
+  SN_OPT_FLUSH = 5,     /* bytes sn_run_timed writes to a scratch buffer before each
                            layer, evicting the caches (0 = off, the default)        */
+  SN_OPT_KEEP = 6       /* 1: the plan gives every intermediate tensor its own bytes
+                           (no reuse by liveness), so sn_layer_output can read any
+                           layer's stored output after a run (default 0)            */
 } sn_option;
 
 /* Creates a graph whose auxiliary input layer (id 0) carries the user tensor
@@ -203,6 +206,22 @@ int sn_run(sn_graph* g, const void* d_in, void* d_out, void* hip_stream);
  * is outside 1..10000. */
 int sn_run_timed(sn_graph* g, const void* d_in, void* d_out, void* hip_stream, int32_t reps,
                  float* layer_ms, int32_t n);
+
+/* Copies the stored output of layer (1 .. n-1) as its selected routine wrote
+ * it -- in the routine's layout (the schema of Sec. III-C), NC8HW8 with its
+ * channels padded to a multiple of 8 -- from the plan's memory into the
+ * caller's device buffer d_dst (cap bytes), as an asynchronous
+ * device-to-device copy on the stream, with no arithmetic.  Read after an
+ * sn_run on the same stream.  *bytes receives the stored size and *layout the
+ * layout value (either may be NULL); d_dst = NULL only queries them.
+ * Intermediate layers keep their output after the run only with SN_OPT_KEEP =
+ * 1; the last layer's output stays until the next run.
+ * Errors: SN_E_STATE (no plan, or an intermediate layer without
+ * SN_OPT_KEEP), SN_E_INVALID (layer out of range), SN_E_NOMEM (cap smaller
+ * than the stored size), SN_E_UNSUPPORTED (the layer stores straight into the
+ * caller's output tensor of sn_run), SN_E_DEVICE. */
+int sn_layer_output(const sn_graph* g, int32_t layer, void* d_dst, size_t cap, size_t* bytes,
+                    int32_t* layout, void* hip_stream);
 
 /* Integrated profiling (Sec. III-C): the unit-profiled table filters the
  * routine patterns down to a short list of whole paths, and those are timed

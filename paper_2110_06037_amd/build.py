@@ -29,14 +29,28 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
 
 
 def sources():
-    return sorted(glob.glob(os.path.join(CSRC, "*.cpp")) +
+    return sorted(glob.glob(os.path.join(CSRC, "*.cpp")) + glob.glob(os.path.join(CSRC, "*.hip")) +
                   glob.glob(os.path.join(CSRC, "kernels", "*.hip")))
 
 
-def _compile(src):
+def _up_to_date(src, obj):
+    """Whether obj is newer than src and every header its dependency file lists."""
+    dep = obj + ".d"
+    if not (os.path.exists(obj) and os.path.exists(dep)):
+        return False
+    t = os.path.getmtime(obj)
+    with open(dep) as f:
+        text = f.read().replace("\\\n", " ")
+    files = text.split(":", 1)[1].split() if ":" in text else [src]
+    return all(os.path.exists(p) and os.path.getmtime(p) <= t for p in files)
+
+
+def _compile(src, incremental=False):
     rel = os.path.relpath(src, CSRC).replace(os.sep, "_")
     obj = os.path.join(OBJ, rel + ".o")
-    cmd = [HIPCC] + FLAGS + ["-c", src, "-o", obj]
+    if incremental and _up_to_date(src, obj):
+        return src, obj, 0, ""
+    cmd = [HIPCC] + FLAGS + ["-MMD", "-MF", obj + ".d", "-c", src, "-o", obj]
     if src.endswith(".hip"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -45,14 +59,16 @@ def _compile(src):
     return src, obj, r.returncode, err
 
 
-def build(verbose=False, jobs=None):
+def build(verbose=False, jobs=None, incremental=False):
+    """Compiles every source (incremental=True skips objects newer than their
+    source and headers) and links the library."""
     os.makedirs(OBJ, exist_ok=True)
     srcs = sources()
     jobs = jobs or min(len(srcs), max(1, (os.cpu_count() or 4)), 16)
     objs = []
     failed = []
     with cf.ThreadPoolExecutor(jobs) as ex:
-        for src, obj, rc, err in ex.map(_compile, srcs):
+        for src, obj, rc, err in ex.map(lambda s: _compile(s, incremental), srcs):
             objs.append(obj)
             if rc != 0:
                 failed.append((src, err))
@@ -71,4 +87,4 @@ def build(verbose=False, jobs=None):
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, incremental="--incremental" in sys.argv))

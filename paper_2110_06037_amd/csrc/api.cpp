@@ -102,6 +102,14 @@ int sn_set_option(sn_graph* gp, int32_t option, int64_t value) {
       case SN_OPT_SEED:
         g.opt_seed = value;
         break;
+      case SN_OPT_KEEP:
+        if (value != 0 && value != 1) fail(SN_E_INVALID, "KEEP is 0 or 1");
+        if (g.opt_keep != value && g.plan) {
+          g.opt_keep = value;
+          plan_compile(g);  // re-place the buffers
+        }
+        g.opt_keep = value;
+        break;
       case SN_OPT_FLUSH:
         if (value < 0 || value > (int64_t(1) << 34)) fail(SN_E_INVALID, "FLUSH is 0..16 GiB");
         g.opt_flush = value;
@@ -199,6 +207,18 @@ int sn_run_timed(sn_graph* gp, const void* d_in, void* d_out, void* stream, int3
     if (n != g.n_layers()) fail(SN_E_INVALID, "layer_ms must have one entry per layer");
     if (reps < 1 || reps > 10000) fail(SN_E_INVALID, "reps must be in 1..10000");
     plan_run(g, d_in, d_out, stream, layer_ms, reps);
+  });
+}
+
+int sn_layer_output(const sn_graph* gp, int32_t layer, void* d_dst, size_t cap, size_t* bytes,
+                    int32_t* layout, void* stream) {
+  return guarded([&] {
+    CHECK_G(gp);
+    const Graph& g = gp->g;
+    if (g.host_only()) fail(SN_E_DEVICE, "host-only graph has no device tensors");
+    int lay = 0;
+    plan_layer_output(g, layer, d_dst, cap, bytes, &lay, stream);
+    if (layout) *layout = lay;
   });
 }
 

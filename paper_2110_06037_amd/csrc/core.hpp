@@ -110,6 +110,7 @@ struct Graph {
   Shape in;
   int64_t opt_layouts = 7, opt_algos = 7, opt_params = 1, opt_hipgraph = 0, opt_seed = 1;
   int64_t opt_flush = 0;  // bytes written before each layer of a timed run (0 = none)
+  int64_t opt_keep = 0;   // 1: the plan gives every buffer its own bytes
   std::vector<Layer> layers;  // layers[0] = auxiliary input
   std::vector<Edge> edges;    // every (input -> layer) edge, in insertion order
   Edge out_edge{};            // (last layer -> auxiliary output); from/to set on use
@@ -159,6 +160,8 @@ void plan_compile(Graph& g);
 void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms = nullptr,
               int reps = 1);
 void plan_destroy(Graph& g);
+void plan_layer_output(const Graph& g, int layer, void* d_dst, size_t cap, size_t* bytes, int* layout,
+                       void* stream);
 // times every candidate end to end and selects the fastest (compiles its plan)
 void integrated_measure(Graph& g, std::vector<Candidate>& cands, int warmup, int reps,
                         void* stream);

@@ -58,6 +58,7 @@ struct Plan {
   void* arena = nullptr;
   size_t arena_bytes = 0;
   std::vector<int> first_step, last_step;  // per layer (steps of a layer are contiguous)
+  std::vector<BufRef> layer_out;           // per layer: where its routine stores its output
   std::vector<hipEvent_t> ev;              // timed runs: 2 per layer
   hipStream_t gstream = nullptr;           // stream the captured graph replays on
   hipGraphExec_t gexec = nullptr;
@@ -422,8 +423,11 @@ void plan_compile(Graph& g) {
     size_t off;
   };
   std::vector<Buf> bufs;
+  // with opt_keep every buffer lives to the end of the plan (nothing shares
+  // bytes), so every layer's stored output can be read after a run
+  const int never = g.opt_keep ? INT32_MAX : -1;
   auto new_buf = [&](size_t bytes, int def) {
-    bufs.push_back(Buf{align256(bytes), def, def, 0});
+    bufs.push_back(Buf{align256(bytes), def, std::max(def, never), 0});
     return (int)bufs.size() - 1;
   };
   // output tensor of each layer: kind/buffer index
@@ -473,6 +477,10 @@ void plan_compile(Graph& g) {
         push(c, cu);
         s.in[q] = c.dst;
         uses.push_back(b);
+        // a timed run repeats the converter after the layer's routine: its
+        // source must outlive the routine, so the routine's output never
+        // takes the source's bytes
+        if (out_buf[j] >= 0) uses.push_back(out_buf[j]);
       }
     }
     s.outd = tdesc(L.out, r.layout);
@@ -544,6 +552,8 @@ void plan_compile(Graph& g) {
       if (s.ws_bytes) resolve(s.ws);
     }
   }
+  P->layer_out = out_ref;
+  for (BufRef& r : P->layer_out) resolve(r);
   P->arena_bytes = std::max<size_t>(total, 256);
   HIPCHK(hipMalloc(&P->arena, P->arena_bytes));
   P->ev.resize(2 * n, nullptr);
@@ -551,9 +561,8 @@ void plan_compile(Graph& g) {
   g.plan = std::move(P);
 }
 
-static void enqueue_step(const Graph& g, const Plan& P, const Step& s, const void* d_in,
+static void enqueue_step(const Graph& g, const Plan& P, char* base, const Step& s, const void* d_in,
                          void* d_out, hipStream_t st) {
-  char* base = static_cast<char*>(P.arena);
   auto ptr = [&](const BufRef& r) -> void* {
     if (r.kind == 1) return const_cast<void*>(d_in);
     if (r.kind == 2) return d_out;
@@ -569,9 +578,9 @@ static void enqueue_step(const Graph& g, const Plan& P, const Step& s, const voi
   }
 }
 
-static void enqueue_steps(const Graph& g, const Plan& P, const void* d_in, void* d_out,
+static void enqueue_steps(const Graph& g, const Plan& P, char* base, const void* d_in, void* d_out,
                           hipStream_t st) {
-  for (const Step& s : P.steps) enqueue_step(g, P, s, d_in, d_out, st);
+  for (const Step& s : P.steps) enqueue_step(g, P, base, s, d_in, d_out, st);
   HIPCHK(hipGetLastError());
 }
 
@@ -595,7 +604,7 @@ static void enqueue_timed(const Graph& g, const Plan& P, const void* d_in, void*
       for (int si = a; si <= b; ++si) {
         k::g_timing = k::LaunchTiming{rep == 0 && si == a ? P.ev[2 * i] : nullptr,
                                       rep == reps - 1 && si == b ? P.ev[2 * i + 1] : nullptr};
-        enqueue_step(g, P, P.steps[si], d_in, d_out, st);
+        enqueue_step(g, P, static_cast<char*>(P.arena), P.steps[si], d_in, d_out, st);
       }
   }
   k::g_timing = k::LaunchTiming{};
@@ -626,7 +635,7 @@ void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* laye
     return;
   }
   if (!g.opt_hipgraph) {
-    enqueue_steps(g, P, d_in, d_out, st);
+    enqueue_steps(g, P, static_cast<char*>(P.arena), d_in, d_out, st);
     return;
   }
   // replay a captured graph on the plan's stream, ordered after/before the caller's stream
@@ -642,7 +651,7 @@ void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* laye
     P.graph = nullptr;
     HIPCHK(hipStreamBeginCapture(P.gstream, hipStreamCaptureModeThreadLocal));
     try {
-      enqueue_steps(g, P, d_in, d_out, P.gstream);
+      enqueue_steps(g, P, static_cast<char*>(P.arena), d_in, d_out, P.gstream);
     } catch (...) {
       hipGraph_t tmp = nullptr;
       (void)hipStreamEndCapture(P.gstream, &tmp);
@@ -659,6 +668,30 @@ void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* laye
   HIPCHK(hipGraphLaunch(P.gexec, P.gstream));
   HIPCHK(hipEventRecord(P.gev[1], P.gstream));
   HIPCHK(hipStreamWaitEvent(st, P.gev[1], 0));
+}
+
+// Copy of a layer's stored output (its routine's layout, channels padded as
+// stored) out of the plan's arena; with opt_keep every layer's output
+// survives the run.
+void plan_layer_output(const Graph& g, int layer, void* d_dst, size_t cap, size_t* bytes,
+                       int* layout, void* stream) {
+  if (!g.plan) fail(SN_E_STATE, "no execution plan");
+  if (layer < 1 || layer >= g.n_layers()) fail(SN_E_INVALID, "unknown layer (the input layer has no stored output)");
+  const Plan& P = *g.plan;
+  const Layer& L = g.layers[layer];
+  const int lay = L.routines[g.path[layer]].layout;
+  const size_t b = (size_t)stored_numel(L.out, lay) * dtype_size(g.dtype);
+  if (bytes) *bytes = b;
+  if (layout) *layout = lay;
+  if (!d_dst) return;
+  if (cap < b) fail(SN_E_NOMEM, "destination smaller than the stored output");
+  const BufRef& r = P.layer_out[layer];
+  if (r.kind != 0) fail(SN_E_UNSUPPORTED, "the layer stores straight into the caller's output tensor");
+  if (!g.opt_keep && layer != g.n_layers() - 1)
+    fail(SN_E_STATE, "intermediate outputs are kept only with SN_OPT_KEEP = 1");
+  HIPCHK(hipSetDevice(g.device));
+  HIPCHK(hipMemcpyAsync(d_dst, static_cast<char*>(P.arena) + r.off, b, hipMemcpyDeviceToDevice,
+                        static_cast<hipStream_t>(stream)));
 }
 
 // ------------------------------------------------------------------ integrated profiling

@@ -943,10 +943,12 @@ static const IgCfg kIg16[] = {
     // small-channel (stem) kernel: NHWC, C <= 4, stride 1 or 2; 7 x 7 and 3 x 3 filters
     {112, 64, 32, 0, 0, 3, 2, 1, 1664, {}, 4, 28}, {224, 64, 32, 0, 0, 3, 2, 1, 2112, {}, 4, 28},
     {112, 64, 32, 0, 0, 3, 2, 1, 704, {}, 4, 8},   {224, 64, 32, 0, 0, 3, 2, 1, 1152, {}, 4, 8},
-    // streaming 1x1 kernel: NHWC, C = bk (BM pixels x BN channels per tile, WM wave rows)
-    {64, 256, 64, 0, 0, 4, 2}, {128, 128, 64, 0, 0, 4, 4}, {128, 64, 64, 0, 0, 4, 4},
-    {64, 128, 128, 0, 0, 4, 2}, {32, 256, 128, 0, 0, 4, 1}, {64, 64, 256, 0, 0, 4, 4},
-    {32, 128, 256, 0, 0, 4, 2}};
+    // streaming 1x1 kernel: NHWC, C = bk (BM pixels x BN channels per tile, WM wave rows,
+    // loads pf tiles ahead)
+#define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM},
+    STREAM_CONFIGS(SN_STREAM_IG)
+#undef SN_STREAM_IG
+};
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 
 int igemm_num_params(int dtype) {
@@ -1209,7 +1211,7 @@ static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t 
     return;
   }
   if (cfg.dma == 4) {
-    conv1x1_stream(dtype, cfg.bk, cfg.bm, cfg.bn, c, st);
+    conv1x1_stream(dtype, cfg.bk, cfg.bm, cfg.bn, cfg.pf, c, st);
     return;
   }
   IgArgs a = make_ig(c);

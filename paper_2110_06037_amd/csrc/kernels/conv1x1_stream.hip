@@ -7,9 +7,11 @@
 // bounds it, and its reduction takes one to four 64-wide steps: a workgroup
 // of the tiled implicit GEMM loads its tiles, waits, computes and stores with
 // little to overlap.  Here workgroups are persistent: each keeps its BN
-// filter rows in LDS and streams tiles of BM pixels, loading the next tile's
-// pixels (LDS direct loads) and its residual (into registers) while the
-// current tile's MFMAs and stores run; each wave holds its filter
+// filter rows in LDS and streams tiles of BM pixels, loading the pixels (LDS
+// direct loads) and the residual (into registers) of the tile PD tiles ahead
+// while the current tile's MFMAs and stores run, so PD tiles' loads are in
+// flight per workgroup (the residual comes from HBM and a tile's own work is
+// far shorter than a load's latency); each wave holds its filter
 // fragments in registers, so LDS serves only pixel fragments.  The tile's fp32 sums go
 // through LDS so that the residual add and the stores move whole 16-byte
 // chunks of consecutive channels with consecutive lanes on consecutive
@@ -36,9 +38,14 @@ struct StreamArgs {
   long long x_elems, w_elems, y_elems;
 };
 
-template <typename T, int CC, int BM, int BN, int WM, bool RES>
+template <int V>
+using SIC = std::integral_constant<int, V>;
+
+template <typename T, int CC, int BM, int BN, int WM, bool RES, int PD>
 __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   static_assert(sizeof(T) == 2 && CC % 64 == 0, "16-bit types, 64-channel slabs");
+  static_assert(PD >= 1 && PD <= 3, "one to three tiles ahead");
+  constexpr int NB = PD + 1;                   // pixel buffers and residual register sets
   constexpr int NWV = 8, NT = 512, WN = NWV / WM;
   constexpr int RB = 128;                      // LDS row of a slab: 64 channels
   constexpr int NSL = CC / 64;                 // slabs
@@ -49,14 +56,16 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   static_assert(NA >= 1 && NBL >= 1 && NE >= 1 && NA * 1024 * NWV == NSL * BM * RB &&
                     NBL * 1024 * NWV == NSL * BN * RB && NE * 8 * NT == BM * BN && FM >= 1 && FN >= 1,
                 "tile shape");
+  constexpr int YR = RES ? NE : 0;             // residual loads per thread and tile
+  static_assert(PD * (NA + YR + NE) <= 63, "outstanding-load counter range");
   constexpr int A_BYTES = NSL * BM * RB, B_BYTES = NSL * BN * RB;
   constexpr int CP = BN + 4;                   // fp32 staging row pitch (floats)
-  constexpr int SM = B_BYTES + 2 * A_BYTES + BM * CP * 4 + BN * 4;
+  constexpr int SM = B_BYTES + NB * A_BYTES + BM * CP * 4 + BN * 4;
   static_assert(SM <= 160 * 1024, "LDS capacity");
   __shared__ __attribute__((aligned(1024))) char smem[SM];
   char* const Bs = smem;
   char* const As = smem + B_BYTES;
-  float* const Cs = reinterpret_cast<float*>(As + 2 * A_BYTES);
+  float* const Cs = reinterpret_cast<float*>(As + NB * A_BYTES);
   float* const Bias = Cs + BM * CP;
   auto swz = [](int row) { return (row >> 1) & 7; };
 
@@ -64,6 +73,7 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
   const int n0 = blockIdx.y * BN;
+  const int G = gridDim.x;
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_elems * 2);
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, a.w_elems * 2);
   const __amdgpu_buffer_rsrc_t ry = make_rsrc(a.y, a.y_elems * 2);
@@ -92,9 +102,11 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
     arow[i] = row;
     achk[i] = (unsigned)(sl * 64 + ((pch ^ swz(row)) << 3)) * 2u;
   }
-  // output pixel m reads input pixel m (stride 1) or (img, 2p, 2q) (stride 2)
-  auto issue_a = [&](int mt, int buf) {
-    const int m0 = mt * BM;
+  // output pixel m reads input pixel m (stride 1) or (img, 2p, 2q) (stride
+  // 2); a tile past the end loads nothing (out-of-range offsets) but still
+  // counts its load instructions, so every wait below has a fixed count
+  auto issue_a = [&](int mtile, int buf) {
+    const int m0 = mtile * BM;
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       const int m = m0 + arow[i];
@@ -105,8 +117,27 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
         pix = (img * a.H + p * a.stride) * a.W + q * a.stride;
       }
       dma16(rx, As + buf * A_BYTES + (wave + NWV * i) * 1024,
-            m < a.M ? (unsigned)pix * (unsigned)(CC * 2) + achk[i] : kOOB, 0);
+            mtile < a.tiles_m && m < a.M ? (unsigned)pix * (unsigned)(CC * 2) + achk[i] : kOOB, 0);
     }
+  };
+  u32x4 res[NB][NE];  // residual register sets, one per tile in flight
+  auto load_res = [&](int mtile, u32x4 (&r)[NE]) {
+    const int m0r = mtile * BM;
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      const int q = tid + e * NT, row = q / (BN / 8), cj = q % (BN / 8);
+      const int m = m0r + row, n = n0 + cj * 8;
+      const unsigned off = mtile < a.tiles_m && m < a.M && n < a.K ? (unsigned)(m * a.Ks + n) * 2u : kOOB;
+      r[e] = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
+    }
+  };
+  // the loads of one tile: residual first, then pixels
+  auto issue_tile = [&](int mtile, auto BC) {
+    constexpr int B = decltype(BC)::value;
+    if constexpr (RES) load_res(mtile, res[B]);
+    __builtin_amdgcn_sched_barrier(0);
+    issue_a(mtile, B);
+    __builtin_amdgcn_sched_barrier(0);
   };
 
   // operand chunk offsets of the 32-wide reduction steps ks (slab ks / 2;
@@ -122,12 +153,17 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   typedef typename Mfma<T>::frag frag;
   const ActClamp ac = act_clamp(a.act);
 
-  int mt = blockIdx.x;
-  issue_a(mt, 0);
+  const int mt0 = blockIdx.x;
+  // prologue: the first PD tiles' loads (tile j into buffer and set j)
+  issue_tile(mt0, SIC<0>{});
+  if constexpr (PD > 1) issue_tile(mt0 + G, SIC<1>{});
+  if constexpr (PD > 2) issue_tile(mt0 + 2 * G, SIC<2>{});
+  // the filter and the first tile have landed once only the later tiles'
+  // loads remain outstanding
+  wait_vmcnt<(PD - 1) * (YR + NA)>();
+  __syncthreads();  // every wave's filter share, first pixel tile and the bias are in LDS
   // the wave's filter fragments stay in registers for the whole kernel, so
   // the tile loop reads only pixel fragments from LDS
-  wait_vmcnt<0>();  // this wave's filter and first-tile loads
-  __syncthreads();  // every wave's filter share, first pixel tile and the bias are in LDS
   frag fbr[KS][FN];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
@@ -139,44 +175,18 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) bias[j][v] = Bias[wn * WTN + j * 16 + (lane >> 4) * 4 + v];
 
-  // the residual of a tile is loaded one tile ahead, like its pixels
-  auto load_res = [&](int mtile, u32x4 (&r)[NE]) {
-    const int m0r = mtile * BM;
-#pragma unroll
-    for (int e = 0; e < NE; ++e) {
-      const int q = tid + e * NT, row = q / (BN / 8), cj = q % (BN / 8);
-      const int m = m0r + row, n = n0 + cj * 8;
-      const unsigned off = m < a.M && n < a.K ? (unsigned)(m * a.Ks + n) * 2u : kOOB;
-      r[e] = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
-    }
-  };
-  // two residual register sets alternate between tiles (a copy from the
-  // set still being loaded would wait for every outstanding load)
-  u32x4 ra[NE], rb[NE];
-  if constexpr (RES) load_res(mt, ra);
-
-  // one tile: its pixels are in LDS buffer t % 2 (the first tile's landed
-  // before the barrier above) and its residual in cur; the next tile's
-  // residual goes to nxt and its pixels to the other buffer; returns whether
-  // another tile follows
-  auto tile = [&](int t, u32x4 (&cur)[NE], u32x4 (&nxt)[NE]) {
-    const int buf = t & 1;
-    const int m0 = mt * BM;
-    const bool next = mt + (int)gridDim.x < a.tiles_m;
-    if constexpr (RES) {
-      if (next) load_res(mt + gridDim.x, nxt);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    if (next) issue_a(mt + gridDim.x, buf ^ 1);
-    __builtin_amdgcn_sched_barrier(0);
-    // wait for this tile's pixels: younger are the previous tile's stores
-    // (NE), the next tile's residual and the next tile's pixel loads; this
-    // tile's residual is older, so it has arrived too
-    constexpr int YR = RES ? NE : 0;
-    if (t > 0) {
-      if (next) wait_vmcnt<NE + YR + NA>();
-      else wait_vmcnt<NE>();
-    }
+  // tile t (index mt0 + t * G) uses buffer and residual set U = t % NB; it
+  // first issues the loads of tile t + PD into set (U + PD) % NB (the set
+  // tile t - 1 used), then waits for its own: younger than them are the
+  // loads of the PD later tiles and the stores of the last min(t, PD)
+  // tiles.  Returns whether tile t + 1 exists.
+  auto tile = [&](auto UC, int t) {
+    constexpr int U = decltype(UC)::value;
+    constexpr int NX = (U + PD) % NB;
+    const int mt = mt0 + t * G;
+    issue_tile(mt + PD * G, SIC<NX>{});
+    if (t < PD) wait_vmcnt<PD * (YR + NA) + (U < PD ? U : PD) * NE>();
+    else wait_vmcnt<PD * (YR + NA + NE)>();
     dma_barrier();  // every wave's share landed; every wave is done with the last tile's Cs
 
     f32x4 acc[FM][FN];
@@ -184,7 +194,7 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{bias[j][0], bias[j][1], bias[j][2], bias[j][3]};
-    const char* A = As + buf * A_BYTES;
+    const char* A = As + U * A_BYTES;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       frag fa[FM];
@@ -204,6 +214,7 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
         *reinterpret_cast<f32x4*>(Cs + (wm * WTM + i * 16 + (lane & 15)) * CP + wn * WTN + j * 16 + (lane >> 4) * 4) =
             acc[i][j];
     lds_barrier();
+    const int m0 = mt * BM;
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
       const int q = tid + e * NT, row = q / (BN / 8), cj = q % (BN / 8);
@@ -214,7 +225,7 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
       float s[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
       if constexpr (RES) {
         T rt[8];
-        __builtin_memcpy(rt, &cur[e], 16);
+        __builtin_memcpy(rt, &res[U][e], 16);
 #pragma unroll
         for (int v = 0; v < 8; ++v) s[v] += to_f(rt[v]);
       }
@@ -225,16 +236,23 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
       __builtin_memcpy(&pk, o, 16);
       __builtin_amdgcn_raw_buffer_store_b128(pk, ry, (int)off, 0, 0);
     }
-    return next;
+    return mt + G < a.tiles_m;
   };
-  // tiles mt, mt + G, ... (G = grid size); the loop is unrolled by two so
-  // that the residual sets swap roles without copies
-  for (int t = 0;; t += 2) {
-    if (!tile(t, ra, rb)) break;
-    mt += gridDim.x;
-    if (!tile(t + 1, rb, ra)) break;
-    mt += gridDim.x;
+  // the loop is unrolled by NB so that buffers and residual sets are
+  // compile-time indices
+  for (int t = 0;; t += NB) {
+    if (!tile(SIC<0>{}, t)) break;
+    if (!tile(SIC<1>{}, t + 1)) break;
+    if constexpr (NB > 2) {
+      if (!tile(SIC<2>{}, t + 2)) break;
+    }
+    if constexpr (NB > 3) {
+      if (!tile(SIC<3>{}, t + 3)) break;
+    }
   }
+  // the loads issued for tiles past the end target LDS: let them land
+  // before the workgroup ends
+  wait_vmcnt<0>();
 }
 
 bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
@@ -245,18 +263,18 @@ bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r,
          (long long)n * p * q * ((k + 7) / 8 * 8) * 2 < (long long)kOOB;
 }
 
-template <typename T, int CC, int BM, int BN, int WM>
+template <typename T, int CC, int BM, int BN, int WM, int PD>
 static void stream_go(const StreamArgs& a, int tiles_n, hipStream_t st) {
   // persistent: about one workgroup per CU over all channel tiles
   const int gx = std::max(1, std::min(a.tiles_m, 256 / tiles_n));
   const dim3 grid(gx, tiles_n);
   if (a.res)
-    SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, true>), grid, dim3(512), 0, st, a);
+    SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, true, PD>), grid, dim3(512), 0, st, a);
   else
-    SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, false>), grid, dim3(512), 0, st, a);
+    SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, false, PD>), grid, dim3(512), 0, st, a);
 }
 
-void conv1x1_stream(int dtype, int cc, int bm, int bn, const ConvArgs& c, hipStream_t st) {
+void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& c, hipStream_t st) {
   check(dtype != 0, "streaming 1x1 kernel runs 16-bit types");
   const long long m = (long long)c.yd.n * c.yd.h * c.yd.w;
   check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.stride >= 1 &&
@@ -286,19 +304,13 @@ void conv1x1_stream(int dtype, int cc, int bm, int bn, const ConvArgs& c, hipStr
   a.w_elems = (long long)((a.K + 7) / 8 * 8) * cc;
   a.y_elems = m * a.Ks;
   const int tiles_n = (a.K + bn - 1) / bn;
-#define SG(CC_, BM_, BN_, WM_)                                                \
-  if (cc == CC_ && bm == BM_ && bn == BN_) {                                  \
-    if (dtype == 1) stream_go<f16, CC_, BM_, BN_, WM_>(a, tiles_n, st);       \
-    else stream_go<bf16, CC_, BM_, BN_, WM_>(a, tiles_n, st);                 \
-    return;                                                                   \
+#define SG(CC_, BM_, BN_, WM_, PD_)                                              \
+  if (cc == CC_ && bm == BM_ && bn == BN_ && pd == PD_) {                        \
+    if (dtype == 1) stream_go<f16, CC_, BM_, BN_, WM_, PD_>(a, tiles_n, st);     \
+    else stream_go<bf16, CC_, BM_, BN_, WM_, PD_>(a, tiles_n, st);               \
+    return;                                                                      \
   }
-  SG(64, 64, 256, 2)
-  SG(64, 128, 128, 4)
-  SG(64, 128, 64, 4)
-  SG(128, 64, 128, 2)
-  SG(128, 32, 256, 1)
-  SG(256, 64, 64, 4)
-  SG(256, 32, 128, 2)
+  STREAM_CONFIGS(SG)
 #undef SG
   check(false, "streaming 1x1 tile not instantiated");
 }

@@ -90,10 +90,27 @@ bool smallc_applicable(int layout, int c, int h, int w, int r, int s, int stride
 void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st);
 // 1x1 convolution (stride 1 or 2, no padding) of an NHWC input with cc =
 // 64, 128 or 256 channels by persistent workgroups streaming pixel tiles
-// (see conv1x1_stream.hip)
+// (see conv1x1_stream.hip).  Instantiated tiles (CC, BM, BN, WM, PD): BM
+// pixels x BN channels per tile, WM wave rows, loads PD tiles ahead; each is
+// one implicit-GEMM routine parameter.
+#define STREAM_CONFIGS(X) \
+  X(64, 64, 256, 2, 1)    \
+  X(64, 128, 128, 4, 1)   \
+  X(64, 128, 64, 4, 1)    \
+  X(128, 64, 128, 2, 1)   \
+  X(128, 32, 256, 1, 1)   \
+  X(256, 64, 64, 4, 1)    \
+  X(256, 32, 128, 2, 1)   \
+  X(64, 64, 256, 2, 2)    \
+  X(64, 128, 128, 4, 2)   \
+  X(128, 64, 128, 2, 2)   \
+  X(128, 32, 256, 1, 3)   \
+  X(256, 64, 64, 4, 2)    \
+  X(256, 32, 128, 2, 2)   \
+  X(256, 32, 128, 2, 3)
 bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
                           int k, int cc);
-void conv1x1_stream(int dtype, int cc, int bm, int bn, const ConvArgs& a, hipStream_t st);
+void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& a, hipStream_t st);
 size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k);
 void conv_winograd(int dtype, const ConvArgs& a, hipStream_t st);
 void dwconv(int dtype, const ConvArgs& a, hipStream_t st);

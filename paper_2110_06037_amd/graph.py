@@ -230,6 +230,18 @@ class Graph:
                                 ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)))
         return out
 
+    def layer_output(self, layer, stream=None):
+        """The stored bytes of a layer's output after a run (its routine's
+        layout; NC8HW8 channels padded), as (uint8 device tensor, layout)."""
+        import torch
+        nb, lay = ctypes.c_size_t(), ctypes.c_int32()
+        N.check(self.lib.sn_layer_output(self._g, layer, None, 0, ctypes.byref(nb), ctypes.byref(lay),
+                                         _stream_ptr(stream)))
+        buf = torch.empty(max(nb.value, 1), dtype=torch.uint8, device=f"cuda:{self.device}")
+        N.check(self.lib.sn_layer_output(self._g, layer, ctypes.c_void_p(buf.data_ptr()), nb.value,
+                                         None, None, _stream_ptr(stream)))
+        return buf[:nb.value], lay.value
+
     def run_timed(self, x, out=None, stream=None, reps=1):
         """Synchronous run with every layer's launches repeated ``reps`` times
         back to back; returns (out, per-layer milliseconds per repetition)."""

@@ -25,7 +25,7 @@ ALGO_NAME = {v: k for k, v in ALGO.items()}
 L_INPUT, L_CONV2D, L_MAXPOOL, L_GAP, L_ADD, L_FC, L_OUTPUT = range(7)
 ACT = {"none": 0, "relu": 1, "relu6": 2}
 SELECT_DPRS, SELECT_FIXED = 0, 1
-OPT_LAYOUTS, OPT_ALGOS, OPT_PARAMS, OPT_HIPGRAPH, OPT_SEED, OPT_FLUSH = range(6)
+OPT_LAYOUTS, OPT_ALGOS, OPT_PARAMS, OPT_HIPGRAPH, OPT_SEED, OPT_FLUSH, OPT_KEEP = range(7)
 
 STATUS = {0: "SN_OK", -1: "SN_E_INVALID", -2: "SN_E_SHAPE", -3: "SN_E_STATE",
           -4: "SN_E_UNSUPPORTED", -5: "SN_E_DEVICE", -6: "SN_E_NOMEM", -7: "SN_E_INTERNAL"}
@@ -63,6 +63,8 @@ SIGNATURES = {
     "sn_set_path": (ctypes.c_int, [_P, _I32P, _I32]),
     "sn_run": (ctypes.c_int, [_P, _P, _P, _P]),
     "sn_run_timed": (ctypes.c_int, [_P, _P, _P, _P, _I32, ctypes.POINTER(ctypes.c_float), _I32]),
+    "sn_layer_output": (ctypes.c_int, [_P, _I32, _P, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t),
+                                       _I32P, _P]),
     "sn_profile_integrated": (ctypes.c_int, [_P, _I32, _I32, _P, _I32P]),
     "sn_integrated_candidate": (ctypes.c_int, [_P, _I32, _I32P, _I32, _I64P, _I64P, _I32P]),
     "sn_get_costs": (ctypes.c_int, [_P, ctypes.c_char_p, ctypes.c_size_t,

@@ -187,3 +187,145 @@ def test_hip_graph_replays_match_eager():
         junk = torch.randn(1 << 20, device="cuda").sum()   # eager work between replays
         torch.cuda.synchronize()
     g.close()
+
+
+def _images_out(g, spec, t, images):
+    import torch
+    xd = to_dev(t["x"], spec["dtype"])
+    y = g.run(xd)
+    torch.cuda.synchronize()
+    out = from_dev(y, spec["dtype"]).reshape(spec["batch"], -1)
+    d = decoded(t, spec["dtype"])
+    d["x"] = d["x"][images]
+    ref = O.forward(with_batch(spec, len(images)), d, storage="dtype")[-1]
+    return out, out[images], ref.reshape(len(images), -1)
+
+
+FULL_BATCH = {
+    # name: (spec factory, images through the oracle: first, middle, last)
+    "resnet50_bs32_bf16_fused": (lambda: fuse_residual(resnet50(32, "bf16")), [0, 13, 31]),
+    "resnet50_bs32_f16_fused": (lambda: fuse_residual(resnet50(32, "f16")), [0, 17, 31]),
+    "resnet50_bs32_f16": (lambda: resnet50(32, "f16"), [2, 31]),
+    "mobilenetv2_bs8_fused": (lambda: fuse_residual(mobilenet_v2(8)), [0, 3, 7]),
+    "mobilenetv2_bs8": (lambda: mobilenet_v2(8), [1, 6]),
+    "vgg16_bs32_224": (lambda: vgg16(32, "bf16"), [0, 31]),
+}
+
+
+@pytest.mark.parametrize("name", list(FULL_BATCH))
+def test_full_batch_paths_on_images_across_the_batch(name):
+    # the benchmark's configurations at their full batch: the DPRS path and
+    # the path integrated profiling keeps (the one bench.py times), checked
+    # on images at the start, middle and end of the batch, so that tiles far
+    # from the first of every persistent workgroup are compared too
+    make, images = FULL_BATCH[name]
+    spec = make()
+    t = generate(spec)
+    g = build_from_spec(spec, t)
+    g.profile(warmup=2, reps=5)
+    g.select("dprs")
+    out, got, ref = _images_out(g, spec, t, images)
+    e = err(got, ref, spec["dtype"])
+    print(f"{name} dprs images {images} err {e:.3e}", flush=True)
+    assert e <= TOL[spec["dtype"]]
+    assert np.all(np.isfinite(out))
+    dprs_ids = g.path()[0]
+    g.profile_integrated(warmup=2, reps=3)
+    if g.path()[0] != dprs_ids:
+        out, got, ref2 = _images_out(g, spec, t, images)
+        e = err(got, ref, spec["dtype"])
+        print(f"{name} selected path images {images} err {e:.3e}", flush=True)
+        assert e <= TOL[spec["dtype"]]
+        assert np.all(np.isfinite(out))
+    g.close()
+
+
+def _rotating_layout_path(g):
+    # a routine of layout (i mod 3) on layer i where one exists (implicit
+    # GEMM first): a converter on almost every edge
+    ids = [0]
+    for i in range(1, g.num_layers()):
+        rts = g.routines(i)
+        want = [r for r in rts if r["layout"] == i % 3] or rts
+        ids.append(min(want, key=lambda r: (r["algo"] != 1, r["id"]))["id"])
+    return ids
+
+
+def test_run_timed_equals_run_on_a_mixed_layout_path():
+    # sn_run_timed repeats every layer's converters and routine; a converter's
+    # source must outlive the layer's routine, so the repeated run gives the
+    # same bits as sn_run on a path that switches layout on every edge
+    import torch
+    spec = resnet18(1)
+    t = generate(spec)
+    g = build_from_spec(spec, t)
+    ids = _rotating_layout_path(g)
+    g.set_path(ids)
+    layouts = [g.routines(i)[ids[i]]["layout"] for i in range(len(ids))]
+    assert len(set(layouts[1:])) == 3
+    out, xd = run_out(g, spec, t)
+    assert err(out, oracle_out(spec, t), "bf16") <= TOL["bf16"]
+    for reps in (3, 1):
+        y, ms = g.run_timed(xd, reps=reps)
+        torch.cuda.synchronize()
+        assert np.array_equal(from_dev(y, "bf16").reshape(1, -1), out), reps
+        assert all(m > 0 for m in ms[1:])
+    g.close()
+
+
+def odd_channel_net():
+    """Channel counts that are not multiples of 8 on every layer: NC8HW8
+    stores them padded."""
+    L = [
+        {"type": "conv", "in": [0], "k": 12, "r": 3, "s": 3, "stride": 1, "pad": 1, "groups": 1, "act": "relu"},
+        {"type": "conv", "in": [1], "k": 12, "r": 3, "s": 3, "stride": 2, "pad": 1, "groups": 12, "act": "relu6"},
+        {"type": "conv", "in": [2], "k": 20, "r": 1, "s": 1, "stride": 1, "pad": 0, "groups": 1, "act": "none"},
+        {"type": "maxpool", "in": [3], "k": 3, "stride": 1, "pad": 1},
+        {"type": "conv", "in": [4], "k": 20, "r": 3, "s": 3, "stride": 1, "pad": 1, "groups": 1, "act": "none"},
+        {"type": "add", "in": [5, 3], "act": "relu"},
+        # a 1x1 convolution with a folded residual input (layer 4)
+        {"type": "conv", "in": [6, 4], "k": 20, "r": 1, "s": 1, "stride": 1, "pad": 0, "groups": 1, "act": "relu"},
+        {"type": "gap", "in": [7]},
+        {"type": "fc", "in": [8], "k": 10},
+    ]
+    return {"name": "odd_channels", "dtype": "bf16", "batch": 3, "in_chw": [3, 13, 11],
+            "input_dist": "uniform", "seed": 5, "layers": L,
+            "layouts": ["NCHW", "NHWC", "NC8HW8"], "algos": ["direct", "igemm", "winograd"]}
+
+
+@pytest.mark.parametrize("algo", ["igemm", "direct", "winograd"])
+def test_nc8hw8_stored_outputs_keep_padded_channels_zero(algo):
+    # every layer's output as its NC8HW8 routine stored it: the channels
+    # padded up to a multiple of 8 hold exact zeros, and the real channels
+    # hold the oracle's layer output
+    import torch
+    spec = odd_channel_net()
+    t = generate(spec)
+    g = build_from_spec(spec, t)
+    g.set_option(N.OPT_KEEP, 1)
+    g.select("fixed", "NC8HW8", algo)
+    xd = to_dev(t["x"], "bf16")
+    y = g.run(xd)
+    torch.cuda.synchronize()
+    refs = O.forward(spec, decoded(t, "bf16"), storage="dtype", keep=True)
+    for i in range(1, g.num_layers()):
+        n, c, h, w = g.layer_shape(i)
+        try:
+            buf, lay = g.layer_output(i)
+        except N.SNError as e:
+            assert i == g.num_layers() - 1 and e.code == -4, e   # stored into the user's output
+            continue
+        torch.cuda.synchronize()
+        assert lay == N.NC8HW8
+        c8 = (c + 7) // 8 * 8
+        bits = buf.cpu().numpy().view(np.uint16)
+        assert bits.size == n * c8 * h * w, (i, bits.size)
+        blk = bits.reshape(n, c8 // 8, h, w, 8).transpose(0, 1, 4, 2, 3).reshape(n, c8, h, w)
+        assert not np.any(blk[:, c:]), f"layer {i}: padded channels hold non-zero bits"
+        got = to_f64(blk[:, :c], "bf16")
+        e = err(got, refs[i].reshape(n, c, h, w), "bf16")
+        print(f"odd-channel net {algo} layer {i} err {e:.2e}", flush=True)
+        assert e <= TOL["bf16"], i
+    out = from_dev(y, "bf16").reshape(3, -1)
+    assert err(out, refs[-1].reshape(3, -1), "bf16") <= TOL["bf16"]
+    g.close()
