@@ -191,6 +191,22 @@ int sn_set_path(sn_graph* g, const int32_t* routine_ids, int32_t n);
  * Errors: SN_E_STATE (no plan), SN_E_DEVICE (host-only graph, HIP error). */
 int sn_run(sn_graph* g, const void* d_in, void* d_out, void* hip_stream);
 
+/* sn_run without allocation, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * it).  The same launches as sn_run on the same selected plan, with the
+ * plan's intermediate tensors and workspaces (split-reduction partial sums,
+ * Winograd transforms) placed in the library's static per-device region of
+ * 64 MiB instead of the plan's own memory; the call itself allocates nothing
+ * and enqueues nothing but kernels (no memset, no copy), so results are
+ * identical to sn_run's.  Every call on one GPU shares that GPU's region, and
+ * the region keeps the last call's contents (no routine relies on it being
+ * zero): calls that overlap in time on one GPU (different streams, different
+ * threads, or different graphs without ordering between them) race and give
+ * undefined results.  d_in / d_out as for sn_run.
+ * Errors: SN_E_STATE (no plan), SN_E_UNSUPPORTED (the plan needs more than
+ * the 64 MiB region, e.g. ResNet-50 at batch 32: use sn_run), SN_E_DEVICE. */
+int sn_run_noalloc(sn_graph* g, const void* d_in, void* d_out, void* hip_stream);
+
 /* Like sn_run, but enqueues every layer's launches (its routine plus the
  * converters feeding it) reps times back to back, then synchronises and
  * writes each layer's mean time per repetition to layer_ms[0..n-1] (layer 0

@@ -3,6 +3,8 @@
 #include <cstdio>
 #include <string>
 
+#include <hip/hip_runtime.h>
+
 #include "core.hpp"
 
 using namespace sn;
@@ -193,6 +195,25 @@ int sn_run(sn_graph* gp, const void* d_in, void* d_out, void* stream) {
     if (g.path.empty()) fail(SN_E_STATE, "no routine path selected");
     if (!d_in || !d_out) fail(SN_E_INVALID, "null device pointer");
     plan_run(g, d_in, d_out, stream, nullptr);
+  });
+}
+
+int sn_run_noalloc(sn_graph* gp, const void* d_in, void* d_out, void* stream) {
+  return guarded([&] {
+    CHECK_G(gp);
+    Graph& g = gp->g;
+    if (g.host_only()) fail(SN_E_DEVICE, "host-only graph cannot run");
+    if (g.path.empty() || !g.plan) fail(SN_E_STATE, "no routine path selected");
+    if (!d_in || !d_out) fail(SN_E_INVALID, "null device pointer");
+    if (plan_arena_bytes(g) > noalloc_scratch_bytes())
+      fail(SN_E_UNSUPPORTED, "the plan needs " + std::to_string(plan_arena_bytes(g)) +
+                                 " bytes of intermediate memory; the static region holds " +
+                                 std::to_string(noalloc_scratch_bytes()));
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) fail(SN_E_DEVICE, "hipGetDevice failed");
+    if (cur != g.device && hipSetDevice(g.device) != hipSuccess) fail(SN_E_DEVICE, "hipSetDevice failed");
+    void* base = noalloc_scratch_ptr(g.device);
+    plan_run_in(g, base, noalloc_scratch_bytes(), d_in, d_out, stream);
   });
 }
 

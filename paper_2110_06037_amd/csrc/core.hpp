@@ -160,6 +160,11 @@ void plan_compile(Graph& g);
 void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms = nullptr,
               int reps = 1);
 void plan_destroy(Graph& g);
+// noalloc_scratch.hip: the static per-device region of sn_run_noalloc
+size_t noalloc_scratch_bytes();
+void* noalloc_scratch_ptr(int device);  // the region's device address (device must be current)
+void plan_run_in(const Graph& g, void* base, size_t cap, const void* d_in, void* d_out, void* stream);
+size_t plan_arena_bytes(const Graph& g);
 void plan_layer_output(const Graph& g, int layer, void* d_dst, size_t cap, size_t* bytes, int* layout,
                        void* stream);
 // times every candidate end to end and selects the fastest (compiles its plan)

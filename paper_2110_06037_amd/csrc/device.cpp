@@ -670,6 +670,23 @@ void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* laye
   HIPCHK(hipStreamWaitEvent(st, P.gev[1], 0));
 }
 
+// sn_run with the plan's intermediate tensors and workspaces placed in a
+// caller-provided device region of cap bytes instead of the plan's own
+// memory (same offsets, same launches, hence the same results).  Enqueues
+// only kernel launches: no allocation, no memset.
+void plan_run_in(const Graph& g, void* base, size_t cap, const void* d_in, void* d_out, void* stream) {
+  if (!g.plan) fail(SN_E_STATE, "no execution plan");
+  const Plan& P = *g.plan;
+  if (P.arena_bytes > cap)
+    fail(SN_E_UNSUPPORTED, "the plan needs " + std::to_string(P.arena_bytes) +
+                               " bytes of intermediate memory, more than the " + std::to_string(cap) +
+                               " bytes of the static scratch region");
+  HIPCHK(hipSetDevice(g.device));
+  enqueue_steps(g, P, static_cast<char*>(base), d_in, d_out, static_cast<hipStream_t>(stream));
+}
+
+size_t plan_arena_bytes(const Graph& g) { return g.plan ? g.plan->arena_bytes : 0; }
+
 // Copy of a layer's stored output (its routine's layout, channels padded as
 // stored) out of the plan's arena; with opt_keep every layer's output
 // survives the run.

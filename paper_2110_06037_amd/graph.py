@@ -230,6 +230,15 @@ class Graph:
                                 ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)))
         return out
 
+    def run_noalloc(self, x, out, stream=None):
+        """sn_run with the intermediate tensors in the library's static
+        per-device region (no allocation); ``out`` must be given."""
+        assert x.is_contiguous() and out.is_contiguous()
+        assert x.dtype == self._torch_dtype() and tuple(x.shape) == tuple(self.in_shape)
+        N.check(self.lib.sn_run_noalloc(self._g, ctypes.c_void_p(x.data_ptr()),
+                                        ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)))
+        return out
+
     def layer_output(self, layer, stream=None):
         """The stored bytes of a layer's output after a run (its routine's
         layout; NC8HW8 channels padded), as (uint8 device tensor, layout)."""

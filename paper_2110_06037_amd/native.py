@@ -62,6 +62,7 @@ SIGNATURES = {
     "sn_select_path": (ctypes.c_int, [_P, _I32, _I32, _I32]),
     "sn_set_path": (ctypes.c_int, [_P, _I32P, _I32]),
     "sn_run": (ctypes.c_int, [_P, _P, _P, _P]),
+    "sn_run_noalloc": (ctypes.c_int, [_P, _P, _P, _P]),
     "sn_run_timed": (ctypes.c_int, [_P, _P, _P, _P, _I32, ctypes.POINTER(ctypes.c_float), _I32]),
     "sn_layer_output": (ctypes.c_int, [_P, _I32, _P, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t),
                                        _I32P, _P]),
