@@ -84,7 +84,8 @@ KERNEL_SOURCES = {
     "conv3x3_patch_kernel": ("conv_patch.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
     "conv1x1_stream_kernel": ("conv1x1_stream.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
 }
-ALL_KERNEL_SOURCES = ("conv.hip", "conv1x1_stream.hip", "conv_patch.hip", "conv_smallc.hip", "fc.hip", "misc.hip",
+ALL_KERNEL_SOURCES = ("conv.hip", "conv1x1_stream.hip", "conv_patch.hip", "conv_smallc.hip", "convert.hip", "fc.hip",
+                      "misc.hip",
                       "gemm_common.hpp",
                       "kcommon.hpp", "launch.hpp")
 

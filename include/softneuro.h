@@ -9,11 +9,15 @@
  * inference with the selected routines (Sec. III-A, step 3).
  *
  * Terms.  A *routine* is one implementation of a layer: an algorithm
- * (direct, implicit GEMM, Winograd F(2x2,3x3)), a tensor layout and a
- * routine parameter (a tile configuration).  The *schema* of a routine is its
- * layout (NCHW, NHWC or NC8HW8 = channel blocks of 8, channels zero-padded to
- * a multiple of 8).  Between two layers whose routines have different
- * schemas an *adapt* routine (a layout converter) runs.
+ * (direct, implicit GEMM, Winograd F(2x2,3x3)), a tensor layout, an element
+ * type and a routine parameter (a tile configuration).  The *schema* of a
+ * routine is its (element type, layout) pair: layouts NCHW, NHWC or NC8HW8
+ * (channel blocks of 8, channels zero-padded to a multiple of 8), element
+ * types float32, float16, bfloat16.  By default a graph computes in its run
+ * dtype only, so schemas differ by layout alone; SN_OPT_DTYPES admits the
+ * other element types (precision-hybrid tuning, Sec. IV-F).  Between two
+ * layers whose routines have different schemas an *adapt* routine (a layout
+ * converter, a cast, or both at once) runs.
  *
  * Conventions.
  *  - Every int-returning call returns SN_OK (0) or a negative sn_status.  No
@@ -28,8 +32,11 @@
  *  - Streams are hipStream_t passed as void*; NULL means the null stream.
  *  - Element types: SN_F32 = IEEE binary32, SN_F16 = binary16, SN_BF16 =
  *    bfloat16 (passed as 16-bit patterns).  Biases are always float32.
- *    Accumulation is float32 in every routine; outputs are rounded to the run
- *    dtype with round-to-nearest-even.
+ *    The user's input and output tensors and the weights passed in are in
+ *    the graph's run dtype.  Accumulation is float32 in every routine;
+ *    outputs are rounded to the routine's element type, and every cast
+ *    (weights at graph build, tensors in adapt routines) rounds once, to
+ *    nearest-even.
  */
 #ifndef SOFTNEURO_H
 #define SOFTNEURO_H
@@ -56,9 +63,12 @@ typedef enum {
 
 typedef enum { SN_F32 = 0, SN_F16 = 1, SN_BF16 = 2 } sn_dtype;
 
-/* Schemas (tensor layouts).  Values index cost matrices and bitmasks. */
+/* Tensor layouts.  Values index bitmasks. */
 typedef enum { SN_NCHW = 0, SN_NHWC = 1, SN_NC8HW8 = 2 } sn_layout;
 #define SN_NUM_LAYOUTS 3
+/* Schema index = dtype * SN_NUM_LAYOUTS + layout (0 .. 8); indexes the
+ * adapt-cost matrices of the cost table. */
+#define SN_NUM_SCHEMAS 9
 
 /* Algorithms.  Non-convolution layers have one algorithm (SN_ALGO_DIRECT) per
  * layout; FC layers also have SN_ALGO_IGEMM, the paper's dense childnet
@@ -99,12 +109,17 @@ typedef struct {
 
 typedef struct {
   int32_t id;        /* routine id, unique within the layer; ids enumerate
-                        layout-major, then algorithm, then parameter index  */
-  int32_t layout;    /* sn_layout = schema                                   */
+                        the run dtype first, then the other allowed dtypes
+                        in sn_dtype order; within a dtype layout-major, then
+                        algorithm, then parameter index                      */
+  int32_t layout;    /* sn_layout                                            */
   int32_t algo;      /* sn_algo                                              */
   int32_t param;     /* routine-parameter index (tile configuration)         */
+  int32_t dtype;     /* sn_dtype the routine computes and stores in          */
+  int32_t schema;    /* dtype * SN_NUM_LAYOUTS + layout                      */
   int64_t cost_ns;   /* profiled time T(r) in ns, -1 if not profiled         */
-  char name[64];     /* descriptor, e.g. "nhwc/igemm:128x128"                */
+  char name[64];     /* descriptor, e.g. "nhwc/igemm:p41"; with several
+                        dtypes allowed prefixed by the dtype, "f16:nhwc/..." */
 } sn_routine_desc;
 
 typedef enum {
@@ -124,9 +139,13 @@ typedef enum {
   SN_OPT_SEED = 4,      /* seed of the profiler's scratch-tensor fill (default 1)    */
   SN_OPT_FLUSH = 5,     /* bytes sn_run_timed writes to a scratch buffer before each
                            layer, evicting the caches (0 = off, the default)        */
-  SN_OPT_KEEP = 6       /* 1: the plan gives every intermediate tensor its own bytes
+  SN_OPT_KEEP = 6,      /* 1: the plan gives every intermediate tensor its own bytes
                            (no reuse by liveness), so sn_layer_output can read any
                            layer's stored output after a run (default 0)            */
+  SN_OPT_DTYPES = 7     /* bitmask of element types routines may compute in (bit =
+                           sn_dtype), default the run dtype only; with more than one
+                           every layer gets routines in each, and adapts cast
+                           between them (precision-hybrid tuning, Sec. IV-F)        */
 } sn_option;
 
 /* Creates a graph whose auxiliary input layer (id 0) carries the user tensor
@@ -141,7 +160,7 @@ int sn_graph_create(int32_t dtype, int32_t n, int32_t c, int32_t h, int32_t w, i
                     sn_graph** out);
 
 /* Sets an sn_option.  Options that change the routine set (LAYOUTS, ALGOS,
- * PARAMS) are accepted only before the first sn_add_layer.
+ * PARAMS, DTYPES) are accepted only before the first sn_add_layer.
  * Errors: SN_E_INVALID (unknown option or value), SN_E_STATE. */
 int sn_set_option(sn_graph* g, int32_t option, int64_t value);
 
@@ -161,6 +180,30 @@ int sn_set_option(sn_graph* g, int32_t option, int64_t value);
 int sn_add_layer(sn_graph* g, const sn_layer_desc* d, const int32_t* inputs, int32_t n_inputs,
                  const void* weight, const float* bias, int32_t* out_id);
 
+/* Adds a further net input (multi-input nets, Sec. IV-E): an input layer
+ * carrying the caller's tensor N x c x h x w (N of the graph, run dtype,
+ * NCHW), with one routine of time 0.  The paper joins the inputs of such a
+ * net with a zero-cost auxiliary input layer; layer 0 (the first input)
+ * plays that role, joined to every further input by an edge that carries no
+ * data and costs nothing.  Input k (0 = the graph's own) is the k-th tensor
+ * of sn_run_mimo.  *out_id receives the layer id.
+ * Errors: SN_E_INVALID (non-positive dims), SN_E_UNSUPPORTED (a tensor of
+ * 2 GiB or more), SN_E_STATE (after selection), SN_E_DEVICE. */
+int sn_add_input(sn_graph* g, int32_t c, int32_t h, int32_t w, int32_t* out_id);
+
+/* Marks a layer as a net output (multi-output nets, Sec. IV-E); outputs are
+ * numbered in marking order and delivered in NCHW, run dtype, by
+ * sn_run_mimo.  Without any mark the last added layer is the one output.
+ * The implicit auxiliary output layer merges all outputs; each output's edge
+ * into it pays its conversion to the run-dtype NCHW schema.  Every layer
+ * must reach an output (else selection fails with SN_E_INVALID).
+ * Errors: SN_E_INVALID (unknown layer, an input layer, marked twice),
+ * SN_E_STATE (after selection). */
+int sn_mark_output(sn_graph* g, int32_t layer);
+
+/* Number of net inputs and outputs (either pointer may be NULL). */
+int sn_num_io(const sn_graph* g, int32_t* n_inputs, int32_t* n_outputs);
+
 /* Unit profiling (Sec. III-C): times every routine of every layer on
  * scratch tensors of the layer's real shape, and every layout converter on
  * every edge (both directions of every schema pair), after warmup runs, as
@@ -179,6 +222,8 @@ int sn_profile(sn_graph* g, int32_t warmup, int32_t reps, void* hip_stream);
  * finite cost in any allowed schema), SN_E_INVALID (bad mode/layout/algo),
  * SN_E_INTERNAL (the dynamic program found inconsistent subpaths). */
 int sn_select_path(sn_graph* g, int32_t mode, int32_t layout, int32_t algo);
+/* (SN_SELECT_FIXED uses the run dtype, or the lowest allowed dtype when the
+ * run dtype is not among SN_OPT_DTYPES.) */
 
 /* Sets the routine path explicitly: routine_ids[i] is the routine id of
  * layer i for i = 0 .. n-1 (n = number of layers including the input).
@@ -188,8 +233,18 @@ int sn_set_path(sn_graph* g, const int32_t* routine_ids, int32_t n);
 /* Enqueues inference on the stream; asynchronous.  d_in: device tensor
  * N x C x H x W (NCHW, run dtype); d_out: device tensor of the output
  * layer's shape in NCHW (N x K for a net ending in FC or GAP).
- * Errors: SN_E_STATE (no plan), SN_E_DEVICE (host-only graph, HIP error). */
+ * Errors: SN_E_STATE (no plan), SN_E_INVALID (a net with several inputs or
+ * outputs: use sn_run_mimo), SN_E_DEVICE (host-only graph, HIP error). */
 int sn_run(sn_graph* g, const void* d_in, void* d_out, void* hip_stream);
+
+/* sn_run for nets with several inputs and outputs: d_ins[k] is input k
+ * (NCHW, run dtype, shape of its input layer), d_outs[k] output k (NCHW,
+ * run dtype, shape of the k-th output layer); n_in and n_out must equal the
+ * net's counts (sn_num_io).  Asynchronous on the stream.
+ * Errors: SN_E_STATE (no plan), SN_E_INVALID (counts, null pointers),
+ * SN_E_DEVICE. */
+int sn_run_mimo(sn_graph* g, const void* const* d_ins, int32_t n_in, void* const* d_outs, int32_t n_out,
+                void* hip_stream);
 
 /* sn_run without allocation, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
@@ -244,10 +299,13 @@ int sn_layer_output(const sn_graph* g, int32_t layer, void* d_dst, size_t cap, s
  * end to end, which sees what a sum of isolated layer times misses (cache
  * reuse between layers, launch gaps).  Candidates, in this order, identical
  * paths kept once:
- *   1. the DPRS path over the allowed schemas (SN_OPT_LAYOUTS);
- *   2. the DPRS path with layers 1..n-1 restricted to each non-empty proper
- *      subset of those schemas, subsets in increasing bitmask order;
- *   3. every fixed path (SN_SELECT_FIXED) of an allowed schema and algorithm.
+ *   1. the DPRS path over the allowed schemas (SN_OPT_LAYOUTS x SN_OPT_DTYPES);
+ *   2. the DPRS path with layers restricted to each non-empty proper subset
+ *      of the allowed layouts, subsets in increasing bitmask order;
+ *   3. with several dtypes allowed, the DPRS path restricted to each one
+ *      dtype (the single-precision tunings, in sn_dtype order);
+ *   4. every fixed path (SN_SELECT_FIXED) of an allowed layout and algorithm
+ *      (run dtype, or the lowest allowed dtype if it is not allowed).
  * A candidate that does not exist (some layer has no routine in the subset)
  * is skipped.  Each candidate's plan is compiled and run on a zero-filled
  * scratch input: warmup runs, then two rounds (candidate order, then
@@ -266,8 +324,9 @@ int sn_profile_integrated(sn_graph* g, int32_t warmup, int32_t reps, void* hip_s
 /* Candidate idx of the last sn_profile_integrated: routine id per layer
  * (routine_ids may be NULL; else n = number of layers), model time T(S) under
  * the unit-profiled table, measured end-to-end ns per run (-1 if not
- * measured), and kind_ab[3] = {kind, a, b}: kind 0 = DPRS over the schema
- * bitmask a, kind 1 = fixed path of layout a and algorithm b.  Any output
+ * measured), and kind_ab[3] = {kind, a, b}: kind 0 = DPRS over the layout
+ * bitmask a and the dtype bitmask b, kind 1 = fixed path of layout a and
+ * algorithm b.  Any output
  * pointer may be NULL.
  * Errors: SN_E_INVALID (idx out of range, n mismatch). */
 int sn_integrated_candidate(const sn_graph* g, int32_t idx, int32_t* routine_ids, int32_t n,
@@ -277,10 +336,12 @@ int sn_integrated_candidate(const sn_graph* g, int32_t idx, int32_t* routine_ids
  * adapt times per edge and schema pair), all times int64 ns, -1 = no
  * routine / unavailable:
  *   {"dtype":..., "layers":[{"id":i,"type":t,"routines":[{"rid":..,"layout":..,
- *     "algo":..,"param":..,"ns":..}]}],
- *    "edges":[{"from":j,"to":i,"ns":[[..3..],[..3..],[..3..]]}]}
- * The implicit auxiliary output layer appears as the last layer with one
- * NCHW routine of time 0, with an edge from the net output layer.
+ *     "algo":..,"param":..,"dtype":..,"schema":..,"ns":..}]}],
+ *    "edges":[{"from":j,"to":i,"ns":M}]}
+ * M is 3 x 3, indexed by layout, when the graph computes in its run dtype
+ * only, else 9 x 9, indexed by schema (dtype * 3 + layout).  The implicit
+ * auxiliary output layer appears as the last layer with one NCHW routine (run
+ * dtype) of time 0, with an edge from the net output layer.
  * sn_get_costs writes at most cap bytes including the terminating NUL; if
  * cap is too small it returns SN_E_NOMEM with *len = required size.
  * sn_set_costs replaces the table (host-only graphs included); it must list

@@ -161,12 +161,30 @@ def layer_forward(layer, inputs, w=None, b=None):
     raise ValueError(t)
 
 
-def forward(spec, tensors, storage="dtype", keep=None):
+def forward(spec, tensors, storage="dtype", keep=None, layer_dtypes=None):
     """Run the whole net.  ``tensors`` comes from ``workloads.generate`` decoded to
-    float64 (keys x, w, b).  Returns the list of layer outputs (index 0 = input);
-    intermediate outputs no longer needed are dropped unless ``keep`` is True."""
+    float64 (keys x, w, b, and ``inputs`` {layer id: tensor} for further net
+    inputs).  Returns the list of layer outputs (index 0 = input);
+    intermediate outputs no longer needed are dropped unless ``keep`` is True
+    (net outputs listed in ``spec["outputs"]`` are always kept).
+
+    ``layer_dtypes`` (storage "dtype" only): the element type each layer
+    computes in, a list indexed by layer id (entries for input layers are
+    ignored; default: the spec's dtype everywhere).  This is the oracle of a
+    precision-hybrid path (Sec. IV-F): a layer reads every input cast to its
+    own type (the adapt between schemas, one rounding of the stored value),
+    uses the caller's weights rounded once to its type (biases stay float32),
+    and stores its output rounded to its type; the net outputs are cast back
+    to the spec's dtype."""
     dtype = spec["dtype"]
     layers = spec["layers"]
+    ldt = [dtype] * (len(layers) + 1)
+    if layer_dtypes is not None:
+        assert storage == "dtype" and len(layer_dtypes) == len(layers) + 1
+        for i, L in enumerate(layers, start=1):
+            if L["type"] != "input":
+                ldt[i] = layer_dtypes[i]
+    keep_ids = set(spec.get("outputs", [len(layers)]))
     last_use = {}
     for i, layer in enumerate(layers, start=1):
         for j in layer["in"]:
@@ -174,15 +192,27 @@ def forward(spec, tensors, storage="dtype", keep=None):
     outs = [None] * (len(layers) + 1)
     outs[0] = _f64(tensors["x"])
     for i, layer in enumerate(layers, start=1):
+        if layer["type"] == "input":
+            outs[i] = _f64(tensors["inputs"][i])
+            continue
         ins = [outs[j] for j in layer["in"]]
-        y = layer_forward(layer, ins, tensors["w"][i - 1], tensors["b"][i - 1])
+        w = tensors["w"][i - 1]
         if storage == "dtype":
-            y = round_to(y, dtype)
+            ins = [x if ldt[j] == ldt[i] else round_to(x, ldt[i]) for x, j in zip(ins, layer["in"])]
+            if ldt[i] != dtype and w is not None:
+                w = round_to(w, ldt[i])
+        y = layer_forward(layer, ins, w, tensors["b"][i - 1])
+        if storage == "dtype":
+            y = round_to(y, ldt[i])
         outs[i] = y
         if not keep:
             for j in layer["in"]:
-                if last_use.get(j) == i and j != 0:
+                if last_use.get(j) == i and j != 0 and j not in keep_ids:
                     outs[j] = None
+    if storage == "dtype":
+        for o in keep_ids:
+            if ldt[o] != dtype:
+                outs[o] = round_to(outs[o], dtype)
     return outs
 
 

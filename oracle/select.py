@@ -156,16 +156,19 @@ def blockwise(problem, schemas):
 def problem_from_costs(costs):
     """Build a problem from the cost-table JSON the library exports (a dict or a
     JSON string): layers with their routines and times, edges with their
-    adapt-time matrices (-1 = unavailable)."""
+    adapt-time matrices (-1 = unavailable).  A routine's schema is its layout
+    when the matrices are 3 x 3 (one element type), else its (dtype, layout)
+    schema index, which the 9 x 9 matrices are indexed by."""
     if isinstance(costs, str):
         costs = json.loads(costs)
     layers = sorted(costs["layers"], key=lambda d: d["id"])
+    by_schema = any(len(e["ns"]) == 9 for e in costs["edges"])
     routines = []
     for d in layers:
         rl = []
         for r in d["routines"]:
             ns = r["ns"]
-            rl.append((r["rid"], r["layout"], None if ns < 0 else ns))
+            rl.append((r["rid"], r["schema"] if by_schema else r["layout"], None if ns < 0 else ns))
         routines.append(rl)
     edges = []
     for e in costs["edges"]:

@@ -81,7 +81,8 @@ int sn_set_option(sn_graph* gp, int32_t option, int64_t value) {
   return guarded([&] {
     CHECK_G(gp);
     Graph& g = gp->g;
-    bool routine_set = option == SN_OPT_LAYOUTS || option == SN_OPT_ALGOS || option == SN_OPT_PARAMS;
+    bool routine_set = option == SN_OPT_LAYOUTS || option == SN_OPT_ALGOS || option == SN_OPT_PARAMS ||
+                       option == SN_OPT_DTYPES;
     if (routine_set && g.n_layers() > 1)
       fail(SN_E_STATE, "routine-set options must be set before adding layers");
     switch (option) {
@@ -103,6 +104,10 @@ int sn_set_option(sn_graph* gp, int32_t option, int64_t value) {
         break;
       case SN_OPT_SEED:
         g.opt_seed = value;
+        break;
+      case SN_OPT_DTYPES:
+        if (value <= 0 || value > 7) fail(SN_E_INVALID, "dtype mask must be in 1..7");
+        g.opt_dtypes = value;
         break;
       case SN_OPT_KEEP:
         if (value != 0 && value != 1) fail(SN_E_INVALID, "KEEP is 0 or 1");
@@ -129,6 +134,29 @@ int sn_add_layer(sn_graph* gp, const sn_layer_desc* d, const int32_t* inputs, in
     if (!d) fail(SN_E_INVALID, "null layer description");
     int id = graph_add_layer(gp->g, *d, inputs, n_inputs, weight, bias);
     if (out_id) *out_id = id;
+  });
+}
+
+int sn_add_input(sn_graph* gp, int32_t c, int32_t h, int32_t w, int32_t* out_id) {
+  return guarded([&] {
+    CHECK_G(gp);
+    int id = graph_add_input(gp->g, c, h, w);
+    if (out_id) *out_id = id;
+  });
+}
+
+int sn_mark_output(sn_graph* gp, int32_t layer) {
+  return guarded([&] {
+    CHECK_G(gp);
+    graph_mark_output(gp->g, layer);
+  });
+}
+
+int sn_num_io(const sn_graph* gp, int32_t* n_inputs, int32_t* n_outputs) {
+  return guarded([&] {
+    CHECK_G(gp);
+    if (n_inputs) *n_inputs = (int32_t)gp->g.net_inputs.size();
+    if (n_outputs) *n_outputs = (int32_t)net_outputs(gp->g).size();
   });
 }
 
@@ -187,6 +215,11 @@ int sn_set_path(sn_graph* gp, const int32_t* ids, int32_t n) {
   });
 }
 
+static void require_single_io(const Graph& g) {
+  if (g.net_inputs.size() != 1 || net_outputs(g).size() != 1)
+    fail(SN_E_INVALID, "the net has several inputs or outputs: use sn_run_mimo");
+}
+
 int sn_run(sn_graph* gp, const void* d_in, void* d_out, void* stream) {
   return guarded([&] {
     CHECK_G(gp);
@@ -194,7 +227,25 @@ int sn_run(sn_graph* gp, const void* d_in, void* d_out, void* stream) {
     if (g.host_only()) fail(SN_E_DEVICE, "host-only graph cannot run");
     if (g.path.empty()) fail(SN_E_STATE, "no routine path selected");
     if (!d_in || !d_out) fail(SN_E_INVALID, "null device pointer");
-    plan_run(g, d_in, d_out, stream, nullptr);
+    require_single_io(g);
+    plan_run(g, &d_in, &d_out, stream, nullptr);
+  });
+}
+
+int sn_run_mimo(sn_graph* gp, const void* const* d_ins, int32_t n_in, void* const* d_outs, int32_t n_out,
+                void* stream) {
+  return guarded([&] {
+    CHECK_G(gp);
+    Graph& g = gp->g;
+    if (g.host_only()) fail(SN_E_DEVICE, "host-only graph cannot run");
+    if (g.path.empty()) fail(SN_E_STATE, "no routine path selected");
+    if (!d_ins || !d_outs || n_in != (int32_t)g.net_inputs.size() || n_out != (int32_t)net_outputs(g).size())
+      fail(SN_E_INVALID, "one device pointer per net input and per net output required");
+    for (int i = 0; i < n_in; ++i)
+      if (!d_ins[i]) fail(SN_E_INVALID, "null device pointer");
+    for (int i = 0; i < n_out; ++i)
+      if (!d_outs[i]) fail(SN_E_INVALID, "null device pointer");
+    plan_run(g, d_ins, d_outs, stream, nullptr);
   });
 }
 
@@ -212,8 +263,9 @@ int sn_run_noalloc(sn_graph* gp, const void* d_in, void* d_out, void* stream) {
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess) fail(SN_E_DEVICE, "hipGetDevice failed");
     if (cur != g.device && hipSetDevice(g.device) != hipSuccess) fail(SN_E_DEVICE, "hipSetDevice failed");
+    require_single_io(g);
     void* base = noalloc_scratch_ptr(g.device);
-    plan_run_in(g, base, noalloc_scratch_bytes(), d_in, d_out, stream);
+    plan_run_in(g, base, noalloc_scratch_bytes(), &d_in, &d_out, stream);
   });
 }
 
@@ -227,7 +279,8 @@ int sn_run_timed(sn_graph* gp, const void* d_in, void* d_out, void* stream, int3
     if (!d_in || !d_out || !layer_ms) fail(SN_E_INVALID, "null pointer");
     if (n != g.n_layers()) fail(SN_E_INVALID, "layer_ms must have one entry per layer");
     if (reps < 1 || reps > 10000) fail(SN_E_INVALID, "reps must be in 1..10000");
-    plan_run(g, d_in, d_out, stream, layer_ms, reps);
+    require_single_io(g);
+    plan_run(g, &d_in, &d_out, stream, layer_ms, reps);
   });
 }
 
@@ -339,6 +392,8 @@ int sn_routine_info(const sn_graph* gp, int32_t layer, int32_t idx, sn_routine_d
     out->layout = r.layout;
     out->algo = r.algo;
     out->param = r.param;
+    out->dtype = r.dtype;
+    out->schema = r.schema();
     out->cost_ns = L.cost[idx];
     std::snprintf(out->name, sizeof(out->name), "%s", r.name.c_str());
   });

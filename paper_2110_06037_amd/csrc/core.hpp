@@ -30,6 +30,14 @@ struct Shape {
 inline int round8(int c) { return (c + 7) / 8 * 8; }
 inline int dtype_size(int dt) { return dt == SN_F32 ? 4 : 2; }
 
+// A schema is a (dtype, layout) pair (Sec. III-C: a routine's schema names
+// the data representation it works in; converting between schemas is an
+// adapt job).  Index = dtype * SN_NUM_LAYOUTS + layout.
+constexpr int kNumSchemas = SN_NUM_SCHEMAS;
+inline int schema_of(int dtype, int layout) { return dtype * SN_NUM_LAYOUTS + layout; }
+inline int schema_dtype(int schema) { return schema / SN_NUM_LAYOUTS; }
+inline int schema_layout(int schema) { return schema % SN_NUM_LAYOUTS; }
+
 // Channels as stored by a layout (NC8HW8 pads to a multiple of 8).
 inline int stored_c(const Shape& s, int layout) { return layout == SN_NC8HW8 ? round8(s.c) : s.c; }
 inline int64_t stored_numel(const Shape& s, int layout) {
@@ -45,8 +53,13 @@ inline void check_tensor_size(const Shape& s, int dtype, const char* what) {
     fail(SN_E_UNSUPPORTED, std::string(what) + " of " + std::to_string(bytes) +
                                " bytes exceeds the 2 GiB a kernel addresses");
 }
+inline void check_tensor_size_any(const Shape& s, int64_t dtype_mask, const char* what) {
+  for (int d = 0; d < 3; ++d)
+    if (dtype_mask >> d & 1) check_tensor_size(s, d, what);
+}
 
-// Two layouts hold identical bytes for this shape (the adapt is void).
+// Two layouts hold identical bytes for this shape (the adapt is void); for
+// schemas the dtypes must agree too (see schemas_equivalent).
 inline bool layouts_equivalent(const Shape& s, int a, int b) {
   if (a == b) return true;
   auto canon = [&](int l) { return l == SN_NC8HW8 && s.c % 8 != 0 ? -1 : l; };
@@ -60,12 +73,19 @@ inline bool layouts_equivalent(const Shape& s, int a, int b) {
   return false;
 }
 
+// Two schemas hold identical bytes for this shape.
+inline bool schemas_equivalent(const Shape& s, int a, int b) {
+  return schema_dtype(a) == schema_dtype(b) && layouts_equivalent(s, schema_layout(a), schema_layout(b));
+}
+
 struct Routine {
   int id = 0;
   int layout = 0;
   int algo = 0;
   int param = 0;
+  int dtype = 0;  // element type it reads and writes
   std::string name;
+  int schema() const { return schema_of(dtype, layout); }
 };
 
 struct Layer {
@@ -84,7 +104,7 @@ struct Layer {
 
 struct Edge {
   int from = 0, to = 0;
-  int64_t adapt[SN_NUM_LAYOUTS][SN_NUM_LAYOUTS];  // ns, -1 = unavailable
+  int64_t adapt[kNumSchemas][kNumSchemas];  // ns by schema index, -1 = unavailable
 };
 
 struct Plan;      // execution plan (plan.cpp)
@@ -109,11 +129,14 @@ struct Graph {
   int device = -1;
   Shape in;
   int64_t opt_layouts = 7, opt_algos = 7, opt_params = 1, opt_hipgraph = 0, opt_seed = 1;
+  int64_t opt_dtypes = 0;  // compute dtypes allowed (bit = sn_dtype); set to the run dtype at init
   int64_t opt_flush = 0;  // bytes written before each layer of a timed run (0 = none)
   int64_t opt_keep = 0;   // 1: the plan gives every buffer its own bytes
   std::vector<Layer> layers;  // layers[0] = auxiliary input
   std::vector<Edge> edges;    // every (input -> layer) edge, in insertion order
-  Edge out_edge{};            // (last layer -> auxiliary output); from/to set on use
+  std::vector<int> net_inputs{0};  // layers carrying the caller's input tensors, in order
+  std::vector<int> marked_outputs; // net outputs in order; empty = the last layer
+  std::vector<Edge> out_edges;     // (net output k -> auxiliary output); from/to set on use
   bool have_costs = false;
   std::vector<int> path;      // routine index per layer; empty = none
   int64_t path_cost = -1;
@@ -122,6 +145,13 @@ struct Graph {
   std::unique_ptr<Plan> plan;
   std::unique_ptr<DevState> dev;
   bool host_only() const { return device < 0; }
+  bool multi_dtype() const { return opt_dtypes != (int64_t(1) << dtype); }
+  // schemas the DP may use: allowed layouts x allowed dtypes, plus the
+  // run-dtype NCHW schema of the auxiliary input and output layers
+  bool schema_allowed(int sc) const {
+    return sc == schema_of(dtype, SN_NCHW) ||
+           ((opt_layouts >> schema_layout(sc) & 1) && (opt_dtypes >> schema_dtype(sc) & 1));
+  }
   int n_layers() const { return (int)layers.size(); }
   Graph();
   ~Graph();
@@ -129,21 +159,27 @@ struct Graph {
 
 // graph.cpp
 void graph_init(Graph& g, int dtype, Shape in, int device);
+// a further net input (N x c x h x w, run dtype, NCHW): a zero-cost input
+// layer joined to the auxiliary input layer 0 by a structural edge
+int graph_add_input(Graph& g, int c, int h, int w);
+void graph_mark_output(Graph& g, int layer);
+std::vector<int> net_outputs(const Graph& g);
 int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int n_inputs,
                     const void* weight, const float* bias);
 // all edges including the one into the auxiliary output layer (id = n_layers())
 std::vector<Edge> all_edges(const Graph& g);
 std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L);
 bool winograd_applicable(const Layer& L, const Shape& in);
-std::string routine_name(const Layer& L, const Routine& r);
+std::string routine_name(const Graph& g, const Layer& L, const Routine& r);
 
 // select.cpp
-void select_dprs(Graph& g, int layout_mask = -1);
+void select_dprs(Graph& g, int layout_mask = -1, int dtype_mask = -1);
 // integrated profiling's candidate paths (Sec. III-C): DPRS over every
 // non-empty subset of the allowed layouts, then every fixed path; identical
 // paths kept once; g.path is left unchanged
 std::vector<Candidate> integrated_candidates(Graph& g);
-void select_fixed(Graph& g, int layout, int algo);
+// dtype -1: the run dtype if allowed, else the lowest allowed one
+void select_fixed(Graph& g, int layout, int algo, int dtype = -1);
 void set_path(Graph& g, const int32_t* ids, int n);
 int64_t path_total(const Graph& g, const std::vector<int>& path);
 
@@ -157,13 +193,15 @@ void dev_destroy(Graph& g);
 void dev_upload_layer(Graph& g, int layer);
 void dev_profile(Graph& g, int warmup, int reps, void* stream);
 void plan_compile(Graph& g);
-void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms = nullptr,
+// d_in / d_out: one device pointer per net input / output, in order
+void plan_run(Graph& g, const void* const* d_in, void* const* d_out, void* stream, float* layer_ms = nullptr,
               int reps = 1);
 void plan_destroy(Graph& g);
 // noalloc_scratch.hip: the static per-device region of sn_run_noalloc
 size_t noalloc_scratch_bytes();
 void* noalloc_scratch_ptr(int device);  // the region's device address (device must be current)
-void plan_run_in(const Graph& g, void* base, size_t cap, const void* d_in, void* d_out, void* stream);
+void plan_run_in(const Graph& g, void* base, size_t cap, const void* const* d_in, void* const* d_out,
+                 void* stream);
 size_t plan_arena_bytes(const Graph& g);
 void plan_layer_output(const Graph& g, int layer, void* d_dst, size_t cap, size_t* bytes, int* layout,
                        void* stream);

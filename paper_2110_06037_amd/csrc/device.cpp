@@ -23,8 +23,8 @@ namespace sn {
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
 struct DevLayer {
-  void* w = nullptr;    // dense [Kp][R][S][C8] | depthwise [R][S][C8] | fc [Kp][C8]
-  void* wu = nullptr;   // Winograd U [16][Kp][C8]
+  void* w[3] = {};      // per dtype: dense [Kp][R][S][C8] | depthwise [R][S][C8] | fc [Kp][C8]
+  void* wu[3] = {};     // per dtype: Winograd U [16][Kp][C8]
   float* bias = nullptr;  // [Kp]
 };
 
@@ -37,6 +37,7 @@ struct DevState {
 struct BufRef {
   int kind = 0;  // 0 arena, 1 user input, 2 user output
   size_t off = 0;
+  int idx = 0;   // which user input / output
 };
 
 struct Step {
@@ -44,6 +45,7 @@ struct Step {
   int layer = 0;  // layer the step is accounted to
   BufRef src, dst;
   k::TDesc sd{}, dd{};
+  int sdt = 0, ddt = 0;  // converter: source and destination element types
   int n_in = 0;
   BufRef in[2];
   k::TDesc ind[2]{};
@@ -63,8 +65,8 @@ struct Plan {
   hipStream_t gstream = nullptr;           // stream the captured graph replays on
   hipGraphExec_t gexec = nullptr;
   hipGraph_t graph = nullptr;
-  const void* g_in = nullptr;
-  void* g_out = nullptr;
+  std::vector<const void*> g_in;           // the user tensors the captured graph was made for
+  std::vector<void*> g_out;
   hipEvent_t gev[2] = {nullptr, nullptr};
 };
 
@@ -147,14 +149,18 @@ void dev_destroy(Graph& g) {
   if (!g.dev) return;
   (void)hipSetDevice(g.dev->device);
   for (auto& d : g.dev->L) {
-    if (d.w) (void)hipFree(d.w);
-    if (d.wu) (void)hipFree(d.wu);
+    for (void* p : d.w)
+      if (p) (void)hipFree(p);
+    for (void* p : d.wu)
+      if (p) (void)hipFree(p);
     if (d.bias) (void)hipFree(d.bias);
   }
   g.dev.reset();
 }
 
-// Prepared weight formats (see kernels/launch.hpp).
+// Prepared weight formats (see kernels/launch.hpp), one copy per allowed
+// dtype: the caller's weights (run dtype) are decoded exactly and rounded
+// once to each dtype.
 void dev_upload_layer(Graph& g, int id) {
   HIPCHK(hipSetDevice(g.device));
   DevState& D = *g.dev;
@@ -162,57 +168,67 @@ void dev_upload_layer(Graph& g, int id) {
   Layer& L = g.layers[id];
   DevLayer& dl = D.L[id];
   if (L.weight.empty()) return;
-  const int es = dtype_size(g.dtype);
+  const int ies = dtype_size(g.dtype);
   const Shape& in = g.layers[L.inputs[0]].out;
   const int K = L.out.c, Kp = round8(K), C = in.c, C8 = round8(C);
   std::vector<float> bias(Kp, 0.f);
   std::copy(L.bias.begin(), L.bias.end(), bias.begin());
   dl.bias = static_cast<float*>(dev_upload(bias.data(), bias.size() * 4));
   const uint8_t* src = L.weight.data();
-  if (L.type == SN_LAYER_FC) {
-    std::vector<uint8_t> w((size_t)Kp * C8 * es, 0);
-    for (int kk = 0; kk < K; ++kk)
-      std::memcpy(&w[((size_t)kk * C8) * es], src + (size_t)kk * C * es, (size_t)C * es);
-    dl.w = dev_upload(w.data(), w.size());
-    return;
-  }
   const int R = L.d.r, S = L.d.s;
-  if (is_depthwise(g, L)) {  // OIHW [C][1][R][S] -> [R][S][C8]
-    std::vector<uint8_t> w((size_t)R * S * C8 * es, 0);
-    for (int c = 0; c < C; ++c)
-      for (int r = 0; r < R; ++r)
-        for (int s = 0; s < S; ++s)
-          std::memcpy(&w[(((size_t)r * S + s) * C8 + c) * es], src + (((size_t)c * R + r) * S + s) * es, es);
-    dl.w = dev_upload(w.data(), w.size());
-    return;
-  }
-  // dense OIHW [K][C][R][S] -> [Kp][R][S][C8]
-  std::vector<uint8_t> w((size_t)Kp * R * S * C8 * es, 0);
-  for (int kk = 0; kk < K; ++kk)
-    for (int c = 0; c < C; ++c)
-      for (int r = 0; r < R; ++r)
-        for (int s = 0; s < S; ++s)
-          std::memcpy(&w[((((size_t)kk * R + r) * S + s) * C8 + c) * es],
-                      src + ((((size_t)kk * C + c) * R + r) * S + s) * es, es);
-  dl.w = dev_upload(w.data(), w.size());
-  if (winograd_applicable(L, in)) {
-    // U = G g G^T per (k, c), in float64, rounded once to the run dtype
-    static const double G[4][3] = {{1, 0, 0}, {0.5, 0.5, 0.5}, {0.5, -0.5, 0.5}, {0, 0, 1}};
-    std::vector<uint8_t> u((size_t)16 * Kp * C8 * es, 0);
+  for (int dt = 0; dt < 3; ++dt) {
+    if (!(g.opt_dtypes >> dt & 1)) continue;
+    const int es = dtype_size(dt);
+    // element e of the caller's weights, in dtype dt
+    auto put = [&](uint8_t* dst, size_t e) {
+      if (dt == g.dtype) std::memcpy(dst, src + e * ies, ies);
+      else encode(decode(src + e * ies, g.dtype), dt, dst);
+    };
+    if (L.type == SN_LAYER_FC) {
+      std::vector<uint8_t> w((size_t)Kp * C8 * es, 0);
+      for (int kk = 0; kk < K; ++kk)
+        for (int c = 0; c < C; ++c) put(&w[((size_t)kk * C8 + c) * es], (size_t)kk * C + c);
+      dl.w[dt] = dev_upload(w.data(), w.size());
+      continue;
+    }
+    if (is_depthwise(g, L)) {  // OIHW [C][1][R][S] -> [R][S][C8]
+      std::vector<uint8_t> w((size_t)R * S * C8 * es, 0);
+      for (int c = 0; c < C; ++c)
+        for (int r = 0; r < R; ++r)
+          for (int s2 = 0; s2 < S; ++s2)
+            put(&w[(((size_t)r * S + s2) * C8 + c) * es], ((size_t)c * R + r) * S + s2);
+      dl.w[dt] = dev_upload(w.data(), w.size());
+      continue;
+    }
+    // dense OIHW [K][C][R][S] -> [Kp][R][S][C8]
+    std::vector<uint8_t> w((size_t)Kp * R * S * C8 * es, 0);
     for (int kk = 0; kk < K; ++kk)
-      for (int c = 0; c < C; ++c) {
-        double gg[3][3], t[4][3];
-        for (int r = 0; r < 3; ++r)
-          for (int s = 0; s < 3; ++s) gg[r][s] = decode(src + ((((size_t)kk * C + c) * 3 + r) * 3 + s) * es, g.dtype);
-        for (int i = 0; i < 4; ++i)
-          for (int s = 0; s < 3; ++s) t[i][s] = G[i][0] * gg[0][s] + G[i][1] * gg[1][s] + G[i][2] * gg[2][s];
-        for (int i = 0; i < 4; ++i)
-          for (int j = 0; j < 4; ++j) {
-            double v = t[i][0] * G[j][0] + t[i][1] * G[j][1] + t[i][2] * G[j][2];
-            encode(v, g.dtype, &u[(((size_t)(i * 4 + j) * Kp + kk) * C8 + c) * es]);
-          }
-      }
-    dl.wu = dev_upload(u.data(), u.size());
+      for (int c = 0; c < C; ++c)
+        for (int r = 0; r < R; ++r)
+          for (int s2 = 0; s2 < S; ++s2)
+            put(&w[((((size_t)kk * R + r) * S + s2) * C8 + c) * es], (((size_t)kk * C + c) * R + r) * S + s2);
+    dl.w[dt] = dev_upload(w.data(), w.size());
+    if (winograd_applicable(L, in)) {
+      // U = G g G^T per (k, c), in float64 from the caller's weights, rounded
+      // once to the dtype
+      static const double G[4][3] = {{1, 0, 0}, {0.5, 0.5, 0.5}, {0.5, -0.5, 0.5}, {0, 0, 1}};
+      std::vector<uint8_t> u((size_t)16 * Kp * C8 * es, 0);
+      for (int kk = 0; kk < K; ++kk)
+        for (int c = 0; c < C; ++c) {
+          double gg[3][3], t[4][3];
+          for (int r = 0; r < 3; ++r)
+            for (int s2 = 0; s2 < 3; ++s2)
+              gg[r][s2] = decode(src + ((((size_t)kk * C + c) * 3 + r) * 3 + s2) * ies, g.dtype);
+          for (int i = 0; i < 4; ++i)
+            for (int s2 = 0; s2 < 3; ++s2) t[i][s2] = G[i][0] * gg[0][s2] + G[i][1] * gg[1][s2] + G[i][2] * gg[2][s2];
+          for (int i = 0; i < 4; ++i)
+            for (int j = 0; j < 4; ++j) {
+              double v = t[i][0] * G[j][0] + t[i][1] * G[j][1] + t[i][2] * G[j][2];
+              encode(v, dt, &u[(((size_t)(i * 4 + j) * Kp + kk) * C8 + c) * es]);
+            }
+        }
+      dl.wu[dt] = dev_upload(u.data(), u.size());
+    }
   }
 }
 
@@ -221,11 +237,11 @@ static size_t layer_ws_bytes(const Graph& g, const Layer& L, const Routine& r) {
   if (L.inputs.empty()) return 0;  // the input layer
   const Shape& in = g.layers[L.inputs[0]].out;
   if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM)
-    return k::igemm_ws_bytes(g.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), 1, 1);
+    return k::igemm_ws_bytes(r.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), 1, 1);
   if (L.type != SN_LAYER_CONV2D || L.d.groups > 1) return 0;
-  if (r.algo == SN_ALGO_WINOGRAD) return k::winograd_ws_bytes(g.dtype, tdesc(in, r.layout), L.out.c);
+  if (r.algo == SN_ALGO_WINOGRAD) return k::winograd_ws_bytes(r.dtype, tdesc(in, r.layout), L.out.c);
   if (r.algo == SN_ALGO_IGEMM)
-    return k::igemm_ws_bytes(g.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), L.d.r, L.d.s);
+    return k::igemm_ws_bytes(r.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), L.d.r, L.d.s);
   return 0;
 }
 
@@ -234,13 +250,13 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
                          size_t ws_bytes, hipStream_t st) {
   const Layer& L = g.layers[id];
   const DevLayer& dl = g.dev->L[id];
-  const int dt = g.dtype;
+  const int dt = r.dtype;
   switch (L.type) {
     case SN_LAYER_CONV2D: {
       k::ConvArgs a{};
       a.x = in[0];
       a.xd = ind[0];
-      a.w = r.algo == SN_ALGO_WINOGRAD ? dl.wu : dl.w;
+      a.w = r.algo == SN_ALGO_WINOGRAD ? dl.wu[dt] : dl.w[dt];
       a.bias = dl.bias;
       a.y = out;
       a.yd = outd;
@@ -280,7 +296,7 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
         k::ConvArgs a{};
         a.x = in[0];
         a.xd = ind[0];
-        a.w = dl.w;
+        a.w = dl.w[dt];
         a.bias = dl.bias;
         a.y = out;
         a.yd = outd;
@@ -292,7 +308,7 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
         a.ws_bytes = ws_bytes;
         k::conv_igemm(dt, r.param, a, st);
       } else {
-        k::fc_direct(dt, in[0], xs.n, xs.c, stored_c(xs, r.layout), dl.w, round8(xs.c), dl.bias, out,
+        k::fc_direct(dt, in[0], xs.n, xs.c, stored_c(xs, r.layout), dl.w[dt], round8(xs.c), dl.bias, out,
                      L.out.c, stored_c(L.out, r.layout), L.d.act, st);
       }
       break;
@@ -307,11 +323,13 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
   HIPCHK(hipSetDevice(g.device));
   hipStream_t st = static_cast<hipStream_t>(stream);
   DevState& D = *g.dev;
-  const int es = dtype_size(g.dtype);
-  // scratch sized for the largest tensor of any layout and the largest workspace
+  // scratch sized for the largest tensor of any schema and the largest workspace
+  int es_max = 2;
+  for (int d = 0; d < 3; ++d)
+    if (g.opt_dtypes >> d & 1 || d == g.dtype) es_max = std::max(es_max, dtype_size(d));
   size_t tmax = 0, wsmax = 0;
   for (const Layer& L : g.layers) {
-    for (int l = 0; l < SN_NUM_LAYOUTS; ++l) tmax = std::max(tmax, (size_t)stored_numel(L.out, l) * es);
+    for (int l = 0; l < SN_NUM_LAYOUTS; ++l) tmax = std::max(tmax, (size_t)stored_numel(L.out, l) * es_max);
     for (const Routine& r : L.routines) wsmax = std::max(wsmax, layer_ws_bytes(g, L, r));
   }
   tmax = align256(tmax);
@@ -329,9 +347,15 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
     HIPCHK(hipMalloc(&outb, tmax));
     if (wsmax) HIPCHK(hipMalloc(&ws, wsmax));
     for (auto& e : ev) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
-    k::fill_random(g.dtype, in0, tmax / es, (uint64_t)g.opt_seed, st);
-    k::fill_random(g.dtype, in1, tmax / es, (uint64_t)g.opt_seed + 7, st);
-    HIPCHK(hipGetLastError());
+    // operands hold values of the dtype being timed (refilled when it changes)
+    int filled = -1;
+    auto fill = [&](int dt) {
+      if (dt == filled) return;
+      k::fill_random(dt, in0, tmax / dtype_size(dt), (uint64_t)g.opt_seed, st);
+      k::fill_random(dt, in1, tmax / dtype_size(dt), (uint64_t)g.opt_seed + 7, st);
+      HIPCHK(hipGetLastError());
+      filled = dt;
+    };
     struct Clear {
       ~Clear() { k::g_timing = k::LaunchTiming{}; }
     } clear_on_exit;
@@ -354,6 +378,7 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
     };
     for (int i = 1; i < g.n_layers(); ++i) {
       Layer& L = g.layers[i];
+      if (L.type == SN_LAYER_INPUT) continue;  // a net input: its one routine costs 0
       for (size_t ri = 0; ri < L.routines.size(); ++ri) {
         const Routine& r = L.routines[ri];
         std::string key = L.signature + "|" + r.name;
@@ -362,6 +387,7 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
           L.cost[ri] = it->second;
           continue;
         }
+        fill(r.dtype);
         const void* ins[2] = {in0, in1};
         k::TDesc ind[2];
         for (size_t q = 0; q < L.inputs.size(); ++q) ind[q] = tdesc(g.layers[L.inputs[q]].out, r.layout);
@@ -372,19 +398,19 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
         L.cost[ri] = ns;
       }
     }
-    int64_t allowed = g.opt_layouts | (1 << SN_NCHW);
+    // adapt costs: every ordered pair of allowed schemas on every edge
     auto edge_costs = [&](Edge& e, const Shape& s) {
-      for (int a = 0; a < SN_NUM_LAYOUTS; ++a)
-        for (int b = 0; b < SN_NUM_LAYOUTS; ++b) {
+      for (int a = 0; a < kNumSchemas; ++a)
+        for (int b = 0; b < kNumSchemas; ++b) {
           if (a == b) {
             e.adapt[a][b] = 0;
             continue;
           }
-          if (!(allowed >> a & 1) || !(allowed >> b & 1)) {
+          if (!g.schema_allowed(a) || !g.schema_allowed(b)) {
             e.adapt[a][b] = -1;
             continue;
           }
-          if (layouts_equivalent(s, a, b)) {
+          if (schemas_equivalent(s, a, b)) {
             e.adapt[a][b] = 0;  // identical bytes: void adapt
             continue;
           }
@@ -393,15 +419,19 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
                             std::to_string(a) + ">" + std::to_string(b);
           auto it = D.cost_cache.find(key);
           if (it == D.cost_cache.end()) {
-            k::TDesc sd = tdesc(s, a), dd = tdesc(s, b);
-            int64_t ns = time_it([&] { k::convert(g.dtype, in0, sd, outb, dd, st); });
+            fill(schema_dtype(a));
+            k::TDesc sd = tdesc(s, schema_layout(a)), dd = tdesc(s, schema_layout(b));
+            int64_t ns = time_it([&] { k::convert_cast(schema_dtype(a), in0, sd, schema_dtype(b), outb, dd, st); });
             it = D.cost_cache.emplace(key, ns).first;
           }
           e.adapt[a][b] = it->second;
         }
     };
-    for (Edge& e : g.edges) edge_costs(e, g.layers[e.from].out);
-    edge_costs(g.out_edge, g.layers.back().out);
+    for (Edge& e : g.edges)
+      if (g.layers[e.to].type != SN_LAYER_INPUT) edge_costs(e, g.layers[e.from].out);
+    const std::vector<int> outs = net_outputs(g);
+    g.out_edges.resize(outs.size());
+    for (size_t k2 = 0; k2 < outs.size(); ++k2) edge_costs(g.out_edges[k2], g.layers[outs[k2]].out);
     HIPCHK(hipStreamSynchronize(st));
   } catch (...) {
     cleanup();
@@ -416,7 +446,8 @@ void plan_compile(Graph& g) {
   plan_destroy(g);
   std::unique_ptr<Plan> P(new Plan);
   const int n = g.n_layers();
-  const int es = dtype_size(g.dtype);
+  const std::vector<int> outs = net_outputs(g);
+  const int io_schema = schema_of(g.dtype, SN_NCHW);
   struct Buf {
     size_t bytes;
     int def, last;
@@ -430,8 +461,11 @@ void plan_compile(Graph& g) {
     bufs.push_back(Buf{align256(bytes), def, std::max(def, never), 0});
     return (int)bufs.size() - 1;
   };
+  auto schema_bytes = [&](const Shape& sh, int sc) {
+    return (size_t)stored_numel(sh, schema_layout(sc)) * dtype_size(schema_dtype(sc));
+  };
   // output tensor of each layer: kind/buffer index
-  std::vector<int> out_buf(n, -1);  // -1 = user input (layer 0) / user output
+  std::vector<int> out_buf(n, -1);  // -1 = a user tensor
   std::vector<BufRef> out_ref(n);
   std::vector<std::vector<int>> step_bufs;
   out_ref[0].kind = 1;
@@ -447,7 +481,13 @@ void plan_compile(Graph& g) {
   };
   for (int i = 1; i < n; ++i) {
     const Layer& L = g.layers[i];
+    if (L.type == SN_LAYER_INPUT) {  // a further net input: the caller's tensor
+      out_ref[i].kind = 1;
+      out_ref[i].idx = (int)(std::find(g.net_inputs.begin(), g.net_inputs.end(), i) - g.net_inputs.begin());
+      continue;
+    }
     const Routine& r = L.routines[g.path[i]];
+    const int rs = r.schema();
     Step s;
     s.type = 1;
     s.layer = i;
@@ -456,9 +496,9 @@ void plan_compile(Graph& g) {
     for (int q = 0; q < s.n_in; ++q) {
       const int j = L.inputs[q];
       const Shape& js = g.layers[j].out;
-      const int lj = g.layers[j].routines[g.path[j]].layout;
+      const int sj = g.layers[j].routines[g.path[j]].schema();
       s.ind[q] = tdesc(js, r.layout);
-      if (layouts_equivalent(js, lj, r.layout)) {
+      if (schemas_equivalent(js, sj, rs)) {
         s.in[q] = out_ref[j];
         if (out_buf[j] >= 0) uses.push_back(out_buf[j]);
       } else {
@@ -466,10 +506,12 @@ void plan_compile(Graph& g) {
         c.type = 0;
         c.layer = i;
         c.src = out_ref[j];
-        c.sd = tdesc(js, lj);
+        c.sd = tdesc(js, schema_layout(sj));
         c.dd = tdesc(js, r.layout);
+        c.sdt = schema_dtype(sj);
+        c.ddt = r.dtype;
         const int step_idx = (int)P->steps.size();
-        int b = new_buf((size_t)stored_numel(js, r.layout) * es, step_idx);
+        int b = new_buf(schema_bytes(js, rs), step_idx);
         c.dst.kind = 0;
         c.dst.off = (size_t)b;  // buffer id; resolved to an offset below
         std::vector<int> cu{b};
@@ -484,12 +526,14 @@ void plan_compile(Graph& g) {
       }
     }
     s.outd = tdesc(L.out, r.layout);
-    const bool last = i == n - 1;
+    const int out_k = (int)(std::find(outs.begin(), outs.end(), i) - outs.begin());
+    const bool is_out = out_k < (int)outs.size();
     const int step_idx = (int)P->steps.size();
-    if (last && layouts_equivalent(L.out, r.layout, SN_NCHW)) {
-      s.out.kind = 2;
+    if (is_out && schemas_equivalent(L.out, rs, io_schema)) {
+      s.out.kind = 2;  // straight into the caller's output tensor
+      s.out.idx = out_k;
     } else {
-      int b = new_buf((size_t)stored_numel(L.out, r.layout) * es, step_idx);
+      int b = new_buf(schema_bytes(L.out, rs), step_idx);
       out_buf[i] = b;
       s.out.kind = 0;
       s.out.off = (size_t)b;
@@ -504,14 +548,17 @@ void plan_compile(Graph& g) {
     }
     out_ref[i] = s.out;
     push(s, uses);
-    if (last && s.out.kind != 2) {  // adapt into the user's NCHW output
+    if (is_out && s.out.kind != 2) {  // adapt into the caller's NCHW output (run dtype)
       Step c;
       c.type = 0;
       c.layer = i;
       c.src = s.out;
       c.sd = s.outd;
       c.dd = tdesc(L.out, SN_NCHW);
+      c.sdt = r.dtype;
+      c.ddt = g.dtype;
       c.dst.kind = 2;
+      c.dst.idx = out_k;
       push(c, {out_buf[i]});
     }
   }
@@ -561,15 +608,15 @@ void plan_compile(Graph& g) {
   g.plan = std::move(P);
 }
 
-static void enqueue_step(const Graph& g, const Plan& P, char* base, const Step& s, const void* d_in,
-                         void* d_out, hipStream_t st) {
+static void enqueue_step(const Graph& g, const Plan& P, char* base, const Step& s, const void* const* d_in,
+                         void* const* d_out, hipStream_t st) {
   auto ptr = [&](const BufRef& r) -> void* {
-    if (r.kind == 1) return const_cast<void*>(d_in);
-    if (r.kind == 2) return d_out;
+    if (r.kind == 1) return const_cast<void*>(d_in[r.idx]);
+    if (r.kind == 2) return d_out[r.idx];
     return base + r.off;
   };
   if (s.type == 0) {
-    k::convert(g.dtype, ptr(s.src), s.sd, ptr(s.dst), s.dd, st);
+    k::convert_cast(s.sdt, ptr(s.src), s.sd, s.ddt, ptr(s.dst), s.dd, st);
   } else {
     const Routine& r = g.layers[s.layer].routines[g.path[s.layer]];
     const void* ins[2] = {ptr(s.in[0]), s.n_in > 1 ? ptr(s.in[1]) : nullptr};
@@ -578,8 +625,8 @@ static void enqueue_step(const Graph& g, const Plan& P, char* base, const Step& 
   }
 }
 
-static void enqueue_steps(const Graph& g, const Plan& P, char* base, const void* d_in, void* d_out,
-                          hipStream_t st) {
+static void enqueue_steps(const Graph& g, const Plan& P, char* base, const void* const* d_in,
+                          void* const* d_out, hipStream_t st) {
   for (const Step& s : P.steps) enqueue_step(g, P, base, s, d_in, d_out, st);
   HIPCHK(hipGetLastError());
 }
@@ -589,13 +636,14 @@ static void enqueue_steps(const Graph& g, const Plan& P, char* base, const void*
 // first repetition's first kernel and the end of the last repetition's last
 // kernel.  Every step writes buffers distinct from the ones it reads, so a
 // repetition recomputes the same values and the run's result is unchanged.
-static void enqueue_timed(const Graph& g, const Plan& P, const void* d_in, void* d_out,
+static void enqueue_timed(const Graph& g, const Plan& P, const void* const* d_in, void* const* d_out,
                           hipStream_t st, int reps, void* flush, int64_t flush_bytes) {
   struct Clear {
     ~Clear() { k::g_timing = k::LaunchTiming{}; }
   } clear_on_exit;
   for (int i = 1; i < g.n_layers(); ++i) {
     const int a = P.first_step[i], b = P.last_step[i];
+    if (a < 0) continue;  // a net input: nothing runs
     if (flush) {  // untimed: evict the caches before the layer
       k::g_timing = k::LaunchTiming{};
       k::fill_random(SN_F32, flush, flush_bytes / 4, (uint64_t)i, st);
@@ -611,7 +659,7 @@ static void enqueue_timed(const Graph& g, const Plan& P, const void* d_in, void*
   HIPCHK(hipGetLastError());
 }
 
-void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* layer_ms, int reps) {
+void plan_run(Graph& g, const void* const* d_in, void* const* d_out, void* stream, float* layer_ms, int reps) {
   if (!g.plan) fail(SN_E_STATE, "no execution plan");
   HIPCHK(hipSetDevice(g.device));
   Plan& P = *g.plan;
@@ -629,6 +677,8 @@ void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* laye
     if (flush) HIPCHK(hipFree(flush));
     layer_ms[0] = 0.f;
     for (int i = 1; i < g.n_layers(); ++i) {
+      layer_ms[i] = 0.f;
+      if (P.first_step[i] < 0) continue;
       HIPCHK(hipEventElapsedTime(&layer_ms[i], P.ev[2 * i], P.ev[2 * i + 1]));
       layer_ms[i] /= (float)reps;
     }
@@ -644,7 +694,9 @@ void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* laye
     HIPCHK(hipEventCreateWithFlags(&P.gev[0], hipEventDisableTiming));
     HIPCHK(hipEventCreateWithFlags(&P.gev[1], hipEventDisableTiming));
   }
-  if (!P.gexec || P.g_in != d_in || P.g_out != d_out) {
+  const std::vector<const void*> ins(d_in, d_in + g.net_inputs.size());
+  const std::vector<void*> outs(d_out, d_out + net_outputs(g).size());
+  if (!P.gexec || P.g_in != ins || P.g_out != outs) {
     if (P.gexec) HIPCHK(hipGraphExecDestroy(P.gexec));
     if (P.graph) HIPCHK(hipGraphDestroy(P.graph));
     P.gexec = nullptr;
@@ -660,8 +712,8 @@ void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* laye
     }
     HIPCHK(hipStreamEndCapture(P.gstream, &P.graph));
     HIPCHK(hipGraphInstantiate(&P.gexec, P.graph, nullptr, nullptr, 0));
-    P.g_in = d_in;
-    P.g_out = d_out;
+    P.g_in = ins;
+    P.g_out = outs;
   }
   HIPCHK(hipEventRecord(P.gev[0], st));
   HIPCHK(hipStreamWaitEvent(P.gstream, P.gev[0], 0));
@@ -674,7 +726,8 @@ void plan_run(Graph& g, const void* d_in, void* d_out, void* stream, float* laye
 // caller-provided device region of cap bytes instead of the plan's own
 // memory (same offsets, same launches, hence the same results).  Enqueues
 // only kernel launches: no allocation, no memset.
-void plan_run_in(const Graph& g, void* base, size_t cap, const void* d_in, void* d_out, void* stream) {
+void plan_run_in(const Graph& g, void* base, size_t cap, const void* const* d_in, void* const* d_out,
+                 void* stream) {
   if (!g.plan) fail(SN_E_STATE, "no execution plan");
   const Plan& P = *g.plan;
   if (P.arena_bytes > cap)
@@ -696,15 +749,18 @@ void plan_layer_output(const Graph& g, int layer, void* d_dst, size_t cap, size_
   if (layer < 1 || layer >= g.n_layers()) fail(SN_E_INVALID, "unknown layer (the input layer has no stored output)");
   const Plan& P = *g.plan;
   const Layer& L = g.layers[layer];
-  const int lay = L.routines[g.path[layer]].layout;
-  const size_t b = (size_t)stored_numel(L.out, lay) * dtype_size(g.dtype);
+  if (L.type == SN_LAYER_INPUT) fail(SN_E_INVALID, "a net input layer has no stored output");
+  const Routine& R = L.routines[g.path[layer]];
+  const int lay = R.layout;
+  const size_t b = (size_t)stored_numel(L.out, lay) * dtype_size(R.dtype);
   if (bytes) *bytes = b;
   if (layout) *layout = lay;
   if (!d_dst) return;
   if (cap < b) fail(SN_E_NOMEM, "destination smaller than the stored output");
   const BufRef& r = P.layer_out[layer];
   if (r.kind != 0) fail(SN_E_UNSUPPORTED, "the layer stores straight into the caller's output tensor");
-  if (!g.opt_keep && layer != g.n_layers() - 1)
+  const std::vector<int> outs = net_outputs(g);
+  if (!g.opt_keep && std::find(outs.begin(), outs.end(), layer) == outs.end())
     fail(SN_E_STATE, "intermediate outputs are kept only with SN_OPT_KEEP = 1");
   HIPCHK(hipSetDevice(g.device));
   HIPCHK(hipMemcpyAsync(d_dst, static_cast<char*>(P.arena) + r.off, b, hipMemcpyDeviceToDevice,
@@ -723,23 +779,27 @@ void integrated_measure(Graph& g, std::vector<Candidate>& cands, int warmup, int
   HIPCHK(hipSetDevice(g.device));
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int es = dtype_size(g.dtype);
-  const size_t in_bytes = (size_t)g.in.numel() * es;
-  const size_t out_bytes = (size_t)g.layers.back().out.numel() * es;
-  void* din = nullptr;
-  void* dout = nullptr;
+  const std::vector<int> outs = net_outputs(g);
+  std::vector<void*> din(g.net_inputs.size(), nullptr), dout(outs.size(), nullptr);
   hipEvent_t ev[2] = {nullptr, nullptr};
   const std::vector<int> saved = g.path;
   const int64_t saved_cost = g.path_cost;
   auto cleanup = [&] {
     for (auto& e : ev)
       if (e) (void)hipEventDestroy(e);
-    if (din) (void)hipFree(din);
-    if (dout) (void)hipFree(dout);
+    for (void* p : din)
+      if (p) (void)hipFree(p);
+    for (void* p : dout)
+      if (p) (void)hipFree(p);
   };
   try {
-    HIPCHK(hipMalloc(&din, std::max<size_t>(in_bytes, 256)));
-    HIPCHK(hipMalloc(&dout, std::max<size_t>(out_bytes, 256)));
-    HIPCHK(hipMemsetAsync(din, 0, in_bytes, st));
+    for (size_t q = 0; q < din.size(); ++q) {
+      const size_t b = (size_t)g.layers[g.net_inputs[q]].out.numel() * es;
+      HIPCHK(hipMalloc(&din[q], std::max<size_t>(b, 256)));
+      HIPCHK(hipMemsetAsync(din[q], 0, b, st));
+    }
+    for (size_t q = 0; q < dout.size(); ++q)
+      HIPCHK(hipMalloc(&dout[q], std::max<size_t>((size_t)g.layers[outs[q]].out.numel() * es, 256)));
     for (auto& e : ev) HIPCHK(hipEventCreate(&e));
     for (Candidate& c : cands) c.measured_ns = -1;
     const int nc = (int)cands.size();
@@ -749,9 +809,9 @@ void integrated_measure(Graph& g, std::vector<Candidate>& cands, int warmup, int
         g.path = c.path;
         g.path_cost = c.model_ns;
         plan_compile(g);
-        for (int w = 0; w < warmup; ++w) plan_run(g, din, dout, st);
+        for (int w = 0; w < warmup; ++w) plan_run(g, din.data(), dout.data(), st);
         HIPCHK(hipEventRecord(ev[0], st));
-        for (int r = 0; r < reps; ++r) plan_run(g, din, dout, st);
+        for (int r = 0; r < reps; ++r) plan_run(g, din.data(), dout.data(), st);
         HIPCHK(hipEventRecord(ev[1], st));
         HIPCHK(hipEventSynchronize(ev[1]));
         float ms = 0.f;

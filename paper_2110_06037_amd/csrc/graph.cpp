@@ -12,36 +12,96 @@
 namespace sn {
 
 static const char* kLayoutName[SN_NUM_LAYOUTS] = {"nchw", "nhwc", "nc8hw8"};
+static const char* kDtypeName[3] = {"f32", "f16", "bf16"};
 static const char* kAlgoName[SN_NUM_ALGOS] = {"direct", "igemm", "winograd"};
 
-std::vector<Edge> all_edges(const Graph& g) {
-  std::vector<Edge> e = g.edges;
-  Edge o = g.out_edge;
-  o.from = g.n_layers() - 1;
-  o.to = g.n_layers();
-  e.push_back(o);
+static Edge blank_edge(int from, int to) {
+  Edge e;
+  e.from = from;
+  e.to = to;
+  for (auto& row : e.adapt)
+    for (auto& v : row) v = -1;
   return e;
 }
 
-void graph_init(Graph& g, int dtype, Shape in, int device) {
-  for (auto& row : g.out_edge.adapt)
-    for (auto& v : row) v = -1;
-  g.dtype = dtype;
-  g.in = in;
-  g.device = device;
+std::vector<int> net_outputs(const Graph& g) {
+  if (!g.marked_outputs.empty()) return g.marked_outputs;
+  return {g.n_layers() - 1};
+}
+
+// The layer edges, then one edge from every net output to the auxiliary
+// output layer (id n_layers()), which merges them (Sec. IV-E).
+std::vector<Edge> all_edges(const Graph& g) {
+  std::vector<Edge> e = g.edges;
+  const std::vector<int> outs = net_outputs(g);
+  for (size_t k = 0; k < outs.size(); ++k) {
+    Edge o = k < g.out_edges.size() ? g.out_edges[k] : blank_edge(0, 0);
+    o.from = outs[k];
+    o.to = g.n_layers();
+    e.push_back(o);
+  }
+  return e;
+}
+
+static Layer input_layer(int id, int dtype, Shape s) {
   Layer L;
-  L.id = 0;
+  L.id = id;
   L.type = SN_LAYER_INPUT;
-  L.out = in;
+  L.out = s;
   Routine r;
   r.id = 0;
   r.layout = SN_NCHW;
   r.algo = SN_ALGO_DIRECT;
+  r.dtype = dtype;
   r.name = "input/nchw";
   L.routines.push_back(r);
   L.cost.push_back(0);
   L.signature = "input";
+  return L;
+}
+
+void graph_init(Graph& g, int dtype, Shape in, int device) {
+  g.dtype = dtype;
+  g.opt_dtypes = int64_t(1) << dtype;
+  g.in = in;
+  g.device = device;
+  g.layers.push_back(input_layer(0, dtype, in));
+}
+
+// The paper joins the inputs of a multi-input net with an auxiliary input
+// layer of zero cost (Sec. IV-E).  Layer 0 carries the first input and plays
+// that role: every further input layer gets an edge from it that carries no
+// data and costs nothing (both ends have the one run-dtype NCHW schema), so
+// the layer graph keeps a single source.
+int graph_add_input(Graph& g, int c, int h, int w) {
+  if (!g.path.empty()) fail(SN_E_STATE, "cannot add inputs after a path was selected");
+  if (c <= 0 || h <= 0 || w <= 0) fail(SN_E_INVALID, "input dims must be positive");
+  const Shape s{g.in.n, c, h, w};
+  check_tensor_size_any(s, g.opt_dtypes | (int64_t(1) << g.dtype), "input tensor");
+  const int id = g.n_layers();
+  Layer L = input_layer(id, g.dtype, s);
+  L.inputs.push_back(0);
   g.layers.push_back(std::move(L));
+  Edge e = blank_edge(0, id);
+  e.adapt[schema_of(g.dtype, SN_NCHW)][schema_of(g.dtype, SN_NCHW)] = 0;
+  g.edges.push_back(e);
+  g.net_inputs.push_back(id);
+  g.have_costs = false;
+  if (!g.host_only()) dev_upload_layer(g, id);
+  return id;
+}
+
+// Net outputs, in the order of the caller's output tensors; the implicit
+// auxiliary output layer merges them (Sec. IV-E).
+void graph_mark_output(Graph& g, int layer) {
+  if (!g.path.empty()) fail(SN_E_STATE, "cannot mark outputs after a path was selected");
+  if (layer < 1 || layer >= g.n_layers()) fail(SN_E_INVALID, "unknown layer");
+  if (g.layers[layer].type == SN_LAYER_INPUT) fail(SN_E_INVALID, "an input layer cannot be a net output");
+  if (std::find(g.marked_outputs.begin(), g.marked_outputs.end(), layer) != g.marked_outputs.end())
+    fail(SN_E_INVALID, "layer is already a net output");
+  g.marked_outputs.push_back(layer);
+  g.out_edges.clear();
+  g.have_costs = false;
 }
 
 bool winograd_applicable(const Layer& L, const Shape& in) {
@@ -54,8 +114,9 @@ static bool is_depthwise(const Layer& L, const Shape& in) {
   return L.type == SN_LAYER_CONV2D && L.d.groups > 1 && L.d.groups == in.c && L.d.k == in.c;
 }
 
-std::string routine_name(const Layer& L, const Routine& r) {
+std::string routine_name(const Graph& g, const Layer& L, const Routine& r) {
   std::ostringstream o;
+  if (g.multi_dtype()) o << kDtypeName[r.dtype] << ":";
   o << kLayoutName[r.layout] << "/" << kAlgoName[r.algo];
   if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_IGEMM) o << ":p" << r.param;
   if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM) o << ":1x1conv:p" << r.param;
@@ -67,46 +128,57 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
   if (L.type == SN_LAYER_INPUT) return out;
   const Shape& in = g.layers[L.inputs[0]].out;
   const int residual = L.type == SN_LAYER_CONV2D && L.inputs.size() == 2;
+  // the run dtype first (so a single-dtype graph numbers its routines as
+  // before), then the other allowed dtypes in sn_dtype order
+  std::vector<int> dts;
+  if (g.opt_dtypes >> g.dtype & 1) dts.push_back(g.dtype);
+  for (int d = 0; d < 3; ++d)
+    if (d != g.dtype && (g.opt_dtypes >> d & 1)) dts.push_back(d);
+  int dt = g.dtype;
   auto add = [&](int layout, int algo, int param) {
     Routine r;
     r.id = (int)out.size();
     r.layout = layout;
     r.algo = algo;
     r.param = param;
-    r.name = routine_name(L, r);
+    r.dtype = dt;
+    r.name = routine_name(g, L, r);
     out.push_back(r);
   };
-  for (int lay = 0; lay < SN_NUM_LAYOUTS; ++lay) {
-    if (!(g.opt_layouts >> lay & 1)) continue;
-    switch (L.type) {
-      case SN_LAYER_CONV2D:
-        if (is_depthwise(L, in)) {
-          add(lay, SN_ALGO_DIRECT, 0);  // depthwise has its own direct routine
+  for (int d : dts) {
+    dt = d;
+    for (int lay = 0; lay < SN_NUM_LAYOUTS; ++lay) {
+      if (!(g.opt_layouts >> lay & 1)) continue;
+      switch (L.type) {
+        case SN_LAYER_CONV2D:
+          if (is_depthwise(L, in)) {
+            add(lay, SN_ALGO_DIRECT, 0);  // depthwise has its own direct routine
+            break;
+          }
+          if (g.opt_algos >> SN_ALGO_DIRECT & 1) add(lay, SN_ALGO_DIRECT, 0);
+          if (g.opt_algos >> SN_ALGO_IGEMM & 1) {
+            int np = g.opt_params ? k::igemm_num_params(dt) : 1;
+            for (int p = 0; p < np; ++p)
+              if (k::igemm_param_valid(dt, p, lay, in.n, in.c, in.h, in.w, L.d.r, L.d.s, L.d.stride,
+                                       L.d.pad, L.d.k) &&
+                  (residual == 0 || k::igemm_param_takes_residual(dt, p, lay, L.d.k)))
+                add(lay, SN_ALGO_IGEMM, p);
+          }
+          if ((g.opt_algos >> SN_ALGO_WINOGRAD & 1) && !residual && winograd_applicable(L, in))
+            add(lay, SN_ALGO_WINOGRAD, 0);
           break;
-        }
-        if (g.opt_algos >> SN_ALGO_DIRECT & 1) add(lay, SN_ALGO_DIRECT, 0);
-        if (g.opt_algos >> SN_ALGO_IGEMM & 1) {
-          int np = g.opt_params ? k::igemm_num_params(g.dtype) : 1;
-          for (int p = 0; p < np; ++p)
-            if (k::igemm_param_valid(g.dtype, p, lay, in.n, in.c, in.h, in.w, L.d.r, L.d.s, L.d.stride,
-                                     L.d.pad, L.d.k) &&
-                (residual == 0 || k::igemm_param_takes_residual(g.dtype, p, lay, L.d.k)))
-              add(lay, SN_ALGO_IGEMM, p);
-        }
-        if ((g.opt_algos >> SN_ALGO_WINOGRAD & 1) && !residual && winograd_applicable(L, in))
-          add(lay, SN_ALGO_WINOGRAD, 0);
-        break;
-      case SN_LAYER_FC:
-        add(lay, SN_ALGO_DIRECT, 0);
-        if (g.opt_algos >> SN_ALGO_IGEMM & 1) {  // the dense childnet: a 1x1 convolution
-          int np = g.opt_params ? k::igemm_num_params(g.dtype) : 1;
-          for (int p = 0; p < np; ++p)
-            if (k::igemm_param_valid(g.dtype, p, lay, in.n, in.c, 1, 1, 1, 1, 1, 0, L.d.k))
-              add(lay, SN_ALGO_IGEMM, p);
-        }
-        break;
-      default:
-        add(lay, SN_ALGO_DIRECT, 0);
+        case SN_LAYER_FC:
+          add(lay, SN_ALGO_DIRECT, 0);
+          if (g.opt_algos >> SN_ALGO_IGEMM & 1) {  // the dense childnet: a 1x1 convolution
+            int np = g.opt_params ? k::igemm_num_params(dt) : 1;
+            for (int p = 0; p < np; ++p)
+              if (k::igemm_param_valid(dt, p, lay, in.n, in.c, 1, 1, 1, 1, 1, 0, L.d.k))
+                add(lay, SN_ALGO_IGEMM, p);
+          }
+          break;
+        default:
+          add(lay, SN_ALGO_DIRECT, 0);
+      }
     }
   }
   return out;
@@ -189,7 +261,7 @@ int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int
       break;
   }
   if (out.h <= 0 || out.w <= 0) fail(SN_E_SHAPE, "empty output");
-  check_tensor_size(out, g.dtype, "layer output");
+  check_tensor_size_any(out, g.opt_dtypes, "layer output");
   L.out = out;
   if (wbytes) {
     L.weight.resize(wbytes);
@@ -202,14 +274,7 @@ int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int
   Layer& ref = g.layers.back();
   ref.routines = enumerate_routines(g, ref);
   ref.cost.assign(ref.routines.size(), -1);
-  for (int j : ref.inputs) {
-    Edge e;
-    e.from = j;
-    e.to = ref.id;
-    for (auto& row : e.adapt)
-      for (auto& v : row) v = -1;
-    g.edges.push_back(e);
-  }
+  for (int j : ref.inputs) g.edges.push_back(blank_edge(j, ref.id));
   g.have_costs = false;
   if (!g.host_only()) dev_upload_layer(g, ref.id);
   return ref.id;

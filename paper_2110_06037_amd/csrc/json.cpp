@@ -21,24 +21,28 @@ std::string costs_to_json(const Graph& g) {
       const Routine& R = L.routines[r];
       if (r) o << ",";
       o << "{\"rid\":" << R.id << ",\"layout\":" << R.layout << ",\"algo\":" << R.algo
-        << ",\"param\":" << R.param << ",\"ns\":" << L.cost[r] << ",\"name\":\"" << R.name << "\"}";
+        << ",\"param\":" << R.param << ",\"dtype\":" << R.dtype << ",\"schema\":" << R.schema()
+        << ",\"ns\":" << L.cost[r] << ",\"name\":\"" << R.name << "\"}";
     }
     o << "]}";
   }
   o << ",{\"id\":" << g.n_layers() << ",\"type\":" << SN_LAYER_OUTPUT
-    << ",\"routines\":[{\"rid\":0,\"layout\":0,\"algo\":0,\"param\":0,\"ns\":0,\"name\":\"output/"
-       "nchw\"}]}";
+    << ",\"routines\":[{\"rid\":0,\"layout\":0,\"algo\":0,\"param\":0,\"dtype\":" << g.dtype
+    << ",\"schema\":" << schema_of(g.dtype, SN_NCHW) << ",\"ns\":0,\"name\":\"output/nchw\"}]}";
   o << "],\"edges\":[";
   auto E = all_edges(g);
   for (size_t k = 0; k < E.size(); ++k) {
     if (k) o << ",";
+    // one dtype: the 3 x 3 layout matrix of the run dtype; else 9 x 9 by schema
     o << "{\"from\":" << E[k].from << ",\"to\":" << E[k].to << ",\"ns\":[";
-    for (int a = 0; a < SN_NUM_LAYOUTS; ++a) {
+    const int S = g.multi_dtype() ? kNumSchemas : SN_NUM_LAYOUTS;
+    const int base = g.multi_dtype() ? 0 : schema_of(g.dtype, 0);
+    for (int a = 0; a < S; ++a) {
       if (a) o << ",";
       o << "[";
-      for (int b = 0; b < SN_NUM_LAYOUTS; ++b) {
+      for (int b = 0; b < S; ++b) {
         if (b) o << ",";
-        o << (a == b ? 0 : E[k].adapt[a][b]);
+        o << (a == b ? 0 : E[k].adapt[base + a][base + b]);
       }
       o << "]";
     }
@@ -200,14 +204,17 @@ void costs_from_json(Graph& g, const char* json) {
     for (size_t r = 0; r < rts.size(); ++r) {
       const Routine& R = L.routines[r];
       if (rts[r].at("rid").as_int() != R.id || rts[r].at("layout").as_int() != R.layout ||
-          rts[r].at("algo").as_int() != R.algo || rts[r].at("param").as_int() != R.param)
+          rts[r].at("algo").as_int() != R.algo || rts[r].at("param").as_int() != R.param ||
+          (rts[r].obj.count("dtype") && rts[r].at("dtype").as_int() != R.dtype))
         fail(SN_E_INVALID, "layer " + std::to_string(i) + ": routine list differs");
       long long ns = rts[r].at("ns").as_int();
       if (ns < -1) fail(SN_E_INVALID, "negative time");
       cost[i].push_back(ns);
     }
   }
-  if (cost[0].empty() || cost[0][0] != 0) fail(SN_E_INVALID, "input layer time must be 0");
+  for (int i = 0; i < g.n_layers(); ++i)
+    if (g.layers[i].type == SN_LAYER_INPUT && (cost[i].empty() || cost[i][0] != 0))
+      fail(SN_E_INVALID, "input layer time must be 0");
   const auto& edges = root.at("edges").as_arr();
   auto E = all_edges(g);
   if (edges.size() != E.size()) fail(SN_E_INVALID, "cost table lists a different number of edges");
@@ -215,22 +222,28 @@ void costs_from_json(Graph& g, const char* json) {
   for (size_t k = 0; k < E.size(); ++k) {
     if (edges[k].at("from").as_int() != E[k].from || edges[k].at("to").as_int() != E[k].to)
       fail(SN_E_INVALID, "edge list differs");
+    // 3 x 3 by layout (a graph with one dtype) or 9 x 9 by schema
     const auto& rows = edges[k].at("ns").as_arr();
-    if (rows.size() != SN_NUM_LAYOUTS) fail(SN_E_INVALID, "adapt matrix must be 3 x 3");
-    for (int a = 0; a < SN_NUM_LAYOUTS; ++a) {
+    const int S = (int)rows.size();
+    if (S != kNumSchemas && !(S == SN_NUM_LAYOUTS && !g.multi_dtype()))
+      fail(SN_E_INVALID, g.multi_dtype() ? "adapt matrix must be 9 x 9" : "adapt matrix must be 3 x 3 or 9 x 9");
+    const int base = S == kNumSchemas ? 0 : schema_of(g.dtype, 0);
+    for (auto& row : parsed[k].adapt)
+      for (auto& v : row) v = -1;
+    for (int a = 0; a < S; ++a) {
       const auto& row = rows[a].as_arr();
-      if (row.size() != SN_NUM_LAYOUTS) fail(SN_E_INVALID, "adapt matrix must be 3 x 3");
-      for (int b = 0; b < SN_NUM_LAYOUTS; ++b) {
+      if ((int)row.size() != S) fail(SN_E_INVALID, "adapt matrix must be square");
+      for (int b = 0; b < S; ++b) {
         long long v = row[b].as_int();
         if (v < -1) fail(SN_E_INVALID, "negative time");
-        parsed[k].adapt[a][b] = a == b ? 0 : v;
+        parsed[k].adapt[base + a][base + b] = a == b ? 0 : v;
       }
     }
   }
   for (int i = 0; i < g.n_layers(); ++i) g.layers[i].cost = cost[i];
-  for (size_t k = 0; k + 1 < E.size(); ++k)
+  for (size_t k = 0; k < g.edges.size(); ++k)
     std::memcpy(g.edges[k].adapt, parsed[k].adapt, sizeof(parsed[k].adapt));
-  std::memcpy(g.out_edge.adapt, parsed.back().adapt, sizeof(parsed.back().adapt));
+  g.out_edges.assign(parsed.begin() + g.edges.size(), parsed.end());
   g.have_costs = true;
 }
 

@@ -124,6 +124,9 @@ void add_act(int dtype, const void* a, const void* b, void* y, int64_t n, int ac
 void fc_direct(int dtype, const void* x, int n, int cin, int cin_s, const void* w, int c8,
                const float* bias, void* y, int kout, int kout_s, int act, hipStream_t st);
 void convert(int dtype, const void* x, const TDesc& xd, void* y, const TDesc& yd, hipStream_t st);
+// schema conversion: layout and element type (sdt -> ddt) at once; equal
+// dtypes fall back to convert (see convert.hip)
+void convert_cast(int sdt, const void* x, const TDesc& xd, int ddt, void* y, const TDesc& yd, hipStream_t st);
 void fill_random(int dtype, void* p, int64_t n, uint64_t seed, hipStream_t st);
 
 }  // namespace k

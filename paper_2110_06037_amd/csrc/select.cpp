@@ -22,9 +22,13 @@
 //    constrained one.
 //  * "fastest" breaks ties by the routine-id vector in layer order, so the
 //    returned path is the unique (time, lexicographic) minimum.
-//  * The auxiliary input layer has one NCHW routine of time 0; an implicit
-//    auxiliary output layer with one NCHW routine of time 0 follows the last
-//    layer (Sec. IV-E), so the final constraint set is empty (Sec. IV-F).
+//  * The auxiliary input layer has one NCHW routine of time 0 (as has every
+//    further net input, joined to it by a zero-cost edge); an implicit
+//    auxiliary output layer with one NCHW routine of time 0 takes every net
+//    output (Sec. IV-E), so the final constraint set is empty (Sec. IV-F).
+//  * A schema is a (dtype, layout) pair; with one dtype the schemas are the
+//    layouts.  The DP is the same for any schema set (Sec. IV-F: hybrid
+//    tuning only enlarges it).
 #include <algorithm>
 #include <numeric>
 
@@ -36,55 +40,57 @@ namespace {
 
 struct Problem {
   int L = 0;                                  // layers incl. auxiliary output
-  int S = 0;                                  // number of schemas
-  std::vector<int> schema_of_layout;          // layout -> schema index or -1
+  int S = 0;                                  // number of schemas in use
+  std::vector<int> index_of_schema;           // schema (dtype x layout) -> index or -1
   std::vector<std::vector<int64_t>> cost;     // [i][r], kInf = unavailable
-  std::vector<std::vector<int>> schema;       // [i][r]
+  std::vector<std::vector<int>> schema;       // [i][r], schema index
   std::vector<std::vector<int>> preds, succs; // distinct neighbours
   struct E {
     int a, b;
-    int64_t A[SN_NUM_LAYOUTS][SN_NUM_LAYOUTS];  // schema-indexed, kInf = unavailable
+    std::vector<int64_t> A;                   // S x S by schema index, kInf = unavailable
+    int64_t at(int x, int y, int S_) const { return A[(size_t)x * S_ + y]; }
   };
   std::vector<E> edges;
 };
 
-// layout_mask restricts the routines of layers 1..n-1 to those layouts
-// (the auxiliary layers keep their NCHW routine)
-Problem make_problem(const Graph& g, int layout_mask = -1) {
+// layout_mask / dtype_mask restrict the routines of layers 1..n-1 to those
+// layouts / dtypes (the auxiliary layers keep their run-dtype NCHW routine)
+Problem make_problem(const Graph& g, int layout_mask = -1, int dtype_mask = -1) {
   Problem P;
   int n = g.n_layers();
   P.L = n + 1;
-  P.schema_of_layout.assign(SN_NUM_LAYOUTS, -1);
-  int64_t mask = g.opt_layouts | (1 << SN_NCHW);  // NCHW carries the user tensors
-  for (int l = 0; l < SN_NUM_LAYOUTS; ++l)
-    if (mask >> l & 1) P.schema_of_layout[l] = P.S++;
+  P.index_of_schema.assign(kNumSchemas, -1);
+  for (int sc = 0; sc < kNumSchemas; ++sc)
+    if (g.schema_allowed(sc)) P.index_of_schema[sc] = P.S++;
   P.cost.resize(P.L);
   P.schema.resize(P.L);
   for (int i = 0; i < n; ++i) {
     const Layer& L = g.layers[i];
     for (size_t r = 0; r < L.routines.size(); ++r) {
+      const Routine& R = L.routines[r];
       int64_t c = L.cost[r];
-      if (i > 0 && !(layout_mask >> L.routines[r].layout & 1)) c = -1;
+      if (L.type != SN_LAYER_INPUT && (!(layout_mask >> R.layout & 1) || !(dtype_mask >> R.dtype & 1))) c = -1;
+      const int si = P.index_of_schema[R.schema()];
+      if (si < 0) c = -1;
       P.cost[i].push_back(c < 0 ? kInf : c);
-      P.schema[i].push_back(P.schema_of_layout[L.routines[r].layout]);
+      P.schema[i].push_back(si < 0 ? 0 : si);
     }
   }
   P.cost[n] = {0};
-  P.schema[n] = {P.schema_of_layout[SN_NCHW]};
+  P.schema[n] = {P.index_of_schema[schema_of(g.dtype, SN_NCHW)]};
   P.preds.resize(P.L);
   P.succs.resize(P.L);
   for (const Edge& e : all_edges(g)) {
     Problem::E pe;
     pe.a = e.from;
     pe.b = e.to;
-    for (int x = 0; x < SN_NUM_LAYOUTS; ++x)
-      for (int y = 0; y < SN_NUM_LAYOUTS; ++y) pe.A[x][y] = kInf;
-    for (int x = 0; x < SN_NUM_LAYOUTS; ++x)
-      for (int y = 0; y < SN_NUM_LAYOUTS; ++y) {
-        int sx = P.schema_of_layout[x], sy = P.schema_of_layout[y];
+    pe.A.assign((size_t)P.S * P.S, kInf);
+    for (int x = 0; x < kNumSchemas; ++x)
+      for (int y = 0; y < kNumSchemas; ++y) {
+        int sx = P.index_of_schema[x], sy = P.index_of_schema[y];
         if (sx < 0 || sy < 0) continue;
         int64_t v = x == y ? 0 : e.adapt[x][y];
-        pe.A[sx][sy] = v < 0 ? kInf : v;
+        pe.A[(size_t)sx * P.S + sy] = v < 0 ? kInf : v;
       }
     P.edges.push_back(pe);
     auto& pr = P.preds[e.to];
@@ -96,7 +102,7 @@ Problem make_problem(const Graph& g, int layout_mask = -1) {
   for (int i = 0; i + 1 < P.L; ++i)
     if (P.succs[i].empty())
       fail(SN_E_INVALID, "layer " + std::to_string(i) +
-                             " has no consumer: the net must have one input and one output");
+                             " has no consumer: every layer must reach a net output");
   return P;
 }
 
@@ -114,7 +120,7 @@ int64_t assignment_time(const Problem& P, const std::vector<int32_t>& U) {
     if (U[e.a] < 0 || U[e.b] < 0) continue;
     int sa = P.schema[e.a][U[e.a]], sb = P.schema[e.b][U[e.b]];
     if (sa == sb) continue;
-    int64_t c = e.A[sa][sb];
+    int64_t c = e.at(sa, sb, P.S);
     if (c >= kInf) return kInf;
     t += c;
   }
@@ -144,9 +150,9 @@ int64_t ipow(int64_t b, int e) {
 
 }  // namespace
 
-void select_dprs(Graph& g, int layout_mask) {
+void select_dprs(Graph& g, int layout_mask, int dtype_mask) {
   if (!g.have_costs) fail(SN_E_STATE, "no cost table: call sn_profile or sn_set_costs first");
-  Problem P = make_problem(g, layout_mask);
+  Problem P = make_problem(g, layout_mask, dtype_mask);
   const int L = P.L, S = P.S;
 
   // post-dominator sets on the 1-in-1-out DAG (the output post-dominates all)
@@ -183,7 +189,8 @@ void select_dprs(Graph& g, int layout_mask) {
       for (int c : T[h].C)
         if (std::find(ti.C.begin(), ti.C.end(), c) == ti.C.end()) ti.C.push_back(c);
     std::sort(ti.C.begin(), ti.C.end());
-    if (ti.C.size() > 12) fail(SN_E_UNSUPPORTED, "too many open branches for DPRS");
+    if (ti.C.size() > 12 || ipow(S, (int)ti.C.size() + 1) > (int64_t(1) << 26))
+      fail(SN_E_UNSUPPORTED, "too many open branches for DPRS");
     const int nc = (int)ti.C.size();
     const int64_t nCt = ipow(S, nc);
     ti.st.assign(S * nCt, State{});
@@ -306,16 +313,23 @@ int64_t path_total(const Graph& g, const std::vector<int>& path) {
   return t >= kInf ? -1 : t;
 }
 
-void select_fixed(Graph& g, int layout, int algo) {
+void select_fixed(Graph& g, int layout, int algo, int dtype) {
   if (layout < 0 || layout >= SN_NUM_LAYOUTS || algo < 0 || algo >= SN_NUM_ALGOS)
     fail(SN_E_INVALID, "bad layout or algorithm");
+  if (dtype < 0) {
+    dtype = g.dtype;
+    for (int d = 2; d >= 0; --d)
+      if (!(g.opt_dtypes >> dtype & 1) && (g.opt_dtypes >> d & 1)) dtype = d;
+  }
+  if (dtype > 2 || !(g.opt_dtypes >> dtype & 1)) fail(SN_E_INVALID, "dtype not allowed");
   std::vector<int> path(g.n_layers(), 0);
   for (int i = 1; i < g.n_layers(); ++i) {
     const Layer& L = g.layers[i];
+    if (L.type == SN_LAYER_INPUT) continue;  // a net input keeps its one routine
     auto pick = [&](int want_algo) {
       int best = -1;
       for (const Routine& r : L.routines) {
-        if (r.layout != layout || r.algo != want_algo) continue;
+        if (r.layout != layout || r.algo != want_algo || r.dtype != dtype) continue;
         if (best < 0) {
           best = r.id;
           continue;
@@ -365,6 +379,7 @@ std::vector<Candidate> integrated_candidates(Graph& g) {
   std::vector<int> masks{full};
   for (int m = 1; m < full; ++m)
     if ((m & full) == m) masks.push_back(m);
+  const int dfull = (int)(g.opt_dtypes & 7);
   try {
     for (int m : masks) {
       try {
@@ -373,8 +388,21 @@ std::vector<Candidate> integrated_candidates(Graph& g) {
         if (e.code != SN_E_UNSUPPORTED) throw;
         continue;  // some layer has no routine in these layouts
       }
-      add(0, m, 0);
+      add(0, m, dfull);
     }
+    // with several dtypes: the best path in each dtype alone (the
+    // single-schema-family tunings that hybrid tuning is measured against)
+    if (g.multi_dtype())
+      for (int d = 0; d < 3; ++d) {
+        if (!(dfull >> d & 1)) continue;
+        try {
+          select_dprs(g, full, 1 << d);
+        } catch (const Error& e) {
+          if (e.code != SN_E_UNSUPPORTED) throw;
+          continue;
+        }
+        add(0, full, 1 << d);
+      }
     for (int l = 0; l < SN_NUM_LAYOUTS; ++l) {
       if (!(full >> l & 1)) continue;
       for (int a = 0; a < SN_NUM_ALGOS; ++a) {

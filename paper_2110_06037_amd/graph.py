@@ -30,7 +30,7 @@ class Graph:
     ``device=-1`` makes a host-only graph: only cost-table import, selection
     and queries work (no weights are uploaded)."""
 
-    def __init__(self, dtype, n, c, h, w, device=0, layouts=None, algos=None, params=True):
+    def __init__(self, dtype, n, c, h, w, device=0, layouts=None, algos=None, params=True, dtypes=None):
         self.lib = N.lib()
         self.dtype = N.DTYPE[dtype] if isinstance(dtype, str) else dtype
         self.dtype_name = {v: k for k, v in N.DTYPE.items()}[self.dtype]
@@ -46,7 +46,11 @@ class Graph:
             self.set_option(N.OPT_ALGOS, mask)
         if not params:
             self.set_option(N.OPT_PARAMS, 0)
+        if dtypes is not None:
+            mask = sum(1 << (N.DTYPE[d] if isinstance(d, str) else d) for d in dtypes)
+            self.set_option(N.OPT_DTYPES, mask)
         self.in_shape = (n, c, h, w)
+        self.in_shapes = [self.in_shape]
 
     # ---------------------------------------------------------------- lifetime
     def close(self):
@@ -107,9 +111,27 @@ class Graph:
         k = weight.shape[0]
         return self._add(N.LayerDesc(N.L_FC, k, 1, 1, 1, 0, 1, N.ACT[act]), [inp], weight, bias)
 
+    def add_input(self, c, h, w):
+        """A further net input N x c x h x w (run dtype, NCHW); returns its layer id."""
+        out = ctypes.c_int32()
+        N.check(self.lib.sn_add_input(self._g, c, h, w, ctypes.byref(out)))
+        self.in_shapes.append((self.in_shape[0], c, h, w))
+        return out.value
+
+    def mark_output(self, layer):
+        """Make ``layer`` the next net output (default: the last layer only)."""
+        N.check(self.lib.sn_mark_output(self._g, layer))
+
+    def num_io(self):
+        a, b = ctypes.c_int32(), ctypes.c_int32()
+        N.check(self.lib.sn_num_io(self._g, ctypes.byref(a), ctypes.byref(b)))
+        return a.value, b.value
+
     def add_spec(self, layer, weight=None, bias=None):
         """Add one layer given as a ``workloads`` spec dict."""
         t = layer["type"]
+        if t == "input":
+            return self.add_input(*layer["chw"])
         if t == "conv":
             res = layer["in"][1] if len(layer["in"]) > 1 else None
             return self.add_conv(layer["in"][0], weight, bias, layer["stride"], layer["pad"],
@@ -193,7 +215,8 @@ class Graph:
             d = N.RoutineDesc()
             N.check(self.lib.sn_routine_info(self._g, layer, i, ctypes.byref(d)))
             out.append({"id": d.id, "layout": d.layout, "algo": d.algo, "param": d.param,
-                        "cost_ns": d.cost_ns, "name": d.name.decode()})
+                        "dtype": d.dtype, "schema": d.schema, "cost_ns": d.cost_ns,
+                        "name": d.name.decode()})
         return out
 
     def layer_shape(self, layer):
@@ -214,11 +237,27 @@ class Graph:
         import torch
         return {N.F32: torch.float32, N.F16: torch.float16, N.BF16: torch.bfloat16}[self.dtype]
 
-    def empty_output(self):
+    def empty_output(self, shape=None):
         import torch
-        n, c, h, w = self.output_shape()
+        n, c, h, w = self.output_shape() if shape is None else shape
         shape = (n, c) if h == 1 and w == 1 else (n, c, h, w)
         return torch.empty(shape, dtype=self._torch_dtype(), device=f"cuda:{self.device}")
+
+    def run_mimo(self, xs, outs=None, output_layers=None, stream=None):
+        """Inference of a net with several inputs / outputs: ``xs`` are the
+        NCHW device tensors of the net inputs in order; returns the outputs
+        (``output_layers``: their layer ids, for the shapes)."""
+        n_in, n_out = self.num_io()
+        assert len(xs) == n_in
+        if outs is None:
+            assert output_layers is not None and len(output_layers) == n_out
+            outs = [self.empty_output(self.layer_shape(l)) for l in output_layers]
+        for x, shp in zip(xs, self.in_shapes):
+            assert x.is_contiguous() and x.dtype == self._torch_dtype() and tuple(x.shape) == tuple(shp)
+        pin = (ctypes.c_void_p * n_in)(*[x.data_ptr() for x in xs])
+        pout = (ctypes.c_void_p * n_out)(*[o.data_ptr() for o in outs])
+        N.check(self.lib.sn_run_mimo(self._g, pin, n_in, pout, n_out, _stream_ptr(stream)))
+        return outs
 
     def run(self, x, out=None, stream=None):
         """Enqueue inference of NCHW device tensor x; returns the output tensor."""
@@ -274,16 +313,19 @@ def to_device(arr, dtype, device=0):
     return torch.from_numpy(a).to(f"cuda:{device}")
 
 
-def build_from_spec(spec, tensors=None, device=0, layouts=None, algos=None, params=True):
+def build_from_spec(spec, tensors=None, device=0, layouts=None, algos=None, params=True, dtypes=None):
     """Create a graph from a ``workloads`` net spec.  ``tensors`` holds the
     generated weights (``workloads.generate``); host-only graphs (device -1)
-    may pass None and get zero weights of the right shapes."""
+    may pass None and get zero weights of the right shapes.  ``dtypes``: the
+    element types routines may compute in (default: the spec's dtype only);
+    a spec's ``outputs`` list marks the net outputs."""
     from workloads import weight_shapes
     n = spec["batch"]
     c, h, w = spec["in_chw"]
     g = Graph(spec["dtype"], n, c, h, w, device=device,
               layouts=spec.get("layouts") if layouts is None else layouts,
-              algos=spec.get("algos") if algos is None else algos, params=params)
+              algos=spec.get("algos") if algos is None else algos, params=params,
+              dtypes=spec.get("dtypes") if dtypes is None else dtypes)
     shapes = weight_shapes(spec)
     for i, layer in enumerate(spec["layers"]):
         wt = bt = None
@@ -294,4 +336,6 @@ def build_from_spec(spec, tensors=None, device=0, layouts=None, algos=None, para
                 wt = np.zeros(shapes[i][0], dtype=_STORAGE[g.dtype])
                 bt = np.zeros(shapes[i][1], dtype=np.float32)
         g.add_spec(layer, wt, bt)
+    for o in spec.get("outputs", []):
+        g.mark_output(o)
     return g

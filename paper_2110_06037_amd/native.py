@@ -25,7 +25,8 @@ ALGO_NAME = {v: k for k, v in ALGO.items()}
 L_INPUT, L_CONV2D, L_MAXPOOL, L_GAP, L_ADD, L_FC, L_OUTPUT = range(7)
 ACT = {"none": 0, "relu": 1, "relu6": 2}
 SELECT_DPRS, SELECT_FIXED = 0, 1
-OPT_LAYOUTS, OPT_ALGOS, OPT_PARAMS, OPT_HIPGRAPH, OPT_SEED, OPT_FLUSH, OPT_KEEP = range(7)
+OPT_LAYOUTS, OPT_ALGOS, OPT_PARAMS, OPT_HIPGRAPH, OPT_SEED, OPT_FLUSH, OPT_KEEP, OPT_DTYPES = range(8)
+DTYPE_NAME = {v: k for k, v in DTYPE.items()}
 
 STATUS = {0: "SN_OK", -1: "SN_E_INVALID", -2: "SN_E_SHAPE", -3: "SN_E_STATE",
           -4: "SN_E_UNSUPPORTED", -5: "SN_E_DEVICE", -6: "SN_E_NOMEM", -7: "SN_E_INTERNAL"}
@@ -45,7 +46,8 @@ class LayerDesc(ctypes.Structure):
 
 class RoutineDesc(ctypes.Structure):
     _fields_ = [("id", ctypes.c_int32), ("layout", ctypes.c_int32), ("algo", ctypes.c_int32),
-                ("param", ctypes.c_int32), ("cost_ns", ctypes.c_int64), ("name", ctypes.c_char * 64)]
+                ("param", ctypes.c_int32), ("dtype", ctypes.c_int32), ("schema", ctypes.c_int32),
+                ("cost_ns", ctypes.c_int64), ("name", ctypes.c_char * 64)]
 
 
 # exported functions: name -> (restype, argtypes)
@@ -58,6 +60,10 @@ SIGNATURES = {
     "sn_set_option": (ctypes.c_int, [_P, _I32, ctypes.c_int64]),
     "sn_add_layer": (ctypes.c_int, [_P, ctypes.POINTER(LayerDesc), _I32P, _I32, _P,
                                     ctypes.POINTER(ctypes.c_float), _I32P]),
+    "sn_add_input": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32P]),
+    "sn_mark_output": (ctypes.c_int, [_P, _I32]),
+    "sn_num_io": (ctypes.c_int, [_P, _I32P, _I32P]),
+    "sn_run_mimo": (ctypes.c_int, [_P, ctypes.POINTER(_P), _I32, ctypes.POINTER(_P), _I32, _P]),
     "sn_profile": (ctypes.c_int, [_P, _I32, _I32, _P]),
     "sn_select_path": (ctypes.c_int, [_P, _I32, _I32, _I32]),
     "sn_set_path": (ctypes.c_int, [_P, _I32P, _I32]),

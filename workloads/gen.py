@@ -2,7 +2,7 @@
 
 Recipe: ``numpy.random.default_rng(seed)`` (PCG64).  Draw order: the input
 tensor first, then for every layer in insertion order its weight, then its
-bias.  Inputs are N(0, 1) or U[-1, 1] as the spec says; convolution and FC
+bias (a further net input layer draws its tensor there instead).  Inputs are N(0, 1) or U[-1, 1] as the spec says; convolution and FC
 weights are He-normal, std = sqrt(2 / fan_in) with fan_in = (C_in / groups)
 * R * S (FC: in_features), untruncated; biases are U[-0.1, 0.1].  Values are
 drawn in float64, then materialised in the run dtype by round-to-nearest-even
@@ -79,6 +79,9 @@ def weight_shapes(spec):
     out = []
     for layer in spec["layers"]:
         t = layer["type"]
+        if t == "input":
+            out.append(None)
+            continue
         cin = ch[layer["in"][0]]
         if t == "conv":
             g = layer["groups"]
@@ -95,17 +98,27 @@ def generate(spec, seed=None):
 
     Returns a dict with ``x`` (N x C x H x W, stored dtype), ``w`` and ``b``
     (lists indexed by layer id - 1; None for layers without weights; weights in
-    the stored dtype, biases float32)."""
+    the stored dtype, biases float32) and ``inputs`` ({layer id: tensor} of the
+    further net inputs)."""
     dtype = spec["dtype"]
     rng = np.random.default_rng(spec.get("seed", 0) if seed is None else seed)
     n = spec["batch"]
     c, h, w = spec["in_chw"]
-    if spec["input_dist"] == "normal":
-        x = rng.standard_normal((n, c, h, w))
-    else:
-        x = rng.uniform(-1.0, 1.0, (n, c, h, w))
+
+    def draw_input(shape):
+        if spec["input_dist"] == "normal":
+            return rng.standard_normal(shape)
+        return rng.uniform(-1.0, 1.0, shape)
+
+    x = draw_input((n, c, h, w))
     ws, bs = [], []
-    for layer, shp in zip(spec["layers"], weight_shapes(spec)):
+    extra = {}
+    for i, (layer, shp) in enumerate(zip(spec["layers"], weight_shapes(spec)), start=1):
+        if layer["type"] == "input":
+            extra[i] = materialise(draw_input((n, *layer["chw"])), dtype)
+            ws.append(None)
+            bs.append(None)
+            continue
         if shp is None:
             ws.append(None)
             bs.append(None)
@@ -116,7 +129,7 @@ def generate(spec, seed=None):
         bt = rng.uniform(-0.1, 0.1, k)
         ws.append(materialise(wt, dtype))
         bs.append(bt.astype(np.float32))
-    return {"x": materialise(x, dtype), "w": ws, "b": bs, "dtype": dtype}
+    return {"x": materialise(x, dtype), "w": ws, "b": bs, "inputs": extra, "dtype": dtype}
 
 
 def random_tensor(shape, dtype, seed, dist="uniform", scale=1.0):

@@ -17,6 +17,9 @@ paper's auxiliary input layer, Sec. IV-E); layers 1..n are listed in
 * ``{"type": "add", "in": [a, b], "act": ...}`` -- residual merge.
 * ``{"type": "fc", "in": [j], "k": out, "act": ...}`` -- dense layer,
   y = act(W x + b) on an N x C x 1 x 1 input ("act" optional, default none).
+* ``{"type": "input", "in": [], "chw": [C, H, W]}`` -- a further net input
+  (batch N of the spec); ``spec["outputs"]`` (optional) lists the net
+  outputs in order, else the last layer is the one output (Sec. IV-E).
 
 The shapes follow the model families the paper evaluates (Sec. V: ResNet50,
 MobileNetV2, VGG16; ResNet-18 and a tiny chain are smaller members of the
@@ -188,6 +191,27 @@ def vgg16(batch=1, dtype="bf16", hw=224):
             "layouts": ["NCHW", "NHWC", "NC8HW8"], "algos": ["direct", "igemm", "winograd"]}
 
 
+def net_d(batch=2, dtype="bf16"):
+    """A two-input, two-output net (the multi-input/multi-output case of the
+    auxiliary layers, Sec. IV-E): input 0 (3 x 20 x 20) and input 1
+    (8 x 10 x 10) each pass a convolution, meet in an add, and the net ends
+    in two heads -- a classifier after the merge and a map computed from the
+    second input's branch."""
+    L = [
+        _conv(0, 16, 3, 2, 1, act="relu"),                    # 1: input 0 -> 16 x 10 x 10
+        {"type": "input", "in": [], "chw": [8, 10, 10]},     # 2: input 1
+        _conv(2, 16, 3, 1, 1, act="relu"),                    # 3: input 1 -> 16 x 10 x 10
+        {"type": "add", "in": [1, 3], "act": "relu"},          # 4: merge
+        _conv(4, 24, 3, 1, 1, act="relu"),                    # 5
+        {"type": "gap", "in": [5]},                           # 6
+        {"type": "fc", "in": [6], "k": 10},                   # 7: output 0
+        _conv(3, 12, 1, 1, 0),                                # 8: output 1 (12 x 10 x 10)
+    ]
+    return {"name": f"net_d_bs{batch}_{dtype}", "dtype": dtype, "batch": batch, "in_chw": [3, 20, 20],
+            "input_dist": "uniform", "seed": 0, "layers": L, "outputs": [7, 8],
+            "layouts": ["NCHW", "NHWC", "NC8HW8"], "algos": ["direct", "igemm", "winograd"]}
+
+
 def with_batch(spec, batch):
     out = copy.deepcopy(spec)
     out["batch"] = batch
@@ -210,7 +234,8 @@ def all_configs():
 
 
 def edges(spec):
-    """Edge list (j, i) of the layer DAG, layer 0 being the input."""
+    """Edge list (j, i) of the layer DAG, layer 0 being the input (further
+    input layers have no data edge)."""
     out = []
     for i, layer in enumerate(spec["layers"], start=1):
         for j in layer["in"]:
@@ -223,7 +248,9 @@ def channels(spec):
     ch = [spec["in_chw"][0]]
     for layer in spec["layers"]:
         t = layer["type"]
-        if t in ("conv", "fc"):
+        if t == "input":
+            ch.append(layer["chw"][0])
+        elif t in ("conv", "fc"):
             ch.append(layer["k"])
         else:
             ch.append(ch[layer["in"][0]])
