@@ -79,13 +79,13 @@ KDIR = os.path.join(ROOT, "paper_2110_06037_amd", "csrc", "kernels")
 # when any of them changes)
 KERNEL_SOURCES = {
     "add_kernel": ("misc.hip", "kcommon.hpp"),
-    "igemm_dma_kernel": ("conv.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
-    "igemm_kernel": ("conv.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
+    "igemm_dma_kernel": ("igemm.hpp", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
+    "igemm_kernel": ("igemm.hpp", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
     "conv3x3_patch_kernel": ("conv_patch.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
     "conv1x1_stream_kernel": ("conv1x1_stream.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
 }
-ALL_KERNEL_SOURCES = ("conv.hip", "conv1x1_stream.hip", "conv_patch.hip", "conv_smallc.hip", "convert.hip", "fc.hip",
-                      "misc.hip",
+ALL_KERNEL_SOURCES = ("conv.hip", "conv_igemm_bf16.hip", "conv_igemm_f16.hip", "conv1x1_stream.hip", "conv_patch.hip",
+                      "conv_smallc.hip", "convert.hip", "dwconv.hip", "fc.hip", "igemm.hpp", "misc.hip",
                       "gemm_common.hpp",
                       "kcommon.hpp", "launch.hpp")
 

@@ -90,10 +90,27 @@ __device__ __forceinline__ V8<T> zero8() {
   return r;
 }
 
+// Sum over the 64 lanes of a wave, in every lane.  Within each row of 16
+// lanes the partial sums move by DPP (data-parallel primitives: the operand
+// of a VALU op read from another lane of the row): XOR 1 and XOR 2 as quad
+// permutations, then the half-row mirror (lane i takes lane 7 - i of its
+// 8-lane half, which holds the other quad's sum) and the row mirror (lane i
+// takes lane 15 - i, the other half's sum).  The two rows of each 32-lane
+// half combine through a swizzle with XOR 16, and the halves through two
+// scalar lane reads.
+template <int CTRL>
+__device__ __forceinline__ float dpp_take(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
+  v += dpp_take<0xB1>(v);   // quad_perm [1, 0, 3, 2]: XOR 1
+  v += dpp_take<0x4E>(v);   // quad_perm [2, 3, 0, 1]: XOR 2
+  v += dpp_take<0x141>(v);  // row_half_mirror
+  v += dpp_take<0x140>(v);  // row_mirror
+  v += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));  // XOR 16
+  const int b = __builtin_bit_cast(int, v);
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 0)) +
+         __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 32));
 }
 
 }  // namespace k

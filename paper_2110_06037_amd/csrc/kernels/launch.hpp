@@ -79,7 +79,10 @@ struct PatchCfg {
   X(13, 32, 16, 4, 1, 2, 3, 256) \
   X(13, 32, 16, 4, 2, 1, 3, 256) \
   X(7, 32, 16, 4, 1, 2, 3, 288)  \
-  X(7, 32, 64, 4, 1, 2, 2, 256)
+  X(7, 32, 64, 4, 1, 2, 2, 256)  \
+  X(25, 64, 64, 4, 1, 2, 2, 576) \
+  X(13, 64, 32, 4, 1, 2, 2, 288) \
+  X(7, 64, 16, 4, 1, 2, 2, 288)
 bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
                       int fmt, int pwt, int prows);
 void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& a, hipStream_t st);
@@ -124,6 +127,9 @@ void add_act(int dtype, const void* a, const void* b, void* y, int64_t n, int ac
 void fc_direct(int dtype, const void* x, int n, int cin, int cin_s, const void* w, int c8,
                const float* bias, void* y, int kout, int kout_s, int act, hipStream_t st);
 void convert(int dtype, const void* x, const TDesc& xd, void* y, const TDesc& yd, hipStream_t st);
+// 16-byte vector layout converters for 16-bit tensors (convert.hip); false
+// when the shape needs the element-wise converter
+bool convert_vec16(const void* x, const TDesc& xd, void* y, const TDesc& yd, hipStream_t st);
 // schema conversion: layout and element type (sdt -> ddt) at once; equal
 // dtypes fall back to convert (see convert.hip)
 void convert_cast(int sdt, const void* x, const TDesc& xd, int ddt, void* y, const TDesc& yd, hipStream_t st);

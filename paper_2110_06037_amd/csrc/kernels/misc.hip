@@ -138,8 +138,11 @@ void maxpool(int dtype, const void* x, const TDesc& xd, void* y, const TDesc& yd
 }
 
 // ------------------------------------------------------------------ global average pooling
-// NCHW: one wave reduces one (n, c) plane with a butterfly of lane shuffles.
-// NHWC / NC8: one thread per (n, stored channel), lanes along channels.
+// NCHW: one wave reduces one (n, c) plane; the lanes' partial sums meet in a
+// DPP reduction (wave_sum).
+// NHWC / NC8: a workgroup takes 64 stored channels of one image; its 4 waves
+// sum interleaved quarters of the pixels with lanes along channels
+// (coalesced), and the 4 partial sums meet in LDS.
 template <typename T, int L>
 __global__ __launch_bounds__(256) void gap_kernel(const T* __restrict__ x, T* __restrict__ y, int N,
                                                   int C, int HW, int Cs) {
@@ -147,34 +150,39 @@ __global__ __launch_bounds__(256) void gap_kernel(const T* __restrict__ x, T* __
   if constexpr (L == NCHW) {
     const long long plane = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
-    if (plane >= (long long)N * C) return;
+    if (plane >= (long long)N * C) return;  // wave-uniform
     const T* xp = x + plane * HW;
     float s = 0.f;
     for (int i = lane; i < HW; i += 64) s += to_f(xp[i]);
     s = wave_sum(s);
     if (lane == 0) y[plane] = from_f<T>(s * inv);
   } else {
-    const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (idx >= (long long)N * Cs) return;
-    const int c = (int)(idx % Cs);
-    const int n = (int)(idx / Cs);
+    __shared__ float part[4][64];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int n = blockIdx.y, c = blockIdx.x * 64 + lane;
     float s = 0.f;
-    if constexpr (L == NC8) {
-      const T* xp = x + ((long long)n * (Cs >> 3) + (c >> 3)) * HW * 8 + (c & 7);
-#pragma unroll 8
-      for (int i = 0; i < HW; ++i) s += to_f(xp[(long long)i * 8]);
-    } else {
-      const T* xp = x + (long long)n * HW * Cs + c;
-#pragma unroll 8
-      for (int i = 0; i < HW; ++i) s += to_f(xp[(long long)i * Cs]);
+    if (c < Cs) {
+      if constexpr (L == NC8) {
+        const T* xp = x + ((size_t)n * (Cs >> 3) + (c >> 3)) * HW * 8 + (c & 7);
+#pragma unroll 4
+        for (int i = wv; i < HW; i += 4) s += to_f(xp[(size_t)i * 8]);
+      } else {
+        const T* xp = x + (size_t)n * HW * Cs + c;
+#pragma unroll 4
+        for (int i = wv; i < HW; i += 4) s += to_f(xp[(size_t)i * Cs]);
+      }
     }
-    y[idx] = from_f<T>(s * inv);  // [N][Cs]: N x C x 1 x 1 in every layout
+    part[wv][lane] = s;
+    __syncthreads();
+    if (wv == 0 && c < Cs)
+      y[(size_t)n * Cs + c] = from_f<T>(((part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane])) * inv);
   }
 }
 
 template <typename T>
 static void gap_t(const void* x, const TDesc& xd, void* y, const TDesc& yd, hipStream_t s) {
   check(xd.layout == yd.layout && yd.h == 1 && yd.w == 1, "gap output is N x C x 1 x 1");
+  check(xd.n <= 65535 && (long long)xd.n * xd.cs * xd.h * xd.w < (1ll << 40), "gap grid");
   const int HW = xd.h * xd.w;
   const T* xp = reinterpret_cast<const T*>(x);
   T* yp = reinterpret_cast<T*>(y);
@@ -184,11 +192,11 @@ static void gap_t(const void* x, const TDesc& xd, void* y, const TDesc& yd, hipS
                          xp, yp, xd.n, xd.c, HW, xd.cs);
       break;
     case NHWC:
-      SN_LAUNCH((gap_kernel<T, NHWC>), dim3(blocks((long long)xd.n * xd.cs)), dim3(256), 0, s,
+      SN_LAUNCH((gap_kernel<T, NHWC>), dim3((xd.cs + 63) / 64, xd.n), dim3(256), 0, s,
                          xp, yp, xd.n, xd.c, HW, xd.cs);
       break;
     case NC8:
-      SN_LAUNCH((gap_kernel<T, NC8>), dim3(blocks((long long)xd.n * xd.cs)), dim3(256), 0, s,
+      SN_LAUNCH((gap_kernel<T, NC8>), dim3((xd.cs + 63) / 64, xd.n), dim3(256), 0, s,
                          xp, yp, xd.n, xd.c, HW, xd.cs);
       break;
   }
@@ -230,7 +238,7 @@ void add_act(int dtype, const void* a, const void* b, void* y, int64_t n, int ac
 // ------------------------------------------------------------------ FC (dot products)
 // One wave per output feature k: lanes stride the input features with 8-wide
 // loads, the batch is processed in groups of 4 sharing each weight load, and
-// each dot product finishes with a lane-shuffle reduction.
+// each dot product finishes with a DPP reduction (wave_sum).
 template <typename T>
 __global__ __launch_bounds__(256) void fc_kernel(const T* __restrict__ x, int N, int cin, int cin_s,
                                                  const T* __restrict__ w, int c8,
@@ -425,6 +433,12 @@ static void convert_e(const void* xv, const TDesc& xd, void* yv, const TDesc& yd
   const E* x = reinterpret_cast<const E*>(xv);
   E* y = reinterpret_cast<E*>(yv);
   const int HW = xd.h * xd.w;
+  if constexpr (sizeof(E) == 2) {
+    // C <= 8 into NHWC keeps its 8-pixel kernel below; the rest of the
+    // 16-bit pairs take the vector converters when the shape allows
+    const bool smallc_nhwc = xd.c <= 8 && yd.layout == NHWC && xd.layout == NCHW;
+    if (!smallc_nhwc && convert_vec16(xv, xd, yv, yd, s)) return;
+  }
   if ((xd.layout == NCHW && yd.layout == NHWC) || (xd.layout == NHWC && yd.layout == NCHW)) {
     if constexpr (sizeof(E) == 2) {
       if (xd.c <= 8 && yd.layout == NHWC && HW % 8 == 0 && (long long)xd.n * HW < (1ll << 31)) {
