@@ -41,7 +41,9 @@ def layer_kind(spec, i):
 
 
 def layer_work(spec, g, i, routine):
-    """(category, flops, algorithmic bytes) of layer i (1-based) for a routine."""
+    """(category, flops, algorithmic bytes) of layer i (1-based) for a routine.
+    The bytes follow the formula input + filters + output (+ residual); see
+    bytes_needed for the bytes a strided 1x1 convolution actually reads."""
     layer = spec["layers"][i - 1]
     es = 4 if spec["dtype"] == "f32" else 2
     n, k, p, q = g.layer_shape(i)
@@ -73,6 +75,20 @@ def layer_work(spec, g, i, routine):
     return t, 0, 0
 
 
+def bytes_needed(spec, g, i, routine):
+    """Algorithmic bytes with the input counted as the pixels the layer
+    reads: a 1x1 convolution without padding at stride s reads one input
+    pixel in s x s (the formula of layer_work counts the whole input)."""
+    _, _, byt = layer_work(spec, g, i, routine)
+    layer = spec["layers"][i - 1]
+    if layer["type"] == "conv" and layer["r"] == 1 and layer["s"] == 1 and layer["pad"] == 0 and layer["stride"] > 1:
+        es = 4 if spec["dtype"] == "f32" else 2
+        n, k, p, q = g.layer_shape(i)
+        _, c, h, w = g.layer_shape(layer["in"][0])
+        byt -= es * n * c * (h * w - p * q)
+    return byt
+
+
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_resnet50_bs32_bf16.json")
 KDIR = os.path.join(ROOT, "paper_2110_06037_amd", "csrc", "kernels")
 # sources each dominant kernel is built from (its traffic summary goes stale
@@ -83,6 +99,8 @@ KERNEL_SOURCES = {
     "igemm_kernel": ("igemm.hpp", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
     "conv3x3_patch_kernel": ("conv_patch.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
     "conv1x1_stream_kernel": ("conv1x1_stream.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
+    "conv_smallc_kernel": ("conv_smallc.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
+    "dw3x3_kernel": ("dwconv.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
 }
 ALL_KERNEL_SOURCES = ("conv.hip", "conv_igemm_bf16.hip", "conv_igemm_f16.hip", "conv1x1_stream.hip", "conv_patch.hip",
                       "conv_smallc.hip", "convert.hip", "dwconv.hip", "fc.hip", "igemm.hpp", "misc.hip",
@@ -91,6 +109,7 @@ ALL_KERNEL_SOURCES = ("conv.hip", "conv_igemm_bf16.hip", "conv_igemm_f16.hip", "
 
 
 def kernel_source_hash(ksub=None):
+    """Hash of the sources a kernel (by a part of its symbol) is built from."""
     import hashlib
     h = hashlib.sha256()
     files = next((v for k, v in KERNEL_SOURCES.items() if ksub and k in ksub), ALL_KERNEL_SOURCES)
@@ -100,21 +119,32 @@ def kernel_source_hash(ksub=None):
     return h.hexdigest()[:16]
 
 
-def _traffic_entries():
+def _traffic_summary(path=TRAFFIC_FILE):
     try:
-        with open(TRAFFIC_FILE) as f:
-            return json.load(f).get("entries", [])
-    except (OSError, ValueError, AttributeError):
-        return []
+        with open(path) as f:
+            return json.load(f)
+    except (OSError, ValueError):
+        return {}
 
 
-def traffic_for(routine):
-    """HBM bytes per launch of `routine` from the committed PMC summaries, or None
-    when there is none for it or its kernel sources changed since it was taken."""
-    for t in _traffic_entries():
-        if t.get("routine") == routine and t.get("source_hash") == kernel_source_hash(t.get("kernel_symbol_part")):
-            return t.get("bytes_per_launch")
-    return None
+def traffic_for_layers(layers, routine, summary=None):
+    """HBM bytes per launch of `routine` averaged over `layers` from the
+    committed per-layer PMC summary: only when the summary holds every one of
+    those layers run by this same routine, with kernel sources unchanged
+    since the counters were taken; else (None, reason)."""
+    summary = _traffic_summary() if summary is None else summary
+    by_layer = {e["layer"]: e for e in summary.get("layers", [])}
+    tot = 0
+    for i in layers:
+        e = by_layer.get(i)
+        if e is None or e.get("routine") != routine:
+            return None, f"layer {i} was profiled with another routine (or not at all)"
+        if e.get("source_hash") != kernel_source_hash(e.get("kernels", [""])[0]):
+            return None, f"the kernel sources of layer {i} changed since its counters were taken"
+        if e.get("bytes") is None:
+            return None, "no calibration"
+        tot += e["bytes"]
+    return tot // max(1, len(layers)), None
 
 
 def _pmc_rows(d):
@@ -126,37 +156,55 @@ def _pmc_rows(d):
     return rows
 
 
-def summarize_pmc(fetch_dir, write_dir, routine, ksub, out, calib_mib):
-    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the DP-path igemm launches,
-    scaled by what the counters read for a plain device copy of known size."""
-    res = {}
+def summarize_pmc(fetch_dir, write_dir, pass_file, out, calib_mib):
+    """Per-layer HBM traffic of a pinned path from two rocprofv3 --pmc runs of
+    `bench.py --pmc-pass` (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch):
+    the library's kernels (namespace sn::k) of the run are the warm-up and
+    timed steps in order, each step's launches attributed to layers by the
+    plan's launch list; counters of the timed steps are averaged per launch,
+    summed per layer and scaled by what each counter reads for a device copy
+    of known size."""
+    with open(pass_file) as f:
+        info = json.load(f)
+    launch_layer = info["launch_layers"]
+    L = len(launch_layer)
+    per_counter = {}
+    calib = {}
+    kernels = None
     for name, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = [r for r in _pmc_rows(d) if r["Counter_Name"] == name]
-        # the calibration copy is by far the largest copy dispatch of the run
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        ours = [r for r in rows if r["Kernel_Name"].startswith("_ZN2sn1k") or "sn::k::" in r["Kernel_Name"]]
+        steps = len(ours) // L
+        if steps * L != len(ours) or steps < info["warmup"] + info["steps"]:
+            raise SystemExit(f"{name}: {len(ours)} library dispatches, not a whole number of {L}-launch steps")
         copy = [float(r["Counter_Value"]) for r in rows if "copy" in r["Kernel_Name"].lower()]
-        conv = [float(r["Counter_Value"]) for r in rows if ksub in r["Kernel_Name"]]
-        known_kib = calib_mib * 1024.0
-        scale = known_kib / max(copy) if copy and calib_mib else None
-        res[name] = {"dispatches": len(conv), "mean_kib": sum(conv) / max(1, len(conv)),
-                     "copy_kib": max(copy) if copy else None, "scale": scale}
-    f, w = res["FETCH_SIZE"], res["WRITE_SIZE"]
-    per = None
-    if f["scale"] and w["scale"]:
-        per = int((f["mean_kib"] * f["scale"] + w["mean_kib"] * w["scale"]) * 1024)
-    t = {"routine": routine, "kernel_symbol_part": ksub, "source_hash": kernel_source_hash(ksub),
-         "bytes_per_launch": per,
-         "counters": res, "calibration": f"device copy of {calib_mib} MiB (read and write)"}
-    # one entry per routine: replace this routine's entry, keep the others
-    entries = []
-    try:
-        with open(out) as fh:
-            entries = json.load(fh).get("entries", [])
-    except (OSError, ValueError, AttributeError):
-        pass
-    entries = [e for e in entries if e.get("routine") != routine] + [t]
+        calib[name] = calib_mib * 1024.0 / max(copy) if copy and calib_mib else None
+        timed = ours[(steps - info["steps"]) * L:]
+        per_launch = [0.0] * L
+        for k, r in enumerate(timed):
+            per_launch[k % L] += float(r["Counter_Value"]) / info["steps"]
+        per_counter[name] = per_launch
+        kernels = [timed[k]["Kernel_Name"] for k in range(L)]
+    layers = []
+    for i, rname in enumerate(info["routines"]):
+        idx = [k for k in range(L) if launch_layer[k] == i]
+        if not idx:
+            continue
+        kib_f = sum(per_counter["FETCH_SIZE"][k] for k in idx)
+        kib_w = sum(per_counter["WRITE_SIZE"][k] for k in idx)
+        ks = [kernels[k] for k in idx]
+        ok = calib["FETCH_SIZE"] and calib["WRITE_SIZE"]
+        layers.append({"layer": i, "routine": rname, "launches": len(idx), "kernels": ks,
+                       "fetch_kib": round(kib_f, 1), "write_kib": round(kib_w, 1),
+                       "bytes": int((kib_f * calib["FETCH_SIZE"] + kib_w * calib["WRITE_SIZE"]) * 1024) if ok else None,
+                       "source_hash": kernel_source_hash(ks[0])})
+    res = {"workload": info["workload"], "steps": info["steps"], "calibration":
+           {"copy_mib": calib_mib, "fetch_scale": calib["FETCH_SIZE"], "write_scale": calib["WRITE_SIZE"]},
+           "layers": layers}
     with open(out, "w") as fh:
-        json.dump({"entries": entries}, fh, indent=1)
-    print(json.dumps(t))
+        json.dump(res, fh, indent=1)
+    print(json.dumps({"layers": len(layers), "calibration": res["calibration"]}))
 
 
 def _mask_name(m):
@@ -243,8 +291,10 @@ def step_stats(g, x, out, n):
             "std": round(statistics.pstdev(ms), 4), "min": round(min(ms), 4), "runs": n}
 
 
-def cpu_baseline(spec, t, budget_s):
-    """The oracle (naive float64, OpenMP) on the first images of the batch."""
+def cpu_baseline(spec, t, budget_s, storage="dtype"):
+    """The oracle (naive float64, OpenMP) on the first images of the batch,
+    with every layer output rounded to the run dtype (storage "dtype", the
+    parity mode) or exact (storage "f64")."""
     import numpy as np
     from oracle import numeric as O
     from workloads import to_f64, with_batch
@@ -256,7 +306,7 @@ def cpu_baseline(spec, t, budget_s):
     while done < spec["batch"]:
         one = dict(d)
         one["x"] = d["x"][done:done + 1]
-        O.forward(with_batch(spec, 1), one, storage="dtype")
+        O.forward(with_batch(spec, 1), one, storage=storage)
         done += 1
         if time.perf_counter() - t0 > budget_s:
             break
@@ -264,7 +314,9 @@ def cpu_baseline(spec, t, budget_s):
     return {"value": round(done / el, 4), "unit": "img/s", "cores": O.num_threads(),
             "kind": "oracle",
             "sample": f"{done} image(s) of the batch-{spec['batch']} {spec['name'].split('_')[0]} input, "
-                      f"naive float64 direct convolution with {spec['dtype']} storage rounding, {el:.1f} s"}
+                      f"naive float64 direct convolution, "
+                      + (f"{spec['dtype']} storage rounding" if storage == "dtype" else "exact float64 storage")
+                      + f", {el:.1f} s"}
 
 
 def main():
@@ -297,11 +349,17 @@ def main():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed region, run one device copy of this size "
                          "(a known-size kernel for scaling PMC byte counters)")
-    ap.add_argument("--summarize-pmc", nargs=5,
-                    metavar=("FETCH_DIR", "WRITE_DIR", "ROUTINE", "KERNEL_SUBSTR", "OUT"),
-                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this script "
-                         "into the traffic summary OUT for the dispatches whose kernel name "
-                         "contains KERNEL_SUBSTR (the routine's kernel symbol), and exit")
+    ap.add_argument("--path-out", default=None, help="write the selected routine path here")
+    ap.add_argument("--path-in", default=None,
+                    help="run this routine path (from --path-out) instead of selecting one")
+    ap.add_argument("--pmc-pass", default=None, metavar="PASS_JSON",
+                    help="run only warmup + steps of the path (then the calibration copy) for "
+                         "counter collection, write the launch list to PASS_JSON, and exit")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "PASS_JSON", "OUT"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --pmc-pass into "
+                         "the per-layer traffic summary OUT, and exit")
+    ap.add_argument("--compare-rounds", type=int, default=4,
+                    help="alternating rounds timing the DPRS path against the best fixed paths")
     args = ap.parse_args()
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, calib_mib=args.calib_copy_mib)
@@ -342,15 +400,49 @@ def main():
     if args.costs_out:
         with open(args.costs_out, "w") as f:
             json.dump(g.costs(), f)
+    dp_ids, dp_model_ns = g.path()
+    pinned = None
+    if args.path_in:
+        with open(args.path_in) as f:
+            pinned = json.load(f)["path"]
+        args.integrated_reps = 0
     if args.tune_only:
+        if args.integrated_reps > 0:
+            g.profile_integrated(warmup=2, reps=args.integrated_reps)
+        if args.path_out:
+            with open(args.path_out, "w") as f:
+                json.dump({"path": g.path()[0], "routines": [g.routines(i)[r]["name"] for i, r in
+                                                              enumerate(g.path()[0])]}, f)
         g.close()
         return
-    dp_ids, dp_model_ns = g.path()
     x = to_dev(t["x"], args.dtype)
     out = g.empty_output()
+    if args.pmc_pass:
+        # counter collection: the pinned path's steps and nothing else (the
+        # library's dispatches are then whole steps in order), then one copy
+        # of known size for scaling the byte counters
+        if pinned:
+            g.set_path(pinned)
+        for _ in range(args.warmup + args.steps):
+            g.run(x, out)
+        torch.cuda.synchronize()
+        if args.calib_copy_mib:
+            src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
+            dst = torch.zeros_like(src)
+            dst.copy_(src)
+            torch.cuda.synchronize()
+        ids = g.path()[0]
+        with open(args.pmc_pass, "w") as f:
+            json.dump({"workload": spec["name"], "warmup": args.warmup, "steps": args.steps,
+                       "routines": [g.routines(i)[r]["name"] for i, r in enumerate(ids)],
+                       "launch_layers": g.plan_launches()}, f)
+        g.close()
+        return
 
     sec_dp = time_steps(g, x, out, args.steps, args.warmup)
     log(f"[bench] DPRS path: {sec_dp * 1e3:.3f} ms/step, {args.batch / sec_dp:.1f} img/s")
+    if pinned:
+        g.set_path(pinned)
     # integrated profiling (Sec. III-C): the DPRS candidates and the fixed
     # paths timed end to end; the library keeps the fastest
     integ = None
@@ -372,7 +464,13 @@ def main():
                                  round(c["measured_ns"] / 1e6, 4) for c in cands}}
         log(f"[bench] integrated profiling: {len(cands)} candidates in {t_int:.1f} s, "
             f"selected {label}: {sec * 1e3:.3f} ms/step")
+    if pinned:
+        sec = time_steps(g, x, out, args.steps, args.warmup)
+        log(f"[bench] pinned path: {sec * 1e3:.3f} ms/step")
     ids, model_ns = g.path()
+    if args.path_out:
+        with open(args.path_out, "w") as f:
+            json.dump({"path": ids, "routines": [g.routines(i)[r]["name"] for i, r in enumerate(ids)]}, f)
     value = args.batch / sec
     steps_dist = step_stats(g, x, out, min(max(args.steps, 10), 100))
     log(f"[bench] per-step latency (ms): {steps_dist}")
@@ -399,17 +497,22 @@ def main():
     for i in range(1, nl):
         rt = g.routines(i)[ids[i]]
         cat, flops, byt = layer_work(spec, g, i, rt)
+        need = bytes_needed(spec, g, i, rt)
         for key, d in ((f"{rt['name']} on {layer_kind(spec, i)}", groups), (cat, cats)):
-            gr = d.setdefault(key, {"ms": 0.0, "flops": 0, "bytes": 0, "launches": 0, "cats": set()})
+            gr = d.setdefault(key, {"ms": 0.0, "flops": 0, "bytes": 0, "needed": 0, "launches": 0, "cats": set(),
+                                    "layers": [], "routine": rt["name"]})
             gr["ms"] += layer_ms[i]
             gr["flops"] += flops
             gr["bytes"] += byt
+            gr["needed"] += need
             gr["launches"] += 1
             gr["cats"].add(cat)
+            gr["layers"].append(i)
         per_layer.append({"layer": i, "type": cat, "routine": rt["name"],
                           "us": round(layer_ms[i] * 1e3, 2), "us_cold": round(float(cold[i]) * 1e3, 2),
                           "tflops": round(flops / (layer_ms[i] * 1e-3) / 1e12, 2) if flops and layer_ms[i] else 0,
-                          "gbs": round(byt / (layer_ms[i] * 1e-3) / 1e9, 1) if layer_ms[i] else 0})
+                          "gbs": round(byt / (layer_ms[i] * 1e-3) / 1e9, 1) if layer_ms[i] else 0,
+                          "gbs_needed": round(need / (layer_ms[i] * 1e-3) / 1e9, 1) if layer_ms[i] else 0})
     dom_key = max(groups, key=lambda k: groups[k]["ms"])
     dom = groups[dom_key]
     avg_s = dom["ms"] / dom["launches"] * 1e-3
@@ -425,13 +528,25 @@ def main():
         ach = dom["bytes"] / dom["launches"] / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = (traffic_for(dom_key)
-                       if (args.net, args.batch, args.dtype) == ("resnet50", 32, "bf16") else None)
+    # HBM traffic from the committed per-layer counter summary, only where it
+    # covers these very layers run by this routine (else null, with the reason)
+    traffic, why = (traffic_for_layers(dom["layers"], dom["routine"])
+                    if (args.net, args.batch, args.dtype) == ("resnet50", 32, "bf16") and not args.no_fuse
+                    else (None, "no counter summary for this workload"))
+    roof["traffic"] = traffic
+    if traffic:
+        roof["traffic_ratio"] = round(traffic / (dom["bytes"] / dom["launches"]), 3)
+    else:
+        roof["traffic_null_reason"] = why
     roof["kernel"] = (f"routine {dom_key} ({dom['launches']} launches/step on "
-                      f"{'/'.join(sorted(dom['cats']))} layers)")
+                      f"{'/'.join(sorted(dom['cats']))} layers {dom['layers']})")
     roof["avg_launch_us"] = round(avg_s * 1e6, 2)
     roof["algorithmic"] = {"flops_per_launch": dom["flops"] // dom["launches"],
-                           "bytes_per_launch": dom["bytes"] // dom["launches"]}
+                           "bytes_per_launch": dom["bytes"] // dom["launches"],
+                           "bytes_needed_per_launch": dom["needed"] // dom["launches"]}
+    if roof["bound"] == "hbm":
+        # the same with a strided 1x1 layer's input counted as the pixels it reads
+        roof["achieved_needed"] = round(dom["needed"] / dom["launches"] / avg_s / 1e9, 1)
     # headline: MFMA utilisation over the 3x3 convolutions
     c3 = cats.get("conv3x3")
     conv3_util = (c3["flops"] / (c3["ms"] * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS[args.dtype]) if c3 else None
@@ -457,6 +572,34 @@ def main():
         g.set_path(ids)
     dp_vs_fixed = round(args.batch / sec_dp / fixed[best_fixed], 4) if best_fixed else None
     sel_vs_fixed = round(value / fixed[best_fixed], 4) if best_fixed else None
+    # the DPRS path, the selected path and the two best fixed paths timed in
+    # alternating rounds (order reversed every other round), so drift and
+    # warm-up favour none of them; medians and per-round ratios reported
+    comparison = None
+    if best_fixed and args.compare_rounds > 0:
+        top = sorted(fixed, key=fixed.get, reverse=True)[:2]
+        cands = [("dprs", dp_ids)] + ([("selected", ids)] if ids != dp_ids else [])
+        for name in top:
+            lay, algo = name.split("/")
+            g.select("fixed", lay, algo)
+            cands.append((f"fixed/{name}", g.path()[0]))
+        times = {nm: [] for nm, _ in cands}
+        for r in range(args.compare_rounds):
+            for nm, path in (cands if r % 2 == 0 else cands[::-1]):
+                g.set_path(path)
+                times[nm].append(time_steps(g, x, out, args.steps, min(args.warmup, 5)) * 1e3)
+        g.set_path(ids)
+        med = {nm: float(np.median(v)) for nm, v in times.items()}
+        bf = min((nm for nm in med if nm.startswith("fixed/")), key=med.get)
+        ratios = [f / d for f, d in zip(times[bf], times["dprs"])]
+        comparison = {"rounds": args.compare_rounds, "steps_per_round": args.steps,
+                      "ms": {nm: {"median": round(med[nm], 4), "min": round(min(v), 4), "max": round(max(v), 4)}
+                             for nm, v in times.items()},
+                      "best_fixed": bf, "dp_vs_best_fixed": round(med[bf] / med["dprs"], 4),
+                      "dp_vs_best_fixed_per_round": [round(q, 4) for q in ratios]}
+        if "selected" in med:
+            comparison["selected_vs_best_fixed"] = round(med[bf] / med["selected"], 4)
+        log(f"[bench] alternating comparison: {comparison}")
 
     bs1 = None
     if not args.no_bs1 and args.net == "resnet50":
@@ -478,6 +621,10 @@ def main():
         g1.close()
 
     cpu = cpu_baseline(spec, t, args.cpu_budget)
+    if args.cpu_budget > 0:
+        cpu64 = cpu_baseline(spec, t, args.cpu_budget / 2, storage="f64")
+        cpu["value_f64_storage"] = cpu64["value"]
+        cpu["sample_f64_storage"] = cpu64["sample"]
     log(f"[bench] cpu oracle: {cpu}")
 
     line = {
@@ -498,7 +645,10 @@ def main():
         "img_s_bs1": bs1,
         "conv3x3_mfma_util": round(conv3_util, 4) if conv3_util else None,
         "dprs_img_s": round(args.batch / sec_dp, 2),
-        "dp_vs_best_fixed": dp_vs_fixed, "selected_vs_best_fixed": sel_vs_fixed,
+        "dp_vs_best_fixed": comparison["dp_vs_best_fixed"] if comparison else dp_vs_fixed,
+        "selected_vs_best_fixed": (comparison.get("selected_vs_best_fixed", comparison["dp_vs_best_fixed"])
+                                   if comparison else sel_vs_fixed),
+        "comparison": comparison, "single_pass_dp_vs_best_fixed": dp_vs_fixed,
         "best_fixed": best_fixed, "fixed_img_s": fixed, "fixed_model_time_ms": fixed_model, "integrated": integ,
         "model_time_ms": round(model_ns / 1e6, 4), "dprs_model_time_ms": round(dp_model_ns / 1e6, 4),
         "tuning_s": round(t_prof + t_sel + t_int, 2),

@@ -294,6 +294,17 @@ int sn_run_timed(sn_graph* g, const void* d_in, void* d_out, void* hip_stream, i
 int sn_layer_output(const sn_graph* g, int32_t layer, void* d_dst, size_t cap, size_t* bytes,
                     int32_t* layout, void* hip_stream);
 
+/* The kernel launches one sn_run of the selected plan makes, in order:
+ * layer_of_launch[i] is the layer launch i belongs to (the adapt routines
+ * feeding a layer count as that layer's; a routine may launch more than one
+ * kernel).  Nothing is launched: the plan's steps are walked with launches
+ * counted only.  Lets a kernel trace of sn_run (for instance per-dispatch
+ * hardware counters) be attributed to layers.  *n receives the count;
+ * layer_of_launch = NULL only queries it.
+ * Errors: SN_E_STATE (no plan), SN_E_NOMEM (cap below the count),
+ * SN_E_DEVICE (host-only graph). */
+int sn_plan_launches(const sn_graph* g, int32_t* layer_of_launch, int32_t cap, int32_t* n);
+
 /* Integrated profiling (Sec. III-C): the unit-profiled table filters the
  * routine patterns down to a short list of whole paths, and those are timed
  * end to end, which sees what a sum of isolated layer times misses (cache

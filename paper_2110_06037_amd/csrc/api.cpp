@@ -296,6 +296,18 @@ int sn_layer_output(const sn_graph* gp, int32_t layer, void* d_dst, size_t cap, 
   });
 }
 
+int sn_plan_launches(const sn_graph* gp, int32_t* layer_of_launch, int32_t cap, int32_t* n) {
+  return guarded([&] {
+    CHECK_G(gp);
+    if (gp->g.host_only()) fail(SN_E_DEVICE, "host-only graph has no plan");
+    const std::vector<int> v = plan_launch_layers(gp->g);
+    if (n) *n = (int32_t)v.size();
+    if (!layer_of_launch) return;
+    if (cap < (int32_t)v.size()) fail(SN_E_NOMEM, "buffer smaller than the launch count");
+    for (size_t i = 0; i < v.size(); ++i) layer_of_launch[i] = v[i];
+  });
+}
+
 int sn_profile_integrated(sn_graph* gp, int32_t warmup, int32_t reps, void* stream,
                           int32_t* n_candidates) {
   return guarded([&] {

@@ -203,6 +203,7 @@ void* noalloc_scratch_ptr(int device);  // the region's device address (device m
 void plan_run_in(const Graph& g, void* base, size_t cap, const void* const* d_in, void* const* d_out,
                  void* stream);
 size_t plan_arena_bytes(const Graph& g);
+std::vector<int> plan_launch_layers(const Graph& g);
 void plan_layer_output(const Graph& g, int layer, void* d_dst, size_t cap, size_t* bytes, int* layout,
                        void* stream);
 // times every candidate end to end and selects the fastest (compiles its plan)

@@ -740,6 +740,28 @@ void plan_run_in(const Graph& g, void* base, size_t cap, const void* const* d_in
 
 size_t plan_arena_bytes(const Graph& g) { return g.plan ? g.plan->arena_bytes : 0; }
 
+// The layer each kernel launch of one sn_run belongs to, in launch order
+// (converters feeding a layer count as the layer's).  The plan's steps are
+// enqueued with launches counted, not issued, on placeholder addresses.
+std::vector<int> plan_launch_layers(const Graph& g) {
+  if (!g.plan) fail(SN_E_STATE, "no execution plan");
+  const Plan& P = *g.plan;
+  std::vector<const void*> ins(g.net_inputs.size(), reinterpret_cast<const void*>(uintptr_t(1) << 20));
+  std::vector<void*> outs(net_outputs(g).size(), reinterpret_cast<void*>(uintptr_t(1) << 21));
+  char* base = reinterpret_cast<char*>(uintptr_t(1) << 22);
+  std::vector<int> layer_of;
+  struct Restore {
+    ~Restore() { k::g_count_only = 0; }
+  } restore;
+  k::g_count_only = 1;
+  for (const Step& s : P.steps) {
+    const long long before = k::g_launches;
+    enqueue_step(g, P, base, s, ins.data(), outs.data(), nullptr);
+    for (long long q = before; q < k::g_launches; ++q) layer_of.push_back(s.layer);
+  }
+  return layer_of;
+}
+
 // Copy of a layer's stored output (its routine's layout, channels padded as
 // stored) out of the plan's arena; with opt_keep every layer's output
 // survives the run.

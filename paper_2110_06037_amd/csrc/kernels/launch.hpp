@@ -21,9 +21,16 @@ struct LaunchTiming {
   hipEvent_t start = nullptr, stop = nullptr;
 };
 extern thread_local LaunchTiming g_timing;
+// Launch accounting: every launch adds one to g_launches; while
+// g_count_only is set the launches are only counted, not enqueued (used to
+// list a plan's kernel launches without running them).
+extern thread_local long long g_launches;
+extern thread_local int g_count_only;
 
 #define SN_LAUNCH(K, G, B, S, ST, ...)                                                  \
   do {                                                                                  \
+    ++::sn::k::g_launches;                                                              \
+    if (::sn::k::g_count_only) break;                                                   \
     if (::sn::k::g_timing.start || ::sn::k::g_timing.stop) {                            \
       hipExtLaunchKernelGGL(K, G, B, S, ST, ::sn::k::g_timing.start, ::sn::k::g_timing.stop, 0, \
                             __VA_ARGS__);                                               \

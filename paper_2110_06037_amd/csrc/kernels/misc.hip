@@ -13,6 +13,8 @@ namespace sn {
 namespace k {
 
 thread_local LaunchTiming g_timing;
+thread_local long long g_launches = 0;
+thread_local int g_count_only = 0;
 
 static void check(bool ok, const char* what) {
   if (!ok) throw std::invalid_argument(std::string("kernel launch: ") + what);

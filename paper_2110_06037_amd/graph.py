@@ -278,6 +278,14 @@ class Graph:
                                         ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)))
         return out
 
+    def plan_launches(self):
+        """The layer of each kernel launch of one run, in launch order."""
+        n = ctypes.c_int32()
+        N.check(self.lib.sn_plan_launches(self._g, None, 0, ctypes.byref(n)))
+        arr = (ctypes.c_int32 * max(n.value, 1))()
+        N.check(self.lib.sn_plan_launches(self._g, arr, n.value, ctypes.byref(n)))
+        return list(arr)[:n.value]
+
     def layer_output(self, layer, stream=None):
         """The stored bytes of a layer's output after a run (its routine's
         layout; NC8HW8 channels padded), as (uint8 device tensor, layout)."""

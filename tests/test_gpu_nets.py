@@ -329,3 +329,30 @@ def test_nc8hw8_stored_outputs_keep_padded_channels_zero(algo):
     out = from_dev(y, "bf16").reshape(3, -1)
     assert err(out, refs[-1].reshape(3, -1), "bf16") <= TOL["bf16"]
     g.close()
+
+
+def test_plan_launch_list_matches_the_routines():
+    # sn_plan_launches lists a run's kernel launches by layer without
+    # launching anything: every layer appears in order, a Winograd layer
+    # with its three kernels (input transform, tile GEMMs, output transform),
+    # converters before the layer they feed; the next run is unaffected
+    import torch
+    spec = resnet18(1)
+    t = generate(spec)
+    g = build_from_spec(spec, t)
+    g.select("fixed", "NHWC", "winograd")
+    out0, xd = run_out(g, spec, t)
+    ids = g.path()[0]
+    lay = g.plan_launches()
+    assert lay == sorted(lay) and set(lay) == set(range(1, g.num_layers()))
+    for i in range(1, g.num_layers()):
+        rt = g.routines(i)[ids[i]]
+        n = lay.count(i)
+        conv = 1 if i == 1 else 0          # the input's NCHW -> NHWC converter feeds layer 1
+        if rt["algo"] == N.WINOGRAD:
+            assert n == 3 + conv, (i, rt["name"], n)
+        elif i == 1:
+            assert n == 2, (i, rt["name"], n)
+    out1, _ = run_out(g, spec, t)
+    assert np.array_equal(out0, out1)
+    g.close()
