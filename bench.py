@@ -101,9 +101,11 @@ KERNEL_SOURCES = {
     "conv1x1_stream_kernel": ("conv1x1_stream.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
     "conv_smallc_kernel": ("conv_smallc.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
     "dw3x3_kernel": ("dwconv.hip", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
+    "wino_fused_kernel": ("wino_fused.hip", "wino.hpp", "gemm_common.hpp", "kcommon.hpp", "launch.hpp"),
 }
 ALL_KERNEL_SOURCES = ("conv.hip", "conv_igemm_bf16.hip", "conv_igemm_f16.hip", "conv1x1_stream.hip", "conv_patch.hip",
                       "conv_smallc.hip", "convert.hip", "dwconv.hip", "fc.hip", "igemm.hpp", "misc.hip",
+                      "wino.hpp", "wino_fused.hip",
                       "gemm_common.hpp",
                       "kcommon.hpp", "launch.hpp")
 

@@ -11,6 +11,7 @@
 
 #include "core.hpp"
 #include "kernels/launch.hpp"
+#include "kernels/wino.hpp"
 
 namespace sn {
 
@@ -239,7 +240,8 @@ static size_t layer_ws_bytes(const Graph& g, const Layer& L, const Routine& r) {
   if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM)
     return k::igemm_ws_bytes(r.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), 1, 1);
   if (L.type != SN_LAYER_CONV2D || L.d.groups > 1) return 0;
-  if (r.algo == SN_ALGO_WINOGRAD) return k::winograd_ws_bytes(r.dtype, tdesc(in, r.layout), L.out.c);
+  if (r.algo == SN_ALGO_WINOGRAD)  // the fused routines keep their transforms on chip
+    return r.param == 0 ? k::winograd_ws_bytes(r.dtype, tdesc(in, r.layout), L.out.c) : 0;
   if (r.algo == SN_ALGO_IGEMM)
     return k::igemm_ws_bytes(r.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), L.d.r, L.d.s);
   return 0;
@@ -274,8 +276,10 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
         k::conv_direct(dt, a, st);
       } else if (r.algo == SN_ALGO_IGEMM) {
         k::conv_igemm(dt, r.param, a, st);
-      } else {
+      } else if (r.param == 0) {
         k::conv_winograd(dt, a, st);
+      } else {
+        k::conv_wino_fused(dt, r.param - 1, a, st);
       }
       break;
     }

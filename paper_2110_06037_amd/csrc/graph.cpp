@@ -8,6 +8,7 @@
 
 #include "core.hpp"
 #include "kernels/launch.hpp"
+#include "kernels/wino.hpp"
 
 namespace sn {
 
@@ -119,6 +120,7 @@ std::string routine_name(const Graph& g, const Layer& L, const Routine& r) {
   if (g.multi_dtype()) o << kDtypeName[r.dtype] << ":";
   o << kLayoutName[r.layout] << "/" << kAlgoName[r.algo];
   if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_IGEMM) o << ":p" << r.param;
+  if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_WINOGRAD && r.param > 0) o << ":fused:p" << r.param - 1;
   if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM) o << ":1x1conv:p" << r.param;
   return o.str();
 }
@@ -164,8 +166,11 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
                   (residual == 0 || k::igemm_param_takes_residual(dt, p, lay, L.d.k)))
                 add(lay, SN_ALGO_IGEMM, p);
           }
-          if ((g.opt_algos >> SN_ALGO_WINOGRAD & 1) && !residual && winograd_applicable(L, in))
-            add(lay, SN_ALGO_WINOGRAD, 0);
+          if ((g.opt_algos >> SN_ALGO_WINOGRAD & 1) && !residual && winograd_applicable(L, in)) {
+            add(lay, SN_ALGO_WINOGRAD, 0);  // transforms and tile GEMMs as three kernels
+            if (g.opt_params && k::wino_fused_applicable(dt, lay, in.c))
+              for (int p = 0; p < k::wino_fused_num_configs(); ++p) add(lay, SN_ALGO_WINOGRAD, p + 1);
+          }
           break;
         case SN_LAYER_FC:
           add(lay, SN_ALGO_DIRECT, 0);
