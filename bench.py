@@ -329,6 +329,8 @@ def main():
     ap.add_argument("--batch", type=int, default=32)
     ap.add_argument("--dtype", default="bf16")
     ap.add_argument("--profile-reps", type=int, default=20)
+    ap.add_argument("--profile-flush-mib", type=int, default=0,
+                    help="cache-cold unit profiling: MiB written before each timed run (0 = warm)")
     ap.add_argument("--timing-reps", type=int, default=50,
                     help="back-to-back repetitions per layer in the per-layer timing pass")
     ap.add_argument("--net", default="resnet50", choices=sorted(NETS),
@@ -392,7 +394,11 @@ def main():
         with open(args.costs_in) as f:
             g.set_costs(f.read())
     else:
+        # cache-cold unit profiling when asked: the library evicts the caches
+        # before every timed run and takes the median
+        g.set_option(N.OPT_FLUSH, args.profile_flush_mib << 20)
         g.profile(warmup=5, reps=args.profile_reps)
+        g.set_option(N.OPT_FLUSH, 0)
     t_prof = time.perf_counter() - t0
     t1 = time.perf_counter()
     g.select("dprs")
@@ -654,6 +660,8 @@ def main():
         "best_fixed": best_fixed, "fixed_img_s": fixed, "fixed_model_time_ms": fixed_model, "integrated": integ,
         "model_time_ms": round(model_ns / 1e6, 4), "dprs_model_time_ms": round(dp_model_ns / 1e6, 4),
         "tuning_s": round(t_prof + t_sel + t_int, 2),
+        "unit_profiling": ("loaded" if args.costs_in else
+                           f"cold/{args.profile_flush_mib}MiB/median" if args.profile_flush_mib else "warm/mean"),
     }
     sel = {}
     for i in range(1, nl):

@@ -137,8 +137,10 @@ typedef enum {
   SN_OPT_PARAMS = 2,    /* 0: one routine parameter per algorithm; 1: all (default 1) */
   SN_OPT_HIPGRAPH = 3,  /* 1: sn_run replays a captured HIP graph (default 0)        */
   SN_OPT_SEED = 4,      /* seed of the profiler's scratch-tensor fill (default 1)    */
-  SN_OPT_FLUSH = 5,     /* bytes sn_run_timed writes to a scratch buffer before each
-                           layer, evicting the caches (0 = off, the default)        */
+  SN_OPT_FLUSH = 5,     /* bytes written to a scratch buffer to evict the caches:
+                           by sn_run_timed before each layer, and by sn_profile
+                           before each timed run (cache-cold unit profiling);
+                           0 = off, the default                                     */
   SN_OPT_KEEP = 6,      /* 1: the plan gives every intermediate tensor its own bytes
                            (no reuse by liveness), so sn_layer_output can read any
                            layer's stored output after a run (default 0)            */
@@ -211,7 +213,10 @@ int sn_num_io(const sn_graph* g, int32_t* n_inputs, int32_t* n_outputs);
  * start of the first run's first kernel dispatch and the end of the last
  * run's last one (hipExtLaunchKernelGGL), so host launch latency and the
  * events' own dispatch gaps are amortised over the block.  Identical layer
- * signatures and converter shapes are timed once.  Synchronous.
+ * signatures and converter shapes are timed once.  With SN_OPT_FLUSH > 0 the
+ * costs are cache-cold instead: before each of the reps runs an untimed
+ * kernel writes that many bytes of scratch, each run is timed on its own, and
+ * the cost is the median (warm and cold costs are cached apart).  Synchronous.
  * Errors: SN_E_STATE (no layers), SN_E_INVALID (reps < 1 or warmup < 0),
  * SN_E_DEVICE (host-only graph, HIP error). */
 int sn_profile(sn_graph* g, int32_t warmup, int32_t reps, void* hip_stream);

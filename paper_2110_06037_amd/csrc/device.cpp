@@ -337,19 +337,22 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
     for (const Routine& r : L.routines) wsmax = std::max(wsmax, layer_ws_bytes(g, L, r));
   }
   tmax = align256(tmax);
-  void *in0 = nullptr, *in1 = nullptr, *outb = nullptr, *ws = nullptr;
+  void *in0 = nullptr, *in1 = nullptr, *outb = nullptr, *ws = nullptr, *flush = nullptr;
   std::vector<hipEvent_t> ev(2, nullptr);
   auto cleanup = [&]() {
     for (auto e : ev)
       if (e) (void)hipEventDestroy(e);
-    for (void* p : {in0, in1, outb, ws})
+    for (void* p : {in0, in1, outb, ws, flush})
       if (p) (void)hipFree(p);
   };
+  // cache-cold mode: costs are keyed apart from the warm ones
+  const std::string mode_key = g.opt_flush > 0 ? "|cold" + std::to_string(g.opt_flush) : std::string();
   try {
     HIPCHK(hipMalloc(&in0, tmax));
     HIPCHK(hipMalloc(&in1, tmax));
     HIPCHK(hipMalloc(&outb, tmax));
     if (wsmax) HIPCHK(hipMalloc(&ws, wsmax));
+    if (g.opt_flush > 0) HIPCHK(hipMalloc(&flush, (size_t)g.opt_flush));
     for (auto& e : ev) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
     // operands hold values of the dtype being timed (refilled when it changes)
     int filled = -1;
@@ -367,7 +370,27 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
     // are tied to the start of the first run's first kernel and to the end
     // of the last run's last kernel, so host launch latency and the events'
     // own dispatch gaps are amortised over the block
+    //
+    // cache-cold mode (SN_OPT_FLUSH > 0): before each run an untimed kernel
+    // writes the flush buffer, evicting the operands and weights from the
+    // caches; each run is timed on its own and the cost is the median
+    auto time_cold = [&](auto&& launch) -> int64_t {
+      for (int i = 0; i < warmup; ++i) launch();
+      std::vector<float> t(reps);
+      for (int i = 0; i < reps; ++i) {
+        k::fill_random(SN_F32, flush, g.opt_flush / 4, (uint64_t)i, st);
+        k::g_timing = k::LaunchTiming{ev[0], ev[1]};
+        launch();
+        k::g_timing = k::LaunchTiming{};
+        HIPCHK(hipGetLastError());
+        HIPCHK(hipEventSynchronize(ev[1]));
+        HIPCHK(hipEventElapsedTime(&t[i], ev[0], ev[1]));
+      }
+      std::nth_element(t.begin(), t.begin() + reps / 2, t.end());
+      return std::max<int64_t>(1, (int64_t)std::llround((double)t[reps / 2] * 1e6));
+    };
     auto time_it = [&](auto&& launch) -> int64_t {
+      if (flush) return time_cold(launch);
       for (int i = 0; i < warmup; ++i) launch();
       for (int i = 0; i < reps; ++i) {
         k::g_timing = k::LaunchTiming{i == 0 ? ev[0] : nullptr, i == reps - 1 ? ev[1] : nullptr};
@@ -385,7 +408,7 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
       if (L.type == SN_LAYER_INPUT) continue;  // a net input: its one routine costs 0
       for (size_t ri = 0; ri < L.routines.size(); ++ri) {
         const Routine& r = L.routines[ri];
-        std::string key = L.signature + "|" + r.name;
+        std::string key = L.signature + "|" + r.name + mode_key;
         auto it = D.cost_cache.find(key);
         if (it != D.cost_cache.end()) {
           L.cost[ri] = it->second;
@@ -420,7 +443,7 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
           }
           std::string key = "cvt|" + std::to_string(s.n) + "," + std::to_string(s.c) + "," +
                             std::to_string(s.h) + "," + std::to_string(s.w) + "|" +
-                            std::to_string(a) + ">" + std::to_string(b);
+                            std::to_string(a) + ">" + std::to_string(b) + mode_key;
           auto it = D.cost_cache.find(key);
           if (it == D.cost_cache.end()) {
             fill(schema_dtype(a));

@@ -72,6 +72,24 @@ def test_tiny_chain_measured_table_dp_equals_exhaustive_and_parity():
             g.select("fixed", lay, algo)
             out, _ = run_out(g, spec, t)
             assert err(out, ref, "f32") <= TOL["f32"], (lay, algo)
+    # cache-cold unit profiling (median of single runs after a flush): a
+    # complete positive cost table, cached apart from the warm one (so a warm
+    # profile afterwards gives back the warm table), and its DP path is again
+    # the exhaustive optimum of that table and matches the oracle
+    g.set_option(N.OPT_FLUSH, 64 << 20)
+    g.profile(warmup=1, reps=5)
+    g.set_option(N.OPT_FLUSH, 0)
+    cold = g.costs()
+    for l in cold["layers"][1:-1]:
+        assert all(r["ns"] > 0 for r in l["routines"]), l
+    g.select("dprs")
+    ids, total = g.path()
+    tt, tup, _ = exhaustive(problem_from_costs(cold))
+    assert tuple(ids) + (0,) == tup and total == tt
+    out, _ = run_out(g, spec, t)
+    assert err(out, ref, "f32") <= TOL["f32"]
+    g.profile(warmup=3, reps=10)
+    assert g.costs() == costs
 
 
 @pytest.mark.parametrize("name", ["tiny", "mobilenetv2"])
