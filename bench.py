@@ -209,6 +209,51 @@ def summarize_pmc(fetch_dir, write_dir, pass_file, out, calib_mib):
     print(json.dumps({"layers": len(layers), "calibration": res["calibration"]}))
 
 
+def summarize_trace(trace_dir, pass_file, out):
+    """Per-layer kernel time of a pinned path from a rocprofv3 --kernel-trace
+    run of `bench.py --pmc-pass`: the library's dispatches are the warm-up and
+    timed steps in order, attributed to layers by the plan's launch list;
+    each launch's duration (end - start timestamp) is averaged over the timed
+    steps and summed per layer.  Adds the layer's minimum bytes (input +
+    filters + output, + residual; strided 1x1 layers count the pixels they
+    read) and the GB/s they give over that time."""
+    import csv
+    import glob
+    with open(pass_file) as f:
+        info = json.load(f)
+    launch_layer = info["launch_layers"]
+    L = len(launch_layer)
+    rows = []
+    for fn in glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True):
+        rows += list(csv.DictReader(open(fn)))
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    ours = [r for r in rows if r["Kernel_Name"].startswith("_ZN2sn1k") or "sn::k::" in r["Kernel_Name"]]
+    steps = len(ours) // L
+    if steps * L != len(ours) or steps < info["warmup"] + info["steps"]:
+        raise SystemExit(f"trace: {len(ours)} library dispatches, not a whole number of {L}-launch steps")
+    timed = ours[(steps - info["steps"]) * L:]
+    dur = [0.0] * L
+    for k, r in enumerate(timed):
+        dur[k % L] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / info["steps"]
+    need = info.get("bytes_needed", {})
+    layers = []
+    for i, rname in enumerate(info["routines"]):
+        idx = [k for k in range(L) if launch_layer[k] == i]
+        if not idx:
+            continue
+        ns = sum(dur[k] for k in idx)
+        b = need.get(str(i))
+        layers.append({"layer": i, "routine": rname, "launches": len(idx),
+                       "kernels": [timed[k]["Kernel_Name"] for k in idx],
+                       "kernel_ns": [round(dur[k], 1) for k in idx], "us": round(ns / 1e3, 3),
+                       "bytes_needed": b, "gbs": round(b / ns, 1) if b and ns else None})
+    res = {"workload": info["workload"], "steps": info["steps"], "layers": layers,
+           "step_kernel_us": round(sum(dur) / 1e3, 2)}
+    with open(out, "w") as fh:
+        json.dump(res, fh, indent=1)
+    print(json.dumps({"layers": len(layers), "step_kernel_us": res["step_kernel_us"]}))
+
+
 def _mask_name(m):
     return "+".join(n for i, n in enumerate(("NCHW", "NHWC", "NC8HW8")) if m >> i & 1)
 
@@ -362,11 +407,19 @@ def main():
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "PASS_JSON", "OUT"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --pmc-pass into "
                          "the per-layer traffic summary OUT, and exit")
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("TRACE_DIR", "PASS_JSON", "OUT"),
+                    help="per-layer kernel durations of a --pmc-pass run under rocprofv3 --kernel-trace")
+    ap.add_argument("--rotate-layouts", action="store_true",
+                    help="with --tune-only: a path whose layer i takes layout i mod 3 (converters on every "
+                         "edge), for profiling the adapt routines")
     ap.add_argument("--compare-rounds", type=int, default=4,
                     help="alternating rounds timing the DPRS path against the best fixed paths")
     args = ap.parse_args()
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, calib_mib=args.calib_copy_mib)
+        return
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the path would shard over "
@@ -408,6 +461,17 @@ def main():
     if args.costs_out:
         with open(args.costs_out, "w") as f:
             json.dump(g.costs(), f)
+    if args.rotate_layouts:
+        # a path for profiling the adapt routines: layer i runs the fastest
+        # routine in layout i mod 3, so every edge between layers converts
+        table = g.costs()["layers"]
+        rot = [0]
+        for i in range(1, g.num_layers()):
+            ns = {r["id"]: (c["ns"] if c["ns"] is not None and c["ns"] >= 0 else float("inf"))
+                  for r, c in zip(g.routines(i), table[i]["routines"])}
+            want = [r for r in g.routines(i) if r["layout"] == i % 3 and ns[r["id"]] < float("inf")]
+            rot.append(min(want or g.routines(i), key=lambda r: ns[r["id"]])["id"])
+        g.set_path(rot)
     dp_ids, dp_model_ns = g.path()
     pinned = None
     if args.path_in:
@@ -440,10 +504,11 @@ def main():
             dst.copy_(src)
             torch.cuda.synchronize()
         ids = g.path()[0]
+        need = {str(i): bytes_needed(spec, g, i, g.routines(i)[ids[i]]) for i in range(1, g.num_layers())}
         with open(args.pmc_pass, "w") as f:
             json.dump({"workload": spec["name"], "warmup": args.warmup, "steps": args.steps,
                        "routines": [g.routines(i)[r]["name"] for i, r in enumerate(ids)],
-                       "launch_layers": g.plan_launches()}, f)
+                       "launch_layers": g.plan_launches(), "bytes_needed": need}, f)
         g.close()
         return
 

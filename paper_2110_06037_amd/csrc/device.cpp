@@ -271,7 +271,7 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
       a.ws_bytes = ws_bytes;
       a.res = L.inputs.size() > 1 ? in[1] : nullptr;
       if (L.d.groups > 1) {
-        k::dwconv(dt, a, st);
+        k::dwconv(dt, a, r.param, st);
       } else if (r.algo == SN_ALGO_DIRECT) {
         k::conv_direct(dt, a, st);
       } else if (r.algo == SN_ALGO_IGEMM) {

@@ -121,6 +121,7 @@ std::string routine_name(const Graph& g, const Layer& L, const Routine& r) {
   o << kLayoutName[r.layout] << "/" << kAlgoName[r.algo];
   if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_IGEMM) o << ":p" << r.param;
   if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_WINOGRAD && r.param > 0) o << ":fused:p" << r.param - 1;
+  if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_DIRECT && r.param > 0) o << ":strip" << k::dw_strip_len(r.param);
   if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM) o << ":1x1conv:p" << r.param;
   return o.str();
 }
@@ -155,6 +156,9 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
         case SN_LAYER_CONV2D:
           if (is_depthwise(L, in)) {
             add(lay, SN_ALGO_DIRECT, 0);  // depthwise has its own direct routine
+            if (g.opt_params)             // ... and strip lengths as routine parameters
+              for (int p = 1; p <= k::dw_num_strip_params(dt, lay, in.c, L.d.r, L.d.s, L.d.stride); ++p)
+                add(lay, SN_ALGO_DIRECT, p);
             break;
           }
           if (g.opt_algos >> SN_ALGO_DIRECT & 1) add(lay, SN_ALGO_DIRECT, 0);

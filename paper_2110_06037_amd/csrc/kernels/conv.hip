@@ -567,11 +567,12 @@ static void dw_dispatch(const ConvArgs& c, hipStream_t st) {
   }
 }
 
-bool dwconv3x3_vec(int dtype, const ConvArgs& c, hipStream_t st);  // dwconv.hip
+bool dwconv3x3_vec(int dtype, const ConvArgs& c, int qs, hipStream_t st);  // dwconv.hip
 
-void dwconv(int dtype, const ConvArgs& c, hipStream_t st) {
+void dwconv(int dtype, const ConvArgs& c, int param, hipStream_t st) {
   check(!c.res, "depthwise routine takes no residual");
-  if (dwconv3x3_vec(dtype, c, st)) return;
+  if (dwconv3x3_vec(dtype, c, param > 0 ? dw_strip_len(param) : 0, st)) return;
+  check(param == 0, "depthwise strip parameter needs the strip kernel");
   if (dtype == 0) dw_dispatch<float>(c, st);
   else if (dtype == 1) dw_dispatch<f16>(c, st);
   else dw_dispatch<bf16>(c, st);

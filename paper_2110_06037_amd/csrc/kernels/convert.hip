@@ -3,16 +3,15 @@
 // Layout converters for 16-bit tensors, moving 16-byte vectors on both
 // sides (every load and store a whole 8-element chunk; 32-bit index math):
 //  * NHWC <-> NC8HW8 with C % 8 == 0: a chunk is 8 channels of one pixel in
-//    both layouts, so the conversion permutes whole chunks; a workgroup
-//    takes 64 pixels of one image and every channel block of them, so the
-//    NC8HW8 side is written in 1 KB runs and the NHWC pixels it reads stay
-//    in L2 until every block of them is taken.
-//  * NCHW <-> NC8HW8 with H*W % 4 == 0: a thread takes 8 channels x G
-//    pixels (G = 8 or 4), reads G pixels of each channel plane, transposes
-//    8 x G in registers and writes G consecutive chunks.
-//  * NCHW <-> NHWC with C % 8 == 0 and H*W % 8 == 0: 64 channels x 64
-//    pixels of one image through an LDS tile: 16-byte rows in, 16-byte
-//    pixel vectors out (gathered from 8 tile rows).
+//    both layouts, so the conversion permutes whole chunks, a wave taking 8
+//    pixels x 8 channel blocks (128-byte runs on both sides).
+//  * NCHW <-> NC8HW8: a thread takes 8 channels x G pixels (G = 8, 4 or 1,
+//    the largest dividing H*W), reads G pixels of each channel plane,
+//    transposes 8 x G in registers and writes G consecutive chunks.
+//  * NCHW <-> NHWC with C % 8 == 0: 64 channels x 64 pixels of one image
+//    through an LDS tile: 16-byte rows (elements when H*W % 8 != 0) on the
+//    NCHW side, 16-byte pixel vectors (gathered from 8 tile rows) on the
+//    NHWC side.
 // Other shapes take the element-wise converters (misc.hip).  Padded NC8HW8
 // channels are written as zero.
 //
@@ -114,22 +113,27 @@ static void cast_from(int ddt, const void* x, const TDesc& xd, void* y, const TD
 typedef unsigned short u16;
 
 // NHWC <-> NC8HW8, C % 8 == 0: chunk (n, cb, hw) of NC8HW8 is NHWC chunk
-// (n, hw, cb).  Workgroup (pixel tile, image); thread k handles pixel
-// k % 64 of channel block k / 64.
+// (n, hw, cb).  A wave takes 8 channel blocks x 8 pixels of one image (lane
+// = block * 8 + pixel), so each load and store instruction covers 8 runs of
+// 128 contiguous bytes on either side; the grid has one wave per such tile,
+// whatever the split between pixels and channel blocks.
 template <bool TO_NC8>
 __global__ __launch_bounds__(256) void nhwc_nc8_kernel(const uint4* __restrict__ x, uint4* __restrict__ y, int HW,
-                                                       int CB) {
-  const int n = blockIdx.y, hw0 = blockIdx.x * 64;
-  const int npx = min(64, HW - hw0);
-  for (int k = threadIdx.x; k < 64 * CB; k += 256) {
-    const int px = k & 63, cb = k >> 6;
-    if (px >= npx) continue;
-    const int hw = hw0 + px;
-    const unsigned nhwc = (unsigned)(n * HW + hw) * (unsigned)CB + (unsigned)cb;
-    const unsigned nc8 = (unsigned)(n * CB + cb) * (unsigned)HW + (unsigned)hw;
-    if (TO_NC8) y[nc8] = x[nhwc];
-    else y[nhwc] = x[nc8];
-  }
+                                                       int CB, int HWT, int CBT, int tiles, FastDiv fd_hwt,
+                                                       FastDiv fd_cbt) {
+  const int tile = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (tile >= tiles) return;
+  const int lane = threadIdx.x & 63;
+  // tile = (n * CBT + cbt) * HWT + hwt
+  int r = fdiv(tile, fd_hwt);
+  const int hwt = tile - r * HWT;
+  const int n = fdiv(r, fd_cbt), cbt = r - n * CBT;
+  const int hw = hwt * 8 + (lane & 7), cb = cbt * 8 + (lane >> 3);
+  if (hw >= HW || cb >= CB) return;
+  const unsigned nhwc = (unsigned)(n * HW + hw) * (unsigned)CB + (unsigned)cb;
+  const unsigned nc8 = (unsigned)(n * CB + cb) * (unsigned)HW + (unsigned)hw;
+  if (TO_NC8) y[nc8] = x[nhwc];
+  else y[nhwc] = x[nc8];
 }
 
 // NCHW <-> NC8HW8 for H*W % G == 0: thread = (image, channel block, group of
@@ -146,21 +150,26 @@ __global__ __launch_bounds__(256) void nchw_nc8_kernel(const u16* __restrict__ x
   const u16* plane = x + ((size_t)n * C + cb * 8) * HW + hw;     // NCHW side (TO_NC8 reads it)
   u16* chunk = y + ((size_t)(n * CB + cb) * HW + hw) * 8;        // NC8HW8 side (TO_NC8 writes it)
   if (TO_NC8) {
+    // every load is issued unconditionally (channels past C read the
+    // block's first row and are zeroed afterwards), so all eight are in
+    // flight together
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      if (cb * 8 + e < C) {
-        if constexpr (G == 8) {
-          const uint4 q = *reinterpret_cast<const uint4*>(plane + (size_t)e * HW);
-          __builtin_memcpy(v[e], &q, 16);
-        } else {
-          const uint2 q = *reinterpret_cast<const uint2*>(plane + (size_t)e * HW);
-          __builtin_memcpy(v[e], &q, 8);
-        }
+      const int er = cb * 8 + e < C ? e : 0;
+      if constexpr (G == 8) {
+        const uint4 q = *reinterpret_cast<const uint4*>(plane + (size_t)er * HW);
+        __builtin_memcpy(v[e], &q, 16);
+      } else if constexpr (G == 4) {
+        const uint2 q = *reinterpret_cast<const uint2*>(plane + (size_t)er * HW);
+        __builtin_memcpy(v[e], &q, 8);
       } else {
-#pragma unroll
-        for (int p = 0; p < G; ++p) v[e][p] = 0;
+        v[e][0] = plane[(size_t)er * HW];
       }
     }
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int p = 0; p < G; ++p) v[e][p] = cb * 8 + e < C ? v[e][p] : (u16)0;
 #pragma unroll
     for (int p = 0; p < G; ++p) {
       u16 o[8];
@@ -181,26 +190,35 @@ __global__ __launch_bounds__(256) void nchw_nc8_kernel(const u16* __restrict__ x
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e][p] = o[e];
     }
+    // a channel row past C is not stored: its store goes to a channel row
+    // that is stored anyway (row 0 of the block, with the same values), so
+    // that no store sits behind a branch (a branch join would wait for the
+    // stores before it to complete)
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      if (cb * 8 + e >= C) continue;
+      const int er = cb * 8 + e < C ? e : 0;
       if constexpr (G == 8) {
         uint4 q;
-        __builtin_memcpy(&q, v[e], 16);
-        *reinterpret_cast<uint4*>(dst + (size_t)e * HW) = q;
-      } else {
+        __builtin_memcpy(&q, v[er == e ? e : 0], 16);
+        *reinterpret_cast<uint4*>(dst + (size_t)er * HW) = q;
+      } else if constexpr (G == 4) {
         uint2 q;
-        __builtin_memcpy(&q, v[e], 8);
-        *reinterpret_cast<uint2*>(dst + (size_t)e * HW) = q;
+        __builtin_memcpy(&q, v[er == e ? e : 0], 8);
+        *reinterpret_cast<uint2*>(dst + (size_t)er * HW) = q;
+      } else {
+        dst[(size_t)er * HW] = v[er == e ? e : 0][0];
       }
     }
   }
 }
 
-// NCHW <-> NHWC for C % 8 == 0 and H*W % 8 == 0: a 64-channel x 64-pixel
-// tile of one image in LDS ([channel][pixel], rows padded to 72 elements so
-// that the 8 rows one pixel vector gathers fall in different banks).
-template <bool TO_NHWC>
+// NCHW <-> NHWC for C % 8 == 0: a 64-channel x 64-pixel tile of one image
+// in LDS ([channel][pixel], rows padded to 72 elements so that the 8 rows
+// one pixel vector gathers fall in different banks); 16-byte pixel vectors
+// on the NHWC side, and on the NCHW side 16-byte row pieces when H*W % 8 ==
+// 0 (VEC), else single elements with consecutive lanes on consecutive
+// pixels (the 14x14 and 7x7 planes of the late stages).
+template <bool TO_NHWC, bool VEC>
 __global__ __launch_bounds__(256) void nchw_nhwc_tile_kernel(const u16* __restrict__ x, u16* __restrict__ y, int C,
                                                              int HW) {
   constexpr int RP = 72;
@@ -209,12 +227,35 @@ __global__ __launch_bounds__(256) void nchw_nhwc_tile_kernel(const u16* __restri
   const int nc = min(64, C - c0), npx = min(64, HW - hw0);
   const size_t img = (size_t)n * C * HW;
   if (TO_NHWC) {
-    // 16-byte rows: chunk j = (channel j / 8, pixels (j % 8) * 8 ..)
-    for (int j = threadIdx.x; j < 512; j += 256) {
-      const int c = j >> 3, p8 = (j & 7) * 8;
-      if (c < nc && p8 < npx) {
-        const uint4 q = *reinterpret_cast<const uint4*>(x + img + (size_t)(c0 + c) * HW + hw0 + p8);
-        *reinterpret_cast<uint4*>(tile + c * RP + p8) = q;
+    // loads are issued unconditionally (outside the tile they read the
+    // image's first element) so that all of a thread's are in flight
+    // together; only the LDS writes are predicated
+    if constexpr (VEC) {
+      // 16-byte rows: chunk j = (channel j / 8, pixels (j % 8) * 8 ..)
+      uint4 q[2];
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int j = threadIdx.x + k * 256, c = j >> 3, p8 = (j & 7) * 8;
+        const size_t o = c < nc && p8 < npx ? (size_t)(c0 + c) * HW + hw0 + p8 : 0;
+        q[k] = *reinterpret_cast<const uint4*>(x + img + o);
+      }
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int j = threadIdx.x + k * 256, c = j >> 3, p8 = (j & 7) * 8;
+        if (c < nc && p8 < npx) *reinterpret_cast<uint4*>(tile + c * RP + p8) = q[k];
+      }
+    } else {
+      u16 q[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int j = threadIdx.x + k * 256, c = j >> 6, px = j & 63;
+        const size_t o = c < nc && px < npx ? (size_t)(c0 + c) * HW + hw0 + px : 0;
+        q[k] = x[img + o];
+      }
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int j = threadIdx.x + k * 256, c = j >> 6, px = j & 63;
+        if (c < nc && px < npx) tile[c * RP + px] = q[k];
       }
     }
     __syncthreads();
@@ -231,22 +272,36 @@ __global__ __launch_bounds__(256) void nchw_nhwc_tile_kernel(const u16* __restri
       }
     }
   } else {
-    for (int j = threadIdx.x; j < 512; j += 256) {
-      const int px = j >> 3, c8 = (j & 7) * 8;
+    uint4 q[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int j = threadIdx.x + k * 256, px = j >> 3, c8 = (j & 7) * 8;
+      const size_t o = px < npx && c8 < nc ? (size_t)(hw0 + px) * C + c0 + c8 : 0;
+      q[k] = *reinterpret_cast<const uint4*>(x + img + o);
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int j = threadIdx.x + k * 256, px = j >> 3, c8 = (j & 7) * 8;
       if (px < npx && c8 < nc) {
-        const uint4 q = *reinterpret_cast<const uint4*>(x + img + (size_t)(hw0 + px) * C + c0 + c8);
         u16 o[8];
-        __builtin_memcpy(o, &q, 16);
+        __builtin_memcpy(o, &q[k], 16);
 #pragma unroll
         for (int e = 0; e < 8; ++e) tile[(c8 + e) * RP + px] = o[e];
       }
     }
     __syncthreads();
-    for (int j = threadIdx.x; j < 512; j += 256) {
-      const int c = j >> 3, p8 = (j & 7) * 8;
-      if (c < nc && p8 < npx)
-        *reinterpret_cast<uint4*>(y + img + (size_t)(c0 + c) * HW + hw0 + p8) =
-            *reinterpret_cast<const uint4*>(tile + c * RP + p8);
+    if constexpr (VEC) {
+      for (int j = threadIdx.x; j < 512; j += 256) {
+        const int c = j >> 3, p8 = (j & 7) * 8;
+        if (c < nc && p8 < npx)
+          *reinterpret_cast<uint4*>(y + img + (size_t)(c0 + c) * HW + hw0 + p8) =
+              *reinterpret_cast<const uint4*>(tile + c * RP + p8);
+      }
+    } else {
+      for (int j = threadIdx.x; j < 4096; j += 256) {
+        const int c = j >> 6, px = j & 63;
+        if (c < nc && px < npx) y[img + (size_t)(c0 + c) * HW + hw0 + px] = tile[c * RP + px];
+      }
     }
   }
 }
@@ -261,17 +316,22 @@ bool convert_vec16(const void* xv, const TDesc& xd, void* yv, const TDesc& yd, h
   u16* y = reinterpret_cast<u16*>(yv);
   if ((a == NHWC && b == NC8) || (a == NC8 && b == NHWC)) {
     if (C % 8 != 0) return false;
-    const dim3 g((HW + 63) / 64, N);
+    const int CB = C / 8, HWT = (HW + 7) / 8, CBT = (CB + 7) / 8;
+    const long long tiles = (long long)N * CBT * HWT;
+    if (tiles >= (1ll << 31) - 4) return false;
+    const dim3 g((unsigned)((tiles + 3) / 4));
+    const FastDiv fh = make_fastdiv(HWT), fc = make_fastdiv(CBT);
     if (b == NC8)
-      SN_LAUNCH((nhwc_nc8_kernel<true>), g, dim3(256), 0, st, (const uint4*)x, (uint4*)y, HW, C / 8);
+      SN_LAUNCH((nhwc_nc8_kernel<true>), g, dim3(256), 0, st, (const uint4*)x, (uint4*)y, HW, CB, HWT, CBT,
+                (int)tiles, fh, fc);
     else
-      SN_LAUNCH((nhwc_nc8_kernel<false>), g, dim3(256), 0, st, (const uint4*)x, (uint4*)y, HW, C / 8);
+      SN_LAUNCH((nhwc_nc8_kernel<false>), g, dim3(256), 0, st, (const uint4*)x, (uint4*)y, HW, CB, HWT, CBT,
+                (int)tiles, fh, fc);
     return true;
   }
   if ((a == NCHW && b == NC8) || (a == NC8 && b == NCHW)) {
     const int CB = (C + 7) / 8;
-    const int G = HW % 8 == 0 ? 8 : HW % 4 == 0 ? 4 : 0;
-    if (!G) return false;
+    const int G = HW % 8 == 0 ? 8 : HW % 4 == 0 ? 4 : 1;
     const int groups = HW / G, total = N * CB * groups;
     const dim3 g((total + 255) / 256);
 #define NC8K(GG, T)                                                                                       \
@@ -279,18 +339,27 @@ bool convert_vec16(const void* xv, const TDesc& xd, void* yv, const TDesc& yd, h
     if (G == 8) {
       if (b == NC8) NC8K(8, true);
       else NC8K(8, false);
-    } else {
+    } else if (G == 4) {
       if (b == NC8) NC8K(4, true);
       else NC8K(4, false);
+    } else {
+      if (b == NC8) NC8K(1, true);
+      else NC8K(1, false);
     }
 #undef NC8K
     return true;
   }
   if ((a == NCHW && b == NHWC) || (a == NHWC && b == NCHW)) {
-    if (C % 8 != 0 || HW % 8 != 0 || C <= 8) return false;
+    if (C % 8 != 0 || C <= 8) return false;
     const dim3 g((HW + 63) / 64, (C + 63) / 64, N);
-    if (b == NHWC) SN_LAUNCH((nchw_nhwc_tile_kernel<true>), g, dim3(256), 0, st, x, y, C, HW);
-    else SN_LAUNCH((nchw_nhwc_tile_kernel<false>), g, dim3(256), 0, st, x, y, C, HW);
+    const bool vec = HW % 8 == 0;
+    if (b == NHWC) {
+      if (vec) SN_LAUNCH((nchw_nhwc_tile_kernel<true, true>), g, dim3(256), 0, st, x, y, C, HW);
+      else SN_LAUNCH((nchw_nhwc_tile_kernel<true, false>), g, dim3(256), 0, st, x, y, C, HW);
+    } else {
+      if (vec) SN_LAUNCH((nchw_nhwc_tile_kernel<false, true>), g, dim3(256), 0, st, x, y, C, HW);
+      else SN_LAUNCH((nchw_nhwc_tile_kernel<false, false>), g, dim3(256), 0, st, x, y, C, HW);
+    }
     return true;
   }
   return false;

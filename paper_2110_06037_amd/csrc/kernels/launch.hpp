@@ -123,7 +123,13 @@ bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r,
 void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& a, hipStream_t st);
 size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k);
 void conv_winograd(int dtype, const ConvArgs& a, hipStream_t st);
-void dwconv(int dtype, const ConvArgs& a, hipStream_t st);
+// param 0: the strip kernel (16-bit NHWC with C % 8 == 0 or NC8HW8, 3x3,
+// stride 1 or 2) with its strip length chosen by the thread count, else the
+// general kernel; param p >= 1: the strip kernel with strips of
+// dw_strip_len(p) output rows (valid for p <= dw_num_strip_params(...)).
+void dwconv(int dtype, const ConvArgs& a, int param, hipStream_t st);
+int dw_num_strip_params(int dtype, int layout, int c, int r, int s, int stride);
+int dw_strip_len(int param);
 
 void maxpool(int dtype, const void* x, const TDesc& xd, void* y, const TDesc& yd, int k,
              int stride, int pad, hipStream_t st);

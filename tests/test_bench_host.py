@@ -72,6 +72,35 @@ def test_summarize_attributes_dispatches_to_layers_and_scales_by_the_copy(tmp_pa
     assert t is None and "changed" in why
 
 
+def test_summarize_trace_averages_timed_steps_per_layer(tmp_path):
+    import json
+    b = load_bench()
+    ka, kb = "_ZN2sn1k12dw3x3_kernelIDF16bLi2ELi1ELi4EEEvNS0_7Dw3ArgsE", "void sn::k::gap_kernel<x>(y)"
+    info = {"workload": "w", "warmup": 1, "steps": 2, "routines": ["input/nchw", "r1", "r2"],
+            "launch_layers": [1, 2, 2], "bytes_needed": {"1": 3000, "2": 8000}}
+    (tmp_path / "pass.json").write_text(json.dumps(info))
+    d = tmp_path / "t"
+    d.mkdir()
+    fields = ["Dispatch_Id", "Kernel_Name", "Start_Timestamp", "End_Timestamp"]
+    with open(d / "x_kernel_trace.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=fields)
+        w.writeheader()
+        rows = [("__amd_rocclr_fillBuffer", 5)]
+        for dur in ([100, 100, 100], [10, 20, 30], [30, 40, 50]):   # warm-up step, two timed steps
+            rows += [(ka, dur[0]), (kb, dur[1]), (kb, dur[2])]
+        t = 1000
+        for k, (name, dur) in enumerate(rows):
+            w.writerow({"Dispatch_Id": k + 1, "Kernel_Name": name, "Start_Timestamp": t, "End_Timestamp": t + dur})
+            t += dur + 7
+    out = tmp_path / "o.json"
+    b.summarize_trace(str(d), str(tmp_path / "pass.json"), str(out))
+    res = json.loads(out.read_text())
+    by = {e["layer"]: e for e in res["layers"]}
+    assert by[1]["us"] == 0.02 and by[1]["gbs"] == 150.0          # (10 + 30) / 2 ns, 3000 B
+    assert by[2]["kernel_ns"] == [30.0, 40.0] and by[2]["gbs"] == round(8000 / 70, 1)
+    assert res["step_kernel_us"] == 0.09
+
+
 def test_strided_pointwise_layers_count_the_pixels_they_read():
     b = load_bench()
     from paper_2110_06037_amd import build_from_spec

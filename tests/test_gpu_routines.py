@@ -94,15 +94,17 @@ def test_conv_bit_exact_small_integers(dtype, c, k):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 # (N, C, H, W, stride): NHWC with C % 8 == 0 and NC8HW8 take the strip kernel
-# (at stride 1 strips of 4, 2 or 1 output pixels per thread by the thread
-# count; output widths not multiples of the strip leave short strips),
-# C % 8 != 0 in NHWC and NCHW the general kernel
+# (vertical strips of 4, 2 or 1 output rows per thread at stride 1, 2 or 1
+# at stride 2, by the thread count; output heights not multiples of the
+# strip leave short strips), C % 8 != 0 in NHWC and NCHW the general kernel
 @pytest.mark.parametrize("case", [(2, 32, 15, 15, 1), (1, 96, 14, 14, 2), (2, 20, 9, 9, 2),
                                   (3, 144, 30, 27, 1), (2, 960, 7, 7, 1), (1, 12, 13, 11, 2),
                                   (2, 24, 33, 34, 2),
                                   (8, 32, 112, 110, 1),    # strips of 4
+                                  (8, 32, 110, 112, 1),    # strips of 4, a short last one
                                   (4, 48, 100, 90, 1),     # strips of 2
-                                  (8, 96, 112, 111, 2)])
+                                  (8, 96, 112, 111, 2),    # stride 2, strips of 2
+                                  (8, 96, 113, 110, 2)])   # ... and a short last one
 def test_depthwise(dtype, case):
     n, c, h, w, st = case
     layer = {"type": "conv", "in": [0], "k": c, "r": 3, "s": 3, "stride": st, "pad": 1,
@@ -193,7 +195,9 @@ def test_fc_activation(dtype, case):
 @pytest.mark.parametrize("c", [12, 3, 1, 8, 72, 136])
 # H * W % 8 == 0 takes the 8-pixel transposes (40 x 40 spans several
 # 64-pixel tiles with a ragged last one), 14 x 14 the 4-pixel NC8HW8 one,
-# odd sizes the element-wise converters
+# odd sizes the 1-pixel one; NCHW <-> NHWC with H * W % 8 != 0 moves single
+# elements on the NCHW side of its tile; C % 8 != 0 takes the element-wise
+# converters
 @pytest.mark.parametrize("hw", [(9, 9), (12, 10), (40, 40), (14, 14), (7, 7)])
 def test_add_and_converters_bit_exact(dtype, c, hw):
     # two maxpools feeding an add: every (layout_a, layout_b, layout_add)
