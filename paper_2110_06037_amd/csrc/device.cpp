@@ -31,6 +31,7 @@ struct DevLayer {
 
 struct DevState {
   int device = 0;
+  unsigned* fixup_cnt = nullptr;  // kFixupMaxTiles zeroed tile counters (split reductions)
   std::vector<DevLayer> L;
   std::map<std::string, int64_t> cost_cache;  // "signature|routine" or "cvt|shape|a|b" -> ns
 };
@@ -131,6 +132,11 @@ void dev_create(Graph& g) {
   g.dev.reset(new DevState);
   g.dev->device = g.device;
   g.dev->L.resize(1);
+  // the tile counters of split-reduction launches: zero here, and every such
+  // launch leaves them at zero
+  HIPCHK(hipMalloc(&g.dev->fixup_cnt, k::kFixupMaxTiles * sizeof(unsigned)));
+  HIPCHK(hipMemset(g.dev->fixup_cnt, 0, k::kFixupMaxTiles * sizeof(unsigned)));
+  HIPCHK(hipDeviceSynchronize());
 }
 
 void plan_destroy(Graph& g) {
@@ -156,6 +162,7 @@ void dev_destroy(Graph& g) {
       if (p) (void)hipFree(p);
     if (d.bias) (void)hipFree(d.bias);
   }
+  if (g.dev->fixup_cnt) (void)hipFree(g.dev->fixup_cnt);
   g.dev.reset();
 }
 
@@ -269,6 +276,7 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
       a.act = L.d.act;
       a.ws = ws;
       a.ws_bytes = ws_bytes;
+      a.cnt = g.dev->fixup_cnt;
       a.res = L.inputs.size() > 1 ? in[1] : nullptr;
       if (L.d.groups > 1) {
         k::dwconv(dt, a, r.param, st);
@@ -310,6 +318,7 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
         a.act = L.d.act;
         a.ws = ws;
         a.ws_bytes = ws_bytes;
+        a.cnt = g.dev->fixup_cnt;
         k::conv_igemm(dt, r.param, a, st);
       } else {
         k::fc_direct(dt, in[0], xs.n, xs.c, stored_c(xs, r.layout), dl.w[dt], round8(xs.c), dl.bias, out,

@@ -56,6 +56,7 @@ size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, in
   a.M = xd.n * yd.h * yd.w;
   ig_decompose(a, c);
   if (a.splits <= 1) return 0;
+  if (c.split == 2) return (size_t)a.splits * a.tiles_m * a.tiles_n * c.bm * c.bn * sizeof(float);
   return (size_t)a.splits * a.M * a.Ng * sizeof(float);
 }
 

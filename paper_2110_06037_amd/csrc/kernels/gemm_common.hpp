@@ -55,6 +55,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, long 
 constexpr int EPI_LAYOUT = 0;  // bias + activation, store in the tensor layout
 constexpr int EPI_RAW = 1;     // raw float32 [M][Ng] (Winograd tile GEMMs)
 constexpr int EPI_SPLIT = 2;   // raw float32 partial tile of one reduction split
+constexpr int EPI_FIXUP = 3;   // reduction split whose last finishing workgroup sums the
+                               // partial tiles and runs the layout epilogue
 
 // Map the linear workgroup id to (m-tile, n-tile): consecutive ids are
 // dispatched round-robin over the 8 XCDs, so first regroup them into one

@@ -45,6 +45,7 @@ struct IgArgs {
   long long y_elems;
   float inv_pq, inv_q;         // 1/(P*Q), 1/Q for sdiv
   const void* res;             // residual [M][Ng] in the output layout, or null
+  unsigned* cnt;               // EPI_FIXUP: per-tile arrival counters (zero between launches)
 };
 
 // Element offset of GEMM position (m, n) in the output tensor's layout (the
@@ -524,9 +525,9 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a) {
 // 16-bit rows of BN + 8 values)
 template <int BM, int BN, int BK, int ST, int EPI>
 constexpr int dma_lds_bytes() {
-  return ST * (BM + BN) * BK * 2 > (EPI == EPI_LAYOUT ? BM * (BN + 4) * 4 : 0)
-             ? ST * (BM + BN) * BK * 2
-             : (EPI == EPI_LAYOUT ? BM * (BN + 4) * 4 : 0);
+  constexpr bool LAYOUT_EPI = EPI == EPI_LAYOUT || EPI == EPI_FIXUP;
+  return ST * (BM + BN) * BK * 2 > (LAYOUT_EPI ? BM * (BN + 4) * 4 : 0) ? ST * (BM + BN) * BK * 2
+                                                                         : (LAYOUT_EPI ? BM * (BN + 4) * 4 : 0);
 }
 template <int BM, int BN, int BK, int ST, int EPI, int NWV = 4>
 constexpr int dma_occ() {
@@ -559,7 +560,7 @@ void igemm_dma_kernel(IgArgs a) {
   constexpr int FM = WTM / 16, FN = WTN / 16;
   constexpr int A_BYTES = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
   constexpr int CPAD = 8;
-  constexpr int SM_C = EPI == EPI_LAYOUT ? BM * (BN + 4) * 4 : 0;  // fp32 epilogue rows
+  constexpr int SM_C = EPI == EPI_LAYOUT || EPI == EPI_FIXUP ? BM * (BN + 4) * 4 : 0;  // fp32 epilogue rows
   constexpr int SM = ST * STAGE > SM_C ? ST * STAGE : SM_C;
   __shared__ __attribute__((aligned(1024))) char smem[SM];
   auto swz = [](int row) { return (row / RPR) % CPR; };
@@ -586,7 +587,8 @@ void igemm_dma_kernel(IgArgs a) {
   for (int j = 0; j < FN; ++j)
 #pragma unroll
     for (int v = 0; v < 4; ++v) bias[j][v] = 0.f;
-  if constexpr (EPI == EPI_LAYOUT) {
+  // (a split reduction: split 0 starts at the bias, the others at zero)
+  if (EPI == EPI_LAYOUT || (EPI == EPI_FIXUP && split == 0)) {
     const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.bias, (long long)a.Ng * 4);
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
@@ -728,6 +730,76 @@ void igemm_dma_kernel(IgArgs a) {
     if constexpr (ST > 3) step(IC<3>{}, t0 + 3);
     if constexpr (ST > 4) step(IC<4>{}, t0 + 4);
     if constexpr (ST > 5) step(IC<5>{}, t0 + 5);
+  }
+
+  // split reduction summed in the kernel: every split stores its partial
+  // tile (each lane its accumulators, in lane order, so the stores and the
+  // loads that read them back are whole contiguous rows) and counts itself
+  // in at the tile's counter; the last split to arrive sums the partial
+  // tiles in split order, clears the counter for the next launch and runs
+  // the layout epilogue; the others are done.  The partial tiles bypass the
+  // per-XCD L2 caches (device-coherent accesses, cache policy sc1:
+  // written through to memory and read from it), and a workgroup's stores
+  // are complete before its count, so no cache-wide fence is needed; the
+  // counters are device-scope atomics.
+  if constexpr (EPI == EPI_FIXUP) {
+    if (a.splits > 1) {
+      constexpr int COHERENT = 16;      // sc1: coherent across the agent
+      __shared__ int fix_last;
+      constexpr int TILE = BM * BN;     // fp32 values of a partial tile
+      const __amdgpu_buffer_rsrc_t rp =
+          make_rsrc(a.part, (long long)a.splits * gridDim.x * TILE * (long long)sizeof(float));
+      const unsigned slot0 = (unsigned)blockIdx.x * (unsigned)a.splits * (unsigned)(TILE * 4);
+      auto lane_off = [&](int sp, int i, int j) {
+        return slot0 + (unsigned)sp * (TILE * 4) + (unsigned)(((i * FN + j) * NT + tid) * 16);
+      };
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[i][j]), rp,
+                                                 (int)lane_off(split, i, j), 0, COHERENT);
+      wait_vmcnt<0>();
+      __syncthreads();
+      if (tid == 0)
+        fix_last = __hip_atomic_fetch_add(a.cnt + blockIdx.x, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                   (unsigned)(a.splits - 1);
+      __syncthreads();
+      if (!fix_last) return;
+      // the partial tiles are summed in split order whichever split is last,
+      // so the result does not depend on the order the workgroups finish in;
+      // the next split's loads are in flight while one is added
+      f32x4 sum[FM][FN];
+      u32x4 cur[FM][FN], nxt[FM][FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          sum[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+          cur[i][j] = __builtin_amdgcn_raw_buffer_load_b128(rp, (int)lane_off(0, i, j), 0, COHERENT);
+        }
+      for (int sp = 0; sp < a.splits; ++sp) {
+        if (sp + 1 < a.splits) {
+#pragma unroll
+          for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+              nxt[i][j] = __builtin_amdgcn_raw_buffer_load_b128(rp, (int)lane_off(sp + 1, i, j), 0, COHERENT);
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) {
+            sum[i][j] += sp == split ? acc[i][j] : __builtin_bit_cast(f32x4, cur[i][j]);
+            cur[i][j] = nxt[i][j];
+          }
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = sum[i][j];
+      if (tid == 0) __hip_atomic_exchange(a.cnt + blockIdx.x, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 
   // accumulator element (i, j, v) is C[wm*WTM + i*16 + (lane&15)][wn*WTN + j*16 + (lane>>4)*4 + v]
@@ -897,7 +969,9 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(IgArgs a) {
 
 // Routine parameters of the implicit-GEMM routine (index = routine param).
 struct IgCfg {
-  int bm, bn, bk, split, pf;  // split: 0 = none, 1 = split the reduction when tiles are few;
+  int bm, bn, bk, split, pf;  // split: 0 = none, 1 = split the reduction when tiles are few
+                              // (partials summed by a second kernel), 2 = likewise, summed by
+                              // the last workgroup of each tile (LDS-DMA kernel only);
                               // pf: prefetch depth (register staging sets)
   int dma = 0, wm = 2, st = 2;  // 1: LDS-DMA kernel, 2: 3x3 patch kernel (bm = 16 * row blocks),
                                 // 3: small-channel kernel, 4: streaming 1x1 kernel (C = bk);
@@ -943,6 +1017,11 @@ static const IgCfg kIg16[] = {
 #define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM},
     STREAM_CONFIGS(SN_STREAM_IG)
 #undef SN_STREAM_IG
+    // LDS-DMA kernel, 8 waves, reduction split over workgroups when the
+    // tiles alone cannot fill the GPU (the last split of a tile sums them)
+    {128, 128, 64, 2, 0, 1, 4, 3, 0, {}, 8}, {128, 64, 64, 2, 0, 1, 4, 4, 0, {}, 8},
+    {64, 128, 64, 2, 0, 1, 2, 4, 0, {}, 8},  {64, 64, 64, 2, 0, 1, 2, 4, 0, {}, 8},
+    {64, 64, 64, 2, 0, 1, 2, 6, 0, {}, 8},   {128, 128, 32, 2, 0, 1, 4, 4, 0, {}, 8},
 };
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 
@@ -961,9 +1040,16 @@ static void ig_decompose(IgArgs& a, const IgCfg& c) {
   const int cpr = c.bk / 8;
   const int KT = (a.KC + cpr - 1) / cpr;
   int splits = 1;
-  if (c.split) {
-    const int tiles = a.tiles_m * a.tiles_n;
+  const int tiles = a.tiles_m * a.tiles_n;
+  if (c.split == 1) {
     if (tiles < 384) splits = std::min(std::min((768 + tiles - 1) / tiles, 8), std::max(1, KT / 2));
+  } else if (c.split == 2) {
+    // as many splits as still run in one round of resident workgroups (the
+    // LDS stages bound the workgroups per CU), each at least two reduction
+    // steps long
+    const int lds = std::max(c.st * (c.bm + c.bn) * c.bk * 2, c.bm * (c.bn + 4) * 4);
+    const int resident = 256 * std::max(1, std::min(160 * 1024 / lds, 2));
+    if (2 * tiles <= resident) splits = std::min(std::min(resident / tiles, 8), std::max(1, KT / 2));
   }
   a.kt_per = (KT + splits - 1) / splits;
   a.splits = (KT + a.kt_per - 1) / a.kt_per;
@@ -1008,6 +1094,18 @@ static void igemm_dma_cfg(const IgCfg& c, const IgArgs& a, hipStream_t st) {
     }
     return;
   }
+  if constexpr (EPI == EPI_FIXUP) {
+    switch (key) {
+      IGDN(128, 128, 64, 4, 3, 8)
+      IGDN(128, 64, 64, 4, 4, 8)
+      IGDN(64, 128, 64, 2, 4, 8)
+      IGDN(64, 64, 64, 2, 4, 8)
+      IGDN(64, 64, 64, 2, 6, 8)
+      IGDN(128, 128, 32, 4, 4, 8)
+      default: check(false, "LDS-DMA tile not instantiated for split reduction");
+    }
+    return;
+  } else if constexpr (EPI == EPI_LAYOUT) {
   switch (key) {
     IGD(128, 128, 64, 2, 2)
     IGD(128, 128, 64, 2, 3)
@@ -1039,6 +1137,7 @@ static void igemm_dma_cfg(const IgCfg& c, const IgArgs& a, hipStream_t st) {
     IGDN(128, 128, 32, 4, 6, 8)
     IGDN(64, 64, 64, 2, 6, 8)
     default: check(false, "LDS-DMA tile not instantiated");
+  }
   }
 #undef IGD
 #undef IGDN
@@ -1140,6 +1239,18 @@ static IgArgs make_ig(const ConvArgs& c) {
 
 template <typename T, int L, bool VEC>
 static void igemm_run(const IgCfg& cfg, IgArgs& a, const ConvArgs& c, hipStream_t st) {
+  if (cfg.split == 2) {
+    // one kernel: with a single split it is the plain layout epilogue
+    if (a.splits > 1) {
+      check(c.ws && c.ws_bytes >= (size_t)a.splits * a.tiles_m * a.tiles_n * cfg.bm * cfg.bn * sizeof(float),
+            "split-K workspace too small");
+      check(c.cnt && a.tiles_m * a.tiles_n <= kFixupMaxTiles, "split-K tile counters");
+      a.part = reinterpret_cast<float*>(c.ws);
+      a.cnt = c.cnt;
+    }
+    igemm_cfg<T, L, VEC, EPI_FIXUP>(cfg, a, 1, st);
+    return;
+  }
   if (a.splits > 1) {
     check(c.ws && c.ws_bytes >= (size_t)a.splits * a.M * a.Ng * sizeof(float), "split-K workspace too small");
     a.part = reinterpret_cast<float*>(c.ws);

@@ -45,6 +45,12 @@ struct TDesc {
   int n, c, h, w, cs, layout;
 };
 
+// Tile counters of implicit-GEMM launches whose reduction is split across
+// workgroups (the last workgroup of a tile to finish sums the partial
+// tiles): tile ids stay below this bound, and a caller's counter array
+// holds this many.
+constexpr int kFixupMaxTiles = 1024;
+
 struct ConvArgs {
   const void* x;
   TDesc xd;
@@ -57,6 +63,8 @@ struct ConvArgs {
   size_t ws_bytes;
   const void* res = nullptr;  // residual of the output's shape and layout, added before the
                               // activation (direct and implicit-GEMM routines), or null
+  unsigned* cnt = nullptr;    // kFixupMaxTiles tile counters for reductions split across
+                              // workgroups: zero before a launch, zero again after it
 };
 
 void conv_direct(int dtype, const ConvArgs& a, hipStream_t st);

@@ -6,6 +6,7 @@
 #include <stdexcept>
 #include <string>
 
+#include "gemm_common.hpp"
 #include "kcommon.hpp"
 #include "launch.hpp"
 
@@ -16,9 +17,6 @@ thread_local LaunchTiming g_timing;
 thread_local long long g_launches = 0;
 thread_local int g_count_only = 0;
 
-static void check(bool ok, const char* what) {
-  if (!ok) throw std::invalid_argument(std::string("kernel launch: ") + what);
-}
 
 static unsigned blocks(long long n, int per = 256) { return (unsigned)((n + per - 1) / per); }
 
@@ -76,7 +74,32 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const T* __restrict__ x, T
     float m[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) m[e] = -INFINITY;
-    for (int r = 0; r < k; ++r) {
+    const bool fast = sizeof(T) == 2 && vec && k == 3;
+    if constexpr (sizeof(T) == 2) if (fast) {
+      // the 3x3 window (every pooling layer of the nets here): all nine
+      // 16-byte loads are issued at once through a buffer resource (taps
+      // outside the image read zero past its end and are masked out of the
+      // maximum), instead of one load round trip per tap
+      const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (long long)N * H * W * ((Cs + 7) / 8 * 8) * sizeof(T));
+      u32x4 raw[9];
+      bool ok[9];
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int h = p * st - pad + t / 3, w = q * st - pad + t % 3;
+        ok[t] = (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+        unsigned off;
+        if constexpr (L == NC8) off = (((unsigned)(n * CB + cb) * (unsigned)H + (unsigned)h) * (unsigned)W + (unsigned)w) * 8u;
+        else off = ((unsigned)(n * H + h) * (unsigned)W + (unsigned)w) * (unsigned)Cs + (unsigned)cb * 8u;
+        raw[t] = __builtin_amdgcn_raw_buffer_load_b128(rx, ok[t] ? (int)(off * sizeof(T)) : (int)kOOB, 0, 0);
+      }
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const V8<T> v = __builtin_bit_cast(V8<T>, raw[t]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m[e] = ok[t] ? fmaxf(m[e], to_f(v.v[e])) : m[e];
+      }
+    }
+    for (int r = 0; r < (fast ? 0 : k); ++r) {
       const int h = p * st - pad + r;
       if ((unsigned)h >= (unsigned)H) continue;
       for (int s = 0; s < k; ++s) {

@@ -312,3 +312,47 @@ def test_conv_with_projection_residual_every_routine(dtype, ci):
     g.close()
     if c in (64, 128, 256):
         assert any("nhwc/igemm" in nm for nm in names)
+
+
+# The last six implicit-GEMM parameters split the reduction over workgroups
+# when the tiles alone are few, and the last workgroup of each tile to finish
+# sums the partial tiles (per-tile counters that every launch leaves at zero).
+SPLIT_PARAMS = range(77, 83)
+SPLIT_CASES = [
+    # (N, C, H, W, K, R, stride, act): ResNet-50 small-M layers (batch cut) and ragged tiles
+    (8, 512, 14, 14, 512, 3, 2, "relu"),    # stage-4 first 3x3 (stride 2)
+    (8, 2048, 7, 7, 512, 1, 1, "relu"),     # stage-4 reduce
+    (4, 1024, 14, 14, 256, 1, 1, "relu"),   # stage-3 reduce
+    (3, 64, 9, 7, 40, 3, 1, "relu6"),       # ragged M and N, few reduction steps
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("ci", range(len(SPLIT_CASES)))
+def test_split_reduction_routines_repeat_exactly(dtype, ci):
+    # every split routine against the oracle, and three launches in a row
+    # give the same bits (the partial tiles are summed in a fixed order, and
+    # a counter left non-zero would make a tile skip or double its sum on the
+    # next launch); then a launch on another input must not see any partial
+    # tile of the previous ones (the slots are reused)
+    n, c, h, w, k, r, st, act = SPLIT_CASES[ci]
+    layer = {"type": "conv", "in": [0], "k": k, "r": r, "s": r, "stride": st, "pad": r // 2,
+             "groups": 1, "act": act}
+    x = random_tensor((n, c, h, w), dtype, seed=70 + ci)
+    wt = random_tensor((k, c, r, r), dtype, seed=80 + ci, dist="normal", scale=np.sqrt(2 / (c * r * r)))
+    b = random_tensor((k,), "f32", seed=90 + ci, scale=0.1)
+    x2 = random_tensor((n, c, h, w), dtype, seed=170 + ci)
+    ref = oracle_layer(layer, x, wt, b, dtype)
+    ref2 = oracle_layer(layer, x2, wt, b, dtype)
+    g = single_layer_graph(dtype, (n, c, h, w), layer, wt, b)
+    xd, xd2 = to_dev(x, dtype), to_dev(x2, dtype)
+    split = [rt for rt in g.routines(1) if rt["algo"] == 1 and rt["param"] in SPLIT_PARAMS]
+    assert split, "the split routines apply"
+    for rt in split:
+        outs = [from_dev(run_routine(g, rt["id"], xd), dtype) for _ in range(3)]
+        e = err(outs[0], ref, dtype)
+        e2 = err(from_dev(run_routine(g, rt["id"], xd2), dtype), ref2, dtype)
+        print(f"{dtype} split case{ci} {rt['name']}: err {e:.2e}, other input {e2:.2e}", flush=True)
+        assert e <= TOL[dtype] and e2 <= TOL[dtype], (rt["name"], e, e2)
+        assert all(np.array_equal(o, outs[0]) for o in outs[1:]), rt["name"]
+    g.close()
