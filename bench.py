@@ -54,11 +54,15 @@ def layer_work(spec, g, i, routine):
         r, s, grp = layer["r"], layer["s"], layer["groups"]
         wbytes = k * (c // grp) * r * s * es
         byt = es * (n * c * h * w + n * k * p * q) + wbytes + 4 * k
-        if len(layer["in"]) > 1:  # residual read in the epilogue
+        flops = 2 * n * k * c * r * s * p * q
+        if layer.get("proj"):  # the shortcut (whole, by the formula) and its 1x1 weights
+            _, c2, h2, w2 = ins[1]
+            byt += es * (n * c2 * h2 * w2 + k * c2)
+            flops += 2 * n * k * c2 * p * q
+        elif len(layer["in"]) > 1:  # residual read in the epilogue
             byt += es * n * k * p * q
         if grp > 1:
             return "dwconv", 2 * n * k * r * s * p * q, byt
-        flops = 2 * n * k * c * r * s * p * q
         if routine["algo"] == 2:  # Winograd: the MFMA work is the 16 tile GEMMs
             tiles = n * ((h + 1) // 2) * ((w + 1) // 2)
             flops = 2 * 16 * k * c * tiles
@@ -81,11 +85,15 @@ def bytes_needed(spec, g, i, routine):
     pixel in s x s (the formula of layer_work counts the whole input)."""
     _, _, byt = layer_work(spec, g, i, routine)
     layer = spec["layers"][i - 1]
+    es = 4 if spec["dtype"] == "f32" else 2
     if layer["type"] == "conv" and layer["r"] == 1 and layer["s"] == 1 and layer["pad"] == 0 and layer["stride"] > 1:
-        es = 4 if spec["dtype"] == "f32" else 2
         n, k, p, q = g.layer_shape(i)
         _, c, h, w = g.layer_shape(layer["in"][0])
         byt -= es * n * c * (h * w - p * q)
+    if layer.get("proj") and layer["proj"]["stride"] > 1:  # a strided shortcut: the pixels read
+        n, k, p, q = g.layer_shape(i)
+        _, c2, h2, w2 = g.layer_shape(layer["in"][1])
+        byt -= es * n * c2 * (h2 * w2 - p * q)
     return byt
 
 
@@ -129,12 +137,15 @@ def _traffic_summary(path=TRAFFIC_FILE):
         return {}
 
 
-def traffic_for_layers(layers, routine, summary=None):
+def traffic_for_layers(layers, routine, summary=None, workload=None):
     """HBM bytes per launch of `routine` averaged over `layers` from the
-    committed per-layer PMC summary: only when the summary holds every one of
-    those layers run by this same routine, with kernel sources unchanged
-    since the counters were taken; else (None, reason)."""
+    committed per-layer PMC summary: only when the summary was taken on this
+    workload and holds every one of those layers run by this same routine,
+    with kernel sources unchanged since the counters were taken; else
+    (None, reason)."""
     summary = _traffic_summary() if summary is None else summary
+    if workload is not None and summary.get("workload") != workload:
+        return None, f"no counter summary for workload {workload}"
     by_layer = {e["layer"]: e for e in summary.get("layers", [])}
     tot = 0
     for i in layers:
@@ -344,10 +355,8 @@ def cpu_baseline(spec, t, budget_s, storage="dtype"):
     parity mode) or exact (storage "f64")."""
     import numpy as np
     from oracle import numeric as O
-    from workloads import to_f64, with_batch
-    d = {"x": to_f64(t["x"], spec["dtype"]),
-         "w": [None if w is None else to_f64(w, spec["dtype"]) for w in t["w"]],
-         "b": [None if b is None else b.astype(np.float64) for b in t["b"]]}
+    from workloads import decode, with_batch
+    d = decode(t, spec["dtype"])
     done = 0
     t0 = time.perf_counter()
     while done < spec["batch"]:
@@ -387,6 +396,9 @@ def main():
     ap.add_argument("--no-fuse", action="store_true",
                     help="keep residual adds as their own layers (default: fold each into the 1x1 "
                          "convolution that produces its operand)")
+    ap.add_argument("--no-proj", action="store_true",
+                    help="keep projection shortcuts as their own 1x1 convolutions (default: fold each, "
+                         "with its residual add, into the convolution the add follows)")
     ap.add_argument("--integrated-reps", type=int, default=20,
                     help="runs per candidate in integrated profiling (0 = keep the DPRS path)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -434,11 +446,13 @@ def main():
     import numpy as np
     import torch
     from paper_2110_06037_amd import build_from_spec, native as N, to_device as to_dev
-    from workloads import fuse_residual, generate, resnet50
+    from workloads import fuse_projection, fuse_residual, generate, resnet50
 
     spec = _nets()[args.net](args.batch, args.dtype)
     if not args.no_fuse:
         spec = fuse_residual(spec)
+        if not args.no_proj:
+            spec = fuse_projection(spec)
     t = generate(spec)
     log(f"[bench] {spec['name']}: building graph")
     g = build_from_spec(spec, t, device=0)
@@ -603,9 +617,7 @@ def main():
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     # HBM traffic from the committed per-layer counter summary, only where it
     # covers these very layers run by this routine (else null, with the reason)
-    traffic, why = (traffic_for_layers(dom["layers"], dom["routine"])
-                    if (args.net, args.batch, args.dtype) == ("resnet50", 32, "bf16") and not args.no_fuse
-                    else (None, "no counter summary for this workload"))
+    traffic, why = traffic_for_layers(dom["layers"], dom["routine"], workload=spec["name"])
     roof["traffic"] = traffic
     if traffic:
         roof["traffic_ratio"] = round(traffic / (dom["bytes"] / dom["launches"]), 3)
@@ -679,6 +691,8 @@ def main():
         spec1 = resnet50(1, args.dtype)
         if not args.no_fuse:
             spec1 = fuse_residual(spec1)
+            if not args.no_proj:
+                spec1 = fuse_projection(spec1)
         t1_ = generate(spec1)
         g1 = build_from_spec(spec1, t1_, device=0)
         g1.profile(warmup=5, reps=args.profile_reps)

@@ -182,6 +182,30 @@ int sn_set_option(sn_graph* g, int32_t option, int64_t value);
 int sn_add_layer(sn_graph* g, const sn_layer_desc* d, const int32_t* inputs, int32_t n_inputs,
                  const void* weight, const float* bias, int32_t* out_id);
 
+/* Appends a dense convolution whose output also takes a projected shortcut:
+ *   y = act(conv(x) + bias + conv1x1_stride(shortcut, shortcut_weight) + shortcut_bias)
+ * with x = layer `input` (d describes the convolution: CONV2D, groups 1) and
+ * the shortcut = layer `shortcut` (N x C2 x H2 x W2) read by a 1 x 1
+ * convolution without padding at `shortcut_stride`, whose output has the
+ * convolution's output shape.  This is the residual add of a bottleneck
+ * block with a projection shortcut, folded together with the projection
+ * into the convolution that produces the add's other operand (layer fusion,
+ * Sec. III-A): one layer of two inputs whose routines compute both products
+ * in one reduction (implicit GEMM on the LDS-DMA tiles, 16-bit channel-vector
+ * layouts with C and C2 multiples of the tile depth) or, in any layout and
+ * dtype, as the projection followed by the convolution with a residual
+ * (direct routine, two launches and a workspace).  weight: OIHW [K][C][R][S],
+ * shortcut_weight [K][C2] in the run dtype, host memory, copied; biases
+ * float32 [K] or NULL = zeros (the two are summed in float64 and rounded
+ * once to float32).
+ * Errors: SN_E_INVALID (unknown ids, not CONV2D, groups != 1, stride < 1,
+ * missing weights), SN_E_SHAPE (the shortcut projection does not give the
+ * output's batch and size), SN_E_UNSUPPORTED, SN_E_STATE, SN_E_DEVICE as for
+ * sn_add_layer. */
+int sn_add_projected_conv(sn_graph* g, const sn_layer_desc* d, int32_t input, int32_t shortcut,
+                          int32_t shortcut_stride, const void* weight, const float* bias,
+                          const void* shortcut_weight, const float* shortcut_bias, int32_t* out_id);
+
 /* Adds a further net input (multi-input nets, Sec. IV-E): an input layer
  * carrying the caller's tensor N x c x h x w (N of the graph, run dtype,
  * NCHW), with one routine of time 0.  The paper joins the inputs of such a

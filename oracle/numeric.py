@@ -145,6 +145,14 @@ def round_to(a, dtype):
 def layer_forward(layer, inputs, w=None, b=None):
     t = layer["type"]
     if t == "conv":
+        if layer.get("proj"):
+            # projected shortcut (a bottleneck block's residual add with its
+            # 1x1 projection, folded into the convolution): the two
+            # convolutions and their biases summed, then the activation
+            (wm, wp), (bm, bp) = w, b
+            y = conv2d(inputs[0], wm, bm, layer["stride"], layer["pad"], 1, "none")
+            y = y + conv2d(inputs[1], wp, bp, layer["proj"]["stride"], 0, 1, "none")
+            return activate(y, layer["act"])
         if len(inputs) > 1:  # residual added before the activation
             y = conv2d(inputs[0], w, b, layer["stride"], layer["pad"], layer["groups"], "none")
             return add(y, inputs[1], layer["act"])
@@ -200,7 +208,7 @@ def forward(spec, tensors, storage="dtype", keep=None, layer_dtypes=None):
         if storage == "dtype":
             ins = [x if ldt[j] == ldt[i] else round_to(x, ldt[i]) for x, j in zip(ins, layer["in"])]
             if ldt[i] != dtype and w is not None:
-                w = round_to(w, ldt[i])
+                w = tuple(round_to(v, ldt[i]) for v in w) if isinstance(w, tuple) else round_to(w, ldt[i])
         y = layer_forward(layer, ins, w, tensors["b"][i - 1])
         if storage == "dtype":
             y = round_to(y, ldt[i])

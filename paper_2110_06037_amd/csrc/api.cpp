@@ -137,6 +137,18 @@ int sn_add_layer(sn_graph* gp, const sn_layer_desc* d, const int32_t* inputs, in
   });
 }
 
+int sn_add_projected_conv(sn_graph* gp, const sn_layer_desc* d, int32_t input, int32_t shortcut,
+                          int32_t shortcut_stride, const void* weight, const float* bias,
+                          const void* shortcut_weight, const float* shortcut_bias, int32_t* out_id) {
+  return guarded([&] {
+    CHECK_G(gp);
+    if (!d) fail(SN_E_INVALID, "null layer description");
+    int id = graph_add_projected(gp->g, *d, input, shortcut, shortcut_stride, weight, bias, shortcut_weight,
+                                 shortcut_bias);
+    if (out_id) *out_id = id;
+  });
+}
+
 int sn_add_input(sn_graph* gp, int32_t c, int32_t h, int32_t w, int32_t* out_id) {
   return guarded([&] {
     CHECK_G(gp);

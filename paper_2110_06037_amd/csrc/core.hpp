@@ -97,6 +97,11 @@ struct Layer {
   // host copies of the user's weights (run dtype bytes, OIHW / [K][C]) and bias
   std::vector<uint8_t> weight;
   std::vector<float> bias;
+  // CONV2D with a projected shortcut (second input read by a 1 x 1
+  // convolution at proj_stride): its weights [K][C2] and bias
+  int proj_stride = 0;
+  std::vector<uint8_t> wproj;
+  std::vector<float> bproj;
   std::vector<Routine> routines;
   std::vector<int64_t> cost;  // per routine, ns; -1 = not profiled
   std::string signature;      // identical signatures share profiling results
@@ -164,6 +169,8 @@ void graph_init(Graph& g, int dtype, Shape in, int device);
 int graph_add_input(Graph& g, int c, int h, int w);
 void graph_mark_output(Graph& g, int layer);
 std::vector<int> net_outputs(const Graph& g);
+int graph_add_projected(Graph& g, const sn_layer_desc& d, int input, int shortcut, int stride,
+                        const void* weight, const float* bias, const void* sc_weight, const float* sc_bias);
 int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int n_inputs,
                     const void* weight, const float* bias);
 // all edges including the one into the auxiliary output layer (id = n_layers())

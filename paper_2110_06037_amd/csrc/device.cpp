@@ -26,7 +26,9 @@ static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 struct DevLayer {
   void* w[3] = {};      // per dtype: dense [Kp][R][S][C8] | depthwise [R][S][C8] | fc [Kp][C8]
   void* wu[3] = {};     // per dtype: Winograd U [16][Kp][C8]
-  float* bias = nullptr;  // [Kp]
+  void* wp[3] = {};     // per dtype: projected-shortcut weights [Kp][C2_8]
+  float* bias = nullptr;  // [Kp] (with a projected shortcut: the two biases summed)
+  float* zbias = nullptr;  // [Kp] zeros (the shortcut's own launch in the two-launch routine)
 };
 
 struct DevState {
@@ -160,7 +162,10 @@ void dev_destroy(Graph& g) {
       if (p) (void)hipFree(p);
     for (void* p : d.wu)
       if (p) (void)hipFree(p);
+    for (void* p : d.wp)
+      if (p) (void)hipFree(p);
     if (d.bias) (void)hipFree(d.bias);
+    if (d.zbias) (void)hipFree(d.zbias);
   }
   if (g.dev->fixup_cnt) (void)hipFree(g.dev->fixup_cnt);
   g.dev.reset();
@@ -181,6 +186,11 @@ void dev_upload_layer(Graph& g, int id) {
   const int K = L.out.c, Kp = round8(K), C = in.c, C8 = round8(C);
   std::vector<float> bias(Kp, 0.f);
   std::copy(L.bias.begin(), L.bias.end(), bias.begin());
+  if (L.proj_stride > 0) {  // the two biases, summed in float64 and rounded once
+    for (int kk = 0; kk < K; ++kk) bias[kk] = (float)((double)L.bias[kk] + (double)L.bproj[kk]);
+    std::vector<float> z(Kp, 0.f);
+    dl.zbias = static_cast<float*>(dev_upload(z.data(), z.size() * 4));
+  }
   dl.bias = static_cast<float*>(dev_upload(bias.data(), bias.size() * 4));
   const uint8_t* src = L.weight.data();
   const int R = L.d.r, S = L.d.s;
@@ -216,6 +226,17 @@ void dev_upload_layer(Graph& g, int id) {
           for (int s2 = 0; s2 < S; ++s2)
             put(&w[((((size_t)kk * R + r) * S + s2) * C8 + c) * es], (((size_t)kk * C + c) * R + r) * S + s2);
     dl.w[dt] = dev_upload(w.data(), w.size());
+    if (L.proj_stride > 0) {  // shortcut [K][C2] -> [Kp][C2_8]
+      const int C2 = g.layers[L.inputs[1]].out.c, C28 = round8(C2);
+      std::vector<uint8_t> w2((size_t)Kp * C28 * es, 0);
+      for (int kk = 0; kk < K; ++kk)
+        for (int c = 0; c < C2; ++c) {
+          const size_t e = (size_t)kk * C2 + c;
+          if (dt == g.dtype) std::memcpy(&w2[((size_t)kk * C28 + c) * es], L.wproj.data() + e * ies, ies);
+          else encode(decode(L.wproj.data() + e * ies, g.dtype), dt, &w2[((size_t)kk * C28 + c) * es]);
+        }
+      dl.wp[dt] = dev_upload(w2.data(), w2.size());
+    }
     if (winograd_applicable(L, in)) {
       // U = G g G^T per (k, c), in float64 from the caller's weights, rounded
       // once to the dtype
@@ -247,6 +268,12 @@ static size_t layer_ws_bytes(const Graph& g, const Layer& L, const Routine& r) {
   if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM)
     return k::igemm_ws_bytes(r.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), 1, 1);
   if (L.type != SN_LAYER_CONV2D || L.d.groups > 1) return 0;
+  if (L.proj_stride > 0) {
+    if (r.algo == SN_ALGO_DIRECT)  // the shortcut's projection, stored in the output's schema
+      return align256((size_t)stored_numel(L.out, r.layout) * dtype_size(r.dtype));
+    return k::igemm_ws_bytes(r.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), L.d.r, L.d.s,
+                             g.layers[L.inputs[1]].out.c);
+  }
   if (r.algo == SN_ALGO_WINOGRAD)  // the fused routines keep their transforms on chip
     return r.param == 0 ? k::winograd_ws_bytes(r.dtype, tdesc(in, r.layout), L.out.c) : 0;
   if (r.algo == SN_ALGO_IGEMM)
@@ -278,6 +305,37 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
       a.ws_bytes = ws_bytes;
       a.cnt = g.dev->fixup_cnt;
       a.res = L.inputs.size() > 1 ? in[1] : nullptr;
+      if (L.proj_stride > 0) {
+        a.res = nullptr;
+        if (r.algo == SN_ALGO_DIRECT) {
+          // two launches: the shortcut's 1 x 1 projection (bias zero, no
+          // activation) into the workspace, then the convolution adding it
+          k::ConvArgs p = a;
+          p.x = in[1];
+          p.xd = ind[1];
+          p.w = dl.wp[dt];
+          p.bias = dl.zbias;
+          p.y = ws;
+          p.r = p.s = 1;
+          p.stride = L.proj_stride;
+          p.pad = 0;
+          p.act = SN_ACT_NONE;
+          p.ws = nullptr;
+          p.ws_bytes = 0;
+          k::conv_direct(dt, p, st);
+          a.res = ws;
+          a.ws = nullptr;
+          a.ws_bytes = 0;
+          k::conv_direct(dt, a, st);
+        } else {
+          a.x2 = in[1];
+          a.x2d = ind[1];
+          a.w2 = dl.wp[dt];
+          a.stride2 = L.proj_stride;
+          k::conv_igemm(dt, r.param, a, st);
+        }
+        break;
+      }
       if (L.d.groups > 1) {
         k::dwconv(dt, a, r.param, st);
       } else if (r.algo == SN_ALGO_DIRECT) {

@@ -154,6 +154,22 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
       if (!(g.opt_layouts >> lay & 1)) continue;
       switch (L.type) {
         case SN_LAYER_CONV2D:
+          if (L.proj_stride > 0) {
+            // projection, then the convolution with it as residual (two
+            // launches, any layout and dtype); both products in one
+            // reduction on the LDS-DMA tiles
+            add(lay, SN_ALGO_DIRECT, 0);
+            if (g.opt_algos >> SN_ALGO_IGEMM & 1) {
+              const Shape& sc = g.layers[L.inputs[1]].out;
+              for (int p = 0; p < k::igemm_num_params(dt); ++p)
+                if (k::igemm_param_takes_projection(dt, p, lay, in.n, in.c, in.h, in.w, L.d.r, L.d.s,
+                                                    L.d.stride, L.d.pad, L.d.k, sc.c)) {
+                  add(lay, SN_ALGO_IGEMM, p);
+                  if (!g.opt_params) break;
+                }
+            }
+            break;
+          }
           if (is_depthwise(L, in)) {
             add(lay, SN_ALGO_DIRECT, 0);  // depthwise has its own direct routine
             if (g.opt_params)             // ... and strip lengths as routine parameters
@@ -196,7 +212,7 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
 static std::string signature(const Graph& g, const Layer& L) {
   std::ostringstream o;
   o << "t" << L.type << " k" << L.d.k << " r" << L.d.r << " s" << L.d.s << " st" << L.d.stride
-    << " p" << L.d.pad << " g" << L.d.groups << " a" << L.d.act << " dt" << g.dtype;
+    << " p" << L.d.pad << " g" << L.d.groups << " a" << L.d.act << " dt" << g.dtype << " pj" << L.proj_stride;
   for (int j : L.inputs) {
     const Shape& s = g.layers[j].out;
     o << " [" << s.n << "," << s.c << "," << s.h << "," << s.w << "]";
@@ -204,8 +220,11 @@ static std::string signature(const Graph& g, const Layer& L) {
   return o.str();
 }
 
-int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int n_inputs,
-                    const void* weight, const float* bias) {
+// proj_stride > 0: a CONV2D whose second input is a shortcut projected by a
+// 1 x 1 convolution (sc_weight, sc_bias) and added before the activation
+static int add_layer_impl(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int n_inputs,
+                          const void* weight, const float* bias, int proj_stride, const void* sc_weight,
+                          const float* sc_bias) {
   if (!g.path.empty()) fail(SN_E_STATE, "cannot add layers after a path was selected");
   Layer L;
   L.id = g.n_layers();
@@ -239,7 +258,13 @@ int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int
         fail(SN_E_SHAPE, "kernel larger than the padded input");
       out = {in.n, d.k, outdim(in.h, d.r, d.stride, d.pad), outdim(in.w, d.s, d.stride, d.pad)};
       wbytes = (int64_t)d.k * (in.c / d.groups) * d.r * d.s * ds;
-      if (L.inputs.size() == 2) {
+      if (L.inputs.size() == 2 && proj_stride > 0) {
+        const Shape& sc = g.layers[L.inputs[1]].out;
+        if (d.groups != 1) fail(SN_E_INVALID, "a projected shortcut needs a dense convolution");
+        if (sc.n != out.n || (sc.h - 1) / proj_stride + 1 != out.h || (sc.w - 1) / proj_stride + 1 != out.w)
+          fail(SN_E_SHAPE, "the projected shortcut does not give the output's size");
+        if (!sc_weight) fail(SN_E_INVALID, "a projected shortcut needs weights");
+      } else if (L.inputs.size() == 2) {
         if (d.groups != 1) fail(SN_E_UNSUPPORTED, "a residual input needs a dense convolution");
         if (!(g.layers[L.inputs[1]].out == out)) fail(SN_E_SHAPE, "residual differs from the output shape");
       }
@@ -278,6 +303,14 @@ int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int
     L.bias.assign(out.c, 0.f);
     if (bias) std::memcpy(L.bias.data(), bias, sizeof(float) * out.c);
   }
+  if (proj_stride > 0) {
+    const int64_t pbytes = (int64_t)out.c * g.layers[L.inputs[1]].out.c * ds;
+    L.proj_stride = proj_stride;
+    L.wproj.resize(pbytes);
+    std::memcpy(L.wproj.data(), sc_weight, pbytes);
+    L.bproj.assign(out.c, 0.f);
+    if (sc_bias) std::memcpy(L.bproj.data(), sc_bias, sizeof(float) * out.c);
+  }
   L.signature = signature(g, L);
   g.layers.push_back(std::move(L));
   Layer& ref = g.layers.back();
@@ -287,6 +320,19 @@ int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int
   g.have_costs = false;
   if (!g.host_only()) dev_upload_layer(g, ref.id);
   return ref.id;
+}
+
+int graph_add_layer(Graph& g, const sn_layer_desc& d, const int32_t* inputs, int n_inputs,
+                    const void* weight, const float* bias) {
+  return add_layer_impl(g, d, inputs, n_inputs, weight, bias, 0, nullptr, nullptr);
+}
+
+int graph_add_projected(Graph& g, const sn_layer_desc& d, int input, int shortcut, int stride,
+                        const void* weight, const float* bias, const void* sc_weight, const float* sc_bias) {
+  if (d.type != SN_LAYER_CONV2D) fail(SN_E_INVALID, "a projected shortcut belongs to a convolution");
+  if (stride < 1) fail(SN_E_INVALID, "shortcut stride must be >= 1");
+  const int32_t ins[2] = {input, shortcut};
+  return add_layer_impl(g, d, ins, 2, weight, bias, stride, sc_weight, sc_bias);
 }
 
 }  // namespace sn

@@ -43,7 +43,15 @@ bool igemm_param_takes_residual(int dtype, int param, int layout, int k) {
   return g.dma == 0 || (g.dma == 1 && (layout == NC8 || k % 8 == 0)) || (g.dma == 4 && layout == NHWC && k % 8 == 0);
 }
 
-size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s) {
+bool igemm_param_takes_projection(int dtype, int param, int layout, int n, int c, int h, int w, int r, int s,
+                                  int stride, int pad, int k, int c2) {
+  if (dtype == 0 || !igemm_param_valid(dtype, param, layout, n, c, h, w, r, s, stride, pad, k)) return false;
+  const IgCfg& g = kIg16[param];
+  // the LDS-DMA tiles (summed in one kernel: no separate reduction pass)
+  return g.dma == 1 && g.split != 1 && c2 % 8 == 0 && (c2 / 8) % (g.bk / 8) == 0;
+}
+
+size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s, int c2) {
   const IgCfg c = ig_cfg(dtype, param);
   if (!c.split) return 0;
   ConvArgs cv{};
@@ -54,6 +62,7 @@ size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, in
   cv.stride = 1;
   IgArgs a = make_ig(cv);
   a.M = xd.n * yd.h * yd.w;
+  a.KC2 = (c2 + 7) / 8;
   ig_decompose(a, c);
   if (a.splits <= 1) return 0;
   if (c.split == 2) return (size_t)a.splits * a.tiles_m * a.tiles_n * c.bm * c.bn * sizeof(float);

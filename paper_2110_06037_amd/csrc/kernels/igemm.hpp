@@ -46,6 +46,13 @@ struct IgArgs {
   float inv_pq, inv_q;         // 1/(P*Q), 1/Q for sdiv
   const void* res;             // residual [M][Ng] in the output layout, or null
   unsigned* cnt;               // EPI_FIXUP: per-tile arrival counters (zero between launches)
+  // projected shortcut (LDS-DMA kernel): x2 [N][H2][W2][Cs2] (or NC8HW8) read
+  // at stride2 by a 1 x 1 convolution with weights w2 [Kp][C2_8], its KC2
+  // chunks of 8 channels reduced after the KC chunks of the convolution
+  const void* x2;
+  const void* w2;
+  int H2, W2, Cs2, CB2, stride2, KC2, Kred2;
+  long long x2_elems, w2_elems;
 };
 
 // Element offset of GEMM position (m, n) in the output tensor's layout (the
@@ -573,7 +580,8 @@ void igemm_dma_kernel(IgArgs a) {
   const int m0 = mt * BM, n0 = nt * BN;
   const int split = blockIdx.y;
   const int kt0 = split * a.kt_per;
-  const int KT = min(a.KC / CPR - kt0, a.kt_per);
+  const int KT1 = a.KC / CPR;  // steps of the convolution; a projected shortcut's follow
+  const int KT = min(KT1 + a.KC2 / CPR - kt0, a.kt_per);
   const T* __restrict__ x = reinterpret_cast<const T*>(a.x);
   const T* __restrict__ w = reinterpret_cast<const T*>(a.w);
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, a.x_elems * 2);
@@ -636,12 +644,56 @@ void igemm_dma_kernel(IgArgs a) {
     const int k = n0 + row;
     bbyte[i] = k < a.Ng ? (unsigned)((__mul24(k, a.Kred) + lc * 8) * 2) : kOOB;
   }
+  // the projected shortcut: output pixel (img, p, q) reads pixel (p, q) *
+  // stride2 of x2 (no padding), and output channel k row k of w2
+  unsigned rbyte2[NA], bbyte2[NB];
+  const bool proj = a.x2 != nullptr;
+  const __amdgpu_buffer_rsrc_t rx2 = make_rsrc(proj ? a.x2 : a.x, proj ? a.x2_elems * 2 : 0);
+  const __amdgpu_buffer_rsrc_t rw2 = make_rsrc(proj ? a.w2 : a.w, proj ? a.w2_elems * 2 : 0);
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    rbyte2[i] = kOOB;
+    if (!proj) continue;
+    const int row = (wave + NWV * i) * RPB + prow;
+    const int lc = pch ^ swz(row);
+    const int m = m0 + row;
+    if (m >= a.M) continue;
+    const int img = sdiv(m, a.inv_pq), pq = m - __mul24(img, a.PQ);
+    const int p = sdiv(pq, a.inv_q), q = pq - __mul24(p, a.Q);
+    const int h = __mul24(p, a.stride2), w2 = __mul24(q, a.stride2);
+    int e;
+    if constexpr (L == NC8)
+      e = __mul24(img, a.CB2 * a.H2 * a.W2 * 8) + __mul24(__mul24(h, a.W2) + w2, 8) + __mul24(lc, a.H2 * a.W2 * 8);
+    else
+      e = __mul24(__mul24(__mul24(img, a.H2) + h, a.W2) + w2, a.Cs2) + lc * 8;
+    rbyte2[i] = (unsigned)e * 2u;
+  }
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int row = (wave + NWV * i) * RPB + prow;
+    const int lc = pch ^ swz(row);
+    const int k = n0 + row;
+    bbyte2[i] = proj && k < a.Ng ? (unsigned)((__mul24(k, a.Kred2) + lc * 8) * 2) : kOOB;
+  }
 
   // reduction position of the next step to load: tap (r, s), channel block cb
   ChunkPos upos;
   chunk_set(upos, kt0 * CPR, a.CB, a.S);
   auto issue = [&](auto SC, int kt) {
     char* base = smem + decltype(SC)::value * STAGE;
+    if (kt >= KT1) {
+      // a step of the projected shortcut: channel block cb2 of x2 (8 CPR
+      // channels per tile row), the matching columns of w2
+      const int k2 = kt - KT1;
+      const unsigned cb = (unsigned)k2 * (unsigned)CPR;
+      const unsigned xo = L == NC8 ? cb * (unsigned)(a.H2 * a.W2 * 8) * 2u : cb * 16u;
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+        dma16(rx2, base + (wave + NWV * i) * 1024, rbyte2[i] == kOOB ? kOOB : rbyte2[i] + xo, 0);
+#pragma unroll
+      for (int i = 0; i < NB; ++i) dma16(rw2, base + A_BYTES + (wave + NWV * i) * 1024, bbyte2[i], k2 * BK * 2);
+      return;
+    }
     const int t = upos.r * a.S + upos.s;
     int tap;
     if constexpr (L == NC8)
@@ -1038,7 +1090,7 @@ static void ig_decompose(IgArgs& a, const IgCfg& c) {
   a.tiles_m = (a.M + c.bm - 1) / c.bm;
   a.tiles_n = (a.Ng + c.bn - 1) / c.bn;
   const int cpr = c.bk / 8;
-  const int KT = (a.KC + cpr - 1) / cpr;
+  const int KT = (a.KC + a.KC2 + cpr - 1) / cpr;  // with a projected shortcut: both reductions
   int splits = 1;
   const int tiles = a.tiles_m * a.tiles_n;
   if (c.split == 1) {
@@ -1233,6 +1285,19 @@ static IgArgs make_ig(const ConvArgs& c) {
   a.inv_pq = 1.f / (float)std::max(a.PQ, 1);
   a.inv_q = 1.f / (float)std::max(a.Q, 1);
   a.res = c.res;
+  a.x2 = c.x2;
+  a.w2 = c.w2;
+  if (c.x2) {
+    a.H2 = c.x2d.h;
+    a.W2 = c.x2d.w;
+    a.Cs2 = c.x2d.cs;
+    a.CB2 = (c.x2d.c + 7) / 8;
+    a.KC2 = a.CB2;
+    a.Kred2 = a.CB2 * 8;
+    a.stride2 = c.stride2;
+    a.x2_elems = (long long)c.x2d.n * c.x2d.cs * c.x2d.h * c.x2d.w;
+    a.w2_elems = (long long)((a.K + 7) / 8 * 8) * a.Kred2;
+  }
   return a;
 }
 
@@ -1267,6 +1332,10 @@ static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t 
   const IgCfg cfg = ig_cfg(dtype, param);
   check(!c.res || cfg.dma == 0 || ((cfg.dma == 1 || cfg.dma == 4) && (c.yd.layout == NC8 || c.yd.cs % 8 == 0)),
         "this tile configuration takes no residual");
+  check(!c.x2 || (cfg.dma == 1 && cfg.split != 1 && !c.res && c.x2d.layout == c.xd.layout &&
+                  (long long)c.x2d.n * c.x2d.cs * c.x2d.h * c.x2d.w * 2 < (long long)kOOB &&
+                  c.x2d.c % cfg.bk == 0),
+        "a projected shortcut runs on the LDS-DMA tiles, in the convolution's layout");
   if (cfg.dma == 2) {
     conv_patch(dtype, cfg.pc, c, st);
     return;

@@ -65,6 +65,13 @@ struct ConvArgs {
                               // activation (direct and implicit-GEMM routines), or null
   unsigned* cnt = nullptr;    // kFixupMaxTiles tile counters for reductions split across
                               // workgroups: zero before a launch, zero again after it
+  // projected shortcut (implicit GEMM on the LDS-DMA tiles): x2 read by a
+  // 1 x 1 convolution without padding at stride2 with weights w2 (dense
+  // [Kp][1][1][C2_8]), added to the sums before the activation; or null
+  const void* x2 = nullptr;
+  TDesc x2d{};
+  const void* w2 = nullptr;
+  int stride2 = 1;
 };
 
 void conv_direct(int dtype, const ConvArgs& a, hipStream_t st);
@@ -77,7 +84,12 @@ int igemm_num_params(int dtype);
 bool igemm_param_takes_residual(int dtype, int param, int layout, int k);
 bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, int w, int r, int s,
                        int stride, int pad, int k);
-size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s);
+// whether the tile configuration takes a projected shortcut of c2 channels
+// (besides being valid for the convolution itself)
+bool igemm_param_takes_projection(int dtype, int param, int layout, int n, int c, int h, int w, int r, int s,
+                                  int stride, int pad, int k, int c2);
+// workspace bytes (c2 > 0: with a projected shortcut of c2 channels)
+size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s, int c2 = 0);
 // 3x3 stride-1 convolution with the input patch in LDS (an implicit-GEMM
 // parameter family; see conv_patch.hip)
 struct PatchCfg {

@@ -98,6 +98,26 @@ class Graph:
         ins = [inp] if residual is None else [inp, residual]
         return self._add(d, ins, weight, bias)
 
+    def add_projected_conv(self, inp, shortcut, weight, bias, proj_weight, proj_bias, stride=1, pad=0,
+                           act="none", proj_stride=1):
+        """Convolution of ``inp`` plus a 1x1 projection of ``shortcut`` (at
+        ``proj_stride``, no padding), both biases, then the activation."""
+        k, _, r, s = weight.shape
+        d = N.LayerDesc(N.L_CONV2D, k, r, s, stride, pad, 1, N.ACT[act])
+        st = _STORAGE[self.dtype]
+        w = np.ascontiguousarray(weight, dtype=st)
+        wp = np.ascontiguousarray(np.asarray(proj_weight).reshape(k, -1), dtype=st)
+        fp = ctypes.POINTER(ctypes.c_float)
+        b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        bp = None if proj_bias is None else np.ascontiguousarray(proj_bias, dtype=np.float32)
+        self._keepp = (w, wp, b, bp)
+        out = ctypes.c_int32()
+        N.check(self.lib.sn_add_projected_conv(
+            self._g, ctypes.byref(d), inp, shortcut, proj_stride, ctypes.c_void_p(w.ctypes.data),
+            None if b is None else b.ctypes.data_as(fp), ctypes.c_void_p(wp.ctypes.data),
+            None if bp is None else bp.ctypes.data_as(fp), ctypes.byref(out)))
+        return out.value
+
     def add_maxpool(self, inp, k=3, stride=2, pad=1):
         return self._add(N.LayerDesc(N.L_MAXPOOL, 0, k, k, stride, pad, 1, 0), [inp])
 
@@ -132,6 +152,9 @@ class Graph:
         t = layer["type"]
         if t == "input":
             return self.add_input(*layer["chw"])
+        if t == "conv" and layer.get("proj"):
+            return self.add_projected_conv(layer["in"][0], layer["in"][1], weight[0], bias[0], weight[1], bias[1],
+                                           layer["stride"], layer["pad"], layer["act"], layer["proj"]["stride"])
         if t == "conv":
             res = layer["in"][1] if len(layer["in"]) > 1 else None
             return self.add_conv(layer["in"][0], weight, bias, layer["stride"], layer["pad"],
@@ -343,6 +366,9 @@ def build_from_spec(spec, tensors=None, device=0, layouts=None, algos=None, para
             else:
                 wt = np.zeros(shapes[i][0], dtype=_STORAGE[g.dtype])
                 bt = np.zeros(shapes[i][1], dtype=np.float32)
+                if len(shapes[i]) == 3:  # a projected shortcut's weights too
+                    wt = (wt, np.zeros(shapes[i][2], dtype=_STORAGE[g.dtype]))
+                    bt = (bt, np.zeros(shapes[i][1], dtype=np.float32))
         g.add_spec(layer, wt, bt)
     for o in spec.get("outputs", []):
         g.mark_output(o)

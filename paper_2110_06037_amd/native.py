@@ -61,6 +61,9 @@ SIGNATURES = {
     "sn_add_layer": (ctypes.c_int, [_P, ctypes.POINTER(LayerDesc), _I32P, _I32, _P,
                                     ctypes.POINTER(ctypes.c_float), _I32P]),
     "sn_add_input": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32P]),
+    "sn_add_projected_conv": (ctypes.c_int, [_P, ctypes.POINTER(LayerDesc), _I32, _I32, _I32, _P,
+                                             ctypes.POINTER(ctypes.c_float), _P, ctypes.POINTER(ctypes.c_float),
+                                             _I32P]),
     "sn_mark_output": (ctypes.c_int, [_P, _I32]),
     "sn_num_io": (ctypes.c_int, [_P, _I32P, _I32P]),
     "sn_run_mimo": (ctypes.c_int, [_P, ctypes.POINTER(_P), _I32, ctypes.POINTER(_P), _I32, _P]),

@@ -9,7 +9,7 @@ from oracle import numeric as O
 from oracle.select import blockwise, problem_from_costs
 from paper_2110_06037_amd import build_from_spec
 from tests.test_dprs_host import randomise
-from workloads import fuse_residual, generate, mobilenet_v2, resnet18, resnet50, weight_shapes
+from workloads import fuse_projection, fuse_residual, generate, mobilenet_v2, resnet18, resnet50, weight_shapes
 
 
 def _topological(spec):
@@ -96,6 +96,62 @@ def test_fused_graph_routines_and_dprs():
             names = [r["name"] for r in g.routines(i)]
             assert names and not any("winograd" in n for n in names)
     costs = randomise(g.costs(), 77, max_cost=100)
+    g.set_costs(costs)
+    g.select("dprs")
+    ids, total = g.path()
+    t, tup = blockwise(problem_from_costs(costs), [0, 1, 2])
+    assert tuple(ids) + (0,) == tup and total == t
+    g.close()
+
+
+def test_resnet50_projection_shortcuts_fold_into_the_expand_convolutions():
+    fused = fuse_residual(resnet50(1))
+    proj = fuse_projection(fused)
+    assert len(proj["layers"]) == len(fused["layers"]) - 4 and _topological(proj)
+    pl = [(i, l) for i, l in enumerate(proj["layers"], start=1) if l.get("proj")]
+    assert [l["proj"]["stride"] for _, l in pl] == [1, 2, 2, 2]
+    for i, l in pl:
+        # the main input is the block's last 1x1 reduce path, the shortcut
+        # the block input (the previous stage's output), both earlier layers
+        assert l["type"] == "conv" and l["r"] == 1 and l["act"] == "relu" and len(l["in"]) == 2
+        assert l["in"][1] < l["in"][0] < i
+    # nothing to fold where the projection is not a lone 1x1 residual operand
+    assert len(fuse_projection(fuse_residual(resnet18(1)))["layers"]) == len(fuse_residual(resnet18(1))["layers"])
+    assert len(fuse_projection(fuse_residual(mobilenet_v2(1)))["layers"]) == \
+        len(fuse_residual(mobilenet_v2(1))["layers"])
+
+
+def test_projection_fused_net_computes_the_unfused_net():
+    # mini_resnet's first block has a projection shortcut: after both folds
+    # one layer computes conv + projection; exact arithmetic gives the same
+    # outputs, storage rounding differs only by the rounding the fold removes
+    from workloads import decode
+    spec = mini_resnet()
+    t = generate(spec)
+    fused, tf = fuse_residual(spec, t)
+    proj, tp = fuse_projection(fused, tf)
+    assert len(proj["layers"]) == len(spec["layers"]) - 3 and _topological(proj)
+    assert sum(bool(l.get("proj")) for l in proj["layers"]) == 1
+    a = O.forward(spec, decode(t, "bf16"), storage="fp64")[-1]
+    b = O.forward(proj, decode(tp, "bf16"), storage="fp64")[-1]
+    assert np.allclose(a, b, rtol=1e-12, atol=1e-12)
+    a = O.forward(spec, decode(t, "bf16"))[-1]
+    b = O.forward(proj, decode(tp, "bf16"))[-1]
+    assert np.linalg.norm(a - b) / np.linalg.norm(a) < 2e-2
+
+
+def test_projected_layers_routines_and_dprs():
+    spec = fuse_projection(fuse_residual(resnet50(1)))
+    g = build_from_spec(spec, device=-1)
+    for i, layer in enumerate(spec["layers"], start=1):
+        if layer.get("proj"):
+            rts = g.routines(i)
+            # the two-launch direct routine in every layout, the one-kernel
+            # implicit GEMM in the channel-vector layouts only
+            assert {r["layout"] for r in rts if r["algo"] == 0} == {0, 1, 2}
+            assert {r["layout"] for r in rts if r["algo"] == 1} == {1, 2}
+            assert not any(r["algo"] == 2 for r in rts)
+    costs = randomise(g.costs(), 91, max_cost=100)
     g.set_costs(costs)
     g.select("dprs")
     ids, total = g.path()

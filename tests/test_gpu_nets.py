@@ -11,16 +11,14 @@ from oracle import numeric as O
 from oracle.select import blockwise, exhaustive, problem_from_costs
 from paper_2110_06037_amd import build_from_spec, native as N
 from tests.gpu_util import TOL, err, from_dev, to_dev
-from workloads import (CONV_SWEEP_SHAPES, conv_sweep, fuse_residual, generate, mobilenet_v2, resnet18, resnet50,
-                       tiny_chain, to_f64, vgg16, with_batch)
+from workloads import (CONV_SWEEP_SHAPES, conv_sweep, decode, fuse_projection, fuse_residual, generate, mobilenet_v2,
+                       resnet18, resnet50, tiny_chain, to_f64, vgg16, with_batch)
 
 pytestmark = pytest.mark.gpu
 
 
 def decoded(t, dtype):
-    return {"x": to_f64(t["x"], dtype),
-            "w": [None if w is None else to_f64(w, dtype) for w in t["w"]],
-            "b": [None if b is None else b.astype(np.float64) for b in t["b"]]}
+    return decode(t, dtype)
 
 
 def oracle_out(spec, t, images=None):
@@ -114,13 +112,14 @@ def test_integrated_profiling_selects_the_measured_fastest_candidate(name):
 
 
 @pytest.mark.parametrize("name", ["resnet18", "mobilenetv2", "resnet50_bf16", "resnet50_f16",
-                                  "resnet50_fused", "mobilenetv2_fused", "vgg16_64px"])
+                                  "resnet50_fused", "resnet50_proj", "mobilenetv2_fused", "vgg16_64px"])
 def test_net_dp_and_fixed_paths_match_oracle(name):
     spec = {"resnet18": lambda: resnet18(1), "mobilenetv2": lambda: mobilenet_v2(1),
             "vgg16_64px": lambda: vgg16(2, "bf16", 64),
             "resnet50_bf16": lambda: resnet50(1, "bf16"),
             "resnet50_f16": lambda: resnet50(1, "f16"),
             "resnet50_fused": lambda: fuse_residual(resnet50(1, "bf16")),
+            "resnet50_proj": lambda: fuse_projection(fuse_residual(resnet50(1, "bf16"))),
             "mobilenetv2_fused": lambda: fuse_residual(mobilenet_v2(1))}[name]()
     t = generate(spec)
     g = build_from_spec(spec, t)
@@ -221,6 +220,8 @@ def _images_out(g, spec, t, images):
 
 FULL_BATCH = {
     # name: (spec factory, images through the oracle: first, middle, last)
+    "resnet50_bs32_bf16_proj": (lambda: fuse_projection(fuse_residual(resnet50(32, "bf16"))), [0, 13, 31]),
+    "resnet50_bs32_f16_proj": (lambda: fuse_projection(fuse_residual(resnet50(32, "f16"))), [1, 19, 30]),
     "resnet50_bs32_bf16_fused": (lambda: fuse_residual(resnet50(32, "bf16")), [0, 13, 31]),
     "resnet50_bs32_f16_fused": (lambda: fuse_residual(resnet50(32, "f16")), [0, 17, 31]),
     "resnet50_bs32_f16": (lambda: resnet50(32, "f16"), [2, 31]),

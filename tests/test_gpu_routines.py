@@ -356,3 +356,52 @@ def test_split_reduction_routines_repeat_exactly(dtype, ci):
         assert e <= TOL[dtype] and e2 <= TOL[dtype], (rt["name"], e, e2)
         assert all(np.array_equal(o, outs[0]) for o in outs[1:]), rt["name"]
     g.close()
+
+
+PROJECTED_CASES = [
+    # (N, C, H, W, K, R, stride, pad, C2, H2, W2, s2, act): y = act(conv(x) + b + conv1x1_s2(sc) + b2)
+    (2, 64, 14, 14, 256, 1, 1, 0, 64, 14, 14, 1, "relu"),       # bottleneck stage 1 (shortcut at stride 1)
+    (2, 128, 7, 7, 512, 1, 1, 0, 256, 14, 14, 2, "relu"),       # later stages (shortcut at stride 2)
+    (8, 256, 14, 14, 1024, 1, 1, 0, 512, 28, 28, 2, "relu"),    # ResNet-50 stage 3 at batch 8: many tiles
+    (3, 64, 9, 11, 72, 3, 1, 1, 128, 17, 21, 2, "relu6"),       # a 3x3 main convolution, ragged tiles
+    (1, 40, 5, 5, 24, 1, 1, 0, 12, 9, 9, 2, "none"),            # channels off the tile depth: two launches only
+]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("ci", range(len(PROJECTED_CASES)))
+def test_projected_shortcut_every_routine(dtype, ci):
+    # every routine of a convolution with a projected shortcut (the shortcut
+    # a second net input) against the oracle's two convolutions summed
+    n, c, h, w, k, r, st, pad, c2, h2, w2, s2, act = PROJECTED_CASES[ci]
+    if dtype == "f32" and ci == 2:
+        pytest.skip("the two-launch float32 routine at this size is slow and covered by the smaller cases")
+    from paper_2110_06037_amd import Graph
+    import torch
+    layer = {"type": "conv", "in": [0, 1], "k": k, "r": r, "s": r, "stride": st, "pad": pad, "groups": 1,
+             "act": act, "proj": {"stride": s2}}
+    x = random_tensor((n, c, h, w), dtype, seed=200 + ci)
+    sc = random_tensor((n, c2, h2, w2), dtype, seed=210 + ci)
+    wt = random_tensor((k, c, r, r), dtype, seed=220 + ci, dist="normal", scale=np.sqrt(2 / (c * r * r)))
+    wp = random_tensor((k, c2, 1, 1), dtype, seed=230 + ci, dist="normal", scale=np.sqrt(2 / c2))
+    b = random_tensor((k,), "f32", seed=240 + ci, scale=0.1)
+    bp = random_tensor((k,), "f32", seed=250 + ci, scale=0.1)
+    ref = O.round_to(O.layer_forward(layer, [to_f64(x, dtype), to_f64(sc, dtype)],
+                                     (to_f64(wt, dtype), to_f64(wp, dtype)),
+                                     (b.astype(np.float64), bp.astype(np.float64))), dtype)
+    g = Graph(dtype, n, c, h, w, device=0)
+    sid = g.add_input(c2, h2, w2)
+    lid = g.add_projected_conv(0, sid, wt, b, wp, bp, st, pad, act, s2)
+    xd, sd = to_dev(x, dtype), to_dev(sc, dtype)
+    rts = g.routines(lid)
+    assert {rt["algo"] for rt in rts} <= {0, 1}, "direct and implicit GEMM only"
+    if dtype != "f32" and c % 32 == 0 and c2 % 32 == 0:
+        assert any(rt["algo"] == 1 for rt in rts), "the one-kernel routines apply"
+    for rt in rts:
+        g.set_path([0, 0, rt["id"]])
+        out = from_dev(g.run_mimo([xd, sd], output_layers=[lid])[0], dtype)
+        torch.cuda.synchronize()
+        e = err(out, ref, dtype)
+        print(f"{dtype} projected case{ci} {rt['name']}: err {e:.2e}", flush=True)
+        assert e <= TOL[dtype], (rt["name"], e)
+    g.close()

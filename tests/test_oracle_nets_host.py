@@ -15,7 +15,8 @@ import torch.nn.functional as F
 
 from oracle import numeric as O
 from tests.test_fusion_host import mini_resnet
-from workloads import fuse_residual, generate, materialise, mobilenet_v2, net_d, resnet18, to_f64, with_batch
+from workloads import (decode, fuse_projection, fuse_residual, generate, materialise, mobilenet_v2, net_d, resnet18,
+                       resnet50, to_f64, with_batch)
 
 
 def _act(t, act):
@@ -51,6 +52,23 @@ def torch_forward(spec, t, round_f32=False, layer_dtypes=None):
             return dt if j == 0 or spec["layers"][j - 1]["type"] == "input" else ldt[j]
 
         ins = [outs[j] if layer_dtypes is None or src_dtype(j) == me else _round(outs[j], me) for j in L["in"]]
+        if L.get("proj"):
+            # a projected shortcut: torch's convolution of each input with its
+            # own weights and bias, summed, then the activation
+            (w1, w2), (b1, b2) = t["w"][i], t["b"][i]
+            ws_ = [torch.from_numpy(to_f64(v, dt)) for v in (w1, w2)]
+            if me != dt:
+                ws_ = [_round(v, me) for v in ws_]
+            y = F.conv2d(ins[0], ws_[0], torch.from_numpy(b1.astype(np.float64)), stride=L["stride"],
+                         padding=L["pad"])
+            y = y + F.conv2d(ins[1], ws_[1], torch.from_numpy(b2.astype(np.float64)), stride=L["proj"]["stride"])
+            y = _act(y, L["act"])
+            if round_f32:
+                y = y.to(torch.float32).to(torch.float64)
+            if layer_dtypes is not None:
+                y = _round(y, me)
+            outs.append(y)
+            continue
         w = None if t["w"][i] is None else torch.from_numpy(to_f64(t["w"][i], dt))
         if w is not None and me != dt:
             w = _round(w, me)
@@ -111,6 +129,22 @@ def inverted_residual_net():
             "layouts": ["NCHW", "NHWC", "NC8HW8"], "algos": ["direct", "igemm", "winograd"]}
 
 
+def resnet50_first_stages():
+    """ResNet-50 at 2x3x48x48 cut after its second stage's first block: the
+    stem, stage 1 (a projection shortcut at stride 1, identity shortcuts) and
+    a stride-2 projection block."""
+    spec = resnet50(2)
+    keep = []
+    for L in spec["layers"]:
+        keep.append(L)
+        if L["type"] == "add" and sum(l["type"] == "add" for l in keep) == 4:
+            break
+    n = len(keep)
+    keep.append({"type": "gap", "in": [n]})
+    keep.append({"type": "fc", "in": [n + 1], "k": 5})
+    return dict(spec, name="resnet50_2stages", in_chw=[3, 48, 48], layers=keep)
+
+
 def resnet18_first_stages():
     """ResNet-18 at 2x3x40x40 cut after its first two stages: basic blocks with
     identity shortcuts and a stride-2 block with a 1x1 projection."""
@@ -133,6 +167,8 @@ NETS = {
     "inverted_residual_fused": lambda: fuse_residual(inverted_residual_net()),
     "resnet18_2stages": resnet18_first_stages,
     "resnet18_2stages_fused": lambda: fuse_residual(resnet18_first_stages()),
+    "mini_resnet_proj": lambda: fuse_projection(fuse_residual(mini_resnet())),
+    "resnet50_2stages_proj": lambda: fuse_projection(fuse_residual(resnet50_first_stages())),
 }
 
 
@@ -142,9 +178,7 @@ def test_forward_on_branching_nets_matches_torch_f64(name):
     assert any(len(L["in"]) == 2 for L in spec["layers"]), "the net must merge branches"
     t = generate(spec)
     dt = spec["dtype"]
-    dec = {"x": to_f64(t["x"], dt), "w": [None if w is None else to_f64(w, dt) for w in t["w"]],
-           "b": [None if b is None else b.astype(np.float64) for b in t["b"]]}
-    ours = O.forward(spec, dec, storage="f64", keep=True)
+    ours = O.forward(spec, decode(t, dt), storage="f64", keep=True)
     ref = torch_forward(spec, t)
     assert len(ours) == len(ref)
     for i, (a, b) in enumerate(zip(ours, ref)):
@@ -196,10 +230,7 @@ def test_mobilenet_v2_block_structure_is_what_the_pin_covers():
 
 
 def _decoded(spec, t):
-    dt = spec["dtype"]
-    return {"x": to_f64(t["x"], dt), "w": [None if w is None else to_f64(w, dt) for w in t["w"]],
-            "b": [None if b is None else b.astype(np.float64) for b in t["b"]],
-            "inputs": {k: to_f64(v, dt) for k, v in t["inputs"].items()}}
+    return decode(t, spec["dtype"])
 
 
 def test_forward_on_a_two_input_two_output_net_matches_torch_f64():
@@ -219,7 +250,7 @@ ULP = {"f32": 2.0 ** -23, "f16": 2.0 ** -10, "bf16": 2.0 ** -7}
 
 
 @pytest.mark.parametrize("io", ["bf16", "f32"])
-@pytest.mark.parametrize("name", ["inverted_residual", "mini_resnet_fused", "net_d"])
+@pytest.mark.parametrize("name", ["inverted_residual", "mini_resnet_fused", "mini_resnet_proj", "net_d"])
 def test_forward_with_per_layer_dtypes_matches_torch(name, io):
     # a precision-hybrid path: layer dtypes cycle through bf16, f32, f16; the
     # oracle and the torch evaluation cast inputs and weights at the same

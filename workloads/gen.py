@@ -85,7 +85,11 @@ def weight_shapes(spec):
         cin = ch[layer["in"][0]]
         if t == "conv":
             g = layer["groups"]
-            out.append(((layer["k"], cin // g, layer["r"], layer["s"]), layer["k"]))
+            if layer.get("proj"):  # and the projected shortcut's 1x1 weights
+                out.append(((layer["k"], cin // g, layer["r"], layer["s"]), layer["k"],
+                            (layer["k"], ch[layer["in"][1]], 1, 1)))
+            else:
+                out.append(((layer["k"], cin // g, layer["r"], layer["s"]), layer["k"]))
         elif t == "fc":
             out.append(((layer["k"], cin), layer["k"]))
         else:
@@ -123,10 +127,17 @@ def generate(spec, seed=None):
             ws.append(None)
             bs.append(None)
             continue
-        wshape, k = shp
+        wshape, k = shp[:2]
         fan_in = int(np.prod(wshape[1:]))
         wt = rng.standard_normal(wshape) * np.sqrt(2.0 / fan_in)
         bt = rng.uniform(-0.1, 0.1, k)
+        if len(shp) == 3:  # a projected shortcut: its weights and bias follow
+            pshape = shp[2]
+            wp = rng.standard_normal(pshape) * np.sqrt(2.0 / int(np.prod(pshape[1:])))
+            bp = rng.uniform(-0.1, 0.1, k)
+            ws.append((materialise(wt, dtype), materialise(wp, dtype)))
+            bs.append((bt.astype(np.float32), bp.astype(np.float32)))
+            continue
         ws.append(materialise(wt, dtype))
         bs.append(bt.astype(np.float32))
     return {"x": materialise(x, dtype), "w": ws, "b": bs, "inputs": extra, "dtype": dtype}
@@ -142,3 +153,16 @@ def random_tensor(shape, dtype, seed, dist="uniform", scale=1.0):
     else:
         v = rng.uniform(-scale, scale, shape)
     return materialise(v, dtype)
+
+
+def decode(tensors, dtype):
+    """The generated tensors in float64: the input, the weights (pairs for a
+    projected shortcut's layer stay pairs), the biases and further inputs."""
+    def dec(v, f):
+        if v is None:
+            return None
+        return tuple(f(e) for e in v) if isinstance(v, tuple) else f(v)
+    return {"x": to_f64(tensors["x"], dtype),
+            "w": [dec(w, lambda e: to_f64(e, dtype)) for w in tensors["w"]],
+            "b": [dec(b, lambda e: e.astype(np.float64)) for b in tensors["b"]],
+            "inputs": {k: to_f64(v, dtype) for k, v in tensors.get("inputs", {}).items()}}

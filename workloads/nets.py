@@ -311,3 +311,57 @@ def fuse_residual(spec, tensors=None, only_1x1=True):
     t2 = dict(tensors, w=[tensors["w"][old - 1] for old in order], b=[tensors["b"][old - 1] for old in order])
     return out, t2
 
+def fuse_projection(spec, tensors=None):
+    """Structure-only transform, after ``fuse_residual``: a dense convolution
+    whose residual input is a dense 1x1 convolution without padding,
+    activation or residual of its own, consumed by it alone (the projection
+    shortcut of a bottleneck block), takes that convolution's input as a
+    projected shortcut (``"proj": {"stride": s}``): one layer computing
+    act(conv(x) + b + conv1x1_s(shortcut) + b_proj).  The projection layer is
+    removed; with ``tensors`` the fused layer's weights and biases become
+    (own, projection) pairs.  Returns the new spec (and tensors)."""
+    layers = spec["layers"]
+    n = len(layers)
+    consumers = {i: [] for i in range(n + 1)}
+    for i, layer in enumerate(layers, start=1):
+        for j in layer["in"]:
+            consumers[j].append(i)
+    fused = {}        # conv id -> projection id
+    for i, layer in enumerate(layers, start=1):
+        if layer["type"] != "conv" or len(layer["in"]) != 2 or layer.get("proj") or layer["groups"] != 1:
+            continue
+        p = layer["in"][1]
+        if p == 0:
+            continue
+        pl = layers[p - 1]
+        if (pl["type"] == "conv" and len(pl["in"]) == 1 and pl["groups"] == 1 and pl["act"] == "none"
+                and pl["r"] == 1 and pl["s"] == 1 and pl["pad"] == 0 and not pl.get("proj")
+                and consumers[p] == [i]):
+            fused[i] = p
+    gone = set(fused.values())
+    order = [i for i in range(1, n + 1) if i not in gone]
+    new_id = {0: 0}
+    for k, old in enumerate(order, start=1):
+        new_id[old] = k
+    out_layers = []
+    for old in order:
+        lay = copy.deepcopy(layers[old - 1])
+        if old in fused:
+            pl = layers[fused[old] - 1]
+            lay["in"] = [lay["in"][0], pl["in"][0]]
+            lay["proj"] = {"stride": pl["stride"]}
+        lay["in"] = [new_id[j] for j in lay["in"]]
+        out_layers.append(lay)
+    out = dict(spec, layers=out_layers, name=spec["name"] + "_proj")
+    if "outputs" in spec:
+        out["outputs"] = [new_id[o] for o in spec["outputs"]]
+    if tensors is None:
+        return out
+    tw, tb = tensors["w"], tensors["b"]
+    t2 = dict(tensors,
+              w=[(tw[old - 1], tw[fused[old] - 1]) if old in fused else tw[old - 1] for old in order],
+              b=[(tb[old - 1], tb[fused[old] - 1]) if old in fused else tb[old - 1] for old in order],
+              inputs={new_id[k]: v for k, v in tensors.get("inputs", {}).items()})
+    return out, t2
+
+
