@@ -1,18 +1,18 @@
-// 3x3 stride-1 convolution as an implicit GEMM whose input tile is a
-// spatial patch kept in LDS.
+// 3x3 convolution (stride SD = 1 or 2, padding 1) as an implicit GEMM whose
+// input tile is a spatial patch kept in LDS.
 //
 // A workgroup computes the outputs of TI whole images, or of TR consecutive
 // output rows of one image (all Q columns), for BN output channels.  For
 // every step of 32 input channels it loads the tile's input patch -- the
-// (TR + 2) x (Q + 2) input pixels (one halo pixel on each side; the zero
-// padding comes from out-of-range buffer offsets) -- and the filter taps of
-// those channels for all 9 taps, then runs the 9 taps' MFMAs out of LDS: tap
-// (r, s) of output pixel (p, q) is patch pixel (p + r, q + s), so the per-tap
-// operand rows are the same patch rows shifted by the uniform offset
-// r * PWT + s (PWT = the patch row pitch, a power of two).  Each input
-// element therefore crosses the memory system about (TR + 2) / TR times per
-// workgroup instead of 9 times, which is what bounds the per-tap (im2col)
-// implicit GEMM.
+// ((TR - 1) SD + 3) x ((Q - 1) SD + 3) input pixels (one halo pixel on each
+// side; the zero padding comes from out-of-range buffer offsets) -- and the
+// filter taps of those channels for all 9 taps, then runs the 9 taps' MFMAs
+// out of LDS: tap (r, s) of output pixel (p, q) is patch pixel
+// (SD p + r, SD q + s), so the per-tap operand rows are the same patch rows
+// shifted by the uniform offset r * PWT + s (PWT = the patch row pitch, a
+// power of two).  Each input element therefore crosses the memory system
+// about once per workgroup (plus the halo rows) instead of 9 / SD^2 times,
+// which is what bounds the per-tap (im2col) implicit GEMM.
 //
 // Tiles move from global memory into LDS with direct loads (16 bytes per
 // lane, 1 KB per wave instruction in lane order) through ST stages, so up to
@@ -49,7 +49,7 @@ struct PatchArgs {
   const void* w;  // [Kp][3][3][C8]
   const float* bias;
   void* y;
-  int N, C, H, W, Cs;  // input (H = P, W = Q: stride 1, pad 1)
+  int N, C, H, W, Cs;  // input (pad 1)
   int K, P, Q, Ks, Ng;
   int act;
   int CB, C8, Kred;      // channel blocks of 8, padded channels, weight row length 9 * C8
@@ -73,7 +73,7 @@ using IC = std::integral_constant<int, V>;
 // WM x WN waves (group g runs taps [9g/TG, 9(g+1)/TG) of every step on the
 // whole tile; the groups' sums meet in LDS at the end); ST LDS stages;
 // PROWS patch rows per stage.
-template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS>
+template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD>
 __global__ __launch_bounds__(512, 1) void conv3x3_patch_kernel(PatchArgs a) {
   static_assert(sizeof(T) == 2 && L != NCHW, "16-bit channel-vector layouts only");
   constexpr int NWV = 8;
@@ -144,7 +144,7 @@ __global__ __launch_bounds__(512, 1) void conv3x3_patch_kernel(PatchArgs a) {
     if (16 * q < PROWS) {
       const int ii = sdiv(row, a.inv_ip), rem = row - __umul24(ii, a.IP);
       const int ph = rem >> LPW, pw = rem & (PWT - 1);
-      const int img = img0 + ii, h = row0 - 1 + ph, ww = pw - 1;
+      const int img = img0 + ii, h = row0 * SD - 1 + ph, ww = pw - 1;
       const bool ok = ii < a.TI && img < a.N && ph < a.PH && (unsigned)h < (unsigned)a.H &&
                       (unsigned)ww < (unsigned)a.W;
       unsigned e;
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(512, 1) void conv3x3_patch_kernel(PatchArgs a) {
     const int m = (blk0 + i) * 16 + (lane & 15);
     const int ii = sdiv(m, a.inv_trq), rem = m - __umul24(ii, a.TR * a.Q);
     const int pr = sdiv(rem, a.inv_q), pc = rem - __umul24(pr, a.Q);
-    const int pb = blk0 + i < FMT && ii < a.TI ? __umul24(ii, a.IP) + (pr << LPW) + pc : 0;
+    const int pb = blk0 + i < FMT && ii < a.TI ? __umul24(ii, a.IP) + ((pr * SD) << LPW) + pc * SD : 0;
 #pragma unroll
     for (int c = 0; c < 3; ++c) {
       const int r = pb + c;
@@ -327,9 +327,9 @@ __global__ __launch_bounds__(512, 1) void conv3x3_patch_kernel(PatchArgs a) {
 // one fits, else as many whole output rows as fit, balanced over the rows.
 // The patch row pitch is pwt and the image pitch PH * pwt.  Returns whether
 // the patch fits `prows`.
-static bool patch_tiling(PatchArgs& a, int fmt, int pwt, int prows) {
+static bool patch_tiling(PatchArgs& a, int fmt, int pwt, int prows, int sd) {
   const int maxpx = fmt * 16;
-  if (a.Q > maxpx || a.Q + 2 > pwt) return false;
+  if (a.Q > maxpx || (a.Q - 1) * sd + 3 > pwt) return false;
   if (a.P * a.Q <= maxpx) {
     a.TI = std::min(a.N, maxpx / (a.P * a.Q));
     a.TR = a.P;
@@ -342,7 +342,7 @@ static bool patch_tiling(PatchArgs& a, int fmt, int pwt, int prows) {
     a.TR = (a.P + a.tiles_img - 1) / a.tiles_img;
     a.tiles_m = a.N * a.tiles_img;
   }
-  a.PH = a.TR + 2;
+  a.PH = (a.TR - 1) * sd + 3;
   a.PW = pwt;
   a.IP = a.PH * pwt;
   a.fd_ti_tiles = make_fastdiv(a.tiles_img);
@@ -383,50 +383,58 @@ static PatchArgs make_patch(const ConvArgs& c) {
 }
 
 bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
-                      int fmt, int pwt, int prows) {
-  if (r != 3 || s != 3 || stride != 1 || pad != 1) return false;
+                      int fmt, int pwt, int prows, int sd) {
+  if (r != 3 || s != 3 || stride != sd || pad != 1) return false;
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
   if (!vec || ((c + 7) / 8) % 4 != 0) return false;
   if ((long long)n * h * w + h * w >= (1 << 21)) return false;  // fp32 index division
   PatchArgs a{};
   a.N = n;
-  a.P = h;
-  a.Q = w;
-  return patch_tiling(a, fmt, pwt, prows);
+  a.P = (h - 1) / sd + 1;
+  a.Q = (w - 1) / sd + 1;
+  return patch_tiling(a, fmt, pwt, prows, sd);
 }
 
-template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS>
+template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD>
 static void patch_go(PatchArgs a, hipStream_t st) {
-  check(patch_tiling(a, FMT, PWT, PROWS), "output too wide for the patch tile");
+  check(patch_tiling(a, FMT, PWT, PROWS, SD), "output too wide for the patch tile");
   check(a.CB % 4 == 0, "patch kernel needs C % 32 == 0");
   check(a.x_elems * 2 < (long long)kOOB && a.w_elems * 2 < (long long)kOOB,
         "tensor too large for 32-bit buffer offsets");
   a.tiles_n = (a.Ng + BN - 1) / BN;
   dim3 grid(a.tiles_m * a.tiles_n);
-  SN_LAUNCH((conv3x3_patch_kernel<T, L, FMT, BN, PWT, WM, WN, TG, ST, PROWS>), grid, dim3(512), 0, st, a);
+  SN_LAUNCH((conv3x3_patch_kernel<T, L, FMT, BN, PWT, WM, WN, TG, ST, PROWS, SD>), grid, dim3(512), 0, st, a);
 }
 
-static long long patch_key(int fmt, int bn, int pwt, int wm, int wn, int tg, int stg, int prows) {
-  return ((((((fmt * 1000LL + bn) * 100 + pwt) * 10 + wm) * 10 + wn) * 10 + tg) * 10 + stg) * 10000 + prows;
+static long long patch_key(int fmt, int bn, int pwt, int wm, int wn, int tg, int stg, int prows, int sd) {
+  return (((((((fmt * 1000LL + bn) * 100 + pwt) * 10 + wm) * 10 + wn) * 10 + tg) * 10 + stg) * 10000 + prows) * 10 +
+         sd;
 }
 
 template <typename T, int L>
 static void patch_layout(const PatchCfg& c, const PatchArgs& a, hipStream_t st) {
-  const long long key = patch_key(c.fmt, c.bn, c.pwt, c.wm, c.wn, c.tg, c.st, c.prows);
+  const long long key = patch_key(c.fmt, c.bn, c.pwt, c.wm, c.wn, c.tg, c.st, c.prows, c.sd);
 #define PGO(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                               \
-  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)) {                  \
-    patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_>(a, st);                 \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1)) {               \
+    patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1>(a, st);              \
+    return;                                                                            \
+  }
+#define PGO2(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                              \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 2)) {               \
+    patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 2>(a, st);              \
     return;                                                                            \
   }
   PATCH_CONFIGS(PGO)
+  PATCH2_CONFIGS(PGO2)
 #undef PGO
+#undef PGO2
   check(false, "patch tile not instantiated");
 }
 
 void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& c, hipStream_t st) {
   check(dtype != 0, "patch kernel runs 16-bit types");
-  check(c.xd.layout == c.yd.layout && c.r == 3 && c.s == 3 && c.stride == 1 && c.pad == 1,
-        "patch kernel: 3x3 stride 1 pad 1, one layout");
+  check(c.xd.layout == c.yd.layout && c.r == 3 && c.s == 3 && c.stride == cfg.sd && c.pad == 1,
+        "patch kernel: 3x3 pad 1 at the tile's stride, one layout");
   check(c.xd.layout == NC8 || (c.xd.layout == NHWC && c.xd.c % 8 == 0), "patch kernel: channel-vector layout");
   check((long long)c.yd.n * c.yd.cs * c.yd.h * c.yd.w * 2 < (long long)kOOB, "tensor too large");
   const PatchArgs a = make_patch(c);

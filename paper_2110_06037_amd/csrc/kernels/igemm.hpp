@@ -1074,6 +1074,11 @@ static const IgCfg kIg16[] = {
     {128, 128, 64, 2, 0, 1, 4, 3, 0, {}, 8}, {128, 64, 64, 2, 0, 1, 4, 4, 0, {}, 8},
     {64, 128, 64, 2, 0, 1, 2, 4, 0, {}, 8},  {64, 64, 64, 2, 0, 1, 2, 4, 0, {}, 8},
     {64, 64, 64, 2, 0, 1, 2, 6, 0, {}, 8},   {128, 128, 32, 2, 0, 1, 4, 4, 0, {}, 8},
+    // 3x3 stride-2 patch kernel
+#define SN_PATCH2_IG(FMT, BN, PWT, WM, WN, TG, ST, PROWS) \
+  {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS, 2}},
+    PATCH2_CONFIGS(SN_PATCH2_IG)
+#undef SN_PATCH2_IG
 };
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 

@@ -90,10 +90,11 @@ bool igemm_param_takes_projection(int dtype, int param, int layout, int n, int c
                                   int stride, int pad, int k, int c2);
 // workspace bytes (c2 > 0: with a projected shortcut of c2 channels)
 size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, int r, int s, int c2 = 0);
-// 3x3 stride-1 convolution with the input patch in LDS (an implicit-GEMM
-// parameter family; see conv_patch.hip)
+// 3x3 stride-1 or stride-2 convolution with the input patch in LDS (an
+// implicit-GEMM parameter family; see conv_patch.hip)
 struct PatchCfg {
   int fmt, bn, pwt, wm, wn, tg, st, prows;  // one PATCH_CONFIGS tuple
+  int sd = 1;                               // convolution stride
 };
 // Instantiated patch tiles (FMT, BN, PWT, WM, WN, TG, ST, PROWS): FMT row
 // blocks of 16 output pixels, BN output channels, patch row pitch PWT, 8
@@ -110,8 +111,16 @@ struct PatchCfg {
   X(25, 64, 64, 4, 1, 2, 2, 576) \
   X(13, 64, 32, 4, 1, 2, 2, 288) \
   X(7, 64, 16, 4, 1, 2, 2, 288)
+// Stride-2 patch tiles (same fields): ResNet-50's first 3x3 of stages 2-4
+// at 56->28, 28->14 and 14->7 (patch width 2Q + 1 within PWT)
+#define PATCH2_CONFIGS(X)        \
+  X(7, 64, 64, 4, 1, 2, 2, 576)  \
+  X(7, 64, 32, 4, 1, 2, 2, 480)  \
+  X(7, 64, 16, 4, 1, 2, 2, 480)  \
+  X(4, 64, 16, 4, 1, 2, 2, 240)  \
+  X(7, 32, 16, 4, 1, 2, 3, 480)
 bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
-                      int fmt, int pwt, int prows);
+                      int fmt, int pwt, int prows, int sd);
 void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& a, hipStream_t st);
 // Stride-1 or -2 convolution of an NHWC input with C <= 4 (a CNN stem; see
 // conv_smallc.hip); gmax: filter chunks the kernel holds (28 for 7 x 7, 8 for 3 x 3)

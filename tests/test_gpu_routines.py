@@ -43,6 +43,12 @@ CONV_CASES = [
     (2, 1, 17, 15, 8, 3, 1, 1, "relu"),      # degenerate channel counts: one input channel,
     (1, 5, 9, 9, 1, 3, 1, 1, "none"),        # one output channel,
     (3, 8, 1, 1, 16, 1, 1, 0, "relu6"),      # a 1 x 1 image
+    # 3x3 stride 2 at the ResNet-50 stage entries (the stride-2 patch tiles;
+    # batch cut), and odd sizes
+    (2, 128, 56, 56, 128, 3, 2, 1, "relu"),
+    (2, 256, 28, 28, 256, 3, 2, 1, "relu"),
+    (3, 512, 14, 14, 512, 3, 2, 1, "relu"),
+    (2, 64, 27, 29, 96, 3, 2, 1, "relu6"),
 ]
 
 
