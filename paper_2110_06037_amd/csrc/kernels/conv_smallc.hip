@@ -280,7 +280,7 @@ static void smallc_go(SmallCArgs a, hipStream_t st) {
   SN_LAUNCH((conv_smallc_kernel<T, FMT, WM, PPX, GMAX, OCC>), grid, dim3(256), 0, st, a);
 }
 
-void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& c, hipStream_t st) {
+void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& c, hipStream_t st, int wm, int occ) {
   check(dtype != 0, "small-channel kernel runs 16-bit types");
   check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.xd.c <= 4 && (c.stride == 1 || c.stride == 2),
         "small-channel kernel: NHWC, C <= 4, stride 1 or 2");
@@ -311,16 +311,17 @@ void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& c, hipStream_t st
   check(a.x_elems * 2 < (long long)kOOB && a.y_elems * 2 < (long long)kOOB && a.w_elems * 2 < (long long)kOOB,
         "tensor too large for 32-bit offsets");
   check(c.yd.cs % 4 == 0 && c.yd.c % 4 == 0, "small-channel kernel stores 4-channel groups");
-#define SC(FMT, PPX, GMAX)                                                  \
-  if (fmt == FMT && gmax == GMAX) {                                         \
-    if (dtype == 1) smallc_go<f16, FMT, 2, PPX, GMAX, 3>(a, st);            \
-    else smallc_go<bf16, FMT, 2, PPX, GMAX, 3>(a, st);                      \
+#define SC(FMT, PPX, GMAX, WM, OCC)                                         \
+  if (fmt == FMT && gmax == GMAX && wm == WM && occ == OCC) {               \
+    if (dtype == 1) smallc_go<f16, FMT, WM, PPX, GMAX, OCC>(a, st);         \
+    else smallc_go<bf16, FMT, WM, PPX, GMAX, OCC>(a, st);                   \
     return;                                                                 \
   }
-  SC(7, 1664, 28)
-  SC(14, 2112, 28)
-  SC(7, 704, 8)
-  SC(14, 1152, 8)
+  SC(7, 1664, 28, 2, 3)
+  SC(14, 2112, 28, 2, 3)
+  SC(7, 704, 8, 2, 3)
+  SC(14, 1152, 8, 2, 3)
+  SC(14, 2112, 28, 4, 2)
 #undef SC
   check(false, "small-channel tile not instantiated");
 }

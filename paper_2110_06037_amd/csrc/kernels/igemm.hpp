@@ -1062,8 +1062,9 @@ static const IgCfg kIg16[] = {
     PATCH_CONFIGS(SN_PATCH_IG)
 #undef SN_PATCH_IG
     // small-channel (stem) kernel: NHWC, C <= 4, stride 1 or 2; 7 x 7 and 3 x 3 filters
-    {112, 64, 32, 0, 0, 3, 2, 1, 1664, {}, 4, 28}, {224, 64, 32, 0, 0, 3, 2, 1, 2112, {}, 4, 28},
-    {112, 64, 32, 0, 0, 3, 2, 1, 704, {}, 4, 8},   {224, 64, 32, 0, 0, 3, 2, 1, 1152, {}, 4, 8},
+    // (wm: wave rows; st: workgroups per CU)
+    {112, 64, 32, 0, 0, 3, 2, 3, 1664, {}, 4, 28}, {224, 64, 32, 0, 0, 3, 2, 3, 2112, {}, 4, 28},
+    {112, 64, 32, 0, 0, 3, 2, 3, 704, {}, 4, 8},   {224, 64, 32, 0, 0, 3, 2, 3, 1152, {}, 4, 8},
     // streaming 1x1 kernel: NHWC, C = bk (BM pixels x BN channels per tile, WM wave rows,
     // loads pf tiles ahead)
 #define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM},
@@ -1079,6 +1080,9 @@ static const IgCfg kIg16[] = {
   {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS, 2}},
     PATCH2_CONFIGS(SN_PATCH2_IG)
 #undef SN_PATCH2_IG
+    // small-channel (stem) kernel, 7 x 7: two output rows per tile, four wave
+    // rows, two workgroups per CU
+    {224, 64, 32, 0, 0, 3, 4, 2, 2112, {}, 4, 28},
 };
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 
@@ -1346,7 +1350,7 @@ static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t 
     return;
   }
   if (cfg.dma == 3) {
-    conv_smallc(dtype, cfg.bm / 16, cfg.gmax, c, st);
+    conv_smallc(dtype, cfg.bm / 16, cfg.gmax, c, st, cfg.wm, cfg.st);
     return;
   }
   if (cfg.dma == 4) {

@@ -126,7 +126,9 @@ void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& a, hipStream_t s
 // conv_smallc.hip); gmax: filter chunks the kernel holds (28 for 7 x 7, 8 for 3 x 3)
 bool smallc_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
                        int k, int fmt, int ppx, int gmax);
-void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st);
+// wm: wave rows (of 4 waves); occ: workgroups per CU the persistent grid and
+// the register budget are sized for
+void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st, int wm = 2, int occ = 3);
 // 1x1 convolution (stride 1 or 2, no padding) of an NHWC input with cc =
 // 64, 128 or 256 channels by persistent workgroups streaming pixel tiles
 // (see conv1x1_stream.hip).  Instantiated tiles (CC, BM, BN, WM, PD): BM
