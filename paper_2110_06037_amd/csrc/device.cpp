@@ -27,6 +27,7 @@ struct DevLayer {
   void* w[3] = {};      // per dtype: dense [Kp][R][S][C8] | depthwise [R][S][C8] | fc [Kp][C8]
   void* wu[3] = {};     // per dtype: Winograd U [16][Kp][C8]
   void* wp[3] = {};     // per dtype: projected-shortcut weights [Kp][C2_8]
+  void* wcat[3] = {};   // per dtype: 1x1 layer with a projected shortcut, both weights [Kp][C + C2]
   float* bias = nullptr;  // [Kp] (with a projected shortcut: the two biases summed)
   float* zbias = nullptr;  // [Kp] zeros (the shortcut's own launch in the two-launch routine)
 };
@@ -164,6 +165,8 @@ void dev_destroy(Graph& g) {
       if (p) (void)hipFree(p);
     for (void* p : d.wp)
       if (p) (void)hipFree(p);
+    for (void* p : d.wcat)
+      if (p) (void)hipFree(p);
     if (d.bias) (void)hipFree(d.bias);
     if (d.zbias) (void)hipFree(d.zbias);
   }
@@ -236,6 +239,14 @@ void dev_upload_layer(Graph& g, int id) {
           else encode(decode(L.wproj.data() + e * ies, g.dtype), dt, &w2[((size_t)kk * C28 + c) * es]);
         }
       dl.wp[dt] = dev_upload(w2.data(), w2.size());
+      if (R == 1 && S == 1 && C % 64 == 0 && C2 % 64 == 0) {  // the streaming kernel's filter rows
+        std::vector<uint8_t> wc((size_t)Kp * (C + C2) * es);
+        for (int kk = 0; kk < Kp; ++kk) {
+          std::memcpy(&wc[(size_t)kk * (C + C2) * es], &w[(size_t)kk * C * es], (size_t)C * es);
+          std::memcpy(&wc[((size_t)kk * (C + C2) + C) * es], &w2[(size_t)kk * C2 * es], (size_t)C2 * es);
+        }
+        dl.wcat[dt] = dev_upload(wc.data(), wc.size());
+      }
     }
     if (winograd_applicable(L, in)) {
       // U = G g G^T per (k, c), in float64 from the caller's weights, rounded
@@ -331,6 +342,7 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
           a.x2 = in[1];
           a.x2d = ind[1];
           a.w2 = dl.wp[dt];
+          a.wcat = dl.wcat[dt];
           a.stride2 = L.proj_stride;
           k::conv_igemm(dt, r.param, a, st);
         }

@@ -46,7 +46,10 @@ bool igemm_param_takes_residual(int dtype, int param, int layout, int k) {
 
 bool igemm_param_takes_projection(int dtype, int param, int layout, int n, int c, int h, int w, int r, int s,
                                   int stride, int pad, int k, int c2) {
-  if (dtype == 0 || !igemm_param_valid(dtype, param, layout, n, c, h, w, r, s, stride, pad, k)) return false;
+  if (dtype == 0 || param < 0 || param >= igemm_num_params(dtype)) return false;
+  if (kIg16[param].dma == 4)  // the streaming 1x1 kernel: both inputs' slabs in one reduction
+    return stream1x1_takes_projection(layout, c, c, n, h, w, r, s, stride, pad, k, c2, kIg16[param].bk);
+  if (!igemm_param_valid(dtype, param, layout, n, c, h, w, r, s, stride, pad, k)) return false;
   const IgCfg& g = kIg16[param];
   // the LDS-DMA tiles (summed in one kernel: no separate reduction pass)
   return g.dma == 1 && g.split != 1 && c2 % 8 == 0 && (c2 / 8) % (g.bk / 8) == 0;

@@ -18,6 +18,11 @@
 // addresses.  In LDS a tile is CC / 64 slabs of 64 channels, each with
 // 128-byte rows (8 chunks); chunk c of row r sits at c ^ ((r >> 1) & 7),
 // which serves an MFMA operand read of 16 consecutive rows in one pass.
+//
+// With a projected shortcut (PJ) the reduction runs over the main input's
+// slabs and then the shortcut's (C1 + C2 = CC channels): the shortcut's slabs
+// load pixel (img, p * stride2, q * stride2) of its own tensor, and the
+// filter rows hold both weights ([Kp][C1 + C2]); nothing else changes.
 #include "gemm_common.hpp"
 #include "kcommon.hpp"
 #include "launch.hpp"
@@ -26,7 +31,7 @@ namespace sn {
 namespace k {
 
 struct StreamArgs {
-  const void* x;     // [N][H][W][CC]
+  const void* x;     // [N][H][W][CC] (with a projected shortcut: [N][H][W][C1])
   const void* w;     // [Kp][CC]
   const float* bias; // [Kp]
   const void* res;   // [M][Ks] or null
@@ -36,14 +41,18 @@ struct StreamArgs {
   FastDiv fd_pq, fd_q;
   int tiles_m;
   long long x_elems, w_elems, y_elems;
+  const void* x2;    // projected shortcut [N][H2][W2][C2], or null
+  int H2, W2, stride2, C1, C2;
+  long long x2_elems;
 };
 
 template <int V>
 using SIC = std::integral_constant<int, V>;
 
-template <typename T, int CC, int BM, int BN, int WM, bool RES, int PD>
+template <typename T, int CC, int BM, int BN, int WM, bool RES, int PD, bool PJ = false>
 __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   static_assert(sizeof(T) == 2 && CC % 64 == 0, "16-bit types, 64-channel slabs");
+  static_assert(!(PJ && RES), "a projected shortcut replaces the residual");
   static_assert(PD >= 1 && PD <= 3, "one to three tiles ahead");
   constexpr int NB = PD + 1;                   // pixel buffers and residual register sets
   constexpr int NWV = 8, NT = 512, WN = NWV / WM;
@@ -78,6 +87,7 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, a.w_elems * 2);
   const __amdgpu_buffer_rsrc_t ry = make_rsrc(a.y, a.y_elems * 2);
   const __amdgpu_buffer_rsrc_t rr = make_rsrc(RES ? a.res : a.y, a.y_elems * 2);
+  const __amdgpu_buffer_rsrc_t rx2 = make_rsrc(PJ ? a.x2 : a.x, PJ ? a.x2_elems * 2 : 0);
 
   // bias of the workgroup's channels through LDS (no global load of it
   // stays outstanding in the tile loop)
@@ -96,12 +106,16 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   }
   unsigned achk[NA];  // the lane's chunk within a pixel's channels (bytes)
   int arow[NA];
+  bool asc[NA];       // (PJ) the slab is the shortcut's (wave-uniform)
+  const int nsl1 = PJ ? a.C1 / 64 : NSL;
 #pragma unroll
   for (int i = 0; i < NA; ++i) {
     const int b = wave + NWV * i, sl = b / (BM / 8), row = (b % (BM / 8)) * 8 + prow;
     arow[i] = row;
-    achk[i] = (unsigned)(sl * 64 + ((pch ^ swz(row)) << 3)) * 2u;
+    asc[i] = PJ && sl >= nsl1;
+    achk[i] = (unsigned)((asc[i] ? sl - nsl1 : sl) * 64 + ((pch ^ swz(row)) << 3)) * 2u;
   }
+  const unsigned xpix = (unsigned)(PJ ? a.C1 : CC) * 2u, x2pix = (unsigned)(PJ ? a.C2 : 0) * 2u;
   // output pixel m reads input pixel m (stride 1) or (img, 2p, 2q) (stride
   // 2); a tile past the end loads nothing (out-of-range offsets) but still
   // counts its load instructions, so every wait below has a fixed count
@@ -110,14 +124,21 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       const int m = m0 + arow[i];
+      const bool ok = mtile < a.tiles_m && m < a.M;
+      if (PJ && asc[i]) {
+        const int img = fdiv(m, a.fd_pq), pq = m - img * (a.P * a.Q);
+        const int p = fdiv(pq, a.fd_q), q = pq - p * a.Q;
+        const int pix2 = (img * a.H2 + p * a.stride2) * a.W2 + q * a.stride2;
+        dma16(rx2, As + buf * A_BYTES + (wave + NWV * i) * 1024, ok ? (unsigned)pix2 * x2pix + achk[i] : kOOB, 0);
+        continue;
+      }
       int pix = m;
       if (a.stride != 1) {
         const int img = fdiv(m, a.fd_pq), pq = m - img * (a.P * a.Q);
         const int p = fdiv(pq, a.fd_q), q = pq - p * a.Q;
         pix = (img * a.H + p * a.stride) * a.W + q * a.stride;
       }
-      dma16(rx, As + buf * A_BYTES + (wave + NWV * i) * 1024,
-            mtile < a.tiles_m && m < a.M ? (unsigned)pix * (unsigned)(CC * 2) + achk[i] : kOOB, 0);
+      dma16(rx, As + buf * A_BYTES + (wave + NWV * i) * 1024, ok ? (unsigned)pix * xpix + achk[i] : kOOB, 0);
     }
   };
   u32x4 res[NB][NE];  // residual register sets, one per tile in flight
@@ -255,6 +276,13 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   wait_vmcnt<0>();
 }
 
+bool stream1x1_takes_projection(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
+                                int k, int c2, int cc) {
+  return layout == NHWC && c % 64 == 0 && cs == c && c2 % 64 == 0 && c + c2 == cc && r == 1 && s == 1 &&
+         stride == 1 && pad == 0 && k % 8 == 0 && (long long)n * h * w * ((k + 7) / 8 * 8) * 2 < (long long)kOOB &&
+         (long long)n * h * w * c * 2 < (long long)kOOB;
+}
+
 bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
                           int k, int cc) {
   const long long p = (h - 1) / stride + 1, q = (w - 1) / stride + 1;
@@ -268,23 +296,36 @@ static void stream_go(const StreamArgs& a, int tiles_n, hipStream_t st) {
   // persistent: about one workgroup per CU over all channel tiles
   const int gx = std::max(1, std::min(a.tiles_m, 256 / tiles_n));
   const dim3 grid(gx, tiles_n);
-  if (a.res)
+  if (a.x2) {
+    if constexpr (CC >= 128) SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, false, PD, true>), grid, dim3(512), 0, st, a);
+    else check(false, "a projected shortcut needs two slabs or more");
+  } else if (a.res) {
     SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, true, PD>), grid, dim3(512), 0, st, a);
-  else
+  } else {
     SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, false, PD>), grid, dim3(512), 0, st, a);
+  }
 }
 
 void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& c, hipStream_t st) {
   check(dtype != 0, "streaming 1x1 kernel runs 16-bit types");
   const long long m = (long long)c.yd.n * c.yd.h * c.yd.w;
-  check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.stride >= 1 &&
-            c.yd.h == (c.xd.h - 1) / c.stride + 1 && c.yd.w == (c.xd.w - 1) / c.stride + 1 &&
-            stream1x1_applicable(c.xd.layout, c.xd.c, c.xd.cs, c.xd.n, c.xd.h, c.xd.w, c.r, c.s, c.stride,
-                                 c.pad, c.yd.c, cc),
-        "streaming 1x1 kernel: NHWC, C = CC, 1x1 stride 1 or 2 without padding, K % 8 == 0");
+  if (c.x2) {
+    check(c.x2d.layout == NHWC && c.wcat && !c.res && c.yd.h == (c.x2d.h - 1) / c.stride2 + 1 &&
+              c.yd.w == (c.x2d.w - 1) / c.stride2 + 1 && c.x2d.cs == c.x2d.c &&
+              (long long)c.x2d.n * c.x2d.h * c.x2d.w * c.x2d.c * 2 < (long long)kOOB &&
+              stream1x1_takes_projection(c.xd.layout, c.xd.c, c.xd.cs, c.xd.n, c.xd.h, c.xd.w, c.r, c.s, c.stride,
+                                         c.pad, c.yd.c, c.x2d.c, cc),
+          "streaming 1x1 kernel with a projected shortcut: NHWC, C + C2 = CC, both multiples of 64");
+  } else {
+    check(c.xd.layout == NHWC && c.yd.layout == NHWC && c.stride >= 1 &&
+              c.yd.h == (c.xd.h - 1) / c.stride + 1 && c.yd.w == (c.xd.w - 1) / c.stride + 1 &&
+              stream1x1_applicable(c.xd.layout, c.xd.c, c.xd.cs, c.xd.n, c.xd.h, c.xd.w, c.r, c.s, c.stride,
+                                   c.pad, c.yd.c, cc),
+          "streaming 1x1 kernel: NHWC, C = CC, 1x1 stride 1 or 2 without padding, K % 8 == 0");
+  }
   StreamArgs a{};
   a.x = c.x;
-  a.w = c.w;
+  a.w = c.x2 ? c.wcat : c.w;
   a.bias = c.bias;
   a.res = c.res;
   a.y = c.y;
@@ -300,7 +341,16 @@ void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& c
   a.stride = c.stride;
   a.fd_pq = make_fastdiv(a.P * a.Q);
   a.fd_q = make_fastdiv(a.Q);
-  a.x_elems = (long long)c.xd.n * c.xd.h * c.xd.w * cc;
+  a.x_elems = (long long)c.xd.n * c.xd.h * c.xd.w * (c.x2 ? c.xd.c : cc);
+  if (c.x2) {
+    a.x2 = c.x2;
+    a.H2 = c.x2d.h;
+    a.W2 = c.x2d.w;
+    a.stride2 = c.stride2;
+    a.C1 = c.xd.c;
+    a.C2 = c.x2d.c;
+    a.x2_elems = (long long)c.x2d.n * c.x2d.h * c.x2d.w * c.x2d.c;
+  }
   a.w_elems = (long long)((a.K + 7) / 8 * 8) * cc;
   a.y_elems = m * a.Ks;
   const int tiles_n = (a.K + bn - 1) / bn;

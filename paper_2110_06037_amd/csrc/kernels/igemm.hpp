@@ -1341,10 +1341,10 @@ static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t 
   const IgCfg cfg = ig_cfg(dtype, param);
   check(!c.res || cfg.dma == 0 || ((cfg.dma == 1 || cfg.dma == 4) && (c.yd.layout == NC8 || c.yd.cs % 8 == 0)),
         "this tile configuration takes no residual");
-  check(!c.x2 || (cfg.dma == 1 && cfg.split != 1 && !c.res && c.x2d.layout == c.xd.layout &&
-                  (long long)c.x2d.n * c.x2d.cs * c.x2d.h * c.x2d.w * 2 < (long long)kOOB &&
-                  c.x2d.c % cfg.bk == 0),
-        "a projected shortcut runs on the LDS-DMA tiles, in the convolution's layout");
+  check(!c.x2 || cfg.dma == 4 ||
+            (cfg.dma == 1 && cfg.split != 1 && !c.res && c.x2d.layout == c.xd.layout &&
+             (long long)c.x2d.n * c.x2d.cs * c.x2d.h * c.x2d.w * 2 < (long long)kOOB && c.x2d.c % cfg.bk == 0),
+        "a projected shortcut runs on the LDS-DMA tiles or the streaming kernel, in the convolution's layout");
   if (cfg.dma == 2) {
     conv_patch(dtype, cfg.pc, c, st);
     return;

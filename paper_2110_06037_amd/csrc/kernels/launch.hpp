@@ -72,6 +72,8 @@ struct ConvArgs {
   TDesc x2d{};
   const void* w2 = nullptr;
   int stride2 = 1;
+  const void* wcat = nullptr;  // 1x1 convolution with a projected shortcut: both weights,
+                               // rows [Kp][C8 + C2_8] (the streaming kernel's filter)
 };
 
 void conv_direct(int dtype, const ConvArgs& a, hipStream_t st);
@@ -151,6 +153,10 @@ void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st
   X(256, 32, 128, 2, 3)
 bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
                           int k, int cc);
+// the streaming kernel with a projected shortcut of c2 channels (slabs of
+// the main input, then of the shortcut: c + c2 = cc, both multiples of 64)
+bool stream1x1_takes_projection(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
+                                int k, int c2, int cc);
 void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& a, hipStream_t st);
 size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k);
 void conv_winograd(int dtype, const ConvArgs& a, hipStream_t st);
