@@ -556,9 +556,10 @@ void igemm_dma_kernel(IgArgs a) {
   constexpr int WN = NWV / WM;
   constexpr int CPR = BK / 8;       // 16-byte chunks per tile row
   constexpr int RPB = 64 / CPR;     // tile rows filled by one load instruction (1 KB)
-  // the chunk XOR key changes every 2 rows: one chunk of 16 consecutive rows
-  // is then read in a single LDS pass on gfx950 for 64- and 128-byte rows
-  constexpr int RPR = 2;
+  // the chunk XOR key changes every 2 rows (64- and 128-byte rows) or every
+  // row (256-byte rows): one chunk of 16 consecutive rows then covers the 64
+  // banks once and is read in a single LDS pass on gfx950
+  constexpr int RPR = CPR == 16 ? 1 : 2;
   constexpr int NA = BM / RPB / NWV;  // A load instructions per wave and stage
   constexpr int NB = BN / RPB / NWV;  // B load instructions per wave and stage
   static_assert(NA * RPB * NWV == BM && NB * RPB * NWV == BN && WM * WN == NWV, "tile shape");
@@ -1083,6 +1084,11 @@ static const IgCfg kIg16[] = {
     // small-channel (stem) kernel, 7 x 7: two output rows per tile, four wave
     // rows, two workgroups per CU
     {224, 64, 32, 0, 0, 3, 4, 2, 2112, {}, 4, 28},
+    // LDS-DMA kernel with 128-channel reduction steps (half the steps, and
+    // barriers, of long reductions)
+    {64, 64, 128, 0, 0, 1, 2, 3},  {64, 64, 128, 0, 0, 1, 2, 4},
+    {64, 128, 128, 0, 0, 1, 2, 3, 0, {}, 8}, {128, 64, 128, 0, 0, 1, 4, 3, 0, {}, 8},
+    {128, 128, 128, 0, 0, 1, 4, 2, 0, {}, 8},
 };
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 
@@ -1197,6 +1203,11 @@ static void igemm_dma_cfg(const IgCfg& c, const IgArgs& a, hipStream_t st) {
     IGDN(128, 64, 64, 4, 6, 8)
     IGDN(128, 128, 32, 4, 6, 8)
     IGDN(64, 64, 64, 2, 6, 8)
+    IGD(64, 64, 128, 2, 3)
+    IGD(64, 64, 128, 2, 4)
+    IGDN(64, 128, 128, 2, 3, 8)
+    IGDN(128, 64, 128, 4, 3, 8)
+    IGDN(128, 128, 128, 4, 2, 8)
     default: check(false, "LDS-DMA tile not instantiated");
   }
   }
