@@ -9,9 +9,12 @@
 // (16-byte aligned with stride 2, 8-byte aligned with stride 1).  The
 // reduction has R * ceil(S / 2) such chunks (28 for a 7 x 7 filter: 224 MFMA
 // elements for 147 real ones; 6 for a 3 x 3 filter).  The filter is
-// repacked into the same chunks in LDS once per workgroup; workgroups are
-// persistent over output-row tiles and prefetch the next tile's input
-// pixels into registers while the current tile's MFMAs run.
+// repacked into the same chunks in LDS once per workgroup (all its loads in
+// flight together); workgroups are persistent over output-row tiles and
+// prefetch the next tile's input pixels into registers while the current
+// tile's MFMAs run.  A tile's outputs are whole output rows of one image,
+// contiguous in NHWC: they go through LDS and leave as 16-byte stores of
+// consecutive addresses (a wave stores 1 KB runs).
 #include "gemm_common.hpp"
 #include "kcommon.hpp"
 #include "launch.hpp"
@@ -51,9 +54,12 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
   constexpr int P_BYTES = PPX * 8;
   constexpr int PAIRS = PPX / 2;                 // patch pixel pairs (16 bytes each)
   constexpr int NPF = (PAIRS + 255) / 256;       // pairs per thread
-  constexpr int SM = P_BYTES + BN * WPITCH + BN * 4;
+  constexpr int OPITCH = BN * 2 + 16;            // output staging row bytes
+  constexpr int SM = P_BYTES + BN * WPITCH + BN * 4 + FMT * 16 * OPITCH;
+  static_assert(SM * OCC <= 160 * 1024, "LDS capacity at the occupancy");
   __shared__ __attribute__((aligned(1024))) char smem[SM];
   char* const Ws = smem + P_BYTES;
+  char* const Os = smem + P_BYTES + BN * WPITCH + BN * 4;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -66,19 +72,29 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
 
   // filter chunks: row n, chunk g = (r, sp) holds taps (r, 2 sp) and
   // (r, 2 sp + 1), channels 0..3 each (zero past C, S, G)
-  for (int idx = tid; idx < BN * GMAX; idx += 256) {
-    const int n = idx / GMAX, g = idx - n * GMAX;
-    const int r = sdiv(g, a.inv_sp), sp = g - __umul24(r, a.SP);
-    const int s0 = 2 * sp, k = n0 + n;
-    u32x4 v = u32x4{0u, 0u, 0u, 0u};
-    if (g < a.G && k < a.Ng) {
+  {
+    constexpr int NFC = BN * GMAX / 256;  // chunks per thread
+    static_assert(NFC * 256 == BN * GMAX, "filter chunks per thread");
+    u32x2 d[NFC][2];
+#pragma unroll
+    for (int u = 0; u < NFC; ++u) {
+      const int idx = tid + u * 256;
+      const int n = idx / GMAX, g = idx - n * GMAX;
+      const int r = sdiv(g, a.inv_sp), sp = g - __umul24(r, a.SP);
+      const int s0 = 2 * sp, k = n0 + n;
+      const bool ok = g < a.G && k < a.Ng;
       const unsigned base = (unsigned)(__umul24(k, a.Kred) + __umul24(__umul24(r, a.S) + s0, a.C8)) * 2u;
-      const unsigned lo = s0 < a.S ? base : kOOB, hi = s0 + 1 < a.S ? base + (unsigned)a.C8 * 2u : kOOB;
-      const auto d0 = __builtin_amdgcn_raw_buffer_load_b64(rw, (int)lo, 0, 0);
-      const auto d1 = __builtin_amdgcn_raw_buffer_load_b64(rw, (int)hi, 0, 0);
-      v = u32x4{d0[0], d0[1], d1[0], d1[1]};  // channels past C are zero in the prepared filter
+      const unsigned lo = ok && s0 < a.S ? base : kOOB, hi = ok && s0 + 1 < a.S ? base + (unsigned)a.C8 * 2u : kOOB;
+      d[u][0] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rw, (int)lo, 0, 0));
+      d[u][1] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rw, (int)hi, 0, 0));
     }
-    *reinterpret_cast<u32x4*>(Ws + n * WPITCH + g * 16) = v;
+#pragma unroll
+    for (int u = 0; u < NFC; ++u) {
+      const int idx = tid + u * 256;
+      const int n = idx / GMAX, g = idx - n * GMAX;
+      // channels past C are zero in the prepared filter
+      *reinterpret_cast<u32x4*>(Ws + n * WPITCH + g * 16) = u32x4{d[u][0][0], d[u][0][1], d[u][1][0], d[u][1][1]};
+    }
   }
 
   // patch pixels of a tile: pair j = (row, column pair), 16 bytes in LDS;
@@ -189,23 +205,31 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
     for (int i = 0; i < FMW; ++i)
 #pragma unroll
       for (int j = 0; j < FNW; ++j) acc[i][j] = bias[j];
-#pragma unroll
-    for (int st = 0; st < GMAX / 4; ++st) {
+    // k-slice st + 1's fragments are read while st's MFMAs run
+    frag fa[2][FMW], fb[2][FNW];
+    auto load = [&](int st, int b) {
       const int g = st * 4 + (lane >> 4);
       const int r = sdiv(g, a.inv_sp), sp = g - __umul24(r, a.SP);
       const int toff = g < a.G ? (r * a.PWP + 2 * sp) * 8 : 0;
-      frag fa[FMW], fb[FNW];
 #pragma unroll
-      for (int i = 0; i < FMW; ++i) fa[i] = *reinterpret_cast<const frag*>(smem + abase[i] + toff);
+      for (int i = 0; i < FMW; ++i) fa[b][i] = *reinterpret_cast<const frag*>(smem + abase[i] + toff);
 #pragma unroll
-      for (int j = 0; j < FNW; ++j) fb[j] = *reinterpret_cast<const frag*>(Ws + bbase + j * 16 * WPITCH + st * 64);
+      for (int j = 0; j < FNW; ++j) fb[b][j] = *reinterpret_cast<const frag*>(Ws + bbase + j * 16 * WPITCH + st * 64);
+    };
+    load(0, 0);
+#pragma unroll
+    for (int st = 0; st < GMAX / 4; ++st) {
+      if (st + 1 < GMAX / 4) load(st + 1, (st + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < FMW; ++i)
 #pragma unroll
-        for (int j = 0; j < FNW; ++j) acc[i][j] = Mfma<T>::run(fb[j], fa[i], acc[i][j]);
+        for (int j = 0; j < FNW; ++j) acc[i][j] = Mfma<T>::run(fb[st & 1][j], fa[st & 1][i], acc[i][j]);
     }
 
-    // epilogue: each lane stores its 4 consecutive channels of a pixel (8 bytes)
+    // epilogue: each lane puts its 4 consecutive channels of a pixel (8
+    // bytes) into the tile's LDS rows; then 16-byte chunks of 8 channels go
+    // out, consecutive threads on consecutive chunks of the tile's pixels
     const int img = fdiv(tile, a.fd_tiles_img), rt = tile - img * a.tiles_img;
     const int row0 = rt * a.TR;
     const int valid = min(a.TR, a.P - row0) * a.Q;
@@ -213,17 +237,34 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
 #pragma unroll
     for (int i = 0; i < FMW; ++i) {
       const int ml = (wm * FMW + i) * 16 + (lane & 15);
-      const bool mok = wm * FMW + i < FMT && ml < valid;
+      if (wm * FMW + i >= FMT) continue;
 #pragma unroll
       for (int j = 0; j < FNW; ++j) {
-        const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
+        const int nl = wn * WTN + j * 16 + (lane >> 4) * 4;
         T o[4];
 #pragma unroll
         for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v], ac.lo, ac.hi));
-        u32x2 pk;
-        __builtin_memcpy(&pk, o, 8);
-        const unsigned off = mok && n < a.Ng ? (unsigned)((mbase + ml) * a.Ks + n) * 2u : kOOB;
-        __builtin_amdgcn_raw_buffer_store_b64(pk, ry, (int)off, 0, 0);
+        __builtin_memcpy(Os + ml * OPITCH + nl * 2, o, 8);
+      }
+    }
+    lds_barrier();  // the tile's outputs are in LDS
+    {
+      constexpr int CPX = BN / 8;  // 16-byte chunks per pixel
+      const bool vec = a.Ks % 8 == 0;
+      for (int q = tid; q < valid * CPX; q += 256) {
+        const int ml = q / CPX, c8 = q - ml * CPX;
+        const int n = n0 + c8 * 8;
+        if (n >= a.Ng) continue;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(Os + ml * OPITCH + c8 * 16);
+        const unsigned e = (unsigned)((mbase + ml) * a.Ks + n);
+        if (vec && n + 8 <= a.Ng) {
+          __builtin_amdgcn_raw_buffer_store_b128(v, ry, (int)(e * 2u), 0, 0);
+        } else {
+          T o[8];
+          __builtin_memcpy(o, &v, 16);
+          T* __restrict__ y = reinterpret_cast<T*>(a.y);
+          for (int t = 0; t < 8 && n + t < a.Ng; ++t) y[e + t] = o[t];
+        }
       }
     }
     if (!more) break;
@@ -317,10 +358,10 @@ void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& c, hipStream_t st
     else smallc_go<bf16, FMT, WM, PPX, GMAX, OCC>(a, st);                   \
     return;                                                                 \
   }
-  SC(7, 1664, 28, 2, 3)
-  SC(14, 2112, 28, 2, 3)
+  SC(7, 1664, 28, 2, 2)
+  SC(14, 2112, 28, 2, 2)
   SC(7, 704, 8, 2, 3)
-  SC(14, 1152, 8, 2, 3)
+  SC(14, 1152, 8, 2, 2)
   SC(14, 2112, 28, 4, 2)
 #undef SC
   check(false, "small-channel tile not instantiated");

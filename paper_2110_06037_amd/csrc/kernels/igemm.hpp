@@ -1064,8 +1064,8 @@ static const IgCfg kIg16[] = {
 #undef SN_PATCH_IG
     // small-channel (stem) kernel: NHWC, C <= 4, stride 1 or 2; 7 x 7 and 3 x 3 filters
     // (wm: wave rows; st: workgroups per CU)
-    {112, 64, 32, 0, 0, 3, 2, 3, 1664, {}, 4, 28}, {224, 64, 32, 0, 0, 3, 2, 3, 2112, {}, 4, 28},
-    {112, 64, 32, 0, 0, 3, 2, 3, 704, {}, 4, 8},   {224, 64, 32, 0, 0, 3, 2, 3, 1152, {}, 4, 8},
+    {112, 64, 32, 0, 0, 3, 2, 2, 1664, {}, 4, 28}, {224, 64, 32, 0, 0, 3, 2, 2, 2112, {}, 4, 28},
+    {112, 64, 32, 0, 0, 3, 2, 3, 704, {}, 4, 8},   {224, 64, 32, 0, 0, 3, 2, 2, 1152, {}, 4, 8},
     // streaming 1x1 kernel: NHWC, C = bk (BM pixels x BN channels per tile, WM wave rows,
     // loads pf tiles ahead)
 #define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM},
