@@ -71,11 +71,12 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
   const __amdgpu_buffer_rsrc_t ry = make_rsrc(a.y, a.y_elems * 2);
 
   // filter chunks: row n, chunk g = (r, sp) holds taps (r, 2 sp) and
-  // (r, 2 sp + 1), channels 0..3 each (zero past C, S, G)
+  // (r, 2 sp + 1), channels 0..3 each (zero past C, S, G); loaded here,
+  // put into LDS once the first patch's loads are in flight too
+  constexpr int NFC = BN * GMAX / 256;  // chunks per thread
+  static_assert(NFC * 256 == BN * GMAX, "filter chunks per thread");
+  u32x2 d[NFC][2];
   {
-    constexpr int NFC = BN * GMAX / 256;  // chunks per thread
-    static_assert(NFC * 256 == BN * GMAX, "filter chunks per thread");
-    u32x2 d[NFC][2];
 #pragma unroll
     for (int u = 0; u < NFC; ++u) {
       const int idx = tid + u * 256;
@@ -87,13 +88,6 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
       const unsigned lo = ok && s0 < a.S ? base : kOOB, hi = ok && s0 + 1 < a.S ? base + (unsigned)a.C8 * 2u : kOOB;
       d[u][0] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rw, (int)lo, 0, 0));
       d[u][1] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rw, (int)hi, 0, 0));
-    }
-#pragma unroll
-    for (int u = 0; u < NFC; ++u) {
-      const int idx = tid + u * 256;
-      const int n = idx / GMAX, g = idx - n * GMAX;
-      // channels past C are zero in the prepared filter
-      *reinterpret_cast<u32x4*>(Ws + n * WPITCH + g * 16) = u32x4{d[u][0][0], d[u][0][1], d[u][1][0], d[u][1][1]};
     }
   }
 
@@ -183,6 +177,13 @@ __global__ __launch_bounds__(256, OCC) void conv_smallc_kernel(SmallCArgs a) {
   int tile = blockIdx.x;
   if (tile >= a.tiles) return;
   fetch(tile, raw, shf, ok);
+#pragma unroll
+  for (int u = 0; u < NFC; ++u) {
+    const int idx = tid + u * 256;
+    const int n = idx / GMAX, g = idx - n * GMAX;
+    // channels past C are zero in the prepared filter
+    *reinterpret_cast<u32x4*>(Ws + n * WPITCH + g * 16) = u32x4{d[u][0][0], d[u][0][1], d[u][1][0], d[u][1][1]};
+  }
   store_patch(raw, shf, ok);
   __syncthreads();  // filter, bias and the first patch are in LDS
   f32x4 bias[FNW];
