@@ -33,8 +33,8 @@
 // when the workgroup tile is small; the groups' sums meet in LDS at the end.
 // The MFMA takes the filter as its first operand, so each lane's 4
 // accumulators are 4 consecutive output channels of one pixel; sums start at
-// the bias, and the epilogue applies the activation and stores each lane's 4
-// channels as one 8-byte store.
+// the bias, and the epilogue applies the activation, stages the tile in LDS
+// and stores it as 16-byte chunks of consecutive addresses.
 #include "gemm_common.hpp"
 #include "kcommon.hpp"
 #include "launch.hpp"
@@ -267,57 +267,79 @@ __global__ __launch_bounds__(512, 1) void conv3x3_patch_kernel(PatchArgs a) {
         }
     }
     __syncthreads();
-    if (grp == 1) return;
+    if (grp == 0) {
 #pragma unroll
-    for (int i = 0; i < FMW; ++i)
+      for (int i = 0; i < FMW; ++i)
 #pragma unroll
-      for (int j = 0; j < FNW; ++j) {
-        const int ml = (blk0 + i) * 16 + (lane & 15);
-        if (blk0 + i < FMT)
-          acc[i][j] += *reinterpret_cast<const f32x4*>(smem + ml * RPITCH + (wn * WTN + j * 16 + (lane >> 4) * 4) * 4);
-      }
+        for (int j = 0; j < FNW; ++j) {
+          const int ml = (blk0 + i) * 16 + (lane & 15);
+          if (blk0 + i < FMT)
+            acc[i][j] += *reinterpret_cast<const f32x4*>(smem + ml * RPITCH + (wn * WTN + j * 16 + (lane >> 4) * 4) * 4);
+        }
+    }
   }
 
   // epilogue: accumulator (i, j, v) is output pixel (blk0 + i)*16 + (lane&15)
-  // of the tile, channel wn*WTN + j*16 + (lane>>4)*4 + v; the tile's valid
-  // pixels are consecutive rows of the GEMM (whole rows of one image, or
-  // whole images); each lane stores its 4 channels as one 8-byte store
+  // of the tile, channel wn*WTN + j*16 + (lane>>4)*4 + v.  Tap group 0 puts
+  // the outputs (activation applied, 16-bit) into LDS rows of BN channels;
+  // then all waves store them as 16-byte chunks of 8 channels, consecutive
+  // threads on consecutive chunks (NHWC: the chunks of a pixel, then the
+  // next pixel; NC8HW8: the pixels of one channel block), so a wave's
+  // stores cover contiguous runs.  The tile's valid pixels are consecutive
+  // rows of the GEMM (whole rows of one image, or whole images).
+  constexpr int OP = BN * 2 + 16;  // staging row bytes
+  static_assert(FMT * 16 * OP <= SM, "output staging fits the tile's LDS");
   const ActClamp ac = act_clamp(a.act);
+  __syncthreads();  // every wave is done with the stages (and group 0 with group 1's sums)
+  if (grp == 0) {
+#pragma unroll
+    for (int i = 0; i < FMW; ++i) {
+      if (blk0 + i >= FMT) continue;
+      const int ml = (blk0 + i) * 16 + (lane & 15);
+#pragma unroll
+      for (int j = 0; j < FNW; ++j) {
+        const int nl = wn * WTN + j * 16 + (lane >> 4) * 4;
+        T o[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v], ac.lo, ac.hi));
+        __builtin_memcpy(smem + ml * OP + nl * 2, o, 8);
+      }
+    }
+  }
+  __syncthreads();
   const int valid = imgs * rows * a.Q;
   const int mbase = img0 * a.P * a.Q + row0 * a.Q;
   const int PQ = a.P * a.Q;
   T* __restrict__ y = reinterpret_cast<T*>(a.y);
   const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, a.y_elems * 2);
-  const bool vec4 = L == NC8 || (a.Ks % 4 == 0 && a.Ng % 4 == 0);
-#pragma unroll
-  for (int i = 0; i < FMW; ++i) {
-    const int ml = (blk0 + i) * 16 + (lane & 15);
-    const bool okm = blk0 + i < FMT && ml < valid;
+  constexpr int CPX = BN / 8;  // 16-byte chunks per pixel
+  const bool vec8 = L == NC8 || a.Ks % 8 == 0;
+  for (int q = tid; q < valid * CPX; q += NWV * 64) {
+    int ml, c8;
+    if constexpr (L == NC8) {
+      c8 = q / valid;
+      ml = q - c8 * valid;
+    } else {
+      ml = q / CPX;
+      c8 = q - ml * CPX;
+    }
+    const int n = n0 + c8 * 8;
+    if (n >= a.Ng) continue;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(smem + ml * OP + c8 * 16);
     const int m = mbase + ml;
-    unsigned mo;
+    unsigned e;
     if constexpr (L == NC8) {
       const int img = sdiv(m, a.inv_pq), pq = m - img * PQ;
-      mo = (unsigned)((img * (a.Ks >> 3) * PQ + pq) * 8);
+      e = (unsigned)(((img * (a.Ks >> 3) + (n >> 3)) * PQ + pq) * 8);
     } else {
-      mo = (unsigned)(m * a.Ks);
+      e = (unsigned)(m * a.Ks + n);
     }
-#pragma unroll
-    for (int j = 0; j < FNW; ++j) {
-      const int n = n0 + wn * WTN + j * 16 + (lane >> 4) * 4;
-      T o[4];
-#pragma unroll
-      for (int v = 0; v < 4; ++v) o[v] = from_f<T>(__builtin_amdgcn_fmed3f(acc[i][j][v], ac.lo, ac.hi));
-      if (vec4) {
-        unsigned e;
-        if constexpr (L == NC8) e = mo + (unsigned)((n >> 3) * PQ * 8 + (n & 7));
-        else e = mo + (unsigned)n;
-        const unsigned off = okm && n < a.Ng ? e * 2u : kOOB;
-        __builtin_amdgcn_raw_buffer_store_b64(*reinterpret_cast<const u32x2*>(o), ry, (int)off, 0, 0);
-      } else if (okm) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          if (n + v < a.Ng) y[(long long)m * a.Ks + n + v] = o[v];
-      }
+    if (vec8 && n + 8 <= a.Ng) {
+      __builtin_amdgcn_raw_buffer_store_b128(v, ry, (int)(e * 2u), 0, 0);
+    } else {
+      T o[8];
+      __builtin_memcpy(o, &v, 16);
+      for (int t = 0; t < 8 && n + t < a.Ng; ++t) y[e + t] = o[t];
     }
   }
 }
