@@ -118,6 +118,10 @@ typedef struct {
   int32_t dtype;     /* sn_dtype the routine computes and stores in          */
   int32_t schema;    /* dtype * SN_NUM_LAYOUTS + layout                      */
   int64_t cost_ns;   /* profiled time T(r) in ns, -1 if not profiled         */
+  int64_t ws_bytes;  /* device workspace the routine needs beyond the layer's
+                        input and output tensors (split reductions, the
+                        three-kernel Winograd's transforms, a projection
+                        stored for the two-launch routine), bytes           */
   char name[64];     /* descriptor, e.g. "nhwc/igemm:p41"; with several
                         dtypes allowed prefixed by the dtype, "f16:nhwc/..." */
 } sn_routine_desc;
@@ -144,10 +148,19 @@ typedef enum {
   SN_OPT_KEEP = 6,      /* 1: the plan gives every intermediate tensor its own bytes
                            (no reuse by liveness), so sn_layer_output can read any
                            layer's stored output after a run (default 0)            */
-  SN_OPT_DTYPES = 7     /* bitmask of element types routines may compute in (bit =
+  SN_OPT_DTYPES = 7,    /* bitmask of element types routines may compute in (bit =
                            sn_dtype), default the run dtype only; with more than one
                            every layer gets routines in each, and adapts cast
                            between them (precision-hybrid tuning, Sec. IV-F)        */
+  SN_OPT_WS_LIMIT = 8   /* largest workspace (sn_routine_desc.ws_bytes) a routine
+                           may use; routines above it are left out of every
+                           layer's routine set, so selection optimises time under
+                           that memory restriction (the restriction Sec. VI names
+                           as future work; Winograd's transforms are its example).
+                           -1 = no limit (the default); 0 = no workspace at all.
+                           A layer left with no routine is refused by
+                           sn_add_layer (SN_E_UNSUPPORTED).  A routine-set option:
+                           set it before adding layers                               */
 } sn_option;
 
 /* Creates a graph whose auxiliary input layer (id 0) carries the user tensor

@@ -82,7 +82,7 @@ int sn_set_option(sn_graph* gp, int32_t option, int64_t value) {
     CHECK_G(gp);
     Graph& g = gp->g;
     bool routine_set = option == SN_OPT_LAYOUTS || option == SN_OPT_ALGOS || option == SN_OPT_PARAMS ||
-                       option == SN_OPT_DTYPES;
+                       option == SN_OPT_DTYPES || option == SN_OPT_WS_LIMIT;
     if (routine_set && g.n_layers() > 1)
       fail(SN_E_STATE, "routine-set options must be set before adding layers");
     switch (option) {
@@ -120,6 +120,10 @@ int sn_set_option(sn_graph* gp, int32_t option, int64_t value) {
       case SN_OPT_FLUSH:
         if (value < 0 || value > (int64_t(1) << 34)) fail(SN_E_INVALID, "FLUSH is 0..16 GiB");
         g.opt_flush = value;
+        break;
+      case SN_OPT_WS_LIMIT:
+        if (value < -1) fail(SN_E_INVALID, "WS_LIMIT is -1 (no limit) or a byte count");
+        g.opt_ws_limit = value;
         break;
       default:
         fail(SN_E_INVALID, "unknown option");
@@ -419,6 +423,7 @@ int sn_routine_info(const sn_graph* gp, int32_t layer, int32_t idx, sn_routine_d
     out->dtype = r.dtype;
     out->schema = r.schema();
     out->cost_ns = L.cost[idx];
+    out->ws_bytes = (int64_t)routine_ws_bytes(g, L, r);
     std::snprintf(out->name, sizeof(out->name), "%s", r.name.c_str());
   });
 }

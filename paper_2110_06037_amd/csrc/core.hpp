@@ -137,6 +137,7 @@ struct Graph {
   int64_t opt_dtypes = 0;  // compute dtypes allowed (bit = sn_dtype); set to the run dtype at init
   int64_t opt_flush = 0;  // bytes written before each layer of a timed run (0 = none)
   int64_t opt_keep = 0;   // 1: the plan gives every buffer its own bytes
+  int64_t opt_ws_limit = -1;  // largest routine workspace admitted (bytes), -1: no limit
   std::vector<Layer> layers;  // layers[0] = auxiliary input
   std::vector<Edge> edges;    // every (input -> layer) edge, in insertion order
   std::vector<int> net_inputs{0};  // layers carrying the caller's input tensors, in order
@@ -198,6 +199,9 @@ void costs_from_json(Graph& g, const char* json);
 void dev_create(Graph& g);
 void dev_destroy(Graph& g);
 void dev_upload_layer(Graph& g, int layer);
+// Device workspace a routine of layer L needs beyond its input and output
+// tensors (host arithmetic only; also for host-only graphs).
+size_t routine_ws_bytes(const Graph& g, const Layer& L, const Routine& r);
 void dev_profile(Graph& g, int warmup, int reps, void* stream);
 void plan_compile(Graph& g);
 // d_in / d_out: one device pointer per net input / output, in order

@@ -273,7 +273,7 @@ void dev_upload_layer(Graph& g, int id) {
 }
 
 // ------------------------------------------------------------------ launching
-static size_t layer_ws_bytes(const Graph& g, const Layer& L, const Routine& r) {
+size_t routine_ws_bytes(const Graph& g, const Layer& L, const Routine& r) {
   if (L.inputs.empty()) return 0;  // the input layer
   const Shape& in = g.layers[L.inputs[0]].out;
   if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM)
@@ -413,7 +413,7 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
   size_t tmax = 0, wsmax = 0;
   for (const Layer& L : g.layers) {
     for (int l = 0; l < SN_NUM_LAYOUTS; ++l) tmax = std::max(tmax, (size_t)stored_numel(L.out, l) * es_max);
-    for (const Routine& r : L.routines) wsmax = std::max(wsmax, layer_ws_bytes(g, L, r));
+    for (const Routine& r : L.routines) wsmax = std::max(wsmax, routine_ws_bytes(g, L, r));
   }
   tmax = align256(tmax);
   void *in0 = nullptr, *in1 = nullptr, *outb = nullptr, *ws = nullptr, *flush = nullptr;
@@ -498,7 +498,7 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
         k::TDesc ind[2];
         for (size_t q = 0; q < L.inputs.size(); ++q) ind[q] = tdesc(g.layers[L.inputs[q]].out, r.layout);
         k::TDesc od = tdesc(L.out, r.layout);
-        size_t wsb = layer_ws_bytes(g, L, r);
+        size_t wsb = routine_ws_bytes(g, L, r);
         int64_t ns = time_it([&] { launch_layer(g, i, r, ins, ind, outb, od, ws, wsb, st); });
         D.cost_cache[key] = ns;
         L.cost[ri] = ns;
@@ -645,7 +645,7 @@ void plan_compile(Graph& g) {
       s.out.off = (size_t)b;
       uses.push_back(b);
     }
-    s.ws_bytes = layer_ws_bytes(g, L, r);
+    s.ws_bytes = routine_ws_bytes(g, L, r);
     if (s.ws_bytes) {
       int b = new_buf(s.ws_bytes, step_idx);
       s.ws.kind = 0;

@@ -206,6 +206,17 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
       }
     }
   }
+  if (g.opt_ws_limit >= 0) {
+    // memory-restricted selection: only routines within the workspace limit
+    std::vector<Routine> kept;
+    for (const Routine& r : out)
+      if ((int64_t)routine_ws_bytes(g, L, r) <= g.opt_ws_limit) {
+        kept.push_back(r);
+        kept.back().id = (int)kept.size() - 1;
+      }
+    if (kept.empty()) fail(SN_E_UNSUPPORTED, "no routine of this layer fits the workspace limit");
+    out.swap(kept);
+  }
   return out;
 }
 
@@ -312,9 +323,9 @@ static int add_layer_impl(Graph& g, const sn_layer_desc& d, const int32_t* input
     if (sc_bias) std::memcpy(L.bproj.data(), sc_bias, sizeof(float) * out.c);
   }
   L.signature = signature(g, L);
+  L.routines = enumerate_routines(g, L);  // (may refuse the layer: the workspace limit)
   g.layers.push_back(std::move(L));
   Layer& ref = g.layers.back();
-  ref.routines = enumerate_routines(g, ref);
   ref.cost.assign(ref.routines.size(), -1);
   for (int j : ref.inputs) g.edges.push_back(blank_edge(j, ref.id));
   g.have_costs = false;

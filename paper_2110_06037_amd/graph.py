@@ -30,7 +30,8 @@ class Graph:
     ``device=-1`` makes a host-only graph: only cost-table import, selection
     and queries work (no weights are uploaded)."""
 
-    def __init__(self, dtype, n, c, h, w, device=0, layouts=None, algos=None, params=True, dtypes=None):
+    def __init__(self, dtype, n, c, h, w, device=0, layouts=None, algos=None, params=True, dtypes=None,
+                 ws_limit=None):
         self.lib = N.lib()
         self.dtype = N.DTYPE[dtype] if isinstance(dtype, str) else dtype
         self.dtype_name = {v: k for k, v in N.DTYPE.items()}[self.dtype]
@@ -49,6 +50,8 @@ class Graph:
         if dtypes is not None:
             mask = sum(1 << (N.DTYPE[d] if isinstance(d, str) else d) for d in dtypes)
             self.set_option(N.OPT_DTYPES, mask)
+        if ws_limit is not None:
+            self.set_option(N.OPT_WS_LIMIT, ws_limit)
         self.in_shape = (n, c, h, w)
         self.in_shapes = [self.in_shape]
 
@@ -238,7 +241,7 @@ class Graph:
             d = N.RoutineDesc()
             N.check(self.lib.sn_routine_info(self._g, layer, i, ctypes.byref(d)))
             out.append({"id": d.id, "layout": d.layout, "algo": d.algo, "param": d.param,
-                        "dtype": d.dtype, "schema": d.schema, "cost_ns": d.cost_ns,
+                        "dtype": d.dtype, "schema": d.schema, "cost_ns": d.cost_ns, "ws_bytes": d.ws_bytes,
                         "name": d.name.decode()})
         return out
 
@@ -344,19 +347,21 @@ def to_device(arr, dtype, device=0):
     return torch.from_numpy(a).to(f"cuda:{device}")
 
 
-def build_from_spec(spec, tensors=None, device=0, layouts=None, algos=None, params=True, dtypes=None):
+def build_from_spec(spec, tensors=None, device=0, layouts=None, algos=None, params=True, dtypes=None,
+                    ws_limit=None):
     """Create a graph from a ``workloads`` net spec.  ``tensors`` holds the
     generated weights (``workloads.generate``); host-only graphs (device -1)
     may pass None and get zero weights of the right shapes.  ``dtypes``: the
     element types routines may compute in (default: the spec's dtype only);
-    a spec's ``outputs`` list marks the net outputs."""
+    a spec's ``outputs`` list marks the net outputs; ``ws_limit``: the
+    largest routine workspace admitted (bytes; None = no limit)."""
     from workloads import weight_shapes
     n = spec["batch"]
     c, h, w = spec["in_chw"]
     g = Graph(spec["dtype"], n, c, h, w, device=device,
               layouts=spec.get("layouts") if layouts is None else layouts,
               algos=spec.get("algos") if algos is None else algos, params=params,
-              dtypes=spec.get("dtypes") if dtypes is None else dtypes)
+              dtypes=spec.get("dtypes") if dtypes is None else dtypes, ws_limit=ws_limit)
     shapes = weight_shapes(spec)
     for i, layer in enumerate(spec["layers"]):
         wt = bt = None

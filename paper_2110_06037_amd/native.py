@@ -25,7 +25,7 @@ ALGO_NAME = {v: k for k, v in ALGO.items()}
 L_INPUT, L_CONV2D, L_MAXPOOL, L_GAP, L_ADD, L_FC, L_OUTPUT = range(7)
 ACT = {"none": 0, "relu": 1, "relu6": 2}
 SELECT_DPRS, SELECT_FIXED = 0, 1
-OPT_LAYOUTS, OPT_ALGOS, OPT_PARAMS, OPT_HIPGRAPH, OPT_SEED, OPT_FLUSH, OPT_KEEP, OPT_DTYPES = range(8)
+OPT_LAYOUTS, OPT_ALGOS, OPT_PARAMS, OPT_HIPGRAPH, OPT_SEED, OPT_FLUSH, OPT_KEEP, OPT_DTYPES, OPT_WS_LIMIT = range(9)
 DTYPE_NAME = {v: k for k, v in DTYPE.items()}
 
 STATUS = {0: "SN_OK", -1: "SN_E_INVALID", -2: "SN_E_SHAPE", -3: "SN_E_STATE",
@@ -47,7 +47,7 @@ class LayerDesc(ctypes.Structure):
 class RoutineDesc(ctypes.Structure):
     _fields_ = [("id", ctypes.c_int32), ("layout", ctypes.c_int32), ("algo", ctypes.c_int32),
                 ("param", ctypes.c_int32), ("dtype", ctypes.c_int32), ("schema", ctypes.c_int32),
-                ("cost_ns", ctypes.c_int64), ("name", ctypes.c_char * 64)]
+                ("cost_ns", ctypes.c_int64), ("ws_bytes", ctypes.c_int64), ("name", ctypes.c_char * 64)]
 
 
 # exported functions: name -> (restype, argtypes)

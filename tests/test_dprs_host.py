@@ -403,3 +403,41 @@ def test_integrated_profiling_needs_costs_and_a_device():
         g.profile_integrated(reps=5)
     with pytest.raises(N.SNError, match="SN_E_INVALID"):
         g.profile_integrated(warmup=-1, reps=0)
+
+
+def test_workspace_limit_restricts_the_routine_set():
+    # Time optimised under a memory restriction (the restriction the paper's
+    # Sec. VI names as future work, Winograd's transforms its example): with
+    # SN_OPT_WS_LIMIT every layer keeps exactly the routines whose workspace
+    # fits, ids stay dense, and the DP path is the exhaustive optimum over the
+    # reduced set
+    w = np.zeros((64, 64, 3, 3), np.uint16)
+    b = np.zeros(64, np.float32)
+
+    def build(limit):
+        g = Graph("bf16", 2, 64, 14, 14, device=-1, ws_limit=limit)
+        c1 = g.add_conv(0, w, b, 1, 1)
+        g.add_conv(c1, w, b, 1, 1)
+        return g
+
+    free = build(None)
+    full = [free.routines(i) for i in (1, 2)]
+    assert any(r["ws_bytes"] > 0 for r in full[0]), "split Winograd and split reductions use workspace"
+    for limit in (0, min(r["ws_bytes"] for r in full[0] if r["ws_bytes"] > 0)):
+        g = build(limit)
+        for li, every in zip((1, 2), full):
+            kept = g.routines(li)
+            assert [r["id"] for r in kept] == list(range(len(kept)))
+            assert [r["name"] for r in kept] == [r["name"] for r in every if r["ws_bytes"] <= limit]
+            assert all(r["ws_bytes"] <= limit for r in kept) and len(kept) < len(every)
+        # random costs: the DP over the reduced set equals exhaustive search over it
+        costs = randomise(g.costs(), 3 + limit % 5, max_cost=50)
+        assert dp_vs(g, costs) == exhaustive(problem_from_costs(costs))[1::-1]
+        g.close()
+    free.close()
+    # the option's range, and it is a routine-set option (before any layer)
+    g = Graph("bf16", 2, 64, 14, 14, device=-1, ws_limit=0)
+    assert status_of(g.set_option, N.OPT_WS_LIMIT, -2) == -1
+    g.add_conv(0, w, b, 1, 1)
+    assert status_of(g.set_option, N.OPT_WS_LIMIT, 1 << 20) == -3   # after layers were added
+    g.close()

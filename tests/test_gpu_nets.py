@@ -143,6 +143,28 @@ def test_net_dp_and_fixed_paths_match_oracle(name):
     g.close()
 
 
+def test_workspace_limited_selection_runs_within_the_limit():
+    # memory-restricted tuning: with no routine workspace allowed, the
+    # profiled DP path of a bs2 ResNet-18 (split-reduction tiles and the
+    # three-kernel Winograd left out) uses none, and matches the oracle
+    spec = fuse_projection(fuse_residual(resnet18(2, "bf16")))
+    t = generate(spec)
+    free = build_from_spec(spec, t)
+    g = build_from_spec(spec, t, ws_limit=0)
+    n_layers = len(spec["layers"]) + 1
+    assert sum(len(g.routines(i)) for i in range(1, n_layers)) < sum(len(free.routines(i)) for i in range(1, n_layers))
+    free.close()
+    g.profile(warmup=2, reps=5)
+    g.select("dprs")
+    ids, _ = g.path()
+    assert all(g.routines(i)[ids[i]]["ws_bytes"] == 0 for i in range(1, n_layers))
+    out, _ = run_out(g, spec, t)
+    e = err(out, oracle_out(spec, t), "bf16")
+    print(f"resnet18 bs2 workspace-free dprs err {e:.3e}", flush=True)
+    assert e <= TOL["bf16"]
+    g.close()
+
+
 def test_resnet50_bs32_dp_path_sampled_images():
     # the benchmark's configuration: full batch on the GPU, images 0 and 1
     # through the oracle (images are independent)
