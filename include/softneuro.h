@@ -395,6 +395,16 @@ int sn_integrated_candidate(const sn_graph* g, int32_t idx, int32_t* routine_ids
  * only, else 9 x 9, indexed by schema (dtype * 3 + layout).  The implicit
  * auxiliary output layer appears as the last layer with one NCHW routine (run
  * dtype) of time 0, with an edge from the net output layer.
+ * A routine built from sub-layers (a childnet, Sec. III-D: the three-kernel
+ * Winograd routine is wgenc -> wgconv -> wgdec, one wgconv sub-routine per
+ * GEMM tile) also carries
+ *   "child":{"layers":[names],"routines":[[names] per sub-layer],
+ *            "ns":[[times] per sub-layer],"path":[chosen sub-routine per sub-layer]}
+ * sn_profile times every sub-routine on its own, and the routine's "ns" is
+ * the DPRS optimum over its sub-layers (Sec. IV-F: the algorithm is applied
+ * to a childnet first).  sn_set_costs recomputes that optimum, and the path
+ * the routine runs with, from "child" whenever any sub-routine time there is
+ * known; with every one unknown (-1) the routine keeps the listed "ns".
  * sn_get_costs writes at most cap bytes including the terminating NUL; if
  * cap is too small it returns SN_E_NOMEM with *len = required size.
  * sn_set_costs replaces the table (host-only graphs included); it must list

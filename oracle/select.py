@@ -175,3 +175,22 @@ def problem_from_costs(costs):
         A = [[None if v < 0 else v for v in row] for row in e["ns"]]
         edges.append((e["from"], e["to"], A))
     return {"n_layers": len(routines), "routines": routines, "edges": edges}
+
+
+def childnet_time(rows):
+    """Time and sub-routine choice of a routine built from sub-layers (a
+    childnet, Sec. III-D): ``rows[s]`` lists the times of sub-layer s's
+    sub-routines (None or a negative value = unavailable).  The sub-layers
+    form a chain passing tensors of one fixed format (no adapts), so a
+    choice's time is the sum of its members' times; every choice is
+    enumerated and the minimum (ties: the lowest tuple of indices) returned,
+    or (None, None) when some sub-layer has no available sub-routine."""
+    best = None
+    for choice in itertools.product(*[range(len(r)) for r in rows]):
+        ts = [rows[s][q] for s, q in enumerate(choice)]
+        if any(t is None or t < 0 for t in ts):
+            continue
+        key = (sum(ts), choice)
+        if best is None or key < best:
+            best = key
+    return (None, None) if best is None else best

@@ -88,6 +88,26 @@ struct Routine {
   int schema() const { return schema_of(dtype, layout); }
 };
 
+// A routine built from sub-layers, each with routines of its own (a
+// childnet, Sec. III-D).  Its sub-routines are profiled one by one and its
+// time is the DPRS optimum over the sub-layers, found before the net's own
+// DPRS runs (the algorithm applied from the innermost childnet outward).
+// The sub-layers pass internal tensors of one fixed format, so the
+// childnet has one schema and no adapts.
+struct ChildNet {
+  std::vector<std::string> layer;                 // sub-layer names
+  std::vector<std::vector<std::string>> routine;  // [sub-layer][sub-routine] names
+  std::vector<std::vector<int64_t>> cost;         // [sub-layer][sub-routine] ns, -1 = unknown
+  std::vector<int> path;                          // selected sub-routine per sub-layer
+  bool empty() const { return layer.empty(); }
+  bool profiled() const {
+    for (const auto& v : cost)
+      for (int64_t c : v)
+        if (c >= 0) return true;
+    return false;
+  }
+};
+
 struct Layer {
   int id = 0;
   int type = SN_LAYER_INPUT;
@@ -104,6 +124,7 @@ struct Layer {
   std::vector<float> bproj;
   std::vector<Routine> routines;
   std::vector<int64_t> cost;  // per routine, ns; -1 = not profiled
+  std::vector<ChildNet> child;  // per routine; empty for routines that are not childnets
   std::string signature;      // identical signatures share profiling results
 };
 
@@ -179,9 +200,16 @@ std::vector<Edge> all_edges(const Graph& g);
 std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L);
 bool winograd_applicable(const Layer& L, const Shape& in);
 std::string routine_name(const Graph& g, const Layer& L, const Routine& r);
+// the childnet of a routine (empty when the routine is a single kernel
+// sequence of its own): the split Winograd F(2x2,3x3) routine is wgenc ->
+// wgconv (one sub-routine per GEMM tile) -> wgdec
+ChildNet make_childnet(const Graph& g, const Layer& L, const Routine& r);
 
 // select.cpp
 void select_dprs(Graph& g, int layout_mask = -1, int dtype_mask = -1);
+// DPRS over a childnet (a chain of sub-layers, one schema): sets c.path and
+// returns its time, -1 when some sub-layer has no timed sub-routine
+int64_t childnet_select(ChildNet& c);
 // integrated profiling's candidate paths (Sec. III-C): DPRS over every
 // non-empty subset of the allowed layouts, then every fixed path; identical
 // paths kept once; g.path is left unchanged

@@ -292,9 +292,11 @@ size_t routine_ws_bytes(const Graph& g, const Layer& L, const Routine& r) {
   return 0;
 }
 
+// sub >= 0 launches only that sub-layer of a childnet routine, with
+// sub-routine sub_routine (unit profiling of the childnet's sub-routines)
 static void launch_layer(const Graph& g, int id, const Routine& r, const void* const* in,
                          const k::TDesc* ind, void* out, const k::TDesc& outd, void* ws,
-                         size_t ws_bytes, hipStream_t st) {
+                         size_t ws_bytes, hipStream_t st, int sub = -1, int sub_routine = 0) {
   const Layer& L = g.layers[id];
   const DevLayer& dl = g.dev->L[id];
   const int dt = r.dtype;
@@ -354,8 +356,13 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
         k::conv_direct(dt, a, st);
       } else if (r.algo == SN_ALGO_IGEMM) {
         k::conv_igemm(dt, r.param, a, st);
-      } else if (r.param == 0) {
-        k::conv_winograd(dt, a, st);
+      } else if (r.param == 0) {  // the childnet wgenc -> wgconv -> wgdec
+        if (sub >= 0) {
+          k::winograd_sub(dt, sub, sub_routine, a, st);
+        } else {
+          const ChildNet& cn = L.child[r.id];
+          k::conv_winograd(dt, a, cn.path.size() > 1 ? cn.path[1] : 0, st);
+        }
       } else {
         k::conv_wino_fused(dt, r.param - 1, a, st);
       }
@@ -487,6 +494,30 @@ void dev_profile(Graph& g, int warmup, int reps, void* stream) {
       if (L.type == SN_LAYER_INPUT) continue;  // a net input: its one routine costs 0
       for (size_t ri = 0; ri < L.routines.size(); ++ri) {
         const Routine& r = L.routines[ri];
+        ChildNet& cn = L.child[ri];
+        if (!cn.empty()) {
+          // a childnet: every sub-routine is profiled on its own, and the
+          // routine's time is the DPRS optimum over the sub-layers
+          fill(r.dtype);
+          const void* ins[2] = {in0, in1};
+          k::TDesc ind[2];
+          for (size_t q = 0; q < L.inputs.size(); ++q) ind[q] = tdesc(g.layers[L.inputs[q]].out, r.layout);
+          const k::TDesc od = tdesc(L.out, r.layout);
+          const size_t wsb = routine_ws_bytes(g, L, r);
+          for (size_t sl = 0; sl < cn.layer.size(); ++sl)
+            for (size_t q = 0; q < cn.routine[sl].size(); ++q) {
+              const std::string skey = L.signature + "|" + r.name + "|" + cn.layer[sl] + "/" + cn.routine[sl][q] + mode_key;
+              auto it = D.cost_cache.find(skey);
+              if (it == D.cost_cache.end()) {
+                const int64_t ns =
+                    time_it([&] { launch_layer(g, i, r, ins, ind, outb, od, ws, wsb, st, (int)sl, (int)q); });
+                it = D.cost_cache.emplace(skey, ns).first;
+              }
+              cn.cost[sl][q] = it->second;
+            }
+          L.cost[ri] = childnet_select(cn);
+          continue;
+        }
         std::string key = L.signature + "|" + r.name + mode_key;
         auto it = D.cost_cache.find(key);
         if (it != D.cost_cache.end()) {

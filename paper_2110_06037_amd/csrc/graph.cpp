@@ -57,6 +57,7 @@ static Layer input_layer(int id, int dtype, Shape s) {
   r.name = "input/nchw";
   L.routines.push_back(r);
   L.cost.push_back(0);
+  L.child.emplace_back();
   L.signature = "input";
   return L;
 }
@@ -220,6 +221,19 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
   return out;
 }
 
+ChildNet make_childnet(const Graph& g, const Layer& L, const Routine& r) {
+  ChildNet c;
+  if (L.type != SN_LAYER_CONV2D || r.algo != SN_ALGO_WINOGRAD || r.param != 0) return c;
+  // one GEMM tile only when routine parameters are restricted
+  const int ng = g.opt_params ? k::winograd_gemm_num_configs(r.dtype) : 1;
+  c.layer = {"wgenc", "wgconv", "wgdec"};
+  c.routine = {{"wgenc"}, {}, {"wgdec"}};
+  for (int q = 0; q < ng; ++q) c.routine[1].push_back("wgconv:p" + std::to_string(q));
+  for (const auto& v : c.routine) c.cost.emplace_back(v.size(), -1);
+  c.path.assign(c.layer.size(), 0);
+  return c;
+}
+
 static std::string signature(const Graph& g, const Layer& L) {
   std::ostringstream o;
   o << "t" << L.type << " k" << L.d.k << " r" << L.d.r << " s" << L.d.s << " st" << L.d.stride
@@ -327,6 +341,7 @@ static int add_layer_impl(Graph& g, const sn_layer_desc& d, const int32_t* input
   g.layers.push_back(std::move(L));
   Layer& ref = g.layers.back();
   ref.cost.assign(ref.routines.size(), -1);
+  for (const Routine& r : ref.routines) ref.child.push_back(make_childnet(g, ref, r));
   for (int j : ref.inputs) g.edges.push_back(blank_edge(j, ref.id));
   g.have_costs = false;
   if (!g.host_only()) dev_upload_layer(g, ref.id);

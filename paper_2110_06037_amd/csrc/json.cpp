@@ -22,7 +22,28 @@ std::string costs_to_json(const Graph& g) {
       if (r) o << ",";
       o << "{\"rid\":" << R.id << ",\"layout\":" << R.layout << ",\"algo\":" << R.algo
         << ",\"param\":" << R.param << ",\"dtype\":" << R.dtype << ",\"schema\":" << R.schema()
-        << ",\"ns\":" << L.cost[r] << ",\"name\":\"" << R.name << "\"}";
+        << ",\"ns\":" << L.cost[r] << ",\"name\":\"" << R.name << "\"";
+      const ChildNet& c = L.child[r];
+      if (!c.empty()) {  // a childnet: its sub-layers, sub-routines, their times and its path
+        o << ",\"child\":{\"layers\":[";
+        for (size_t s = 0; s < c.layer.size(); ++s) o << (s ? "," : "") << "\"" << c.layer[s] << "\"";
+        o << "],\"routines\":[";
+        for (size_t s = 0; s < c.routine.size(); ++s) {
+          o << (s ? "," : "") << "[";
+          for (size_t q = 0; q < c.routine[s].size(); ++q) o << (q ? "," : "") << "\"" << c.routine[s][q] << "\"";
+          o << "]";
+        }
+        o << "],\"ns\":[";
+        for (size_t s = 0; s < c.cost.size(); ++s) {
+          o << (s ? "," : "") << "[";
+          for (size_t q = 0; q < c.cost[s].size(); ++q) o << (q ? "," : "") << c.cost[s][q];
+          o << "]";
+        }
+        o << "],\"path\":[";
+        for (size_t s = 0; s < c.path.size(); ++s) o << (s ? "," : "") << c.path[s];
+        o << "]}";
+      }
+      o << "}";
     }
     o << "]}";
   }
@@ -194,6 +215,7 @@ void costs_from_json(Graph& g, const char* json) {
   if ((int)layers.size() != g.n_layers() + 1)
     fail(SN_E_INVALID, "cost table lists a different number of layers");
   std::vector<std::vector<int64_t>> cost(g.n_layers());
+  std::vector<std::vector<ChildNet>> child(g.n_layers());
   for (int i = 0; i < g.n_layers(); ++i) {
     const JVal& jl = layers[i];
     if (jl.at("id").as_int() != i) fail(SN_E_INVALID, "layers must be listed in id order");
@@ -209,7 +231,27 @@ void costs_from_json(Graph& g, const char* json) {
         fail(SN_E_INVALID, "layer " + std::to_string(i) + ": routine list differs");
       long long ns = rts[r].at("ns").as_int();
       if (ns < -1) fail(SN_E_INVALID, "negative time");
+      ChildNet c = L.child[r];
+      if (rts[r].obj.count("child")) {
+        // a childnet's sub-routine times: when any is known, the routine's
+        // time is the DPRS optimum over them (the listed "ns" is not used);
+        // a childnet never profiled keeps the routine's own time
+        if (c.empty()) fail(SN_E_INVALID, "layer " + std::to_string(i) + ": child times for a plain routine");
+        const auto& rows = rts[r].at("child").at("ns").as_arr();
+        if (rows.size() != c.cost.size()) fail(SN_E_INVALID, "childnet sub-layer count differs");
+        for (size_t s = 0; s < rows.size(); ++s) {
+          const auto& row = rows[s].as_arr();
+          if (row.size() != c.cost[s].size()) fail(SN_E_INVALID, "childnet sub-routine count differs");
+          for (size_t q = 0; q < row.size(); ++q) {
+            const long long v = row[q].as_int();
+            if (v < -1) fail(SN_E_INVALID, "negative time");
+            c.cost[s][q] = v;
+          }
+        }
+        if (c.profiled()) ns = childnet_select(c);
+      }
       cost[i].push_back(ns);
+      child[i].push_back(c);
     }
   }
   for (int i = 0; i < g.n_layers(); ++i)
@@ -240,7 +282,10 @@ void costs_from_json(Graph& g, const char* json) {
       }
     }
   }
-  for (int i = 0; i < g.n_layers(); ++i) g.layers[i].cost = cost[i];
+  for (int i = 0; i < g.n_layers(); ++i) {
+    g.layers[i].cost = cost[i];
+    g.layers[i].child = child[i];
+  }
   for (size_t k = 0; k < g.edges.size(); ++k)
     std::memcpy(g.edges[k].adapt, parsed[k].adapt, sizeof(parsed[k].adapt));
   g.out_edges.assign(parsed.begin() + g.edges.size(), parsed.end());

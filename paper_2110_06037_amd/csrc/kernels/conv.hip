@@ -259,8 +259,7 @@ __global__ __launch_bounds__(256) void wino_in_kernel(WinoArgs a) {
     }
   T* __restrict__ vout = reinterpret_cast<T*>(a.v);
   const long long plane = (long long)a.T * a.C8;
-#pragma unroll
-  for (int e0 = 0; e0 < 1; ++e0) {
+  {
     float u[4][4][8];
     // rows: B^T d
 #pragma unroll
@@ -369,10 +368,23 @@ size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k) {
   return align256(16 * T * C8 * es) + align256(16 * T * Kp * 4);
 }
 
+// The routine is a childnet of three sub-layers, each launched on its own:
+// the input transform (wgenc), the 16 batched GEMMs (wgconv, whose tile is
+// the sub-routine: index into kWinoGemm), the output transform (wgdec).
+// V and M live in the workspace between them.
+static const IgCfg kWinoGemm16[] = {{64, 64, 64, 0, 4}, {128, 64, 64, 0, 4}, {128, 128, 64, 0, 2}};
+static const IgCfg kWinoGemm32[] = {{64, 64, 32, 0, 2}};
+
+int winograd_gemm_num_configs(int dtype) {
+  return dtype == 0 ? (int)(sizeof(kWinoGemm32) / sizeof(kWinoGemm32[0]))
+                    : (int)(sizeof(kWinoGemm16) / sizeof(kWinoGemm16[0]));
+}
+
 template <typename T>
-static void wino_dispatch(int dtype, const ConvArgs& c, hipStream_t st) {
+static WinoArgs wino_args(int dtype, const ConvArgs& c) {
   check(c.r == 3 && c.s == 3 && c.stride == 1 && c.pad == 1, "Winograd F(2x2,3x3) needs 3x3/1 pad 1");
   check(c.xd.layout == c.yd.layout, "Winograd reads and writes one layout");
+  check(!c.res, "Winograd routine takes no residual");
   WinoArgs a{};
   a.x = c.x;
   a.bias = c.bias;
@@ -390,22 +402,36 @@ static void wino_dispatch(int dtype, const ConvArgs& c, hipStream_t st) {
   a.Ks = c.yd.cs;
   a.act = c.act;
   const int Kp = (c.yd.c + 7) / 8 * 8;
-  const size_t es = sizeof(T);
-  const size_t vbytes = align256(16ull * a.T * a.C8 * es);
+  const size_t vbytes = align256(16ull * a.T * a.C8 * sizeof(T));
   check(c.ws && c.ws_bytes >= winograd_ws_bytes(dtype, c.xd, c.yd.c), "Winograd workspace too small");
   check(16ll * a.T * std::max(a.C8, Kp) < (1ll << 31), "tensor too large");
   a.v = c.ws;
-  float* mbuf = reinterpret_cast<float*>(reinterpret_cast<char*>(c.ws) + vbytes);
-  a.m = mbuf;
-  const int CB = a.C8 / 8, NB = (a.Ng + 7) / 8;
-  dim3 gin((unsigned)(((long long)a.T * CB + 255) / 256));
-  dim3 gout((unsigned)(((long long)a.T * NB + 255) / 256));
+  a.m = reinterpret_cast<float*>(reinterpret_cast<char*>(c.ws) + vbytes);
+  return a;
+}
+
+template <typename T>
+static void wino_enc_t(int dtype, const ConvArgs& c, hipStream_t st) {
+  const WinoArgs a = wino_args<T>(dtype, c);
+  dim3 g((unsigned)(((long long)a.T * (a.C8 / 8) + 255) / 256));
+  switch (c.xd.layout) {
+    case NCHW: SN_LAUNCH((wino_in_kernel<T, NCHW>), g, dim3(256), 0, st, a); break;
+    case NHWC: SN_LAUNCH((wino_in_kernel<T, NHWC>), g, dim3(256), 0, st, a); break;
+    case NC8: SN_LAUNCH((wino_in_kernel<T, NC8>), g, dim3(256), 0, st, a); break;
+  }
+}
+
+template <typename T>
+static void wino_gemm_t(int dtype, const ConvArgs& c, int cfg, hipStream_t st) {
+  const WinoArgs a = wino_args<T>(dtype, c);
+  check(cfg >= 0 && cfg < winograd_gemm_num_configs(dtype), "unknown Winograd GEMM tile");
+  const int Kp = (c.yd.c + 7) / 8 * 8;
   // batched GEMM: A = V_xi as a [T][C8] matrix (1x1 "NHWC" convolution), B = U_xi [Kp][C8]
   IgArgs g{};
   g.x = a.v;
   g.w = c.w;
   g.bias = c.bias;
-  g.y = mbuf;
+  g.y = const_cast<float*>(a.m);
   g.C = a.C8;
   g.H = 1;
   g.W = a.T;
@@ -421,8 +447,8 @@ static void wino_dispatch(int dtype, const ConvArgs& c, hipStream_t st) {
   g.PQ = a.T;
   g.M = a.T;
   g.Ng = a.Ng;
-  g.CB = CB;
-  g.KC = CB;
+  g.CB = a.C8 / 8;
+  g.KC = a.C8 / 8;
   g.Kred = a.C8;
   g.x_bs = (long long)a.T * a.C8;
   g.w_bs = (long long)Kp * a.C8;
@@ -430,27 +456,36 @@ static void wino_dispatch(int dtype, const ConvArgs& c, hipStream_t st) {
   g.vec = 1;
   g.x_elems = (long long)a.T * a.C8;
   g.w_elems = (long long)Kp * a.C8;
-  const IgCfg gc = std::is_same<T, float>::value ? IgCfg{64, 64, 32, 0, 2}
-                   : (a.T >= 4096 && a.Ng >= 128 ? IgCfg{128, 64, 64, 0, 4} : IgCfg{64, 64, 64, 0, 4});
+  const IgCfg gc = std::is_same<T, float>::value ? kWinoGemm32[cfg] : kWinoGemm16[cfg];
   ig_decompose(g, gc);
-  switch (c.xd.layout) {
-    case NCHW: SN_LAUNCH((wino_in_kernel<T, NCHW>), gin, dim3(256), 0, st, a); break;
-    case NHWC: SN_LAUNCH((wino_in_kernel<T, NHWC>), gin, dim3(256), 0, st, a); break;
-    case NC8: SN_LAUNCH((wino_in_kernel<T, NC8>), gin, dim3(256), 0, st, a); break;
-  }
   igemm_cfg<T, NHWC, true, EPI_RAW>(gc, g, 16, st);
+}
+
+template <typename T>
+static void wino_dec_t(int dtype, const ConvArgs& c, hipStream_t st) {
+  const WinoArgs a = wino_args<T>(dtype, c);
+  dim3 g((unsigned)(((long long)a.T * ((a.Ng + 7) / 8) + 255) / 256));
   switch (c.xd.layout) {
-    case NCHW: SN_LAUNCH((wino_out_kernel<T, NCHW>), gout, dim3(256), 0, st, a); break;
-    case NHWC: SN_LAUNCH((wino_out_kernel<T, NHWC>), gout, dim3(256), 0, st, a); break;
-    case NC8: SN_LAUNCH((wino_out_kernel<T, NC8>), gout, dim3(256), 0, st, a); break;
+    case NCHW: SN_LAUNCH((wino_out_kernel<T, NCHW>), g, dim3(256), 0, st, a); break;
+    case NHWC: SN_LAUNCH((wino_out_kernel<T, NHWC>), g, dim3(256), 0, st, a); break;
+    case NC8: SN_LAUNCH((wino_out_kernel<T, NC8>), g, dim3(256), 0, st, a); break;
   }
 }
 
-void conv_winograd(int dtype, const ConvArgs& c, hipStream_t st) {
-  check(!c.res, "Winograd routine takes no residual");
-  if (dtype == 0) wino_dispatch<float>(dtype, c, st);
-  else if (dtype == 1) wino_dispatch<f16>(dtype, c, st);
-  else wino_dispatch<bf16>(dtype, c, st);
+void winograd_sub(int dtype, int sub, int cfg, const ConvArgs& c, hipStream_t st) {
+  check(sub >= 0 && sub <= 2, "Winograd sub-layer is 0 (wgenc), 1 (wgconv) or 2 (wgdec)");
+#define WSUB(T_)                                    \
+  if (sub == 0) wino_enc_t<T_>(dtype, c, st);       \
+  else if (sub == 1) wino_gemm_t<T_>(dtype, c, cfg, st); \
+  else wino_dec_t<T_>(dtype, c, st);
+  if (dtype == 0) { WSUB(float) }
+  else if (dtype == 1) { WSUB(f16) }
+  else { WSUB(bf16) }
+#undef WSUB
+}
+
+void conv_winograd(int dtype, const ConvArgs& c, int gemm_cfg, hipStream_t st) {
+  for (int sub = 0; sub < 3; ++sub) winograd_sub(dtype, sub, gemm_cfg, c, st);
 }
 
 // ------------------------------------------------------------------ depthwise

@@ -1236,6 +1236,7 @@ static void igemm_cfg(const IgCfg& c, const IgArgs& a, int batch, hipStream_t st
       switch (key) {
         IGC(64, 64, 64, 4)
         IGC(128, 64, 64, 4)
+        IGC(128, 128, 64, 2)
         default: check(false, "tile not instantiated for the raw epilogue");
       }
       return;

@@ -148,11 +148,9 @@ int64_t ipow(int64_t b, int e) {
   return r;
 }
 
-}  // namespace
-
-void select_dprs(Graph& g, int layout_mask, int dtype_mask) {
-  if (!g.have_costs) fail(SN_E_STATE, "no cost table: call sn_profile or sn_set_costs first");
-  Problem P = make_problem(g, layout_mask, dtype_mask);
+// DPRS over a problem: the (time, lexicographic) minimum complete state;
+// per-layer statistics into *stats when given.
+State dprs_solve(const Problem& P, std::vector<DPLayerStats>* stats) {
   const int L = P.L, S = P.S;
 
   // post-dominator sets on the 1-in-1-out DAG (the output post-dominates all)
@@ -180,7 +178,7 @@ void select_dprs(Graph& g, int layout_mask, int dtype_mask) {
     }
 
   std::vector<Table> T(L);
-  g.dp_stats.assign(L, DPLayerStats{});
+  if (stats) stats->assign(L, DPLayerStats{});
   int64_t conflicts = 0;
   for (int i = 0; i < L; ++i) {
     const auto& H = P.preds[i];
@@ -200,8 +198,10 @@ void select_dprs(Graph& g, int layout_mask, int dtype_mask) {
       for (int c : T[H[k]].C)
         pos[k].push_back((int)(std::find(ti.C.begin(), ti.C.end(), c) - ti.C.begin()));
     const int64_t nH = ipow(S, (int)H.size());
-    g.dp_stats[i].states = S * nCt;
-    g.dp_stats[i].candidates = nH;
+    if (stats) {
+      (*stats)[i].states = S * nCt;
+      (*stats)[i].candidates = nH;
+    }
     std::vector<int> lc(nc), lh(H.size());
     for (int64_t ci = 0; ci < nCt; ++ci) {
       for (int k = 0, v = (int)ci; k < nc; ++k, v /= S) lc[k] = v % S;
@@ -301,8 +301,55 @@ void select_dprs(Graph& g, int layout_mask, int dtype_mask) {
   for (const State& s : last.st)
     if (s.t < kInf && (!best || better(s, *best))) best = &s;
   if (!best) fail(SN_E_UNSUPPORTED, "no routine path of finite time");
-  g.path.assign(best->U.begin(), best->U.begin() + g.n_layers());
-  g.path_cost = best->t;
+  return *best;
+}
+
+}  // namespace
+
+void select_dprs(Graph& g, int layout_mask, int dtype_mask) {
+  if (!g.have_costs) fail(SN_E_STATE, "no cost table: call sn_profile or sn_set_costs first");
+  const Problem P = make_problem(g, layout_mask, dtype_mask);
+  const State best = dprs_solve(P, &g.dp_stats);
+  g.path.assign(best.U.begin(), best.U.begin() + g.n_layers());
+  g.path_cost = best.t;
+}
+
+// The childnet as a net of its own: sub-layer 0 takes the role of the
+// input layer, the sub-layers form a chain, an auxiliary output closes it,
+// and the one schema makes every adapt void.
+int64_t childnet_select(ChildNet& c) {
+  const int m = (int)c.layer.size();
+  Problem P;
+  P.L = m + 1;
+  P.S = 1;
+  P.index_of_schema.assign(kNumSchemas, -1);
+  P.cost.resize(P.L);
+  P.schema.resize(P.L);
+  P.preds.resize(P.L);
+  P.succs.resize(P.L);
+  for (int i = 0; i < m; ++i) {
+    bool any = false;
+    for (int64_t v : c.cost[i]) {
+      P.cost[i].push_back(v < 0 ? kInf : v);
+      P.schema[i].push_back(0);
+      any = any || v >= 0;
+    }
+    if (!any) return -1;
+  }
+  P.cost[m] = {0};
+  P.schema[m] = {0};
+  for (int i = 0; i < m; ++i) {
+    Problem::E e;
+    e.a = i;
+    e.b = i + 1;
+    e.A = {0};
+    P.edges.push_back(e);
+    P.preds[i + 1] = {i};
+    P.succs[i] = {i + 1};
+  }
+  const State best = dprs_solve(P, nullptr);
+  c.path.assign(best.U.begin(), best.U.begin() + m);
+  return best.t;
 }
 
 int64_t path_total(const Graph& g, const std::vector<int>& path) {

@@ -441,3 +441,53 @@ def test_workspace_limit_restricts_the_routine_set():
     g.add_conv(0, w, b, 1, 1)
     assert status_of(g.set_option, N.OPT_WS_LIMIT, 1 << 20) == -3   # after layers were added
     g.close()
+
+
+def test_childnet_routine_time_is_the_optimum_over_its_sub_layers():
+    # The three-kernel Winograd routine is a childnet (Sec. III-D): wgenc ->
+    # wgconv (one sub-routine per GEMM tile) -> wgdec.  Its time in the cost
+    # table is the DPRS optimum over its sub-routines' times (the algorithm
+    # applied to the childnet before the net), which must equal the
+    # enumeration of every sub-routine choice; the net's DP then uses it.
+    from oracle.select import childnet_time
+    w = np.zeros((64, 64, 3, 3), np.uint16)
+    b = np.zeros(64, np.float32)
+    g = Graph("bf16", 2, 64, 14, 14, device=-1)
+    c1 = g.add_conv(0, w, b, 1, 1)
+    g.add_conv(c1, w, b, 1, 1)
+    costs = g.costs()
+    kids = [r for l in costs["layers"] for r in l["routines"] if "child" in r]
+    assert kids and all(r["algo"] == 2 and r["param"] == 0 for r in kids)
+    assert all(r["child"]["layers"] == ["wgenc", "wgconv", "wgdec"] and len(r["child"]["routines"][1]) >= 2
+               for r in kids)
+    rng = np.random.default_rng(5)
+    for trial in range(6):
+        costs = randomise(g.costs(), trial, max_cost=40)
+        for l in costs["layers"]:
+            for r in l["routines"]:
+                if "child" in r:
+                    r["child"]["ns"] = [[int(rng.integers(-1 if trial % 2 else 0, 30)) for _ in row]
+                                        for row in r["child"]["ns"]]
+        g.set_costs(costs)
+        got = g.costs()
+        for l, lg in zip(costs["layers"], got["layers"]):
+            for r, rg in zip(l["routines"], lg["routines"]):
+                if "child" not in r:
+                    assert rg["ns"] == r["ns"]
+                    continue
+                t, choice = childnet_time(r["child"]["ns"])
+                assert rg["ns"] == (-1 if t is None else t)
+                if t is not None:
+                    assert tuple(rg["child"]["path"]) == choice
+        assert dp_vs(g, got) == exhaustive(problem_from_costs(got))[1::-1]
+    # a childnet never profiled (every sub-routine time unknown) keeps the
+    # routine's own listed time
+    costs = randomise(g.costs(), 9, max_cost=40)
+    for l in costs["layers"]:
+        for r in l["routines"]:
+            if "child" in r:
+                r["child"]["ns"] = [[-1 for _ in row] for row in r["child"]["ns"]]
+                r["ns"] = 17
+    g.set_costs(costs)
+    assert all(r["ns"] == 17 for l in g.costs()["layers"] for r in l["routines"] if "child" in r)
+    g.close()

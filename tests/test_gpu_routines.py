@@ -415,3 +415,40 @@ def test_projected_shortcut_every_routine(dtype, ci):
         print(f"{dtype} projected case{ci} {rt['name']}: err {e:.2e}", flush=True)
         assert e <= TOL[dtype], (rt["name"], e)
     g.close()
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_winograd_childnet_sub_routines(dtype):
+    # the three-kernel Winograd routine is a childnet (Sec. III-D): profiling
+    # times each of its sub-routines (wgenc, every wgconv GEMM tile, wgdec)
+    # on its own, the routine's time is the optimum over them, and each GEMM
+    # tile, selected through the cost table, computes the layer (ragged K)
+    from oracle.select import childnet_time
+    n, c, h, w, k = 2, 64, 13, 14, 72
+    layer = {"type": "conv", "in": [0], "k": k, "r": 3, "s": 3, "stride": 1, "pad": 1, "groups": 1,
+             "act": "relu"}
+    x = random_tensor((n, c, h, w), dtype, seed=301)
+    wt = random_tensor((k, c, 3, 3), dtype, seed=302, dist="normal", scale=np.sqrt(2 / (c * 9)))
+    b = random_tensor((k,), "f32", seed=303, scale=0.1)
+    ref = oracle_layer(layer, x, wt, b, dtype)
+    g = single_layer_graph(dtype, (n, c, h, w), layer, wt, b)
+    g.profile(warmup=1, reps=3)
+    kids = [r for r in g.costs()["layers"][1]["routines"] if "child" in r]
+    assert kids and all(r["algo"] == 2 and r["param"] == 0 for r in kids)
+    xd = to_dev(x, dtype)
+    for r in kids:
+        rows = r["child"]["ns"]
+        assert all(v > 0 for row in rows for v in row), rows
+        t, choice = childnet_time(rows)
+        assert r["ns"] == t and tuple(r["child"]["path"]) == choice
+        for q in range(len(rows[1])):
+            costs = g.costs()
+            mine = costs["layers"][1]["routines"][r["rid"]]
+            mine["child"]["ns"][1] = [1 if j == q else 10 ** 6 for j in range(len(rows[1]))]
+            g.set_costs(costs)
+            assert g.costs()["layers"][1]["routines"][r["rid"]]["child"]["path"][1] == q
+            out = from_dev(run_routine(g, r["rid"], xd), dtype)
+            e = err(out, ref, dtype)
+            print(f"{dtype} {r['name']} wgconv:p{q}: err {e:.2e}", flush=True)
+            assert e <= TOL[dtype], (r["name"], q, e)
+    g.close()

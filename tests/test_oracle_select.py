@@ -131,3 +131,15 @@ def test_path_time_counts_each_edge_once():
          "edges": [(0, 1, A), (0, 2, A), (1, 3, A), (2, 3, A)]}
     # two edges 0->{1,2} adapt 0->1 (7 each), two edges {1,2}->3 adapt 1->0 (5 each)
     assert path_time(p, (0, 0, 0, 0)) == 2 + 3 + 7 + 7 + 5 + 5
+
+
+def test_childnet_time_hand_worked():
+    # a chain of sub-layers with one format between them: the time of a
+    # choice is the sum of its sub-routines' times, the minimum over choices
+    # (ties to the lowest index tuple), unavailable when a sub-layer has none
+    from oracle.select import childnet_time
+    assert childnet_time([[3], [5, 2, 7], [4]]) == (9, (0, 1, 0))
+    assert childnet_time([[3, 1], [5, None, 2], [4]]) == (7, (1, 2, 0))
+    assert childnet_time([[1], [2, 2], [0]]) == (3, (0, 0, 0))          # tie: lowest tuple
+    assert childnet_time([[1], [-1, None], [0]]) == (None, None)        # wgconv unavailable
+    assert childnet_time([[0]]) == (0, (0,))
