@@ -26,6 +26,7 @@ static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 struct DevLayer {
   void* w[3] = {};      // per dtype: dense [Kp][R][S][C8] | depthwise [R][S][C8] | fc [Kp][C8]
   void* wu[3] = {};     // per dtype: Winograd U [16][Kp][C8]
+  void* wu4[3] = {};    // per dtype: Winograd F(4x4,3x3) U [36][Kp][C8]
   void* wp[3] = {};     // per dtype: projected-shortcut weights [Kp][C2_8]
   void* wcat[3] = {};   // per dtype: 1x1 layer with a projected shortcut, both weights [Kp][C + C2]
   float* bias = nullptr;  // [Kp] (with a projected shortcut: the two biases summed)
@@ -163,6 +164,8 @@ void dev_destroy(Graph& g) {
       if (p) (void)hipFree(p);
     for (void* p : d.wu)
       if (p) (void)hipFree(p);
+    for (void* p : d.wu4)
+      if (p) (void)hipFree(p);
     for (void* p : d.wp)
       if (p) (void)hipFree(p);
     for (void* p : d.wcat)
@@ -268,6 +271,30 @@ void dev_upload_layer(Graph& g, int id) {
             }
         }
       dl.wu[dt] = dev_upload(u.data(), u.size());
+      // F(4x4,3x3): G of the Toom-Cook construction on 0, 1, -1, 2, -2, infinity
+      static const double G4[6][3] = {{1.0 / 4, 0, 0},
+                                      {-1.0 / 6, -1.0 / 6, -1.0 / 6},
+                                      {-1.0 / 6, 1.0 / 6, -1.0 / 6},
+                                      {1.0 / 24, 1.0 / 12, 1.0 / 6},
+                                      {1.0 / 24, -1.0 / 12, 1.0 / 6},
+                                      {0, 0, 1}};
+      std::vector<uint8_t> u4((size_t)36 * Kp * C8 * es, 0);
+      for (int kk = 0; kk < K; ++kk)
+        for (int c = 0; c < C; ++c) {
+          double gg[3][3], t[6][3];
+          for (int r = 0; r < 3; ++r)
+            for (int s2 = 0; s2 < 3; ++s2)
+              gg[r][s2] = decode(src + ((((size_t)kk * C + c) * 3 + r) * 3 + s2) * ies, g.dtype);
+          for (int i = 0; i < 6; ++i)
+            for (int s2 = 0; s2 < 3; ++s2)
+              t[i][s2] = G4[i][0] * gg[0][s2] + G4[i][1] * gg[1][s2] + G4[i][2] * gg[2][s2];
+          for (int i = 0; i < 6; ++i)
+            for (int j = 0; j < 6; ++j) {
+              double v = t[i][0] * G4[j][0] + t[i][1] * G4[j][1] + t[i][2] * G4[j][2];
+              encode(v, dt, &u4[(((size_t)(i * 6 + j) * Kp + kk) * C8 + c) * es]);
+            }
+        }
+      dl.wu4[dt] = dev_upload(u4.data(), u4.size());
     }
   }
 }
@@ -285,8 +312,11 @@ size_t routine_ws_bytes(const Graph& g, const Layer& L, const Routine& r) {
     return k::igemm_ws_bytes(r.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), L.d.r, L.d.s,
                              g.layers[L.inputs[1]].out.c);
   }
-  if (r.algo == SN_ALGO_WINOGRAD)  // the fused routines keep their transforms on chip
-    return r.param == 0 ? k::winograd_ws_bytes(r.dtype, tdesc(in, r.layout), L.out.c) : 0;
+  if (r.algo == SN_ALGO_WINOGRAD) {  // the fused routines keep their transforms on chip
+    if (r.param == 0) return k::winograd_ws_bytes(r.dtype, tdesc(in, r.layout), L.out.c, 2);
+    if (r.param == k::winograd_f4_param()) return k::winograd_ws_bytes(r.dtype, tdesc(in, r.layout), L.out.c, 4);
+    return 0;
+  }
   if (r.algo == SN_ALGO_IGEMM)
     return k::igemm_ws_bytes(r.dtype, r.param, tdesc(in, r.layout), tdesc(L.out, r.layout), L.d.r, L.d.s);
   return 0;
@@ -305,7 +335,7 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
       k::ConvArgs a{};
       a.x = in[0];
       a.xd = ind[0];
-      a.w = r.algo == SN_ALGO_WINOGRAD ? dl.wu[dt] : dl.w[dt];
+      a.w = r.algo != SN_ALGO_WINOGRAD ? dl.w[dt] : r.param == k::winograd_f4_param() ? dl.wu4[dt] : dl.wu[dt];
       a.bias = dl.bias;
       a.y = out;
       a.yd = outd;
@@ -356,12 +386,13 @@ static void launch_layer(const Graph& g, int id, const Routine& r, const void* c
         k::conv_direct(dt, a, st);
       } else if (r.algo == SN_ALGO_IGEMM) {
         k::conv_igemm(dt, r.param, a, st);
-      } else if (r.param == 0) {  // the childnet wgenc -> wgconv -> wgdec
+      } else if (r.param == 0 || r.param == k::winograd_f4_param()) {  // childnet wgenc -> wgconv -> wgdec
+        const int tile = r.param == 0 ? 2 : 4;
         if (sub >= 0) {
-          k::winograd_sub(dt, sub, sub_routine, a, st);
+          k::winograd_sub(dt, tile, sub, sub_routine, a, st);
         } else {
           const ChildNet& cn = L.child[r.id];
-          k::conv_winograd(dt, a, cn.path.size() > 1 ? cn.path[1] : 0, st);
+          k::conv_winograd(dt, tile, a, cn.path.size() > 1 ? cn.path[1] : 0, st);
         }
       } else {
         k::conv_wino_fused(dt, r.param - 1, a, st);

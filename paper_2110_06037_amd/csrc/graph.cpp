@@ -121,7 +121,8 @@ std::string routine_name(const Graph& g, const Layer& L, const Routine& r) {
   if (g.multi_dtype()) o << kDtypeName[r.dtype] << ":";
   o << kLayoutName[r.layout] << "/" << kAlgoName[r.algo];
   if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_IGEMM) o << ":p" << r.param;
-  if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_WINOGRAD && r.param > 0) o << ":fused:p" << r.param - 1;
+  if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_WINOGRAD && r.param == k::winograd_f4_param()) o << ":f4x4";
+  else if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_WINOGRAD && r.param > 0) o << ":fused:p" << r.param - 1;
   if (L.type == SN_LAYER_CONV2D && r.algo == SN_ALGO_DIRECT && r.param > 0) o << ":strip" << k::dw_strip_len(r.param);
   if (L.type == SN_LAYER_FC && r.algo == SN_ALGO_IGEMM) o << ":1x1conv:p" << r.param;
   return o.str();
@@ -191,6 +192,9 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
             add(lay, SN_ALGO_WINOGRAD, 0);  // transforms and tile GEMMs as three kernels
             if (g.opt_params && k::wino_fused_applicable(dt, lay, in.c))
               for (int p = 0; p < k::wino_fused_num_configs(); ++p) add(lay, SN_ALGO_WINOGRAD, p + 1);
+            // F(4x4,3x3) in fp32 and fp16: its transforms (coefficients up to
+            // 8 and 1/24) amplify bf16's rounding of V and U past the tolerance
+            if (g.opt_params && dt != SN_BF16) add(lay, SN_ALGO_WINOGRAD, k::winograd_f4_param());
           }
           break;
         case SN_LAYER_FC:
@@ -223,7 +227,9 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
 
 ChildNet make_childnet(const Graph& g, const Layer& L, const Routine& r) {
   ChildNet c;
-  if (L.type != SN_LAYER_CONV2D || r.algo != SN_ALGO_WINOGRAD || r.param != 0) return c;
+  if (L.type != SN_LAYER_CONV2D || r.algo != SN_ALGO_WINOGRAD ||
+      (r.param != 0 && r.param != k::winograd_f4_param()))
+    return c;
   // one GEMM tile only when routine parameters are restricted
   const int ng = g.opt_params ? k::winograd_gemm_num_configs(r.dtype) : 1;
   c.layer = {"wgenc", "wgconv", "wgdec"};

@@ -10,6 +10,7 @@
 // zero-filled), so the reduction index runs over (r, s, 8-channel chunk,
 // lane-in-chunk) for every layout.
 #include "igemm.hpp"
+#include "wino.hpp"
 
 namespace sn {
 namespace k {
@@ -358,14 +359,233 @@ __global__ __launch_bounds__(256) void wino_out_kernel(WinoArgs a) {
     }
 }
 
+// ------------------------------------------------------------------ Winograd F(4x4, 3x3)
+// The same three steps with 4x4 output tiles: a 6x6 input patch per tile
+// (stride 4), V = B^T d B with 36 positions, 36 batched GEMMs, Y = A^T M A.
+// The matrices are those of the Toom-Cook construction of F(4, 3) on the
+// points 0, 1, -1, 2, -2 and infinity, nested with themselves.  A thread
+// transforms one tile for 4 channels (the 6x6x4 patch in registers).
+template <typename T>
+__device__ __forceinline__ void ld4f(const T* p, float* v) {
+  if constexpr (sizeof(T) == 2) {
+    const u32x2 w = *reinterpret_cast<const u32x2*>(p);
+    T e[4];
+    __builtin_memcpy(e, &w, 8);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = to_f(e[i]);
+  } else {
+    const f32x4 w = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = w[i];
+  }
+}
+template <typename T>
+__device__ __forceinline__ void st4f(T* p, const float* v) {
+  if constexpr (sizeof(T) == 2) {
+    T e[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) e[i] = from_f<T>(v[i]);
+    u32x2 w;
+    __builtin_memcpy(&w, e, 8);
+    *reinterpret_cast<u32x2*>(p) = w;
+  } else {
+    *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+  }
+}
+// B^T applied to six values (rows of the patch, then columns of the result)
+__device__ __forceinline__ void bt6(const float* x, float* r) {
+  r[0] = 4.f * x[0] - 5.f * x[2] + x[4];
+  r[1] = -4.f * x[1] - 4.f * x[2] + x[3] + x[4];
+  r[2] = 4.f * x[1] - 4.f * x[2] - x[3] + x[4];
+  r[3] = -2.f * x[1] - x[2] + 2.f * x[3] + x[4];
+  r[4] = 2.f * x[1] - x[2] - 2.f * x[3] + x[4];
+  r[5] = 4.f * x[1] - 5.f * x[3] + x[5];
+}
+// A^T applied to six values
+__device__ __forceinline__ void at6(const float* m, float* o) {
+  o[0] = m[0] + m[1] + m[2] + m[3] + m[4];
+  o[1] = m[1] - m[2] + 2.f * (m[3] - m[4]);
+  o[2] = m[1] + m[2] + 4.f * (m[3] + m[4]);
+  o[3] = m[1] - m[2] + 8.f * (m[3] - m[4]) + m[5];
+}
+
+template <typename T, int L>
+__global__ __launch_bounds__(256) void wino4_in_kernel(WinoArgs a) {
+  const int CQ = a.C8 >> 2;  // channel quads
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  int t, cq;
+  if constexpr (L == NCHW) {
+    t = (int)(idx % a.T);
+    cq = (int)(idx / a.T);
+  } else {
+    cq = (int)(idx % CQ);
+    t = (int)(idx / CQ);
+  }
+  if (t >= a.T || cq >= CQ) return;
+  const int per = a.TH * a.TW;
+  const int n = t / per, tt = t - n * per;
+  const int ty = tt / a.TW, tx = tt - ty * a.TW;
+  const int h0 = ty * 4 - 1, w0 = tx * 4 - 1;
+  const T* __restrict__ x = reinterpret_cast<const T*>(a.x);
+  // whole 4-channel vectors: NC8HW8 (padded channels are stored), or NHWC
+  // quads inside the real channels with aligned pixel rows
+  const bool vec = L == NC8 || (L == NHWC && a.Cs % 4 == 0 && cq * 4 + 4 <= a.C);
+  float d[6][6][4];
+#pragma unroll
+  for (int i = 0; i < 6; ++i)
+#pragma unroll
+    for (int j = 0; j < 6; ++j) {
+      const int h = h0 + i, w = w0 + j;
+      const bool ok = (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) d[i][j][e] = 0.f;
+      if (!ok) continue;
+      if (vec) {
+        if constexpr (L == NC8)
+          ld4f(x + ((((long long)n * (a.C8 >> 3) + (cq >> 1)) * a.H + h) * a.W + w) * 8 + (cq & 1) * 4, d[i][j]);
+        else
+          ld4f(x + (((long long)n * a.H + h) * a.W + w) * a.Cs + cq * 4, d[i][j]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int c = cq * 4 + e;
+          if (c >= a.C) continue;
+          if constexpr (L == NCHW)
+            d[i][j][e] = to_f(x[(((long long)n * a.Cs + c) * a.H + h) * a.W + w]);
+          else
+            d[i][j][e] = to_f(x[(((long long)n * a.H + h) * a.W + w) * a.Cs + c]);
+        }
+      }
+    }
+  // columns: B^T d, in place
+#pragma unroll
+  for (int j = 0; j < 6; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float col[6], r[6];
+#pragma unroll
+      for (int i = 0; i < 6; ++i) col[i] = d[i][j][e];
+      bt6(col, r);
+#pragma unroll
+      for (int i = 0; i < 6; ++i) d[i][j][e] = r[i];
+    }
+  // rows: (B^T d) B, stored as position xi = 6 i + j
+  T* __restrict__ vout = reinterpret_cast<T*>(a.v);
+  const long long plane = (long long)a.T * a.C8;
+  T* base = vout + (long long)t * a.C8 + cq * 4;
+#pragma unroll
+  for (int i = 0; i < 6; ++i) {
+    float r[6][4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float row[6], o[6];
+#pragma unroll
+      for (int j = 0; j < 6; ++j) row[j] = d[i][j][e];
+      bt6(row, o);
+#pragma unroll
+      for (int j = 0; j < 6; ++j) r[j][e] = o[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 6; ++j) st4f(base + (i * 6 + j) * plane, r[j]);
+  }
+}
+
+template <typename T, int L>
+__global__ __launch_bounds__(256) void wino4_out_kernel(WinoArgs a) {
+  const int NQ = (a.Ng + 3) / 4;
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  int t, kq;
+  if constexpr (L == NCHW) {
+    t = (int)(idx % a.T);
+    kq = (int)(idx / a.T);
+  } else {
+    kq = (int)(idx % NQ);
+    t = (int)(idx / NQ);
+  }
+  if (t >= a.T || kq >= NQ) return;
+  const int per = a.TH * a.TW;
+  const int n = t / per, tt = t - n * per;
+  const int ty = tt / a.TW, tx = tt - ty * a.TW;
+  const long long plane = (long long)a.T * a.Ng;
+  const float* __restrict__ mp = a.m + (long long)t * a.Ng + kq * 4;
+  const bool full = kq * 4 + 4 <= a.Ng && a.Ng % 4 == 0;
+  // rows of M: A^T M, four output rows of six
+  float tmp[4][6][4];
+#pragma unroll
+  for (int j = 0; j < 6; ++j) {
+    float col[6][4];
+#pragma unroll
+    for (int i = 0; i < 6; ++i) {
+      const float* q = mp + (i * 6 + j) * plane;
+      if (full) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(q);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) col[i][e] = v[e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) col[i][e] = kq * 4 + e < a.Ng ? q[e] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float m6[6], o4[4];
+#pragma unroll
+      for (int i = 0; i < 6; ++i) m6[i] = col[i][e];
+      at6(m6, o4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) tmp[i][j][e] = o4[i];
+    }
+  }
+  float bias[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) bias[e] = kq * 4 + e < a.Ng ? a.bias[kq * 4 + e] : 0.f;
+  T* __restrict__ y = reinterpret_cast<T*>(a.y);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float out[4][4];  // [column][channel]
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float m6[6], o4[4];
+#pragma unroll
+      for (int j = 0; j < 6; ++j) m6[j] = tmp[i][j][e];
+      at6(m6, o4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) out[j][e] = act_f(o4[j] + bias[e], a.act);
+    }
+    const int p = ty * 4 + i;
+    if (p >= a.H) continue;  // output size equals input size
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int q = tx * 4 + j;
+      if (q >= a.W) continue;
+      if constexpr (L == NC8) {
+        st4f(y + ((((long long)n * (a.Ks >> 3) + (kq >> 1)) * a.H + p) * a.W + q) * 8 + (kq & 1) * 4, out[j]);
+      } else if constexpr (L == NHWC) {
+        if (full && a.Ks % 4 == 0) {
+          st4f(y + (((long long)n * a.H + p) * a.W + q) * a.Ks + kq * 4, out[j]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (kq * 4 + e < a.Ng) y[(((long long)n * a.H + p) * a.W + q) * a.Ks + kq * 4 + e] = from_f<T>(out[j][e]);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (kq * 4 + e < a.Ng) y[(((long long)n * a.Ks + kq * 4 + e) * a.H + p) * a.W + q] = from_f<T>(out[j][e]);
+      }
+    }
+  }
+}
+
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
-size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k) {
-  const long long T = (long long)xd.n * ((xd.h + 1) / 2) * ((xd.w + 1) / 2);
+size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k, int tile) {
+  const long long T = (long long)xd.n * ((xd.h + tile - 1) / tile) * ((xd.w + tile - 1) / tile);
   const long long C8 = (xd.c + 7) / 8 * 8;
   const long long Kp = (k + 7) / 8 * 8;
+  const long long np = (long long)(tile + 2) * (tile + 2);  // positions
   const size_t es = dtype == 0 ? 4 : 2;
-  return align256(16 * T * C8 * es) + align256(16 * T * Kp * 4);
+  return align256(np * T * C8 * es) + align256(np * T * Kp * 4);
 }
 
 // The routine is a childnet of three sub-layers, each launched on its own:
@@ -381,8 +601,9 @@ int winograd_gemm_num_configs(int dtype) {
 }
 
 template <typename T>
-static WinoArgs wino_args(int dtype, const ConvArgs& c) {
-  check(c.r == 3 && c.s == 3 && c.stride == 1 && c.pad == 1, "Winograd F(2x2,3x3) needs 3x3/1 pad 1");
+static WinoArgs wino_args(int dtype, int tile, const ConvArgs& c) {
+  check(tile == 2 || tile == 4, "Winograd output tile 2x2 or 4x4");
+  check(c.r == 3 && c.s == 3 && c.stride == 1 && c.pad == 1, "Winograd F(mxm,3x3) needs 3x3/1 pad 1");
   check(c.xd.layout == c.yd.layout, "Winograd reads and writes one layout");
   check(!c.res, "Winograd routine takes no residual");
   WinoArgs a{};
@@ -395,24 +616,34 @@ static WinoArgs wino_args(int dtype, const ConvArgs& c) {
   a.W = c.xd.w;
   a.Cs = c.xd.cs;
   a.C8 = (a.C + 7) / 8 * 8;
-  a.TH = (a.H + 1) / 2;
-  a.TW = (a.W + 1) / 2;
+  a.TH = (a.H + tile - 1) / tile;
+  a.TW = (a.W + tile - 1) / tile;
   a.T = a.N * a.TH * a.TW;
   a.Ng = c.yd.layout == NC8 ? c.yd.cs : c.yd.c;
   a.Ks = c.yd.cs;
   a.act = c.act;
   const int Kp = (c.yd.c + 7) / 8 * 8;
-  const size_t vbytes = align256(16ull * a.T * a.C8 * sizeof(T));
-  check(c.ws && c.ws_bytes >= winograd_ws_bytes(dtype, c.xd, c.yd.c), "Winograd workspace too small");
-  check(16ll * a.T * std::max(a.C8, Kp) < (1ll << 31), "tensor too large");
+  const long long np = (long long)(tile + 2) * (tile + 2);
+  const size_t vbytes = align256((size_t)np * a.T * a.C8 * sizeof(T));
+  check(c.ws && c.ws_bytes >= winograd_ws_bytes(dtype, c.xd, c.yd.c, tile), "Winograd workspace too small");
+  check(np * a.T * std::max(a.C8, Kp) < (1ll << 31), "tensor too large");
   a.v = c.ws;
   a.m = reinterpret_cast<float*>(reinterpret_cast<char*>(c.ws) + vbytes);
   return a;
 }
 
 template <typename T>
-static void wino_enc_t(int dtype, const ConvArgs& c, hipStream_t st) {
-  const WinoArgs a = wino_args<T>(dtype, c);
+static void wino_enc_t(int dtype, int tile, const ConvArgs& c, hipStream_t st) {
+  const WinoArgs a = wino_args<T>(dtype, tile, c);
+  if (tile == 4) {
+    dim3 g((unsigned)(((long long)a.T * (a.C8 / 4) + 255) / 256));
+    switch (c.xd.layout) {
+      case NCHW: SN_LAUNCH((wino4_in_kernel<T, NCHW>), g, dim3(256), 0, st, a); break;
+      case NHWC: SN_LAUNCH((wino4_in_kernel<T, NHWC>), g, dim3(256), 0, st, a); break;
+      case NC8: SN_LAUNCH((wino4_in_kernel<T, NC8>), g, dim3(256), 0, st, a); break;
+    }
+    return;
+  }
   dim3 g((unsigned)(((long long)a.T * (a.C8 / 8) + 255) / 256));
   switch (c.xd.layout) {
     case NCHW: SN_LAUNCH((wino_in_kernel<T, NCHW>), g, dim3(256), 0, st, a); break;
@@ -422,8 +653,8 @@ static void wino_enc_t(int dtype, const ConvArgs& c, hipStream_t st) {
 }
 
 template <typename T>
-static void wino_gemm_t(int dtype, const ConvArgs& c, int cfg, hipStream_t st) {
-  const WinoArgs a = wino_args<T>(dtype, c);
+static void wino_gemm_t(int dtype, int tile, const ConvArgs& c, int cfg, hipStream_t st) {
+  const WinoArgs a = wino_args<T>(dtype, tile, c);
   check(cfg >= 0 && cfg < winograd_gemm_num_configs(dtype), "unknown Winograd GEMM tile");
   const int Kp = (c.yd.c + 7) / 8 * 8;
   // batched GEMM: A = V_xi as a [T][C8] matrix (1x1 "NHWC" convolution), B = U_xi [Kp][C8]
@@ -458,12 +689,21 @@ static void wino_gemm_t(int dtype, const ConvArgs& c, int cfg, hipStream_t st) {
   g.w_elems = (long long)Kp * a.C8;
   const IgCfg gc = std::is_same<T, float>::value ? kWinoGemm32[cfg] : kWinoGemm16[cfg];
   ig_decompose(g, gc);
-  igemm_cfg<T, NHWC, true, EPI_RAW>(gc, g, 16, st);
+  igemm_cfg<T, NHWC, true, EPI_RAW>(gc, g, (tile + 2) * (tile + 2), st);
 }
 
 template <typename T>
-static void wino_dec_t(int dtype, const ConvArgs& c, hipStream_t st) {
-  const WinoArgs a = wino_args<T>(dtype, c);
+static void wino_dec_t(int dtype, int tile, const ConvArgs& c, hipStream_t st) {
+  const WinoArgs a = wino_args<T>(dtype, tile, c);
+  if (tile == 4) {
+    dim3 g((unsigned)(((long long)a.T * ((a.Ng + 3) / 4) + 255) / 256));
+    switch (c.xd.layout) {
+      case NCHW: SN_LAUNCH((wino4_out_kernel<T, NCHW>), g, dim3(256), 0, st, a); break;
+      case NHWC: SN_LAUNCH((wino4_out_kernel<T, NHWC>), g, dim3(256), 0, st, a); break;
+      case NC8: SN_LAUNCH((wino4_out_kernel<T, NC8>), g, dim3(256), 0, st, a); break;
+    }
+    return;
+  }
   dim3 g((unsigned)(((long long)a.T * ((a.Ng + 7) / 8) + 255) / 256));
   switch (c.xd.layout) {
     case NCHW: SN_LAUNCH((wino_out_kernel<T, NCHW>), g, dim3(256), 0, st, a); break;
@@ -472,21 +712,23 @@ static void wino_dec_t(int dtype, const ConvArgs& c, hipStream_t st) {
   }
 }
 
-void winograd_sub(int dtype, int sub, int cfg, const ConvArgs& c, hipStream_t st) {
+void winograd_sub(int dtype, int tile, int sub, int cfg, const ConvArgs& c, hipStream_t st) {
   check(sub >= 0 && sub <= 2, "Winograd sub-layer is 0 (wgenc), 1 (wgconv) or 2 (wgdec)");
-#define WSUB(T_)                                    \
-  if (sub == 0) wino_enc_t<T_>(dtype, c, st);       \
-  else if (sub == 1) wino_gemm_t<T_>(dtype, c, cfg, st); \
-  else wino_dec_t<T_>(dtype, c, st);
+#define WSUB(T_)                                            \
+  if (sub == 0) wino_enc_t<T_>(dtype, tile, c, st);         \
+  else if (sub == 1) wino_gemm_t<T_>(dtype, tile, c, cfg, st); \
+  else wino_dec_t<T_>(dtype, tile, c, st);
   if (dtype == 0) { WSUB(float) }
   else if (dtype == 1) { WSUB(f16) }
   else { WSUB(bf16) }
 #undef WSUB
 }
 
-void conv_winograd(int dtype, const ConvArgs& c, int gemm_cfg, hipStream_t st) {
-  for (int sub = 0; sub < 3; ++sub) winograd_sub(dtype, sub, gemm_cfg, c, st);
+void conv_winograd(int dtype, int tile, const ConvArgs& c, int gemm_cfg, hipStream_t st) {
+  for (int sub = 0; sub < 3; ++sub) winograd_sub(dtype, tile, sub, gemm_cfg, c, st);
 }
+
+int winograd_f4_param() { return 1 + wino_fused_num_configs(); }
 
 // ------------------------------------------------------------------ depthwise
 // Per-channel R x S convolution; weights [R][S][C8].  Channel-vector layouts

@@ -158,13 +158,16 @@ bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r,
 bool stream1x1_takes_projection(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
                                 int k, int c2, int cc);
 void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& a, hipStream_t st);
-size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k);
-// Winograd F(2x2,3x3) as three sub-layers (a childnet): sub 0 = input
-// transform, 1 = the batched GEMMs with tile `cfg` (one of
-// winograd_gemm_num_configs), 2 = output transform; V and M in the workspace
+// Winograd F(m x m, 3x3), m = tile 2 or 4, as three sub-layers (a
+// childnet): sub 0 = input transform, 1 = the (m+2)^2 batched GEMMs with
+// GEMM tile `cfg` (one of winograd_gemm_num_configs), 2 = output transform;
+// V and M in the workspace (winograd_ws_bytes)
+size_t winograd_ws_bytes(int dtype, const TDesc& xd, int k, int tile = 2);
 int winograd_gemm_num_configs(int dtype);
-void winograd_sub(int dtype, int sub, int cfg, const ConvArgs& a, hipStream_t st);
-void conv_winograd(int dtype, const ConvArgs& a, int gemm_cfg, hipStream_t st);
+void winograd_sub(int dtype, int tile, int sub, int cfg, const ConvArgs& a, hipStream_t st);
+void conv_winograd(int dtype, int tile, const ConvArgs& a, int gemm_cfg, hipStream_t st);
+// routine parameter of the F(4x4,3x3) routine (after the fused F(2x2,3x3) ones)
+int winograd_f4_param();
 // param 0: the strip kernel (16-bit NHWC with C % 8 == 0 or NC8HW8, 3x3,
 // stride 1 or 2) with its strip length chosen by the thread count, else the
 // general kernel; param p >= 1: the strip kernel with strips of

@@ -97,6 +97,8 @@ def test_conv_bit_exact_small_integers(dtype, c, k):
     g = single_layer_graph(dtype, (n, c, h, w), layer, wt, b)
     xd = to_dev(x, dtype)
     for rt in g.routines(1):
+        if "f4x4" in rt["name"]:
+            continue  # F(4x4,3x3)'s filter transform (1/6, 1/24) is inexact in binary floating point
         out = from_dev(run_routine(g, rt["id"], xd), dtype)
         assert np.array_equal(out, ref), rt["name"]
 
@@ -419,8 +421,9 @@ def test_projected_shortcut_every_routine(dtype, ci):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_winograd_childnet_sub_routines(dtype):
-    # the three-kernel Winograd routine is a childnet (Sec. III-D): profiling
-    # times each of its sub-routines (wgenc, every wgconv GEMM tile, wgdec)
+    # the three-kernel Winograd routines (F(2x2,3x3) and F(4x4,3x3)) are
+    # childnets (Sec. III-D): profiling times each of their sub-routines
+    # (wgenc, every wgconv GEMM tile, wgdec)
     # on its own, the routine's time is the optimum over them, and each GEMM
     # tile, selected through the cost table, computes the layer (ragged K)
     from oracle.select import childnet_time
@@ -434,7 +437,7 @@ def test_winograd_childnet_sub_routines(dtype):
     g = single_layer_graph(dtype, (n, c, h, w), layer, wt, b)
     g.profile(warmup=1, reps=3)
     kids = [r for r in g.costs()["layers"][1]["routines"] if "child" in r]
-    assert kids and all(r["algo"] == 2 and r["param"] == 0 for r in kids)
+    assert kids and all(r["algo"] == 2 and "fused" not in r["name"] for r in kids)
     xd = to_dev(x, dtype)
     for r in kids:
         rows = r["child"]["ns"]
