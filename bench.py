@@ -297,7 +297,12 @@ def sweep(args):
         for r in costs["layers"][1]["routines"]:
             if r["ns"] is None or r["ns"] < 0:
                 continue
-            f = 2 * 16 * c * c * tiles if "winograd" in r["name"] else flops
+            if "f4x4" in r["name"]:   # F(4x4,3x3): 36 tile GEMMs over 4x4-pixel tiles
+                f = 2 * 36 * c * c * args.batch * ((hw + 3) // 4) ** 2
+            elif "winograd" in r["name"]:
+                f = 2 * 16 * c * c * tiles
+            else:
+                f = flops
             tfl = f / (r["ns"] * 1e-9) / 1e12
             rows.append({"routine": r["name"], "us": round(r["ns"] / 1e3, 2),
                          "tflops": round(tfl, 1),
