@@ -192,9 +192,10 @@ std::vector<Routine> enumerate_routines(const Graph& g, const Layer& L) {
             add(lay, SN_ALGO_WINOGRAD, 0);  // transforms and tile GEMMs as three kernels
             if (g.opt_params && k::wino_fused_applicable(dt, lay, in.c))
               for (int p = 0; p < k::wino_fused_num_configs(); ++p) add(lay, SN_ALGO_WINOGRAD, p + 1);
-            // F(4x4,3x3) in fp32 and fp16: its transforms (coefficients up to
-            // 8 and 1/24) amplify bf16's rounding of V and U past the tolerance
-            if (g.opt_params && dt != SN_BF16) add(lay, SN_ALGO_WINOGRAD, k::winograd_f4_param());
+            // F(4x4,3x3) in fp32 only: its input transform scales values by up
+            // to 100 (coefficients up to 5 in each direction), past fp16's range
+            // on deep layers, and bf16's 8-bit mantissa loses the tolerance
+            if (g.opt_params && dt == SN_F32) add(lay, SN_ALGO_WINOGRAD, k::winograd_f4_param());
           }
           break;
         case SN_LAYER_FC:
