@@ -73,8 +73,8 @@ using IC = std::integral_constant<int, V>;
 // WM x WN waves (group g runs taps [9g/TG, 9(g+1)/TG) of every step on the
 // whole tile; the groups' sums meet in LDS at the end); ST LDS stages;
 // PROWS patch rows per stage.
-template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD>
-__global__ __launch_bounds__(512, 1) void conv3x3_patch_kernel(PatchArgs a) {
+template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD, int OCC = 1>
+__global__ __launch_bounds__(512, OCC) void conv3x3_patch_kernel(PatchArgs a) {
   static_assert(sizeof(T) == 2 && L != NCHW, "16-bit channel-vector layouts only");
   constexpr int NWV = 8;
   static_assert(WM * WN * TG == NWV, "8 waves");
@@ -93,7 +93,7 @@ __global__ __launch_bounds__(512, 1) void conv3x3_patch_kernel(PatchArgs a) {
   constexpr int RPITCH = BN * 4 + 16;                // partial-sum row pitch (bytes)
   constexpr int RED = TG > 1 ? FMT * 16 * RPITCH : 0;
   constexpr int SM = ST * STAGE > RED ? ST * STAGE : RED;
-  static_assert(SM <= 160 * 1024, "LDS capacity");
+  static_assert(SM * OCC <= 160 * 1024, "LDS capacity at the occupancy");
   __shared__ __attribute__((aligned(1024))) char smem[SM];
   lds_char* const sl = (lds_char*)smem;
   auto swz = [](int row) { return (row >> 1) & 3; };
@@ -417,7 +417,7 @@ bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride,
   return patch_tiling(a, fmt, pwt, prows, sd);
 }
 
-template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD>
+template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD, int OCC = 1>
 static void patch_go(PatchArgs a, hipStream_t st) {
   check(patch_tiling(a, FMT, PWT, PROWS, SD), "output too wide for the patch tile");
   check(a.CB % 4 == 0, "patch kernel needs C % 32 == 0");
@@ -425,31 +425,38 @@ static void patch_go(PatchArgs a, hipStream_t st) {
         "tensor too large for 32-bit buffer offsets");
   a.tiles_n = (a.Ng + BN - 1) / BN;
   dim3 grid(a.tiles_m * a.tiles_n);
-  SN_LAUNCH((conv3x3_patch_kernel<T, L, FMT, BN, PWT, WM, WN, TG, ST, PROWS, SD>), grid, dim3(512), 0, st, a);
+  SN_LAUNCH((conv3x3_patch_kernel<T, L, FMT, BN, PWT, WM, WN, TG, ST, PROWS, SD, OCC>), grid, dim3(512), 0, st, a);
 }
 
-static long long patch_key(int fmt, int bn, int pwt, int wm, int wn, int tg, int stg, int prows, int sd) {
-  return (((((((fmt * 1000LL + bn) * 100 + pwt) * 10 + wm) * 10 + wn) * 10 + tg) * 10 + stg) * 10000 + prows) * 10 +
-         sd;
+static long long patch_key(int fmt, int bn, int pwt, int wm, int wn, int tg, int stg, int prows, int sd, int occ) {
+  return ((((((((fmt * 1000LL + bn) * 100 + pwt) * 10 + wm) * 10 + wn) * 10 + tg) * 10 + stg) * 10000 + prows) * 10 +
+          sd) * 10 + occ;
 }
 
 template <typename T, int L>
 static void patch_layout(const PatchCfg& c, const PatchArgs& a, hipStream_t st) {
-  const long long key = patch_key(c.fmt, c.bn, c.pwt, c.wm, c.wn, c.tg, c.st, c.prows, c.sd);
+  const long long key = patch_key(c.fmt, c.bn, c.pwt, c.wm, c.wn, c.tg, c.st, c.prows, c.sd, c.occ);
 #define PGO(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                               \
-  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1)) {               \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 1)) {            \
     patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1>(a, st);              \
     return;                                                                            \
   }
 #define PGO2(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                              \
-  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 2)) {               \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 2, 1)) {            \
     patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 2>(a, st);              \
+    return;                                                                            \
+  }
+#define PGOO2(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                             \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 2)) {            \
+    patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 2>(a, st);           \
     return;                                                                            \
   }
   PATCH_CONFIGS(PGO)
   PATCH2_CONFIGS(PGO2)
+  PATCH_OCC2_CONFIGS(PGOO2)
 #undef PGO
 #undef PGO2
+#undef PGOO2
   check(false, "patch tile not instantiated");
 }
 

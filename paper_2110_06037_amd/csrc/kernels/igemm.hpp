@@ -1089,6 +1089,11 @@ static const IgCfg kIg16[] = {
     {64, 64, 128, 0, 0, 1, 2, 3},  {64, 64, 128, 0, 0, 1, 2, 4},
     {64, 128, 128, 0, 0, 1, 2, 3, 0, {}, 8}, {128, 64, 128, 0, 0, 1, 4, 3, 0, {}, 8},
     {128, 128, 128, 0, 0, 1, 4, 2, 0, {}, 8},
+    // 3x3 stride-1 patch kernel, two workgroups per CU
+#define SN_PATCHO2_IG(FMT, BN, PWT, WM, WN, TG, ST, PROWS) \
+  {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS, 1, 2}},
+    PATCH_OCC2_CONFIGS(SN_PATCHO2_IG)
+#undef SN_PATCHO2_IG
 };
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 

@@ -97,6 +97,7 @@ size_t igemm_ws_bytes(int dtype, int param, const TDesc& xd, const TDesc& yd, in
 struct PatchCfg {
   int fmt, bn, pwt, wm, wn, tg, st, prows;  // one PATCH_CONFIGS tuple
   int sd = 1;                               // convolution stride
+  int occ = 1;                              // workgroups per CU the tile is sized for
 };
 // Instantiated patch tiles (FMT, BN, PWT, WM, WN, TG, ST, PROWS): FMT row
 // blocks of 16 output pixels, BN output channels, patch row pitch PWT, 8
@@ -121,6 +122,11 @@ struct PatchCfg {
   X(7, 64, 16, 4, 1, 2, 2, 480)  \
   X(4, 64, 16, 4, 1, 2, 2, 240)  \
   X(7, 32, 16, 4, 1, 2, 3, 480)
+// Stride-1 patch tiles for two workgroups per CU (at most 80 KB of LDS and
+// 128 registers each), so that one workgroup's prologue and stores overlap
+// the other's steps (7 x 7 and 14 x 14 at 32 output channels per tile)
+#define PATCH_OCC2_CONFIGS(X)    \
+  X(7, 32, 16, 4, 1, 2, 2, 288)
 bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
                       int fmt, int pwt, int prows, int sd);
 void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& a, hipStream_t st);
