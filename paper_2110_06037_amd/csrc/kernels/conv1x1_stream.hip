@@ -1,5 +1,5 @@
 // 1x1 convolution (stride 1 or 2, no padding) of an NHWC input with CC =
-// 64, 128 or 256 channels (16-bit types), an implicit-GEMM routine for the pointwise layers
+// 64, 128, 256 or 512 channels (16-bit types), an implicit-GEMM routine for the pointwise layers
 // of a bottleneck whose reduction is short.
 //
 // Such a layer reads each pixel once and writes K channels (plus a residual
@@ -61,9 +61,13 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   constexpr int WTM = BM / WM, WTN = BN / WN, FM = WTM / 16, FN = WTN / 16;
   constexpr int NA = NSL * BM * RB / 1024 / NWV;   // pixel-tile load instructions per wave
   constexpr int NBL = NSL * BN * RB / 1024 / NWV;  // filter load instructions per wave
-  constexpr int NE = BM * BN / 8 / NT;             // 16-byte output chunks per thread and tile
+  constexpr int NEC = BM * BN / 8;                 // 16-byte output chunks per tile
+  // chunks per thread and tile; with fewer chunks than threads the rest
+  // issue their stores (and residual loads) at out-of-range offsets, so every
+  // wave counts the same memory instructions
+  constexpr int NE = (NEC + NT - 1) / NT;
   static_assert(NA >= 1 && NBL >= 1 && NE >= 1 && NA * 1024 * NWV == NSL * BM * RB &&
-                    NBL * 1024 * NWV == NSL * BN * RB && NE * 8 * NT == BM * BN && FM >= 1 && FN >= 1,
+                    NBL * 1024 * NWV == NSL * BN * RB && (NEC % NT == 0 || NE == 1) && FM >= 1 && FN >= 1,
                 "tile shape");
   constexpr int YR = RES ? NE : 0;             // residual loads per thread and tile
   static_assert(PD * (NA + YR + NE) <= 63, "outstanding-load counter range");
@@ -146,9 +150,10 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
     const int m0r = mtile * BM;
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-      const int q = tid + e * NT, row = q / (BN / 8), cj = q % (BN / 8);
+      const int q = tid + e * NT, qc = q < NEC ? q : 0, row = qc / (BN / 8), cj = qc % (BN / 8);
       const int m = m0r + row, n = n0 + cj * 8;
-      const unsigned off = mtile < a.tiles_m && m < a.M && n < a.K ? (unsigned)(m * a.Ks + n) * 2u : kOOB;
+      const unsigned off =
+          q < NEC && mtile < a.tiles_m && m < a.M && n < a.K ? (unsigned)(m * a.Ks + n) * 2u : kOOB;
       r[e] = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
     }
   };
@@ -238,9 +243,9 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
     const int m0 = mt * BM;
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-      const int q = tid + e * NT, row = q / (BN / 8), cj = q % (BN / 8);
+      const int q = tid + e * NT, qc = q < NEC ? q : 0, row = qc / (BN / 8), cj = qc % (BN / 8);
       const int m = m0 + row, n = n0 + cj * 8;
-      const unsigned off = m < a.M && n < a.K ? (unsigned)(m * a.Ks + n) * 2u : kOOB;
+      const unsigned off = q < NEC && m < a.M && n < a.K ? (unsigned)(m * a.Ks + n) * 2u : kOOB;
       const f32x4 c0 = *reinterpret_cast<const f32x4*>(Cs + row * CP + cj * 8);
       const f32x4 c1 = *reinterpret_cast<const f32x4*>(Cs + row * CP + cj * 8 + 4);
       float s[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
@@ -361,6 +366,7 @@ void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& c
     return;                                                                      \
   }
   STREAM_CONFIGS(SG)
+  STREAM512_CONFIGS(SG)
 #undef SG
   check(false, "streaming 1x1 tile not instantiated");
 }

@@ -1094,6 +1094,10 @@ static const IgCfg kIg16[] = {
   {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS, 1, 2}},
     PATCH_OCC2_CONFIGS(SN_PATCHO2_IG)
 #undef SN_PATCHO2_IG
+    // streaming 1x1 kernel for 512-channel inputs
+#define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM},
+    STREAM512_CONFIGS(SN_STREAM_IG)
+#undef SN_STREAM_IG
 };
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 

@@ -138,7 +138,7 @@ bool smallc_applicable(int layout, int c, int h, int w, int r, int s, int stride
 // the register budget are sized for
 void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st, int wm = 2, int occ = 3);
 // 1x1 convolution (stride 1 or 2, no padding) of an NHWC input with cc =
-// 64, 128 or 256 channels by persistent workgroups streaming pixel tiles
+// 64, 128, 256 or 512 channels by persistent workgroups streaming pixel tiles
 // (see conv1x1_stream.hip).  Instantiated tiles (CC, BM, BN, WM, PD): BM
 // pixels x BN channels per tile, WM wave rows, loads PD tiles ahead; each is
 // one implicit-GEMM routine parameter.
@@ -157,6 +157,9 @@ void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st
   X(256, 64, 64, 4, 2)    \
   X(256, 32, 128, 2, 2)   \
   X(256, 32, 128, 2, 3)
+// 512-channel inputs (routine parameters after the others)
+#define STREAM512_CONFIGS(X) \
+  X(512, 32, 64, 2, 1)
 bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
                           int k, int cc);
 // the streaming kernel with a projected shortcut of c2 channels (slabs of

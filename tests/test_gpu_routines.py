@@ -31,6 +31,8 @@ CONV_CASES = [
     (2, 64, 14, 14, 96, 3, 1, 1, "relu"),     # 14 x 14: two row tiles per image, ragged channel tile
     (3, 32, 28, 28, 40, 3, 1, 1, "relu6"),    # 28 x 28: four row tiles per image, K = 40
     (3, 1024, 7, 9, 200, 1, 1, 0, "relu"),    # long reduction (128-channel steps), ragged M and N
+    (4, 512, 15, 17, 200, 1, 1, 0, "relu6"),  # C = 512: streaming kernel, ragged pixel and channel tiles
+    (2, 512, 29, 27, 64, 1, 2, 0, "relu"),    # C = 512 at stride 2
     (2, 3, 45, 38, 64, 7, 2, 3, "relu"),      # stem: C = 3, 7x7/2, odd output sizes
     (1, 2, 21, 24, 72, 5, 2, 2, "relu6"),     # C = 2, 5x5/2, K = 72 (two channel tiles)
     (2, 3, 40, 36, 64, 3, 1, 1, "relu"),      # C = 3, 3x3/1: a VGG-style first layer, several rows per tile
@@ -244,6 +246,7 @@ RESIDUAL_CASES = [
     (1, 256, 14, 14, 1, "relu"),    # split-reduction parameters apply
     (4, 64, 72, 64, 1, "relu"),     # C = 64: streaming kernel, several tiles per workgroup
     (8, 128, 50, 50, 1, "relu"),    # C = 128: streaming kernel with two 64-channel slabs
+    (4, 512, 28, 28, 1, "relu"),    # C = 512: streaming kernel, half the threads store each tile
 ]
 
 
