@@ -380,6 +380,7 @@ PROJECTED_CASES = [
     (3, 64, 9, 11, 72, 3, 1, 1, 128, 17, 21, 2, "relu6"),       # a 3x3 main convolution, ragged tiles
     (1, 40, 5, 5, 24, 1, 1, 0, 12, 9, 9, 2, "none"),            # channels off the tile depth: two launches only
     (3, 64, 13, 15, 72, 1, 1, 0, 64, 25, 29, 2, "relu"),        # streaming 1x1 tiles: ragged pixels and channels
+    (4, 128, 28, 28, 512, 1, 1, 0, 256, 56, 56, 2, "relu"),     # ResNet-50 stage 2 entry: 384-channel streaming tiles
 ]
 
 
