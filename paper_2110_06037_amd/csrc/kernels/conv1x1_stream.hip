@@ -1,5 +1,5 @@
 // 1x1 convolution (stride 1 or 2, no padding) of an NHWC input with CC =
-// 64, 128, 256 or 512 channels (16-bit types), an implicit-GEMM routine for the pointwise layers
+// 64, 128, 256, 384 or 512 channels (16-bit types), an implicit-GEMM routine for the pointwise layers
 // of a bottleneck whose reduction is short.
 //
 // Such a layer reads each pixel once and writes K channels (plus a residual
@@ -73,13 +73,20 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   static_assert(PD * (NA + YR + NE) <= 63, "outstanding-load counter range");
   constexpr int A_BYTES = NSL * BM * RB, B_BYTES = NSL * BN * RB;
   constexpr int CP = BN + 4;                   // fp32 staging row pitch (floats)
-  constexpr int SM = B_BYTES + NB * A_BYTES + BM * CP * 4 + BN * 4;
+  constexpr int CS_BYTES = BM * CP * 4;
+  // when a staging buffer of its own does not fit, a tile's sums are staged
+  // in the tile's own pixel buffer once every wave has read it (ALIAS); the
+  // loads of a later tile into a buffer then wait for the barrier after
+  // which no wave reads that buffer's staging any more
+  constexpr bool ALIAS = B_BYTES + NB * A_BYTES + CS_BYTES + BN * 4 > 160 * 1024;
+  static_assert(!ALIAS || A_BYTES >= CS_BYTES, "staging fits the pixel buffer");
+  constexpr int SM = B_BYTES + NB * A_BYTES + (ALIAS ? 0 : CS_BYTES) + BN * 4;
   static_assert(SM <= 160 * 1024, "LDS capacity");
   __shared__ __attribute__((aligned(1024))) char smem[SM];
   char* const Bs = smem;
   char* const As = smem + B_BYTES;
-  float* const Cs = reinterpret_cast<float*>(As + NB * A_BYTES);
-  float* const Bias = Cs + BM * CP;
+  float* const Cs0 = reinterpret_cast<float*>(As + NB * A_BYTES);  // the staging buffer (without ALIAS)
+  float* const Bias = reinterpret_cast<float*>(As + NB * A_BYTES + (ALIAS ? 0 : CS_BYTES));
   auto swz = [](int row) { return (row >> 1) & 7; };
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -210,10 +217,20 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
     constexpr int U = decltype(UC)::value;
     constexpr int NX = (U + PD) % NB;
     const int mt = mt0 + t * G;
-    issue_tile(mt + PD * G, SIC<NX>{});
-    if (t < PD) wait_vmcnt<PD * (YR + NA) + (U < PD ? U : PD) * NE>();
-    else wait_vmcnt<PD * (YR + NA + NE)>();
-    dma_barrier();  // every wave's share landed; every wave is done with the last tile's Cs
+    float* const Cs = ALIAS ? reinterpret_cast<float*>(As + U * A_BYTES) : Cs0;
+    if constexpr (!ALIAS) {
+      issue_tile(mt + PD * G, SIC<NX>{});
+      if (t < PD) wait_vmcnt<PD * (YR + NA) + (U < PD ? U : PD) * NE>();
+      else wait_vmcnt<PD * (YR + NA + NE)>();
+      dma_barrier();  // every wave's share landed; every wave is done with the last tile's Cs
+    } else {
+      // younger than this tile's loads: the PD - 1 later tiles' loads and
+      // the stores of the last min(t, PD) tiles
+      if (t < PD) wait_vmcnt<(PD - 1) * (YR + NA) + (U < PD ? U : PD) * NE>();
+      else wait_vmcnt<(PD - 1) * (YR + NA) + PD * NE>();
+      dma_barrier();  // every wave's share landed; no wave reads the last tile's staging
+      issue_tile(mt + PD * G, SIC<NX>{});
+    }
 
     f32x4 acc[FM][FN];
 #pragma unroll
@@ -231,6 +248,7 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fbr[ks][j], fa[i], acc[i][j]);
     }
+    if constexpr (ALIAS) lds_barrier();  // every wave has read the tile's pixels
     // sums (bias included) to LDS: element (i, j, v) is pixel
     // wm*WTM + i*16 + (lane&15), channel wn*WTN + j*16 + (lane>>4)*4 + v
 #pragma unroll

@@ -157,9 +157,12 @@ void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st
   X(256, 64, 64, 4, 2)    \
   X(256, 32, 128, 2, 2)   \
   X(256, 32, 128, 2, 3)
-// 512-channel inputs (routine parameters after the others)
+// 512-channel inputs, and 384 = 128 + 256 (a 128-channel 1x1 convolution
+// with a 256-channel projected shortcut) with the sums staged in the pixel
+// buffer; routine parameters after the others
 #define STREAM512_CONFIGS(X) \
-  X(512, 32, 64, 2, 1)
+  X(512, 32, 64, 2, 1)       \
+  X(384, 32, 128, 2, 1)
 bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
                           int k, int cc);
 // the streaming kernel with a projected shortcut of c2 channels (slabs of

@@ -247,6 +247,7 @@ RESIDUAL_CASES = [
     (4, 64, 72, 64, 1, "relu"),     # C = 64: streaming kernel, several tiles per workgroup
     (8, 128, 50, 50, 1, "relu"),    # C = 128: streaming kernel with two 64-channel slabs
     (4, 512, 28, 28, 1, "relu"),    # C = 512: streaming kernel, half the threads store each tile
+    (8, 384, 28, 28, 1, "relu"),    # C = 384: streaming kernel staging its sums in the pixel buffer
 ]
 
 
@@ -381,6 +382,7 @@ PROJECTED_CASES = [
     (1, 40, 5, 5, 24, 1, 1, 0, 12, 9, 9, 2, "none"),            # channels off the tile depth: two launches only
     (3, 64, 13, 15, 72, 1, 1, 0, 64, 25, 29, 2, "relu"),        # streaming 1x1 tiles: ragged pixels and channels
     (4, 128, 28, 28, 512, 1, 1, 0, 256, 56, 56, 2, "relu"),     # ResNet-50 stage 2 entry: 384-channel streaming tiles
+    (16, 128, 28, 28, 512, 1, 1, 0, 256, 56, 56, 2, "relu"),    # the same with several tiles per streaming workgroup
 ]
 
 
