@@ -404,6 +404,12 @@ def main():
     ap.add_argument("--no-proj", action="store_true",
                     help="keep projection shortcuts as their own 1x1 convolutions (default: fold each, "
                          "with its residual add, into the convolution the add follows)")
+    ap.add_argument("--refine-reps", type=int, default=15,
+                    help="in-path refinement after integrated profiling: timed runs per trial "
+                         "(0 = off; near-tied routines of each layer timed inside the whole path)")
+    ap.add_argument("--refine-tol", type=int, default=150,
+                    help="in-path refinement: alternatives within this many per mille of the "
+                         "selected routine's unit-profiled time")
     ap.add_argument("--integrated-reps", type=int, default=20,
                     help="runs per candidate in integrated profiling (0 = keep the DPRS path)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -500,6 +506,9 @@ def main():
     if args.tune_only:
         if args.integrated_reps > 0:
             g.profile_integrated(warmup=2, reps=args.integrated_reps)
+        if args.refine_reps > 0 and not args.rotate_layouts:
+            n_ref = g.refine_in_path(tol_permille=args.refine_tol, reps=args.refine_reps)
+            log(f"[bench] in-path refinement: {n_ref} layer(s) changed")
         if args.path_out:
             with open(args.path_out, "w") as f:
                 json.dump({"path": g.path()[0], "routines": [g.routines(i)[r]["name"] for i, r in
@@ -556,6 +565,23 @@ def main():
                                  round(c["measured_ns"] / 1e6, 4) for c in cands}}
         log(f"[bench] integrated profiling: {len(cands)} candidates in {t_int:.1f} s, "
             f"selected {label}: {sec * 1e3:.3f} ms/step")
+    # in-path refinement: near-tied routines of each layer's schema timed
+    # inside the whole path; the library keeps the refined path only if it
+    # also wins end to end
+    refine = None
+    t_ref = 0.0
+    if args.refine_reps > 0 and not pinned:
+        before = g.path()[0]
+        t3 = time.perf_counter()
+        n_ref = g.refine_in_path(tol_permille=args.refine_tol, reps=args.refine_reps)
+        t_ref = time.perf_counter() - t3
+        after = g.path()[0]
+        refine = {"layers_changed": n_ref, "seconds": round(t_ref, 2), "tol_permille": args.refine_tol,
+                  "changes": {str(i): [g.routines(i)[before[i]]["name"], g.routines(i)[after[i]]["name"]]
+                              for i in range(len(after)) if after[i] != before[i]}}
+        if n_ref:
+            sec = time_steps(g, x, out, args.steps, args.warmup)
+        log(f"[bench] in-path refinement: {n_ref} layer(s) changed in {t_ref:.1f} s: {sec * 1e3:.3f} ms/step")
     if pinned:
         sec = time_steps(g, x, out, args.steps, args.warmup)
         log(f"[bench] pinned path: {sec * 1e3:.3f} ms/step")
@@ -704,6 +730,8 @@ def main():
         g1.select("dprs")
         if args.integrated_reps > 0:
             g1.profile_integrated(warmup=2, reps=max(args.integrated_reps, 20))
+        if args.refine_reps > 0:
+            g1.refine_in_path(tol_permille=args.refine_tol, reps=args.refine_reps)
         x1 = to_dev(t1_["x"], args.dtype)
         o1 = g1.empty_output()
         # eager launches and the same plan replayed as a HIP graph; the
@@ -733,7 +761,8 @@ def main():
                                   else ", residual adds folded into the 1x1 convolutions that produce them"),
                    "batch": args.batch,
                    "path": ("DPRS candidates + fixed paths, integrated profiling keeps the fastest"
-                            if integ else "DPRS-selected routines")},
+                            if integ else "DPRS-selected routines")
+                           + (", in-path refinement" if refine else "")},
         "roofline": roof,
         "cpu_baseline": cpu,
         "step_ms": steps_dist,
@@ -746,8 +775,9 @@ def main():
                                    if comparison else sel_vs_fixed),
         "comparison": comparison, "single_pass_dp_vs_best_fixed": dp_vs_fixed,
         "best_fixed": best_fixed, "fixed_img_s": fixed, "fixed_model_time_ms": fixed_model, "integrated": integ,
+        "in_path_refinement": refine,
         "model_time_ms": round(model_ns / 1e6, 4), "dprs_model_time_ms": round(dp_model_ns / 1e6, 4),
-        "tuning_s": round(t_prof + t_sel + t_int, 2),
+        "tuning_s": round(t_prof + t_sel + t_int + t_ref, 2),
         "unit_profiling": ("loaded" if args.costs_in else
                            f"cold/{args.profile_flush_mib}MiB/median" if args.profile_flush_mib else "warm/mean"),
     }

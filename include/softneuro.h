@@ -385,6 +385,32 @@ int sn_profile_integrated(sn_graph* g, int32_t warmup, int32_t reps, void* hip_s
 int sn_integrated_candidate(const sn_graph* g, int32_t idx, int32_t* routine_ids, int32_t n,
                             int64_t* model_ns, int64_t* measured_ns, int32_t* kind_ab);
 
+/* In-path refinement of the selected path: integrated profiling (Sec.
+ * III-C) applied one layer at a time.  A routine's unit-profiled time is
+ * taken with its input and weights hot in the caches; inside the net its
+ * input was just written by the layer before and its weights were last read
+ * a whole run earlier, and near-tied routines can rank differently there.
+ * For each layer, in order, the selected routine and the other routines of
+ * its schema whose unit-profiled time is at most (1 + tol_permille / 1000)
+ * times the selected one's (the max_alts fastest of them) are each run
+ * inside the whole path with only that layer's routine swapped (adapts are
+ * unchanged: the schema is the same), on a zero-filled scratch input; the
+ * layer's time is read from HIP events tied to its first and last launch,
+ * the median over reps runs after two warm-up runs.  A routine that beats
+ * the selected one by more than 2 % replaces it for the later layers'
+ * trials.  Finally the selected and the refined path are timed end to end
+ * (four alternating rounds of 20 runs, block means, the median of each) and
+ * the faster is kept; its plan is compiled, as after sn_select_path.
+ * *n_changed (may be NULL) receives the number of layers whose routine
+ * changed (0 when the refined path lost or nothing changed).  Synchronous.
+ * Errors: SN_E_STATE (no costs, no selected path), SN_E_INVALID
+ * (tol_permille outside 0..1000, max_alts outside 1..16, reps outside
+ * 1..1000), SN_E_DEVICE (host-only graph, HIP error); after an error
+ * during timing the previous path is selected again but has no plan (select
+ * or set the path again before running). */
+int sn_refine_in_path(sn_graph* g, int32_t tol_permille, int32_t max_alts, int32_t reps, void* hip_stream,
+                      int32_t* n_changed);
+
 /* Cost table as JSON (the profiling data of Sec. IV-A: T(r) per routine,
  * adapt times per edge and schema pair), all times int64 ns, -1 = no
  * routine / unavailable:

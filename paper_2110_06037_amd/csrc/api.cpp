@@ -340,6 +340,21 @@ int sn_profile_integrated(sn_graph* gp, int32_t warmup, int32_t reps, void* stre
   });
 }
 
+int sn_refine_in_path(sn_graph* gp, int32_t tol_permille, int32_t max_alts, int32_t reps, void* stream,
+                      int32_t* n_changed) {
+  return guarded([&] {
+    CHECK_G(gp);
+    Graph& g = gp->g;
+    if (tol_permille < 0 || tol_permille > 1000 || max_alts < 1 || max_alts > 16 || reps < 1 || reps > 1000)
+      fail(SN_E_INVALID, "tol_permille in 0..1000, max_alts in 1..16 and reps in 1..1000 required");
+    if (!g.have_costs) fail(SN_E_STATE, "no costs: profile or load a cost table first");
+    if (g.path.empty()) fail(SN_E_STATE, "no selected path");
+    if (g.host_only()) fail(SN_E_DEVICE, "host-only graph cannot run paths");
+    const int c = refine_in_path(g, tol_permille, max_alts, reps, stream);
+    if (n_changed) *n_changed = c;
+  });
+}
+
 int sn_integrated_candidate(const sn_graph* gp, int32_t idx, int32_t* routine_ids, int32_t n,
                             int64_t* model_ns, int64_t* measured_ns, int32_t* kind_ab) {
   return guarded([&] {

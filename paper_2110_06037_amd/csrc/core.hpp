@@ -248,5 +248,8 @@ void plan_layer_output(const Graph& g, int layer, void* d_dst, size_t cap, size_
 // times every candidate end to end and selects the fastest (compiles its plan)
 void integrated_measure(Graph& g, std::vector<Candidate>& cands, int warmup, int reps,
                         void* stream);
+// in-path refinement of g.path (sn_refine_in_path); returns the number of
+// layers whose routine changed
+int refine_in_path(Graph& g, int tol_permille, int max_alts, int reps, void* stream);
 
 }  // namespace sn

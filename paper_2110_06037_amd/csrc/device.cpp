@@ -963,34 +963,62 @@ void plan_layer_output(const Graph& g, int layer, void* d_dst, size_t cap, size_
 // reverse order, so slow drift does not favour one end of the list) of reps
 // back-to-back runs between HIP events; a candidate's time is the smaller of
 // its two block means.  The fastest candidate (earliest on ties) is selected.
+// Zero-filled scratch tensors for the net inputs and outputs, and a pair of
+// HIP events, for timing whole paths; freed when it goes out of scope.
+struct ScratchIO {
+  std::vector<void*> din, dout;
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  ScratchIO(const Graph& g, hipStream_t st) {
+    const int es = dtype_size(g.dtype);
+    const std::vector<int> outs = net_outputs(g);
+    din.assign(g.net_inputs.size(), nullptr);
+    dout.assign(outs.size(), nullptr);
+    try {
+      for (size_t q = 0; q < din.size(); ++q) {
+        const size_t b = (size_t)g.layers[g.net_inputs[q]].out.numel() * es;
+        HIPCHK(hipMalloc(&din[q], std::max<size_t>(b, 256)));
+        HIPCHK(hipMemsetAsync(din[q], 0, b, st));
+      }
+      for (size_t q = 0; q < dout.size(); ++q)
+        HIPCHK(hipMalloc(&dout[q], std::max<size_t>((size_t)g.layers[outs[q]].out.numel() * es, 256)));
+      for (auto& e : ev) HIPCHK(hipEventCreate(&e));
+    } catch (...) {
+      release();
+      throw;
+    }
+  }
+  ~ScratchIO() { release(); }
+  ScratchIO(const ScratchIO&) = delete;
+  ScratchIO& operator=(const ScratchIO&) = delete;
+  void release() {
+    for (auto& e : ev)
+      if (e) (void)hipEventDestroy(e), e = nullptr;
+    for (void*& p : din)
+      if (p) (void)hipFree(p), p = nullptr;
+    for (void*& p : dout)
+      if (p) (void)hipFree(p), p = nullptr;
+  }
+  // mean ns per run of the compiled plan over reps back-to-back runs
+  int64_t block_ns(Graph& g, hipStream_t st, int reps) {
+    HIPCHK(hipEventRecord(ev[0], st));
+    for (int r = 0; r < reps; ++r) plan_run(g, din.data(), dout.data(), st);
+    HIPCHK(hipEventRecord(ev[1], st));
+    HIPCHK(hipEventSynchronize(ev[1]));
+    float ms = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms, ev[0], ev[1]));
+    return std::max<int64_t>(1, (int64_t)((double)ms * 1e6 / reps + 0.5));
+  }
+};
+
 void integrated_measure(Graph& g, std::vector<Candidate>& cands, int warmup, int reps,
                         void* stream) {
   if (cands.empty()) fail(SN_E_INTERNAL, "no candidate paths");
   HIPCHK(hipSetDevice(g.device));
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int es = dtype_size(g.dtype);
-  const std::vector<int> outs = net_outputs(g);
-  std::vector<void*> din(g.net_inputs.size(), nullptr), dout(outs.size(), nullptr);
-  hipEvent_t ev[2] = {nullptr, nullptr};
   const std::vector<int> saved = g.path;
   const int64_t saved_cost = g.path_cost;
-  auto cleanup = [&] {
-    for (auto& e : ev)
-      if (e) (void)hipEventDestroy(e);
-    for (void* p : din)
-      if (p) (void)hipFree(p);
-    for (void* p : dout)
-      if (p) (void)hipFree(p);
-  };
   try {
-    for (size_t q = 0; q < din.size(); ++q) {
-      const size_t b = (size_t)g.layers[g.net_inputs[q]].out.numel() * es;
-      HIPCHK(hipMalloc(&din[q], std::max<size_t>(b, 256)));
-      HIPCHK(hipMemsetAsync(din[q], 0, b, st));
-    }
-    for (size_t q = 0; q < dout.size(); ++q)
-      HIPCHK(hipMalloc(&dout[q], std::max<size_t>((size_t)g.layers[outs[q]].out.numel() * es, 256)));
-    for (auto& e : ev) HIPCHK(hipEventCreate(&e));
+    ScratchIO io(g, st);
     for (Candidate& c : cands) c.measured_ns = -1;
     const int nc = (int)cands.size();
     for (int round = 0; round < 2; ++round) {
@@ -999,14 +1027,8 @@ void integrated_measure(Graph& g, std::vector<Candidate>& cands, int warmup, int
         g.path = c.path;
         g.path_cost = c.model_ns;
         plan_compile(g);
-        for (int w = 0; w < warmup; ++w) plan_run(g, din.data(), dout.data(), st);
-        HIPCHK(hipEventRecord(ev[0], st));
-        for (int r = 0; r < reps; ++r) plan_run(g, din.data(), dout.data(), st);
-        HIPCHK(hipEventRecord(ev[1], st));
-        HIPCHK(hipEventSynchronize(ev[1]));
-        float ms = 0.f;
-        HIPCHK(hipEventElapsedTime(&ms, ev[0], ev[1]));
-        const int64_t ns = std::max<int64_t>(1, (int64_t)((double)ms * 1e6 / reps + 0.5));
+        for (int w = 0; w < warmup; ++w) plan_run(g, io.din.data(), io.dout.data(), st);
+        const int64_t ns = io.block_ns(g, st, reps);
         if (c.measured_ns < 0 || ns < c.measured_ns) c.measured_ns = ns;
       }
     }
@@ -1017,13 +1039,95 @@ void integrated_measure(Graph& g, std::vector<Candidate>& cands, int warmup, int
     g.path_cost = cands[best].model_ns;
     plan_compile(g);
   } catch (...) {
-    cleanup();
     g.path = saved;
     g.path_cost = saved_cost;
     plan_destroy(g);
     throw;
   }
-  cleanup();
+}
+
+// ------------------------------------------------------------------ in-path refinement
+// Layer by layer, the selected routine and its near-tied alternatives of the
+// same schema are timed inside the whole path (only that layer swapped; the
+// layer's time from the events tied to its first and last launch, median of
+// reps timed runs); a clear winner (more than 2 % faster) is kept for the
+// later layers' trials.  The refined path then has to beat the selected one
+// end to end (alternating rounds) to be kept.
+int refine_in_path(Graph& g, int tol_permille, int max_alts, int reps, void* stream) {
+  if (!g.have_costs) fail(SN_E_STATE, "no costs: profile or load a cost table first");
+  if (g.path.empty()) fail(SN_E_STATE, "no selected path");
+  HIPCHK(hipSetDevice(g.device));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const std::vector<int> saved = g.path;
+  const int64_t saved_cost = g.path_cost;
+  const int nl = g.n_layers();
+  int changed = 0;
+  try {
+    ScratchIO io(g, st);
+    std::vector<float> ms(nl);
+    std::vector<float> v(reps);
+    auto layer_time = [&](const std::vector<int>& path, int layer) {
+      g.path = path;
+      plan_compile(g);
+      for (int w = 0; w < 2; ++w) plan_run(g, io.din.data(), io.dout.data(), st, ms.data(), 1);
+      for (int r = 0; r < reps; ++r) {
+        plan_run(g, io.din.data(), io.dout.data(), st, ms.data(), 1);
+        v[r] = ms[layer];
+      }
+      std::nth_element(v.begin(), v.begin() + reps / 2, v.end());
+      return v[reps / 2];
+    };
+    std::vector<int> cur = saved;
+    for (int i = 1; i < nl; ++i) {
+      const Layer& L = g.layers[i];
+      const int r0 = cur[i];
+      const int64_t c0 = L.cost[r0];
+      if (c0 <= 0) continue;
+      std::vector<int> alts;
+      for (int r = 0; r < (int)L.routines.size(); ++r)
+        if (r != r0 && L.routines[r].schema() == L.routines[r0].schema() && L.cost[r] > 0 &&
+            (double)L.cost[r] <= (double)c0 * (1.0 + tol_permille / 1000.0))
+          alts.push_back(r);
+      if (alts.empty()) continue;
+      std::stable_sort(alts.begin(), alts.end(), [&](int a, int b) { return L.cost[a] < L.cost[b]; });
+      if ((int)alts.size() > max_alts) alts.resize(max_alts);
+      const float t0 = layer_time(cur, i);
+      float best_t = t0;
+      int best = r0;
+      for (int r : alts) {
+        std::vector<int> p = cur;
+        p[i] = r;
+        const float t = layer_time(p, i);
+        if (t < best_t) best_t = t, best = r;
+      }
+      if (best != r0 && best_t < 0.98f * t0) cur[i] = best;
+    }
+    for (int i = 0; i < nl; ++i) changed += cur[i] != saved[i];
+    if (changed) {
+      // the refined path has to win end to end: four alternating rounds
+      std::vector<int64_t> ta, tb;
+      for (int round = 0; round < 4; ++round)
+        for (int k = 0; k < 2; ++k) {
+          const bool refined = (round % 2 == 0) == (k == 1);
+          g.path = refined ? cur : saved;
+          plan_compile(g);
+          for (int w = 0; w < 3; ++w) plan_run(g, io.din.data(), io.dout.data(), st);
+          (refined ? tb : ta).push_back(io.block_ns(g, st, 20));
+        }
+      std::sort(ta.begin(), ta.end());
+      std::sort(tb.begin(), tb.end());
+      if (tb[1] + tb[2] >= ta[1] + ta[2]) changed = 0;
+    }
+    g.path = changed ? cur : saved;
+    g.path_cost = changed ? path_total(g, cur) : saved_cost;
+    plan_compile(g);
+  } catch (...) {
+    g.path = saved;
+    g.path_cost = saved_cost;
+    plan_destroy(g);
+    throw;
+  }
+  return changed;
 }
 
 }  // namespace sn

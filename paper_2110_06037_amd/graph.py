@@ -216,6 +216,18 @@ class Graph:
                         "kind": "dprs" if kab[0] == 0 else "fixed", "a": kab[1], "b": kab[2]})
         return out
 
+    def refine_in_path(self, tol_permille=150, max_alts=3, reps=15, stream=None):
+        """In-path refinement of the selected path (integrated profiling of
+        Sec. III-C applied one layer at a time): near-tied routines of each
+        layer's schema are timed inside the whole path and a clear winner
+        replaces the selected routine, if the refined path also wins end to
+        end.  Returns the number of layers whose routine changed."""
+        n = ctypes.c_int32()
+        sp = _stream_ptr(stream) if self.device >= 0 else ctypes.c_void_p(0)
+        N.check(self.lib.sn_refine_in_path(self._g, int(tol_permille), int(max_alts), int(reps), sp,
+                                           ctypes.byref(n)))
+        return n.value
+
     def set_path(self, ids):
         arr = (ctypes.c_int32 * len(ids))(*ids)
         N.check(self.lib.sn_set_path(self._g, arr, len(ids)))

@@ -78,6 +78,7 @@ SIGNATURES = {
     "sn_plan_launches": (ctypes.c_int, [_P, _I32P, _I32, _I32P]),
     "sn_profile_integrated": (ctypes.c_int, [_P, _I32, _I32, _P, _I32P]),
     "sn_integrated_candidate": (ctypes.c_int, [_P, _I32, _I32P, _I32, _I64P, _I64P, _I32P]),
+    "sn_refine_in_path": (ctypes.c_int, [_P, _I32, _I32, _I32, _P, _I32P]),
     "sn_get_costs": (ctypes.c_int, [_P, ctypes.c_char_p, ctypes.c_size_t,
                                     ctypes.POINTER(ctypes.c_size_t)]),
     "sn_set_costs": (ctypes.c_int, [_P, ctypes.c_char_p]),

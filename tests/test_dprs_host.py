@@ -405,6 +405,24 @@ def test_integrated_profiling_needs_costs_and_a_device():
         g.profile_integrated(warmup=-1, reps=0)
 
 
+def test_in_path_refinement_needs_costs_a_path_and_a_device():
+    g = graph_from_edges(3, [(0, 1), (1, 2)])
+    with pytest.raises(N.SNError, match="SN_E_STATE"):
+        g.refine_in_path()
+    g.set_costs(randomise(g.costs(), 1))
+    with pytest.raises(N.SNError, match="SN_E_STATE"):
+        g.refine_in_path()  # costs but no selected path
+    g.select("dprs")
+    with pytest.raises(N.SNError, match="SN_E_DEVICE"):
+        g.refine_in_path()
+    for kw in ({"tol_permille": -1}, {"tol_permille": 1001}, {"max_alts": 0}, {"max_alts": 17},
+               {"reps": 0}, {"reps": 1001}):
+        with pytest.raises(N.SNError, match="SN_E_INVALID"):
+            g.refine_in_path(**kw)
+    path = g.path()
+    assert g.path() == path  # the failed calls leave the selection alone
+
+
 def test_workspace_limit_restricts_the_routine_set():
     # Time optimised under a memory restriction (the restriction the paper's
     # Sec. VI names as future work, Winograd's transforms its example): with

@@ -111,6 +111,31 @@ def test_integrated_profiling_selects_the_measured_fastest_candidate(name):
     g.close()
 
 
+def test_in_path_refinement_keeps_schemas_and_parity():
+    # in-path refinement swaps a layer's routine only for one of the same
+    # schema whose unit-profiled time is within the tolerance of the selected
+    # one's, so the adapts stay as they were and the output still matches the
+    # oracle
+    spec = fuse_projection(fuse_residual(resnet50(2, "bf16")))
+    t = generate(spec)
+    g = build_from_spec(spec, t)
+    g.profile(warmup=2, reps=5)
+    g.select("dprs")
+    before, _ = g.path()
+    n = g.refine_in_path(tol_permille=200, max_alts=3, reps=5)
+    after, total = g.path()
+    changed = [i for i in range(len(after)) if after[i] != before[i]]
+    print("refined layers", changed, [g.routines(i)[after[i]]["name"] for i in changed], flush=True)
+    assert n == len(changed)
+    for i in changed:
+        r0, r1 = g.routines(i)[before[i]], g.routines(i)[after[i]]
+        assert r1["schema"] == r0["schema"]
+        assert r1["cost_ns"] <= r0["cost_ns"] * 1.2 + 1
+    out, _ = run_out(g, spec, t)
+    assert err(out, oracle_out(spec, t), spec["dtype"]) <= TOL[spec["dtype"]]
+    g.close()
+
+
 @pytest.mark.parametrize("name", ["resnet18", "mobilenetv2", "resnet50_bf16", "resnet50_f16",
                                   "resnet50_fused", "resnet50_proj", "mobilenetv2_fused", "vgg16_64px"])
 def test_net_dp_and_fixed_paths_match_oracle(name):
