@@ -410,6 +410,8 @@ def main():
     ap.add_argument("--refine-tol", type=int, default=150,
                     help="in-path refinement: alternatives within this many per mille of the "
                          "selected routine's unit-profiled time")
+    ap.add_argument("--refine-alts", type=int, default=3,
+                    help="in-path refinement: alternatives tried per layer (the fastest by unit cost)")
     ap.add_argument("--integrated-reps", type=int, default=20,
                     help="runs per candidate in integrated profiling (0 = keep the DPRS path)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -507,7 +509,7 @@ def main():
         if args.integrated_reps > 0:
             g.profile_integrated(warmup=2, reps=args.integrated_reps)
         if args.refine_reps > 0 and not args.rotate_layouts:
-            n_ref = g.refine_in_path(tol_permille=args.refine_tol, reps=args.refine_reps)
+            n_ref = g.refine_in_path(tol_permille=args.refine_tol, max_alts=args.refine_alts, reps=args.refine_reps)
             log(f"[bench] in-path refinement: {n_ref} layer(s) changed")
         if args.path_out:
             with open(args.path_out, "w") as f:
@@ -573,7 +575,7 @@ def main():
     if args.refine_reps > 0 and not pinned:
         before = g.path()[0]
         t3 = time.perf_counter()
-        n_ref = g.refine_in_path(tol_permille=args.refine_tol, reps=args.refine_reps)
+        n_ref = g.refine_in_path(tol_permille=args.refine_tol, max_alts=args.refine_alts, reps=args.refine_reps)
         t_ref = time.perf_counter() - t3
         after = g.path()[0]
         refine = {"layers_changed": n_ref, "seconds": round(t_ref, 2), "tol_permille": args.refine_tol,
@@ -731,7 +733,7 @@ def main():
         if args.integrated_reps > 0:
             g1.profile_integrated(warmup=2, reps=max(args.integrated_reps, 20))
         if args.refine_reps > 0:
-            g1.refine_in_path(tol_permille=args.refine_tol, reps=args.refine_reps)
+            g1.refine_in_path(tol_permille=args.refine_tol, max_alts=args.refine_alts, reps=args.refine_reps)
         x1 = to_dev(t1_["x"], args.dtype)
         o1 = g1.empty_output()
         # eager launches and the same plan replayed as a HIP graph; the

@@ -396,9 +396,9 @@ int sn_integrated_candidate(const sn_graph* g, int32_t idx, int32_t* routine_ids
  * inside the whole path with only that layer's routine swapped (adapts are
  * unchanged: the schema is the same), on a zero-filled scratch input; the
  * layer's time is read from HIP events tied to its first and last launch,
- * the median over reps runs after two warm-up runs.  A routine that beats
- * the selected one by more than 2 % replaces it for the later layers'
- * trials.  Finally the selected and the refined path are timed end to end
+ * the median over reps runs after two warm-up runs.  The fastest routine,
+ * when it beats the selected one by more than 2 % and does so again in a
+ * second pair of timings, replaces it for the later layers' trials.  Finally the selected and the refined path are timed end to end
  * (four alternating rounds of 20 runs, block means, the median of each) and
  * the faster is kept; its plan is compiled, as after sn_select_path.
  * *n_changed (may be NULL) receives the number of layers whose routine

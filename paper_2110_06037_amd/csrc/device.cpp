@@ -1050,9 +1050,9 @@ void integrated_measure(Graph& g, std::vector<Candidate>& cands, int warmup, int
 // Layer by layer, the selected routine and its near-tied alternatives of the
 // same schema are timed inside the whole path (only that layer swapped; the
 // layer's time from the events tied to its first and last launch, median of
-// reps timed runs); a clear winner (more than 2 % faster) is kept for the
-// later layers' trials.  The refined path then has to beat the selected one
-// end to end (alternating rounds) to be kept.
+// reps timed runs); a clear winner (more than 2 % faster, confirmed by a second
+// pair of timings) is kept for the later layers' trials.  The refined path then
+// has to beat the selected one end to end (alternating rounds) to be kept.
 int refine_in_path(Graph& g, int tol_permille, int max_alts, int reps, void* stream) {
   if (!g.have_costs) fail(SN_E_STATE, "no costs: profile or load a cost table first");
   if (g.path.empty()) fail(SN_E_STATE, "no selected path");
@@ -1100,7 +1100,14 @@ int refine_in_path(Graph& g, int tol_permille, int max_alts, int reps, void* str
         const float t = layer_time(p, i);
         if (t < best_t) best_t = t, best = r;
       }
-      if (best != r0 && best_t < 0.98f * t0) cur[i] = best;
+      if (best == r0 || best_t >= 0.98f * t0) continue;
+      // a second, fresh pair of timings has to confirm the win: with several
+      // alternatives the fastest of a noisy set is biased low
+      std::vector<int> p = cur;
+      p[i] = best;
+      const float t0b = layer_time(cur, i);
+      const float t1b = layer_time(p, i);
+      if (t1b < 0.98f * t0b) cur[i] = best;
     }
     for (int i = 0; i < nl; ++i) changed += cur[i] != saved[i];
     if (changed) {
