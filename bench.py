@@ -668,6 +668,18 @@ def main():
     # headline: MFMA utilisation over the 3x3 convolutions
     c3 = cats.get("conv3x3")
     conv3_util = (c3["flops"] / (c3["ms"] * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS[args.dtype]) if c3 else None
+    # every layer category against both roofs (per-layer block means): the
+    # dominant routine above is one tile configuration, this is the whole
+    # category (all routines and tiles of that layer kind)
+    step_layer_ms = float(layer_ms[1:].sum())
+    cat_roof = {}
+    for cname, cv in sorted(cats.items(), key=lambda kv: -kv[1]["ms"]):
+        sec_c = cv["ms"] * 1e-3
+        cat_roof[cname] = {
+            "layers": cv["launches"], "ms": round(cv["ms"], 4), "share": round(cv["ms"] / step_layer_ms, 4),
+            "mfma_frac": round(cv["flops"] / sec_c / 1e12 / PEAK_MFMA_TFLOPS[args.dtype], 4) if cv["flops"] else 0.0,
+            "hbm_frac": round(cv["bytes"] / sec_c / 1e9 / PEAK_HBM_GBS, 4),
+            "hbm_frac_needed": round(cv["needed"] / sec_c / 1e9 / PEAK_HBM_GBS, 4)}
 
     if args.calib_copy_mib:
         src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
@@ -771,6 +783,7 @@ def main():
         "layer_sum_ms": {"warm": round(float(layer_ms[1:].sum()), 4), "cold": round(float(cold[1:].sum()), 4)},
         "img_s_bs1": bs1, "bs1_ms": bs1_detail,
         "conv3x3_mfma_util": round(conv3_util, 4) if conv3_util else None,
+        "category_roofline": cat_roof,
         "dprs_img_s": round(args.batch / sec_dp, 2),
         "dp_vs_best_fixed": comparison["dp_vs_best_fixed"] if comparison else dp_vs_fixed,
         "selected_vs_best_fixed": (comparison.get("selected_vs_best_fixed", comparison["dp_vs_best_fixed"])
