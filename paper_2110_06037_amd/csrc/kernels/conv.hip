@@ -27,7 +27,8 @@ bool igemm_param_valid(int dtype, int param, int layout, int n, int c, int h, in
   const IgCfg& g = dtype == 0 ? kIg32[param] : kIg16[param];
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
   if (g.dma == 2)
-    return patch_applicable(layout, c, h, w, r, s, stride, pad, n, g.pc.fmt, g.pc.pwt, g.pc.prows, g.pc.sd);
+    return patch_applicable(layout, c, h, w, r, s, stride, pad, n, g.pc.fmt, g.pc.pwt, g.pc.prows, g.pc.sd,
+                            g.pc.ra);
   if (g.dma == 3) return smallc_applicable(layout, c, h, w, r, s, stride, pad, n, k, g.bm / 16, g.ppx, g.gmax);
   if (g.dma == 4) return stream1x1_applicable(layout, c, c, n, h, w, r, s, stride, pad, k, g.bk);
   if (g.dma) {

@@ -61,6 +61,7 @@ struct PatchArgs {
   float inv_pw, inv_ip, inv_trq, inv_q;   // 1/PW, 1/IP, 1/(TR*Q), 1/Q for sdiv
   int HW8, W8;                            // NC8HW8 strides: H*W*8, W*8
   float inv_pq;                           // 1/(P*Q) for sdiv
+  float inv_tr;                           // 1/TR (row-aligned tiles)
   long long y_elems;
   long long x_elems, w_elems;
 };
@@ -73,9 +74,11 @@ using IC = std::integral_constant<int, V>;
 // WM x WN waves (group g runs taps [9g/TG, 9(g+1)/TG) of every step on the
 // whole tile; the groups' sums meet in LDS at the end); ST LDS stages;
 // PROWS patch rows per stage.
-template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD, int OCC = 1>
+template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD, int OCC = 1,
+          bool RA = false>
 __global__ __launch_bounds__(512, OCC) void conv3x3_patch_kernel(PatchArgs a) {
   static_assert(sizeof(T) == 2 && L != NCHW, "16-bit channel-vector layouts only");
+  static_assert(!RA || SD == 1, "row-aligned blocks at stride 1");
   constexpr int NWV = 8;
   static_assert(WM * WN * TG == NWV, "8 waves");
   static_assert(PWT == 16 || PWT == 32 || PWT == 64, "patch pitch: a multiple of 16 rows");
@@ -184,9 +187,19 @@ __global__ __launch_bounds__(512, OCC) void conv3x3_patch_kernel(PatchArgs a) {
 #pragma unroll
   for (int i = 0; i < FMW; ++i) {
     const int m = (blk0 + i) * 16 + (lane & 15);
-    const int ii = sdiv(m, a.inv_trq), rem = m - __umul24(ii, a.TR * a.Q);
-    const int pr = sdiv(rem, a.inv_q), pc = rem - __umul24(pr, a.Q);
-    const int pb = blk0 + i < FMT && ii < a.TI ? __umul24(ii, a.IP) + ((pr * SD) << LPW) + pc * SD : 0;
+    int pb;
+    if constexpr (RA) {
+      // virtual pixel m: row vr = m / PWT of the tile (image ii, row pr),
+      // column pc = m % PWT; columns past Q compute values nobody stores,
+      // from rows of the same stage (at most one row past the patch)
+      const int vr = m >> LPW, pc = m & (PWT - 1);
+      const int ii = sdiv(vr, a.inv_tr), pr = vr - __umul24(ii, a.TR);
+      pb = blk0 + i < FMT && ii < a.TI ? __umul24(ii, a.IP) + (pr << LPW) + pc : 0;
+    } else {
+      const int ii = sdiv(m, a.inv_trq), rem = m - __umul24(ii, a.TR * a.Q);
+      const int pr = sdiv(rem, a.inv_q), pc = rem - __umul24(pr, a.Q);
+      pb = blk0 + i < FMT && ii < a.TI ? __umul24(ii, a.IP) + ((pr * SD) << LPW) + pc * SD : 0;
+    }
 #pragma unroll
     for (int c = 0; c < 3; ++c) {
       const int r = pb + c;
@@ -295,7 +308,15 @@ __global__ __launch_bounds__(512, OCC) void conv3x3_patch_kernel(PatchArgs a) {
 #pragma unroll
     for (int i = 0; i < FMW; ++i) {
       if (blk0 + i >= FMT) continue;
-      const int ml = (blk0 + i) * 16 + (lane & 15);
+      int ml = (blk0 + i) * 16 + (lane & 15);
+      if constexpr (RA) {
+        // the valid virtual pixels move to their place among the tile's
+        // output pixels; the others are dropped
+        const int vr = ml >> LPW, pc = ml & (PWT - 1);
+        const int ii = sdiv(vr, a.inv_tr), pr = vr - ii * a.TR;
+        if (pc >= a.Q || pr >= rows || ii >= imgs) continue;
+        ml = (ii * rows + pr) * a.Q + pc;
+      }
 #pragma unroll
       for (int j = 0; j < FNW; ++j) {
         const int nl = wn * WTN + j * 16 + (lane >> 4) * 4;
@@ -349,16 +370,20 @@ __global__ __launch_bounds__(512, OCC) void conv3x3_patch_kernel(PatchArgs a) {
 // one fits, else as many whole output rows as fit, balanced over the rows.
 // The patch row pitch is pwt and the image pitch PH * pwt.  Returns whether
 // the patch fits `prows`.
-static bool patch_tiling(PatchArgs& a, int fmt, int pwt, int prows, int sd) {
+static bool patch_tiling(PatchArgs& a, int fmt, int pwt, int prows, int sd, int ra = 0) {
   const int maxpx = fmt * 16;
-  if (a.Q > maxpx || (a.Q - 1) * sd + 3 > pwt) return false;
-  if (a.P * a.Q <= maxpx) {
-    a.TI = std::min(a.N, maxpx / (a.P * a.Q));
+  if (a.Q > maxpx || (a.Q - 1) * sd + 3 > pwt || (ra && sd != 1)) return false;
+  if (ra && 2 * a.Q <= pwt) return false;  // most virtual columns would be dropped
+  // row-aligned tiles count an output row as pwt (virtual) pixels
+  const int rowpx = ra ? pwt : a.Q;
+  if (rowpx > maxpx) return false;
+  if (a.P * rowpx <= maxpx) {
+    a.TI = std::min(a.N, maxpx / (a.P * rowpx));
     a.TR = a.P;
     a.tiles_img = 1;
     a.tiles_m = (a.N + a.TI - 1) / a.TI;
   } else {
-    const int fit = maxpx / a.Q;
+    const int fit = maxpx / rowpx;
     a.TI = 1;
     a.tiles_img = (a.P + fit - 1) / fit;
     a.TR = (a.P + a.tiles_img - 1) / a.tiles_img;
@@ -375,6 +400,7 @@ static bool patch_tiling(PatchArgs& a, int fmt, int pwt, int prows, int sd) {
   a.W8 = a.W * 8;
   a.inv_trq = 1.f / (float)(a.TR * a.Q);
   a.inv_q = 1.f / (float)a.Q;
+  a.inv_tr = 1.f / (float)a.TR;
   return (long long)a.TI * a.IP <= prows;
 }
 
@@ -405,7 +431,7 @@ static PatchArgs make_patch(const ConvArgs& c) {
 }
 
 bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
-                      int fmt, int pwt, int prows, int sd) {
+                      int fmt, int pwt, int prows, int sd, int ra) {
   if (r != 3 || s != 3 || stride != sd || pad != 1) return false;
   const bool vec = layout == NC8 || (layout == NHWC && c % 8 == 0);
   if (!vec || ((c + 7) / 8) % 4 != 0) return false;
@@ -414,49 +440,59 @@ bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride,
   a.N = n;
   a.P = (h - 1) / sd + 1;
   a.Q = (w - 1) / sd + 1;
-  return patch_tiling(a, fmt, pwt, prows, sd);
+  return patch_tiling(a, fmt, pwt, prows, sd, ra);
 }
 
-template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD, int OCC = 1>
+template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD, int OCC = 1,
+          bool RA = false>
 static void patch_go(PatchArgs a, hipStream_t st) {
-  check(patch_tiling(a, FMT, PWT, PROWS, SD), "output too wide for the patch tile");
+  check(patch_tiling(a, FMT, PWT, PROWS, SD, RA), "output too wide for the patch tile");
   check(a.CB % 4 == 0, "patch kernel needs C % 32 == 0");
   check(a.x_elems * 2 < (long long)kOOB && a.w_elems * 2 < (long long)kOOB,
         "tensor too large for 32-bit buffer offsets");
   a.tiles_n = (a.Ng + BN - 1) / BN;
   dim3 grid(a.tiles_m * a.tiles_n);
-  SN_LAUNCH((conv3x3_patch_kernel<T, L, FMT, BN, PWT, WM, WN, TG, ST, PROWS, SD, OCC>), grid, dim3(512), 0, st, a);
+  SN_LAUNCH((conv3x3_patch_kernel<T, L, FMT, BN, PWT, WM, WN, TG, ST, PROWS, SD, OCC, RA>), grid, dim3(512), 0, st,
+            a);
 }
 
-static long long patch_key(int fmt, int bn, int pwt, int wm, int wn, int tg, int stg, int prows, int sd, int occ) {
-  return ((((((((fmt * 1000LL + bn) * 100 + pwt) * 10 + wm) * 10 + wn) * 10 + tg) * 10 + stg) * 10000 + prows) * 10 +
-          sd) * 10 + occ;
+static long long patch_key(int fmt, int bn, int pwt, int wm, int wn, int tg, int stg, int prows, int sd, int occ,
+                           int ra) {
+  return (((((((((fmt * 1000LL + bn) * 100 + pwt) * 10 + wm) * 10 + wn) * 10 + tg) * 10 + stg) * 10000 + prows) * 10 +
+           sd) * 10 + occ) * 2 + ra;
 }
 
 template <typename T, int L>
 static void patch_layout(const PatchCfg& c, const PatchArgs& a, hipStream_t st) {
-  const long long key = patch_key(c.fmt, c.bn, c.pwt, c.wm, c.wn, c.tg, c.st, c.prows, c.sd, c.occ);
+  const long long key = patch_key(c.fmt, c.bn, c.pwt, c.wm, c.wn, c.tg, c.st, c.prows, c.sd, c.occ, c.ra);
 #define PGO(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                               \
-  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 1)) {            \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 1, 0)) {         \
     patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1>(a, st);              \
     return;                                                                            \
   }
 #define PGO2(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                              \
-  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 2, 1)) {            \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 2, 1, 0)) {         \
     patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 2>(a, st);              \
     return;                                                                            \
   }
 #define PGOO2(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                             \
-  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 2)) {            \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 2, 0)) {         \
     patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 2>(a, st);           \
+    return;                                                                            \
+  }
+#define PGORA(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                             \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 1, 1)) {         \
+    patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 1, true>(a, st);     \
     return;                                                                            \
   }
   PATCH_CONFIGS(PGO)
   PATCH2_CONFIGS(PGO2)
   PATCH_OCC2_CONFIGS(PGOO2)
+  PATCH_RA_CONFIGS(PGORA)
 #undef PGO
 #undef PGO2
 #undef PGOO2
+#undef PGORA
   check(false, "patch tile not instantiated");
 }
 

@@ -1098,6 +1098,11 @@ static const IgCfg kIg16[] = {
 #define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM},
     STREAM512_CONFIGS(SN_STREAM_IG)
 #undef SN_STREAM_IG
+    // 3x3 stride-1 patch kernel with row-aligned row blocks
+#define SN_PATCHRA_IG(FMT, BN, PWT, WM, WN, TG, ST, PROWS) \
+  {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS, 1, 1, 1}},
+    PATCH_RA_CONFIGS(SN_PATCHRA_IG)
+#undef SN_PATCHRA_IG
 };
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 

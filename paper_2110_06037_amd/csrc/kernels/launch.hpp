@@ -98,6 +98,7 @@ struct PatchCfg {
   int fmt, bn, pwt, wm, wn, tg, st, prows;  // one PATCH_CONFIGS tuple
   int sd = 1;                               // convolution stride
   int occ = 1;                              // workgroups per CU the tile is sized for
+  int ra = 0;                               // 1: row-aligned row blocks (stride 1)
 };
 // Instantiated patch tiles (FMT, BN, PWT, WM, WN, TG, ST, PROWS): FMT row
 // blocks of 16 output pixels, BN output channels, patch row pitch PWT, 8
@@ -127,8 +128,17 @@ struct PatchCfg {
 // the other's steps (7 x 7 and 14 x 14 at 32 output channels per tile)
 #define PATCH_OCC2_CONFIGS(X)    \
   X(7, 32, 16, 4, 1, 2, 2, 288)
+// Row-aligned stride-1 patch tiles (same fields): a row block is 16
+// consecutive patch columns of one output row (PWT / 16 blocks per row, the
+// columns past Q computed and dropped), so every operand read covers 16
+// consecutive LDS rows; at 56, 28 and 14 columns the blocks computed are as
+// many as the unaligned tiles' waves cover anyway
+#define PATCH_RA_CONFIGS(X)      \
+  X(28, 64, 64, 4, 2, 1, 2, 576) \
+  X(14, 64, 32, 4, 2, 1, 2, 288) \
+  X(8, 64, 16, 4, 1, 2, 2, 288)
 bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
-                      int fmt, int pwt, int prows, int sd);
+                      int fmt, int pwt, int prows, int sd, int ra = 0);
 void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& a, hipStream_t st);
 // Stride-1 or -2 convolution of an NHWC input with C <= 4 (a CNN stem; see
 // conv_smallc.hip); gmax: filter chunks the kernel holds (28 for 7 x 7, 8 for 3 x 3)
