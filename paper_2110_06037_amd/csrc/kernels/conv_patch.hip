@@ -480,9 +480,9 @@ static void patch_layout(const PatchCfg& c, const PatchArgs& a, hipStream_t st) 
     patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 2>(a, st);           \
     return;                                                                            \
   }
-#define PGORA(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_)                             \
-  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 1, 1)) {         \
-    patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, 1, true>(a, st);     \
+#define PGORA(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, OCC_)                       \
+  if (key == patch_key(FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, OCC_, 1)) {      \
+    patch_go<T, L, FMT_, BN_, PWT_, WM_, WN_, TG_, ST_, PROWS_, 1, OCC_, true>(a, st);  \
     return;                                                                            \
   }
   PATCH_CONFIGS(PGO)

@@ -1099,8 +1099,8 @@ static const IgCfg kIg16[] = {
     STREAM512_CONFIGS(SN_STREAM_IG)
 #undef SN_STREAM_IG
     // 3x3 stride-1 patch kernel with row-aligned row blocks
-#define SN_PATCHRA_IG(FMT, BN, PWT, WM, WN, TG, ST, PROWS) \
-  {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS, 1, 1, 1}},
+#define SN_PATCHRA_IG(FMT, BN, PWT, WM, WN, TG, ST, PROWS, OCC) \
+  {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS, 1, OCC, 1}},
     PATCH_RA_CONFIGS(SN_PATCHRA_IG)
 #undef SN_PATCHRA_IG
 };

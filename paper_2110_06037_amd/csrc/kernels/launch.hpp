@@ -133,10 +133,12 @@ struct PatchCfg {
 // columns past Q computed and dropped), so every operand read covers 16
 // consecutive LDS rows; at 56, 28 and 14 columns the blocks computed are as
 // many as the unaligned tiles' waves cover anyway
-#define PATCH_RA_CONFIGS(X)      \
-  X(28, 64, 64, 4, 2, 1, 2, 576) \
-  X(14, 64, 32, 4, 2, 1, 2, 288) \
-  X(8, 64, 16, 4, 1, 2, 2, 288)
+// (the last field: workgroups per CU the tile is sized for)
+#define PATCH_RA_CONFIGS(X)         \
+  X(28, 64, 64, 4, 2, 1, 2, 576, 1) \
+  X(14, 64, 32, 4, 2, 1, 2, 288, 1) \
+  X(8, 64, 16, 4, 1, 2, 2, 288, 1)  \
+  X(8, 32, 16, 4, 1, 2, 2, 160, 2)
 bool patch_applicable(int layout, int c, int h, int w, int r, int s, int stride, int pad, int n,
                       int fmt, int pwt, int prows, int sd, int ra = 0);
 void conv_patch(int dtype, const PatchCfg& cfg, const ConvArgs& a, hipStream_t st);
