@@ -76,7 +76,9 @@ using IC = std::integral_constant<int, V>;
 // PROWS patch rows per stage.
 template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD, int OCC = 1,
           bool RA = false>
-__global__ __launch_bounds__(512, OCC) void conv3x3_patch_kernel(PatchArgs a) {
+// (the launch bound's second figure is waves per SIMD: OCC workgroups of 8
+// waves per CU are 2 OCC waves on each of its 4 SIMDs)
+__global__ __launch_bounds__(512, 2 * OCC) void conv3x3_patch_kernel(PatchArgs a) {
   static_assert(sizeof(T) == 2 && L != NCHW, "16-bit channel-vector layouts only");
   static_assert(!RA || SD == 1, "row-aligned blocks at stride 1");
   constexpr int NWV = 8;
