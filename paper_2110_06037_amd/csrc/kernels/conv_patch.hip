@@ -73,11 +73,11 @@ using IC = std::integral_constant<int, V>;
 // row pitch (a power of two >= Q + 2); the 8 waves form TG tap groups of
 // WM x WN waves (group g runs taps [9g/TG, 9(g+1)/TG) of every step on the
 // whole tile; the groups' sums meet in LDS at the end); ST LDS stages;
-// PROWS patch rows per stage.
+// PROWS patch rows per stage; OCC workgroups per CU (the launch bound's
+// second figure counts waves per SIMD: 2 OCC, 8 waves on 4 SIMDs each);
+// RA: row-aligned row blocks.
 template <typename T, int L, int FMT, int BN, int PWT, int WM, int WN, int TG, int ST, int PROWS, int SD, int OCC = 1,
           bool RA = false>
-// (the launch bound's second figure is waves per SIMD: OCC workgroups of 8
-// waves per CU are 2 OCC waves on each of its 4 SIMDs)
 __global__ __launch_bounds__(512, 2 * OCC) void conv3x3_patch_kernel(PatchArgs a) {
   static_assert(sizeof(T) == 2 && L != NCHW, "16-bit channel-vector layouts only");
   static_assert(!RA || SD == 1, "row-aligned blocks at stride 1");
