@@ -713,6 +713,14 @@ def main():
             lay, algo = name.split("/")
             g.select("fixed", lay, algo)
             cands.append((f"fixed/{name}", g.path()[0]))
+        if refine:
+            # the fastest fixed path given the same in-path refinement (it
+            # stays within its one layout), so the selected path is also
+            # compared with a fixed path tuned as far as the DPRS one
+            lay, algo = top[0].split("/")
+            g.select("fixed", lay, algo)
+            g.refine_in_path(tol_permille=args.refine_tol, max_alts=args.refine_alts, reps=args.refine_reps)
+            cands.append((f"fixed_refined/{top[0]}", g.path()[0]))
         times = {nm: [] for nm, _ in cands}
         for r in range(args.compare_rounds):
             for nm, path in (cands if r % 2 == 0 else cands[::-1]):
@@ -729,6 +737,9 @@ def main():
                       "dp_vs_best_fixed_per_round": [round(q, 4) for q in ratios]}
         if "selected" in med:
             comparison["selected_vs_best_fixed"] = round(med[bf] / med["selected"], 4)
+            fr = next((nm for nm in med if nm.startswith("fixed_refined/")), None)
+            if fr:
+                comparison["selected_vs_refined_best_fixed"] = round(med[fr] / med["selected"], 4)
         log(f"[bench] alternating comparison: {comparison}")
 
     bs1 = bs1_detail = None
@@ -788,6 +799,7 @@ def main():
         "dp_vs_best_fixed": comparison["dp_vs_best_fixed"] if comparison else dp_vs_fixed,
         "selected_vs_best_fixed": (comparison.get("selected_vs_best_fixed", comparison["dp_vs_best_fixed"])
                                    if comparison else sel_vs_fixed),
+        "selected_vs_refined_best_fixed": comparison.get("selected_vs_refined_best_fixed") if comparison else None,
         "comparison": comparison, "single_pass_dp_vs_best_fixed": dp_vs_fixed,
         "best_fixed": best_fixed, "fixed_img_s": fixed, "fixed_model_time_ms": fixed_model, "integrated": integ,
         "in_path_refinement": refine,
