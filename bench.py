@@ -783,7 +783,9 @@ def main():
         "data": "synthetic (seeded random input and He-normal weights)",
         "config": {"workload": f"{args.net}-shaped CNN, batch {args.batch}, {args.dtype}, 224x224"
                                + ("" if not any(l["type"] == "conv" and len(l["in"]) > 1 for l in spec["layers"])
-                                  else ", residual adds folded into the 1x1 convolutions that produce them"),
+                                  else ", residual adds folded into the 1x1 convolutions that produce them")
+                               + (", projection shortcuts folded into the convolution their add follows"
+                                  if any(l.get("proj") for l in spec["layers"]) else ""),
                    "batch": args.batch,
                    "path": ("DPRS candidates + fixed paths, integrated profiling keeps the fastest"
                             if integ else "DPRS-selected routines")
