@@ -134,9 +134,12 @@ def test_depthwise(dtype, case):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("shape", [(2, 16, 17, 17), (1, 3, 12, 10), (2, 64, 56, 56), (1, 8, 9, 14), (1, 8, 1, 1)])
-def test_maxpool_exact(dtype, shape):
-    layer = {"type": "maxpool", "in": [0], "k": 3, "stride": 2, "pad": 1}
+@pytest.mark.parametrize("shape,stride", [((2, 16, 17, 17), 2), ((1, 3, 12, 10), 2), ((2, 64, 56, 56), 2),
+                                          ((1, 8, 9, 14), 2), ((1, 8, 1, 1), 2), ((3, 64, 112, 112), 2),
+                                          ((2, 16, 9, 9), 1), ((1, 24, 8, 7), 1)])
+def test_maxpool_exact(dtype, shape, stride):
+    # stride 2 at 112 x 112 is ResNet's pooling layer
+    layer = {"type": "maxpool", "in": [0], "k": 3, "stride": stride, "pad": 1}
     x = random_tensor(shape, dtype, seed=6)
     ref = oracle_layer(layer, x, None, None, dtype)
     g = single_layer_graph(dtype, shape, layer)
