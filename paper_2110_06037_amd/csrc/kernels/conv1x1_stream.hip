@@ -49,8 +49,9 @@ struct StreamArgs {
 template <int V>
 using SIC = std::integral_constant<int, V>;
 
-template <typename T, int CC, int BM, int BN, int WM, bool RES, int PD, bool PJ = false>
-__global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
+// OCC: workgroups per CU (the launch bound counts waves per SIMD: 2 OCC)
+template <typename T, int CC, int BM, int BN, int WM, bool RES, int PD, bool PJ = false, int OCC = 1>
+__global__ __launch_bounds__(512, 2 * OCC) void conv1x1_stream_kernel(StreamArgs a) {
   static_assert(sizeof(T) == 2 && CC % 64 == 0, "16-bit types, 64-channel slabs");
   static_assert(!(PJ && RES), "a projected shortcut replaces the residual");
   static_assert(PD >= 1 && PD <= 3, "one to three tiles ahead");
@@ -78,10 +79,11 @@ __global__ __launch_bounds__(512, 1) void conv1x1_stream_kernel(StreamArgs a) {
   // in the tile's own pixel buffer once every wave has read it (ALIAS); the
   // loads of a later tile into a buffer then wait for the barrier after
   // which no wave reads that buffer's staging any more
-  constexpr bool ALIAS = B_BYTES + NB * A_BYTES + CS_BYTES + BN * 4 > 160 * 1024;
+  constexpr int LDS_CAP = 160 * 1024 / OCC;
+  constexpr bool ALIAS = B_BYTES + NB * A_BYTES + CS_BYTES + BN * 4 > LDS_CAP;
   static_assert(!ALIAS || A_BYTES >= CS_BYTES, "staging fits the pixel buffer");
   constexpr int SM = B_BYTES + NB * A_BYTES + (ALIAS ? 0 : CS_BYTES) + BN * 4;
-  static_assert(SM <= 160 * 1024, "LDS capacity");
+  static_assert(SM <= LDS_CAP, "LDS capacity at the occupancy");
   __shared__ __attribute__((aligned(1024))) char smem[SM];
   char* const Bs = smem;
   char* const As = smem + B_BYTES;
@@ -314,22 +316,23 @@ bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r,
          (long long)n * p * q * ((k + 7) / 8 * 8) * 2 < (long long)kOOB;
 }
 
-template <typename T, int CC, int BM, int BN, int WM, int PD>
+template <typename T, int CC, int BM, int BN, int WM, int PD, int OCC = 1>
 static void stream_go(const StreamArgs& a, int tiles_n, hipStream_t st) {
-  // persistent: about one workgroup per CU over all channel tiles
-  const int gx = std::max(1, std::min(a.tiles_m, 256 / tiles_n));
+  // persistent: about OCC workgroups per CU over all channel tiles
+  const int gx = std::max(1, std::min(a.tiles_m, 256 * OCC / tiles_n));
   const dim3 grid(gx, tiles_n);
   if (a.x2) {
-    if constexpr (CC >= 128) SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, false, PD, true>), grid, dim3(512), 0, st, a);
+    if constexpr (CC >= 128)
+      SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, false, PD, true, OCC>), grid, dim3(512), 0, st, a);
     else check(false, "a projected shortcut needs two slabs or more");
   } else if (a.res) {
-    SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, true, PD>), grid, dim3(512), 0, st, a);
+    SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, true, PD, false, OCC>), grid, dim3(512), 0, st, a);
   } else {
-    SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, false, PD>), grid, dim3(512), 0, st, a);
+    SN_LAUNCH((conv1x1_stream_kernel<T, CC, BM, BN, WM, false, PD, false, OCC>), grid, dim3(512), 0, st, a);
   }
 }
 
-void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& c, hipStream_t st) {
+void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& c, hipStream_t st, int occ) {
   check(dtype != 0, "streaming 1x1 kernel runs 16-bit types");
   const long long m = (long long)c.yd.n * c.yd.h * c.yd.w;
   if (c.x2) {
@@ -378,14 +381,22 @@ void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& c
   a.y_elems = m * a.Ks;
   const int tiles_n = (a.K + bn - 1) / bn;
 #define SG(CC_, BM_, BN_, WM_, PD_)                                              \
-  if (cc == CC_ && bm == BM_ && bn == BN_ && pd == PD_) {                        \
+  if (cc == CC_ && bm == BM_ && bn == BN_ && pd == PD_ && occ == 1) {            \
     if (dtype == 1) stream_go<f16, CC_, BM_, BN_, WM_, PD_>(a, tiles_n, st);     \
     else stream_go<bf16, CC_, BM_, BN_, WM_, PD_>(a, tiles_n, st);               \
     return;                                                                      \
   }
+#define SG2(CC_, BM_, BN_, WM_, PD_)                                             \
+  if (cc == CC_ && bm == BM_ && bn == BN_ && pd == PD_ && occ == 2) {            \
+    if (dtype == 1) stream_go<f16, CC_, BM_, BN_, WM_, PD_, 2>(a, tiles_n, st);  \
+    else stream_go<bf16, CC_, BM_, BN_, WM_, PD_, 2>(a, tiles_n, st);            \
+    return;                                                                      \
+  }
   STREAM_CONFIGS(SG)
   STREAM512_CONFIGS(SG)
+  STREAM_OCC2_CONFIGS(SG2)
 #undef SG
+#undef SG2
   check(false, "streaming 1x1 tile not instantiated");
 }
 

@@ -1067,8 +1067,8 @@ static const IgCfg kIg16[] = {
     {112, 64, 32, 0, 0, 3, 2, 2, 1664, {}, 4, 28}, {224, 64, 32, 0, 0, 3, 2, 2, 2112, {}, 4, 28},
     {112, 64, 32, 0, 0, 3, 2, 3, 704, {}, 4, 8},   {224, 64, 32, 0, 0, 3, 2, 2, 1152, {}, 4, 8},
     // streaming 1x1 kernel: NHWC, C = bk (BM pixels x BN channels per tile, WM wave rows,
-    // loads pf tiles ahead)
-#define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM},
+    // loads pf tiles ahead; st: workgroups per CU)
+#define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM, 1},
     STREAM_CONFIGS(SN_STREAM_IG)
 #undef SN_STREAM_IG
     // LDS-DMA kernel, 8 waves, reduction split over workgroups when the
@@ -1095,7 +1095,7 @@ static const IgCfg kIg16[] = {
     PATCH_OCC2_CONFIGS(SN_PATCHO2_IG)
 #undef SN_PATCHO2_IG
     // streaming 1x1 kernel for 512-channel inputs
-#define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM},
+#define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM, 1},
     STREAM512_CONFIGS(SN_STREAM_IG)
 #undef SN_STREAM_IG
     // 3x3 stride-1 patch kernel with row-aligned row blocks
@@ -1103,6 +1103,10 @@ static const IgCfg kIg16[] = {
   {16 * FMT, BN, 32, 0, 0, 2, WM, ST, 0, {FMT, BN, PWT, WM, WN, TG, ST, PROWS, 1, OCC, 1}},
     PATCH_RA_CONFIGS(SN_PATCHRA_IG)
 #undef SN_PATCHRA_IG
+    // streaming 1x1 kernel, two workgroups per CU
+#define SN_STREAM_IG(CC, BM, BN, WM, PD) {BM, BN, CC, 0, PD, 4, WM, 2},
+    STREAM_OCC2_CONFIGS(SN_STREAM_IG)
+#undef SN_STREAM_IG
 };
 static const IgCfg kIg32[] = {{64, 64, 32, 0, 2}};
 
@@ -1380,7 +1384,7 @@ static void igemm_dispatch(int dtype, int param, const ConvArgs& c, hipStream_t 
     return;
   }
   if (cfg.dma == 4) {
-    conv1x1_stream(dtype, cfg.bk, cfg.bm, cfg.bn, cfg.pf, c, st);
+    conv1x1_stream(dtype, cfg.bk, cfg.bm, cfg.bn, cfg.pf, c, st, cfg.st);
     return;
   }
   IgArgs a = make_ig(c);

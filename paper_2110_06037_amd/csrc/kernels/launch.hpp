@@ -175,13 +175,21 @@ void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st
 #define STREAM512_CONFIGS(X) \
   X(512, 32, 64, 2, 1)       \
   X(384, 32, 128, 2, 1)
+// Streaming tiles sized for two workgroups per CU (at most 80 KB of LDS and
+// 128 registers each), so that one workgroup's loads and epilogue overlap
+// the other's MFMAs
+#define STREAM_OCC2_CONFIGS(X) \
+  X(256, 32, 64, 2, 1)         \
+  X(128, 32, 64, 2, 2)         \
+  X(64, 64, 64, 4, 2)
 bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
                           int k, int cc);
 // the streaming kernel with a projected shortcut of c2 channels (slabs of
 // the main input, then of the shortcut: c + c2 = cc, both multiples of 64)
 bool stream1x1_takes_projection(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
                                 int k, int c2, int cc);
-void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& a, hipStream_t st);
+// occ: workgroups per CU the persistent grid and the LDS are sized for
+void conv1x1_stream(int dtype, int cc, int bm, int bn, int pd, const ConvArgs& a, hipStream_t st, int occ = 1);
 // Winograd F(m x m, 3x3), m = tile 2 or 4, as three sub-layers (a
 // childnet): sub 0 = input transform, 1 = the (m+2)^2 batched GEMMs with
 // GEMM tile `cfg` (one of winograd_gemm_num_configs), 2 = output transform;
