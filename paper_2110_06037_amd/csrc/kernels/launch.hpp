@@ -181,7 +181,9 @@ void conv_smallc(int dtype, int fmt, int gmax, const ConvArgs& a, hipStream_t st
 #define STREAM_OCC2_CONFIGS(X) \
   X(256, 32, 64, 2, 1)         \
   X(128, 32, 64, 2, 2)         \
-  X(64, 64, 64, 4, 2)
+  X(64, 64, 64, 4, 2)          \
+  X(64, 64, 128, 4, 2)         \
+  X(128, 32, 128, 2, 1)
 bool stream1x1_applicable(int layout, int c, int cs, int n, int h, int w, int r, int s, int stride, int pad,
                           int k, int cc);
 // the streaming kernel with a projected shortcut of c2 channels (slabs of
