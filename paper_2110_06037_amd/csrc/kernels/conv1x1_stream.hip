@@ -18,9 +18,6 @@
 // addresses.  In LDS a tile is CC / 64 slabs of 64 channels, each with
 // 128-byte rows (8 chunks); chunk c of row r sits at c ^ ((r >> 1) & 7),
 // which serves an MFMA operand read of 16 consecutive rows in one pass.
-// Tiles small enough (at most 80 KB of LDS, 128 registers) run two
-// workgroups per CU (OCC = 2), so that one workgroup's loads and epilogue
-// overlap the other's MFMAs.
 //
 // With a projected shortcut (PJ) the reduction runs over the main input's
 // slabs and then the shortcut's (C1 + C2 = CC channels): the shortcut's slabs
